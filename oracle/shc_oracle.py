@@ -1,0 +1,283 @@
+"""CPU oracle for the sparse contact-layer operators -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the package's smoke check and the benchmark's CPU-baseline leg
+may import this module.  The library's product path never calls it, and it
+shares no code with the HIP kernels (no common helpers, tables or constants).
+
+What it computes (Sec. 3.1-3.2 of the paper, arXiv 2608.09388):
+
+* Eq. 1: the contact mask multiplies the per-vertex input elementwise.  The
+  mask is per vertex and broadcast over channels; masks are given per body /
+  frame b, so ``m`` is [B][V].
+* Eq. 2: the masked tensor is decomposed into a coordinate list C' of
+  (frame b, vertex x) pairs and the feature rows S' of the non-zero entries.
+  The list order is (b, x) ascending (the paper leaves it open).
+* Eqs. 4-5: a sparse convolution produces output only at the active centre
+  coordinate and sums, over the kernel slots, the slot weight times the
+  feature of the neighbour that slot points at, where that neighbour is
+  present in C_k.  On a mesh the slots are the 9 neighbour positions of
+  ``nbr[v]``; every slot carries a C_in x C_out channel-mixing matrix W[j]
+  (the paper's scalar slot weight is the special case W[j] = w_j * I).
+* Eq. 6: the sparse linear layer maps each feature row through W_l and adds
+  b; coordinates are unchanged.
+* Eq. 10: an activation acts elementwise on the feature rows.
+* Pooling is named alongside the other sparse layers but not defined; here
+  it is the maximum over the active rows of each body / frame, 0 for a body
+  with no active row.
+
+Every layer is computed the plain way: the DENSE operator is applied to the
+masked input x (.) m on all B*V rows in fp64, and the result is then read at
+the active rows.  Since a sparse operator only ever reads active rows, this
+restriction is exactly the sparse operator's result (up to rounding order).
+
+Precision: inputs are widened exactly to fp64 and all sums are fp64.  For
+bfloat16 stacks each layer output is rounded to bfloat16 (round to nearest,
+ties to even) by :func:`round_bf16` before it feeds the next layer, which is
+how bfloat16 activations are stored between layers.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+# ----------------------------------------------------------------------------
+# Eq. 2: decomposition of the masked tensor into (C', S')
+# ----------------------------------------------------------------------------
+
+
+def compact(mask: np.ndarray):
+    """Decompose a [B][V] 0/1 mask (Eq. 2).
+
+    Returns ``coords`` int32 [N'][2] of (b, v) in row-major order, ``inv``
+    int32 [B*V] (row index of (b, v) in C', or -1 when inactive), ``row_ptr``
+    int32 [B+1] (first row of body b; row_ptr[B] = N'), and N'.
+
+    An entry is active when it is non-zero.  Row i of C' is the i-th active
+    entry in row-major order, so its index is the number of active entries
+    before it: an exclusive running count.
+    """
+    m = np.asarray(mask)
+    B, V = m.shape
+    active = (m.reshape(-1) != 0)
+    count_before = np.cumsum(active, dtype=np.int64) - active   # exclusive count
+    n = int(active.sum())
+    inv = np.where(active, count_before, -1).astype(np.int32)
+    flat = np.arange(B * V, dtype=np.int64)
+    coords = np.empty((n, 2), dtype=np.int32)
+    coords[count_before[active], 0] = flat[active] // V
+    coords[count_before[active], 1] = flat[active] % V
+    # body b starts after every active entry that precedes its first element
+    row_ptr = np.empty(B + 1, dtype=np.int32)
+    row_ptr[:B] = count_before[np.arange(B, dtype=np.int64) * V]
+    row_ptr[B] = n
+    return coords, inv, row_ptr, n
+
+
+def gather(x: np.ndarray, coords: np.ndarray, V: int) -> np.ndarray:
+    """S'[i] = x[b_i, v_i]: the feature rows of the active coordinates (Eq. 2)."""
+    x = np.asarray(x)
+    flat = coords[:, 0].astype(np.int64) * V + coords[:, 1].astype(np.int64)
+    return x[flat]
+
+
+def densify(S: np.ndarray, coords: np.ndarray, B: int, V: int) -> np.ndarray:
+    """The masked dense tensor x (.) m rebuilt from (C', S'): zeros at inactive rows."""
+    S = np.asarray(S)
+    D = np.zeros((B * V, S.shape[1]), dtype=S.dtype)
+    flat = coords[:, 0].astype(np.int64) * V + coords[:, 1].astype(np.int64)
+    D[flat] = S
+    return D
+
+
+# ----------------------------------------------------------------------------
+# dense operators (fp64) applied to the masked input
+# ----------------------------------------------------------------------------
+
+
+def dense_linear(xm: np.ndarray, W: np.ndarray, bias=None) -> np.ndarray:
+    """Eq. 6 on every row: y = x W + b  (W is [C_in][C_out]), fp64."""
+    y = np.asarray(xm, dtype=np.float64) @ np.asarray(W, dtype=np.float64)
+    if bias is not None:
+        y = y + np.asarray(bias, dtype=np.float64)[None, :]
+    return y
+
+
+def dense_conv(xm: np.ndarray, nbr: np.ndarray, W: np.ndarray, B: int, V: int,
+               bias=None) -> np.ndarray:
+    """Eqs. 4-5 on every vertex of every body, fp64.
+
+    y[b, v] = bias + sum over slots j with nbr[v, j] >= 0 of x[b, nbr[v, j]] W[j],
+    with W [K][C_in][C_out].  A slot whose neighbour index is -1 adds nothing.
+    ``xm`` is the masked input (inactive rows zero), so an inactive neighbour
+    also adds nothing -- only neighbours present in C_k contribute.
+    """
+    x = np.asarray(xm, dtype=np.float64).reshape(B, V, -1)
+    W = np.asarray(W, dtype=np.float64)
+    K = W.shape[0]
+    y = np.zeros((B, V, W.shape[2]), dtype=np.float64)
+    for j in range(K):
+        n_j = nbr[:, j].astype(np.int64)
+        has = n_j >= 0
+        contrib = x[:, np.where(has, n_j, 0), :] @ W[j]       # [B][V][C_out]
+        y += np.where(has[None, :, None], contrib, 0.0)
+    if bias is not None:
+        y = y + np.asarray(bias, dtype=np.float64)[None, None, :]
+    return y.reshape(B * V, -1)
+
+
+def relu(y: np.ndarray) -> np.ndarray:
+    """Eq. 10 with f_act = ReLU: y if y > 0 else 0 (NaN maps to 0)."""
+    return np.where(y > 0, y, 0.0)
+
+
+def restrict(yd: np.ndarray, coords: np.ndarray, V: int) -> np.ndarray:
+    """Read a dense result at the active coordinates (C' unchanged, Eqs. 5-6, 10)."""
+    return gather(yd, coords, V)
+
+
+# ----------------------------------------------------------------------------
+# sparse layers by their definition: dense op on x (.) m, then restriction
+# ----------------------------------------------------------------------------
+
+
+def sparse_linear(S, coords, B, V, W, bias=None, act=False):
+    """Sparse linear layer on the active rows S (Eq. 6 [+ Eq. 10])."""
+    y = dense_linear(densify(np.asarray(S, np.float64), coords, B, V), W, bias)
+    if act:
+        y = relu(y)
+    return restrict(y, coords, V)
+
+
+def sparse_conv(S, coords, B, V, nbr, W, bias=None, act=False):
+    """Sparse neighbourhood convolution on the active rows S (Eqs. 4-5 [+ Eq. 10])."""
+    y = dense_conv(densify(np.asarray(S, np.float64), coords, B, V), nbr, W, B, V, bias)
+    if act:
+        y = relu(y)
+    return restrict(y, coords, V)
+
+
+def sparse_linear_scale(S, coords, B, V, W, bias=None):
+    """Abs-sum of every output's dot product: sum |s_t||w_t| + |b| (error scale)."""
+    return sparse_linear(np.abs(np.asarray(S, np.float64)), coords, B, V, np.abs(W),
+                         None if bias is None else np.abs(bias))
+
+
+def sparse_conv_scale(S, coords, B, V, nbr, W, bias=None):
+    """Abs-sum of every output's dot product over all slots (error scale)."""
+    return sparse_conv(np.abs(np.asarray(S, np.float64)), coords, B, V, nbr, np.abs(W),
+                       None if bias is None else np.abs(bias))
+
+
+def scatter(S: np.ndarray, inv: np.ndarray, zero_fill: bool = True, D=None) -> np.ndarray:
+    """Compact rows back to the dense [B*V] layout: D[r] = S[inv[r]] if active.
+
+    With zero_fill, inactive rows become 0 (this is y (.) m); otherwise they
+    keep the contents of ``D``.
+    """
+    S = np.asarray(S)
+    if D is None:
+        D = np.zeros((inv.shape[0], S.shape[1]), dtype=S.dtype)
+    else:
+        D = np.array(D, copy=True)
+    act = inv >= 0
+    if zero_fill:
+        D[~act] = 0
+    D[act] = S[inv[act]]
+    return D
+
+
+def segment_max(S: np.ndarray, row_ptr: np.ndarray, empty_value: float = 0.0) -> np.ndarray:
+    """Per-body maximum over its active rows (the paper's sparse pooling).
+
+    P[b, c] = max over row_ptr[b] <= i < row_ptr[b+1] of S[i, c], ignoring NaN
+    (IEEE maxNum), and ``empty_value`` for a body with no active row.
+    """
+    S = np.asarray(S)
+    B = row_ptr.shape[0] - 1
+    P = np.full((B, S.shape[1]), empty_value, dtype=S.dtype)
+    for b in range(B):
+        lo, hi = int(row_ptr[b]), int(row_ptr[b + 1])
+        if hi > lo:
+            P[b] = np.fmax.reduce(S[lo:hi], axis=0)
+    return P
+
+
+# ----------------------------------------------------------------------------
+# bfloat16 rounding (storage of bf16 activations between layers)
+# ----------------------------------------------------------------------------
+
+_BF16_SIG_BITS = 8            # 1 implicit + 7 stored significand bits
+_BF16_EMIN = -126             # smallest normal exponent (shared with fp32)
+_BF16_MAX = (2.0 - 2.0 ** -7) * 2.0 ** 127
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round fp64 values to the nearest bfloat16 value, ties to even (fp64 out).
+
+    A bfloat16 number has 8 significant bits and fp32's exponent range.  For
+    a finite x with 2^e <= |x| < 2^(e+1) the spacing of representable values
+    is 2^(e-7), or 2^(-133) below the normal range; x is divided by that
+    spacing, rounded half-to-even to an integer (np.rint) and scaled back.
+    Results past the largest finite value round to +-inf the IEEE way: a
+    value at or above max + half a spacing overflows.  NaN stays NaN.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    out = np.array(x, copy=True)
+    fin = np.isfinite(x) & (x != 0)
+    ax = np.abs(x[fin])
+    _, e = np.frexp(ax)                      # ax = f * 2^e, 0.5 <= f < 1
+    e = e - 1                                # 2^e <= ax < 2^(e+1)
+    e = np.maximum(e, _BF16_EMIN)            # subnormals share the min spacing
+    spacing_exp = e - (_BF16_SIG_BITS - 1)
+    q = np.rint(np.ldexp(ax, -spacing_exp))  # exact scaling, RNE to integer
+    r = np.ldexp(q, spacing_exp)
+    overflow_at = _BF16_MAX + 2.0 ** (127 - _BF16_SIG_BITS)   # max + half spacing
+    r = np.where(ax >= overflow_at, np.inf, r)
+    out[fin] = np.sign(x[fin]) * r
+    return out
+
+
+def round_f32(x: np.ndarray) -> np.ndarray:
+    """Round fp64 values to fp32 storage (IEEE conversion), returned as fp64."""
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def store(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round to the storage dtype ('f32' or 'bf16'); values returned as fp64."""
+    if dtype == "bf16":
+        return round_bf16(x)
+    if dtype == "f32":
+        return round_f32(x)
+    raise ValueError(dtype)
+
+
+# ----------------------------------------------------------------------------
+# stacks: x^{l+1} = act(op_l(x^l (.) m)) (.) m, active set fixed (C'_k = C_k)
+# ----------------------------------------------------------------------------
+
+
+def run_stack(x, mask, nbr, layers, dtype: str, pool: bool = False):
+    """Evaluate a whole sparse stack from the dense input and the mask.
+
+    ``layers`` is a sequence of (kind, W, bias, relu) with kind 'conv' or
+    'linear'.  Returns a dict with coords/inv/row_ptr/n, the active rows
+    after every layer (stored-dtype values, fp64) and, if ``pool``, the
+    per-body maximum of the last layer.
+    """
+    mask = np.asarray(mask)
+    B, V = mask.shape
+    coords, inv, row_ptr, n = compact(mask)
+    S = gather(np.asarray(x, np.float64), coords, V)
+    outs = []
+    for kind, W, bias, act in layers:
+        if kind == "conv":
+            y = sparse_conv(S, coords, B, V, nbr, W, bias, act)
+        elif kind == "linear":
+            y = sparse_linear(S, coords, B, V, W, bias, act)
+        else:
+            raise ValueError(kind)
+        S = store(y, dtype)
+        outs.append(S)
+    res = dict(coords=coords, inv=inv, row_ptr=row_ptr, n=n, outs=outs)
+    if pool:
+        res["pool"] = segment_max(S, row_ptr, 0.0)
+    return res

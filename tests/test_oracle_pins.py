@@ -1,0 +1,458 @@
+"""Pins of the CPU oracle against facts other than its own formulas.
+
+Each operator of the oracle is checked against something that does not reuse
+its code: a library routine that computes the same thing by another route
+(numpy.flatnonzero, scipy.sparse products, numpy.maximum.reduceat, torch's
+bfloat16 conversion), exact rational arithmetic, closed forms and special
+cases the paper's definitions reduce to, invariants (linearity, relabelling
+equivariance, masking), and pure-Python brute force on tiny meshes.  The
+cases are chosen so that a dropped term, a wrong sign, a wrong index or a
+transposed operand in the oracle makes at least one of them fail.
+"""
+import itertools
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+import torch
+
+from oracle import shc_oracle as O
+
+RNG = np.random.default_rng(20240611)
+
+
+def rand_nbr(V, K, rng, p_missing=0.15, self_first=True):
+    """Random neighbour lists with -1 holes (not a geometric kNN on purpose)."""
+    nbr = rng.integers(0, V, size=(V, K)).astype(np.int32)
+    nbr[rng.random((V, K)) < p_missing] = -1
+    if self_first:
+        nbr[:, 0] = np.arange(V)
+    return nbr
+
+
+# ----------------------------------------------------------------------------
+# compaction (Eq. 2)
+# ----------------------------------------------------------------------------
+
+
+def brute_compact(m):
+    B, V = len(m), len(m[0])
+    coords, inv, row_ptr = [], [-1] * (B * V), []
+    for b in range(B):
+        row_ptr.append(len(coords))
+        for v in range(V):
+            if m[b][v] != 0:
+                inv[b * V + v] = len(coords)
+                coords.append((b, v))
+    row_ptr.append(len(coords))
+    return coords, inv, row_ptr
+
+
+@pytest.mark.parametrize("B,V", [(1, 10), (3, 4)])
+def test_compact_exhaustive_tiny(B, V):
+    n_bits = B * V
+    for code in range(1 << n_bits):
+        m = np.array([(code >> k) & 1 for k in range(n_bits)], dtype=np.uint8).reshape(B, V)
+        coords, inv, row_ptr, n = O.compact(m)
+        bc, binv, brp = brute_compact(m.tolist())
+        assert n == len(bc)
+        assert [tuple(r) for r in coords.tolist()] == bc
+        assert inv.tolist() == binv
+        assert row_ptr.tolist() == brp
+
+
+@pytest.mark.parametrize("B,V,p", [(5, 655, 0.1), (2, 10475, 0.05), (7, 33, 0.0),
+                                   (4, 17, 1.0), (1, 1, 1.0), (300, 3, 0.5)])
+def test_compact_vs_flatnonzero(B, V, p):
+    m = (RNG.random((B, V)) < p).astype(np.uint8)
+    m[m != 0] = RNG.integers(1, 256, size=int(m.sum()))     # any non-zero byte is active
+    coords, inv, row_ptr, n = O.compact(m)
+    nz = np.flatnonzero(m.ravel())
+    b, v = np.divmod(nz, V)
+    assert n == nz.size
+    assert np.array_equal(coords[:, 0], b) and np.array_equal(coords[:, 1], v)
+    expect_rp = np.concatenate([[0], np.cumsum((m != 0).sum(1))])
+    assert np.array_equal(row_ptr, expect_rp)
+    # invariants
+    assert np.array_equal(inv[nz], np.arange(n))
+    assert np.all(inv[m.ravel() == 0] == -1)
+    assert np.all(np.diff(row_ptr) == (m != 0).sum(1))
+
+
+# ----------------------------------------------------------------------------
+# gather / scatter
+# ----------------------------------------------------------------------------
+
+
+def test_scatter_gather_roundtrip():
+    B, V, C = 3, 50, 8
+    m = (RNG.random((B, V)) < 0.3).astype(np.uint8)
+    x = RNG.standard_normal((B * V, C)).astype(np.float32)
+    coords, inv, row_ptr, n = O.compact(m)
+    S = O.gather(x, coords, V)
+    D = O.scatter(S, inv, zero_fill=True)
+    assert np.array_equal(D, x * m.reshape(-1, 1))               # scatter o gather = x (.) m
+    assert np.array_equal(O.gather(D, coords, V), S)             # gather o scatter = id
+    # active-only scatter leaves inactive rows untouched
+    sentinel = np.full_like(x, np.nan)
+    D2 = O.scatter(S, inv, zero_fill=False, D=sentinel)
+    assert np.all(np.isnan(D2[inv < 0])) and np.array_equal(D2[inv >= 0], S)
+    assert np.array_equal(O.densify(S, coords, B, V), D)
+
+
+# ----------------------------------------------------------------------------
+# linear layer (Eq. 6)
+# ----------------------------------------------------------------------------
+
+
+def test_linear_density_one_is_library_linear():
+    B, V, Ci, Co = 2, 30, 16, 24
+    x = RNG.standard_normal((B * V, Ci))
+    W = RNG.standard_normal((Ci, Co))
+    b = RNG.standard_normal(Co)
+    m = np.ones((B, V), np.uint8)
+    coords, inv, rp, n = O.compact(m)
+    got = O.sparse_linear(O.gather(x, coords, V), coords, B, V, W, b)
+    ref = torch.nn.functional.linear(torch.from_numpy(x), torch.from_numpy(W.T.copy()),
+                                     torch.from_numpy(b)).numpy()
+    np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-13)
+
+
+def test_linear_rows_are_independent_and_masked():
+    B, V, Ci, Co = 2, 40, 8, 8
+    m = (RNG.random((B, V)) < 0.3).astype(np.uint8)
+    coords, inv, rp, n = O.compact(m)
+    S = RNG.standard_normal((n, Ci))
+    W = RNG.standard_normal((Ci, Co))
+    b = RNG.standard_normal(Co)
+    got = O.sparse_linear(S, coords, B, V, W, b, act=True)
+    # closed form per row, in pure Python
+    for i in range(n):
+        for c in range(Co):
+            acc = b[c] + sum(float(S[i, k]) * float(W[k, c]) for k in range(Ci))
+            assert got[i, c] == pytest.approx(max(acc, 0.0), rel=1e-12, abs=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# convolution (Eqs. 4-5)
+# ----------------------------------------------------------------------------
+
+
+def brute_conv(x, m, nbr, W, bias, B, V, act):
+    """Pure-Python loops: output at active (b, v) only, neighbours present in C."""
+    K, Ci, Co = W.shape
+    rows = []
+    for b in range(B):
+        for v in range(V):
+            if not m[b][v]:
+                continue
+            out = []
+            for c in range(Co):
+                acc = 0.0 if bias is None else float(bias[c])
+                for j in range(K):
+                    u = int(nbr[v][j])
+                    if u < 0 or not m[b][u]:
+                        continue
+                    for k in range(Ci):
+                        acc += float(x[b * V + u][k]) * float(W[j][k][c])
+                out.append(max(acc, 0.0) if act else acc)
+            rows.append(out)
+    return np.array(rows, dtype=np.float64).reshape(-1, Co)
+
+
+@pytest.mark.parametrize("B,V,K,Ci,Co,p", [(1, 6, 3, 2, 3, 0.6), (3, 11, 9, 4, 2, 0.5),
+                                           (2, 24, 5, 8, 3, 0.3), (2, 9, 1, 3, 5, 1.0)])
+def test_conv_brute_force_tiny(B, V, K, Ci, Co, p):
+    rng = np.random.default_rng(B * 100 + V)
+    m = (rng.random((B, V)) < p).astype(np.uint8)
+    nbr = rand_nbr(V, K, rng)
+    x = rng.standard_normal((B * V, Ci))
+    W = rng.standard_normal((K, Ci, Co))
+    bias = rng.standard_normal(Co)
+    coords, inv, rp, n = O.compact(m)
+    for act in (False, True):
+        got = O.sparse_conv(O.gather(x, coords, V), coords, B, V, nbr, W, bias, act)
+        ref = brute_conv(x, m, nbr, W, bias, B, V, act)
+        np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_conv_equals_scipy_sparse_adjacency_products():
+    """y_b = sum_j A_j (x_b (.) m_b) W_j with A_j[v, nbr[v,j]] = 1 (scipy sparse)."""
+    B, V, K, Ci, Co = 3, 200, 9, 6, 7
+    m = (RNG.random((B, V)) < 0.25).astype(np.uint8)
+    nbr = rand_nbr(V, K, RNG)
+    x = RNG.standard_normal((B * V, Ci))
+    W = RNG.standard_normal((K, Ci, Co))
+    coords, inv, rp, n = O.compact(m)
+    got = O.sparse_conv(O.gather(x, coords, V), coords, B, V, nbr, W)
+    ref_rows = []
+    for b in range(B):
+        xb = x[b * V:(b + 1) * V] * m[b][:, None]
+        yb = np.zeros((V, Co))
+        for j in range(K):
+            valid = nbr[:, j] >= 0
+            A = sp.csr_matrix((np.ones(valid.sum()), (np.flatnonzero(valid), nbr[valid, j])),
+                              shape=(V, V))
+            yb += A @ xb @ W[j]
+        ref_rows.append(yb[m[b] != 0])
+    np.testing.assert_allclose(got, np.concatenate(ref_rows), rtol=1e-12, atol=1e-12)
+
+
+def test_conv_density_one_is_concatenated_spiral_conv():
+    """At density 1 the conv equals concat_j(x[nbr(v, j)]) @ W.reshape(K*Ci, Co)."""
+    B, V, K, Ci, Co = 2, 64, 9, 5, 3
+    nbr = rand_nbr(V, K, RNG)
+    x = RNG.standard_normal((B * V, Ci))
+    W = RNG.standard_normal((K, Ci, Co))
+    m = np.ones((B, V), np.uint8)
+    coords, inv, rp, n = O.compact(m)
+    got = O.sparse_conv(O.gather(x, coords, V), coords, B, V, nbr, W)
+    xpad = np.concatenate([x.reshape(B, V, Ci), np.zeros((B, 1, Ci))], axis=1)
+    idx = np.where(nbr >= 0, nbr, V)                   # -1 -> the zero row
+    cat = xpad[:, idx, :].reshape(B * V, K * Ci)
+    np.testing.assert_allclose(got, cat @ W.reshape(K * Ci, Co), rtol=1e-12, atol=1e-12)
+
+
+def test_conv_single_self_slot_is_linear():
+    B, V, Ci, Co = 2, 40, 6, 4
+    m = (RNG.random((B, V)) < 0.5).astype(np.uint8)
+    coords, inv, rp, n = O.compact(m)
+    S = RNG.standard_normal((n, Ci))
+    W = RNG.standard_normal((Ci, Co))
+    b = RNG.standard_normal(Co)
+    self_nbr = np.arange(V, dtype=np.int32)[:, None]
+    got = O.sparse_conv(S, coords, B, V, self_nbr, W[None], b, act=True)
+    ref = np.maximum(S @ W + b, 0.0)
+    np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-13)
+
+
+def test_conv_lone_active_vertex_sees_only_itself():
+    V, K, Ci, Co = 30, 9, 4, 3
+    nbr = rand_nbr(V, K, RNG, p_missing=0.0)
+    nbr[7, 3] = 7                                   # self also in a second slot
+    m = np.zeros((1, V), np.uint8)
+    m[0, 7] = 1
+    x = RNG.standard_normal((V, Ci))
+    W = RNG.standard_normal((K, Ci, Co))
+    b = RNG.standard_normal(Co)
+    coords, inv, rp, n = O.compact(m)
+    got = O.sparse_conv(O.gather(x, coords, V), coords, 1, V, nbr, W, b)
+    selfslots = [j for j in range(K) if nbr[7, j] == 7]
+    ref = b + sum(x[7] @ W[j] for j in selfslots)
+    np.testing.assert_allclose(got[0], ref, rtol=1e-13, atol=1e-13)
+
+
+def test_conv_is_linear_in_features():
+    B, V, K, Ci, Co = 2, 50, 9, 4, 5
+    m = (RNG.random((B, V)) < 0.4).astype(np.uint8)
+    nbr = rand_nbr(V, K, RNG)
+    coords, inv, rp, n = O.compact(m)
+    W = RNG.standard_normal((K, Ci, Co))
+    S1, S2 = RNG.standard_normal((n, Ci)), RNG.standard_normal((n, Ci))
+    a = -1.75
+    lhs = O.sparse_conv(a * S1 + S2, coords, B, V, nbr, W)
+    rhs = a * O.sparse_conv(S1, coords, B, V, nbr, W) + O.sparse_conv(S2, coords, B, V, nbr, W)
+    np.testing.assert_allclose(lhs, rhs, rtol=1e-11, atol=1e-11)
+
+
+def test_conv_relabelling_equivariance():
+    """Renumbering the vertices renumbers the outputs and nothing else."""
+    B, V, K, Ci, Co = 2, 45, 9, 3, 4
+    rng = np.random.default_rng(5)
+    m = (rng.random((B, V)) < 0.5).astype(np.uint8)
+    nbr = rand_nbr(V, K, rng)
+    x = rng.standard_normal((B * V, Ci))
+    W = rng.standard_normal((K, Ci, Co))
+    perm = rng.permutation(V)                      # new label of old vertex u is perm[u]
+    inv_perm = np.argsort(perm)
+    nbr2 = np.where(nbr[inv_perm] >= 0, perm[np.maximum(nbr[inv_perm], 0)], -1).astype(np.int32)
+    m2 = m[:, inv_perm]
+    x2 = x.reshape(B, V, Ci)[:, inv_perm].reshape(B * V, Ci)
+    c1, _, _, _ = O.compact(m)
+    c2, _, _, _ = O.compact(m2)
+    y1 = O.sparse_conv(O.gather(x, c1, V), c1, B, V, nbr, W)
+    y2 = O.sparse_conv(O.gather(x2, c2, V), c2, B, V, nbr2, W)
+    d1 = O.densify(y1, c1, B, V).reshape(B, V, Co)
+    d2 = O.densify(y2, c2, B, V).reshape(B, V, Co)
+    np.testing.assert_allclose(d2, d1[:, inv_perm], rtol=1e-12, atol=1e-12)
+
+
+def test_conv_scalar_slot_weights_match_paper_eq5_literal():
+    """W[j] = w_j * I gives the paper's scalar form: sum_j w_j * s[idx(nbr(v, j))]."""
+    B, V, K, C = 2, 40, 9, 6
+    rng = np.random.default_rng(9)
+    m = (rng.random((B, V)) < 0.35).astype(np.uint8)
+    nbr = rand_nbr(V, K, rng)
+    w = rng.standard_normal(K)
+    x = rng.standard_normal((B * V, C))
+    coords, inv, rp, n = O.compact(m)
+    S = O.gather(x, coords, V)
+    got = O.sparse_conv(S, coords, B, V, nbr, w[:, None, None] * np.eye(C)[None])
+    ref = np.zeros_like(S)
+    for i, (b, v) in enumerate(coords):
+        for j in range(K):
+            u = nbr[v, j]
+            if u >= 0 and inv[b * V + u] >= 0:
+                ref[i] += w[j] * S[inv[b * V + u]]
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_conv_abs_scale_bounds_output():
+    B, V, K, Ci, Co = 2, 60, 9, 8, 8
+    m = (RNG.random((B, V)) < 0.3).astype(np.uint8)
+    nbr = rand_nbr(V, K, RNG)
+    coords, inv, rp, n = O.compact(m)
+    S = RNG.standard_normal((n, Ci))
+    W = RNG.standard_normal((K, Ci, Co))
+    b = RNG.standard_normal(Co)
+    y = O.sparse_conv(S, coords, B, V, nbr, W, b)
+    s = O.sparse_conv_scale(S, coords, B, V, nbr, W, b)
+    assert np.all(np.abs(y) <= s * (1 + 1e-12))
+    # all-positive data: the scale is the output itself
+    yp = O.sparse_conv(np.abs(S), coords, B, V, nbr, np.abs(W), np.abs(b))
+    np.testing.assert_allclose(yp, s, rtol=1e-13)
+
+
+# ----------------------------------------------------------------------------
+# pooling
+# ----------------------------------------------------------------------------
+
+
+def test_segment_max_vs_reduceat_and_empty_segments():
+    B, V, C = 40, 25, 7
+    m = (RNG.random((B, V)) < 0.1).astype(np.uint8)
+    m[3] = 0
+    m[17] = 0
+    coords, inv, rp, n = O.compact(m)
+    S = RNG.standard_normal((n, C)).astype(np.float32)
+    P = O.segment_max(S, rp, empty_value=-5.0)
+    nonempty = np.flatnonzero(np.diff(rp) > 0)
+    ref = np.maximum.reduceat(S, rp[nonempty], axis=0)
+    assert np.array_equal(P[nonempty], ref)
+    empty = np.flatnonzero(np.diff(rp) == 0)
+    assert 3 in empty and 17 in empty
+    assert np.all(P[empty] == -5.0)
+
+
+def test_segment_max_ignores_nan_and_equals_dense_pool_after_relu():
+    S = np.array([[np.nan, 1.0], [2.0, np.nan], [0.5, 0.25]], np.float32)
+    P = O.segment_max(S, np.array([0, 3]))
+    assert P.tolist() == [[2.0, 1.0]]
+    # after ReLU, the per-body max over active rows equals a dense max over all
+    # vertices of relu(y) (.) m, empty bodies included (inactive rows are 0)
+    B, V, C = 6, 20, 4
+    m = (RNG.random((B, V)) < 0.2).astype(np.uint8)
+    m[0] = 0
+    coords, inv, rp, n = O.compact(m)
+    y = np.maximum(RNG.standard_normal((n, C)), 0)
+    dense = O.densify(y, coords, B, V).reshape(B, V, C).max(axis=1)
+    assert np.array_equal(O.segment_max(y, rp), dense)
+
+
+# ----------------------------------------------------------------------------
+# bfloat16 round-to-nearest-even
+# ----------------------------------------------------------------------------
+
+
+def bf16_exact_rne(x: float) -> float:
+    """Nearest bf16 by exact rational comparison of the two bracketing values."""
+    if x == 0 or not np.isfinite(x):
+        return x
+    fx = Fraction(x)
+    ax = abs(fx)
+    e = 0
+    while ax >= 2:
+        ax /= 2
+        e += 1
+    while ax < 1:
+        ax *= 2
+        e -= 1
+    e = max(e, -126)
+    spacing = Fraction(2) ** (e - 7)
+    lo = (abs(fx) // spacing) * spacing
+    hi = lo + spacing
+    dlo, dhi = abs(fx) - lo, hi - abs(fx)
+    if dlo < dhi:
+        r = lo
+    elif dhi < dlo:
+        r = hi
+    else:
+        r = lo if (lo / spacing) % 2 == 0 else hi
+    maxf = (2 - Fraction(1, 128)) * Fraction(2) ** 127
+    if r > maxf:
+        return float(np.copysign(np.inf, x))
+    return float(r) if x > 0 else -float(r)
+
+
+def test_round_bf16_matches_torch_on_fp32_inputs():
+    vals = np.concatenate([
+        RNG.standard_normal(200000).astype(np.float32) * np.float32(7.0),
+        (RNG.standard_normal(20000) * 1e-39).astype(np.float32),          # subnormals
+        np.array([3.3895e38, 3.39e38, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -1.0 - 2 ** -8,
+                  2 ** -133, 3 * 2 ** -134, 0.0, -0.0, np.inf, -np.inf], np.float32),
+    ])
+    ref = torch.from_numpy(vals).to(torch.bfloat16).to(torch.float64).numpy()
+    got = O.round_bf16(vals.astype(np.float64))
+    assert np.array_equal(got, ref)
+
+
+def test_round_bf16_exact_rational_on_fp64_inputs():
+    vals = list(RNG.standard_normal(3000) * 10.0 ** RNG.integers(-40, 38, 3000))
+    # exact ties of the bf16 grid in fp64, and near-ties one fp64 ulp away
+    for k in range(200):
+        base = float(np.float32(RNG.standard_normal()))
+        t = float(torch.tensor(base).to(torch.bfloat16).double())
+        spacing = 2.0 ** (np.frexp(abs(t))[1] - 1 - 7) if t != 0 else 2.0 ** -133
+        tie = t + spacing / 2
+        vals += [tie, np.nextafter(tie, np.inf), np.nextafter(tie, -np.inf)]
+    got = O.round_bf16(np.array(vals))
+    ref = np.array([bf16_exact_rne(v) for v in vals])
+    assert np.array_equal(got, ref)
+    assert np.isnan(O.round_bf16(np.array([np.nan]))[0])
+
+
+# ----------------------------------------------------------------------------
+# stacks and the paper's density reading
+# ----------------------------------------------------------------------------
+
+
+def test_stack_matches_chained_brute_force_bf16():
+    B, V, K = 2, 14, 4
+    rng = np.random.default_rng(77)
+    m = (rng.random((B, V)) < 0.6).astype(np.uint8)
+    nbr = rand_nbr(V, K, rng)
+    x = torch.from_numpy(rng.standard_normal((B * V, 3))).to(torch.bfloat16).double().numpy()
+    W1 = rng.standard_normal((K, 3, 4))
+    W2 = rng.standard_normal((4, 2))
+    layers = [("conv", W1, None, True), ("linear", W2, None, True)]
+    res = O.run_stack(x, m, nbr, layers, "bf16", pool=True)
+    # chained brute force with torch's conversion between layers
+    h = brute_conv(x, m, nbr, W1, None, B, V, True)
+    h = torch.from_numpy(h).to(torch.bfloat16).double().numpy()
+    h2 = np.maximum(h @ W2, 0)
+    h2 = torch.from_numpy(h2).to(torch.bfloat16).double().numpy()
+    np.testing.assert_array_equal(res["outs"][1], h2)
+    rp = res["row_ptr"]
+    for b in range(B):
+        seg = h2[rp[b]:rp[b + 1]]
+        ref = seg.max(0) if len(seg) else np.zeros(2)
+        np.testing.assert_array_equal(res["pool"][b], ref)
+
+
+def test_density_reading_matches_table4(request):
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "table4_vertex_counts.txt")
+    kv = {}
+    for line in open(path):
+        if line.strip() and not line.startswith("#"):
+            k, v = line.split()
+            kv[k] = float(v)
+    density = 1.0 - kv["sparsity_ratio"]
+    expected = kv["vertices_dense"] * density
+    assert abs(expected - kv["vertices_processed_one_mask"]) < 1.0
+    B = 4000
+    m = (np.random.default_rng(3).random((B, int(kv["vertices_dense"]))) < density)
+    _, _, rp, n = O.compact(m.astype(np.uint8))
+    sigma = np.sqrt(kv["vertices_dense"] * density * (1 - density) / B)
+    assert abs(n / B - expected) < 4 * sigma
