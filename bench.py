@@ -1,0 +1,273 @@
+#!/usr/bin/env python3
+"""Benchmark of the sparse contact-layer path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input:
+
+    mask compaction -> gather of the active rows -> sparse linear + ReLU ->
+    sparse 9-slot neighbourhood conv + ReLU -> zero-fill scatter + per-body max-pool
+
+on the density-sweep workload at 5% density: B = 128 bodies, V = 10475 mesh
+vertices (ellipsoid, exact 9-NN), C = 128 bf16 channels, i.i.d. Bernoulli(0.05)
+mask.  `value` is active-vertex rows per second per sparse layer over the whole
+step: N' * (number of sparse layers) / step time, with every input resident in
+HBM when the timed region starts.  The line also carries the roofline of the
+dominant kernel (HIP events on the stream it runs on), the speed-up of each
+sparse layer over the same layer run densely on all B*V rows, and the CPU
+oracle timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_conv_c4_5pct.txt")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_09388_amd", "csrc", "gemm.hip")
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--density", type=float, default=0.05)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-dense", action="store_true", help="skip the dense-layer comparison")
+    p.add_argument("--cpu-seconds", type=float, default=15.0)
+    return p.parse_args()
+
+
+def algorithmic_conv(w, coords, inv, n, e):
+    """Bytes and useful flops the conv must move/do for N' rows (per launch)."""
+    K, Cin, Cout = w.layers[1].W.shape
+    b = coords[:, 0].astype(np.int64)
+    v = coords[:, 1].astype(np.int64)
+    present = 0
+    for j in range(K):
+        u = w.nbr[v, j].astype(np.int64)
+        present += int(np.count_nonzero((u >= 0) & (inv[b * w.V + np.maximum(u, 0)] >= 0)))
+    bytes_ = (present * Cin * e        # present neighbour rows read
+              + n * 8 * K              # nbr + inv lookups per slot
+              + n * 8                  # coords
+              + n * Cout * e           # output rows
+              + K * Cin * Cout * e)    # weights once
+    flops = 2.0 * present * Cin * Cout
+    return bytes_, flops, present / (n * K)
+
+
+def traffic_from_profile():
+    """HBM bytes per conv launch from the committed rocprofv3 counter summary,
+    or None if absent or taken on a different version of the kernel source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.lstrip().startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    if kv.get("kernel_source_sha256") != src or "hbm_bytes_per_launch" not in kv:
+        return None
+    return float(kv["hbm_bytes_per_launch"])
+
+
+def cpu_baseline(w, layers_spec, budget_s):
+    """The oracle as it stands on a bounded sample of bodies of the same workload."""
+    import threadpoolctl
+    from oracle import shc_oracle as O
+
+    def run(nb):
+        t = time.perf_counter()
+        r = O.run_stack(w.x[: nb * w.V], w.mask[:nb], w.nbr, layers_spec, w.dtype, pool=True)
+        O.scatter(r["outs"][-1], r["inv"], zero_fill=True)
+        return time.perf_counter() - t, r["n"]
+
+    t1, _ = run(1)
+    nb = int(max(1, min(w.B, budget_s / max(t1, 1e-3))))
+    t, n = run(nb)
+    info = threadpoolctl.threadpool_info()
+    cores = max([i.get("num_threads", 1) for i in info] + [1])
+    return {"value": n * len(layers_spec) / t, "unit": "active-vertex rows/s per sparse layer",
+            "cores": cores, "kind": "oracle",
+            "sample": f"{nb} of {w.B} bodies ({n} active rows), full step, {t:.1f} s, fp64 numpy"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the path is single-GPU; sharding across GPUs is described, not built)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_09388_amd import binding as shc
+    from paper_2608_09388_amd import synth
+    from paper_2608_09388_amd.pipeline import SparseStack
+
+    shc.load()
+    dev = torch.device("cuda:0")
+    w = synth.workload_c4(args.density)
+    st = SparseStack(w, device="cuda:0")
+    n = st.compact()
+    L = len(w.layers)
+    stream = torch.cuda.current_stream()
+
+    names = ["compact", "gather", "linear", "conv", "scatter", "pool"]
+
+    def timed_step(ev):
+        ev[0].record(stream)
+        st.compact()
+        ev[1].record(stream)
+        st.gather()
+        ev[2].record(stream)
+        st.layer(0)
+        ev[3].record(stream)
+        st.layer(1)
+        ev[4].record(stream)
+        shc.scatter(st.acts[-1], st.inv, st.coords, st.n, st.B, st.V, st.dense_out, True)
+        ev[5].record(stream)
+        shc.segment_maxpool(st.acts[-1], st.row_ptr, st.n, st.B, st.pooled, 0.0)
+        ev[6].record(stream)
+
+    for _ in range(args.warmup):
+        st.step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        timed_step(events[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_kernel_ms = {}
+    for k, name in enumerate(names):
+        per_kernel_ms[name] = float(np.mean([events[s][k].elapsed_time(events[s][k + 1])
+                                             for s in range(args.steps)]))
+    ms_per_step = wall * 1e3 / args.steps
+    value = n * L / (ms_per_step / 1e3)
+
+    # roofline of the dominant kernel (the conv layer)
+    coords = st.coords[:n].cpu().numpy()
+    inv = st.inv.cpu().numpy()
+    e = 2
+    cbytes, cflops, a_present = algorithmic_conv(w, coords, inv, n, e)
+    conv_s = per_kernel_ms["conv"] / 1e3
+    ridge = BF16_MFMA_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    traffic = traffic_from_profile()
+    if cflops / cbytes < ridge:
+        ach = cbytes / conv_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": traffic}
+    else:
+        ach = cflops / conv_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(ach / BF16_MFMA_PEAK_TFLOPS, 4),
+                "traffic": traffic}
+    roof["kernel"] = "sparse_neighbor_conv (gather_gemm_kernel<bf16,128,conv>)"
+    roof["algorithmic_bytes"] = int(cbytes)
+    roof["useful_flops"] = cflops
+    roof["executed_slot_gemm_flops"] = 2.0 * n * 9 * 128 * 128
+    roof["present_slot_fraction"] = round(a_present, 4)
+    roof["launch_us"] = round(per_kernel_ms["conv"] * 1e3, 2)
+
+    out = {
+        "metric": "active-vertex rows/sec per sparse contact layer; speed-up vs dense layer",
+        "value": round(value, 1),
+        "unit": "active-vertex rows/s per sparse layer",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"density sweep point p={args.density:g}: B=128 bodies, "
+                               f"V=10475 ellipsoid mesh, K=9 exact kNN, C=128->128 bf16, "
+                               f"sparse linear + sparse conv (+ReLU), scatter + max-pool",
+                   "B": w.B, "V": w.V, "K": w.K, "C": 128, "density": args.density,
+                   "n_active": n, "sparse_layers": L, "parallelism": "single GPU"},
+        "per_kernel_us": {k: round(v * 1e3, 2) for k, v in per_kernel_ms.items()},
+        "roofline": roof,
+    }
+
+    if not args.no_dense:
+        out["speedup_vs_dense"] = dense_comparison(st, w, per_kernel_ms, torch, shc, synth)
+    if not args.no_cpu_baseline:
+        spec = [(l.kind, l.W, l.bias, l.relu) for l in w.layers]
+        out["cpu_baseline"] = cpu_baseline(w, spec, args.cpu_seconds)
+    print(json.dumps(out))
+
+
+def dense_comparison(st, w, per_kernel_ms, torch, shc, synth):
+    """Each sparse layer against the same layer run densely on all B*V rows:
+    (i) this library's kernels with every vertex active, (ii) PyTorch-ROCm
+    (hipBLASLt) matmul, with an index_select for the conv."""
+    import copy
+    from paper_2608_09388_amd.pipeline import SparseStack
+
+    wd = copy.copy(w)
+    wd.mask = np.ones_like(w.mask)
+    sd = SparseStack(wd, device="cuda:0")
+    sd.compact()
+    sd.gather()
+
+    def time_it(fn, reps=10):
+        for _ in range(3):
+            fn()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s.record()
+        for _ in range(reps):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / reps
+
+    t_lin_own = time_it(lambda: sd.layer(0))
+    t_conv_own = time_it(lambda: sd.layer(1))
+    x = sd.acts[1]
+    Wl = sd.weights[0]
+    Wc = sd.weights[1].reshape(-1, sd.weights[1].shape[-1]).contiguous()
+    nbr_flat = sd.nbr.long()
+    BV = w.B * w.V
+
+    def torch_linear():
+        torch.relu(x @ Wl)
+
+    def torch_conv():
+        xg = x.view(w.B, w.V, -1)[:, nbr_flat.view(-1)].reshape(BV, -1)
+        torch.relu(xg @ Wc)
+
+    t_lin_t = time_it(torch_linear, 5)
+    t_conv_t = time_it(torch_conv, 5)
+    res = {
+        "linear": {"sparse_us": round(per_kernel_ms["linear"] * 1e3, 2),
+                   "dense_own_kernel_us": round(t_lin_own * 1e3, 2),
+                   "dense_torch_hipblaslt_us": round(t_lin_t * 1e3, 2),
+                   "speedup_vs_own_dense": round(t_lin_own / per_kernel_ms["linear"], 2),
+                   "speedup_vs_torch_dense": round(t_lin_t / per_kernel_ms["linear"], 2)},
+        "conv": {"sparse_us": round(per_kernel_ms["conv"] * 1e3, 2),
+                 "dense_own_kernel_us": round(t_conv_own * 1e3, 2),
+                 "dense_torch_gather_matmul_us": round(t_conv_t * 1e3, 2),
+                 "speedup_vs_own_dense": round(t_conv_own / per_kernel_ms["conv"], 2),
+                 "speedup_vs_torch_dense": round(t_conv_t / per_kernel_ms["conv"], 2)},
+        "dense_rows": BV,
+    }
+    del sd
+    torch.cuda.empty_cache()
+    return res
+
+
+if __name__ == "__main__":
+    main()

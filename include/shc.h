@@ -1,0 +1,181 @@
+/*
+ * shc.h -- sparse contact-layer operators on one AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of libshc.so.  The operators follow Sec. 3 of "Efficient Human-Contact
+ * Representation for Human-Scene Interaction" (ECO, arXiv 2608.09388):
+ *
+ *   Eq. 1    a 0/1 contact mask multiplies the per-vertex input;
+ *   Eq. 2    the masked tensor is decomposed into a coordinate list C' of
+ *            (frame/body b, vertex v) pairs and the compact feature rows S';
+ *   Eqs. 4-5 the sparse convolution is evaluated only at active centre
+ *            coordinates, summing slot weight x neighbour feature over the
+ *            kernel slots whose neighbour is present in C;
+ *   Eq. 6    the sparse linear layer maps every feature row, C unchanged;
+ *   Eq. 10   activations act elementwise on the rows, C unchanged;
+ *   pooling  (named with the sparse layers, Sec. 3.2) is a per-body maximum.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - All array arguments are DEVICE pointers (memory on the current HIP device)
+ *   unless the comment says "host".  The caller owns every buffer; the library
+ *   keeps no pointer after the work it enqueues has run, allocates nothing and
+ *   holds no state between calls.
+ * - Every call validates its arguments on the host, then enqueues its kernels
+ *   on `stream` and returns without waiting (the one exception is the optional
+ *   host count of shc_compact_mask).  Calls are thread-safe.
+ * - Layouts are row-major and contiguous.  Feature rows hold C channels of
+ *   `dtype`: SHC_F32 (IEEE binary32) or SHC_BF16 (bfloat16 stored as uint16).
+ *   Features, weights and outputs of one call share the dtype; bias is always
+ *   fp32; products are accumulated in fp32; bf16 outputs are rounded to
+ *   nearest, ties to even.
+ * - Every device pointer must be 16-byte aligned (SHC_ERR_MISALIGNED), and
+ *   channel counts must be multiples of 16 in [16, 4096] (SHC_ERR_UNSUPPORTED).
+ * - Index arrays are int32.  C' is ordered by (b, v) ascending; inv[b*V + v]
+ *   is the row of (b, v) in C' or -1; row_ptr[b] is the first row of body b
+ *   and row_ptr[B] = N'.  B*V must be below 2^31.
+ * - Index entries outside their valid range (a neighbour outside [-1, V), an
+ *   inv entry outside [-1, n_rows), a coordinate outside [0, B) x [0, V)) are
+ *   treated as absent rows, never dereferenced.
+ * - Inputs and outputs of one call must not overlap.
+ * - Return value: SHC_OK (0) or a negative SHC_ERR_* code.  Nothing is
+ *   launched when validation fails.  SHC_ERR_HIP reports a HIP runtime or
+ *   launch failure; shc_last_error() then holds the message (thread-local).
+ */
+#ifndef SHC_H_
+#define SHC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* dtype codes */
+#define SHC_F32 0
+#define SHC_BF16 1
+
+/* activation codes (Eq. 10) */
+#define SHC_ACT_NONE 0
+#define SHC_ACT_RELU 1 /* y if y > 0 else 0 */
+
+/* status codes */
+#define SHC_OK 0
+#define SHC_ERR_INVALID_ARG (-1) /* NULL pointer, negative or zero size, bad flag */
+#define SHC_ERR_CAPACITY (-2)    /* workspace too small, or N' above `cap` */
+#define SHC_ERR_MISALIGNED (-3)  /* a device pointer is not 16-byte aligned */
+#define SHC_ERR_UNSUPPORTED (-4) /* channels not a multiple of 16, K > 32, dtype/act code */
+#define SHC_ERR_HIP (-5)         /* HIP runtime or launch failure */
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* shc_status_string(int status);
+
+/* Detail of the last failure on this thread ("" if none). */
+const char* shc_last_error(void);
+
+/* Bytes of device workspace shc_compact_mask needs for a B x V mask. */
+size_t shc_compact_mask_workspace(int32_t B, int32_t V);
+
+/*
+ * Mask compaction -- the decomposition of Eq. 2 (Sec. 3.1), for the per-vertex
+ * mask of Eq. 1 given per body/frame.
+ *
+ *   mask      [B*V] uint8, entry (b, v) is active when non-zero.
+ *   coords    [cap][2] int32 out: row i of C' is (b_i, v_i), rows in (b, v)
+ *             ascending order; only the first min(N', cap) rows are written.
+ *   inv       [B*V] int32 out: row of (b, v) in C', or -1.  Entries whose row
+ *             would be >= cap are still written with that row number.
+ *   row_ptr   [B+1] int32 out: first row of every body, row_ptr[B] = N'.
+ *   n_active_dev  [1] int32 out: N'.
+ *   n_active_host host int64*, may be NULL.  When set, the call waits for the
+ *             stream, stores N' there and returns SHC_ERR_CAPACITY if N' > cap.
+ *   cap       rows available in `coords` (>= 0).
+ *   ws, ws_bytes  device workspace of at least shc_compact_mask_workspace(B, V)
+ *             bytes; its contents on entry do not matter.
+ * Results are deterministic and bit-exact (integer work only).
+ */
+int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
+                     int32_t* row_ptr, int32_t* n_active_dev, int64_t* n_active_host, int64_t cap,
+                     void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Gather of the active feature rows -- S' of Eq. 2: S[i] = x[b_i * V + v_i].
+ *
+ *   x       [B*V][C] dense per-vertex features.
+ *   coords  [n_rows][2] from shc_compact_mask.
+ *   S       [n_rows][C] out.
+ * An exact copy; rows whose coordinate is out of range are written as zeros.
+ */
+int shc_gather_rows(const void* x, const int32_t* coords, int64_t n_rows, int32_t B, int32_t V,
+                    int32_t C, int32_t dtype, void* S, hipStream_t stream);
+
+/*
+ * Sparse linear layer -- Eq. 6 (+ Eq. 10): out[i] = act(S[i] W + bias).
+ *
+ *   S     [n_rows][Cin] active feature rows (coordinates unchanged, C' = C).
+ *   W     [Cin][Cout] (row-major: W[k][n] multiplies channel k into output n).
+ *   bias  [Cout] fp32, or NULL for none.
+ *   out   [n_rows][Cout].
+ * n_rows = 0 is a no-op.
+ */
+int shc_sparse_linear(const void* S, int64_t n_rows, const void* W, const float* bias, int32_t Cin,
+                      int32_t Cout, int32_t dtype, int32_t act, void* out, hipStream_t stream);
+
+/*
+ * Sparse neighbourhood (spiral / k-NN) convolution -- Eqs. 4-5 (+ Eq. 10),
+ * output only at the active rows:
+ *
+ *   out[i] = act( bias + sum_{j<K} S[r_ij] W[j] ),
+ *   r_ij   = inv[b_i * V + nbr[v_i * K + j]]; a slot adds nothing when its
+ *            neighbour is -1 or the neighbour vertex is inactive (r_ij = -1).
+ *
+ *   S       [n_rows][Cin] active rows, coords/inv from shc_compact_mask.
+ *   nbr     [V][K] int32 neighbour vertex of every slot, -1 for none.  The
+ *           mesh is shared by all bodies.  Slot j plays the part of kernel
+ *           position j of Eq. 4; the centre vertex is simply the slot whose
+ *           entry is v itself.
+ *   W       [K][Cin][Cout]: a Cin x Cout channel-mixing matrix per slot (the
+ *           paper's scalar slot weight w_j is the case W[j] = w_j * I).
+ *   bias    [Cout] fp32 or NULL.   K in [1, 32].
+ *   out     [n_rows][Cout], must not overlap S.
+ * n_rows = 0 is a no-op.
+ */
+int shc_sparse_neighbor_conv(const void* S, const int32_t* coords, const int32_t* inv,
+                             int64_t n_rows, int32_t B, int32_t V, const int32_t* nbr, int32_t K,
+                             const void* W, const float* bias, int32_t Cin, int32_t Cout,
+                             int32_t dtype, int32_t act, void* out, hipStream_t stream);
+
+/*
+ * Scatter back to the dense per-vertex layout (C' = C, so row i returns to
+ * (b_i, v_i)):
+ *
+ *   zero_fill = 1: D[r] = S[inv[r]] if inv[r] >= 0 else 0, for all r < B*V
+ *                  (D = y (.) m, every row of D written).
+ *   zero_fill = 0: D[b_i * V + v_i] = S[i] for i < n_rows; the rows of inactive
+ *                  vertices are left untouched.
+ *   S [n_rows][C], D [B*V][C].  An exact copy.
+ */
+int shc_scatter(const void* S, const int32_t* inv, const int32_t* coords, int64_t n_rows,
+                int32_t B, int32_t V, int32_t C, int32_t dtype, int32_t zero_fill, void* D,
+                hipStream_t stream);
+
+/*
+ * Segmented max-pool per body/frame -- the sparse pooling layer (Sec. 3.2):
+ *
+ *   P[b][c] = max over row_ptr[b] <= i < row_ptr[b+1] of S[i][c]
+ *   (IEEE maxNum: a NaN loses to any number), or `empty_value` for a body
+ *   without active rows.  Segment bounds are clamped to [0, n_rows).
+ *
+ *   S [n_rows][C], row_ptr [B+1], P [B][C] out (same dtype as S; empty_value
+ *   is converted to it).  Exact (a selection, no rounding).
+ */
+int shc_segment_maxpool(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
+                        int32_t C, int32_t dtype, float empty_value, void* P, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SHC_H_ */

@@ -1,0 +1,205 @@
+"""Python binding of libshc.so: the same entry points, torch tensors in.
+
+Argument marshalling only -- every step of the path runs in the library's HIP
+kernels.  PyTorch supplies device memory and the current HIP stream.  Before
+any call the binding checks that every tensor is on the GPU, contiguous, of
+the expected dtype and large enough for the sizes passed, so a kernel never
+sees a buffer smaller than its launch assumes.  There is no fallback: if
+libshc.so is missing or cannot be loaded, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libshc.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "shc.h")
+
+SHC_F32, SHC_BF16 = 0, 1
+SHC_ACT_NONE, SHC_ACT_RELU = 0, 1
+STATUS = {0: "SHC_OK", -1: "SHC_ERR_INVALID_ARG", -2: "SHC_ERR_CAPACITY",
+          -3: "SHC_ERR_MISALIGNED", -4: "SHC_ERR_UNSUPPORTED", -5: "SHC_ERR_HIP"}
+
+
+class ShcError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)}: {detail}")
+
+
+_lib = None
+
+_c_i32, _c_i64, _c_ptr, _c_sz, _c_f = (ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p,
+                                        ctypes.c_size_t, ctypes.c_float)
+_SIGS = {
+    "shc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "shc_last_error": (ctypes.c_char_p, []),
+    "shc_compact_mask_workspace": (_c_sz, [_c_i32, _c_i32]),
+    "shc_compact_mask": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
+                                        _c_ptr, _c_i64, _c_ptr, _c_sz, _c_ptr]),
+    "shc_gather_rows": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
+                                       _c_ptr, _c_ptr]),
+    "shc_sparse_linear": (ctypes.c_int, [_c_ptr, _c_i64, _c_ptr, _c_ptr, _c_i32, _c_i32, _c_i32,
+                                         _c_i32, _c_ptr, _c_ptr]),
+    "shc_sparse_neighbor_conv": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32,
+                                                _c_ptr, _c_i32, _c_ptr, _c_ptr, _c_i32, _c_i32,
+                                                _c_i32, _c_i32, _c_ptr, _c_ptr]),
+    "shc_scatter": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
+                                   _c_i32, _c_ptr, _c_ptr]),
+    "shc_segment_maxpool": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_f,
+                                           _c_ptr, _c_ptr]),
+}
+
+
+def load(path: Optional[str] = None):
+    """Load libshc.so (once) and declare the C signatures."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is not built: run `python -m paper_2608_09388_amd.build`")
+    lib = ctypes.CDLL(p)
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def header_symbols(header: str = HEADER):
+    """Names of the functions include/shc.h declares."""
+    text = open(header).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(shc_[a-z_]+)\s*\(", text)))
+
+
+def _check(rc: int, where: str):
+    if rc != 0:
+        detail = load().shc_last_error().decode(errors="replace")
+        raise ShcError(rc, where, detail)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return SHC_F32
+    if t.dtype == torch.bfloat16:
+        return SHC_BF16
+    raise TypeError(f"feature tensors must be float32 or bfloat16, got {t.dtype}")
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None, min_numel: int = 0):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.numel() < min_numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, needs {min_numel}")
+    return t.data_ptr()
+
+
+def _opt_dev(t, name, dtype=None, min_numel=0):
+    return None if t is None else _dev(t, name, dtype, min_numel)
+
+
+# ----------------------------------------------------------------------------
+# entry points (same names as the C ABI, minus the prefix)
+# ----------------------------------------------------------------------------
+
+
+def compact_mask_workspace(B: int, V: int) -> int:
+    return int(load().shc_compact_mask_workspace(B, V))
+
+
+def compact_mask(mask: torch.Tensor, B: int, V: int, coords: torch.Tensor, inv: torch.Tensor,
+                 row_ptr: torch.Tensor, n_active: torch.Tensor, ws: torch.Tensor,
+                 want_host_count: bool = True, stream=None) -> Optional[int]:
+    """shc_compact_mask.  ``coords`` is int32 [cap][2]; returns N' if asked (syncs)."""
+    lib = load()
+    cap = coords.numel() // 2
+    args = [_dev(mask, "mask", torch.uint8, B * V), B, V,
+            _dev(coords, "coords", torch.int32) if cap > 0 else None,
+            _dev(inv, "inv", torch.int32, B * V), _dev(row_ptr, "row_ptr", torch.int32, B + 1),
+            _dev(n_active, "n_active", torch.int32, 1)]
+    host = ctypes.c_int64(-1)
+    args += [ctypes.addressof(host) if want_host_count else None, cap,
+             _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)]
+    _check(lib.shc_compact_mask(*args), "shc_compact_mask")
+    return int(host.value) if want_host_count else None
+
+
+def gather_rows(x: torch.Tensor, coords: torch.Tensor, n_rows: int, B: int, V: int,
+                S: torch.Tensor, stream=None):
+    """shc_gather_rows: S[i] = x[b_i * V + v_i]."""
+    C = x.shape[-1]
+    dt = _dtype_code(x)
+    args = [_dev(x, "x", x.dtype, B * V * C), _dev(coords, "coords", torch.int32, 2 * n_rows),
+            n_rows, B, V, C, dt, _dev(S, "S", x.dtype, n_rows * C), _stream(stream)]
+    _check(load().shc_gather_rows(*args), "shc_gather_rows")
+
+
+def sparse_linear(S: torch.Tensor, n_rows: int, W: torch.Tensor, bias: Optional[torch.Tensor],
+                  out: torch.Tensor, act: int = SHC_ACT_RELU, stream=None):
+    """shc_sparse_linear: out = act(S W + bias), W [Cin][Cout]."""
+    Cin, Cout = W.shape
+    dt = _dtype_code(S)
+    args = [_dev(S, "S", S.dtype, n_rows * Cin), n_rows, _dev(W, "W", S.dtype, Cin * Cout),
+            _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, dt, act,
+            _dev(out, "out", S.dtype, n_rows * Cout), _stream(stream)]
+    _check(load().shc_sparse_linear(*args), "shc_sparse_linear")
+
+
+def sparse_neighbor_conv(S: torch.Tensor, coords: torch.Tensor, inv: torch.Tensor, n_rows: int,
+                         B: int, V: int, nbr: torch.Tensor, W: torch.Tensor,
+                         bias: Optional[torch.Tensor], out: torch.Tensor,
+                         act: int = SHC_ACT_RELU, stream=None):
+    """shc_sparse_neighbor_conv: W [K][Cin][Cout], nbr [V][K]."""
+    K, Cin, Cout = W.shape
+    dt = _dtype_code(S)
+    args = [_dev(S, "S", S.dtype, n_rows * Cin), _dev(coords, "coords", torch.int32, 2 * n_rows),
+            _dev(inv, "inv", torch.int32, B * V), n_rows, B, V,
+            _dev(nbr, "nbr", torch.int32, V * K), K, _dev(W, "W", S.dtype, K * Cin * Cout),
+            _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, dt, act,
+            _dev(out, "out", S.dtype, n_rows * Cout), _stream(stream)]
+    _check(load().shc_sparse_neighbor_conv(*args), "shc_sparse_neighbor_conv")
+
+
+def scatter(S: torch.Tensor, inv: torch.Tensor, coords: torch.Tensor, n_rows: int, B: int,
+            V: int, D: torch.Tensor, zero_fill: bool = True, stream=None):
+    """shc_scatter: compact rows back to D [B*V][C]."""
+    C = D.shape[-1]
+    dt = _dtype_code(D)
+    args = [_opt_dev(S, "S", D.dtype, n_rows * C) if n_rows > 0 else None,
+            _dev(inv, "inv", torch.int32, B * V) if zero_fill else None,
+            _dev(coords, "coords", torch.int32, 2 * n_rows) if (not zero_fill and n_rows) else None,
+            n_rows, B, V, C, dt, 1 if zero_fill else 0, _dev(D, "D", D.dtype, B * V * C),
+            _stream(stream)]
+    _check(load().shc_scatter(*args), "shc_scatter")
+
+
+def segment_maxpool(S: torch.Tensor, row_ptr: torch.Tensor, n_rows: int, B: int,
+                    P: torch.Tensor, empty_value: float = 0.0, stream=None):
+    """shc_segment_maxpool: P [B][C] = per-body max of the active rows."""
+    C = P.shape[-1]
+    dt = _dtype_code(P)
+    args = [_dev(S, "S", P.dtype, n_rows * C) if n_rows > 0 else None,
+            _dev(row_ptr, "row_ptr", torch.int32, B + 1), n_rows, B, C, dt, float(empty_value),
+            _dev(P, "P", P.dtype, B * C), _stream(stream)]
+    _check(load().shc_segment_maxpool(*args), "shc_segment_maxpool")

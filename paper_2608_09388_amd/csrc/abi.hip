@@ -1,0 +1,263 @@
+// C ABI of libshc.so: argument validation on the host, then kernel launches.
+// Validation never touches the device, so every error path can be exercised
+// without a GPU.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/shc.h"
+#include "shc_internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int hip_status(hipError_t err, const char* where) {
+  if (err == hipSuccess) return SHC_OK;
+  return fail(SHC_ERR_HIP, "%s: %s (%d)", where, hipGetErrorString(err), (int)err);
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int32_t kMaxChannels = 4096;
+constexpr int32_t kMaxSlots = 32;
+
+int check_dtype(int32_t dtype) {
+  if (dtype != SHC_F32 && dtype != SHC_BF16)
+    return fail(SHC_ERR_UNSUPPORTED, "unknown dtype code %d", dtype);
+  return SHC_OK;
+}
+
+int check_channels(const char* name, int32_t C) {
+  if (C <= 0) return fail(SHC_ERR_INVALID_ARG, "%s = %d must be positive", name, C);
+  if (C % 16 != 0 || C > kMaxChannels)
+    return fail(SHC_ERR_UNSUPPORTED, "%s = %d must be a multiple of 16 in [16, %d]", name, C,
+                kMaxChannels);
+  return SHC_OK;
+}
+
+int check_bv(int32_t B, int32_t V) {
+  if (B <= 0 || V <= 0) return fail(SHC_ERR_INVALID_ARG, "B = %d and V = %d must be positive", B, V);
+  if ((int64_t)B * V > INT32_MAX)
+    return fail(SHC_ERR_UNSUPPORTED, "B * V = %lld exceeds 2^31 - 1", (long long)B * V);
+  return SHC_OK;
+}
+
+int check_rows(int64_t n_rows) {
+  if (n_rows < 0 || n_rows > INT32_MAX)
+    return fail(SHC_ERR_INVALID_ARG, "n_rows = %lld outside [0, 2^31)", (long long)n_rows);
+  return SHC_OK;
+}
+
+#define SHC_TRY(expr)          \
+  do {                         \
+    int _rc = (expr);          \
+    if (_rc != SHC_OK) return _rc; \
+  } while (0)
+
+#define SHC_PTR(p, name)                                                           \
+  do {                                                                             \
+    if ((p) == nullptr) return fail(SHC_ERR_INVALID_ARG, "%s is NULL", name);      \
+    if (!aligned16(p)) return fail(SHC_ERR_MISALIGNED, "%s is not 16-byte aligned", name); \
+  } while (0)
+
+#define SHC_OPT_PTR(p, name)                                                       \
+  do {                                                                             \
+    if ((p) != nullptr && !aligned16(p))                                           \
+      return fail(SHC_ERR_MISALIGNED, "%s is not 16-byte aligned", name);          \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char* shc_status_string(int status) {
+  switch (status) {
+    case SHC_OK: return "SHC_OK";
+    case SHC_ERR_INVALID_ARG: return "SHC_ERR_INVALID_ARG";
+    case SHC_ERR_CAPACITY: return "SHC_ERR_CAPACITY";
+    case SHC_ERR_MISALIGNED: return "SHC_ERR_MISALIGNED";
+    case SHC_ERR_UNSUPPORTED: return "SHC_ERR_UNSUPPORTED";
+    case SHC_ERR_HIP: return "SHC_ERR_HIP";
+    default: return "SHC_ERR_UNKNOWN";
+  }
+}
+
+const char* shc_last_error(void) { return g_last_error; }
+
+size_t shc_compact_mask_workspace(int32_t B, int32_t V) {
+  if (B <= 0 || V <= 0) return 0;
+  int32_t nblocks;
+  int64_t per_block;
+  shc::compact_plan((int64_t)B * V, &nblocks, &per_block);
+  return (((size_t)nblocks * sizeof(int32_t)) + 255u) & ~(size_t)255u;
+}
+
+int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
+                     int32_t* row_ptr, int32_t* n_active_dev, int64_t* n_active_host, int64_t cap,
+                     void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_PTR(mask, "mask");
+  SHC_PTR(inv, "inv");
+  SHC_PTR(row_ptr, "row_ptr");
+  SHC_PTR(n_active_dev, "n_active_dev");
+  SHC_PTR(ws, "ws");
+  if (cap < 0) return fail(SHC_ERR_INVALID_ARG, "cap = %lld is negative", (long long)cap);
+  if (cap > 0) SHC_PTR(coords, "coords");
+  const size_t need = shc_compact_mask_workspace(B, V);
+  if (ws_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "workspace of %zu bytes is below the %zu needed", ws_bytes, need);
+  int rc = hip_status(shc::launch_compact(mask, B, V, coords, inv, row_ptr, n_active_dev, cap,
+                                          static_cast<int32_t*>(ws), stream),
+                      "compact_mask launch");
+  if (rc != SHC_OK || n_active_host == nullptr) return rc;
+  int32_t n = 0;
+  rc = hip_status(hipMemcpyAsync(&n, n_active_dev, sizeof(int32_t), hipMemcpyDeviceToHost, stream),
+                  "compact_mask count copy");
+  if (rc != SHC_OK) return rc;
+  rc = hip_status(hipStreamSynchronize(stream), "compact_mask stream sync");
+  if (rc != SHC_OK) return rc;
+  *n_active_host = n;
+  if (n > cap)
+    return fail(SHC_ERR_CAPACITY, "N' = %d active rows exceed cap = %lld", n, (long long)cap);
+  return SHC_OK;
+}
+
+int shc_gather_rows(const void* x, const int32_t* coords, int64_t n_rows, int32_t B, int32_t V,
+                    int32_t C, int32_t dtype, void* S, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("C", C));
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(x, "x");
+  SHC_PTR(coords, "coords");
+  SHC_PTR(S, "S");
+  const int32_t row_bytes = C * (dtype == SHC_BF16 ? 2 : 4);
+  return hip_status(shc::launch_gather(x, coords, n_rows, B, V, row_bytes, S, stream),
+                    "gather_rows launch");
+}
+
+int shc_sparse_linear(const void* S, int64_t n_rows, const void* W, const float* bias, int32_t Cin,
+                      int32_t Cout, int32_t dtype, int32_t act, void* out, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("Cin", Cin));
+  SHC_TRY(check_channels("Cout", Cout));
+  if (act != SHC_ACT_NONE && act != SHC_ACT_RELU)
+    return fail(SHC_ERR_UNSUPPORTED, "unknown activation code %d", act);
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(S, "S");
+  SHC_PTR(W, "W");
+  SHC_OPT_PTR(bias, "bias");
+  SHC_PTR(out, "out");
+  shc::GemmArgs a{};
+  a.S = S;
+  a.W = W;
+  a.bias = bias;
+  a.out = out;
+  a.n_rows = n_rows;
+  a.B = 1;
+  a.V = 1;
+  a.K = 1;
+  a.Cin = Cin;
+  a.Cout = Cout;
+  a.relu = act == SHC_ACT_RELU;
+  return hip_status(shc::launch_gather_gemm(a, false, dtype == SHC_BF16, stream),
+                    "sparse_linear launch");
+}
+
+int shc_sparse_neighbor_conv(const void* S, const int32_t* coords, const int32_t* inv,
+                             int64_t n_rows, int32_t B, int32_t V, const int32_t* nbr, int32_t K,
+                             const void* W, const float* bias, int32_t Cin, int32_t Cout,
+                             int32_t dtype, int32_t act, void* out, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("Cin", Cin));
+  SHC_TRY(check_channels("Cout", Cout));
+  if (K <= 0) return fail(SHC_ERR_INVALID_ARG, "K = %d must be positive", K);
+  if (K > kMaxSlots) return fail(SHC_ERR_UNSUPPORTED, "K = %d exceeds %d slots", K, kMaxSlots);
+  if (act != SHC_ACT_NONE && act != SHC_ACT_RELU)
+    return fail(SHC_ERR_UNSUPPORTED, "unknown activation code %d", act);
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(S, "S");
+  SHC_PTR(coords, "coords");
+  SHC_PTR(inv, "inv");
+  SHC_PTR(nbr, "nbr");
+  SHC_PTR(W, "W");
+  SHC_OPT_PTR(bias, "bias");
+  SHC_PTR(out, "out");
+  shc::GemmArgs a{};
+  a.S = S;
+  a.coords = coords;
+  a.inv = inv;
+  a.nbr = nbr;
+  a.W = W;
+  a.bias = bias;
+  a.out = out;
+  a.n_rows = n_rows;
+  a.B = B;
+  a.V = V;
+  a.K = K;
+  a.Cin = Cin;
+  a.Cout = Cout;
+  a.relu = act == SHC_ACT_RELU;
+  return hip_status(shc::launch_gather_gemm(a, true, dtype == SHC_BF16, stream),
+                    "sparse_neighbor_conv launch");
+}
+
+int shc_scatter(const void* S, const int32_t* inv, const int32_t* coords, int64_t n_rows,
+                int32_t B, int32_t V, int32_t C, int32_t dtype, int32_t zero_fill, void* D,
+                hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("C", C));
+  if (zero_fill != 0 && zero_fill != 1)
+    return fail(SHC_ERR_INVALID_ARG, "zero_fill = %d must be 0 or 1", zero_fill);
+  SHC_PTR(D, "D");
+  if (zero_fill) {
+    SHC_PTR(inv, "inv");
+    if (n_rows > 0) SHC_PTR(S, "S");
+  } else {
+    if (n_rows == 0) return SHC_OK;
+    SHC_PTR(coords, "coords");
+    SHC_PTR(S, "S");
+  }
+  const int32_t row_bytes = C * (dtype == SHC_BF16 ? 2 : 4);
+  return hip_status(
+      shc::launch_scatter(S, inv, coords, n_rows, B, V, row_bytes, zero_fill, D, stream),
+      "scatter launch");
+}
+
+int shc_segment_maxpool(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
+                        int32_t C, int32_t dtype, float empty_value, void* P, hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (B <= 0) return fail(SHC_ERR_INVALID_ARG, "B = %d must be positive", B);
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("C", C));
+  SHC_PTR(row_ptr, "row_ptr");
+  SHC_PTR(P, "P");
+  if (n_rows > 0) SHC_PTR(S, "S");
+  return hip_status(shc::launch_segment_max(S, row_ptr, n_rows, B, C, dtype == SHC_BF16,
+                                            empty_value, P, stream),
+                    "segment_maxpool launch");
+}
+
+}  // extern "C"

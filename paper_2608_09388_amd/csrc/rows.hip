@@ -1,0 +1,213 @@
+// Row movers of the sparse path: gather of the active rows (S' of Eq. 2),
+// scatter back to the dense per-vertex layout, and the per-body max-pool.
+//
+// All three are HBM-bound copies/selections.  Rows are moved as 16-byte
+// vectors: a block is a (tx, ty) grid of threads where tx threads cover one
+// row (tx = vectors per row, capped at 256) and ty rows are in flight, so
+// every wavefront issues contiguous 16-byte accesses along a row and no
+// integer division is needed per element.
+#include "shc_internal.h"
+
+namespace shc {
+namespace {
+
+constexpr int kThreads = 256;
+
+struct RowShape {
+  int vpr;  // 16-byte vectors per row
+  int tx;   // threads per row
+  int ty;   // rows per block
+};
+
+RowShape row_shape(int32_t row_bytes) {
+  RowShape s;
+  s.vpr = row_bytes / 16;
+  s.tx = s.vpr < kThreads ? s.vpr : kThreads;
+  s.ty = kThreads / s.tx;
+  return s;
+}
+
+__global__ __launch_bounds__(kThreads) void gather_kernel(const i32x4* __restrict__ x,
+                                                          const int2* __restrict__ coords,
+                                                          int64_t n_rows, int32_t B, int32_t V,
+                                                          int vpr, i32x4* __restrict__ S) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.y + threadIdx.y;
+  if (i >= n_rows) return;
+  const int2 c = coords[i];
+  const bool ok = c.x >= 0 && c.x < B && c.y >= 0 && c.y < V;
+  const i32x4* src = x + ((int64_t)c.x * V + c.y) * vpr;
+  i32x4* dst = S + i * vpr;
+  for (int q = threadIdx.x; q < vpr; q += blockDim.x) {
+    i32x4 val = {0, 0, 0, 0};
+    if (ok) val = __builtin_nontemporal_load(src + q);
+    dst[q] = val;
+  }
+}
+
+// D[r] = S[inv[r]] or zeros, for every dense row r.
+__global__ __launch_bounds__(kThreads) void scatter_fill_kernel(const i32x4* __restrict__ S,
+                                                                const int32_t* __restrict__ inv,
+                                                                int64_t n_dense, int64_t n_rows,
+                                                                int vpr, i32x4* __restrict__ D) {
+  const int64_t r = (int64_t)blockIdx.x * blockDim.y + threadIdx.y;
+  if (r >= n_dense) return;
+  const int32_t s = inv[r];
+  const bool ok = s >= 0 && s < n_rows;
+  const i32x4* src = S + (int64_t)s * vpr;
+  i32x4* dst = D + r * vpr;
+  for (int q = threadIdx.x; q < vpr; q += blockDim.x) {
+    i32x4 val = {0, 0, 0, 0};
+    if (ok) val = src[q];
+    __builtin_nontemporal_store(val, dst + q);
+  }
+}
+
+// D[b_i * V + v_i] = S[i] for every active row i; other rows untouched.
+__global__ __launch_bounds__(kThreads) void scatter_active_kernel(const i32x4* __restrict__ S,
+                                                                  const int2* __restrict__ coords,
+                                                                  int64_t n_rows, int32_t B,
+                                                                  int32_t V, int vpr,
+                                                                  i32x4* __restrict__ D) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.y + threadIdx.y;
+  if (i >= n_rows) return;
+  const int2 c = coords[i];
+  if (!(c.x >= 0 && c.x < B && c.y >= 0 && c.y < V)) return;
+  const i32x4* src = S + i * vpr;
+  i32x4* dst = D + ((int64_t)c.x * V + c.y) * vpr;
+  for (int q = threadIdx.x; q < vpr; q += blockDim.x) dst[q] = src[q];
+}
+
+// ---------------------------------------------------------------------------
+// segmented max-pool: one block per body.  Each thread keeps the running
+// maximum of one 16-byte vector of channels over rows lo + ty_id, lo + ty_id + ty, ...
+// (values widened to fp32, which is exact for bf16), then the ty partial
+// maxima are combined through LDS.  NaN is the "no value yet" state:
+// fmaxf(NaN, a) = a, so NaNs in the data lose to numbers as maxNum requires.
+// ---------------------------------------------------------------------------
+
+template <bool BF16>
+struct PoolVec;
+
+template <>
+struct PoolVec<false> {  // 4 fp32 channels
+  static constexpr int N = 4;
+  __device__ static void widen(const i32x4& v, float* f) {
+    for (int k = 0; k < 4; ++k) f[k] = __int_as_float(v[k]);
+  }
+  __device__ static i32x4 narrow(const float* f) {
+    return i32x4{__float_as_int(f[0]), __float_as_int(f[1]), __float_as_int(f[2]),
+                 __float_as_int(f[3])};
+  }
+};
+
+template <>
+struct PoolVec<true> {  // 8 bf16 channels
+  static constexpr int N = 8;
+  __device__ static void widen(const i32x4& v, float* f) {
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t u = (uint32_t)v[k];
+      f[2 * k] = bf16_bits_to_f32(u & 0xFFFFu);
+      f[2 * k + 1] = bf16_bits_to_f32(u >> 16);
+    }
+  }
+  __device__ static i32x4 narrow(const float* f) {
+    i32x4 r;
+    for (int k = 0; k < 4; ++k)
+      r[k] = (int)(f32_to_bf16_bits(f[2 * k]) | (f32_to_bf16_bits(f[2 * k + 1]) << 16));
+    return r;
+  }
+};
+
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void segment_max_kernel(const i32x4* __restrict__ S,
+                                                               const int32_t* __restrict__ row_ptr,
+                                                               int64_t n_rows, int vpr,
+                                                               float empty_value,
+                                                               i32x4* __restrict__ P) {
+  using PV = PoolVec<BF16>;
+  extern __shared__ float part[];  // [ty][tx][N]
+  const int b = blockIdx.x;
+  int64_t lo = row_ptr[b], hi = row_ptr[b + 1];
+  lo = lo < 0 ? 0 : (lo > n_rows ? n_rows : lo);
+  hi = hi < lo ? lo : (hi > n_rows ? n_rows : hi);
+  const int tx = blockDim.x, ty = blockDim.y;
+  const float nanv = __builtin_nanf("");
+  for (int q0 = 0; q0 < vpr; q0 += tx) {
+    const int q = q0 + threadIdx.x;
+    float m[PV::N];
+    for (int k = 0; k < PV::N; ++k) m[k] = nanv;
+    if (q < vpr) {
+      for (int64_t i = lo + threadIdx.y; i < hi; i += ty) {
+        float f[PV::N];
+        PV::widen(S[i * vpr + q], f);
+        for (int k = 0; k < PV::N; ++k) m[k] = fmaxf(m[k], f[k]);
+      }
+    }
+    float* mine = part + ((size_t)threadIdx.y * tx + threadIdx.x) * PV::N;
+    for (int k = 0; k < PV::N; ++k) mine[k] = m[k];
+    __syncthreads();
+    if (threadIdx.y == 0 && q < vpr) {
+      for (int y = 1; y < ty; ++y) {
+        const float* o = part + ((size_t)y * tx + threadIdx.x) * PV::N;
+        for (int k = 0; k < PV::N; ++k) m[k] = fmaxf(m[k], o[k]);
+      }
+      if (hi == lo)
+        for (int k = 0; k < PV::N; ++k) m[k] = empty_value;
+      P[(int64_t)b * vpr + q] = PV::narrow(m);
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gather(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
+                         int32_t V, int32_t row_bytes, void* S, hipStream_t stream) {
+  const RowShape s = row_shape(row_bytes);
+  const int64_t blocks = (n_rows + s.ty - 1) / s.ty;
+  hipLaunchKernelGGL(gather_kernel, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0, stream,
+                     static_cast<const i32x4*>(x), reinterpret_cast<const int2*>(coords), n_rows,
+                     B, V, s.vpr, static_cast<i32x4*>(S));
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter(const void* S, const int32_t* inv, const int32_t* coords,
+                          int64_t n_rows, int32_t B, int32_t V, int32_t row_bytes, int zero_fill,
+                          void* D, hipStream_t stream) {
+  const RowShape s = row_shape(row_bytes);
+  if (zero_fill) {
+    const int64_t n_dense = (int64_t)B * V;
+    const int64_t blocks = (n_dense + s.ty - 1) / s.ty;
+    hipLaunchKernelGGL(scatter_fill_kernel, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0, stream,
+                       static_cast<const i32x4*>(S), inv, n_dense, n_rows, s.vpr,
+                       static_cast<i32x4*>(D));
+  } else {
+    if (n_rows == 0) return hipSuccess;
+    const int64_t blocks = (n_rows + s.ty - 1) / s.ty;
+    hipLaunchKernelGGL(scatter_active_kernel, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0,
+                       stream, static_cast<const i32x4*>(S),
+                       reinterpret_cast<const int2*>(coords), n_rows, B, V, s.vpr,
+                       static_cast<i32x4*>(D));
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_segment_max(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
+                              int32_t C, int is_bf16, float empty_value, void* P,
+                              hipStream_t stream) {
+  const int32_t row_bytes = C * (is_bf16 ? 2 : 4);
+  const RowShape s = row_shape(row_bytes);
+  const int n_per_vec = is_bf16 ? 8 : 4;
+  const size_t lds = (size_t)s.tx * s.ty * n_per_vec * sizeof(float);
+  if (is_bf16)
+    hipLaunchKernelGGL(segment_max_kernel<true>, dim3(B), dim3(s.tx, s.ty), lds, stream,
+                       static_cast<const i32x4*>(S), row_ptr, n_rows, s.vpr, empty_value,
+                       static_cast<i32x4*>(P));
+  else
+    hipLaunchKernelGGL(segment_max_kernel<false>, dim3(B), dim3(s.tx, s.ty), lds, stream,
+                       static_cast<const i32x4*>(S), row_ptr, n_rows, s.vpr, empty_value,
+                       static_cast<i32x4*>(P));
+  return hipGetLastError();
+}
+
+}  // namespace shc

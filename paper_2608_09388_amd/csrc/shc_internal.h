@@ -1,0 +1,75 @@
+// Internal declarations shared by the HIP translation units of libshc.so.
+// Nothing here is part of the public ABI (include/shc.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace shc {
+
+// ---------------------------------------------------------------------------
+// small device helpers
+// ---------------------------------------------------------------------------
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) {
+  return __uint_as_float(h << 16);
+}
+
+// fp32 -> bf16 bits, round to nearest, ties to even; NaN -> quiet NaN.
+// Adding 0x7FFF plus the lowest kept bit to the fp32 pattern carries into the
+// kept part exactly when the dropped half is above one half ulp, or equal to
+// it with an odd kept part.
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u | ((u >> 16) & 0x8000u);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+template <typename T>
+__device__ __forceinline__ T ceil_div(T a, T b) {
+  return (a + b - 1) / b;
+}
+
+// ---------------------------------------------------------------------------
+// launchers (host side, enqueue only; arguments already validated)
+// ---------------------------------------------------------------------------
+
+// compaction: number of blocks and per-block element span for a mask of `total` entries
+void compact_plan(int64_t total, int32_t* nblocks, int64_t* per_block);
+
+hipError_t launch_compact(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
+                          int32_t* row_ptr, int32_t* n_active, int64_t cap, int32_t* block_counts,
+                          hipStream_t stream);
+
+hipError_t launch_gather(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
+                         int32_t V, int32_t row_bytes, void* S, hipStream_t stream);
+
+hipError_t launch_scatter(const void* S, const int32_t* inv, const int32_t* coords,
+                          int64_t n_rows, int32_t B, int32_t V, int32_t row_bytes, int zero_fill,
+                          void* D, hipStream_t stream);
+
+hipError_t launch_segment_max(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
+                              int32_t C, int is_bf16, float empty_value, void* P,
+                              hipStream_t stream);
+
+struct GemmArgs {
+  const void* S;        // [n_rows][Cin]
+  const int32_t* coords;  // conv only
+  const int32_t* inv;     // conv only
+  const int32_t* nbr;     // conv only, [V][K]
+  const void* W;        // [K][Cin][Cout] (linear: K = 1)
+  const float* bias;    // [Cout] or null
+  void* out;            // [n_rows][Cout]
+  int64_t n_rows;
+  int32_t B, V, K, Cin, Cout;
+  int32_t relu;
+};
+
+hipError_t launch_gather_gemm(const GemmArgs& a, bool conv, bool bf16, hipStream_t stream);
+
+}  // namespace shc

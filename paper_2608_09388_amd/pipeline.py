@@ -1,0 +1,119 @@
+"""A sparse contact-layer stack driven through the C ABI.
+
+``SparseStack`` uploads one workload (mesh neighbour lists, mask, dense
+features, layer weights) to the GPU once, allocates every buffer the path
+needs at its worst-case size (all B*V rows active), and then runs the path
+as a sequence of library calls:
+
+    shc_compact_mask -> shc_gather_rows -> (shc_sparse_linear |
+    shc_sparse_neighbor_conv) per layer -> shc_scatter / shc_segment_maxpool
+
+The active set never changes across layers (C'_k = C_k, Sec. 3.2), so the
+active count is read back once per mask and passed to every layer call.
+This module only moves buffers and issues calls; all arithmetic runs in the
+library's kernels.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+from . import binding as shc
+from .synth import BF16, Workload
+
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def to_device(a: np.ndarray, dtype: str, device) -> torch.Tensor:
+    """Upload fp32 values that are exact in `dtype` as a tensor of that dtype."""
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(device=device, dtype=TORCH_DTYPE[dtype])
+
+
+class SparseStack:
+    def __init__(self, w: Workload, device: str = "cuda", act: int = shc.SHC_ACT_RELU):
+        self.w = w
+        self.device = torch.device(device)
+        self.dtype = TORCH_DTYPE[w.dtype]
+        self.B, self.V, self.K = w.B, w.V, w.K
+        self.act = act
+        dev = self.device
+        BV = self.B * self.V
+        self.mask = torch.from_numpy(np.ascontiguousarray(w.mask.reshape(-1))).to(dev)
+        self.nbr = torch.from_numpy(np.ascontiguousarray(w.nbr, dtype=np.int32)).to(dev)
+        self.x = to_device(w.x, w.dtype, dev)
+        self.weights = [to_device(l.W, w.dtype, dev) for l in w.layers]
+        self.biases = [None if l.bias is None else
+                       torch.from_numpy(l.bias.astype(np.float32)).to(dev) for l in w.layers]
+        # compaction outputs (capacity: every row active)
+        self.coords = torch.empty((BV, 2), dtype=torch.int32, device=dev)
+        self.inv = torch.empty(BV, dtype=torch.int32, device=dev)
+        self.row_ptr = torch.empty(self.B + 1, dtype=torch.int32, device=dev)
+        self.n_active = torch.empty(4, dtype=torch.int32, device=dev)
+        ws = shc.compact_mask_workspace(self.B, self.V)
+        self.ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=dev)
+        # activations: gathered input + one buffer per layer
+        chans = [w.C0] + [l.Cout for l in w.layers]
+        self.acts = [torch.empty((BV, c), dtype=self.dtype, device=dev) for c in chans]
+        Cl = chans[-1]
+        self.dense_out = torch.empty((BV, Cl), dtype=self.dtype, device=dev) if w.scatter else None
+        self.pooled = torch.empty((self.B, Cl), dtype=self.dtype, device=dev) if w.pool else None
+        self.n = None
+
+    # -- individual steps -----------------------------------------------------
+    def compact(self, stream=None) -> int:
+        self.n = shc.compact_mask(self.mask, self.B, self.V, self.coords, self.inv, self.row_ptr,
+                                  self.n_active, self.ws, want_host_count=True, stream=stream)
+        return self.n
+
+    def gather(self, stream=None):
+        shc.gather_rows(self.x, self.coords, self.n, self.B, self.V, self.acts[0], stream=stream)
+
+    def layer(self, l: int, stream=None):
+        spec = self.w.layers[l]
+        src, dst = self.acts[l], self.acts[l + 1]
+        act = self.act if spec.relu else shc.SHC_ACT_NONE
+        if spec.kind == "conv":
+            shc.sparse_neighbor_conv(src, self.coords, self.inv, self.n, self.B, self.V, self.nbr,
+                                     self.weights[l], self.biases[l], dst, act, stream=stream)
+        else:
+            shc.sparse_linear(src, self.n, self.weights[l], self.biases[l], dst, act,
+                              stream=stream)
+
+    def finish(self, stream=None):
+        last = self.acts[-1]
+        if self.dense_out is not None:
+            shc.scatter(last, self.inv, self.coords, self.n, self.B, self.V, self.dense_out,
+                        zero_fill=True, stream=stream)
+        if self.pooled is not None:
+            shc.segment_maxpool(last, self.row_ptr, self.n, self.B, self.pooled, 0.0,
+                                stream=stream)
+
+    def step(self, stream=None) -> int:
+        """One pass of the whole path over the workload's batch."""
+        self.compact(stream)
+        self.gather(stream)
+        for l in range(len(self.w.layers)):
+            self.layer(l, stream)
+        self.finish(stream)
+        return self.n
+
+    # -- results on the host --------------------------------------------------
+    def rows(self, l: int) -> np.ndarray:
+        """Active rows of activation l (0 = gathered input) as fp64 numpy."""
+        return self.acts[l][: self.n].float().cpu().numpy().astype(np.float64)
+
+    def results(self) -> Dict[str, object]:
+        torch.cuda.synchronize(self.device)
+        n = self.n
+        out = dict(n=n, coords=self.coords[:n].cpu().numpy(), inv=self.inv.cpu().numpy(),
+                   row_ptr=self.row_ptr.cpu().numpy(),
+                   n_dev=int(self.n_active[0].item()),
+                   outs=[self.rows(l + 1) for l in range(len(self.w.layers))])
+        if self.pooled is not None:
+            out["pool"] = self.pooled.float().cpu().numpy().astype(np.float64)
+        if self.dense_out is not None:
+            out["dense"] = self.dense_out.float().cpu().numpy().astype(np.float64)
+        return out

@@ -1,0 +1,127 @@
+"""The C ABI without a GPU: the library loads, exports what shc.h declares, and
+rejects bad arguments on the host before any HIP call.
+
+Only validation failures are exercised here (no call below reaches a kernel
+launch), so no device is touched.  Fake "device pointers" are plain integers
+with the alignment each case needs; validation never dereferences them.
+"""
+import ctypes
+import subprocess
+
+import pytest
+
+from paper_2608_09388_amd import binding as shc
+
+A = 0x10000          # a 16-byte aligned fake address
+MIS = 0x10004        # a misaligned one
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return shc.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    declared = shc.header_symbols()
+    assert len(declared) >= 9
+    out = subprocess.run(["nm", "-D", "--defined-only", shc.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    for name in declared:
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings(lib):
+    for code, name in shc.STATUS.items():
+        assert lib.shc_status_string(code).decode() == name
+    assert lib.shc_status_string(-99).decode() == "SHC_ERR_UNKNOWN"
+
+
+def test_workspace_query(lib):
+    assert lib.shc_compact_mask_workspace(0, 5) == 0
+    ws = lib.shc_compact_mask_workspace(128, 10475)
+    assert ws > 0 and ws % 256 == 0
+    assert lib.shc_compact_mask_workspace(1, 1) >= 4
+
+
+def err(lib):
+    return lib.shc_last_error().decode()
+
+
+def test_compact_mask_validation(lib):
+    ws = lib.shc_compact_mask_workspace(4, 655)
+    ok = dict(mask=A, B=4, V=655, coords=A, inv=A, row_ptr=A, n_dev=A, n_host=None, cap=2620,
+              ws=A, ws_bytes=ws)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return lib.shc_compact_mask(a["mask"], a["B"], a["V"], a["coords"], a["inv"], a["row_ptr"],
+                                    a["n_dev"], a["n_host"], a["cap"], a["ws"], a["ws_bytes"], None)
+
+    assert call(B=0) == -1 and "B = 0" in err(lib)
+    assert call(V=-3) == -1
+    assert call(B=1 << 16, V=1 << 16) == -4
+    assert call(mask=None) == -1 and "mask" in err(lib)
+    assert call(inv=MIS) == -3 and "inv" in err(lib)
+    assert call(row_ptr=None) == -1
+    assert call(n_dev=MIS) == -3
+    assert call(ws=None) == -1
+    assert call(cap=-1) == -1
+    assert call(coords=None) == -1            # cap > 0 needs coords
+    assert call(ws_bytes=ws - 1) == -2 and "workspace" in err(lib)
+
+
+def test_gather_scatter_pool_validation(lib):
+    g = lib.shc_gather_rows
+    assert g(A, A, 10, 4, 655, 24, 0, A, None) == -4
+    assert g(A, A, 10, 4, 655, 16, 7, A, None) == -4
+    assert g(A, A, -1, 4, 655, 16, 0, A, None) == -1
+    assert g(A, A, 1 << 31, 4, 655, 16, 0, A, None) == -1
+    assert g(None, A, 10, 4, 655, 16, 0, A, None) == -1
+    assert g(A, MIS, 10, 4, 655, 16, 1, A, None) == -3
+    assert g(A, A, 10, 4, 655, 0, 1, A, None) == -1
+    assert g(A, A, 10, 4, 655, 4112, 1, A, None) == -4
+    s = lib.shc_scatter
+    assert s(A, A, A, 10, 4, 655, 16, 0, 2, A, None) == -1
+    assert s(A, None, A, 10, 4, 655, 16, 0, 1, A, None) == -1       # zero-fill needs inv
+    assert s(A, A, None, 10, 4, 655, 16, 0, 0, A, None) == -1       # active-only needs coords
+    assert s(A, A, A, 10, 4, 655, 16, 0, 1, MIS, None) == -3
+    p = lib.shc_segment_maxpool
+    assert p(A, A, 10, 0, 16, 0, 0.0, A, None) == -1
+    assert p(A, None, 10, 4, 16, 0, 0.0, A, None) == -1
+    assert p(MIS, A, 10, 4, 16, 0, 0.0, A, None) == -3
+    assert p(A, A, 10, 4, 20, 0, 0.0, A, None) == -4
+
+
+def test_layer_validation(lib):
+    L = lib.shc_sparse_linear
+    assert L(A, 10, A, None, 16, 24, 0, 1, A, None) == -4
+    assert L(A, 10, A, None, 16, 16, 0, 5, A, None) == -4
+    assert L(None, 10, A, None, 16, 16, 0, 1, A, None) == -1
+    assert L(A, 10, A, MIS, 16, 16, 0, 1, A, None) == -3           # bias alignment
+    assert L(A, 10, None, None, 16, 16, 1, 0, A, None) == -1
+    C = lib.shc_sparse_neighbor_conv
+
+    def conv(**kw):
+        a = dict(S=A, coords=A, inv=A, n=10, B=4, V=655, nbr=A, K=9, W=A, bias=None, Cin=16,
+                 Cout=64, dt=0, act=1, out=A)
+        a.update(kw)
+        return C(a["S"], a["coords"], a["inv"], a["n"], a["B"], a["V"], a["nbr"], a["K"], a["W"],
+                 a["bias"], a["Cin"], a["Cout"], a["dt"], a["act"], a["out"], None)
+
+    assert conv(K=0) == -1
+    assert conv(K=33) == -4 and "K = 33" in err(lib)
+    assert conv(nbr=None) == -1
+    assert conv(inv=MIS) == -3
+    assert conv(Cout=8) == -4
+    assert conv(B=0) == -1
+    assert conv(dt=2) == -4
+    assert conv(out=None) == -1
+
+
+def test_binding_refuses_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(4 * 655, 16)
+    with pytest.raises(ValueError):
+        shc.gather_rows(x, torch.zeros(10, 2, dtype=torch.int32), 10, 4, 655, torch.zeros(10, 16))

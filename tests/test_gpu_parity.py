@@ -1,0 +1,431 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bit-exact: compaction (coords, inv, row_ptr, count), gather, scatter, pool.
+Floating point: |gpu - oracle| <= rtol * (abs-sum scale) per element, with
+rtol 1e-5 for fp32 and 2e-2 for bf16; stacks are also checked normwise.
+Every input is seeded and synthetic; no expected value comes from the GPU.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import shc_oracle as O
+from paper_2608_09388_amd import binding as shc
+from paper_2608_09388_amd import synth
+from tests.gpu_util import (Compaction, assert_normwise_close, assert_scaled_close, down,
+                            require_gpu, up)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    return require_gpu()
+
+
+def rand_nbr(V, K, rng, p_missing=0.1):
+    nbr = rng.integers(0, V, size=(V, K)).astype(np.int32)
+    nbr[rng.random((V, K)) < p_missing] = -1
+    nbr[:, 0] = np.arange(V)
+    return nbr
+
+
+def check_compaction(mask, cap=None):
+    ref_c, ref_inv, ref_rp, ref_n = O.compact(mask)
+    c = Compaction(mask, cap)
+    n = c.run(want_host=(cap is None))
+    torch.cuda.synchronize()
+    n_dev = int(c.n_dev[0].item())
+    assert n_dev == ref_n
+    if cap is None:
+        assert n == ref_n
+    assert np.array_equal(down(c.inv), ref_inv)
+    assert np.array_equal(down(c.row_ptr), ref_rp)
+    k = min(ref_n, c.cap)
+    got_c = down(c.coords)
+    assert np.array_equal(got_c[:k], ref_c[:k])
+    assert np.all(got_c[k:] == -7)          # rows past N' (or past cap) untouched
+    return c
+
+
+# ----------------------------------------------------------------------------
+# compaction
+# ----------------------------------------------------------------------------
+
+
+def test_compact_exhaustive_v10(dev):
+    """All 2^10 masks of one V = 10 body at once: body b carries the bits of b."""
+    codes = np.arange(1 << 10)
+    mask = ((codes[:, None] >> np.arange(10)[None, :]) & 1).astype(np.uint8)
+    check_compaction(mask)
+
+
+def test_compact_exhaustive_v12(dev):
+    codes = np.arange(1 << 12)
+    mask = ((codes[:, None] >> np.arange(12)[None, :]) & 1).astype(np.uint8)
+    check_compaction(mask)
+
+
+@pytest.mark.parametrize("B,V,p", [(1, 1, 1.0), (1, 1, 0.0), (3, 1, 0.5), (2, 3, 0.5),
+                                   (1, 4095, 0.3), (1, 4096, 0.3), (1, 4097, 0.3),
+                                   (7, 655, 0.1), (64, 655, 0.0), (64, 655, 1.0),
+                                   (5, 10475, 0.05), (1025, 4096, 0.02), (300, 10475, 0.5)])
+def test_compact_shapes(dev, B, V, p):
+    rng = np.random.default_rng(B * 7919 + V)
+    m = (rng.random((B, V)) < p).astype(np.uint8)
+    m[m != 0] = rng.integers(1, 256, size=int(m.sum()))   # any non-zero byte is active
+    check_compaction(m)
+
+
+def test_compact_paper_workload_masks(dev):
+    for w in (synth.workload_c1(), synth.workload_c2(), synth.workload_c5()):
+        check_compaction(w.mask)
+    check_compaction(synth.workload_c4(0.05).mask)
+
+
+def test_compact_capacity(dev):
+    rng = np.random.default_rng(5)
+    m = (rng.random((10, 500)) < 0.2).astype(np.uint8)
+    n = int(m.sum())
+    check_compaction(m, cap=n // 2)          # coords truncated at cap, inv/row_ptr complete
+    check_compaction(m, cap=0)
+    c = Compaction(m, cap=n - 1)
+    with pytest.raises(shc.ShcError) as e:
+        c.run(want_host=True)
+    assert e.value.status == -2
+
+
+def test_compact_deterministic(dev):
+    m = synth.workload_c4(0.05).mask
+    c1 = Compaction(m)
+    c1.run()
+    c2 = Compaction(m)
+    c2.run()
+    assert torch.equal(c1.coords, c2.coords) and torch.equal(c1.inv, c2.inv)
+
+
+# ----------------------------------------------------------------------------
+# gather / scatter / pool (exact)
+# ----------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 48, 128, 256])
+def test_gather_scatter_exact(dev, dtype, C):
+    rng = np.random.default_rng(C)
+    B, V = 9, 1000
+    m = (rng.random((B, V)) < 0.13).astype(np.uint8)
+    x = synth.as_dtype(rng.standard_normal((B * V, C)).astype(np.float32), dtype)[1]
+    c = Compaction(m)
+    n = c.run()
+    xd = up(x, dtype)
+    S = torch.full((n + 5, C), float("nan"), dtype=xd.dtype, device=dev)
+    shc.gather_rows(xd, c.coords, n, B, V, S)
+    ref_c, ref_inv, _, _ = O.compact(m)
+    ref_S = O.gather(x, ref_c, V)
+    got = down(S)
+    assert np.array_equal(got[:n], ref_S) and np.all(np.isnan(got[n:]))
+    # zero-fill scatter: D = x (.) m exactly
+    D = torch.full((B * V, C), float("nan"), dtype=xd.dtype, device=dev)
+    shc.scatter(S, c.inv, c.coords, n, B, V, D, zero_fill=True)
+    assert np.array_equal(down(D), O.scatter(ref_S, ref_inv, zero_fill=True))
+    # active-only scatter keeps the sentinel in inactive rows
+    D2 = torch.full((B * V, C), float("nan"), dtype=xd.dtype, device=dev)
+    shc.scatter(S, c.inv, c.coords, n, B, V, D2, zero_fill=False)
+    exp = O.scatter(ref_S, ref_inv, zero_fill=False, D=np.full((B * V, C), np.nan))
+    got2 = down(D2)
+    assert np.array_equal(np.isnan(got2), np.isnan(exp))
+    assert np.array_equal(got2[~np.isnan(exp)], exp[~np.isnan(exp)])
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 128, 256])
+def test_segment_maxpool_exact(dev, dtype, C):
+    rng = np.random.default_rng(100 + C)
+    B, V = 70, 300
+    m = (rng.random((B, V)) < 0.05).astype(np.uint8)
+    m[[0, 13, 69]] = 0                       # empty bodies, first and last included
+    m[5] = 1                                 # a full body
+    c = Compaction(m)
+    n = c.run()
+    S = synth.as_dtype(rng.standard_normal((n, C)).astype(np.float32), dtype)[1]
+    S[rng.random(S.shape) < 0.01] = np.nan   # NaN loses to numbers
+    Sd = up(S, dtype)
+    P = torch.full((B, C), 123.0, dtype=Sd.dtype, device=dev)
+    shc.segment_maxpool(Sd, c.row_ptr, n, B, P, empty_value=-2.5)
+    ref = O.segment_max(S.astype(np.float64), O.compact(m)[2], -2.5)
+    got = down(P)
+    assert np.array_equal(np.isnan(got), np.isnan(ref))
+    assert np.array_equal(got[~np.isnan(ref)], ref[~np.isnan(ref)])
+
+
+# ----------------------------------------------------------------------------
+# sparse linear (Eq. 6)
+# ----------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("Cin,Cout", [(16, 16), (16, 64), (64, 64), (128, 128), (48, 80),
+                                      (256, 256), (32, 192)])
+def test_sparse_linear(dev, dtype, Cin, Cout):
+    rng = np.random.default_rng(Cin * 1000 + Cout)
+    n = 1000 + Cin                                   # ragged: not a multiple of the 64-row tile
+    S = synth.as_dtype(rng.standard_normal((n, Cin)).astype(np.float32), dtype)[1]
+    W = synth.as_dtype((rng.standard_normal((Cin, Cout)) / np.sqrt(Cin)).astype(np.float32),
+                       dtype)[1]
+    bias = rng.standard_normal(Cout).astype(np.float32)
+    rows = np.arange(n)
+    for b, act in ((None, shc.SHC_ACT_NONE), (bias, shc.SHC_ACT_RELU)):
+        out = torch.full((n + 3, Cout), float("nan"), dtype=synth_dtype(dtype), device=dev)
+        shc.sparse_linear(up(S, dtype), n, up(W, dtype), None if b is None else up(b), out, act)
+        got = down(out)
+        ref = O.linear_at(S, W, rows, b, act == shc.SHC_ACT_RELU)
+        scale = O.linear_at(S, W, rows, b, scale=True)
+        assert_scaled_close(got[:n], ref, scale, dtype, f"linear {Cin}->{Cout}")
+        assert np.all(np.isnan(got[n:]))
+
+
+def synth_dtype(dtype):
+    return torch.float32 if dtype == "f32" else torch.bfloat16
+
+
+def test_sparse_linear_zero_rows_is_noop(dev):
+    out = torch.full((4, 16), 7.0, device=dev)
+    shc.sparse_linear(torch.zeros(4, 16, device=dev), 0, torch.zeros(16, 16, device=dev), None,
+                      out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0)
+
+
+# ----------------------------------------------------------------------------
+# sparse neighbourhood conv (Eqs. 4-5)
+# ----------------------------------------------------------------------------
+
+
+def run_conv(dev, m, nbr, S_vals, W, bias, dtype, act=shc.SHC_ACT_RELU):
+    B, V = m.shape
+    c = Compaction(m)
+    n = c.run()
+    K, Cin, Cout = W.shape
+    out = torch.full((n + 2, Cout), float("nan"), dtype=synth_dtype(dtype), device=dev)
+    shc.sparse_neighbor_conv(up(S_vals, dtype), c.coords, c.inv, n, B, V, up(nbr), up(W, dtype),
+                             None if bias is None else up(bias), out, act)
+    got = down(out)
+    assert np.all(np.isnan(got[n:]))
+    return got[:n], n
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("B,V,K,Cin,Cout,p", [
+    (3, 200, 9, 16, 64, 0.3), (2, 333, 9, 64, 64, 0.5), (4, 150, 4, 48, 32, 0.4),
+    (2, 500, 9, 128, 128, 0.1), (1, 300, 1, 32, 16, 0.6), (2, 100, 32, 16, 16, 0.7),
+    (2, 257, 9, 256, 256, 0.2), (3, 211, 5, 32, 192, 0.9)])
+def test_sparse_conv_full_oracle(dev, dtype, B, V, K, Cin, Cout, p):
+    rng = np.random.default_rng(B * V + K * 7 + Cin)
+    m = (rng.random((B, V)) < p).astype(np.uint8)
+    nbr = rand_nbr(V, K, rng)
+    coords, inv, rp, n = O.compact(m)
+    S = synth.as_dtype(rng.standard_normal((n, Cin)).astype(np.float32), dtype)[1]
+    W = synth.as_dtype((rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin))
+                       .astype(np.float32), dtype)[1]
+    bias = rng.standard_normal(Cout).astype(np.float32)
+    for b, act in ((None, shc.SHC_ACT_NONE), (bias, shc.SHC_ACT_RELU)):
+        got, n2 = run_conv(dev, m, nbr, S, W, b, dtype, act)
+        assert n2 == n
+        ref = O.sparse_conv(S, coords, B, V, nbr, W, b, act == shc.SHC_ACT_RELU)
+        scale = O.sparse_conv_scale(S, coords, B, V, nbr, W, b)
+        assert_scaled_close(got, ref, scale, dtype, f"conv K={K} {Cin}->{Cout} p={p}")
+
+
+def test_sparse_conv_edge_cases(dev):
+    rng = np.random.default_rng(3)
+    V, K, C = 50, 9, 16
+    nbr = rand_nbr(V, K, rng)
+    nbr[7, 4] = 7
+    W = (rng.standard_normal((K, C, C)) / 12).astype(np.float32)
+    b = rng.standard_normal(C).astype(np.float32)
+    # a lone active vertex sees only its own slots
+    m = np.zeros((2, V), np.uint8)
+    m[1, 7] = 1
+    S = rng.standard_normal((1, C)).astype(np.float32)
+    got, n = run_conv(dev, m, nbr, S, W, b, "f32", shc.SHC_ACT_NONE)
+    ref = b + sum(S[0].astype(np.float64) @ W[j] for j in range(K) if nbr[7, j] == 7)
+    assert_scaled_close(got[0], ref, O.conv_at(S, O.compact(m)[0], 2, V, nbr, W, [0], b,
+                                                scale=True)[0], "f32", "lone vertex")
+    # out-of-range neighbour entries count as absent
+    nbr_bad = nbr.copy()
+    nbr_bad[:, 3] = V + 5
+    nbr_bad[:, 5] = -9
+    nbr_ok = nbr.copy()
+    nbr_ok[:, 3] = -1
+    nbr_ok[:, 5] = -1
+    m = (rng.random((2, V)) < 0.6).astype(np.uint8)
+    n = int(m.sum())
+    S = rng.standard_normal((n, C)).astype(np.float32)
+    g_bad, _ = run_conv(dev, m, nbr_bad, S, W, b, "f32")
+    g_ok, _ = run_conv(dev, m, nbr_ok, S, W, b, "f32")
+    assert np.array_equal(g_bad, g_ok)
+    # K = 1 self-neighbour conv is the linear layer
+    self_nbr = np.arange(V, dtype=np.int32)[:, None]
+    g_c, _ = run_conv(dev, m, self_nbr, S, W[:1], b, "f32")
+    out = torch.empty((n, C), device=dev)
+    shc.sparse_linear(up(S, "f32"), n, up(W[0], "f32"), up(b), out, shc.SHC_ACT_RELU)
+    assert np.array_equal(g_c, down(out))
+
+
+def test_sparse_conv_deterministic(dev):
+    w = synth.workload_c4(0.05)
+    rng = np.random.default_rng(1)
+    m = w.mask[:16]
+    n = int(m.sum())
+    S = synth.as_dtype(rng.standard_normal((n, 128)).astype(np.float32), "bf16")[1]
+    W = w.layers[1].W
+    g1, _ = run_conv(dev, m, w.nbr, S, W, None, "bf16")
+    g2, _ = run_conv(dev, m, w.nbr, S, W, None, "bf16")
+    assert np.array_equal(g1, g2)
+
+
+# ----------------------------------------------------------------------------
+# workloads at their full sizes (sampled rows) and whole stacks
+# ----------------------------------------------------------------------------
+
+
+def test_c1_full_stack(dev):
+    from paper_2608_09388_amd.pipeline import SparseStack
+    w = synth.workload_c1()
+    st = SparseStack(w, device=str(dev))
+    st.step()
+    res = st.results()
+    ref = O.run_stack(w.x, w.mask, w.nbr, [(l.kind, l.W, l.bias, l.relu) for l in w.layers],
+                      w.dtype)
+    assert res["n"] == ref["n"] == res["n_dev"]
+    assert np.array_equal(res["coords"], ref["coords"])
+    S0 = O.gather(w.x, ref["coords"], w.V)
+    scale = O.sparse_conv_scale(S0, ref["coords"], w.B, w.V, w.nbr, w.layers[0].W)
+    assert_scaled_close(res["outs"][0], ref["outs"][0], scale, "f32", "C1 conv")
+    dense_ref = O.scatter(res["outs"][0], ref["inv"], zero_fill=True)
+    assert np.array_equal(res["dense"], dense_ref)
+
+
+def test_c2_full_stack_bf16(dev):
+    from paper_2608_09388_amd.pipeline import SparseStack
+    w = synth.workload_c2()
+    st = SparseStack(w, device=str(dev))
+    st.step()
+    res = st.results()
+    ref = O.run_stack(w.x, w.mask, w.nbr, [(l.kind, l.W, l.bias, l.relu) for l in w.layers],
+                      w.dtype, pool=True)
+    assert res["n"] == ref["n"]
+    # first layer: identical inputs, per-element bound
+    S0 = O.gather(w.x, ref["coords"], w.V)
+    scale = O.sparse_conv_scale(S0, ref["coords"], w.B, w.V, w.nbr, w.layers[0].W)
+    ref0 = O.sparse_conv(S0, ref["coords"], w.B, w.V, w.nbr, w.layers[0].W, None, True)
+    assert_scaled_close(res["outs"][0], ref0, scale, "bf16", "C2 layer 0")
+    for l in range(len(w.layers)):
+        assert_normwise_close(res["outs"][l], ref["outs"][l], "bf16", f"C2 layer {l}")
+    assert_normwise_close(res["pool"], ref["pool"], "bf16", "C2 pool")
+    # the pool is exactly the per-body max of the GPU's own last layer
+    rp = res["row_ptr"]
+    last = res["outs"][-1]
+    for b in range(w.B):
+        seg = last[rp[b]:rp[b + 1]]
+        assert np.array_equal(res["pool"][b], seg.max(0) if len(seg) else np.zeros(seg.shape[1]))
+
+
+def sampled_layer_check(res_rows_in, got, w, layer, coords, rows, dtype, what):
+    """Check sampled output rows of one layer against the oracle's by-row definition."""
+    if layer.kind == "conv":
+        ref = O.conv_at(res_rows_in, coords, w.B, w.V, w.nbr, layer.W, rows, layer.bias,
+                        layer.relu)
+        sc = O.conv_at(res_rows_in, coords, w.B, w.V, w.nbr, layer.W, rows, layer.bias,
+                       scale=True)
+    else:
+        ref = O.linear_at(res_rows_in, layer.W, rows, layer.bias, layer.relu)
+        sc = O.linear_at(res_rows_in, layer.W, rows, layer.bias, scale=True)
+    assert_scaled_close(got[rows], ref, sc, dtype, what)
+
+
+@pytest.mark.parametrize("name", ["c3_f32", "c3_bf16", "c3_5pct_bf16", "c4_0.01", "c4_0.05",
+                                  "c4_0.2", "c4_1.0"])
+def test_full_size_workloads_sampled(dev, name):
+    from paper_2608_09388_amd.pipeline import SparseStack
+    if name.startswith("c3"):
+        w = synth.workload_c3("f32" if "f32" in name else "bf16", five_percent="5pct" in name)
+    else:
+        w = synth.workload_c4(float(name.split("_")[1]))
+    st = SparseStack(w, device=str(dev))
+    st.step()
+    res = st.results()
+    coords, inv, rp, n = O.compact(w.mask)
+    assert res["n"] == n and np.array_equal(res["coords"], coords)
+    assert np.array_equal(res["inv"], inv) and np.array_equal(res["row_ptr"], rp)
+    rng = np.random.default_rng(17)
+    rows = np.unique(np.concatenate([rng.choice(n, size=min(n, 1500), replace=False),
+                                     [0, n - 1]]))
+    # layer 0 input is the exact gather; later layers take the oracle's own
+    # previous layer at every row the sampled rows read (computed in full)
+    S_in = O.gather(w.x, coords, w.V)
+    for l, layer in enumerate(w.layers):
+        sampled_layer_check(S_in, res["outs"][l], w, layer, coords, rows, w.dtype,
+                            f"{name} layer {l}")
+        if l + 1 < len(w.layers):
+            full_rows = np.arange(n)
+            if layer.kind == "conv":
+                y = O.conv_at(S_in, coords, w.B, w.V, w.nbr, layer.W, full_rows, layer.bias,
+                              layer.relu)
+            else:
+                y = O.linear_at(S_in, layer.W, full_rows, layer.bias, layer.relu)
+            S_in = O.store(y, w.dtype)
+            assert_normwise_close(res["outs"][l], S_in, w.dtype, f"{name} layer {l} full")
+    if w.scatter:
+        dense = res["dense"]
+        act_rows = inv >= 0
+        assert np.all(dense[~act_rows] == 0)
+        assert np.array_equal(dense[act_rows], res["outs"][-1][inv[act_rows]])
+    if w.pool:
+        last = res["outs"][-1]
+        P = res["pool"]
+        for b in rng.choice(w.B, size=min(w.B, 40), replace=False):
+            seg = last[rp[b]:rp[b + 1]]
+            assert np.array_equal(P[b], seg.max(0) if len(seg) else np.zeros(last.shape[1]))
+
+
+def test_c5_sequences_stack(dev):
+    """C5 shape (V=655, C=256 bf16, Markov masks, 3 convs + per-frame pool) on one of
+    the 32 sequences end to end against the full oracle stack; all 32 sequences for
+    compaction and the pool property."""
+    from paper_2608_09388_amd.pipeline import SparseStack
+    w_full = synth.workload_c5()
+    st = SparseStack(w_full, device=str(dev))
+    st.step()
+    res = st.results()
+    coords, inv, rp, n = O.compact(w_full.mask)
+    assert res["n"] == n and np.array_equal(res["row_ptr"], rp)
+    last = res["outs"][-1]
+    for b in np.random.default_rng(2).choice(w_full.B, 50, replace=False):
+        seg = last[rp[b]:rp[b + 1]]
+        assert np.array_equal(res["pool"][b], seg.max(0) if len(seg) else np.zeros(256))
+    # one sequence (64 frames) through the full oracle
+    w = synth.workload_c5(n_seq=1)
+    st2 = SparseStack(w, device=str(dev))
+    st2.step()
+    r2 = st2.results()
+    ref = O.run_stack(w.x, w.mask, w.nbr, [(l.kind, l.W, l.bias, l.relu) for l in w.layers],
+                      w.dtype, pool=True)
+    for l in range(3):
+        assert_normwise_close(r2["outs"][l], ref["outs"][l], "bf16", f"C5 layer {l}")
+    assert_normwise_close(r2["pool"], ref["pool"], "bf16", "C5 pool")
+
+
+def test_empty_mask_path(dev):
+    from paper_2608_09388_amd.pipeline import SparseStack
+    w = synth.workload_c1()
+    w.mask = np.zeros_like(w.mask)
+    w.pool = True
+    st = SparseStack(w, device=str(dev))
+    st.dense_out.fill_(float("nan"))
+    st.pooled.fill_(float("nan"))
+    assert st.step() == 0
+    res = st.results()
+    assert res["n"] == 0 and np.all(res["row_ptr"] == 0) and np.all(res["inv"] == -1)
+    assert np.all(res["dense"] == 0) and np.all(res["pool"] == 0)

@@ -456,3 +456,24 @@ def test_density_reading_matches_table4(request):
     _, _, rp, n = O.compact(m.astype(np.uint8))
     sigma = np.sqrt(kv["vertices_dense"] * density * (1 - density) / B)
     assert abs(n / B - expected) < 4 * sigma
+
+
+def test_conv_at_and_linear_at_agree_with_full_layers():
+    B, V, K, Ci, Co = 3, 70, 9, 8, 5
+    rng = np.random.default_rng(13)
+    m = (rng.random((B, V)) < 0.3).astype(np.uint8)
+    nbr = rand_nbr(V, K, rng)
+    coords, inv, rp, n = O.compact(m)
+    S = rng.standard_normal((n, Ci))
+    W = rng.standard_normal((K, Ci, Co))
+    b = rng.standard_normal(Co)
+    rows = rng.choice(n, size=min(n, 25), replace=False)
+    for act in (False, True):
+        full = O.sparse_conv(S, coords, B, V, nbr, W, b, act)
+        np.testing.assert_allclose(O.conv_at(S, coords, B, V, nbr, W, rows, b, act), full[rows],
+                                   rtol=1e-12, atol=1e-12)
+        fl = O.sparse_linear(S, coords, B, V, W[0], b, act)
+        np.testing.assert_allclose(O.linear_at(S, W[0], rows, b, act), fl[rows],
+                                   rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(O.conv_at(S, coords, B, V, nbr, W, rows, b, scale=True),
+                               O.sparse_conv_scale(S, coords, B, V, nbr, W, b)[rows], rtol=1e-12)
