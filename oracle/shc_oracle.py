@@ -167,6 +167,56 @@ def sparse_conv_scale(S, coords, B, V, nbr, W, bias=None):
                        None if bias is None else np.abs(bias))
 
 
+def conv_at(S, coords, B, V, nbr, W, rows, bias=None, act=False, scale=False):
+    """Eqs. 4-5 evaluated at selected active rows only (for full-size checks).
+
+    Same definition as :func:`sparse_conv`: the dense convolution of the
+    masked input, read at the centre coordinates (b_i, v_i) of the selected
+    rows ``rows``.  The masked input at (b, u) is the C' feature row of
+    (b, u) when that coordinate is in C', else zero.  With ``scale`` the
+    abs-sum error scale is returned instead of the output.
+    """
+    S = np.asarray(S)
+    rows = np.asarray(rows, dtype=np.int64)
+    n = S.shape[0]
+    W = np.asarray(W, dtype=np.float64)
+    if scale:
+        W = np.abs(W)
+    K, _, Cout = W.shape
+    where = np.full(B * V, -1, dtype=np.int64)         # coordinate -> row of C'
+    where[coords[:, 0].astype(np.int64) * V + coords[:, 1]] = np.arange(n)
+    b = coords[rows, 0].astype(np.int64)
+    v = coords[rows, 1].astype(np.int64)
+    y = np.zeros((rows.size, Cout), dtype=np.float64)
+    for j in range(K):
+        u = nbr[v, j].astype(np.int64)
+        r = np.where(u >= 0, where[b * V + np.maximum(u, 0)], -1)
+        xm = np.where((r >= 0)[:, None], S[np.maximum(r, 0)].astype(np.float64), 0.0)
+        if scale:
+            xm = np.abs(xm)
+        y += xm @ W[j]
+    if bias is not None:
+        y += np.abs(bias) if scale else np.asarray(bias, dtype=np.float64)
+    if act and not scale:
+        y = relu(y)
+    return y
+
+
+def linear_at(S, W, rows, bias=None, act=False, scale=False):
+    """Eq. 6 at selected rows (row i of the result depends on S[i] only)."""
+    rows = np.asarray(rows, dtype=np.int64)
+    x = np.asarray(S)[rows].astype(np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    if scale:
+        x, W = np.abs(x), np.abs(W)
+    y = x @ W
+    if bias is not None:
+        y += np.abs(bias) if scale else np.asarray(bias, dtype=np.float64)
+    if act and not scale:
+        y = relu(y)
+    return y
+
+
 def scatter(S: np.ndarray, inv: np.ndarray, zero_fill: bool = True, D=None) -> np.ndarray:
     """Compact rows back to the dense [B*V] layout: D[r] = S[inv[r]] if active.
 
