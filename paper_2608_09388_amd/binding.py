@@ -61,7 +61,8 @@ def load(path: Optional[str] = None):
     global _lib
     if _lib is not None and path is None:
         return _lib
-    p = path or LIB_PATH
+    # SHC_LIB may name another build of the library (same ABI)
+    p = path or os.environ.get("SHC_LIB") or LIB_PATH
     if not os.path.exists(p):
         raise RuntimeError(f"{p} is not built: run `python -m paper_2608_09388_amd.build`")
     lib = ctypes.CDLL(p)

@@ -54,12 +54,10 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int BM = 128;
 constexpr int kRowBlocks = BM / 16;
-constexpr int kChunkBytes = 64;            // reduction bytes per row per chunk (one k-step)
-constexpr int kARow = kChunkBytes + 16;    // padded LDS row of the A stage (bytes)
 constexpr int kMaxSlots = 32;
-constexpr int kSlotsPerThread = kMaxSlots / 2;  // two threads build one row's index list
 
 typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
+
 #define SHC_LDS __attribute__((address_space(3)))
 
 template <bool BF16>
@@ -75,36 +73,39 @@ struct Elem<false> {
   static constexpr int per_vec = 4;
 };
 
-template <bool BF16, int BN>
+template <bool BF16, int BN, int CHUNK, int STAGES>
 struct Layout {
   using E = Elem<BF16>;
-  static constexpr int KC = kChunkBytes / E::bytes;   // reduction entries per chunk
+  static constexpr int KC = CHUNK / E::bytes;          // reduction entries per chunk
+  static constexpr int KSTEP = 64 / E::bytes;          // entries per MFMA k-step (64 bytes)
+  static constexpr int ARow = CHUNK + 16;              // padded LDS row of the A stage
   static constexpr int WRow = BN * E::bytes + 16;      // padded LDS row of the W stage
-  static constexpr int AStage = BM * kARow;
+  static constexpr int AStage = BM * ARow;
   static constexpr int WStage = KC * WRow;
   static constexpr int Stage = AStage + WStage;
   static constexpr int ORow = BN * E::bytes + 16;      // padded LDS row of the output stage
-  static constexpr int OutHalf = (BM / 2) * ORow;      // epilogue writes 64 rows at a time
-  static constexpr int Main = (2 * Stage > OutHalf) ? 2 * Stage : OutHalf;
-  static constexpr int AVecPerRow = kChunkBytes / 16;
+  static constexpr int Out = BM * ORow;                // whole output tile
+  static constexpr int OutHalf = (BM / 2) * ORow;      // half of it
+  static constexpr int Main = (STAGES * Stage > OutHalf) ? STAGES * Stage : OutHalf;
+  static constexpr bool OnePassOut = Out <= Main;      // else the epilogue runs in two halves
+  static constexpr int AVecPerRow = CHUNK / 16;
   static constexpr int AVecs = BM * AVecPerRow / kThreads;  // per thread
   static constexpr int WVecPerRow = BN * E::bytes / 16;
   static constexpr int WVecs = (KC * WVecPerRow + kThreads - 1) / kThreads;
 };
 
-template <int BN, bool BF16>
-size_t lds_bytes(int K) {
-  return (size_t)Layout<BF16, BN>::Main + (size_t)BM * K * sizeof(int32_t) +
-         kRowBlocks * sizeof(uint32_t) + 2 * BM * sizeof(int32_t);
+// Index area after the staging buffers (int32 words):
+//   srcs[BM*K] (row-major in tile order), srcs_p[BM*K] (permuted order),
+//   row_b[BM], row_v[BM], rowmask[BM], perm[BM], blk_slots[BM/16],
+//   bcnt[2][kMaxSlots + 2], scnt[2][kMaxSlots]
+constexpr int kBuckets = kMaxSlots + 2;
+inline size_t index_words(int K) {
+  return 2 * (size_t)BM * K + 4 * BM + kRowBlocks + 2 * kBuckets + 2 * kMaxSlots;
 }
 
-// (slot, offset) of reduction entry `off` entries past (j, c)
-__device__ __forceinline__ void advance(int& j, int& c, int off, int Cin) {
-  c += off;
-  while (c >= Cin) {
-    c -= Cin;
-    ++j;
-  }
+template <bool BF16, int BN, int CHUNK, int STAGES>
+size_t lds_bytes(int K) {
+  return (size_t)Layout<BF16, BN, CHUNK, STAGES>::Main + index_words(K) * sizeof(int32_t);
 }
 
 __device__ __forceinline__ uint32_t slot_range_bits(int j0, int j1) {
@@ -112,20 +113,27 @@ __device__ __forceinline__ uint32_t slot_range_bits(int j0, int j1) {
   return upto & ~((1u << j0) - 1u);
 }
 
-template <bool BF16, int BN, bool CONV>
-__global__ __launch_bounds__(kThreads, 3) void gather_gemm_kernel(GemmArgs a) {
+// SPT: neighbour slots per thread when building the index lists (two threads
+// per row), a bound on (K + 1) / 2 fixed at compile time.
+template <bool BF16, int BN, bool CONV, int CHUNK, int STAGES, int SPT>
+__global__ __launch_bounds__(kThreads, 2) void gather_gemm_kernel(GemmArgs a) {
   using E = Elem<BF16>;
-  using Lt = Layout<BF16, BN>;
+  using Lt = Layout<BF16, BN, CHUNK, STAGES>;
   constexpr int KC = Lt::KC;
   constexpr int WN = BN / 2;   // columns per wavefront
   constexpr int NB = WN / 16;  // 16-column blocks per wavefront
 
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int K = CONV ? a.K : 1;
-  int32_t* srcs = reinterpret_cast<int32_t*>(smem + Lt::Main);        // [BM][K]
-  uint32_t* blk_slots = reinterpret_cast<uint32_t*>(srcs + BM * K);    // [BM/16]
-  int32_t* row_b = reinterpret_cast<int32_t*>(blk_slots + kRowBlocks);  // [BM]
-  int32_t* row_v = row_b + BM;                                         // [BM]
+  int32_t* srcs0 = reinterpret_cast<int32_t*>(smem + Lt::Main);  // [BM][K], tile order
+  int32_t* srcs = srcs0 + BM * K;                                // [BM][K], permuted order
+  int32_t* row_b = srcs + BM * K;                                // [BM]
+  int32_t* row_v = row_b + BM;                                   // [BM]
+  uint32_t* rowmask = reinterpret_cast<uint32_t*>(row_v + BM);   // [BM]
+  int32_t* perm = reinterpret_cast<int32_t*>(rowmask + BM);      // [BM] tile row at position p
+  uint32_t* blk_slots = reinterpret_cast<uint32_t*>(perm + BM);  // [BM/16]
+  int32_t* bcnt = reinterpret_cast<int32_t*>(blk_slots + kRowBlocks);  // [2][kBuckets]
+  int32_t* scnt = bcnt + 2 * kBuckets;                                 // [2][kMaxSlots]
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -158,19 +166,15 @@ __global__ __launch_bounds__(kThreads, 3) void gather_gemm_kernel(GemmArgs a) {
 
   // ---- index lists of the tile -----------------------------------------------
   if (tid < kRowBlocks) blk_slots[tid] = 0;
+  if (tid < BM) rowmask[tid] = 0;
   if (CONV) {
     if (tid < BM) {
       const int64_t i = row0 + tid;
-      int b = -1, v = -1;
-      if (i < a.n_rows) {
-        const int2 c = reinterpret_cast<const int2*>(a.coords)[i];
-        if (c.x >= 0 && c.x < a.B && c.y >= 0 && c.y < a.V) {
-          b = c.x;
-          v = c.y;
-        }
-      }
-      row_b[tid] = b;
-      row_v[tid] = v;
+      const bool in = i < a.n_rows;
+      const int2 c = reinterpret_cast<const int2*>(a.coords)[in ? i : 0];
+      const bool ok = in && c.x >= 0 && c.x < a.B && c.y >= 0 && c.y < a.V;
+      row_b[tid] = ok ? c.x : -1;
+      row_v[tid] = ok ? c.y : -1;
     }
     __syncthreads();
     // two threads per row; thread h of row r takes slots h, h + 2, h + 4, ...
@@ -178,32 +182,91 @@ __global__ __launch_bounds__(kThreads, 3) void gather_gemm_kernel(GemmArgs a) {
     const int h = tid & 1;
     const int b = row_b[r];
     const int v = row_v[r];
-    int32_t nb[kSlotsPerThread];
+    // All loads of one level are issued before any is used, unconditionally
+    // (entries past K read a valid address and are masked afterwards), so the
+    // whole list costs two memory round trips.
+    const int vv = v >= 0 ? v : 0;
+    int32_t nb[SPT];
 #pragma unroll
-    for (int m = 0; m < kSlotsPerThread; ++m) {
+    for (int m = 0; m < SPT; ++m) {
       const int j = h + 2 * m;
-      nb[m] = -1;
-      if (j < K && v >= 0) nb[m] = a.nbr[(int64_t)v * K + j];
+      nb[m] = a.nbr[(int64_t)vv * K + (j < K ? j : K - 1)];
     }
+#pragma unroll
+    for (int m = 0; m < SPT; ++m) {
+      const int j = h + 2 * m;
+      nb[m] = (j < K && v >= 0 && nb[m] >= 0 && nb[m] < a.V) ? nb[m] : -1;
+    }
+    const int bb = b >= 0 ? b : 0;
+    int32_t sv[SPT];
+#pragma unroll
+    for (int m = 0; m < SPT; ++m) sv[m] = a.inv[(int64_t)bb * a.V + (nb[m] >= 0 ? nb[m] : 0)];
     uint32_t bits = 0;
 #pragma unroll
-    for (int m = 0; m < kSlotsPerThread; ++m) {
+    for (int m = 0; m < SPT; ++m) {
       const int j = h + 2 * m;
-      int32_t src = -1;
-      if (j < K && nb[m] >= 0 && nb[m] < a.V) {
-        const int32_t s = a.inv[(int64_t)b * a.V + nb[m]];
-        if (s >= 0 && (int64_t)s < a.n_rows) src = s;
-      }
-      if (j < K) srcs[r * K + j] = src;
+      const int32_t src = (nb[m] >= 0 && sv[m] >= 0 && (int64_t)sv[m] < a.n_rows) ? sv[m] : -1;
+      if (j < K) srcs0[r * K + j] = src;
       if (src >= 0) bits |= 1u << j;
     }
-    __syncthreads();  // blk_slots cleared above before any atomic
-    if (bits) atomicOr(&blk_slots[r >> 4], bits);
+    if (bits) atomicOr(&rowmask[r], bits);
+    __syncthreads();
+
+    // Row permutation: order the tile's rows by their first "sparse" slot
+    // (a slot present in fewer than half of the rows), rows with no sparse
+    // slot first and rows past the end last.  Rows sharing a sparse slot then
+    // sit in the same 16-row MFMA blocks, so far fewer (block, slot) products
+    // have to be computed.  Stable counting sort with wavefront ballots,
+    // done by waves 0 and 1 (one row per lane).
+    uint32_t rm = 0;
+    int bucket = 0, rank = 0;
+    if (tid < BM) {
+      rm = rowmask[tid];
+      const uint64_t lt = (1ull << lane) - 1ull;
+      for (int j = 0; j < K; ++j) {
+        const uint64_t bal = __ballot((rm >> j) & 1u);
+        if (lane == 0) scnt[wave * kMaxSlots + j] = __popcll(bal);
+      }
+      // rows past the end and their slot counts do not matter: they are zero
+      (void)lt;
+    }
+    __syncthreads();
+    if (tid < BM) {
+      uint32_t dense = 0;
+      for (int j = 0; j < K; ++j)
+        if (2 * (scnt[j] + scnt[kMaxSlots + j]) >= BM) dense |= 1u << j;
+      const uint32_t key = rm & ~dense;
+      const bool valid = row0 + tid < a.n_rows;
+      bucket = !valid ? K + 1 : (key ? 1 + __builtin_ctz(key) : 0);
+      const uint64_t lt = (1ull << lane) - 1ull;
+      for (int bk = 0; bk <= K + 1; ++bk) {
+        const uint64_t bal = __ballot(bucket == bk);
+        if (bucket == bk) rank = __popcll(bal & lt);
+        if (lane == 0) bcnt[wave * kBuckets + bk] = __popcll(bal);
+      }
+    }
+    __syncthreads();
+    if (tid < BM) {
+      int pos = rank + (wave == 1 ? bcnt[bucket] : 0);
+      for (int bk = 0; bk < bucket; ++bk) pos += bcnt[bk] + bcnt[kBuckets + bk];
+      perm[pos] = tid;
+    }
+    __syncthreads();
+    for (int e = tid; e < BM * K; e += kThreads) {
+      const int p = e / K;
+      const int j = e - p * K;
+      srcs[e] = srcs0[perm[p] * K + j];
+    }
+    if (tid < BM) {
+      const uint32_t m = rowmask[perm[tid]];
+      if (m) atomicOr(&blk_slots[tid >> 4], m);
+    }
   } else {
     __syncthreads();
     if (tid < BM) {
       const int64_t i = row0 + tid;
       srcs[tid] = i < a.n_rows ? (int32_t)i : -1;
+      perm[tid] = tid;
       if (i < a.n_rows) atomicOr(&blk_slots[tid >> 4], 1u);
     }
   }
@@ -211,57 +274,54 @@ __global__ __launch_bounds__(kThreads, 3) void gather_gemm_kernel(GemmArgs a) {
   uint32_t tile_slots = 0;
 #pragma unroll
   for (int q = 0; q < kRowBlocks; ++q) tile_slots |= blk_slots[q];
+  tile_slots = __builtin_amdgcn_readfirstlane(tile_slots);
   uint32_t my_blk[4];
 #pragma unroll
-  for (int rb = 0; rb < 4; ++rb) my_blk[rb] = blk_slots[wm * 4 + rb];
+  for (int rb = 0; rb < 4; ++rb)
+    my_blk[rb] = __builtin_amdgcn_readfirstlane(blk_slots[wm * 4 + rb]);
 
-  // ---- chunk bookkeeping (no division in the loop) ---------------------------
-  // A chunk starts at reduction entry k0 = chunk * KC, i.e. slot js, offset cs.
-  struct Pos {
-    int chunk, js, cs;
-  };
-  auto chunk_bits = [&](const Pos& p) -> uint32_t {
-    int je = p.js, ce = p.cs;
-    advance(je, ce, min(KC, Ktot - p.chunk * KC) - 1, Cin);
-    return slot_range_bits(p.js, je);
-  };
-  // first live chunk at or after p (p.chunk == nchunks when none)
-  auto next_live = [&](Pos p) -> Pos {
-    while (p.chunk < nchunks && (chunk_bits(p) & tile_slots) == 0u) {
-      ++p.chunk;
-      advance(p.js, p.cs, KC, Cin);
-    }
-    return p;
-  };
-  auto step = [&](Pos p) -> Pos {
-    ++p.chunk;
-    advance(p.js, p.cs, KC, Cin);
-    return next_live(p);
+  // ---- reduction walk ----------------------------------------------------------
+  // Slot of reduction entry kk: kk / Cin by multiply-high with the host's
+  // reciprocal ceil(2^32 / Cin) (exact for kk * Cin < 2^32), no division.
+  const uint32_t magic = a.cin_magic;
+  auto slot_of = [&](int kk) -> int { return (int)__umulhi((uint32_t)kk, magic); };
+  // slots touched by reduction entries [k_lo, k_hi), 0 past the end
+  auto range_bits = [&](int k_lo, int k_hi) -> uint32_t {
+    if (k_lo >= Ktot) return 0u;
+    return slot_range_bits(slot_of(k_lo), slot_of(min(k_hi, Ktot) - 1));
   };
 
   // ---- global -> register -> LDS staging -------------------------------------
+  // Every global load is issued unconditionally: an absent neighbour row or an
+  // out-of-range entry reads a valid address (the first row of S or of W) and
+  // the value is replaced by zero when it is written to LDS.  (Loads under a
+  // divergent branch would make the compiler wait for all outstanding loads
+  // and serialise the prefetch pipeline.)
   struct Regs {
     i32x4 a[Lt::AVecs];
     i32x4 w[Lt::WVecs];
+    uint32_t a_ok;  // bit u: a[u] holds data (else zeros are stored)
+    uint32_t w_ok;
   };
 
-  auto load_chunk = [&](const Pos& p, Regs& R) {
-    const int k0 = p.chunk * KC;
+  auto load_chunk = [&](int chunk, Regs& R) {
+    const int k0 = chunk * KC;
+    R.a_ok = 0;
 #pragma unroll
     for (int u = 0; u < Lt::AVecs; ++u) {
       const int idx = tid + u * kThreads;
       const int r = idx / Lt::AVecPerRow;
       const int q = idx % Lt::AVecPerRow;
-      int j = p.js, c = p.cs;
-      advance(j, c, q * E::per_vec, Cin);
-      i32x4 v = {0, 0, 0, 0};
-      if (k0 + q * E::per_vec < Ktot) {
-        const int32_t src = srcs[r * K + j];
-        if (src >= 0)
-          v = *reinterpret_cast<const i32x4*>(S + ((int64_t)src * Cin + c) * E::bytes);
-      }
-      R.a[u] = v;
+      const int kk = k0 + q * E::per_vec;
+      const int j = CONV ? slot_of(kk) : 0;
+      const int c = kk - j * Cin;
+      const int32_t src = srcs[r * K + (j < K ? j : K - 1)];
+      const bool ok = kk < Ktot && src >= 0;
+      const int64_t off = ok ? ((int64_t)src * Cin + c) * E::bytes : 0;
+      R.a[u] = *reinterpret_cast<const i32x4*>(S + off);
+      R.a_ok |= ok ? (1u << u) : 0u;
     }
+    R.w_ok = 0;
 #pragma unroll
     for (int u = 0; u < Lt::WVecs; ++u) {
       const int idx = tid + u * kThreads;
@@ -269,29 +329,33 @@ __global__ __launch_bounds__(kThreads, 3) void gather_gemm_kernel(GemmArgs a) {
       const int q = idx % Lt::WVecPerRow;
       const int kk = k0 + kr;
       const int n = n0 + q * E::per_vec;
-      i32x4 v = {0, 0, 0, 0};
-      if (kr < KC && kk < Ktot && n < Cout)
-        v = *reinterpret_cast<const i32x4*>(W + ((int64_t)kk * Cout + n) * E::bytes);
-      R.w[u] = v;
+      const bool ok = kr < KC && kk < Ktot && n < Cout;
+      const int64_t off = ok ? ((int64_t)kk * Cout + n) * E::bytes : 0;
+      R.w[u] = *reinterpret_cast<const i32x4*>(W + off);
+      R.w_ok |= ok ? (1u << u) : 0u;
     }
   };
 
   auto store_chunk = [&](const Regs& R, int buf) {
     unsigned char* a_lds = smem + buf * Lt::Stage;
     unsigned char* w_lds = a_lds + Lt::AStage;
+    const i32x4 zero = {0, 0, 0, 0};
 #pragma unroll
     for (int u = 0; u < Lt::AVecs; ++u) {
       const int idx = tid + u * kThreads;
       const int r = idx / Lt::AVecPerRow;
       const int q = idx % Lt::AVecPerRow;
-      *reinterpret_cast<i32x4*>(a_lds + r * kARow + q * 16) = R.a[u];
+      *reinterpret_cast<i32x4*>(a_lds + r * Lt::ARow + q * 16) =
+          ((R.a_ok >> u) & 1u) ? R.a[u] : zero;
     }
 #pragma unroll
     for (int u = 0; u < Lt::WVecs; ++u) {
       const int idx = tid + u * kThreads;
       const int kr = idx / Lt::WVecPerRow;
       const int q = idx % Lt::WVecPerRow;
-      if (kr < KC) *reinterpret_cast<i32x4*>(w_lds + kr * Lt::WRow + q * 16) = R.w[u];
+      if (kr < KC)
+        *reinterpret_cast<i32x4*>(w_lds + kr * Lt::WRow + q * 16) =
+            ((R.w_ok >> u) & 1u) ? R.w[u] : zero;
     }
   };
 
@@ -301,17 +365,16 @@ __global__ __launch_bounds__(kThreads, 3) void gather_gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute = [&](const Pos& p, int buf) {
-    const unsigned char* a_lds = smem + buf * Lt::Stage;
-    const unsigned char* w_lds = a_lds + Lt::AStage;
-    const uint32_t bits = chunk_bits(p);
+  // one 64-byte k-step (32 bf16 / 16 fp32 reduction entries) of a staged chunk
+  auto compute_step = [&](const unsigned char* a_lds, const unsigned char* w_lds, int ks,
+                          uint32_t bits) {
     if (BF16) {
       bf16x8 bfrag[NB];
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
-        // k rows 8g + (0..3 | 4..7), columns cb*16 + 4*(l16 % 4) of this lane's group
+        // k rows 8g + (0..3 | 4..7) of the step, columns cb*16 + 4*(l16 % 4) + 0..3
         const int col = wn * WN + cb * 16 + 4 * (l16 & 3);
-        const int kr = 8 * g + (l16 >> 2);
+        const int kr = ks * 32 + 8 * g + (l16 >> 2);
         const unsigned char* p0 = w_lds + kr * Lt::WRow + col * 2;
         const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
             (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0)));
@@ -323,7 +386,8 @@ __global__ __launch_bounds__(kThreads, 3) void gather_gemm_kernel(GemmArgs a) {
       for (int rb = 0; rb < 4; ++rb) {
         if ((my_blk[rb] & bits) == 0u) continue;
         const int row = wm * 64 + rb * 16 + l16;
-        const i32x4 af = *reinterpret_cast<const i32x4*>(a_lds + row * kARow + g * 16);
+        const i32x4 af =
+            *reinterpret_cast<const i32x4*>(a_lds + row * Lt::ARow + ks * 64 + g * 16);
         const bf16x8 afrag = __builtin_bit_cast(bf16x8, af);
 #pragma unroll
         for (int cb = 0; cb < NB; ++cb)
@@ -331,94 +395,125 @@ __global__ __launch_bounds__(kThreads, 3) void gather_gemm_kernel(GemmArgs a) {
               __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag, bfrag[cb], acc[rb][cb], 0, 0, 0);
       }
     } else {
-      // fp32: lane group g holds k = 4g .. 4g+3 of this 16-entry chunk;
+      // fp32: lane group g holds k = 4g .. 4g+3 of the step's 16 entries;
       // MFMA s uses component s of the A vector and W row 4g + s.
       float bw[NB][4];
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
         const int col = wn * WN + cb * 16 + l16;
 #pragma unroll
-        for (int s = 0; s < 4; ++s)
-          bw[cb][s] = *reinterpret_cast<const float*>(w_lds + (4 * g + s) * Lt::WRow + col * 4);
+        for (int s2 = 0; s2 < 4; ++s2)
+          bw[cb][s2] = *reinterpret_cast<const float*>(
+              w_lds + (ks * 16 + 4 * g + s2) * Lt::WRow + col * 4);
       }
 #pragma unroll
       for (int rb = 0; rb < 4; ++rb) {
         if ((my_blk[rb] & bits) == 0u) continue;
         const int row = wm * 64 + rb * 16 + l16;
-        const i32x4 af = *reinterpret_cast<const i32x4*>(a_lds + row * kARow + g * 16);
+        const i32x4 af =
+            *reinterpret_cast<const i32x4*>(a_lds + row * Lt::ARow + ks * 64 + g * 16);
 #pragma unroll
         for (int cb = 0; cb < NB; ++cb)
 #pragma unroll
-          for (int s = 0; s < 4; ++s)
-            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(af[s]), bw[cb][s],
-                                                               acc[rb][cb], 0, 0, 0);
+          for (int s2 = 0; s2 < 4; ++s2)
+            acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                __int_as_float(af[s2]), bw[cb][s2], acc[rb][cb], 0, 0, 0);
       }
     }
   };
 
-  // ---- main loop: loads two chunks ahead, LDS double buffer -------------------
-  // Invariant at the top of an iteration: chunk `c0` is in LDS buffer `buf`,
-  // chunk `c1` (the next live one) is in registers R[x] (or absent), and R[x^1]
-  // is free.
-  Regs R0, R1;
-  Pos c0 = next_live(Pos{0, 0, 0});
-  Pos c1 = c0.chunk < nchunks ? step(c0) : c0;
-  if (c0.chunk < nchunks) {
-    load_chunk(c0, R0);
-    if (c1.chunk < nchunks) load_chunk(c1, R1);
-    store_chunk(R0, 0);
-  }
-  __syncthreads();
-  int buf = 0;
-  // two iterations per trip so that the register sets keep fixed roles
-  while (c0.chunk < nchunks) {
-    {
-      const Pos c2 = c1.chunk < nchunks ? step(c1) : c1;
-      if (c2.chunk < nchunks) load_chunk(c2, R0);
-      compute(c0, buf);
-      if (c1.chunk < nchunks) store_chunk(R1, buf ^ 1);
-      __syncthreads();
-      buf ^= 1;
-      c0 = c1;
-      c1 = c2;
+  auto compute = [&](int chunk, int buf) {
+    const unsigned char* a_lds = smem + buf * Lt::Stage;
+    const unsigned char* w_lds = a_lds + Lt::AStage;
+    constexpr int KS = KC / Lt::KSTEP;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int klo = chunk * KC + ks * Lt::KSTEP;
+      const uint32_t bits = __builtin_amdgcn_readfirstlane(range_bits(klo, klo + Lt::KSTEP));
+      compute_step(a_lds, w_lds, ks, bits);
     }
-    if (c0.chunk >= nchunks) break;
-    {
-      const Pos c2 = c1.chunk < nchunks ? step(c1) : c1;
-      if (c2.chunk < nchunks) load_chunk(c2, R1);
-      compute(c0, buf);
-      if (c1.chunk < nchunks) store_chunk(R0, buf ^ 1);
+  };
+
+  // ---- main loop -------------------------------------------------------------
+  // bias of this lane's columns, read once, long before the epilogue needs it
+  float bias_v[NB];
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) {
+    const int col = n0 + wn * WN + cb * 16 + l16;
+    const bool ok = a.bias != nullptr && col < Cout;
+    const float* bp = a.bias != nullptr ? a.bias : reinterpret_cast<const float*>(a.W);
+    const float bvl = bp[ok ? col : 0];
+    bias_v[cb] = ok ? bvl : 0.f;
+  }
+
+  // ---- main loop: software pipeline over steps t = 0, 1, ... ---------------------
+  // Step t loads chunk t into register set t % 2, runs the MFMAs of chunk
+  // t - 2 from LDS buffer t % 2, and stores chunk t - 1 (register set
+  // (t - 1) % 2, loaded one step earlier) into LDS buffer (t - 1) % 2; one
+  // barrier per step.  A chunk's loads thus have two steps of MFMA work to
+  // arrive.  Every step issues its loads (past the end they re-read the last
+  // chunk): a load under even a uniform branch leaves the compiler unsure how
+  // many loads are outstanding, and it then waits for all of them.  The trip
+  // count is even so the two register sets keep fixed roles.
+  if (STAGES == 2) {
+    const int last = nchunks - 1;
+    const int nsteps = (nchunks + 3) & ~1;  // >= nchunks + 2, even
+    Regs R0, R1;
+    for (int t = 0; t < nsteps; t += 2) {
+      // even step t: buffers t % 2 = 0 (compute) and 1 (store)
+      load_chunk(min(t, last), R0);
+      if (t >= 2) compute(t - 2, 0);
+      if (t >= 1 && t - 1 < nchunks) store_chunk(R1, 1);
       __syncthreads();
-      buf ^= 1;
-      c0 = c1;
-      c1 = c2;
+      // odd step t + 1
+      load_chunk(min(t + 1, last), R1);
+      if (t + 1 >= 2 && t - 1 < nchunks) compute(t - 1, 1);
+      if (t < nchunks) store_chunk(R0, 0);
+      __syncthreads();
+    }
+  } else {
+    // single LDS buffer: loads run one chunk ahead in registers; two barriers per chunk
+    const int last = nchunks - 1;
+    Regs R;
+    load_chunk(0, R);
+    store_chunk(R, 0);
+    __syncthreads();
+    for (int c = 0; c < nchunks; ++c) {
+      load_chunk(min(c + 1, last), R);
+      compute(c, 0);
+      __syncthreads();
+      if (c + 1 < nchunks) {
+        store_chunk(R, 0);
+        __syncthreads();
+      }
     }
   }
 
   // ---- epilogue: bias + activation + rounding, staged through LDS -----------
-  // rows 0..63 (wm = 0) first, then rows 64..127 (wm = 1)
+  // LDS row p holds tile row perm[p]; rows are written back as 16-byte vectors.
   unsigned char* o_lds = smem;
   unsigned char* out = static_cast<unsigned char*>(a.out);
   constexpr int kVecPerRow = BN * E::bytes / 16;
+  constexpr int kPasses = Lt::OnePassOut ? 1 : 2;
+  constexpr int kRowsPerPass = BM / kPasses;
   const int ncols = min(BN, Cout - n0);
   const int vec_valid = ncols * E::bytes / 16;
-  for (int half = 0; half < 2; ++half) {
-    if (wm == half) {
+  for (int pass = 0; pass < kPasses; ++pass) {
+    if (kPasses == 1 || wm == pass) {
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
         const int col_l = wn * WN + cb * 16 + l16;
-        const int col = n0 + col_l;
-        const float bv = (a.bias != nullptr && col < Cout) ? a.bias[col] : 0.f;
+        const float bv = bias_v[cb];
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const int row_l = rb * 16 + g * 4 + r;
+            const int row_l = (kPasses == 1 ? wm * 64 : 0) + rb * 16 + g * 4 + r;
             float v = acc[rb][cb][r] + bv;
             if (a.relu) v = v > 0.f ? v : 0.f;
             unsigned char* p = o_lds + row_l * Lt::ORow + col_l * E::bytes;
-            if (BF16)
-              *reinterpret_cast<uint16_t*>(p) = (uint16_t)f32_to_bf16_bits(v);
+            if (BF16)  // hardware round-to-nearest-even conversion
+              *reinterpret_cast<__bf16*>(p) = static_cast<__bf16>(v);
             else
               *reinterpret_cast<float*>(p) = v;
           }
@@ -426,25 +521,22 @@ __global__ __launch_bounds__(kThreads, 3) void gather_gemm_kernel(GemmArgs a) {
       }
     }
     __syncthreads();
-    for (int idx = tid; idx < (BM / 2) * kVecPerRow; idx += kThreads) {
+    for (int idx = tid; idx < kRowsPerPass * kVecPerRow; idx += kThreads) {
       const int r = idx / kVecPerRow;
       const int q = idx % kVecPerRow;
-      const int64_t i = row0 + half * (BM / 2) + r;
+      const int64_t i = row0 + perm[pass * kRowsPerPass + r];
       if (i < a.n_rows && q < vec_valid) {
         const i32x4 v = *reinterpret_cast<const i32x4*>(o_lds + r * Lt::ORow + q * 16);
         *reinterpret_cast<i32x4*>(out + (i * Cout + n0) * E::bytes + q * 16) = v;
       }
     }
-    __syncthreads();
+    if (kPasses == 2) __syncthreads();
   }
 }
 
-template <bool BF16, int BN, bool CONV>
-hipError_t launch_tile(const GemmArgs& a, hipStream_t stream) {
-  const unsigned gx = (unsigned)((a.n_rows + BM - 1) / BM);
-  const unsigned gy = (unsigned)((a.Cout + BN - 1) / BN);
-  const size_t lds = lds_bytes<BN, BF16>(CONV ? a.K : 1);
-  auto kern = gather_gemm_kernel<BF16, BN, CONV>;
+template <typename Kern>
+hipError_t launch_kernel(Kern kern, unsigned gx, unsigned gy, size_t lds, hipStream_t stream,
+                         const GemmArgs& a) {
   // allow more than 64 KB of dynamic LDS (gfx950 has 160 KB per CU); once per instantiation
   static std::once_flag once;
   static hipError_t attr_err = hipSuccess;
@@ -455,6 +547,29 @@ hipError_t launch_tile(const GemmArgs& a, hipStream_t stream) {
   if (attr_err != hipSuccess) return attr_err;
   hipLaunchKernelGGL(kern, dim3(gx, gy), dim3(kThreads), lds, stream, a);
   return hipGetLastError();
+}
+
+#ifndef SHC_GEMM_CHUNK
+#define SHC_GEMM_CHUNK 64
+#endif
+#ifndef SHC_GEMM_STAGES
+#define SHC_GEMM_STAGES 2
+#endif
+
+template <bool BF16, int BN, bool CONV>
+hipError_t launch_tile(const GemmArgs& a_in, hipStream_t stream) {
+  constexpr int CH = SHC_GEMM_CHUNK;
+  constexpr int ST = SHC_GEMM_STAGES;
+  GemmArgs a = a_in;
+  a.cin_magic = (uint32_t)(((1ull << 32) + (uint64_t)a.Cin - 1) / (uint64_t)a.Cin);
+  const unsigned gx = (unsigned)((a.n_rows + BM - 1) / BM);
+  const unsigned gy = (unsigned)((a.Cout + BN - 1) / BN);
+  const size_t lds = lds_bytes<BF16, BN, CH, ST>(CONV ? a.K : 1);
+  if (!CONV || a.K <= 10)
+    return launch_kernel(gather_gemm_kernel<BF16, BN, CONV, CH, ST, CONV ? 5 : 1>, gx, gy, lds,
+                         stream, a);
+  return launch_kernel(gather_gemm_kernel<BF16, BN, CONV, CH, ST, kMaxSlots / 2>, gx, gy, lds,
+                       stream, a);
 }
 
 template <bool BF16, bool CONV>

@@ -68,6 +68,7 @@ struct GemmArgs {
   int64_t n_rows;
   int32_t B, V, K, Cin, Cout;
   int32_t relu;
+  uint32_t cin_magic;   // ceil(2^32 / Cin), filled in by the launcher
 };
 
 hipError_t launch_gather_gemm(const GemmArgs& a, bool conv, bool bf16, hipStream_t stream);
