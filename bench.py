@@ -37,6 +37,10 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_conv_c4_5pct.txt")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_09388_amd", "csrc", "gemm.hip")
 
 
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -122,6 +126,7 @@ def main():
     w = synth.workload_c4(args.density)
     st = SparseStack(w, device="cuda:0")
     n = st.compact()
+    log(f"workload ready: N'={n} active rows of {w.B * w.V}")
     L = len(w.layers)
     stream = torch.cuda.current_stream()
 
@@ -158,6 +163,7 @@ def main():
         per_kernel_ms[name] = float(np.mean([events[s][k].elapsed_time(events[s][k + 1])
                                              for s in range(args.steps)]))
     ms_per_step = wall * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.4f} ms/step")
     value = n * L / (ms_per_step / 1e3)
 
     # roofline of the dominant kernel (the conv layer)
@@ -203,9 +209,11 @@ def main():
 
     if not args.no_dense:
         out["speedup_vs_dense"] = dense_comparison(st, w, per_kernel_ms, torch, shc, synth)
+        log("dense comparison done")
     if not args.no_cpu_baseline:
         spec = [(l.kind, l.W, l.bias, l.relu) for l in w.layers]
         out["cpu_baseline"] = cpu_baseline(w, spec, args.cpu_seconds)
+        log("cpu baseline done")
     print(json.dumps(out))
 
 

@@ -1,0 +1,519 @@
+// Weight-stationary gathered-row contraction: the sparse neighbourhood
+// convolution (Eqs. 4-5) and the sparse linear layer (Eq. 6) for the shapes
+// where a column slice of the weights fits in LDS.
+//
+// The computed quantity is the same as in gemm.hip:
+//
+//   out[i][n] = act( bias[n] + sum_{j<K} sum_{c<Cin} S[r_ij][c] * W[j][c][n] ),
+//
+// with r_ij = inv[b_i*V + nbr[v_i*K + j]] (conv) or i (linear, K = 1), and a
+// slot with r_ij = -1 adding nothing.
+//
+// Organisation (one workgroup = 8 wavefronts = 512 threads, one per CU):
+//   * the grid is (row groups) x (column slices of width WS).  A workgroup
+//     copies W[:, :, slice] (all K*Cin reduction rows) into LDS once and keeps
+//     it there, so the weights cross the memory system once per workgroup;
+//   * it builds the index lists of its whole row range with three rounds of
+//     loads (coordinates, neighbour vertices, inverse-map rows), each round
+//     fully in flight, while the weight slice streams in alongside;
+//   * the rows are counting-sorted (wavefront ballots, stable) by their first
+//     sparse slot -- a slot present in fewer than half of the rows.  16-row
+//     blocks then hold rows with only dense slots, or rows sharing a sparse
+//     slot, and each block carries the set of slots any of its rows has;
+//   * every wavefront walks a list of jobs (block, live slot) over blocks
+//     b = wave, wave + 8, ...  A job loads the A fragments of its slot (16
+//     bytes per lane of the gathered neighbour rows, one per 64-byte k-step)
+//     straight from global memory; jobs are issued D ahead through a ring of
+//     register sets, so about 16 fragment loads per wave are in flight.  The
+//     B fragments come from the resident slice (ds_read_b64_tr_b16 for bf16)
+//     and each feeds one MFMA per 16 output columns.  No barrier in this loop;
+//   * when a block's last job is done its 16 rows x WS columns get the bias,
+//     the activation and the rounding, and go back through a per-wave LDS
+//     scratch as 16-byte vectors to the rows' original positions.
+// Every output row is accumulated over the same (slot, k-step) sequence
+// whatever block it lands in (absent slots contribute exact zeros), so the
+// result does not depend on the order the sort produced.
+#include <mutex>
+
+#include "shc_internal.h"
+
+namespace shc {
+namespace {
+
+constexpr int kThreads = 512;
+constexpr int kWaves = kThreads / 64;
+constexpr int kMaxSlots = 32;
+constexpr int kBuckets = kMaxSlots + 2;
+constexpr int kRPT = 3;                       // rows per thread in the index build
+constexpr int kMaxRows = kRPT * kThreads;     // rows per workgroup
+constexpr int kLdsLimit = 160 * 1024;
+constexpr int kWBatch = 8;                    // weight vectors in flight per thread
+
+typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
+#define SHC_LDS __attribute__((address_space(3)))
+
+template <bool BF16>
+struct WElem;
+template <>
+struct WElem<true> {
+  static constexpr int bytes = 2;
+  static constexpr int per_vec = 8;
+  static constexpr int kstep = 32;  // entries per MFMA k-step (64 bytes)
+};
+template <>
+struct WElem<false> {
+  static constexpr int bytes = 4;
+  static constexpr int per_vec = 4;
+  static constexpr int kstep = 16;
+};
+
+__host__ __device__ inline int ws_wrow(int ws, int e) { return ws * e + 16; }
+// srcs[rows*K], perm[rows], blkmask[rows/16], scnt[waves][kMaxSlots],
+// bcnt[kBuckets][kRPT][waves] (counts, then exclusive starts, in scan order)
+__host__ __device__ inline int ws_idx_bytes(int rows, int K) {
+  return (4 * (rows * K + rows + rows / 16 + kWaves * kMaxSlots + kRPT * kWaves * kBuckets) +
+          15) & ~15;
+}
+__host__ __device__ inline int ws_scratch(int ws, int e) { return kWaves * 16 * ws_wrow(ws, e); }
+
+// KM: slots held per row in registers during the index build (>= K).
+// KSM: k-steps per slot held per job (>= Cin / kstep); D jobs in flight.
+template <bool BF16, int WS, bool CONV, int KM, int KSM>
+__global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
+  using E = WElem<BF16>;
+  constexpr int NCB = WS / 16;             // 16-column blocks in the slice
+  constexpr int WROW = WS * E::bytes + 16;
+  constexpr int VPR = WS * E::bytes / 16;  // 16-byte vectors per slice row
+  constexpr int D = 16 / KSM;              // jobs in flight
+
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int K = CONV ? a.K : 1;
+  const int Cin = a.Cin;
+  const int Cout = a.Cout;
+  const int Ktot = K * Cin;
+  const int KS = Cin / E::kstep;  // k-steps per slot (Cin * e is a multiple of 64)
+
+  unsigned char* wl = smem;  // [Ktot][WROW]
+  const int wbytes = (Ktot * WROW + 15) & ~15;
+  int32_t* srcs = reinterpret_cast<int32_t*>(smem + wbytes);    // [R][K], sorted order
+  int32_t* perm = srcs + R * K;                                 // [R] position -> row
+  uint32_t* blkmask = reinterpret_cast<uint32_t*>(perm + R);    // [R/16]
+  int32_t* scnt = reinterpret_cast<int32_t*>(blkmask + R / 16); // [waves][kMaxSlots]
+  int32_t* bcnt = scnt + kWaves * kMaxSlots;                    // [kBuckets][kRPT][waves]
+  unsigned char* scratch = smem + wbytes + ws_idx_bytes(R, K);  // [waves][16][WROW]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int g = lane >> 4;
+  const int l16 = lane & 15;
+
+  const int64_t row0 = (int64_t)blockIdx.x * R;
+  const int nrows = (int)min((int64_t)R, a.n_rows - row0);
+  const int nblk = (nrows + 15) / 16;
+  const int n0 = blockIdx.y * WS;
+  const unsigned char* S = static_cast<const unsigned char*>(a.S);
+  const unsigned char* W = static_cast<const unsigned char*>(a.W);
+
+  // ---- weight slice W[k][n0 .. n0 + WS) -> LDS, kWBatch vectors per thread at a time
+  const int wvecs = Ktot * VPR;
+  auto load_w = [&](int base, i32x4* wv) {
+#pragma unroll
+    for (int u = 0; u < kWBatch; ++u) {
+      const int v = base + u * kThreads + tid;
+      const int k = v / VPR;
+      const int q = v - k * VPR;
+      const int n = n0 + q * E::per_vec;
+      const bool ok = v < wvecs && n < Cout;
+      wv[u] = *reinterpret_cast<const i32x4*>(
+          W + (ok ? ((int64_t)k * Cout + n) * E::bytes : 0));
+      if (!ok) wv[u] = i32x4{0, 0, 0, 0};
+    }
+  };
+  auto store_w = [&](int base, const i32x4* wv) {
+#pragma unroll
+    for (int u = 0; u < kWBatch; ++u) {
+      const int v = base + u * kThreads + tid;
+      const int k = v / VPR;
+      const int q = v - k * VPR;
+      if (v < wvecs) *reinterpret_cast<i32x4*>(wl + k * WROW + q * 16) = wv[u];
+    }
+  };
+  i32x4 wv[kWBatch];
+  load_w(0, wv);
+
+  for (int q = tid; q < R / 16; q += kThreads) blkmask[q] = 0;
+  const uint64_t lt = (1ull << lane) - 1ull;
+
+  // ---- index lists, sorted by first sparse slot ---------------------------------
+  // thread tid handles rows t = tid + rr * 512 (rr < kRPT) of this workgroup
+  if (CONV) {
+    int rb[kRPT], rv[kRPT];
+#pragma unroll
+    for (int rr = 0; rr < kRPT; ++rr) {
+      const int t = tid + rr * kThreads;
+      const bool in = t < nrows;
+      const int2 c = reinterpret_cast<const int2*>(a.coords)[row0 + (in ? t : 0)];
+      const bool ok = in && c.x >= 0 && c.x < a.B && c.y >= 0 && c.y < a.V;
+      rb[rr] = ok ? c.x : -1;
+      rv[rr] = ok ? c.y : -1;
+    }
+    int32_t sv[kRPT][KM];
+#pragma unroll
+    for (int rr = 0; rr < kRPT; ++rr)
+#pragma unroll
+      for (int j = 0; j < KM; ++j)
+        sv[rr][j] = a.nbr[(int64_t)(rv[rr] >= 0 ? rv[rr] : 0) * K + (j < K ? j : K - 1)];
+    store_w(0, wv);
+    load_w(kWBatch * kThreads, wv);  // possibly all dummies: kept unconditional
+#pragma unroll
+    for (int rr = 0; rr < kRPT; ++rr)
+#pragma unroll
+      for (int j = 0; j < KM; ++j) {
+        const int32_t nb = sv[rr][j];
+        sv[rr][j] = (j < K && rv[rr] >= 0 && nb >= 0 && nb < a.V) ? nb : -1;
+      }
+#pragma unroll
+    for (int rr = 0; rr < kRPT; ++rr)
+#pragma unroll
+      for (int j = 0; j < KM; ++j) {
+        const int32_t nb = sv[rr][j];
+        sv[rr][j] = a.inv[(int64_t)(rb[rr] >= 0 ? rb[rr] : 0) * a.V + (nb >= 0 ? nb : 0)] |
+                    (nb >= 0 ? 0 : int32_t(0x80000000));
+      }
+    store_w(kWBatch * kThreads, wv);
+    uint32_t rmask[kRPT];
+#pragma unroll
+    for (int rr = 0; rr < kRPT; ++rr) {
+      rmask[rr] = 0;
+#pragma unroll
+      for (int j = 0; j < KM; ++j) {
+        const int32_t s = sv[rr][j];
+        sv[rr][j] = (s >= 0 && (int64_t)s < a.n_rows) ? s : -1;
+        if (sv[rr][j] >= 0) rmask[rr] |= 1u << j;
+      }
+    }
+    // weight vectors past the first two batches (large slices only)
+    for (int base = 2 * kWBatch * kThreads; base < wvecs; base += kWBatch * kThreads) {
+      load_w(base, wv);
+      store_w(base, wv);
+    }
+    // rows per slot, then the dense slots
+    for (int j = 0; j < K; ++j) {
+      int c = 0;
+#pragma unroll
+      for (int rr = 0; rr < kRPT; ++rr) c += __popcll(__ballot((rmask[rr] >> j) & 1u));
+      if (lane == 0) scnt[wave * kMaxSlots + j] = c;
+    }
+    __syncthreads();
+    uint32_t dense = 0;
+    for (int j = 0; j < K; ++j) {
+      int c = 0;
+      for (int w = 0; w < kWaves; ++w) c += scnt[w * kMaxSlots + j];
+      if (2 * c >= nrows) dense |= 1u << j;
+    }
+    // buckets: 0 = dense slots only, 1 + j = first sparse slot j, K + 1 = past
+    // the end, -1 = no such row (t >= R)
+    int bkt[kRPT], rank[kRPT];
+#pragma unroll
+    for (int rr = 0; rr < kRPT; ++rr) {
+      const int t = tid + rr * kThreads;
+      const uint32_t key = rmask[rr] & ~dense;
+      bkt[rr] = t >= R ? -1 : (t >= nrows ? K + 1 : (key ? 1 + __builtin_ctz(key) : 0));
+      rank[rr] = 0;
+    }
+    for (int bk = 0; bk <= K + 1; ++bk) {
+#pragma unroll
+      for (int rr = 0; rr < kRPT; ++rr) {
+        const uint64_t bal = __ballot(bkt[rr] == bk);
+        if (bkt[rr] == bk) rank[rr] = __popcll(bal & lt);
+        if (lane == 0) bcnt[(bk * kRPT + rr) * kWaves + wave] = __popcll(bal);
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {  // exclusive scan in (bucket, rr, wave) order: stable in row order
+      const int ne = (K + 2) * kRPT * kWaves;
+      const int per = (ne + 63) / 64;
+      const int e0 = lane * per;
+      int local = 0;
+      for (int e = e0; e < e0 + per && e < ne; ++e) local += bcnt[e];
+      int inc = local;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int y = __shfl_up(inc, d, 64);
+        if (lane >= d) inc += y;
+      }
+      int run = inc - local;
+      for (int e = e0; e < e0 + per && e < ne; ++e) {
+        const int n = bcnt[e];
+        bcnt[e] = run;
+        run += n;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int rr = 0; rr < kRPT; ++rr) {
+      if (bkt[rr] >= 0) {
+        const int pos = bcnt[(bkt[rr] * kRPT + rr) * kWaves + wave] + rank[rr];
+        perm[pos] = tid + rr * kThreads;
+#pragma unroll
+        for (int j = 0; j < KM; ++j)
+          if (j < K) srcs[pos * K + j] = sv[rr][j];
+        if (rmask[rr]) atomicOr(&blkmask[pos >> 4], rmask[rr]);
+      }
+    }
+  } else {
+    for (int base = 0; base < wvecs; base += kWBatch * kThreads) {
+      if (base > 0) load_w(base, wv);
+      store_w(base, wv);
+    }
+    __syncthreads();
+    for (int t = tid; t < R; t += kThreads) {
+      srcs[t] = t < nrows ? (int32_t)(row0 + t) : -1;
+      perm[t] = t;
+    }
+    for (int q = tid; q < R / 16; q += kThreads) blkmask[q] = (16 * q < nrows) ? 1u : 0u;
+  }
+  __syncthreads();
+
+  // ---- per-wave job loop -----------------------------------------------------------
+  float bias_v[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    const int col = n0 + cb * 16 + l16;
+    const bool ok = a.bias != nullptr && col < Cout;
+    const float* bp = a.bias != nullptr ? a.bias : reinterpret_cast<const float*>(a.W);
+    const float bvl = bp[ok ? col : 0];
+    bias_v[cb] = ok ? bvl : 0.f;
+  }
+  unsigned char* my_scratch = scratch + wave * 16 * WROW;
+  unsigned char* out = static_cast<unsigned char*>(a.out);
+
+  struct Job {
+    int blk;    // block, or -1 past the end
+    int j;      // slot, or -1 for a block with no present slot (bias only)
+    bool last;  // last job of its block
+  };
+  int gb = wave - kWaves;  // job generator: current block and its slots left
+  uint32_t grem = 0;
+  bool gpending = false;   // block gb still owes its (bias-only) job
+  auto next_job = [&]() -> Job {
+    while (grem == 0 && !gpending) {
+      gb += kWaves;
+      if (gb >= nblk) return Job{-1, -1, true};
+      grem = __builtin_amdgcn_readfirstlane(blkmask[gb]);
+      gpending = grem == 0;  // rows without any present slot still need an output
+    }
+    if (gpending) {
+      gpending = false;
+      return Job{gb, -1, true};
+    }
+    const int j = __builtin_ctz(grem);
+    grem &= grem - 1;
+    return Job{gb, j, grem == 0};
+  };
+
+  struct Frags {
+    i32x4 v[KSM];
+    uint32_t ok;
+  };
+  // A fragments of a job (dummy loads of a valid address when there is nothing to load)
+  auto issue = [&](const Job& jb, Frags& f) {
+    const bool live = jb.blk >= 0 && jb.j >= 0;
+    const int32_t src = live ? srcs[(jb.blk * 16 + l16) * K + jb.j] : -1;
+    f.ok = 0;
+#pragma unroll
+    for (int ks = 0; ks < KSM; ++ks) {
+      const bool ok = src >= 0 && ks < KS;
+      const int c = ks * E::kstep + g * E::per_vec;
+      f.v[ks] = *reinterpret_cast<const i32x4*>(
+          S + (ok ? ((int64_t)src * Cin + c) * E::bytes : 0));
+      f.ok |= ok ? (1u << ks) : 0u;
+    }
+  };
+
+  f32x4 acc[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](const Job& jb, const Frags& f) {
+    if (jb.blk < 0 || jb.j < 0) return;
+#pragma unroll
+    for (int ks = 0; ks < KSM; ++ks) {
+      if (ks >= KS) break;
+      const i32x4 af = ((f.ok >> ks) & 1u) ? f.v[ks] : i32x4{0, 0, 0, 0};
+      const int krow = jb.j * Cin + ks * E::kstep;  // first reduction row of the k-step
+      if (BF16) {
+        const bf16x8 afrag = __builtin_bit_cast(bf16x8, af);
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          const unsigned char* p0 =
+              wl + (krow + 8 * g + (l16 >> 2)) * WROW + (cb * 16 + 4 * (l16 & 3)) * 2;
+          const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0)));
+          const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0 + 4 * WROW)));
+          const bf16x8 bfrag = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afrag, bfrag, acc[cb], 0, 0, 0);
+        }
+      } else {
+        // lane group g holds k = 4g .. 4g+3 of the k-step; MFMA s uses
+        // component s of the A vector and slice row 4g + s
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+          for (int s2 = 0; s2 < 4; ++s2) {
+            const float bw = *reinterpret_cast<const float*>(
+                wl + (krow + 4 * g + s2) * WROW + (cb * 16 + l16) * 4);
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(af[s2]), bw, acc[cb],
+                                                           0, 0, 0);
+          }
+      }
+    }
+  };
+
+  auto epilogue = [&](int blk) {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float v = acc[cb][r] + bias_v[cb];
+        if (a.relu) v = v > 0.f ? v : 0.f;
+        unsigned char* pp = my_scratch + (g * 4 + r) * WROW + (cb * 16 + l16) * E::bytes;
+        if (BF16)  // hardware round-to-nearest-even conversion
+          *reinterpret_cast<__bf16*>(pp) = static_cast<__bf16>(v);
+        else
+          *reinterpret_cast<float*>(pp) = v;
+      }
+      acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int idx0 = 0; idx0 < 16 * VPR; idx0 += 64) {
+      const int idx = idx0 + lane;
+      const int r = idx / VPR;
+      const int q = idx % VPR;
+      const int pos = blk * 16 + r;
+      const int n = n0 + q * E::per_vec;
+      if (idx < 16 * VPR && pos < nrows && n < Cout) {
+        const int64_t i = row0 + perm[pos];
+        const i32x4 v = *reinterpret_cast<const i32x4*>(my_scratch + r * WROW + q * 16);
+        *reinterpret_cast<i32x4*>(out + (i * Cout + n) * E::bytes) = v;
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+
+  // ring of D jobs; every slot of the ring issues its loads unconditionally
+  Job jobs[D];
+  Frags fr[D];
+#pragma unroll
+  for (int u = 0; u < D; ++u) {
+    jobs[u] = next_job();
+    issue(jobs[u], fr[u]);
+  }
+  // Every ring slot is processed on every trip (an exhausted job computes
+  // nothing and reloads a dummy address), so the loads of the other D - 1
+  // jobs are never under a branch and stay in flight while one computes.
+  while (jobs[0].blk >= 0) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      compute(jobs[u], fr[u]);
+      if (jobs[u].blk >= 0 && jobs[u].last) epilogue(jobs[u].blk);
+      jobs[u] = next_job();
+      issue(jobs[u], fr[u]);
+    }
+  }
+}
+
+template <bool BF16, int WS, bool CONV, int KM, int KSM>
+hipError_t launch_ws(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) {
+  const unsigned gx = (unsigned)((a.n_rows + pl.rows - 1) / pl.rows);
+  const unsigned gy = (unsigned)((a.Cout + WS - 1) / WS);
+  auto kern = ws_kernel<BF16, WS, CONV, KM, KSM>;
+  // allow the large dynamic LDS allocation; once per instantiation
+  static std::once_flag once;
+  static hipError_t attr_err = hipSuccess;
+  std::call_once(once, [&] {
+    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit);
+  });
+  if (attr_err != hipSuccess) return attr_err;
+  hipLaunchKernelGGL(kern, dim3(gx, gy), dim3(kThreads), (size_t)pl.total, stream, a, pl.rows);
+  return hipGetLastError();
+}
+
+template <bool BF16, int WS, bool CONV>
+hipError_t launch_ws_k(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) {
+  constexpr int kstep = BF16 ? 32 : 16;
+  const int ks = a.Cin / kstep;
+  if (!CONV) {
+    if (ks <= 4) return launch_ws<BF16, WS, false, 1, 4>(a, pl, stream);
+    return launch_ws<BF16, WS, false, 1, 8>(a, pl, stream);
+  }
+  if (ks <= 4) return launch_ws<BF16, WS, true, 10, 4>(a, pl, stream);
+  return launch_ws<BF16, WS, true, 10, 8>(a, pl, stream);
+}
+
+}  // namespace
+
+// Plan for the weight-stationary kernel, or false when the shape does not fit.
+bool ws_plan(const GemmArgs& a, bool conv, bool bf16, int num_cus, WsPlan* pl) {
+  const int e = bf16 ? 2 : 4;
+  const int K = conv ? a.K : 1;
+  const int Ktot = K * a.Cin;
+  const int kstep = bf16 ? 32 : 16;
+  if ((a.Cin * e) % 64 != 0) return false;  // whole 64-byte k-steps per slot
+  if (a.Cin / kstep > 8) return false;       // at most 8 k-steps per slot job
+  if (conv && K > 10) return false;          // index build keeps <= 10 slots per row
+  // sparse inputs only: at high density the tiled kernel (gemm.hip) is faster
+  if (conv && (double)a.n_rows > 0.3 * (double)a.B * (double)a.V) return false;
+  int ws = 0;
+  for (int cand : {128, 64, 32}) {
+    if (cand > ((a.Cout + 15) / 16) * 16 && cand != 32) continue;
+    const int wb = ((Ktot * ws_wrow(cand, e) + 15) & ~15);
+    if (wb + ws_scratch(cand, e) + ws_idx_bytes(256, K) <= kLdsLimit) {
+      ws = cand;
+      break;
+    }
+  }
+  if (ws == 0) return false;
+  const int slices = (a.Cout + ws - 1) / ws;
+  const int wb = (Ktot * ws_wrow(ws, e) + 15) & ~15;
+  // rows per workgroup: one workgroup per CU when the rows fit, within LDS
+  int64_t target = (a.n_rows * slices + num_cus - 1) / num_cus;
+  int rows = (int)((target + 15) / 16) * 16;
+  if (rows < 64) rows = 64;
+  if (rows > kMaxRows) rows = kMaxRows;
+  while (rows > 64 && wb + ws_scratch(ws, e) + ws_idx_bytes(rows, K) > kLdsLimit) rows -= 16;
+  if (wb + ws_scratch(ws, e) + ws_idx_bytes(rows, K) > kLdsLimit) return false;
+  pl->ws = ws;
+  pl->wrow = ws_wrow(ws, e);
+  pl->wbytes = wb;
+  pl->rows = rows;
+  pl->idx_bytes = ws_idx_bytes(rows, K);
+  pl->scratch = ws_scratch(ws, e);
+  pl->total = wb + pl->idx_bytes + pl->scratch;
+  return true;
+}
+
+hipError_t launch_ws_gemm(const GemmArgs& a, bool conv, bool bf16, const WsPlan& pl,
+                          hipStream_t stream) {
+#define SHC_WS_CASE(BF, WSV)                                                               \
+  if (pl.ws == WSV)                                                                        \
+    return conv ? launch_ws_k<BF, WSV, true>(a, pl, stream)                                \
+                : launch_ws_k<BF, WSV, false>(a, pl, stream);
+  if (bf16) {
+    SHC_WS_CASE(true, 128) SHC_WS_CASE(true, 64) SHC_WS_CASE(true, 32)
+  } else {
+    SHC_WS_CASE(false, 128) SHC_WS_CASE(false, 64) SHC_WS_CASE(false, 32)
+  }
+#undef SHC_WS_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace shc

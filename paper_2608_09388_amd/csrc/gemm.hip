@@ -582,6 +582,13 @@ hipError_t launch_typed(const GemmArgs& a, hipStream_t stream) {
 
 hipError_t launch_gather_gemm(const GemmArgs& a, bool conv, bool bf16, hipStream_t stream) {
   if (a.n_rows == 0) return hipSuccess;
+  // weight-stationary kernel when a column slice of W fits in LDS
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  WsPlan plan;
+  if (ws_plan(a, conv, bf16, cus, &plan)) return launch_ws_gemm(a, conv, bf16, plan, stream);
   if (bf16) return conv ? launch_typed<true, true>(a, stream) : launch_typed<true, false>(a, stream);
   return conv ? launch_typed<false, true>(a, stream) : launch_typed<false, false>(a, stream);
 }

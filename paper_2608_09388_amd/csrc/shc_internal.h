@@ -73,4 +73,18 @@ struct GemmArgs {
 
 hipError_t launch_gather_gemm(const GemmArgs& a, bool conv, bool bf16, hipStream_t stream);
 
+// weight-stationary variant (conv_ws.hip): LDS plan, all sizes in bytes
+struct WsPlan {
+  int ws;         // output-column slice width held in LDS
+  int wrow;       // padded LDS row of the weight slice
+  int wbytes;     // weight slice
+  int rows;       // active rows per workgroup (multiple of 16)
+  int idx_bytes;  // index lists
+  int scratch;    // epilogue staging (all waves)
+  int total;
+};
+bool ws_plan(const GemmArgs& a, bool conv, bool bf16, int num_cus, WsPlan* plan);
+hipError_t launch_ws_gemm(const GemmArgs& a, bool conv, bool bf16, const WsPlan& plan,
+                          hipStream_t stream);
+
 }  // namespace shc
