@@ -34,7 +34,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_conv_c4_5pct.txt")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_09388_amd", "csrc", "gemm.hip")
+# sources of the conv launch (dispatch and kernel): the counter summary is
+# only used while they are unchanged
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_09388_amd", "csrc", f)
+                  for f in ("gemm.hip", "conv_ws.hip", "shc_internal.h")]
 
 
 def log(msg):
@@ -50,6 +53,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-dense", action="store_true", help="skip the dense-layer comparison")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
+    p.add_argument("--reps", type=int, default=50,
+                   help="back-to-back launches per kernel for the per-kernel times")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="only run a plain device copy of MIB MiB (counter calibration) and exit")
     return p.parse_args()
 
 
@@ -71,6 +78,13 @@ def algorithmic_conv(w, coords, inv, n, e):
     return bytes_, flops, present / (n * K)
 
 
+def kernel_source_digest():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
+
+
 def traffic_from_profile():
     """HBM bytes per conv launch from the committed rocprofv3 counter summary,
     or None if absent or taken on a different version of the kernel source."""
@@ -81,7 +95,7 @@ def traffic_from_profile():
         if ":" in line and not line.lstrip().startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    src = kernel_source_digest()
     if kv.get("kernel_source_sha256") != src or "hbm_bytes_per_launch" not in kv:
         return None
     return float(kv["hbm_bytes_per_launch"])
@@ -108,6 +122,47 @@ def cpu_baseline(w, layers_spec, budget_s):
             "sample": f"{nb} of {w.B} bodies ({n} active rows), full step, {t:.1f} s, fp64 numpy"}
 
 
+def kernel_times(st, shc, torch, reps):
+    """Average duration of each kernel of the path: `reps` launches back to
+    back on the stream the calls use, bracketed by two HIP events there."""
+    stream = torch.cuda.current_stream()
+    n = st.n
+
+    def compact_async():  # compaction without the host count (no sync per call)
+        shc.compact_mask(st.mask, st.B, st.V, st.coords, st.inv, st.row_ptr, st.n_active, st.ws,
+                         want_host_count=False)
+
+    calls = {"compact": compact_async, "gather": st.gather,
+             "linear": lambda: st.layer(0), "conv": lambda: st.layer(1),
+             "scatter": st.scatter, "pool": st.pool}
+    out = {}
+    for name, fn in calls.items():
+        for _ in range(3):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        out[name] = a.elapsed_time(b) / reps
+    st.n = n
+    return out
+
+
+def copy_calibration(torch, mib):
+    """A plain device-to-device copy of `mib` MiB, five times: the reference
+    for scaling the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    n = mib * 1024 * 1024 // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_mib": mib, "copies": 5}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -122,7 +177,9 @@ def main():
     from paper_2608_09388_amd.pipeline import SparseStack
 
     shc.load()
-    dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        copy_calibration(torch, args.copy_calibration)
+        return
     w = synth.workload_c4(args.density)
     st = SparseStack(w, device="cuda:0")
     n = st.compact()
@@ -130,48 +187,40 @@ def main():
     L = len(w.layers)
     stream = torch.cuda.current_stream()
 
-    names = ["compact", "gather", "linear", "conv", "scatter", "pool"]
-
-    def timed_step(ev):
-        ev[0].record(stream)
-        st.compact()
-        ev[1].record(stream)
-        st.gather()
-        ev[2].record(stream)
-        st.layer(0)
-        ev[3].record(stream)
-        st.layer(1)
-        ev[4].record(stream)
-        shc.scatter(st.acts[-1], st.inv, st.coords, st.n, st.B, st.V, st.dense_out, True)
-        ev[5].record(stream)
-        shc.segment_maxpool(st.acts[-1], st.row_ptr, st.n, st.B, st.pooled, 0.0)
-        ev[6].record(stream)
-
     for _ in range(args.warmup):
         st.step()
     torch.cuda.synchronize()
 
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(args.steps)]
+    # timed region: K whole steps; HIP events around the conv launch of each
+    # step, on the stream it runs on
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
-        timed_step(events[s])
+        st.compact()
+        st.gather()
+        st.layer(0)
+        ev[s][0].record(stream)
+        st.layer(1)
+        ev[s][1].record(stream)
+        st.finish()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_kernel_ms = {}
-    for k, name in enumerate(names):
-        per_kernel_ms[name] = float(np.mean([events[s][k].elapsed_time(events[s][k + 1])
-                                             for s in range(args.steps)]))
     ms_per_step = wall * 1e3 / args.steps
+    conv_in_step_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     log(f"timed {args.steps} steps: {ms_per_step:.4f} ms/step")
     value = n * L / (ms_per_step / 1e3)
+
+    per_kernel_ms = kernel_times(st, shc, torch, args.reps)
+    log("per-kernel times done")
 
     # roofline of the dominant kernel (the conv layer)
     coords = st.coords[:n].cpu().numpy()
     inv = st.inv.cpu().numpy()
     e = 2
     cbytes, cflops, a_present = algorithmic_conv(w, coords, inv, n, e)
-    conv_s = per_kernel_ms["conv"] / 1e3
+    conv_s = conv_in_step_ms / 1e3
     ridge = BF16_MFMA_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
     traffic = traffic_from_profile()
     if cflops / cbytes < ridge:
@@ -183,12 +232,13 @@ def main():
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(ach / BF16_MFMA_PEAK_TFLOPS, 4),
                 "traffic": traffic}
-    roof["kernel"] = "sparse_neighbor_conv (gather_gemm_kernel<bf16,128,conv>)"
+    roof["kernel"] = "shc_sparse_neighbor_conv (ws_kernel: weight slice resident in LDS)"
     roof["algorithmic_bytes"] = int(cbytes)
     roof["useful_flops"] = cflops
     roof["executed_slot_gemm_flops"] = 2.0 * n * 9 * 128 * 128
     roof["present_slot_fraction"] = round(a_present, 4)
-    roof["launch_us"] = round(per_kernel_ms["conv"] * 1e3, 2)
+    roof["launch_us"] = round(conv_in_step_ms * 1e3, 2)
+    roof["launch_us_back_to_back"] = round(per_kernel_ms["conv"] * 1e3, 2)
 
     out = {
         "metric": "active-vertex rows/sec per sparse contact layer; speed-up vs dense layer",

@@ -91,6 +91,10 @@ size_t shc_compact_mask_workspace(int32_t B, int32_t V);
  *   n_active_dev  [1] int32 out: N'.
  *   n_active_host host int64*, may be NULL.  When set, the call waits for the
  *             stream, stores N' there and returns SHC_ERR_CAPACITY if N' > cap.
+ *             If it lies in page-locked host memory mapped into the device
+ *             (hipHostMalloc), the kernel stores the count there itself and
+ *             the call only waits; pageable memory costs one extra
+ *             device-to-host copy.
  *   cap       rows available in `coords` (>= 0).
  *   ws, ws_bytes  device workspace of at least shc_compact_mask_workspace(B, V)
  *             bytes; its contents on entry do not matter.

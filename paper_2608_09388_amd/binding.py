@@ -129,10 +129,22 @@ def compact_mask_workspace(B: int, V: int) -> int:
     return int(load().shc_compact_mask_workspace(B, V))
 
 
+def _host_count_ptr(host_count: Optional[torch.Tensor]) -> int:
+    if not isinstance(host_count, torch.Tensor) or host_count.is_cuda or \
+            host_count.dtype != torch.int64 or host_count.numel() < 1:
+        raise ValueError("host_count must be a CPU int64 tensor of at least one element")
+    return host_count.data_ptr()
+
+
 def compact_mask(mask: torch.Tensor, B: int, V: int, coords: torch.Tensor, inv: torch.Tensor,
                  row_ptr: torch.Tensor, n_active: torch.Tensor, ws: torch.Tensor,
-                 want_host_count: bool = True, stream=None) -> Optional[int]:
-    """shc_compact_mask.  ``coords`` is int32 [cap][2]; returns N' if asked (syncs)."""
+                 want_host_count: bool = True, stream=None,
+                 host_count: Optional[torch.Tensor] = None) -> Optional[int]:
+    """shc_compact_mask.  ``coords`` is int32 [cap][2]; returns N' if asked (syncs).
+
+    ``host_count`` (optional) is a CPU int64 tensor that receives N'; when it
+    is pinned (``pin_memory=True``) the kernel writes it directly.
+    """
     lib = load()
     cap = coords.numel() // 2
     args = [_dev(mask, "mask", torch.uint8, B * V), B, V,
@@ -140,9 +152,14 @@ def compact_mask(mask: torch.Tensor, B: int, V: int, coords: torch.Tensor, inv: 
             _dev(inv, "inv", torch.int32, B * V), _dev(row_ptr, "row_ptr", torch.int32, B + 1),
             _dev(n_active, "n_active", torch.int32, 1)]
     host = ctypes.c_int64(-1)
-    args += [ctypes.addressof(host) if want_host_count else None, cap,
-             _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)]
+    if host_count is not None:
+        hp = _host_count_ptr(host_count)
+    else:
+        hp = ctypes.addressof(host) if want_host_count else None
+    args += [hp, cap, _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)]
     _check(lib.shc_compact_mask(*args), "shc_compact_mask")
+    if host_count is not None:
+        return int(host_count[0])
     return int(host.value) if want_host_count else None
 
 
@@ -204,3 +221,105 @@ def segment_maxpool(S: torch.Tensor, row_ptr: torch.Tensor, n_rows: int, B: int,
             _dev(row_ptr, "row_ptr", torch.int32, B + 1), n_rows, B, C, dt, float(empty_value),
             _dev(P, "P", P.dtype, B * C), _stream(stream)]
     _check(load().shc_segment_maxpool(*args), "shc_segment_maxpool")
+
+
+# ----------------------------------------------------------------------------
+# prepared calls: every argument marshalled and checked once, against the
+# capacity of the buffers; a call then only substitutes the row count
+# ----------------------------------------------------------------------------
+
+
+class Prepared:
+    """One library call with its arguments resolved up front.
+
+    The tensors are checked once, at their full size, so any row count up to
+    ``n_max`` is valid; ``__call__(n_rows)`` enqueues the call on the stream
+    captured at preparation.  The tensors are kept alive by this object.
+    """
+
+    __slots__ = ("_fn", "_args", "_n_at", "n_max", "_where", "_keep")
+
+    def __init__(self, where: str, args, n_at: Optional[int], n_max: int, keep):
+        self._fn = getattr(load(), where)
+        self._args = list(args)
+        self._n_at = n_at
+        self.n_max = int(n_max)
+        self._where = where
+        self._keep = keep
+
+    def __call__(self, n_rows: int = 0) -> int:
+        if self._n_at is not None:
+            if not 0 <= n_rows <= self.n_max:
+                raise ValueError(f"{self._where}: n_rows = {n_rows} outside [0, {self.n_max}]")
+            self._args[self._n_at] = n_rows
+        rc = self._fn(*self._args)
+        if rc != 0:
+            _check(rc, self._where)
+        return rc
+
+
+class PreparedCompact:
+    """shc_compact_mask with a pinned host count; calling it returns N'."""
+
+    def __init__(self, mask, B, V, coords, inv, row_ptr, n_active, ws, stream=None):
+        self.host = torch.zeros(1, dtype=torch.int64, pin_memory=True)
+        self._host_view = self.host.numpy()
+        cap = coords.numel() // 2
+        args = [_dev(mask, "mask", torch.uint8, B * V), B, V,
+                _dev(coords, "coords", torch.int32) if cap > 0 else None,
+                _dev(inv, "inv", torch.int32, B * V),
+                _dev(row_ptr, "row_ptr", torch.int32, B + 1),
+                _dev(n_active, "n_active", torch.int32, 1), self.host.data_ptr(), cap,
+                _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)]
+        self._call = Prepared("shc_compact_mask", args, None, 0,
+                              (mask, coords, inv, row_ptr, n_active, ws, self.host))
+
+    def __call__(self) -> int:
+        self._call()
+        return int(self._host_view[0])
+
+
+def prepare_gather_rows(x, coords, B, V, S, stream=None) -> Prepared:
+    C = x.shape[-1]
+    n_max = min(coords.numel() // 2, S.numel() // C)
+    args = [_dev(x, "x", x.dtype, B * V * C), _dev(coords, "coords", torch.int32), 0, B, V, C,
+            _dtype_code(x), _dev(S, "S", x.dtype), _stream(stream)]
+    return Prepared("shc_gather_rows", args, 2, n_max, (x, coords, S))
+
+
+def prepare_sparse_linear(S, W, bias, out, act=SHC_ACT_RELU, stream=None) -> Prepared:
+    Cin, Cout = W.shape
+    n_max = min(S.numel() // Cin, out.numel() // Cout)
+    args = [_dev(S, "S", S.dtype), 0, _dev(W, "W", S.dtype, Cin * Cout),
+            _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, _dtype_code(S), act,
+            _dev(out, "out", S.dtype), _stream(stream)]
+    return Prepared("shc_sparse_linear", args, 1, n_max, (S, W, bias, out))
+
+
+def prepare_sparse_neighbor_conv(S, coords, inv, B, V, nbr, W, bias, out, act=SHC_ACT_RELU,
+                                 stream=None) -> Prepared:
+    K, Cin, Cout = W.shape
+    n_max = min(S.numel() // Cin, coords.numel() // 2, out.numel() // Cout)
+    args = [_dev(S, "S", S.dtype), _dev(coords, "coords", torch.int32),
+            _dev(inv, "inv", torch.int32, B * V), 0, B, V,
+            _dev(nbr, "nbr", torch.int32, V * K), K, _dev(W, "W", S.dtype, K * Cin * Cout),
+            _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, _dtype_code(S), act,
+            _dev(out, "out", S.dtype), _stream(stream)]
+    return Prepared("shc_sparse_neighbor_conv", args, 3, n_max, (S, coords, inv, nbr, W, bias, out))
+
+
+def prepare_scatter(S, inv, coords, B, V, D, zero_fill=True, stream=None) -> Prepared:
+    C = D.shape[-1]
+    n_max = S.numel() // C if zero_fill else min(S.numel() // C, coords.numel() // 2)
+    args = [_dev(S, "S", D.dtype), _dev(inv, "inv", torch.int32, B * V) if zero_fill else None,
+            None if zero_fill else _dev(coords, "coords", torch.int32), 0, B, V, C,
+            _dtype_code(D), 1 if zero_fill else 0, _dev(D, "D", D.dtype, B * V * C),
+            _stream(stream)]
+    return Prepared("shc_scatter", args, 3, n_max, (S, inv, coords, D))
+
+
+def prepare_segment_maxpool(S, row_ptr, B, P, empty_value=0.0, stream=None) -> Prepared:
+    C = P.shape[-1]
+    args = [_dev(S, "S", P.dtype), _dev(row_ptr, "row_ptr", torch.int32, B + 1), 0, B, C,
+            _dtype_code(P), float(empty_value), _dev(P, "P", P.dtype, B * C), _stream(stream)]
+    return Prepared("shc_segment_maxpool", args, 2, S.numel() // C, (S, row_ptr, P))

@@ -102,6 +102,18 @@ size_t shc_compact_mask_workspace(int32_t B, int32_t V) {
   return (((size_t)nblocks * sizeof(int32_t)) + 255u) & ~(size_t)255u;
 }
 
+// Device address of a caller's host variable when it lies in page-locked
+// memory mapped into the device's address space, else null (pageable memory).
+static int64_t* mapped_host_count(int64_t* host) {
+  hipPointerAttribute_t attr;
+  if (hipPointerGetAttributes(&attr, host) != hipSuccess) {
+    (void)hipGetLastError();  // pageable memory: clear the lookup's error
+    return nullptr;
+  }
+  if (attr.type != hipMemoryTypeHost || attr.devicePointer == nullptr) return nullptr;
+  return static_cast<int64_t*>(attr.devicePointer);
+}
+
 int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
                      int32_t* row_ptr, int32_t* n_active_dev, int64_t* n_active_host, int64_t cap,
                      void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -117,19 +129,30 @@ int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
   const size_t need = shc_compact_mask_workspace(B, V);
   if (ws_bytes < need)
     return fail(SHC_ERR_CAPACITY, "workspace of %zu bytes is below the %zu needed", ws_bytes, need);
-  int rc = hip_status(shc::launch_compact(mask, B, V, coords, inv, row_ptr, n_active_dev, cap,
-                                          static_cast<int32_t*>(ws), stream),
+  int64_t* mapped = n_active_host ? mapped_host_count(n_active_host) : nullptr;
+  int rc = hip_status(shc::launch_compact(mask, B, V, coords, inv, row_ptr, n_active_dev, mapped,
+                                          cap, static_cast<int32_t*>(ws), stream),
                       "compact_mask launch");
   if (rc != SHC_OK || n_active_host == nullptr) return rc;
-  int32_t n = 0;
-  rc = hip_status(hipMemcpyAsync(&n, n_active_dev, sizeof(int32_t), hipMemcpyDeviceToHost, stream),
-                  "compact_mask count copy");
-  if (rc != SHC_OK) return rc;
-  rc = hip_status(hipStreamSynchronize(stream), "compact_mask stream sync");
-  if (rc != SHC_OK) return rc;
+  int64_t n = 0;
+  if (mapped == nullptr) {
+    int32_t n32 = 0;
+    rc = hip_status(
+        hipMemcpyAsync(&n32, n_active_dev, sizeof(int32_t), hipMemcpyDeviceToHost, stream),
+        "compact_mask count copy");
+    if (rc != SHC_OK) return rc;
+    rc = hip_status(hipStreamSynchronize(stream), "compact_mask stream sync");
+    if (rc != SHC_OK) return rc;
+    n = n32;
+  } else {
+    rc = hip_status(hipStreamSynchronize(stream), "compact_mask stream sync");
+    if (rc != SHC_OK) return rc;
+    n = *static_cast<volatile int64_t*>(n_active_host);
+  }
   *n_active_host = n;
   if (n > cap)
-    return fail(SHC_ERR_CAPACITY, "N' = %d active rows exceed cap = %lld", n, (long long)cap);
+    return fail(SHC_ERR_CAPACITY, "N' = %lld active rows exceed cap = %lld", (long long)n,
+                (long long)cap);
   return SHC_OK;
 }
 

@@ -89,7 +89,7 @@ __global__ __launch_bounds__(kThreads) void compact_count_kernel(const uint8_t* 
 __global__ __launch_bounds__(kThreads) void compact_write_kernel(
     const uint8_t* __restrict__ mask, int64_t total, int64_t per_block, int32_t B, int32_t V,
     const int32_t* __restrict__ counts, int32_t* __restrict__ coords, int32_t* __restrict__ inv,
-    int32_t* __restrict__ row_ptr, int32_t* __restrict__ n_active, int64_t cap) {
+    int32_t* __restrict__ row_ptr, int32_t* __restrict__ n_active, int64_t* n_host, int64_t cap) {
   __shared__ uint32_t red[kWaves];
   __shared__ uint32_t wave_tot[2][kWaves];
   const int tid = threadIdx.x;
@@ -174,6 +174,9 @@ __global__ __launch_bounds__(kThreads) void compact_write_kernel(
   if (blockIdx.x == gridDim.x - 1 && tid == 0) {
     row_ptr[B] = (int32_t)base;
     *n_active = (int32_t)base;
+    // page-locked host copy of the count: a system-scope store reaches host
+    // memory before the kernel's completion is signalled
+    if (n_host != nullptr) __hip_atomic_store(n_host, base, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
 }
 
@@ -190,8 +193,8 @@ void compact_plan(int64_t total, int32_t* nblocks, int64_t* per_block) {
 }
 
 hipError_t launch_compact(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
-                          int32_t* row_ptr, int32_t* n_active, int64_t cap, int32_t* block_counts,
-                          hipStream_t stream) {
+                          int32_t* row_ptr, int32_t* n_active, int64_t* n_host, int64_t cap,
+                          int32_t* block_counts, hipStream_t stream) {
   const int64_t total = (int64_t)B * V;
   int32_t nblocks;
   int64_t per_block;
@@ -201,7 +204,7 @@ hipError_t launch_compact(const uint8_t* mask, int32_t B, int32_t V, int32_t* co
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   hipLaunchKernelGGL(compact_write_kernel, dim3(nblocks), dim3(kThreads), 0, stream, mask, total,
-                     per_block, B, V, block_counts, coords, inv, row_ptr, n_active, cap);
+                     per_block, B, V, block_counts, coords, inv, row_ptr, n_active, n_host, cap);
   return hipGetLastError();
 }
 

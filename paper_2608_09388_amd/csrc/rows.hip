@@ -27,20 +27,37 @@ RowShape row_shape(int32_t row_bytes) {
   return s;
 }
 
+// Each thread moves vector q of kGatherRows rows (ty apart), issuing every
+// coordinate load, then every row load, before the first store, so each
+// thread keeps kGatherRows 16-byte loads in flight.  Rows past n_rows clamp to
+// the last row (loaded, never stored); a coordinate outside [0,B)x[0,V)
+// reads row 0 and stores zeros.
+constexpr int kGatherRows = 4;
+
 __global__ __launch_bounds__(kThreads) void gather_kernel(const i32x4* __restrict__ x,
                                                           const int2* __restrict__ coords,
                                                           int64_t n_rows, int32_t B, int32_t V,
                                                           int vpr, i32x4* __restrict__ S) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.y + threadIdx.y;
-  if (i >= n_rows) return;
-  const int2 c = coords[i];
-  const bool ok = c.x >= 0 && c.x < B && c.y >= 0 && c.y < V;
-  const i32x4* src = x + ((int64_t)c.x * V + c.y) * vpr;
-  i32x4* dst = S + i * vpr;
+  const int ty = blockDim.y;
+  const int64_t i0 = (int64_t)blockIdx.x * kGatherRows * ty + threadIdx.y;
+  int64_t src[kGatherRows];
+  bool ok[kGatherRows];
+#pragma unroll
+  for (int k = 0; k < kGatherRows; ++k) {
+    const int64_t i = min(i0 + (int64_t)k * ty, n_rows - 1);
+    const int2 c = coords[i];
+    ok[k] = c.x >= 0 && c.x < B && c.y >= 0 && c.y < V;
+    src[k] = ok[k] ? ((int64_t)c.x * V + c.y) * vpr : 0;
+  }
   for (int q = threadIdx.x; q < vpr; q += blockDim.x) {
-    i32x4 val = {0, 0, 0, 0};
-    if (ok) val = __builtin_nontemporal_load(src + q);
-    dst[q] = val;
+    i32x4 val[kGatherRows];
+#pragma unroll
+    for (int k = 0; k < kGatherRows; ++k) val[k] = __builtin_nontemporal_load(x + src[k] + q);
+#pragma unroll
+    for (int k = 0; k < kGatherRows; ++k) {
+      const int64_t i = i0 + (int64_t)k * ty;
+      if (i < n_rows) S[i * vpr + q] = ok[k] ? val[k] : i32x4{0, 0, 0, 0};
+    }
   }
 }
 
@@ -118,37 +135,55 @@ struct PoolVec<true> {  // 8 bf16 channels
   }
 };
 
+// One block of kPoolThreads threads per segment: tx threads span a row, ty
+// row slots; each thread folds kPoolRows rows per batch, all loaded before the
+// first maximum.  A row index past the segment clamps to its last row:
+// repeating a row leaves a maximum unchanged, so no select is needed.
+constexpr int kPoolThreads = 1024;
+constexpr int kPoolRows = 8;
+
 template <bool BF16>
-__global__ __launch_bounds__(kThreads) void segment_max_kernel(const i32x4* __restrict__ S,
-                                                               const int32_t* __restrict__ row_ptr,
-                                                               int64_t n_rows, int vpr,
-                                                               float empty_value,
-                                                               i32x4* __restrict__ P) {
+__global__ __launch_bounds__(kPoolThreads) void segment_max_kernel(
+    const i32x4* __restrict__ S, const int32_t* __restrict__ row_ptr, int64_t n_rows, int vpr,
+    float empty_value, i32x4* __restrict__ P) {
   using PV = PoolVec<BF16>;
   extern __shared__ float part[];  // [ty][tx][N]
   const int b = blockIdx.x;
   int64_t lo = row_ptr[b], hi = row_ptr[b + 1];
   lo = lo < 0 ? 0 : (lo > n_rows ? n_rows : lo);
   hi = hi < lo ? lo : (hi > n_rows ? n_rows : hi);
-  const int tx = blockDim.x, ty = blockDim.y;
+  const int tx = blockDim.x, ty = blockDim.y, y = threadIdx.y;
   const float nanv = __builtin_nanf("");
   for (int q0 = 0; q0 < vpr; q0 += tx) {
-    const int q = q0 + threadIdx.x;
+    const int q = min(q0 + (int)threadIdx.x, vpr - 1);
     float m[PV::N];
     for (int k = 0; k < PV::N; ++k) m[k] = nanv;
-    if (q < vpr) {
-      for (int64_t i = lo + threadIdx.y; i < hi; i += ty) {
+    for (int64_t i0 = lo + y; i0 < hi; i0 += (int64_t)kPoolRows * ty) {
+      i32x4 v[kPoolRows];
+#pragma unroll
+      for (int r = 0; r < kPoolRows; ++r) v[r] = S[min(i0 + (int64_t)r * ty, hi - 1) * vpr + q];
+#pragma unroll
+      for (int r = 0; r < kPoolRows; ++r) {
         float f[PV::N];
-        PV::widen(S[i * vpr + q], f);
+        PV::widen(v[r], f);
         for (int k = 0; k < PV::N; ++k) m[k] = fmaxf(m[k], f[k]);
       }
     }
-    float* mine = part + ((size_t)threadIdx.y * tx + threadIdx.x) * PV::N;
+    // fold the ty partial maxima: slots y >= 8 into y % 8, then 1..7 into 0
+    float* mine = part + ((size_t)y * tx + threadIdx.x) * PV::N;
     for (int k = 0; k < PV::N; ++k) mine[k] = m[k];
     __syncthreads();
-    if (threadIdx.y == 0 && q < vpr) {
-      for (int y = 1; y < ty; ++y) {
-        const float* o = part + ((size_t)y * tx + threadIdx.x) * PV::N;
+    if (y < 8) {
+      for (int yy = y + 8; yy < ty; yy += 8) {
+        const float* o = part + ((size_t)yy * tx + threadIdx.x) * PV::N;
+        for (int k = 0; k < PV::N; ++k) m[k] = fmaxf(m[k], o[k]);
+      }
+      for (int k = 0; k < PV::N; ++k) mine[k] = m[k];
+    }
+    __syncthreads();
+    if (y == 0 && q0 + (int)threadIdx.x < vpr) {
+      for (int yy = 1; yy < 8 && yy < ty; ++yy) {
+        const float* o = part + ((size_t)yy * tx + threadIdx.x) * PV::N;
         for (int k = 0; k < PV::N; ++k) m[k] = fmaxf(m[k], o[k]);
       }
       if (hi == lo)
@@ -163,8 +198,10 @@ __global__ __launch_bounds__(kThreads) void segment_max_kernel(const i32x4* __re
 
 hipError_t launch_gather(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
                          int32_t V, int32_t row_bytes, void* S, hipStream_t stream) {
+  if (n_rows <= 0) return hipSuccess;
   const RowShape s = row_shape(row_bytes);
-  const int64_t blocks = (n_rows + s.ty - 1) / s.ty;
+  const int64_t per_block = (int64_t)s.ty * kGatherRows;
+  const int64_t blocks = (n_rows + per_block - 1) / per_block;
   hipLaunchKernelGGL(gather_kernel, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0, stream,
                      static_cast<const i32x4*>(x), reinterpret_cast<const int2*>(coords), n_rows,
                      B, V, s.vpr, static_cast<i32x4*>(S));
@@ -196,7 +233,8 @@ hipError_t launch_segment_max(const void* S, const int32_t* row_ptr, int64_t n_r
                               int32_t C, int is_bf16, float empty_value, void* P,
                               hipStream_t stream) {
   const int32_t row_bytes = C * (is_bf16 ? 2 : 4);
-  const RowShape s = row_shape(row_bytes);
+  RowShape s = row_shape(row_bytes);
+  s.ty = kPoolThreads / s.tx;
   const int n_per_vec = is_bf16 ? 8 : 4;
   const size_t lds = (size_t)s.tx * s.ty * n_per_vec * sizeof(float);
   if (is_bf16)

@@ -43,8 +43,8 @@ __device__ __forceinline__ T ceil_div(T a, T b) {
 void compact_plan(int64_t total, int32_t* nblocks, int64_t* per_block);
 
 hipError_t launch_compact(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
-                          int32_t* row_ptr, int32_t* n_active, int64_t cap, int32_t* block_counts,
-                          hipStream_t stream);
+                          int32_t* row_ptr, int32_t* n_active, int64_t* n_host, int64_t cap,
+                          int32_t* block_counts, hipStream_t stream);
 
 hipError_t launch_gather(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
                          int32_t V, int32_t row_bytes, void* S, hipStream_t stream);

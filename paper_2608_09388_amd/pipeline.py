@@ -61,43 +61,59 @@ class SparseStack:
         self.dense_out = torch.empty((BV, Cl), dtype=self.dtype, device=dev) if w.scatter else None
         self.pooled = torch.empty((self.B, Cl), dtype=self.dtype, device=dev) if w.pool else None
         self.n = None
+        # every call of the path marshalled once, on the current stream; the
+        # buffers are at full capacity, so each call only takes the row count
+        B, V = self.B, self.V
+        self._compact = shc.PreparedCompact(self.mask, B, V, self.coords, self.inv, self.row_ptr,
+                                            self.n_active, self.ws)
+        self._gather = shc.prepare_gather_rows(self.x, self.coords, B, V, self.acts[0])
+        self._layers = []
+        for l, spec in enumerate(w.layers):
+            src, dst = self.acts[l], self.acts[l + 1]
+            a = act if spec.relu else shc.SHC_ACT_NONE
+            if spec.kind == "conv":
+                call = shc.prepare_sparse_neighbor_conv(src, self.coords, self.inv, B, V, self.nbr,
+                                                        self.weights[l], self.biases[l], dst, a)
+            else:
+                call = shc.prepare_sparse_linear(src, self.weights[l], self.biases[l], dst, a)
+            self._layers.append(call)
+        last = self.acts[-1]
+        self._scatter = (shc.prepare_scatter(last, self.inv, self.coords, B, V, self.dense_out)
+                         if self.dense_out is not None else None)
+        self._pool = (shc.prepare_segment_maxpool(last, self.row_ptr, B, self.pooled, 0.0)
+                      if self.pooled is not None else None)
 
     # -- individual steps -----------------------------------------------------
-    def compact(self, stream=None) -> int:
-        self.n = shc.compact_mask(self.mask, self.B, self.V, self.coords, self.inv, self.row_ptr,
-                                  self.n_active, self.ws, want_host_count=True, stream=stream)
+    def compact(self) -> int:
+        """Compaction; waits for the active count (one host sync per mask)."""
+        self.n = self._compact()
         return self.n
 
-    def gather(self, stream=None):
-        shc.gather_rows(self.x, self.coords, self.n, self.B, self.V, self.acts[0], stream=stream)
+    def gather(self):
+        self._gather(self.n)
 
-    def layer(self, l: int, stream=None):
-        spec = self.w.layers[l]
-        src, dst = self.acts[l], self.acts[l + 1]
-        act = self.act if spec.relu else shc.SHC_ACT_NONE
-        if spec.kind == "conv":
-            shc.sparse_neighbor_conv(src, self.coords, self.inv, self.n, self.B, self.V, self.nbr,
-                                     self.weights[l], self.biases[l], dst, act, stream=stream)
-        else:
-            shc.sparse_linear(src, self.n, self.weights[l], self.biases[l], dst, act,
-                              stream=stream)
+    def layer(self, l: int):
+        self._layers[l](self.n)
 
-    def finish(self, stream=None):
-        last = self.acts[-1]
-        if self.dense_out is not None:
-            shc.scatter(last, self.inv, self.coords, self.n, self.B, self.V, self.dense_out,
-                        zero_fill=True, stream=stream)
-        if self.pooled is not None:
-            shc.segment_maxpool(last, self.row_ptr, self.n, self.B, self.pooled, 0.0,
-                                stream=stream)
+    def scatter(self):
+        self._scatter(self.n)
 
-    def step(self, stream=None) -> int:
+    def pool(self):
+        self._pool(self.n)
+
+    def finish(self):
+        if self._scatter is not None:
+            self._scatter(self.n)
+        if self._pool is not None:
+            self._pool(self.n)
+
+    def step(self) -> int:
         """One pass of the whole path over the workload's batch."""
-        self.compact(stream)
-        self.gather(stream)
-        for l in range(len(self.w.layers)):
-            self.layer(l, stream)
-        self.finish(stream)
+        self.compact()
+        self.gather()
+        for call in self._layers:
+            call(self.n)
+        self.finish()
         return self.n
 
     # -- results on the host --------------------------------------------------

@@ -77,6 +77,41 @@ def test_compact_shapes(dev, B, V, p):
     check_compaction(m)
 
 
+@pytest.mark.parametrize("pinned", [True, False])
+def test_compact_host_count_tensor(dev, pinned):
+    """The count lands in a caller's host tensor: written by the kernel itself
+    when the tensor is page-locked, copied back when it is pageable; a second
+    mask with fewer rows overwrites the first count."""
+    rng = np.random.default_rng(91)
+    for B, V, p in [(16, 10475, 0.05), (3, 655, 0.01)]:
+        m = (rng.random((B, V)) < p).astype(np.uint8)
+        ref_c, ref_inv, ref_rp, ref_n = O.compact(m)
+        c = Compaction(m)
+        hc = torch.full((1,), -1, dtype=torch.int64, pin_memory=pinned)
+        n = shc.compact_mask(c.mask, B, V, c.coords, c.inv, c.row_ptr, c.n_dev, c.ws,
+                             host_count=hc)
+        assert n == ref_n and int(hc[0]) == ref_n
+        assert np.array_equal(down(c.inv), ref_inv)
+        assert np.array_equal(down(c.coords)[:ref_n], ref_c)
+
+
+def test_compact_prepared_pinned(dev):
+    """The prepared compaction (pinned count, as the pipeline runs it) over
+    three masks in a row of decreasing size."""
+    rng = np.random.default_rng(92)
+    B, V = 32, 10475
+    c = Compaction(np.zeros((B, V), np.uint8))
+    call = shc.PreparedCompact(c.mask, B, V, c.coords, c.inv, c.row_ptr, c.n_dev, c.ws)
+    for p in (0.2, 0.05, 0.0):
+        m = (rng.random((B, V)) < p).astype(np.uint8)
+        c.mask.copy_(up(m.reshape(-1)))
+        ref_c, ref_inv, ref_rp, ref_n = O.compact(m)
+        assert call() == ref_n
+        assert np.array_equal(down(c.inv), ref_inv)
+        assert np.array_equal(down(c.row_ptr), ref_rp)
+        assert np.array_equal(down(c.coords)[:ref_n], ref_c)
+
+
 def test_compact_paper_workload_masks(dev):
     for w in (synth.workload_c1(), synth.workload_c2(), synth.workload_c5()):
         check_compaction(w.mask)
@@ -139,12 +174,15 @@ def test_gather_scatter_exact(dev, dtype, C):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("C", [16, 128, 256])
-def test_segment_maxpool_exact(dev, dtype, C):
+@pytest.mark.parametrize("C,B,V", [(16, 70, 3000), (48, 70, 3000), (128, 70, 3000),
+                                   (256, 70, 3000), (2048, 9, 700), (4096, 9, 700)])
+def test_segment_maxpool_exact(dev, dtype, C, B, V):
+    """Empty, short and long segments (body 5 is full: several batches of rows
+    per thread), row widths that do and do not fill a wavefront, and rows
+    wider than one block's threads."""
     rng = np.random.default_rng(100 + C)
-    B, V = 70, 300
     m = (rng.random((B, V)) < 0.05).astype(np.uint8)
-    m[[0, 13, 69]] = 0                       # empty bodies, first and last included
+    m[[0, B // 2 + 1, B - 1]] = 0             # empty bodies, first and last included
     m[5] = 1                                 # a full body
     c = Compaction(m)
     n = c.run()
