@@ -3,8 +3,9 @@
 
 One step = one pass of the whole path over one batch of synthetic input:
 
-    mask compaction -> gather of the active rows -> sparse linear + ReLU ->
-    sparse 9-slot neighbourhood conv + ReLU -> zero-fill scatter + per-body max-pool
+    mask compaction (+ neighbour-row table of the active set) -> gather of the
+    active rows -> sparse linear + ReLU -> sparse 9-slot neighbourhood conv +
+    ReLU -> zero-fill scatter + per-body max-pool
 
 on the density-sweep workload at 5% density: B = 128 bodies, V = 10475 mesh
 vertices (ellipsoid, exact 9-NN), C = 128 bf16 channels, i.i.d. Bernoulli(0.05)
@@ -70,8 +71,7 @@ def algorithmic_conv(w, coords, inv, n, e):
         u = w.nbr[v, j].astype(np.int64)
         present += int(np.count_nonzero((u >= 0) & (inv[b * w.V + np.maximum(u, 0)] >= 0)))
     bytes_ = (present * Cin * e        # present neighbour rows read
-              + n * 8 * K              # nbr + inv lookups per slot
-              + n * 8                  # coords
+              + n * 4 * K              # neighbour-row table entries
               + n * Cout * e           # output rows
               + K * Cin * Cout * e)    # weights once
     flops = 2.0 * present * Cin * Cout
@@ -124,19 +124,20 @@ def cpu_baseline(w, layers_spec, budget_s):
 
 def kernel_times(st, shc, torch, reps):
     """Average duration of each kernel of the path: `reps` launches back to
-    back on the stream the calls use, bracketed by two HIP events there."""
-    stream = torch.cuda.current_stream()
+    back on the stream each call uses, bracketed by two HIP events there."""
+    main = torch.cuda.current_stream()
     n = st.n
 
     def compact_async():  # compaction without the host count (no sync per call)
         shc.compact_mask(st.mask, st.B, st.V, st.coords, st.inv, st.row_ptr, st.n_active, st.ws,
                          want_host_count=False)
 
-    calls = {"compact": compact_async, "gather": st.gather,
-             "linear": lambda: st.layer(0), "conv": lambda: st.layer(1),
-             "scatter": st.scatter, "pool": st.pool}
+    calls = {"compact": (compact_async, main), "table": (lambda: st._table(n), main),
+             "gather": (st.gather, main), "linear": (lambda: st.layer(0), main),
+             "conv": (lambda: st.layer(1), main), "scatter": (st.scatter, main),
+             "pool": (st.pool, main)}
     out = {}
-    for name, fn in calls.items():
+    for name, (fn, stream) in calls.items():
         for _ in range(3):
             fn()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -232,7 +233,8 @@ def main():
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(ach / BF16_MFMA_PEAK_TFLOPS, 4),
                 "traffic": traffic}
-    roof["kernel"] = "shc_sparse_neighbor_conv (ws_kernel: weight slice resident in LDS)"
+    roof["kernel"] = ("shc_sparse_neighbor_conv_table (ws_kernel: weight slice resident in "
+                      "LDS, index sets from the neighbour-row table)")
     roof["algorithmic_bytes"] = int(cbytes)
     roof["useful_flops"] = cflops
     roof["executed_slot_gemm_flops"] = 2.0 * n * 9 * 128 * 128

@@ -152,6 +152,41 @@ int shc_sparse_neighbor_conv(const void* S, const int32_t* coords, const int32_t
                              int32_t dtype, int32_t act, void* out, hipStream_t stream);
 
 /*
+ * Neighbour-row table of an active set -- the index sets of Eqs. 4-5 in
+ * compact row numbers, built once per mask:
+ *
+ *   table[j * n_rows + i] = r_ij = inv[b_i * V + nbr[v_i * K + j]], or -1
+ *
+ * for every active row i < n_rows and slot j < K (slot-major: row stride
+ * n_rows).  The active set is the same for every layer (C' = C), so every
+ * convolution over this mask can read the table instead of rebuilding it.
+ *
+ *   coords, inv  from shc_compact_mask (n_rows = N').
+ *   nbr     [V][K] as for shc_sparse_neighbor_conv; entries outside [0, V)
+ *           and inactive neighbours give -1.
+ *   table   [K][n_rows] int32 out, device memory owned by the caller.
+ * n_rows = 0 is a no-op.  Results are exact and deterministic.
+ */
+int shc_build_neighbor_table(const int32_t* coords, const int32_t* inv, int64_t n_rows,
+                             int32_t B, int32_t V, const int32_t* nbr, int32_t K, int32_t* table,
+                             hipStream_t stream);
+
+/*
+ * Sparse neighbourhood convolution reading its index sets from a table built
+ * by shc_build_neighbor_table for the same active set (same n_rows, K):
+ *
+ *   out[i] = act( bias + sum_{j<K} S[table[j * n_rows + i]] W[j] ),
+ *
+ * a slot whose entry is outside [0, n_rows) adding nothing.  Same result as
+ * shc_sparse_neighbor_conv on the mask the table came from; arguments as
+ * there, with `table` in place of coords / inv / nbr / B / V.
+ */
+int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t n_rows,
+                                   int32_t K, const void* W, const float* bias, int32_t Cin,
+                                   int32_t Cout, int32_t dtype, int32_t act, void* out,
+                                   hipStream_t stream);
+
+/*
  * Scatter back to the dense per-vertex layout (C' = C, so row i returns to
  * (b_i, v_i)):
  *

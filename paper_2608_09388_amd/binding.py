@@ -49,6 +49,11 @@ _SIGS = {
     "shc_sparse_neighbor_conv": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32,
                                                 _c_ptr, _c_i32, _c_ptr, _c_ptr, _c_i32, _c_i32,
                                                 _c_i32, _c_i32, _c_ptr, _c_ptr]),
+    "shc_build_neighbor_table": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_ptr,
+                                                _c_i32, _c_ptr, _c_ptr]),
+    "shc_sparse_neighbor_conv_table": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_ptr,
+                                                      _c_ptr, _c_i32, _c_i32, _c_i32, _c_i32,
+                                                      _c_ptr, _c_ptr]),
     "shc_scatter": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
                                    _c_i32, _c_ptr, _c_ptr]),
     "shc_segment_maxpool": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_f,
@@ -199,6 +204,29 @@ def sparse_neighbor_conv(S: torch.Tensor, coords: torch.Tensor, inv: torch.Tenso
     _check(load().shc_sparse_neighbor_conv(*args), "shc_sparse_neighbor_conv")
 
 
+def build_neighbor_table(coords: torch.Tensor, inv: torch.Tensor, n_rows: int, B: int, V: int,
+                         nbr: torch.Tensor, table: torch.Tensor, stream=None):
+    """shc_build_neighbor_table: table[j * n_rows + i] = neighbour row of slot j, or -1."""
+    K = nbr.shape[-1]
+    args = [_dev(coords, "coords", torch.int32, 2 * n_rows), _dev(inv, "inv", torch.int32, B * V),
+            n_rows, B, V, _dev(nbr, "nbr", torch.int32, V * K), K,
+            _dev(table, "table", torch.int32, K * n_rows), _stream(stream)]
+    _check(load().shc_build_neighbor_table(*args), "shc_build_neighbor_table")
+
+
+def sparse_neighbor_conv_table(S: torch.Tensor, table: torch.Tensor, n_rows: int,
+                               W: torch.Tensor, bias: Optional[torch.Tensor], out: torch.Tensor,
+                               act: int = SHC_ACT_RELU, stream=None):
+    """shc_sparse_neighbor_conv_table: W [K][Cin][Cout], table from build_neighbor_table."""
+    K, Cin, Cout = W.shape
+    dt = _dtype_code(S)
+    args = [_dev(S, "S", S.dtype, n_rows * Cin), _dev(table, "table", torch.int32, K * n_rows),
+            n_rows, K, _dev(W, "W", S.dtype, K * Cin * Cout),
+            _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, dt, act,
+            _dev(out, "out", S.dtype, n_rows * Cout), _stream(stream)]
+    _check(load().shc_sparse_neighbor_conv_table(*args), "shc_sparse_neighbor_conv_table")
+
+
 def scatter(S: torch.Tensor, inv: torch.Tensor, coords: torch.Tensor, n_rows: int, B: int,
             V: int, D: torch.Tensor, zero_fill: bool = True, stream=None):
     """shc_scatter: compact rows back to D [B*V][C]."""
@@ -306,6 +334,25 @@ def prepare_sparse_neighbor_conv(S, coords, inv, B, V, nbr, W, bias, out, act=SH
             _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, _dtype_code(S), act,
             _dev(out, "out", S.dtype), _stream(stream)]
     return Prepared("shc_sparse_neighbor_conv", args, 3, n_max, (S, coords, inv, nbr, W, bias, out))
+
+
+def prepare_build_neighbor_table(coords, inv, B, V, nbr, table, stream=None) -> Prepared:
+    K = nbr.shape[-1]
+    n_max = min(coords.numel() // 2, table.numel() // K)
+    args = [_dev(coords, "coords", torch.int32), _dev(inv, "inv", torch.int32, B * V), 0, B, V,
+            _dev(nbr, "nbr", torch.int32, V * K), K, _dev(table, "table", torch.int32),
+            _stream(stream)]
+    return Prepared("shc_build_neighbor_table", args, 2, n_max, (coords, inv, nbr, table))
+
+
+def prepare_sparse_neighbor_conv_table(S, table, W, bias, out, act=SHC_ACT_RELU,
+                                       stream=None) -> Prepared:
+    K, Cin, Cout = W.shape
+    n_max = min(S.numel() // Cin, table.numel() // K, out.numel() // Cout)
+    args = [_dev(S, "S", S.dtype), _dev(table, "table", torch.int32), 0, K,
+            _dev(W, "W", S.dtype, K * Cin * Cout), _opt_dev(bias, "bias", torch.float32, Cout),
+            Cin, Cout, _dtype_code(S), act, _dev(out, "out", S.dtype), _stream(stream)]
+    return Prepared("shc_sparse_neighbor_conv_table", args, 2, n_max, (S, table, W, bias, out))
 
 
 def prepare_scatter(S, inv, coords, B, V, D, zero_fill=True, stream=None) -> Prepared:

@@ -243,6 +243,59 @@ int shc_sparse_neighbor_conv(const void* S, const int32_t* coords, const int32_t
                     "sparse_neighbor_conv launch");
 }
 
+int shc_build_neighbor_table(const int32_t* coords, const int32_t* inv, int64_t n_rows,
+                             int32_t B, int32_t V, const int32_t* nbr, int32_t K, int32_t* table,
+                             hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_rows(n_rows));
+  if (K <= 0) return fail(SHC_ERR_INVALID_ARG, "K = %d must be positive", K);
+  if (K > kMaxSlots) return fail(SHC_ERR_UNSUPPORTED, "K = %d exceeds %d slots", K, kMaxSlots);
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(coords, "coords");
+  SHC_PTR(inv, "inv");
+  SHC_PTR(nbr, "nbr");
+  SHC_PTR(table, "table");
+  return hip_status(shc::launch_neighbor_table(coords, inv, n_rows, B, V, nbr, K, table, stream),
+                    "build_neighbor_table launch");
+}
+
+int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t n_rows,
+                                   int32_t K, const void* W, const float* bias, int32_t Cin,
+                                   int32_t Cout, int32_t dtype, int32_t act, void* out,
+                                   hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("Cin", Cin));
+  SHC_TRY(check_channels("Cout", Cout));
+  if (K <= 0) return fail(SHC_ERR_INVALID_ARG, "K = %d must be positive", K);
+  if (K > kMaxSlots) return fail(SHC_ERR_UNSUPPORTED, "K = %d exceeds %d slots", K, kMaxSlots);
+  if (act != SHC_ACT_NONE && act != SHC_ACT_RELU)
+    return fail(SHC_ERR_UNSUPPORTED, "unknown activation code %d", act);
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(S, "S");
+  SHC_PTR(table, "table");
+  SHC_PTR(W, "W");
+  SHC_OPT_PTR(bias, "bias");
+  SHC_PTR(out, "out");
+  shc::GemmArgs a{};
+  a.S = S;
+  a.table = table;
+  a.W = W;
+  a.bias = bias;
+  a.out = out;
+  a.n_rows = n_rows;
+  a.B = 1;
+  a.V = 1;
+  a.K = K;
+  a.Cin = Cin;
+  a.Cout = Cout;
+  a.relu = act == SHC_ACT_RELU;
+  return hip_status(shc::launch_gather_gemm(a, true, dtype == SHC_BF16, stream),
+                    "sparse_neighbor_conv_table launch");
+}
+
 int shc_scatter(const void* S, const int32_t* inv, const int32_t* coords, int64_t n_rows,
                 int32_t B, int32_t V, int32_t C, int32_t dtype, int32_t zero_fill, void* D,
                 hipStream_t stream) {

@@ -115,7 +115,7 @@ __device__ __forceinline__ uint32_t slot_range_bits(int j0, int j1) {
 
 // SPT: neighbour slots per thread when building the index lists (two threads
 // per row), a bound on (K + 1) / 2 fixed at compile time.
-template <bool BF16, int BN, bool CONV, int CHUNK, int STAGES, int SPT>
+template <bool BF16, int BN, bool CONV, bool TBL, int CHUNK, int STAGES, int SPT>
 __global__ __launch_bounds__(kThreads, 2) void gather_gemm_kernel(GemmArgs a) {
   using E = Elem<BF16>;
   using Lt = Layout<BF16, BN, CHUNK, STAGES>;
@@ -168,46 +168,66 @@ __global__ __launch_bounds__(kThreads, 2) void gather_gemm_kernel(GemmArgs a) {
   if (tid < kRowBlocks) blk_slots[tid] = 0;
   if (tid < BM) rowmask[tid] = 0;
   if (CONV) {
-    if (tid < BM) {
-      const int64_t i = row0 + tid;
-      const bool in = i < a.n_rows;
-      const int2 c = reinterpret_cast<const int2*>(a.coords)[in ? i : 0];
-      const bool ok = in && c.x >= 0 && c.x < a.B && c.y >= 0 && c.y < a.V;
-      row_b[tid] = ok ? c.x : -1;
-      row_v[tid] = ok ? c.y : -1;
-    }
-    __syncthreads();
     // two threads per row; thread h of row r takes slots h, h + 2, h + 4, ...
     const int r = tid >> 1;
     const int h = tid & 1;
-    const int b = row_b[r];
-    const int v = row_v[r];
-    // All loads of one level are issued before any is used, unconditionally
-    // (entries past K read a valid address and are masked afterwards), so the
-    // whole list costs two memory round trips.
-    const int vv = v >= 0 ? v : 0;
-    int32_t nb[SPT];
-#pragma unroll
-    for (int m = 0; m < SPT; ++m) {
-      const int j = h + 2 * m;
-      nb[m] = a.nbr[(int64_t)vv * K + (j < K ? j : K - 1)];
-    }
-#pragma unroll
-    for (int m = 0; m < SPT; ++m) {
-      const int j = h + 2 * m;
-      nb[m] = (j < K && v >= 0 && nb[m] >= 0 && nb[m] < a.V) ? nb[m] : -1;
-    }
-    const int bb = b >= 0 ? b : 0;
-    int32_t sv[SPT];
-#pragma unroll
-    for (int m = 0; m < SPT; ++m) sv[m] = a.inv[(int64_t)bb * a.V + (nb[m] >= 0 ? nb[m] : 0)];
     uint32_t bits = 0;
+    if (TBL) {
+      // one round of loads from the slot-major neighbour-row table
+      const bool in = row0 + r < a.n_rows;
+      const int64_t i = in ? row0 + r : 0;
+      int32_t sv[SPT];
 #pragma unroll
-    for (int m = 0; m < SPT; ++m) {
-      const int j = h + 2 * m;
-      const int32_t src = (nb[m] >= 0 && sv[m] >= 0 && (int64_t)sv[m] < a.n_rows) ? sv[m] : -1;
-      if (j < K) srcs0[r * K + j] = src;
-      if (src >= 0) bits |= 1u << j;
+      for (int m = 0; m < SPT; ++m) {
+        const int j = h + 2 * m;
+        sv[m] = a.table[(int64_t)(j < K ? j : K - 1) * a.n_rows + i];
+      }
+#pragma unroll
+      for (int m = 0; m < SPT; ++m) {
+        const int j = h + 2 * m;
+        const int32_t src = (in && sv[m] >= 0 && (int64_t)sv[m] < a.n_rows) ? sv[m] : -1;
+        if (j < K) srcs0[r * K + j] = src;
+        if (j < K && src >= 0) bits |= 1u << j;
+      }
+      __syncthreads();  // rowmask zeroed above before any thread ORs into it
+    } else {
+      if (tid < BM) {
+        const int64_t i = row0 + tid;
+        const bool in = i < a.n_rows;
+        const int2 c = reinterpret_cast<const int2*>(a.coords)[in ? i : 0];
+        const bool ok = in && c.x >= 0 && c.x < a.B && c.y >= 0 && c.y < a.V;
+        row_b[tid] = ok ? c.x : -1;
+        row_v[tid] = ok ? c.y : -1;
+      }
+      __syncthreads();
+      const int b = row_b[r];
+      const int v = row_v[r];
+      // All loads of one level are issued before any is used, unconditionally
+      // (entries past K read a valid address and are masked afterwards), so the
+      // whole list costs two memory round trips.
+      const int vv = v >= 0 ? v : 0;
+      int32_t nb[SPT];
+#pragma unroll
+      for (int m = 0; m < SPT; ++m) {
+        const int j = h + 2 * m;
+        nb[m] = a.nbr[(int64_t)vv * K + (j < K ? j : K - 1)];
+      }
+#pragma unroll
+      for (int m = 0; m < SPT; ++m) {
+        const int j = h + 2 * m;
+        nb[m] = (j < K && v >= 0 && nb[m] >= 0 && nb[m] < a.V) ? nb[m] : -1;
+      }
+      const int bb = b >= 0 ? b : 0;
+      int32_t sv[SPT];
+#pragma unroll
+      for (int m = 0; m < SPT; ++m) sv[m] = a.inv[(int64_t)bb * a.V + (nb[m] >= 0 ? nb[m] : 0)];
+#pragma unroll
+      for (int m = 0; m < SPT; ++m) {
+        const int j = h + 2 * m;
+        const int32_t src = (nb[m] >= 0 && sv[m] >= 0 && (int64_t)sv[m] < a.n_rows) ? sv[m] : -1;
+        if (j < K) srcs0[r * K + j] = src;
+        if (src >= 0) bits |= 1u << j;
+      }
     }
     if (bits) atomicOr(&rowmask[r], bits);
     __syncthreads();
@@ -565,11 +585,21 @@ hipError_t launch_tile(const GemmArgs& a_in, hipStream_t stream) {
   const unsigned gx = (unsigned)((a.n_rows + BM - 1) / BM);
   const unsigned gy = (unsigned)((a.Cout + BN - 1) / BN);
   const size_t lds = lds_bytes<BF16, BN, CH, ST>(CONV ? a.K : 1);
-  if (!CONV || a.K <= 10)
-    return launch_kernel(gather_gemm_kernel<BF16, BN, CONV, CH, ST, CONV ? 5 : 1>, gx, gy, lds,
+  if (!CONV)
+    return launch_kernel(gather_gemm_kernel<BF16, BN, false, false, CH, ST, 1>, gx, gy, lds,
                          stream, a);
-  return launch_kernel(gather_gemm_kernel<BF16, BN, CONV, CH, ST, kMaxSlots / 2>, gx, gy, lds,
-                       stream, a);
+  if (a.table != nullptr) {
+    if (a.K <= 10)
+      return launch_kernel(gather_gemm_kernel<BF16, BN, true, true, CH, ST, 5>, gx, gy, lds,
+                           stream, a);
+    return launch_kernel(gather_gemm_kernel<BF16, BN, true, true, CH, ST, kMaxSlots / 2>, gx,
+                         gy, lds, stream, a);
+  }
+  if (a.K <= 10)
+    return launch_kernel(gather_gemm_kernel<BF16, BN, true, false, CH, ST, 5>, gx, gy, lds,
+                         stream, a);
+  return launch_kernel(gather_gemm_kernel<BF16, BN, true, false, CH, ST, kMaxSlots / 2>, gx, gy,
+                       lds, stream, a);
 }
 
 template <bool BF16, bool CONV>

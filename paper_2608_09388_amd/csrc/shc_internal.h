@@ -57,11 +57,18 @@ hipError_t launch_segment_max(const void* S, const int32_t* row_ptr, int64_t n_r
                               int32_t C, int is_bf16, float empty_value, void* P,
                               hipStream_t stream);
 
+// neighbour-row table of the active set: table[j * n_rows + i] = row of slot j's
+// neighbour of active row i, or -1
+hipError_t launch_neighbor_table(const int32_t* coords, const int32_t* inv, int64_t n_rows,
+                                 int32_t B, int32_t V, const int32_t* nbr, int32_t K,
+                                 int32_t* table, hipStream_t stream);
+
 struct GemmArgs {
   const void* S;        // [n_rows][Cin]
   const int32_t* coords;  // conv only
   const int32_t* inv;     // conv only
   const int32_t* nbr;     // conv only, [V][K]
+  const int32_t* table;   // conv from a neighbour-row table, [K][n_rows]; else null
   const void* W;        // [K][Cin][Cout] (linear: K = 1)
   const float* bias;    // [Cout] or null
   void* out;            // [n_rows][Cout]

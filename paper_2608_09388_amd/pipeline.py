@@ -5,8 +5,9 @@ features, layer weights) to the GPU once, allocates every buffer the path
 needs at its worst-case size (all B*V rows active), and then runs the path
 as a sequence of library calls:
 
-    shc_compact_mask -> shc_gather_rows -> (shc_sparse_linear |
-    shc_sparse_neighbor_conv) per layer -> shc_scatter / shc_segment_maxpool
+    shc_compact_mask (+ shc_build_neighbor_table) -> shc_gather_rows ->
+    (shc_sparse_linear | shc_sparse_neighbor_conv_table) per layer ->
+    shc_scatter / shc_segment_maxpool
 
 The active set never changes across layers (C'_k = C_k, Sec. 3.2), so the
 active count is read back once per mask and passed to every layer call.
@@ -61,19 +62,26 @@ class SparseStack:
         self.dense_out = torch.empty((BV, Cl), dtype=self.dtype, device=dev) if w.scatter else None
         self.pooled = torch.empty((self.B, Cl), dtype=self.dtype, device=dev) if w.pool else None
         self.n = None
+        # neighbour-row table of the active set, shared by every conv layer
+        has_conv = any(l.kind == "conv" for l in w.layers)
+        self.table = (torch.empty((self.K, BV), dtype=torch.int32, device=dev)
+                      if has_conv else None)
         # every call of the path marshalled once, on the current stream; the
         # buffers are at full capacity, so each call only takes the row count
         B, V = self.B, self.V
         self._compact = shc.PreparedCompact(self.mask, B, V, self.coords, self.inv, self.row_ptr,
                                             self.n_active, self.ws)
         self._gather = shc.prepare_gather_rows(self.x, self.coords, B, V, self.acts[0])
+        self._table = (shc.prepare_build_neighbor_table(self.coords, self.inv, B, V, self.nbr,
+                                                        self.table)
+                       if self.table is not None else None)
         self._layers = []
         for l, spec in enumerate(w.layers):
             src, dst = self.acts[l], self.acts[l + 1]
             a = act if spec.relu else shc.SHC_ACT_NONE
             if spec.kind == "conv":
-                call = shc.prepare_sparse_neighbor_conv(src, self.coords, self.inv, B, V, self.nbr,
-                                                        self.weights[l], self.biases[l], dst, a)
+                call = shc.prepare_sparse_neighbor_conv_table(src, self.table, self.weights[l],
+                                                              self.biases[l], dst, a)
             else:
                 call = shc.prepare_sparse_linear(src, self.weights[l], self.biases[l], dst, a)
             self._layers.append(call)
@@ -85,8 +93,12 @@ class SparseStack:
 
     # -- individual steps -----------------------------------------------------
     def compact(self) -> int:
-        """Compaction; waits for the active count (one host sync per mask)."""
+        """Compaction; waits for the active count (one host sync per mask),
+        then builds the neighbour-row table of the active set if a conv layer
+        will read it."""
         self.n = self._compact()
+        if self._table is not None:
+            self._table(self.n)
         return self.n
 
     def gather(self):

@@ -120,6 +120,39 @@ def test_layer_validation(lib):
     assert conv(out=None) == -1
 
 
+def test_neighbor_table_validation(lib):
+    T = lib.shc_build_neighbor_table
+
+    def table(**kw):
+        a = dict(coords=A, inv=A, n=10, B=4, V=655, nbr=A, K=9, table=A)
+        a.update(kw)
+        return T(a["coords"], a["inv"], a["n"], a["B"], a["V"], a["nbr"], a["K"], a["table"], None)
+
+    assert table(K=0) == -1
+    assert table(K=33) == -4
+    assert table(V=0) == -1
+    assert table(n=-1) == -1
+    assert table(coords=None) == -1 and "coords" in err(lib)
+    assert table(table=None) == -1 and "table" in err(lib)
+    assert table(nbr=MIS) == -3
+    assert table(n=0, coords=None, table=None) == 0     # N' = 0 is a no-op
+    C = lib.shc_sparse_neighbor_conv_table
+
+    def conv(**kw):
+        a = dict(S=A, table=A, n=10, K=9, W=A, bias=None, Cin=16, Cout=64, dt=1, act=1, out=A)
+        a.update(kw)
+        return C(a["S"], a["table"], a["n"], a["K"], a["W"], a["bias"], a["Cin"], a["Cout"],
+                 a["dt"], a["act"], a["out"], None)
+
+    assert conv(table=None) == -1 and "table" in err(lib)
+    assert conv(table=MIS) == -3
+    assert conv(K=40) == -4
+    assert conv(Cin=20) == -4
+    assert conv(act=3) == -4
+    assert conv(bias=MIS) == -3
+    assert conv(n=0, S=None, table=None, out=None) == 0
+
+
 def test_binding_refuses_cpu_tensors():
     torch = pytest.importorskip("torch")
     x = torch.zeros(4 * 655, 16)

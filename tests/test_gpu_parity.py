@@ -240,14 +240,41 @@ def test_sparse_linear_zero_rows_is_noop(dev):
 # ----------------------------------------------------------------------------
 
 
-def run_conv(dev, m, nbr, S_vals, W, bias, dtype, act=shc.SHC_ACT_RELU):
+def table_reference(m, nbr):
+    """table[j][i] = inv[b_i, nbr[v_i][j]] or -1, from the oracle's compaction
+    (the definition of the neighbour rows of Eqs. 4-5, written out)."""
+    B, V = m.shape
+    coords, inv, _, n = O.compact(m)
+    K = nbr.shape[1]
+    t = np.full((K, n), -1, np.int64)
+    for j in range(K):
+        u = nbr[coords[:, 1], j].astype(np.int64)
+        ok = (u >= 0) & (u < V)
+        r = inv[coords[:, 0] * V + np.where(ok, u, 0)]
+        t[j] = np.where(ok, r, -1)
+    return t
+
+
+def run_conv(dev, m, nbr, S_vals, W, bias, dtype, act=shc.SHC_ACT_RELU, path="direct"):
+    """One conv through the C ABI: `direct` (coords, inv, nbr) or `table`
+    (neighbour-row table built by the library, checked exactly first)."""
     B, V = m.shape
     c = Compaction(m)
     n = c.run()
     K, Cin, Cout = W.shape
     out = torch.full((n + 2, Cout), float("nan"), dtype=synth_dtype(dtype), device=dev)
-    shc.sparse_neighbor_conv(up(S_vals, dtype), c.coords, c.inv, n, B, V, up(nbr), up(W, dtype),
-                             None if bias is None else up(bias), out, act)
+    Sd = up(S_vals, dtype)
+    Wd = up(W, dtype)
+    bd = None if bias is None else up(bias)
+    if path == "direct":
+        shc.sparse_neighbor_conv(Sd, c.coords, c.inv, n, B, V, up(nbr), Wd, bd, out, act)
+    else:
+        table = torch.full((K * n + 3,), -7, dtype=torch.int32, device=dev)
+        shc.build_neighbor_table(c.coords, c.inv, n, B, V, up(nbr), table)
+        got_t = down(table)
+        assert np.array_equal(got_t[:K * n].reshape(K, n), table_reference(m, nbr))
+        assert np.all(got_t[K * n:] == -7)
+        shc.sparse_neighbor_conv_table(Sd, table, n, Wd, bd, out, act)
     got = down(out)
     assert np.all(np.isnan(got[n:]))
     return got[:n], n
@@ -258,7 +285,8 @@ def run_conv(dev, m, nbr, S_vals, W, bias, dtype, act=shc.SHC_ACT_RELU):
     (3, 200, 9, 16, 64, 0.3), (2, 333, 9, 64, 64, 0.5), (4, 150, 4, 48, 32, 0.4),
     (2, 500, 9, 128, 128, 0.1), (1, 300, 1, 32, 16, 0.6), (2, 100, 32, 16, 16, 0.7),
     (2, 257, 9, 256, 256, 0.2), (3, 211, 5, 32, 192, 0.9)])
-def test_sparse_conv_full_oracle(dev, dtype, B, V, K, Cin, Cout, p):
+@pytest.mark.parametrize("path", ["direct", "table"])
+def test_sparse_conv_full_oracle(dev, dtype, B, V, K, Cin, Cout, p, path):
     rng = np.random.default_rng(B * V + K * 7 + Cin)
     m = (rng.random((B, V)) < p).astype(np.uint8)
     nbr = rand_nbr(V, K, rng)
@@ -268,14 +296,15 @@ def test_sparse_conv_full_oracle(dev, dtype, B, V, K, Cin, Cout, p):
                        .astype(np.float32), dtype)[1]
     bias = rng.standard_normal(Cout).astype(np.float32)
     for b, act in ((None, shc.SHC_ACT_NONE), (bias, shc.SHC_ACT_RELU)):
-        got, n2 = run_conv(dev, m, nbr, S, W, b, dtype, act)
+        got, n2 = run_conv(dev, m, nbr, S, W, b, dtype, act, path)
         assert n2 == n
         ref = O.sparse_conv(S, coords, B, V, nbr, W, b, act == shc.SHC_ACT_RELU)
         scale = O.sparse_conv_scale(S, coords, B, V, nbr, W, b)
         assert_scaled_close(got, ref, scale, dtype, f"conv K={K} {Cin}->{Cout} p={p}")
 
 
-def test_sparse_conv_edge_cases(dev):
+@pytest.mark.parametrize("path", ["direct", "table"])
+def test_sparse_conv_edge_cases(dev, path):
     rng = np.random.default_rng(3)
     V, K, C = 50, 9, 16
     nbr = rand_nbr(V, K, rng)
@@ -286,7 +315,7 @@ def test_sparse_conv_edge_cases(dev):
     m = np.zeros((2, V), np.uint8)
     m[1, 7] = 1
     S = rng.standard_normal((1, C)).astype(np.float32)
-    got, n = run_conv(dev, m, nbr, S, W, b, "f32", shc.SHC_ACT_NONE)
+    got, n = run_conv(dev, m, nbr, S, W, b, "f32", shc.SHC_ACT_NONE, path)
     ref = b + sum(S[0].astype(np.float64) @ W[j] for j in range(K) if nbr[7, j] == 7)
     assert_scaled_close(got[0], ref, O.conv_at(S, O.compact(m)[0], 2, V, nbr, W, [0], b,
                                                 scale=True)[0], "f32", "lone vertex")
@@ -300,18 +329,20 @@ def test_sparse_conv_edge_cases(dev):
     m = (rng.random((2, V)) < 0.6).astype(np.uint8)
     n = int(m.sum())
     S = rng.standard_normal((n, C)).astype(np.float32)
-    g_bad, _ = run_conv(dev, m, nbr_bad, S, W, b, "f32")
-    g_ok, _ = run_conv(dev, m, nbr_ok, S, W, b, "f32")
+    g_bad, _ = run_conv(dev, m, nbr_bad, S, W, b, "f32", path=path)
+    g_ok, _ = run_conv(dev, m, nbr_ok, S, W, b, "f32", path=path)
     assert np.array_equal(g_bad, g_ok)
     # K = 1 self-neighbour conv is the linear layer
     self_nbr = np.arange(V, dtype=np.int32)[:, None]
-    g_c, _ = run_conv(dev, m, self_nbr, S, W[:1], b, "f32")
+    g_c, _ = run_conv(dev, m, self_nbr, S, W[:1], b, "f32", path=path)
     out = torch.empty((n, C), device=dev)
     shc.sparse_linear(up(S, "f32"), n, up(W[0], "f32"), up(b), out, shc.SHC_ACT_RELU)
     assert np.array_equal(g_c, down(out))
 
 
 def test_sparse_conv_deterministic(dev):
+    """Repeated calls give identical bits, and the table path gives the same
+    bits as the direct path (same kernel, same row blocks)."""
     w = synth.workload_c4(0.05)
     rng = np.random.default_rng(1)
     m = w.mask[:16]
@@ -320,7 +351,26 @@ def test_sparse_conv_deterministic(dev):
     W = w.layers[1].W
     g1, _ = run_conv(dev, m, w.nbr, S, W, None, "bf16")
     g2, _ = run_conv(dev, m, w.nbr, S, W, None, "bf16")
+    g3, _ = run_conv(dev, m, w.nbr, S, W, None, "bf16", path="table")
+    g4, _ = run_conv(dev, m, w.nbr, S, W, None, "bf16", path="table")
     assert np.array_equal(g1, g2)
+    assert np.array_equal(g3, g4)
+    assert np.array_equal(g1, g3)
+
+
+def test_neighbor_table_zero_rows(dev):
+    """N' = 0: building the table and the table conv are no-ops."""
+    V, K = 20, 9
+    nbr = up(rand_nbr(V, K, np.random.default_rng(5)))
+    c = Compaction(np.zeros((2, V), np.uint8))
+    assert c.run() == 0
+    table = torch.full((8,), -7, dtype=torch.int32, device=dev)
+    shc.build_neighbor_table(c.coords, c.inv, 0, 2, V, nbr, table)
+    S = torch.zeros((1, 16), device=dev)
+    out = torch.full((1, 16), 3.0, device=dev)
+    shc.sparse_neighbor_conv_table(S, table, 0, torch.zeros((K, 16, 16), device=dev), None, out)
+    torch.cuda.synchronize()
+    assert np.all(down(table) == -7) and np.all(down(out) == 3.0)
 
 
 # ----------------------------------------------------------------------------
