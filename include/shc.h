@@ -93,8 +93,11 @@ size_t shc_compact_mask_workspace(int32_t B, int32_t V);
  *             stream, stores N' there and returns SHC_ERR_CAPACITY if N' > cap.
  *             If it lies in page-locked host memory mapped into the device
  *             (hipHostMalloc), the kernel stores the count there itself and
- *             the call only waits; pageable memory costs one extra
- *             device-to-host copy.
+ *             the call returns as soon as the count has arrived: the other
+ *             outputs may still be being written, and work enqueued later on
+ *             the same stream is ordered after them (synchronise the stream
+ *             before reading them on the host).  Pageable memory costs one
+ *             device-to-host copy and a full stream synchronisation.
  *   cap       rows available in `coords` (>= 0).
  *   ws, ws_bytes  device workspace of at least shc_compact_mask_workspace(B, V)
  *             bytes; its contents on entry do not matter.

@@ -130,6 +130,8 @@ int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
   if (ws_bytes < need)
     return fail(SHC_ERR_CAPACITY, "workspace of %zu bytes is below the %zu needed", ws_bytes, need);
   int64_t* mapped = n_active_host ? mapped_host_count(n_active_host) : nullptr;
+  volatile int64_t* host_count = n_active_host;
+  if (mapped != nullptr) *host_count = -1;  // set by the kernel once N' is known
   int rc = hip_status(shc::launch_compact(mask, B, V, coords, inv, row_ptr, n_active_dev, mapped,
                                           cap, static_cast<int32_t*>(ws), stream),
                       "compact_mask launch");
@@ -145,9 +147,23 @@ int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
     if (rc != SHC_OK) return rc;
     n = n32;
   } else {
-    rc = hip_status(hipStreamSynchronize(stream), "compact_mask stream sync");
-    if (rc != SHC_OK) return rc;
-    n = *static_cast<volatile int64_t*>(n_active_host);
+    // The last block stores the final N' into the page-locked variable; poll
+    // it rather than waiting for the whole stream (later work on the stream
+    // is ordered after the compaction anyway).  Every few thousand polls the
+    // stream is queried, so a failed launch or a finished stream ends the wait.
+    for (uint64_t it = 1;; ++it) {
+      n = *host_count;
+      if (n >= 0) break;
+      if ((it & 4095u) == 0) {
+        const hipError_t q = hipStreamQuery(stream);
+        if (q == hipSuccess) {
+          n = *host_count;
+          if (n < 0) return fail(SHC_ERR_HIP, "compact_mask: stream finished without a count");
+          break;
+        }
+        if (q != hipErrorNotReady) return hip_status(q, "compact_mask stream query");
+      }
+    }
   }
   *n_active_host = n;
   if (n > cap)
