@@ -20,16 +20,17 @@
 //     sparse slot -- a slot present in fewer than half of the rows.  16-row
 //     blocks then hold rows with only dense slots, or rows sharing a sparse
 //     slot, and each block carries the set of slots any of its rows has;
-//   * every wavefront walks a list of jobs (block, live slot) over blocks
-//     b = wave, wave + 8, ...  A job loads the A fragments of its slot (16
-//     bytes per lane of the gathered neighbour rows, one per 64-byte k-step)
-//     straight from global memory; jobs are issued D ahead through a ring of
-//     register sets, so about 16 fragment loads per wave are in flight.  The
-//     B fragments come from the resident slice (ds_read_b64_tr_b16 for bf16)
-//     and each feeds one MFMA per 16 output columns.  No barrier in this loop;
-//   * when a block's last job is done its 16 rows x WS columns get the bias,
-//     the activation and the rounding, and go back through a per-wave LDS
-//     scratch as 16-byte vectors to the rows' original positions.
+//   * every wavefront walks its list of jobs (block, live slot), built once,
+//     over blocks b = wave, wave + 8, ...  A job loads the A fragments of its
+//     slot (16 bytes per lane of the gathered neighbour rows, one per 64-byte
+//     k-step) with raw buffer loads, an absent row reading zeros; jobs are
+//     issued D ahead through a ring of register sets.  All B fragments of a
+//     job are read from the resident slice (ds_read_b64_tr_b16 for bf16)
+//     before its MFMAs (one per 16 output columns).  No barrier in this loop;
+//   * accumulators start at the bias; when a block's last job is done its 16
+//     rows x WS columns get the activation and the rounding, and go back
+//     through a per-wave LDS scratch as 16-byte vectors to the rows' original
+//     positions.
 // Every output row is accumulated over the same (slot, k-step) sequence
 // whatever block it lands in (absent slots contribute exact zeros), so the
 // result does not depend on the order the sort produced.
@@ -48,9 +49,14 @@ constexpr int kRPT = 3;                       // rows per thread in the index bu
 constexpr int kMaxRows = kRPT * kThreads;     // rows per workgroup
 constexpr int kLdsLimit = 160 * 1024;
 constexpr int kWBatch = 8;                    // weight vectors in flight per thread
+// jobs of one wavefront: at most kMaxRows / 16 / kWaves blocks of at most 10 live slots
+constexpr int kMaxJobs = 128;
+static_assert((kMaxRows / 16 + kWaves - 1) / kWaves * 10 <= kMaxJobs, "job list too short");
 
 typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
 typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 // third word of a raw buffer resource on gfx9-family parts (32-bit data, no swizzle)
 constexpr int kBufferWord3 = 0x00020000;
 // a buffer offset past any buffer the kernel is given (buffers are < 2 GiB)
@@ -74,9 +80,11 @@ struct WElem<false> {
 
 __host__ __device__ inline int ws_wrow(int ws, int e) { return ws * e + 16; }
 // srcs[rows*K], perm[rows], blkmask[rows/16], scnt[waves][kMaxSlots],
-// bcnt[kBuckets][kRPT][waves] (counts, then exclusive starts, in scan order)
+// bcnt[kBuckets][kRPT][waves] (counts, then exclusive starts, in scan order),
+// jobl[waves][kMaxJobs] (each wavefront's job list)
 __host__ __device__ inline int ws_idx_bytes(int rows, int K) {
-  return (4 * (rows * K + rows + rows / 16 + kWaves * kMaxSlots + kRPT * kWaves * kBuckets) +
+  return (4 * (rows * K + rows + rows / 16 + kWaves * kMaxSlots + kRPT * kWaves * kBuckets +
+               kWaves * kMaxJobs) +
           15) & ~15;
 }
 // epilogue staging for every wave, then one k-step of zero weight rows
@@ -93,7 +101,7 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
   constexpr int WROW = WS * E::bytes + 16;
   constexpr int VPR = WS * E::bytes / 16;  // 16-byte vectors per slice row
   // jobs in flight (fewer when the linear layer keeps its B fragments in registers)
-  constexpr int D = (BF16 && !CONV && KSM * NCB <= 32) ? 12 / KSM : 16 / KSM;
+  constexpr int D = (BF16 && !CONV && KSM * NCB <= 32) ? 8 / KSM : 16 / KSM;
 
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int K = CONV ? a.K : 1;
@@ -109,6 +117,7 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
   uint32_t* blkmask = reinterpret_cast<uint32_t*>(perm + R);    // [R/16]
   int32_t* scnt = reinterpret_cast<int32_t*>(blkmask + R / 16); // [waves][kMaxSlots]
   int32_t* bcnt = scnt + kWaves * kMaxSlots;                    // [kBuckets][kRPT][waves]
+  int32_t* jobl = bcnt + kBuckets * kRPT * kWaves;              // [waves][kMaxJobs]
   unsigned char* scratch = smem + wbytes + ws_idx_bytes(R, K);  // [waves][16][WROW]
   unsigned char* zrows = scratch + kWaves * 16 * WROW;           // [kstep][WROW] zeros
 
@@ -221,7 +230,7 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
 #pragma unroll
       for (int j = 0; j < KM; ++j) {
         const int32_t s = sv[rr][j];
-        sv[rr][j] = (s >= 0 && (int64_t)s < a.n_rows) ? s : -1;
+        sv[rr][j] = (uint32_t)s < (uint32_t)a.n_rows ? s : -1;  // 0 <= s < n_rows
         if (sv[rr][j] >= 0) rmask[rr] |= 1u << j;
       }
     }
@@ -318,6 +327,7 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
     const float bvl = bp[ok ? col : 0];
     bias_v[cb] = ok ? bvl : 0.f;
   }
+  const bool relu = a.relu != 0;
   unsigned char* my_scratch = scratch + wave * 16 * WROW;
   unsigned char* out = static_cast<unsigned char*>(a.out);
 
@@ -326,23 +336,52 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
     int j;      // slot, or -1 for a block with no present slot (bias only)
     bool last;  // last job of its block
   };
-  int gb = wave - kWaves;  // job generator: current block and its slots left
-  uint32_t grem = 0;
-  bool gpending = false;   // block gb still owes its (bias-only) job
+  // This wavefront's job list, built once: its blocks b = wave, wave + 8, ...
+  // in order, each with one job per live slot (ascending) or a single
+  // bias-only job; packed as b << 8 | (slot + 1) << 1 | last.
+  int njobs = 0;
+  {
+    const int nb = nblk > wave ? (nblk - wave + kWaves - 1) / kWaves : 0;
+    int32_t* mine = jobl + wave * kMaxJobs;
+    for (int i0 = 0; i0 < nb; i0 += 64) {
+      const int i = i0 + lane;
+      const int b = wave + kWaves * (i < nb ? i : 0);
+      const uint32_t m = blkmask[b];
+      const int c = i < nb ? (m ? __popc(m) : 1) : 0;
+      int inc = c;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int y = __shfl_up(inc, d, 64);
+        if (lane >= d) inc += y;
+      }
+      int k = njobs + inc - c;
+      if (i < nb) {
+        if (m == 0) {
+          mine[k] = (b << 8) | 1;
+        } else {
+          for (uint32_t mm = m; mm != 0;) {
+            const int j = __builtin_ctz(mm);
+            mm &= mm - 1;
+            mine[k++] = (b << 8) | ((j + 1) << 1) | (mm == 0 ? 1 : 0);
+          }
+        }
+      }
+      njobs += __shfl(inc, 63, 64);
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  njobs = __builtin_amdgcn_readfirstlane(njobs);
+  // lane l holds job (jt & ~63) + l; refilled every 64 jobs
+  int jt = 0;
+  int jreg = jobl[wave * kMaxJobs + lane];
   auto next_job = [&]() -> Job {
-    while (grem == 0 && !gpending) {
-      gb += kWaves;
-      if (gb >= nblk) return Job{-1, -1, true};
-      grem = __builtin_amdgcn_readfirstlane(blkmask[gb]);
-      gpending = grem == 0;  // rows without any present slot still need an output
-    }
-    if (gpending) {
-      gpending = false;
-      return Job{gb, -1, true};
-    }
-    const int j = __builtin_ctz(grem);
-    grem &= grem - 1;
-    return Job{gb, j, grem == 0};
+    if (jt >= njobs) return Job{-1, -1, true};
+    if ((jt & 63) == 0 && jt > 0) jreg = jobl[wave * kMaxJobs + ((jt + lane) & (kMaxJobs - 1))];
+    const int w = __builtin_amdgcn_readlane(jreg, jt & 63);
+    ++jt;
+    return Job{w >> 8, ((w >> 1) & 127) - 1, (w & 1) != 0};
   };
 
   // A fragments come through raw buffer loads with 32-bit offsets: an absent
@@ -365,9 +404,10 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
                      s_rsrc, ks < KS ? off + (uint32_t)ks * 64u : kOutOfRange, 0, 0));
   };
 
+  // accumulators start at the bias of their column (lane l16 of block cb)
   f32x4 acc[NCB];
 #pragma unroll
-  for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x4{bias_v[cb], bias_v[cb], bias_v[cb], bias_v[cb]};
 
   // B fragments of one k-step row block (bf16): two transposing LDS reads per
   // 16 output columns give lane (g, i) rows 8g .. 8g+7 of column i.
@@ -471,17 +511,22 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
   auto epilogue = [&](int blk) {
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
+      float v[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float v = acc[cb][r] + bias_v[cb];
-        if (a.relu) v = v > 0.f ? v : 0.f;
-        unsigned char* pp = my_scratch + (g * 4 + r) * WROW + (cb * 16 + l16) * E::bytes;
-        if (BF16)  // hardware round-to-nearest-even conversion
-          *reinterpret_cast<__bf16*>(pp) = static_cast<__bf16>(v);
-        else
-          *reinterpret_cast<float*>(pp) = v;
+      for (int r = 0; r < 4; ++r) v[r] = (!relu || acc[cb][r] > 0.f) ? acc[cb][r] : 0.f;
+      unsigned char* pp = my_scratch + (g * 4) * WROW + (cb * 16 + l16) * E::bytes;
+      if (BF16) {  // hardware round-to-nearest-even conversion, two rows per instruction
+#pragma unroll
+        for (int r = 0; r < 4; r += 2) {
+          const bf16x2 h = __builtin_convertvector(f32x2{v[r], v[r + 1]}, bf16x2);
+          *reinterpret_cast<__bf16*>(pp + r * WROW) = h[0];
+          *reinterpret_cast<__bf16*>(pp + (r + 1) * WROW) = h[1];
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) *reinterpret_cast<float*>(pp + r * WROW) = v[r];
       }
-      acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      acc[cb] = f32x4{bias_v[cb], bias_v[cb], bias_v[cb], bias_v[cb]};
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();

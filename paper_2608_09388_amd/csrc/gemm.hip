@@ -35,7 +35,7 @@
 //     load; a 16-row MFMA block whose rows have no present neighbour in the
 //     slot(s) of a chunk is skipped (its product would be zero), and so is a
 //     chunk that no row of the tile needs;
-//   * the epilogue adds the bias, applies the activation, rounds to the
+//   * the accumulators start at the bias; the epilogue applies the activation, rounds to the
 //     output dtype and writes whole rows through LDS as 16-byte vectors.
 //
 // MFMA operand layout (CDNA3/CDNA4, 64 lanes, g = lane / 16, i = lane % 16):
@@ -379,11 +379,22 @@ __global__ __launch_bounds__(kThreads, 2) void gather_gemm_kernel(GemmArgs a) {
     }
   };
 
+  // bias of this lane's columns: the accumulators start at it
+  float bias_v[NB];
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) {
+    const int col = n0 + wn * WN + cb * 16 + l16;
+    const bool ok = a.bias != nullptr && col < Cout;
+    const float* bp = a.bias != nullptr ? a.bias : reinterpret_cast<const float*>(a.W);
+    const float bvl = bp[ok ? col : 0];
+    bias_v[cb] = ok ? bvl : 0.f;
+  }
   f32x4 acc[4][NB];
 #pragma unroll
   for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) acc[rb][cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int cb = 0; cb < NB; ++cb)
+      acc[rb][cb] = f32x4{bias_v[cb], bias_v[cb], bias_v[cb], bias_v[cb]};
 
   // one 64-byte k-step (32 bf16 / 16 fp32 reduction entries) of a staged chunk
   auto compute_step = [&](const unsigned char* a_lds, const unsigned char* w_lds, int ks,
@@ -455,16 +466,6 @@ __global__ __launch_bounds__(kThreads, 2) void gather_gemm_kernel(GemmArgs a) {
   };
 
   // ---- main loop -------------------------------------------------------------
-  // bias of this lane's columns, read once, long before the epilogue needs it
-  float bias_v[NB];
-#pragma unroll
-  for (int cb = 0; cb < NB; ++cb) {
-    const int col = n0 + wn * WN + cb * 16 + l16;
-    const bool ok = a.bias != nullptr && col < Cout;
-    const float* bp = a.bias != nullptr ? a.bias : reinterpret_cast<const float*>(a.W);
-    const float bvl = bp[ok ? col : 0];
-    bias_v[cb] = ok ? bvl : 0.f;
-  }
 
   // ---- main loop: software pipeline over steps t = 0, 1, ... ---------------------
   // Step t loads chunk t into register set t % 2, runs the MFMAs of chunk
@@ -523,13 +524,12 @@ __global__ __launch_bounds__(kThreads, 2) void gather_gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
         const int col_l = wn * WN + cb * 16 + l16;
-        const float bv = bias_v[cb];
 #pragma unroll
         for (int rb = 0; rb < 4; ++rb) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int row_l = (kPasses == 1 ? wm * 64 : 0) + rb * 16 + g * 4 + r;
-            float v = acc[rb][cb][r] + bv;
+            float v = acc[rb][cb][r];  // the bias is already in
             if (a.relu) v = v > 0.f ? v : 0.f;
             unsigned char* p = o_lds + row_l * Lt::ORow + col_l * E::bytes;
             if (BF16)  // hardware round-to-nearest-even conversion
