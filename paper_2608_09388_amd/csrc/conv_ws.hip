@@ -41,17 +41,19 @@
 namespace shc {
 namespace {
 
-constexpr int kThreads = 512;
-constexpr int kWaves = kThreads / 64;
+// 8 wavefronts (two per SIMD) for both; 12 for the conv fit its registers
+// but measured slower (more loads in flight contend in the memory path)
+constexpr int kThreadsConv = 512;
+constexpr int kThreadsLin = 512;
 constexpr int kMaxSlots = 32;
 constexpr int kBuckets = kMaxSlots + 2;
-constexpr int kRPT = 3;                       // rows per thread in the index build
-constexpr int kMaxRows = kRPT * kThreads;     // rows per workgroup
+constexpr int kMaxRows = 1536;                // rows per workgroup
 constexpr int kLdsLimit = 160 * 1024;
 constexpr int kWBatch = 8;                    // weight vectors in flight per thread
-// jobs of one wavefront: at most kMaxRows / 16 / kWaves blocks of at most 10 live slots
+// jobs of one wavefront: at most kMaxRows / 16 / waves blocks of at most 10 live slots
 constexpr int kMaxJobs = 128;
-static_assert((kMaxRows / 16 + kWaves - 1) / kWaves * 10 <= kMaxJobs, "job list too short");
+static_assert((kMaxRows / 16 + 7) / 8 * 10 <= kMaxJobs, "job list too short");
+static_assert(kMaxRows % kThreadsConv == 0 && kMaxRows % kThreadsLin == 0, "rows per thread");
 
 typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
 typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
@@ -78,27 +80,36 @@ struct WElem<false> {
   static constexpr int kstep = 16;
 };
 
+// epilogue staging row (padded)
 __host__ __device__ inline int ws_wrow(int ws, int e) { return ws * e + 16; }
+// weight-slice row: unpadded for bf16 (the 32-byte column chunks are
+// XOR-swizzled instead, see swz_chunk), padded for fp32
+__host__ __device__ inline int ws_wrow_w(int ws, int e) { return e == 2 ? ws * e : ws * e + 16; }
 // srcs[rows*K], perm[rows], blkmask[rows/16], scnt[waves][kMaxSlots],
 // bcnt[kBuckets][kRPT][waves] (counts, then exclusive starts, in scan order),
 // jobl[waves][kMaxJobs] (each wavefront's job list)
-__host__ __device__ inline int ws_idx_bytes(int rows, int K) {
-  return (4 * (rows * K + rows + rows / 16 + kWaves * kMaxSlots + kRPT * kWaves * kBuckets +
-               kWaves * kMaxJobs) +
+__host__ __device__ inline int ws_idx_bytes(int rows, int K, int waves, int rpt) {
+  return (4 * (rows * K + rows + rows / 16 + waves * kMaxSlots + rpt * waves * kBuckets +
+               waves * kMaxJobs) +
           15) & ~15;
 }
 // epilogue staging for every wave, then one k-step of zero weight rows
-__host__ __device__ inline int ws_scratch(int ws, int e) {
-  return kWaves * 16 * ws_wrow(ws, e) + (e == 2 ? 32 : 16) * ws_wrow(ws, e);
+__host__ __device__ inline int ws_scratch(int ws, int e, int waves) {
+  return waves * 16 * ws_wrow(ws, e) + (e == 2 ? 32 : 16) * ws_wrow_w(ws, e);
 }
 
 // KM: slots held per row in registers during the index build (>= K).
 // KSM: k-steps per slot held per job (>= Cin / kstep); D jobs in flight.
 template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM>
-__global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
+__global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kernel(GemmArgs a,
+                                                                                   int R) {
+  constexpr int kThreads = CONV ? kThreadsConv : kThreadsLin;
+  constexpr int kWaves = kThreads / 64;
+  constexpr int kRPT = kMaxRows / kThreads;  // rows per thread in the index build
   using E = WElem<BF16>;
   constexpr int NCB = WS / 16;             // 16-column blocks in the slice
-  constexpr int WROW = WS * E::bytes + 16;
+  constexpr int WROW = WS * E::bytes + 16;        // epilogue staging row
+  constexpr int WROWW = BF16 ? WS * 2 : WROW;      // weight-slice row
   constexpr int VPR = WS * E::bytes / 16;  // 16-byte vectors per slice row
   // jobs in flight (fewer when the linear layer keeps its B fragments in registers)
   constexpr int D = (BF16 && !CONV && KSM * NCB <= 32) ? 8 / KSM : 16 / KSM;
@@ -110,16 +121,16 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
   const int Ktot = K * Cin;
   const int KS = Cin / E::kstep;  // k-steps per slot (Cin * e is a multiple of 64)
 
-  unsigned char* wl = smem;  // [Ktot][WROW]
-  const int wbytes = (Ktot * WROW + 15) & ~15;
+  unsigned char* wl = smem;  // [Ktot][WROWW]
+  const int wbytes = (Ktot * WROWW + 15) & ~15;
   int32_t* srcs = reinterpret_cast<int32_t*>(smem + wbytes);    // [R][K], sorted order
   int32_t* perm = srcs + R * K;                                 // [R] position -> row
   uint32_t* blkmask = reinterpret_cast<uint32_t*>(perm + R);    // [R/16]
   int32_t* scnt = reinterpret_cast<int32_t*>(blkmask + R / 16); // [waves][kMaxSlots]
   int32_t* bcnt = scnt + kWaves * kMaxSlots;                    // [kBuckets][kRPT][waves]
   int32_t* jobl = bcnt + kBuckets * kRPT * kWaves;              // [waves][kMaxJobs]
-  unsigned char* scratch = smem + wbytes + ws_idx_bytes(R, K);  // [waves][16][WROW]
-  unsigned char* zrows = scratch + kWaves * 16 * WROW;           // [kstep][WROW] zeros
+  unsigned char* scratch = smem + wbytes + ws_idx_bytes(R, K, kWaves, kRPT);  // [waves][16][WROW]
+  unsigned char* zrows = scratch + kWaves * 16 * WROW;           // [kstep][WROWW] zeros
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -133,6 +144,19 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
   const int n0 = blockIdx.y * WS;
   const unsigned char* S = static_cast<const unsigned char*>(a.S);
   const unsigned char* W = static_cast<const unsigned char*>(a.W);
+
+  // Byte offset of 16-byte vector q in weight-slice row k.  For bf16 the
+  // 32-byte column chunk (16 output columns) is XOR-ed with bit 1 ^ bit 3 of
+  // the row: the transposing reads of a wavefront then touch rows r and r + 8
+  // (and r, r + 2) in different chunks, so no two lanes of a cycle share an
+  // LDS bank.  For a reduction row 8g + i (+4) of a 32-row k-step the swizzle
+  // bit is ((i >> 1) ^ g) & 1, a per-lane constant (swz_lane).
+  auto w_col = [&](int k, int q) -> int {
+    if (!BF16 || NCB < 2) return q * 16;
+    const int h = ((k >> 1) ^ (k >> 3)) & 1;
+    return ((((q >> 1) ^ h)) << 5) + ((q & 1) << 4);
+  };
+  const int swz_lane = (BF16 && NCB >= 2) ? ((((l16 >> 2) >> 1) ^ g) & 1) : 0;
 
   // ---- weight slice W[k][n0 .. n0 + WS) -> LDS, kWBatch vectors per thread at a time
   const int wvecs = Ktot * VPR;
@@ -155,19 +179,19 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
       const int v = base + u * kThreads + tid;
       const int k = v / VPR;
       const int q = v - k * VPR;
-      if (v < wvecs) *reinterpret_cast<i32x4*>(wl + k * WROW + q * 16) = wv[u];
+      if (v < wvecs) *reinterpret_cast<i32x4*>(wl + k * WROWW + w_col(k, q)) = wv[u];
     }
   };
   i32x4 wv[kWBatch];
   load_w(0, wv);
 
   for (int q = tid; q < R / 16; q += kThreads) blkmask[q] = 0;
-  for (int q = tid; q < E::kstep * WROW / 16; q += kThreads)
+  for (int q = tid; q < E::kstep * WROWW / 16; q += kThreads)
     reinterpret_cast<i32x4*>(zrows)[q] = i32x4{0, 0, 0, 0};
   const uint64_t lt = (1ull << lane) - 1ull;
 
   // ---- index lists, sorted by first sparse slot ---------------------------------
-  // thread tid handles rows t = tid + rr * 512 (rr < kRPT) of this workgroup
+  // thread tid handles rows t = tid + rr * kThreads (rr < kRPT) of this workgroup
   if (CONV) {
     int32_t sv[kRPT][KM];
     if (TBL) {
@@ -414,11 +438,12 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
   auto read_b = [&](const unsigned char* base, bf16x8* out_cb) {
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
-      const unsigned char* p0 = base + (8 * g + (l16 >> 2)) * WROW + (cb * 16 + 4 * (l16 & 3)) * 2;
+      const unsigned char* p0 =
+          base + (8 * g + (l16 >> 2)) * WROWW + (((cb ^ swz_lane) << 5) + 8 * (l16 & 3));
       const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
           (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0)));
       const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-          (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0 + 4 * WROW)));
+          (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0 + 4 * WROWW)));
       out_cb[cb] = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     }
   };
@@ -429,7 +454,7 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
   if constexpr (kResidentB) {
 #pragma unroll
     for (int ks = 0; ks < KSM; ++ks)
-      read_b(ks < KS ? wl + ks * E::kstep * WROW : zrows, wres[kResidentB ? ks : 0]);
+      read_b(ks < KS ? wl + ks * E::kstep * WROWW : zrows, wres[kResidentB ? ks : 0]);
   }
 
   // Branch-free contraction of one job: every B fragment of the job is read
@@ -450,7 +475,7 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
         return;
       }
       auto kbase = [&](int ks) {
-        return ks < KS ? wl + (jb.j * Cin + ks * E::kstep) * WROW : zrows;
+        return ks < KS ? wl + (jb.j * Cin + ks * E::kstep) * WROWW : zrows;
       };
       if constexpr (KSM * NCB <= 8) {  // all of the job's B fragments: <= 32 VGPRs
         bf16x8 bfr[KSM][NCB];
@@ -486,13 +511,13 @@ __global__ __launch_bounds__(kThreads, 1) void ws_kernel(GemmArgs a, int R) {
 #pragma unroll
       for (int ks = 0; ks < KSM; ++ks) {
         const unsigned char* base =
-            ks < KS ? wl + (jb.j * Cin + ks * E::kstep) * WROW : zrows;
+            ks < KS ? wl + (jb.j * Cin + ks * E::kstep) * WROWW : zrows;
         float bw[NCB][4];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
           for (int s2 = 0; s2 < 4; ++s2)
-            bw[cb][s2] = *reinterpret_cast<const float*>(base + (4 * g + s2) * WROW +
+            bw[cb][s2] = *reinterpret_cast<const float*>(base + (4 * g + s2) * WROWW +
                                                          (cb * 16 + l16) * 4);
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
@@ -585,7 +610,8 @@ hipError_t launch_ws(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) {
                                    hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit);
   });
   if (attr_err != hipSuccess) return attr_err;
-  hipLaunchKernelGGL(kern, dim3(gx, gy), dim3(kThreads), (size_t)pl.total, stream, a, pl.rows);
+  hipLaunchKernelGGL(kern, dim3(gx, gy), dim3(CONV ? kThreadsConv : kThreadsLin), (size_t)pl.total,
+                     stream, a, pl.rows);
   return hipGetLastError();
 }
 
@@ -609,6 +635,8 @@ hipError_t launch_ws_k(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) 
 
 // Plan for the weight-stationary kernel, or false when the shape does not fit.
 bool ws_plan(const GemmArgs& a, bool conv, bool bf16, int num_cus, WsPlan* pl) {
+  const int nt = conv ? kThreadsConv : kThreadsLin;
+  const int waves = nt / 64, rpt = kMaxRows / nt;
   const int e = bf16 ? 2 : 4;
   const int K = conv ? a.K : 1;
   const int Ktot = K * a.Cin;
@@ -626,15 +654,15 @@ bool ws_plan(const GemmArgs& a, bool conv, bool bf16, int num_cus, WsPlan* pl) {
   int ws = 0;
   for (int cand : {128, 64, 32}) {
     if (cand > ((a.Cout + 15) / 16) * 16 && cand != 32) continue;
-    const int wb = ((Ktot * ws_wrow(cand, e) + 15) & ~15);
-    if (wb + ws_scratch(cand, e) + ws_idx_bytes(256, K) <= kLdsLimit) {
+    const int wb = ((Ktot * ws_wrow_w(cand, e) + 15) & ~15);
+    if (wb + ws_scratch(cand, e, waves) + ws_idx_bytes(256, K, waves, rpt) <= kLdsLimit) {
       ws = cand;
       break;
     }
   }
   if (ws == 0) return false;
   const int slices = (a.Cout + ws - 1) / ws;
-  const int wb = (Ktot * ws_wrow(ws, e) + 15) & ~15;
+  const int wb = (Ktot * ws_wrow_w(ws, e) + 15) & ~15;
   // rows per workgroup: one workgroup per CU when the rows fit, within LDS
   int64_t target = (a.n_rows * slices + num_cus - 1) / num_cus;
   // Beyond one wave of workgroups the tiled kernel is faster for the conv
@@ -644,14 +672,14 @@ bool ws_plan(const GemmArgs& a, bool conv, bool bf16, int num_cus, WsPlan* pl) {
   int rows = (int)((target + 15) / 16) * 16;
   if (rows < 64) rows = 64;
   if (rows > kMaxRows) rows = kMaxRows;
-  while (rows > 64 && wb + ws_scratch(ws, e) + ws_idx_bytes(rows, K) > kLdsLimit) rows -= 16;
-  if (wb + ws_scratch(ws, e) + ws_idx_bytes(rows, K) > kLdsLimit) return false;
+  while (rows > 64 && wb + ws_scratch(ws, e, waves) + ws_idx_bytes(rows, K, waves, rpt) > kLdsLimit) rows -= 16;
+  if (wb + ws_scratch(ws, e, waves) + ws_idx_bytes(rows, K, waves, rpt) > kLdsLimit) return false;
   pl->ws = ws;
-  pl->wrow = ws_wrow(ws, e);
+  pl->wrow = ws_wrow_w(ws, e);
   pl->wbytes = wb;
   pl->rows = rows;
-  pl->idx_bytes = ws_idx_bytes(rows, K);
-  pl->scratch = ws_scratch(ws, e);
+  pl->idx_bytes = ws_idx_bytes(rows, K, waves, rpt);
+  pl->scratch = ws_scratch(ws, e, waves);
   pl->total = wb + pl->idx_bytes + pl->scratch;
   return true;
 }
