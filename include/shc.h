@@ -131,6 +131,23 @@ int shc_sparse_linear(const void* S, int64_t n_rows, const void* W, const float*
                       int32_t Cout, int32_t dtype, int32_t act, void* out, hipStream_t stream);
 
 /*
+ * Gather fused into the sparse linear layer -- Eq. 2 then Eq. 6 (+ Eq. 10):
+ *
+ *   out[i] = act(x[b_i * V + v_i] W + bias)
+ *
+ * the result of shc_gather_rows followed by shc_sparse_linear (bit for bit
+ * when both calls take the same kernel), without writing the gathered rows.
+ *   x       [B*V][Cin] dense per-vertex features; coords [n_rows][2] from
+ *           shc_compact_mask (a coordinate outside [0,B)x[0,V) reads zeros).
+ *   W, bias, out, act as for shc_sparse_linear; out must not overlap x.
+ * n_rows = 0 is a no-op.
+ */
+int shc_gather_sparse_linear(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
+                             int32_t V, const void* W, const float* bias, int32_t Cin,
+                             int32_t Cout, int32_t dtype, int32_t act, void* out,
+                             hipStream_t stream);
+
+/*
  * Sparse neighbourhood (spiral / k-NN) convolution -- Eqs. 4-5 (+ Eq. 10),
  * output only at the active rows:
  *

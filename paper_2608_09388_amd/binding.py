@@ -46,6 +46,9 @@ _SIGS = {
                                        _c_ptr, _c_ptr]),
     "shc_sparse_linear": (ctypes.c_int, [_c_ptr, _c_i64, _c_ptr, _c_ptr, _c_i32, _c_i32, _c_i32,
                                          _c_i32, _c_ptr, _c_ptr]),
+    "shc_gather_sparse_linear": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_ptr,
+                                                _c_ptr, _c_i32, _c_i32, _c_i32, _c_i32, _c_ptr,
+                                                _c_ptr]),
     "shc_sparse_neighbor_conv": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32,
                                                 _c_ptr, _c_i32, _c_ptr, _c_ptr, _c_i32, _c_i32,
                                                 _c_i32, _c_i32, _c_ptr, _c_ptr]),
@@ -189,6 +192,19 @@ def sparse_linear(S: torch.Tensor, n_rows: int, W: torch.Tensor, bias: Optional[
     _check(load().shc_sparse_linear(*args), "shc_sparse_linear")
 
 
+def gather_sparse_linear(x: torch.Tensor, coords: torch.Tensor, n_rows: int, B: int, V: int,
+                         W: torch.Tensor, bias: Optional[torch.Tensor], out: torch.Tensor,
+                         act: int = SHC_ACT_RELU, stream=None):
+    """shc_gather_sparse_linear: out[i] = act(x[b_i * V + v_i] W + bias)."""
+    Cin, Cout = W.shape
+    dt = _dtype_code(x)
+    args = [_dev(x, "x", x.dtype, B * V * Cin), _dev(coords, "coords", torch.int32, 2 * n_rows),
+            n_rows, B, V, _dev(W, "W", x.dtype, Cin * Cout),
+            _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, dt, act,
+            _dev(out, "out", x.dtype, n_rows * Cout), _stream(stream)]
+    _check(load().shc_gather_sparse_linear(*args), "shc_gather_sparse_linear")
+
+
 def sparse_neighbor_conv(S: torch.Tensor, coords: torch.Tensor, inv: torch.Tensor, n_rows: int,
                          B: int, V: int, nbr: torch.Tensor, W: torch.Tensor,
                          bias: Optional[torch.Tensor], out: torch.Tensor,
@@ -322,6 +338,16 @@ def prepare_sparse_linear(S, W, bias, out, act=SHC_ACT_RELU, stream=None) -> Pre
             _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, _dtype_code(S), act,
             _dev(out, "out", S.dtype), _stream(stream)]
     return Prepared("shc_sparse_linear", args, 1, n_max, (S, W, bias, out))
+
+
+def prepare_gather_sparse_linear(x, coords, B, V, W, bias, out, act=SHC_ACT_RELU,
+                                 stream=None) -> Prepared:
+    Cin, Cout = W.shape
+    n_max = min(coords.numel() // 2, out.numel() // Cout)
+    args = [_dev(x, "x", x.dtype, B * V * Cin), _dev(coords, "coords", torch.int32), 0, B, V,
+            _dev(W, "W", x.dtype, Cin * Cout), _opt_dev(bias, "bias", torch.float32, Cout),
+            Cin, Cout, _dtype_code(x), act, _dev(out, "out", x.dtype), _stream(stream)]
+    return Prepared("shc_gather_sparse_linear", args, 2, n_max, (x, coords, W, bias, out))
 
 
 def prepare_sparse_neighbor_conv(S, coords, inv, B, V, nbr, W, bias, out, act=SHC_ACT_RELU,

@@ -218,6 +218,42 @@ int shc_sparse_linear(const void* S, int64_t n_rows, const void* W, const float*
                     "sparse_linear launch");
 }
 
+int shc_gather_sparse_linear(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
+                             int32_t V, const void* W, const float* bias, int32_t Cin,
+                             int32_t Cout, int32_t dtype, int32_t act, void* out,
+                             hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("Cin", Cin));
+  SHC_TRY(check_channels("Cout", Cout));
+  if (act != SHC_ACT_NONE && act != SHC_ACT_RELU)
+    return fail(SHC_ERR_UNSUPPORTED, "unknown activation code %d", act);
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(x, "x");
+  SHC_PTR(coords, "coords");
+  SHC_PTR(W, "W");
+  SHC_OPT_PTR(bias, "bias");
+  SHC_PTR(out, "out");
+  shc::GemmArgs a{};
+  a.S = x;
+  a.coords = coords;
+  a.W = W;
+  a.bias = bias;
+  a.out = out;
+  a.n_rows = n_rows;
+  a.B = B;
+  a.V = V;
+  a.K = 1;
+  a.Cin = Cin;
+  a.Cout = Cout;
+  a.relu = act == SHC_ACT_RELU;
+  a.gather = 1;
+  return hip_status(shc::launch_gather_gemm(a, false, dtype == SHC_BF16, stream),
+                    "gather_sparse_linear launch");
+}
+
 int shc_sparse_neighbor_conv(const void* S, const int32_t* coords, const int32_t* inv,
                              int64_t n_rows, int32_t B, int32_t V, const int32_t* nbr, int32_t K,
                              const void* W, const float* bias, int32_t Cin, int32_t Cout,

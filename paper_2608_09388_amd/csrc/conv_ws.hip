@@ -333,9 +333,24 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
       store_w(base, wv);
     }
     __syncthreads();
-    for (int t = tid; t < R; t += kThreads) {
-      srcs[t] = t < nrows ? (int32_t)(row0 + t) : -1;
-      perm[t] = t;
+    // input rows: row i itself, or (gather) row b_i * V + v_i of the dense
+    // tensor; every coordinate load of the thread is issued before any is used
+    int2 cr[kRPT];
+#pragma unroll
+    for (int rr = 0; rr < kRPT; ++rr) {
+      const int t = tid + rr * kThreads;
+      cr[rr] = a.gather ? reinterpret_cast<const int2*>(a.coords)[row0 + (t < nrows ? t : 0)]
+                        : int2{0, 0};
+    }
+#pragma unroll
+    for (int rr = 0; rr < kRPT; ++rr) {
+      const int t = tid + rr * kThreads;
+      if (t < R) {
+        const int2 c = cr[rr];
+        const bool ok = c.x >= 0 && c.x < a.B && c.y >= 0 && c.y < a.V;
+        srcs[t] = t >= nrows ? -1 : (!a.gather ? (int32_t)(row0 + t) : (ok ? c.x * a.V + c.y : -1));
+        perm[t] = t;
+      }
     }
     for (int q = tid; q < R / 16; q += kThreads) blkmask[q] = (16 * q < nrows) ? 1u : 0u;
   }
@@ -411,8 +426,9 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   // A fragments come through raw buffer loads with 32-bit offsets: an absent
   // row (or a k-step past Cin) gets an offset beyond the buffer, and the
   // hardware returns zeros without touching memory.
+  const int64_t s_rows = a.gather ? (int64_t)a.B * a.V : a.n_rows;  // rows of the input
   const __amdgpu_buffer_rsrc_t s_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<void*>(a.S), (short)0, (int)(a.n_rows * Cin * E::bytes), kBufferWord3);
+      const_cast<void*>(a.S), (short)0, (int)(s_rows * Cin * E::bytes), kBufferWord3);
   const uint32_t row_bytes = (uint32_t)Cin * E::bytes;
   struct Frags {
     i32x4 v[KSM];
@@ -645,7 +661,7 @@ bool ws_plan(const GemmArgs& a, bool conv, bool bf16, int num_cus, WsPlan* pl) {
   if (a.Cin / kstep > 8) return false;       // at most 8 k-steps per slot job
   if (conv && K > 10) return false;          // index build keeps <= 10 slots per row
   // 32-bit buffer offsets, with kOutOfRange past the end of every buffer
-  if ((int64_t)a.n_rows * a.Cin * e > 0x7FFF0000LL) return false;
+  if ((a.gather ? (int64_t)a.B * a.V : a.n_rows) * a.Cin * e > 0x7FFF0000LL) return false;
   if ((int64_t)a.n_rows * a.Cout * e > 0x7FFF0000LL) return false;
   // sparse inputs only: at high density the tiled kernel (gemm.hip) is faster
   // than building the index lists here (with a prebuilt table there is none)

@@ -285,9 +285,16 @@ __global__ __launch_bounds__(kThreads, 2) void gather_gemm_kernel(GemmArgs a) {
     __syncthreads();
     if (tid < BM) {
       const int64_t i = row0 + tid;
-      srcs[tid] = i < a.n_rows ? (int32_t)i : -1;
+      const bool in = i < a.n_rows;
+      int32_t src = in ? (int32_t)i : -1;
+      if (a.gather) {  // input row b_i * V + v_i of the dense tensor
+        const int2 c = reinterpret_cast<const int2*>(a.coords)[in ? i : 0];
+        const bool ok = in && c.x >= 0 && c.x < a.B && c.y >= 0 && c.y < a.V;
+        src = ok ? c.x * a.V + c.y : -1;
+      }
+      srcs[tid] = src;
       perm[tid] = tid;
-      if (i < a.n_rows) atomicOr(&blk_slots[tid >> 4], 1u);
+      if (in) atomicOr(&blk_slots[tid >> 4], 1u);
     }
   }
   __syncthreads();

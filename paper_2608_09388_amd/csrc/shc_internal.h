@@ -75,6 +75,7 @@ struct GemmArgs {
   int64_t n_rows;
   int32_t B, V, K, Cin, Cout;
   int32_t relu;
+  int32_t gather;       // linear only: input row i is S[coords b_i * V + v_i] (S = dense x)
   uint32_t cin_magic;   // ceil(2^32 / Cin), filled in by the launcher
 };
 

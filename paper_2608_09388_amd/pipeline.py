@@ -9,6 +9,9 @@ as a sequence of library calls:
     (shc_sparse_linear | shc_sparse_neighbor_conv_table) per layer ->
     shc_scatter / shc_segment_maxpool
 
+with the gather fused into the first layer (shc_gather_sparse_linear) when
+that layer is linear.
+
 The active set never changes across layers (C'_k = C_k, Sec. 3.2), so the
 active count is read back once per mask and passed to every layer call.
 This module only moves buffers and issues calls; all arithmetic runs in the
@@ -71,6 +74,9 @@ class SparseStack:
         B, V = self.B, self.V
         self._compact = shc.PreparedCompact(self.mask, B, V, self.coords, self.inv, self.row_ptr,
                                             self.n_active, self.ws)
+        # A first linear layer reads its rows straight from x (gather fused in);
+        # otherwise the active rows are gathered into acts[0] first.
+        self.fused_gather = len(w.layers) > 0 and w.layers[0].kind == "linear"
         self._gather = shc.prepare_gather_rows(self.x, self.coords, B, V, self.acts[0])
         self._table = (shc.prepare_build_neighbor_table(self.coords, self.inv, B, V, self.nbr,
                                                         self.table)
@@ -82,6 +88,9 @@ class SparseStack:
             if spec.kind == "conv":
                 call = shc.prepare_sparse_neighbor_conv_table(src, self.table, self.weights[l],
                                                               self.biases[l], dst, a)
+            elif l == 0 and self.fused_gather:
+                call = shc.prepare_gather_sparse_linear(self.x, self.coords, B, V,
+                                                        self.weights[l], self.biases[l], dst, a)
             else:
                 call = shc.prepare_sparse_linear(src, self.weights[l], self.biases[l], dst, a)
             self._layers.append(call)
@@ -102,6 +111,8 @@ class SparseStack:
         return self.n
 
     def gather(self):
+        """Gather the active rows into acts[0] (not needed by the step when
+        the first layer fuses the gather)."""
         self._gather(self.n)
 
     def layer(self, l: int):
@@ -122,7 +133,8 @@ class SparseStack:
     def step(self) -> int:
         """One pass of the whole path over the workload's batch."""
         self.compact()
-        self.gather()
+        if not self.fused_gather:
+            self.gather()
         for call in self._layers:
             call(self.n)
         self.finish()

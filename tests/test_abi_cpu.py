@@ -120,6 +120,25 @@ def test_layer_validation(lib):
     assert conv(out=None) == -1
 
 
+def test_gather_sparse_linear_validation(lib):
+    G = lib.shc_gather_sparse_linear
+
+    def call(**kw):
+        a = dict(x=A, coords=A, n=10, B=4, V=655, W=A, bias=None, Cin=128, Cout=128, dt=1, act=1,
+                 out=A)
+        a.update(kw)
+        return G(a["x"], a["coords"], a["n"], a["B"], a["V"], a["W"], a["bias"], a["Cin"],
+                 a["Cout"], a["dt"], a["act"], a["out"], None)
+
+    assert call(coords=None) == -1 and "coords" in err(lib)
+    assert call(x=MIS) == -3
+    assert call(B=0) == -1
+    assert call(Cin=40) == -4
+    assert call(act=9) == -4
+    assert call(n=-2) == -1
+    assert call(n=0, x=None, coords=None, W=None, out=None) == 0
+
+
 def test_neighbor_table_validation(lib):
     T = lib.shc_build_neighbor_table
 
