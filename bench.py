@@ -132,7 +132,7 @@ def kernel_times(st, shc, torch, reps):
         shc.compact_mask(st.mask, st.B, st.V, st.coords, st.inv, st.row_ptr, st.n_active, st.ws,
                          want_host_count=False)
 
-    calls = {"compact": (compact_async, main), "table": (lambda: st._table(n), main),
+    calls = {"compact": (compact_async, main), "table": (st.build_table, main),
              "gather": (st.gather, main),
              ("gather+linear" if st.fused_gather else "linear"): (lambda: st.layer(0), main),
              "conv": (lambda: st.layer(1), main), "scatter": (st.scatter, main),
@@ -191,25 +191,17 @@ def main():
     L = len(w.layers)
     stream = torch.cuda.current_stream()
 
-    for _ in range(args.warmup):
-        st.step()
+    st.run(args.warmup)
     torch.cuda.synchronize()
 
-    # timed region: K whole steps; HIP events around the conv launch of each
-    # step, on the stream it runs on
+    # timed region: K whole steps over consecutive batches (each step's
+    # compaction overlapped with the previous step's scatter and pool); HIP
+    # events around the conv launch of each step, on the stream it runs on
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for s in range(args.steps):
-        st.compact()
-        if not st.fused_gather:
-            st.gather()
-        st.layer(0)
-        ev[s][0].record(stream)
-        st.layer(1)
-        ev[s][1].record(stream)
-        st.finish()
+    st.run(args.steps, around_layer=(1, ev))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps

@@ -108,6 +108,27 @@ int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
                      void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * shc_compact_mask in two halves, for a caller with work to enqueue before it
+ * needs N' (work that reads only inv, such as shc_clear_inactive_rows):
+ *
+ * shc_compact_mask_start -- the same compaction, launched on `stream` without
+ *   waiting.  n_active_host must lie in page-locked host memory mapped into
+ *   the device (hipHostMalloc), else SHC_ERR_INVALID_ARG: the call stores -1
+ *   there and the kernel stores N' as soon as it is known.  Other arguments
+ *   and outputs as for shc_compact_mask.
+ * shc_compact_mask_wait -- waits until that count has arrived in
+ *   *n_active_host (leaving it there); SHC_ERR_CAPACITY if N' > cap (the cap
+ *   given to the start call), SHC_ERR_HIP if the stream fails or drains
+ *   without a count.  The other outputs may still be being written; work
+ *   enqueued on the stream is ordered after them.
+ */
+int shc_compact_mask_start(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
+                           int32_t* inv, int32_t* row_ptr, int32_t* n_active_dev,
+                           int64_t* n_active_host, int64_t cap, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+int shc_compact_mask_wait(int64_t* n_active_host, int64_t cap, hipStream_t stream);
+
+/*
  * Gather of the active feature rows -- S' of Eq. 2: S[i] = x[b_i * V + v_i].
  *
  *   x       [B*V][C] dense per-vertex features.
@@ -219,6 +240,20 @@ int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t 
 int shc_scatter(const void* S, const int32_t* inv, const int32_t* coords, int64_t n_rows,
                 int32_t B, int32_t V, int32_t C, int32_t dtype, int32_t zero_fill, void* D,
                 hipStream_t stream);
+
+/*
+ * The zeros of the zero-filled scatter (D = y (.) m, Sec. 3.2), which need
+ * only the inverse map:
+ *
+ *   D[r] = 0 for every r < B*V with inv[r] < 0; the other rows untouched.
+ *
+ * Followed by shc_scatter with zero_fill = 0 this gives shc_scatter's
+ * zero_fill = 1 result for a consistent compaction (inv and coords from the
+ * same shc_compact_mask, N' <= cap), and it can run before N' is known.
+ *   inv [B*V] int32, D [B*V][C] of `dtype`.
+ */
+int shc_clear_inactive_rows(const int32_t* inv, int32_t B, int32_t V, int32_t C, int32_t dtype,
+                            void* D, hipStream_t stream);
 
 /*
  * Segmented max-pool per body/frame -- the sparse pooling layer (Sec. 3.2):

@@ -42,6 +42,11 @@ _SIGS = {
     "shc_compact_mask_workspace": (_c_sz, [_c_i32, _c_i32]),
     "shc_compact_mask": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                         _c_ptr, _c_i64, _c_ptr, _c_sz, _c_ptr]),
+    "shc_compact_mask_start": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr,
+                                              _c_ptr, _c_ptr, _c_i64, _c_ptr, _c_sz, _c_ptr]),
+    "shc_compact_mask_wait": (ctypes.c_int, [_c_ptr, _c_i64, _c_ptr]),
+    "shc_clear_inactive_rows": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_i32, _c_i32, _c_ptr,
+                                               _c_ptr]),
     "shc_gather_rows": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
                                        _c_ptr, _c_ptr]),
     "shc_sparse_linear": (ctypes.c_int, [_c_ptr, _c_i64, _c_ptr, _c_ptr, _c_i32, _c_i32, _c_i32,
@@ -256,6 +261,35 @@ def scatter(S: torch.Tensor, inv: torch.Tensor, coords: torch.Tensor, n_rows: in
     _check(load().shc_scatter(*args), "shc_scatter")
 
 
+def compact_mask_start(mask: torch.Tensor, B: int, V: int, coords: torch.Tensor,
+                       inv: torch.Tensor, row_ptr: torch.Tensor, n_active: torch.Tensor,
+                       ws: torch.Tensor, host_count: torch.Tensor, stream=None):
+    """shc_compact_mask_start: launch only; ``host_count`` is a pinned CPU int64
+    tensor that receives N' (read it after ``compact_mask_wait``)."""
+    cap = coords.numel() // 2
+    args = [_dev(mask, "mask", torch.uint8, B * V), B, V,
+            _dev(coords, "coords", torch.int32) if cap > 0 else None,
+            _dev(inv, "inv", torch.int32, B * V), _dev(row_ptr, "row_ptr", torch.int32, B + 1),
+            _dev(n_active, "n_active", torch.int32, 1), _host_count_ptr(host_count), cap,
+            _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)]
+    _check(load().shc_compact_mask_start(*args), "shc_compact_mask_start")
+
+
+def compact_mask_wait(host_count: torch.Tensor, cap: int, stream=None) -> int:
+    """shc_compact_mask_wait: N' once it has arrived in ``host_count``."""
+    _check(load().shc_compact_mask_wait(_host_count_ptr(host_count), cap, _stream(stream)),
+           "shc_compact_mask_wait")
+    return int(host_count[0])
+
+
+def clear_inactive_rows(inv: torch.Tensor, B: int, V: int, D: torch.Tensor, stream=None):
+    """shc_clear_inactive_rows: D[r] = 0 wherever inv[r] < 0, other rows untouched."""
+    C = D.shape[-1]
+    args = [_dev(inv, "inv", torch.int32, B * V), B, V, C, _dtype_code(D),
+            _dev(D, "D", D.dtype, B * V * C), _stream(stream)]
+    _check(load().shc_clear_inactive_rows(*args), "shc_clear_inactive_rows")
+
+
 def segment_maxpool(S: torch.Tensor, row_ptr: torch.Tensor, n_rows: int, B: int,
                     P: torch.Tensor, empty_value: float = 0.0, stream=None):
     """shc_segment_maxpool: P [B][C] = per-body max of the active rows."""
@@ -303,7 +337,12 @@ class Prepared:
 
 
 class PreparedCompact:
-    """shc_compact_mask with a pinned host count; calling it returns N'."""
+    """shc_compact_mask with a pinned host count; calling it returns N'.
+
+    ``start()`` and ``wait()`` are the two halves (shc_compact_mask_start /
+    shc_compact_mask_wait): work that needs only ``inv`` can be enqueued
+    between them, while the count is on its way.
+    """
 
     def __init__(self, mask, B, V, coords, inv, row_ptr, n_active, ws, stream=None):
         self.host = torch.zeros(1, dtype=torch.int64, pin_memory=True)
@@ -315,11 +354,21 @@ class PreparedCompact:
                 _dev(row_ptr, "row_ptr", torch.int32, B + 1),
                 _dev(n_active, "n_active", torch.int32, 1), self.host.data_ptr(), cap,
                 _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)]
-        self._call = Prepared("shc_compact_mask", args, None, 0,
-                              (mask, coords, inv, row_ptr, n_active, ws, self.host))
+        keep = (mask, coords, inv, row_ptr, n_active, ws, self.host)
+        self._call = Prepared("shc_compact_mask", args, None, 0, keep)
+        self._start = Prepared("shc_compact_mask_start", args, None, 0, keep)
+        self._wait = Prepared("shc_compact_mask_wait", [self.host.data_ptr(), cap, args[-1]],
+                              None, 0, keep)
 
     def __call__(self) -> int:
         self._call()
+        return int(self._host_view[0])
+
+    def start(self):
+        self._start()
+
+    def wait(self) -> int:
+        self._wait()
         return int(self._host_view[0])
 
 
@@ -389,6 +438,13 @@ def prepare_scatter(S, inv, coords, B, V, D, zero_fill=True, stream=None) -> Pre
             _dtype_code(D), 1 if zero_fill else 0, _dev(D, "D", D.dtype, B * V * C),
             _stream(stream)]
     return Prepared("shc_scatter", args, 3, n_max, (S, inv, coords, D))
+
+
+def prepare_clear_inactive_rows(inv, B, V, D, stream=None) -> Prepared:
+    C = D.shape[-1]
+    args = [_dev(inv, "inv", torch.int32, B * V), B, V, C, _dtype_code(D),
+            _dev(D, "D", D.dtype, B * V * C), _stream(stream)]
+    return Prepared("shc_clear_inactive_rows", args, None, 0, (inv, D))
 
 
 def prepare_segment_maxpool(S, row_ptr, B, P, empty_value=0.0, stream=None) -> Prepared:

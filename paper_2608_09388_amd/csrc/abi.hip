@@ -114,10 +114,16 @@ static int64_t* mapped_host_count(int64_t* host) {
   return static_cast<int64_t*>(attr.devicePointer);
 }
 
-int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
-                     int32_t* row_ptr, int32_t* n_active_dev, int64_t* n_active_host, int64_t cap,
-                     void* ws, size_t ws_bytes, hipStream_t stream) {
-  g_last_error[0] = 0;
+// Validation and launch shared by shc_compact_mask and shc_compact_mask_start.
+// *mapped receives the device address of a page-locked host count, or null
+// (no host count, or pageable memory: refused when require_mapped).
+static int compact_launch(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
+                          int32_t* row_ptr, int32_t* n_active_dev, int64_t* n_active_host,
+                          bool require_mapped, int64_t** mapped_out, int64_t cap, void* ws,
+                          size_t ws_bytes, hipStream_t stream) {
+  *mapped_out = nullptr;
+  if (require_mapped && n_active_host == nullptr)
+    return fail(SHC_ERR_INVALID_ARG, "n_active_host is NULL");
   SHC_TRY(check_bv(B, V));
   SHC_PTR(mask, "mask");
   SHC_PTR(inv, "inv");
@@ -130,44 +136,74 @@ int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
   if (ws_bytes < need)
     return fail(SHC_ERR_CAPACITY, "workspace of %zu bytes is below the %zu needed", ws_bytes, need);
   int64_t* mapped = n_active_host ? mapped_host_count(n_active_host) : nullptr;
+  if (require_mapped && mapped == nullptr)
+    return fail(SHC_ERR_INVALID_ARG, "n_active_host is not page-locked host memory mapped "
+                                     "into the device");
+  *mapped_out = mapped;
+  if (mapped != nullptr) *reinterpret_cast<volatile int64_t*>(n_active_host) = -1;  // set by the kernel
+  return hip_status(shc::launch_compact(mask, B, V, coords, inv, row_ptr, n_active_dev, mapped,
+                                        cap, static_cast<int32_t*>(ws), stream),
+                    "compact_mask launch");
+}
+
+int shc_compact_mask_start(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
+                           int32_t* inv, int32_t* row_ptr, int32_t* n_active_dev,
+                           int64_t* n_active_host, int64_t cap, void* ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  g_last_error[0] = 0;
+  int64_t* mapped = nullptr;
+  return compact_launch(mask, B, V, coords, inv, row_ptr, n_active_dev, n_active_host, true,
+                        &mapped, cap, ws, ws_bytes, stream);
+}
+
+int shc_compact_mask_wait(int64_t* n_active_host, int64_t cap, hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (n_active_host == nullptr) return fail(SHC_ERR_INVALID_ARG, "n_active_host is NULL");
+  // The compaction stores N' into the page-locked variable as soon as it is
+  // known; poll it rather than waiting for the whole stream (later work on
+  // the stream is ordered after the compaction anyway).  Every few thousand
+  // polls the stream is queried, so a failed launch or a stream that drains
+  // without a count ends the wait.
   volatile int64_t* host_count = n_active_host;
-  if (mapped != nullptr) *host_count = -1;  // set by the kernel once N' is known
-  int rc = hip_status(shc::launch_compact(mask, B, V, coords, inv, row_ptr, n_active_dev, mapped,
-                                          cap, static_cast<int32_t*>(ws), stream),
-                      "compact_mask launch");
-  if (rc != SHC_OK || n_active_host == nullptr) return rc;
   int64_t n = 0;
-  if (mapped == nullptr) {
-    int32_t n32 = 0;
-    rc = hip_status(
-        hipMemcpyAsync(&n32, n_active_dev, sizeof(int32_t), hipMemcpyDeviceToHost, stream),
-        "compact_mask count copy");
-    if (rc != SHC_OK) return rc;
-    rc = hip_status(hipStreamSynchronize(stream), "compact_mask stream sync");
-    if (rc != SHC_OK) return rc;
-    n = n32;
-  } else {
-    // The last block stores the final N' into the page-locked variable; poll
-    // it rather than waiting for the whole stream (later work on the stream
-    // is ordered after the compaction anyway).  Every few thousand polls the
-    // stream is queried, so a failed launch or a finished stream ends the wait.
-    for (uint64_t it = 1;; ++it) {
-      n = *host_count;
-      if (n >= 0) break;
-      if ((it & 4095u) == 0) {
-        const hipError_t q = hipStreamQuery(stream);
-        if (q == hipSuccess) {
-          n = *host_count;
-          if (n < 0) return fail(SHC_ERR_HIP, "compact_mask: stream finished without a count");
-          break;
-        }
-        if (q != hipErrorNotReady) return hip_status(q, "compact_mask stream query");
+  for (uint64_t it = 1;; ++it) {
+    n = *host_count;
+    if (n >= 0) break;
+    if ((it & 4095u) == 0) {
+      const hipError_t q = hipStreamQuery(stream);
+      if (q == hipSuccess) {
+        n = *host_count;
+        if (n < 0) return fail(SHC_ERR_HIP, "compact_mask: stream finished without a count");
+        break;
       }
+      if (q != hipErrorNotReady) return hip_status(q, "compact_mask stream query");
     }
   }
-  *n_active_host = n;
   if (n > cap)
     return fail(SHC_ERR_CAPACITY, "N' = %lld active rows exceed cap = %lld", (long long)n,
+                (long long)cap);
+  return SHC_OK;
+}
+
+int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
+                     int32_t* row_ptr, int32_t* n_active_dev, int64_t* n_active_host, int64_t cap,
+                     void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  int64_t* mapped = nullptr;
+  int rc = compact_launch(mask, B, V, coords, inv, row_ptr, n_active_dev, n_active_host, false,
+                          &mapped, cap, ws, ws_bytes, stream);
+  if (rc != SHC_OK || n_active_host == nullptr) return rc;
+  if (mapped != nullptr) return shc_compact_mask_wait(n_active_host, cap, stream);
+  // pageable host memory: a copy and a full stream synchronisation
+  int32_t n32 = 0;
+  rc = hip_status(hipMemcpyAsync(&n32, n_active_dev, sizeof(int32_t), hipMemcpyDeviceToHost, stream),
+                  "compact_mask count copy");
+  if (rc != SHC_OK) return rc;
+  rc = hip_status(hipStreamSynchronize(stream), "compact_mask stream sync");
+  if (rc != SHC_OK) return rc;
+  *n_active_host = n32;
+  if (n32 > cap)
+    return fail(SHC_ERR_CAPACITY, "N' = %lld active rows exceed cap = %lld", (long long)n32,
                 (long long)cap);
   return SHC_OK;
 }
@@ -371,6 +407,19 @@ int shc_scatter(const void* S, const int32_t* inv, const int32_t* coords, int64_
   return hip_status(
       shc::launch_scatter(S, inv, coords, n_rows, B, V, row_bytes, zero_fill, D, stream),
       "scatter launch");
+}
+
+int shc_clear_inactive_rows(const int32_t* inv, int32_t B, int32_t V, int32_t C, int32_t dtype,
+                            void* D, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("C", C));
+  SHC_PTR(inv, "inv");
+  SHC_PTR(D, "D");
+  const int32_t row_bytes = C * (dtype == SHC_BF16 ? 2 : 4);
+  return hip_status(shc::launch_clear_inactive(inv, B, V, row_bytes, D, stream),
+                    "clear_inactive_rows launch");
 }
 
 int shc_segment_maxpool(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,

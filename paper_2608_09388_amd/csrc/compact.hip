@@ -4,8 +4,11 @@
 //
 // Two launches over the flattened mask of B*V bytes:
 //   1. count   -- every block counts the non-zero bytes of its span;
-//   2. write   -- every block sums the counts of the blocks before it, then
-//                 walks its span in chunks of 4096 entries.  Inside a chunk a
+//   2. write   -- every block sums the counts of the blocks before it (block
+//                 0 sums them all and publishes N' -- row_ptr[B], the device
+//                 and the host count -- before writing anything else, so a
+//                 host waiting for the count wakes while the lists are still
+//                 being written), then walks its span in chunks of 4096 entries.  Inside a chunk a
 //                 thread owns four 4-byte groups (one per 1024-entry
 //                 sub-chunk, so each load and each int4 store of `inv` is
 //                 contiguous across the wavefront); the four per-thread counts
@@ -96,10 +99,20 @@ __global__ __launch_bounds__(kThreads) void compact_write_kernel(
   const int lane = tid & 63;
   const int wave = tid >> 6;
 
-  // rows taken by the blocks before this one
+  // rows taken by the blocks before this one (block 0: by every block, N')
+  const int upto = blockIdx.x == 0 ? (int)gridDim.x : (int)blockIdx.x;
   uint32_t before = 0;
-  for (int q = tid; q < (int)blockIdx.x; q += kThreads) before += (uint32_t)counts[q];
+  for (int q = tid; q < upto; q += kThreads) before += (uint32_t)counts[q];
   int64_t base = block_sum(before, red);
+  if (blockIdx.x == 0) {
+    if (tid == 0) {
+      row_ptr[B] = (int32_t)base;
+      *n_active = (int32_t)base;
+      // page-locked host copy of the count: a system-scope store
+      if (n_host != nullptr) __hip_atomic_store(n_host, base, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+    base = 0;
+  }
 
   const int64_t start = (int64_t)blockIdx.x * per_block;
   const int64_t end = min(start + per_block, total);
@@ -170,13 +183,6 @@ __global__ __launch_bounds__(kThreads) void compact_write_kernel(
       sub_base += tot[k];
     }
     base = sub_base;
-  }
-  if (blockIdx.x == gridDim.x - 1 && tid == 0) {
-    row_ptr[B] = (int32_t)base;
-    *n_active = (int32_t)base;
-    // page-locked host copy of the count: a system-scope store reaches host
-    // memory before the kernel's completion is signalled
-    if (n_host != nullptr) __hip_atomic_store(n_host, base, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
 }
 

@@ -61,7 +61,11 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const i32x4* __restric
   }
 }
 
-// D[r] = S[inv[r]] or zeros, for every dense row r.
+// D[r] = S[inv[r]] or zeros, for every dense row r (COPY); or (!COPY) zeros
+// for the rows with inv[r] < 0 only, the others untouched and S unused.  One
+// block of ty rows each, dispatched in row order, so the chip writes one
+// moving window of the output.
+template <bool COPY>
 __global__ __launch_bounds__(kThreads) void scatter_fill_kernel(const i32x4* __restrict__ S,
                                                                 const int32_t* __restrict__ inv,
                                                                 int64_t n_dense, int64_t n_rows,
@@ -69,7 +73,8 @@ __global__ __launch_bounds__(kThreads) void scatter_fill_kernel(const i32x4* __r
   const int64_t r = (int64_t)blockIdx.x * blockDim.y + threadIdx.y;
   if (r >= n_dense) return;
   const int32_t s = inv[r];
-  const bool ok = s >= 0 && s < n_rows;
+  if (!COPY && s >= 0) return;
+  const bool ok = COPY && s >= 0 && s < n_rows;
   const i32x4* src = S + (int64_t)s * vpr;
   i32x4* dst = D + r * vpr;
   for (int q = threadIdx.x; q < vpr; q += blockDim.x) {
@@ -215,8 +220,8 @@ hipError_t launch_scatter(const void* S, const int32_t* inv, const int32_t* coor
   if (zero_fill) {
     const int64_t n_dense = (int64_t)B * V;
     const int64_t blocks = (n_dense + s.ty - 1) / s.ty;
-    hipLaunchKernelGGL(scatter_fill_kernel, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0, stream,
-                       static_cast<const i32x4*>(S), inv, n_dense, n_rows, s.vpr,
+    hipLaunchKernelGGL(scatter_fill_kernel<true>, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0,
+                       stream, static_cast<const i32x4*>(S), inv, n_dense, n_rows, s.vpr,
                        static_cast<i32x4*>(D));
   } else {
     if (n_rows == 0) return hipSuccess;
@@ -226,6 +231,16 @@ hipError_t launch_scatter(const void* S, const int32_t* inv, const int32_t* coor
                        reinterpret_cast<const int2*>(coords), n_rows, B, V, s.vpr,
                        static_cast<i32x4*>(D));
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_inactive(const int32_t* inv, int32_t B, int32_t V, int32_t row_bytes,
+                                 void* D, hipStream_t stream) {
+  const RowShape s = row_shape(row_bytes);
+  const int64_t n_dense = (int64_t)B * V;
+  const int64_t blocks = (n_dense + s.ty - 1) / s.ty;
+  hipLaunchKernelGGL(scatter_fill_kernel<false>, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0,
+                     stream, nullptr, inv, n_dense, (int64_t)0, s.vpr, static_cast<i32x4*>(D));
   return hipGetLastError();
 }
 

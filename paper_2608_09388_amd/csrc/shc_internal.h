@@ -49,6 +49,8 @@ hipError_t launch_compact(const uint8_t* mask, int32_t B, int32_t V, int32_t* co
 hipError_t launch_gather(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
                          int32_t V, int32_t row_bytes, void* S, hipStream_t stream);
 
+hipError_t launch_clear_inactive(const int32_t* inv, int32_t B, int32_t V, int32_t row_bytes,
+                                 void* D, hipStream_t stream);
 hipError_t launch_scatter(const void* S, const int32_t* inv, const int32_t* coords,
                           int64_t n_rows, int32_t B, int32_t V, int32_t row_bytes, int zero_fill,
                           void* D, hipStream_t stream);

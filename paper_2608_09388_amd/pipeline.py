@@ -5,27 +5,35 @@ features, layer weights) to the GPU once, allocates every buffer the path
 needs at its worst-case size (all B*V rows active), and then runs the path
 as a sequence of library calls:
 
-    shc_compact_mask (+ shc_build_neighbor_table) -> shc_gather_rows ->
-    (shc_sparse_linear | shc_sparse_neighbor_conv_table) per layer ->
-    shc_scatter / shc_segment_maxpool
+    shc_compact_mask_start -> shc_compact_mask_wait (-> shc_build_neighbor_table)
+    -> shc_gather_rows -> (shc_sparse_linear | shc_sparse_neighbor_conv_table)
+    per layer -> shc_scatter / shc_segment_maxpool
 
 with the gather fused into the first layer (shc_gather_sparse_linear) when
 that layer is linear.
 
 The active set never changes across layers (C'_k = C_k, Sec. 3.2), so the
 active count is read back once per mask and passed to every layer call.
+
+The index buffers of a mask (coords, inv, row_ptr, the neighbour-row table)
+exist twice.  ``run(steps)`` uses this for consecutive batches: the
+compaction of batch k + 1 goes into the other set and is enqueued before the
+scatter and pool of batch k, so the host learns the next active count while
+the GPU still has batch k's tail to run, and the stream never idles on that
+wait.  Every batch still runs the whole path.
+
 This module only moves buffers and issues calls; all arithmetic runs in the
 library's kernels.
 """
 from __future__ import annotations
 
-from typing import Dict, List, Optional
+from typing import Callable, Dict, Optional, Sequence, Tuple
 
 import numpy as np
 import torch
 
 from . import binding as shc
-from .synth import BF16, Workload
+from .synth import Workload
 
 TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
 
@@ -34,6 +42,51 @@ def to_device(a: np.ndarray, dtype: str, device) -> torch.Tensor:
     """Upload fp32 values that are exact in `dtype` as a tensor of that dtype."""
     t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
     return t.to(device=device, dtype=TORCH_DTYPE[dtype])
+
+
+class _IndexSet:
+    """The compaction outputs of one mask and every call that reads them."""
+
+    def __init__(self, st: "SparseStack"):
+        dev, B, V, K = st.device, st.B, st.V, st.K
+        BV = B * V
+        self.coords = torch.empty((BV, 2), dtype=torch.int32, device=dev)
+        self.inv = torch.empty(BV, dtype=torch.int32, device=dev)
+        self.row_ptr = torch.empty(B + 1, dtype=torch.int32, device=dev)
+        self.n_active = torch.empty(4, dtype=torch.int32, device=dev)
+        ws = shc.compact_mask_workspace(B, V)
+        self.ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=dev)
+        has_conv = any(l.kind == "conv" for l in st.w.layers)
+        # neighbour-row table of the active set, shared by every conv layer
+        self.table = (torch.empty((K, BV), dtype=torch.int32, device=dev)
+                      if has_conv else None)
+        self.n: Optional[int] = None
+        # every call marshalled once, on the current stream; the buffers are at
+        # full capacity, so each call only takes the row count
+        self.compact = shc.PreparedCompact(st.mask, B, V, self.coords, self.inv, self.row_ptr,
+                                           self.n_active, self.ws)
+        self.gather = shc.prepare_gather_rows(st.x, self.coords, B, V, st.acts[0])
+        self.table_call = (shc.prepare_build_neighbor_table(self.coords, self.inv, B, V, st.nbr,
+                                                            self.table)
+                           if self.table is not None else None)
+        self.layers = []
+        for l, spec in enumerate(st.w.layers):
+            src, dst = st.acts[l], st.acts[l + 1]
+            a = st.act if spec.relu else shc.SHC_ACT_NONE
+            if spec.kind == "conv":
+                call = shc.prepare_sparse_neighbor_conv_table(src, self.table, st.weights[l],
+                                                              st.biases[l], dst, a)
+            elif l == 0 and st.fused_gather:
+                call = shc.prepare_gather_sparse_linear(st.x, self.coords, B, V, st.weights[l],
+                                                        st.biases[l], dst, a)
+            else:
+                call = shc.prepare_sparse_linear(src, st.weights[l], st.biases[l], dst, a)
+            self.layers.append(call)
+        last = st.acts[-1]
+        self.scatter = (shc.prepare_scatter(last, self.inv, self.coords, B, V, st.dense_out)
+                        if st.dense_out is not None else None)
+        self.pool = (shc.prepare_segment_maxpool(last, self.row_ptr, B, st.pooled, 0.0)
+                     if st.pooled is not None else None)
 
 
 class SparseStack:
@@ -51,94 +104,135 @@ class SparseStack:
         self.weights = [to_device(l.W, w.dtype, dev) for l in w.layers]
         self.biases = [None if l.bias is None else
                        torch.from_numpy(l.bias.astype(np.float32)).to(dev) for l in w.layers]
-        # compaction outputs (capacity: every row active)
-        self.coords = torch.empty((BV, 2), dtype=torch.int32, device=dev)
-        self.inv = torch.empty(BV, dtype=torch.int32, device=dev)
-        self.row_ptr = torch.empty(self.B + 1, dtype=torch.int32, device=dev)
-        self.n_active = torch.empty(4, dtype=torch.int32, device=dev)
-        ws = shc.compact_mask_workspace(self.B, self.V)
-        self.ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=dev)
         # activations: gathered input + one buffer per layer
         chans = [w.C0] + [l.Cout for l in w.layers]
         self.acts = [torch.empty((BV, c), dtype=self.dtype, device=dev) for c in chans]
         Cl = chans[-1]
         self.dense_out = torch.empty((BV, Cl), dtype=self.dtype, device=dev) if w.scatter else None
         self.pooled = torch.empty((self.B, Cl), dtype=self.dtype, device=dev) if w.pool else None
-        self.n = None
-        # neighbour-row table of the active set, shared by every conv layer
-        has_conv = any(l.kind == "conv" for l in w.layers)
-        self.table = (torch.empty((self.K, BV), dtype=torch.int32, device=dev)
-                      if has_conv else None)
-        # every call of the path marshalled once, on the current stream; the
-        # buffers are at full capacity, so each call only takes the row count
-        B, V = self.B, self.V
-        self._compact = shc.PreparedCompact(self.mask, B, V, self.coords, self.inv, self.row_ptr,
-                                            self.n_active, self.ws)
         # A first linear layer reads its rows straight from x (gather fused in);
         # otherwise the active rows are gathered into acts[0] first.
         self.fused_gather = len(w.layers) > 0 and w.layers[0].kind == "linear"
-        self._gather = shc.prepare_gather_rows(self.x, self.coords, B, V, self.acts[0])
-        self._table = (shc.prepare_build_neighbor_table(self.coords, self.inv, B, V, self.nbr,
-                                                        self.table)
-                       if self.table is not None else None)
-        self._layers = []
-        for l, spec in enumerate(w.layers):
-            src, dst = self.acts[l], self.acts[l + 1]
-            a = act if spec.relu else shc.SHC_ACT_NONE
-            if spec.kind == "conv":
-                call = shc.prepare_sparse_neighbor_conv_table(src, self.table, self.weights[l],
-                                                              self.biases[l], dst, a)
-            elif l == 0 and self.fused_gather:
-                call = shc.prepare_gather_sparse_linear(self.x, self.coords, B, V,
-                                                        self.weights[l], self.biases[l], dst, a)
-            else:
-                call = shc.prepare_sparse_linear(src, self.weights[l], self.biases[l], dst, a)
-            self._layers.append(call)
-        last = self.acts[-1]
-        self._scatter = (shc.prepare_scatter(last, self.inv, self.coords, B, V, self.dense_out)
-                         if self.dense_out is not None else None)
-        self._pool = (shc.prepare_segment_maxpool(last, self.row_ptr, B, self.pooled, 0.0)
-                      if self.pooled is not None else None)
+        self._sets = [_IndexSet(self), _IndexSet(self)]
+        self._cur = 0
 
-    # -- individual steps -----------------------------------------------------
+    # -- the index set of the current mask -------------------------------------
+    @property
+    def _set(self) -> _IndexSet:
+        return self._sets[self._cur]
+
+    @property
+    def n(self) -> Optional[int]:
+        return self._set.n
+
+    @n.setter
+    def n(self, value: Optional[int]):
+        self._set.n = value
+
+    coords = property(lambda self: self._set.coords)
+    inv = property(lambda self: self._set.inv)
+    row_ptr = property(lambda self: self._set.row_ptr)
+    n_active = property(lambda self: self._set.n_active)
+    ws = property(lambda self: self._set.ws)
+    table = property(lambda self: self._set.table)
+
+    # -- individual steps (on the current index set) ---------------------------
     def compact(self) -> int:
-        """Compaction; waits for the active count (one host sync per mask),
+        """Compaction; waits for the active count (one host wait per mask),
         then builds the neighbour-row table of the active set if a conv layer
         will read it."""
-        self.n = self._compact()
-        if self._table is not None:
-            self._table(self.n)
-        return self.n
+        s = self._set
+        s.n = s.compact()
+        if s.table_call is not None:
+            s.table_call(s.n)
+        return s.n
+
+    def build_table(self):
+        self._set.table_call(self.n)
 
     def gather(self):
         """Gather the active rows into acts[0] (not needed by the step when
         the first layer fuses the gather)."""
-        self._gather(self.n)
+        self._set.gather(self.n)
 
     def layer(self, l: int):
-        self._layers[l](self.n)
+        self._set.layers[l](self.n)
 
     def scatter(self):
-        self._scatter(self.n)
+        self._set.scatter(self.n)
 
     def pool(self):
-        self._pool(self.n)
+        self._set.pool(self.n)
 
     def finish(self):
-        if self._scatter is not None:
-            self._scatter(self.n)
-        if self._pool is not None:
-            self._pool(self.n)
+        """Scatter and pool of the current batch."""
+        s = self._set
+        if s.scatter is not None:
+            s.scatter(s.n)
+        if s.pool is not None:
+            s.pool(s.n)
+
+    def _front(self, s: _IndexSet, around=None):
+        """Everything of a batch after its compaction, up to its last layer;
+        ``around = (l, ev_a, ev_b)`` records the events around layer l."""
+        if s.table_call is not None:
+            s.table_call(s.n)
+        if not self.fused_gather:
+            s.gather(s.n)
+        for l, call in enumerate(s.layers):
+            if around is not None and around[0] == l:
+                around[1].record()
+            call(s.n)
+            if around is not None and around[0] == l:
+                around[2].record()
 
     def step(self) -> int:
-        """One pass of the whole path over the workload's batch."""
-        self.compact()
-        if not self.fused_gather:
-            self.gather()
-        for call in self._layers:
-            call(self.n)
+        """One pass of the whole path over the workload's batch, on its own."""
+        s = self._set
+        s.n = s.compact()
+        self._front(s)
         self.finish()
-        return self.n
+        return s.n
+
+    def run(self, steps: int, around_layer: Optional[Tuple[int, Sequence]] = None,
+            feed: Optional[Callable[[int], None]] = None) -> int:
+        """`steps` passes of the whole path over consecutive batches, the
+        compaction of each batch overlapped with the scatter and pool of the
+        one before (module docstring).
+
+        ``feed(k)``, if given, is called just before batch k's compaction is
+        enqueued and may write batch k's mask and features into ``mask`` and
+        ``x`` with work on the current stream (without it every batch reuses
+        them).  ``around_layer = (l, [(ev_a, ev_b), ...])`` records one pair of
+        events around layer l of every batch.  The outputs left behind are the
+        last batch's.  Returns its N'."""
+        if steps <= 0:
+            return self.n or 0
+        s = self._set
+        if feed is not None:
+            feed(0)
+        s.compact.start()
+        s.n = s.compact.wait()
+        for k in range(steps):
+            ev = None
+            if around_layer is not None:
+                ev = (around_layer[0], *around_layer[1][k])
+            self._front(s, ev)
+            nxt = None
+            if k + 1 < steps:
+                self._cur ^= 1
+                nxt = self._set
+                if feed is not None:
+                    feed(k + 1)
+                nxt.compact.start()
+            if s.scatter is not None:
+                s.scatter(s.n)
+            if s.pool is not None:
+                s.pool(s.n)
+            if nxt is not None:
+                nxt.n = nxt.compact.wait()
+                s = nxt
+        return s.n
 
     # -- results on the host --------------------------------------------------
     def rows(self, l: int) -> np.ndarray:

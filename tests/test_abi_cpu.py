@@ -72,6 +72,31 @@ def test_compact_mask_validation(lib):
     assert call(ws_bytes=ws - 1) == -2 and "workspace" in err(lib)
 
 
+def test_compact_mask_start_wait_validation(lib):
+    ws = lib.shc_compact_mask_workspace(4, 655)
+
+    def start(n_host=None, **kw):
+        a = dict(dict(mask=A, B=4, V=655, coords=A, inv=A, row_ptr=A, n_dev=A, cap=2620, ws=A,
+                      ws_bytes=ws), **kw)
+        return lib.shc_compact_mask_start(a["mask"], a["B"], a["V"], a["coords"], a["inv"],
+                                          a["row_ptr"], a["n_dev"], n_host, a["cap"], a["ws"],
+                                          a["ws_bytes"], None)
+
+    assert start() == -1 and "n_active_host" in err(lib)   # the host count is required
+    assert lib.shc_compact_mask_wait(None, 10, None) == -1 and "n_active_host" in err(lib)
+
+
+def test_clear_inactive_rows_validation(lib):
+    def call(inv=A, B=4, V=655, C=16, dtype=0, D=A):
+        return lib.shc_clear_inactive_rows(inv, B, V, C, dtype, D, None)
+
+    assert call(inv=None) == -1 and "inv" in err(lib)
+    assert call(D=MIS) == -3 and "D" in err(lib)
+    assert call(C=8) == -4
+    assert call(dtype=5) < 0
+    assert call(B=0) == -1
+
+
 def test_gather_scatter_pool_validation(lib):
     g = lib.shc_gather_rows
     assert g(A, A, 10, 4, 655, 24, 0, A, None) == -4

@@ -112,6 +112,46 @@ def test_compact_prepared_pinned(dev):
         assert np.array_equal(down(c.coords)[:ref_n], ref_c)
 
 
+def test_compact_start_wait(dev):
+    """The two halves of the compaction with work enqueued between them (the
+    zeros of a dense output): same outputs as the oracle over three masks in a
+    row of decreasing size, through the prepared call and the plain wrappers."""
+    rng = np.random.default_rng(93)
+    B, V, C = 24, 10475, 16
+    c = Compaction(np.zeros((B, V), np.uint8))
+    call = shc.PreparedCompact(c.mask, B, V, c.coords, c.inv, c.row_ptr, c.n_dev, c.ws)
+    D = torch.full((B * V, C), float("nan"), dtype=torch.float32, device=dev)
+    hc = torch.full((1,), -5, dtype=torch.int64, pin_memory=True)
+    for p in (0.3, 0.05, 0.0):
+        m = (rng.random((B, V)) < p).astype(np.uint8)
+        c.mask.copy_(up(m.reshape(-1)))
+        ref_c, ref_inv, ref_rp, ref_n = O.compact(m)
+        call.start()
+        shc.clear_inactive_rows(c.inv, B, V, D)
+        assert call.wait() == ref_n
+        assert np.array_equal(down(c.inv), ref_inv)
+        assert np.array_equal(down(c.row_ptr), ref_rp)
+        assert np.array_equal(down(c.coords)[:ref_n], ref_c)
+        assert int(c.n_dev[0].item()) == ref_n
+        got = down(D)
+        assert np.all(got[ref_inv < 0] == 0)
+        shc.compact_mask_start(c.mask, B, V, c.coords, c.inv, c.row_ptr, c.n_dev, c.ws, hc)
+        assert shc.compact_mask_wait(hc, c.cap) == ref_n
+    # a count above the capacity given to the wait
+    m = (rng.random((B, V)) < 0.1).astype(np.uint8)
+    c.mask.copy_(up(m.reshape(-1)))
+    shc.compact_mask_start(c.mask, B, V, c.coords, c.inv, c.row_ptr, c.n_dev, c.ws, hc)
+    with pytest.raises(shc.ShcError) as e:
+        shc.compact_mask_wait(hc, int(m.sum()) - 1)
+    assert e.value.status == -2
+    torch.cuda.synchronize()
+    # pageable host memory is refused by the start call, before any launch
+    with pytest.raises(shc.ShcError) as e:
+        shc.compact_mask_start(c.mask, B, V, c.coords, c.inv, c.row_ptr, c.n_dev, c.ws,
+                               torch.zeros(1, dtype=torch.int64))
+    assert e.value.status == -1
+
+
 def test_compact_paper_workload_masks(dev):
     for w in (synth.workload_c1(), synth.workload_c2(), synth.workload_c5()):
         check_compaction(w.mask)
@@ -171,6 +211,15 @@ def test_gather_scatter_exact(dev, dtype, C):
     got2 = down(D2)
     assert np.array_equal(np.isnan(got2), np.isnan(exp))
     assert np.array_equal(got2[~np.isnan(exp)], exp[~np.isnan(exp)])
+    # the zeros alone (inactive rows; active rows keep the sentinel), then the
+    # active rows: together the zero-fill scatter's result
+    D3 = torch.full((B * V, C), float("nan"), dtype=xd.dtype, device=dev)
+    shc.clear_inactive_rows(c.inv, B, V, D3)
+    got3 = down(D3)
+    act = ref_inv >= 0
+    assert np.all(got3[~act] == 0) and np.all(np.isnan(got3[act]))
+    shc.scatter(S, c.inv, c.coords, n, B, V, D3, zero_fill=False)
+    assert torch.equal(D3, D)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -527,6 +576,41 @@ def test_full_size_workloads_sampled(dev, name):
         for b in rng.choice(w.B, size=min(w.B, 40), replace=False):
             seg = last[rp[b]:rp[b + 1]]
             assert np.array_equal(P[b], seg.max(0) if len(seg) else np.zeros(last.shape[1]))
+
+
+@pytest.mark.parametrize("steps", [1, 2, 3])
+def test_overlapped_run_new_mask_per_batch(dev, steps):
+    """SparseStack.run: each batch's compaction (into the other index set) is
+    enqueued before the previous batch's scatter and pool.  Every batch gets
+    its own mask and features; the outputs left behind must be the oracle's
+    for the last batch, with index sets that last held another mask."""
+    from paper_2608_09388_amd.pipeline import SparseStack, to_device
+    w = synth.workload_c4(0.05, B=6, V=655)
+    rng = np.random.default_rng(400 + steps)
+    masks = [(rng.random((w.B, w.V)) < p).astype(np.uint8) for p in (0.3, 0.05, 0.2)][:steps]
+    xs = [synth.as_dtype(rng.standard_normal(w.x.shape).astype(np.float32), w.dtype)[1]
+          for _ in range(steps)]
+    st = SparseStack(w, device=str(dev))
+    st.run(2)                               # both index sets hold the workload's own mask
+
+    def feed(k):
+        st.mask.copy_(up(masks[k].reshape(-1)))
+        st.x.copy_(to_device(xs[k], w.dtype, st.device))
+
+    n = st.run(steps, feed=feed)
+    m, x = masks[-1], xs[-1]
+    spec = [(l.kind, l.W, l.bias, l.relu) for l in w.layers]
+    ref = O.run_stack(x, m, w.nbr, spec, w.dtype, pool=True)
+    got = st.results()
+    assert n == ref["n"] == got["n"] == got["n_dev"]
+    assert np.array_equal(got["coords"], ref["coords"])
+    assert np.array_equal(got["inv"], ref["inv"])
+    for l in range(len(w.layers)):
+        assert_normwise_close(got["outs"][l], ref["outs"][l], w.dtype, f"layer {l}")
+    dense_ref = O.scatter(ref["outs"][-1], ref["inv"], zero_fill=True)
+    assert_normwise_close(got["dense"], dense_ref, w.dtype, "dense")
+    assert np.all(got["dense"][ref["inv"] < 0] == 0)
+    assert_normwise_close(got["pool"], ref["pool"], w.dtype, "pool")
 
 
 def test_c5_sequences_stack(dev):
