@@ -204,7 +204,8 @@ class SparseStack:
         enqueued and may write batch k's mask and features into ``mask`` and
         ``x`` with work on the current stream (without it every batch reuses
         them).  ``around_layer = (l, [(ev_a, ev_b), ...])`` records one pair of
-        events around layer l of every batch.  The outputs left behind are the
+        events around layer l of every batch (a pair of None: none for that
+        batch).  The outputs left behind are the
         last batch's.  Returns its N'."""
         if steps <= 0:
             return self.n or 0
@@ -215,7 +216,7 @@ class SparseStack:
         s.n = s.compact.wait()
         for k in range(steps):
             ev = None
-            if around_layer is not None:
+            if around_layer is not None and around_layer[1][k][0] is not None:
                 ev = (around_layer[0], *around_layer[1][k])
             self._front(s, ev)
             nxt = None
