@@ -99,6 +99,12 @@ __global__ __launch_bounds__(kThreads) void compact_write_kernel(
   const int lane = tid & 63;
   const int wave = tid >> 6;
 
+  const int64_t start = (int64_t)blockIdx.x * per_block;
+  const int64_t end = min(start + per_block, total);
+  // the first chunk's mask bytes are loaded while the prefix below is formed
+  uint32_t w[4];
+  load_groups(mask, start, end, w);
+
   // rows taken by the blocks before this one (block 0: by every block, N')
   const int upto = blockIdx.x == 0 ? (int)gridDim.x : (int)blockIdx.x;
   uint32_t before = 0;
@@ -114,11 +120,9 @@ __global__ __launch_bounds__(kThreads) void compact_write_kernel(
     base = 0;
   }
 
-  const int64_t start = (int64_t)blockIdx.x * per_block;
-  const int64_t end = min(start + per_block, total);
   for (int64_t c0 = start; c0 < end; c0 += kChunk) {
-    uint32_t w[4], nz[4];
-    load_groups(mask, c0, end, w);
+    uint32_t nz[4];
+    if (c0 != start) load_groups(mask, c0, end, w);
     // per-thread counts of the four groups, packed 16 bits each (a block sum
     // per field is at most 1024, so the fields never carry into each other)
     uint32_t lo = 0, hi = 0;

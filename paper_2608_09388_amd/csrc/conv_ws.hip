@@ -142,7 +142,6 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   const int nrows = (int)min((int64_t)R, a.n_rows - row0);
   const int nblk = (nrows + 15) / 16;
   const int n0 = blockIdx.y * WS;
-  const unsigned char* S = static_cast<const unsigned char*>(a.S);
   const unsigned char* W = static_cast<const unsigned char*>(a.W);
 
   // Byte offset of 16-byte vector q in weight-slice row k.  For bf16 the
@@ -328,19 +327,19 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
       }
     }
   } else {
-    for (int base = 0; base < wvecs; base += kWBatch * kThreads) {
-      if (base > 0) load_w(base, wv);
-      store_w(base, wv);
-    }
-    __syncthreads();
     // input rows: row i itself, or (gather) row b_i * V + v_i of the dense
-    // tensor; every coordinate load of the thread is issued before any is used
+    // tensor; the coordinate loads go out with the weight slice's, before
+    // either is used
     int2 cr[kRPT];
 #pragma unroll
     for (int rr = 0; rr < kRPT; ++rr) {
       const int t = tid + rr * kThreads;
       cr[rr] = a.gather ? reinterpret_cast<const int2*>(a.coords)[row0 + (t < nrows ? t : 0)]
                         : int2{0, 0};
+    }
+    for (int base = 0; base < wvecs; base += kWBatch * kThreads) {
+      if (base > 0) load_w(base, wv);
+      store_w(base, wv);
     }
 #pragma unroll
     for (int rr = 0; rr < kRPT; ++rr) {
@@ -368,7 +367,6 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   }
   const bool relu = a.relu != 0;
   unsigned char* my_scratch = scratch + wave * 16 * WROW;
-  unsigned char* out = static_cast<unsigned char*>(a.out);
 
   struct Job {
     int blk;    // block, or -1 past the end
