@@ -24,11 +24,20 @@ What it computes (Sec. 3.1-3.2 of the paper, arXiv 2608.09388):
 * Pooling is named alongside the other sparse layers but not defined; here
   it is the maximum over the active rows of each body / frame, 0 for a body
   with no active row.
+* Eqs. 7-9: sparse group normalization.  The channels are split into G
+  groups of C/G; for every body / frame b and group g the mean and the
+  (biased, 1/N) variance are taken over the group's values in the ACTIVE rows
+  of b only, and those values are centred and divided by sqrt(var + eps).
+  No affine term; eps = 1e-5 unless given.  G = 1 is layer normalization.
 
-Every layer is computed the plain way: the DENSE operator is applied to the
-masked input x (.) m on all B*V rows in fp64, and the result is then read at
-the active rows.  Since a sparse operator only ever reads active rows, this
-restriction is exactly the sparse operator's result (up to rounding order).
+Every layer but the normalization is computed the plain way: the DENSE
+operator is applied to the masked input x (.) m on all B*V rows in fp64, and
+the result is then read at the active rows.  Since a sparse operator only ever
+reads active rows, this restriction is exactly the sparse operator's result
+(up to rounding order).  Group normalization is the exception: the dense
+operator on x (.) m would let the inactive rows' zeros into the statistics,
+so it is written out per body and group over the active rows, as Eqs. 7-9
+define it.
 
 Precision: inputs are widened exactly to fp64 and all sums are fp64.  For
 bfloat16 stacks each layer output is rounded to bfloat16 (round to nearest,
@@ -249,6 +258,39 @@ def segment_max(S: np.ndarray, row_ptr: np.ndarray, empty_value: float = 0.0) ->
         if hi > lo:
             P[b] = np.fmax.reduce(S[lo:hi], axis=0)
     return P
+
+
+# ----------------------------------------------------------------------------
+# Eqs. 7-9: sparse group normalization
+# ----------------------------------------------------------------------------
+
+
+def group_norm(S: np.ndarray, row_ptr: np.ndarray, G: int, eps: float = 1e-5) -> np.ndarray:
+    """Sparse group normalization of the active rows (Eqs. 7-9).
+
+    ``S`` [N'][C] holds the active rows of every body in order, ``row_ptr``
+    [B+1] the first row of each body.  For body b and channel group g (C/G
+    consecutive channels), mu is the mean and var the mean squared deviation
+    of the group's values over the rows of b (Eqs. 7 and 8); each value
+    becomes (value - mu) / sqrt(var + eps) (Eq. 9).  A body without rows has
+    nothing to normalize.  Computed in fp64.
+    """
+    S = np.asarray(S, dtype=np.float64)
+    n, C = S.shape
+    if C % G != 0:
+        raise ValueError(f"C = {C} is not a multiple of G = {G}")
+    cg = C // G
+    out = np.empty_like(S)
+    for b in range(len(row_ptr) - 1):
+        lo, hi = int(row_ptr[b]), int(row_ptr[b + 1])
+        if hi <= lo:
+            continue
+        for g in range(G):
+            vals = S[lo:hi, g * cg:(g + 1) * cg]
+            mu = vals.mean()
+            var = ((vals - mu) ** 2).mean()
+            out[lo:hi, g * cg:(g + 1) * cg] = (vals - mu) / np.sqrt(var + eps)
+    return out
 
 
 # ----------------------------------------------------------------------------

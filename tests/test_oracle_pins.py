@@ -351,6 +351,107 @@ def test_segment_max_ignores_nan_and_equals_dense_pool_after_relu():
 
 
 # ----------------------------------------------------------------------------
+# group normalization (Eqs. 7-9)
+# ----------------------------------------------------------------------------
+
+
+def gn_case(rng, B=5, V=40, C=12, p=0.4):
+    m = (rng.random((B, V)) < p).astype(np.uint8)
+    m[2] = 0                                # one body without rows
+    m[3] = 0
+    m[3, 7] = 1                             # one body with a single row
+    coords, inv, rp, n = O.compact(m)
+    x = rng.standard_normal((B * V, C)) * 3.0 + rng.standard_normal(C)
+    return m, coords, rp, O.gather(x, coords, V), x
+
+
+@pytest.mark.parametrize("G", [1, 3, 4, 12])
+def test_group_norm_full_mask_is_torch_group_norm(G):
+    """All rows active: each body's statistics cover all V rows, which is
+    torch's group_norm on the body's [C, V] feature map."""
+    rng = np.random.default_rng(G)
+    B, V, C = 3, 30, 12
+    m = np.ones((B, V), np.uint8)
+    coords, inv, rp, n = O.compact(m)
+    x = rng.standard_normal((B * V, C)) * 2 + 1
+    S = O.gather(x, coords, V)
+    got = O.group_norm(S, rp, G)
+    xt = torch.from_numpy(x.reshape(B, V, C).transpose(0, 2, 1).copy())   # [B][C][V]
+    ref = torch.nn.functional.group_norm(xt, G, eps=1e-5).numpy().transpose(0, 2, 1).reshape(-1, C)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_group_norm_one_group_is_torch_layer_norm_per_body():
+    """G = 1 (the paper's layer-normalization case): per body, torch's
+    layer_norm over all of its active rows and channels at once."""
+    rng = np.random.default_rng(11)
+    m, coords, rp, S, _ = gn_case(rng)
+    got = O.group_norm(S, rp, 1)
+    for b in range(len(rp) - 1):
+        lo, hi = rp[b], rp[b + 1]
+        if hi > lo:
+            blk = torch.from_numpy(S[lo:hi])
+            ref = torch.nn.functional.layer_norm(blk, blk.shape, eps=1e-5).numpy()
+            np.testing.assert_allclose(got[lo:hi], ref, rtol=1e-12, atol=1e-12)
+
+
+def test_group_norm_two_rows_closed_form():
+    """Two rows, one channel per group: mu = (a + c) / 2, biased variance
+    ((a - c) / 2)^2, so the outputs are +-d / sqrt(d^2 + eps), d = (a - c) / 2."""
+    a = np.array([[1.5, -2.0, 7.0], [-0.5, 4.0, 7.0]])
+    got = O.group_norm(a, np.array([0, 2]), 3, eps=0.25)
+    d = (a[0] - a[1]) / 2
+    exp = np.stack([d, -d]) / np.sqrt(d * d + 0.25)
+    np.testing.assert_allclose(got, exp, rtol=1e-15, atol=0)
+    assert np.all(got[:, 2] == 0)           # equal values: zero deviation
+
+
+def test_group_norm_single_row_and_empty_bodies():
+    rng = np.random.default_rng(12)
+    m, coords, rp, S, _ = gn_case(rng, C=8)
+    got = O.group_norm(S, rp, 8)            # one channel per group
+    lo = rp[3]
+    assert rp[4] - lo == 1
+    assert np.all(got[lo] == 0)             # a lone value has zero deviation
+    assert rp[3] == rp[2]                   # body 2 contributes no row
+
+
+def test_group_norm_invariants():
+    """Per (body, group): the output has mean 0 and mean square var/(var+eps);
+    a constant added to a (body, group) block changes nothing; scaling the
+    input by s and eps by s^2 changes nothing; bodies do not interact; and
+    the statistics use the body's ACTIVE rows only (a dense normalization of
+    x (.) m over all V rows differs)."""
+    rng = np.random.default_rng(13)
+    m, coords, rp, S, x = gn_case(rng, C=12)
+    G, eps = 3, 1e-5
+    out = O.group_norm(S, rp, G, eps)
+    for b in range(len(rp) - 1):
+        lo, hi = rp[b], rp[b + 1]
+        if hi - lo < 2:
+            continue
+        for g in range(G):
+            blk = out[lo:hi, 4 * g:4 * g + 4]
+            v = S[lo:hi, 4 * g:4 * g + 4]
+            var = v.var()
+            assert abs(blk.mean()) < 1e-12
+            assert abs((blk ** 2).mean() - var / (var + eps)) < 1e-12
+    S2 = S.copy()
+    S2[rp[1]:rp[2], 4:8] += 123.0
+    np.testing.assert_allclose(O.group_norm(S2, rp, G, eps), out, atol=1e-9)
+    np.testing.assert_allclose(O.group_norm(S * 7.0, rp, G, eps * 49.0), out, atol=1e-12)
+    S3 = S.copy()
+    S3[rp[0]:rp[1]] *= -5.0
+    o3 = O.group_norm(S3, rp, G, eps)
+    np.testing.assert_array_equal(o3[rp[1]:], out[rp[1]:])
+    # dense group norm of x (.) m over all V rows of body 0 is a different thing
+    V = m.shape[1]
+    xm = (x * m.reshape(-1, 1))[:V]
+    dense = torch.nn.functional.group_norm(torch.from_numpy(xm.T[None].copy()), G).numpy()[0].T
+    assert not np.allclose(dense[m[0] != 0], out[rp[0]:rp[1]], atol=1e-3)
+
+
+# ----------------------------------------------------------------------------
 # bfloat16 round-to-nearest-even
 # ----------------------------------------------------------------------------
 
