@@ -260,6 +260,9 @@ def main():
         "roofline": roof,
     }
 
+    out["next_rows"] = {"group_norm": group_norm_measure(st, shc, torch, args.reps)}
+    log("group norm measured")
+
     if not args.no_dense:
         out["speedup_vs_dense"] = dense_comparison(st, w, per_kernel_ms, torch, shc, synth)
         log("dense comparison done")
@@ -268,6 +271,34 @@ def main():
         out["cpu_baseline"] = cpu_baseline(w, spec, args.cpu_seconds)
         log("cpu baseline done")
     print(json.dumps(out))
+
+
+def group_norm_measure(st, shc, torch, reps, G=32):
+    """Sparse group normalization (Eqs. 7-9) of the conv layer's output rows,
+    per body and channel group: back-to-back launches between HIP events on
+    the stream it runs on, and its HBM fraction (one read and one write of
+    every active value, plus the body offsets)."""
+    n = st.n
+    S = st.acts[-1]
+    C = S.shape[-1]
+    out = torch.empty_like(S)
+    call = shc.prepare_segment_group_norm(S, st.row_ptr, st.B, G, out)
+    for _ in range(3):
+        call(n)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        call(n)
+    b.record()
+    torch.cuda.synchronize()
+    us = a.elapsed_time(b) / reps * 1e3
+    nbytes = 2 * n * C * S.element_size() + 4 * (st.B + 1)
+    ach = nbytes / (us * 1e-6) / 1e9
+    return {"config": f"N'={n} rows of the density-sweep conv output, C={C}, G={G}, "
+                      f"{st.B} bodies", "launch_us": round(us, 2), "algorithmic_bytes": nbytes,
+            "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(ach / HBM_PEAK_GBS, 4)}
 
 
 def dense_comparison(st, w, per_kernel_ms, torch, shc, synth):

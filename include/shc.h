@@ -256,6 +256,28 @@ int shc_clear_inactive_rows(const int32_t* inv, int32_t B, int32_t V, int32_t C,
                             void* D, hipStream_t stream);
 
 /*
+ * Sparse group normalization per body/frame -- Eqs. 7-9 (Sec. 3.2): for every
+ * body b and group g of C/G consecutive channels,
+ *
+ *   mu  = mean of the group's values over rows row_ptr[b] <= i < row_ptr[b+1]
+ *   var = mean of (value - mu)^2 over the same values (biased, 1/N)
+ *   out = (value - mu) / sqrt(var + eps)
+ *
+ * Only the active rows enter the statistics (a body's rows are its active
+ * vertices), so this is not the dense normalization of the masked tensor.
+ * No affine term.  G = 1 is layer normalization.
+ *
+ *   S [n_rows][C], row_ptr [B+1] (bounds clamped to [0, n_rows]), out
+ *   [n_rows][C] of the same dtype, must not overlap S.  G must divide C; eps
+ *   must be positive and finite (1e-5 is the usual value).
+ * Statistics are accumulated in fp32 (two passes: the mean, then the squared
+ * deviations from it); bf16 outputs are rounded to nearest even.
+ */
+int shc_segment_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
+                           int32_t C, int32_t G, float eps, int32_t dtype, void* out,
+                           hipStream_t stream);
+
+/*
  * Segmented max-pool per body/frame -- the sparse pooling layer (Sec. 3.2):
  *
  *   P[b][c] = max over row_ptr[b] <= i < row_ptr[b+1] of S[i][c]

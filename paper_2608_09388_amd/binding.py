@@ -64,6 +64,8 @@ _SIGS = {
                                                       _c_ptr, _c_ptr]),
     "shc_scatter": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
                                    _c_i32, _c_ptr, _c_ptr]),
+    "shc_segment_group_norm": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32,
+                                              _c_f, _c_i32, _c_ptr, _c_ptr]),
     "shc_segment_maxpool": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_f,
                                            _c_ptr, _c_ptr]),
 }
@@ -288,6 +290,25 @@ def clear_inactive_rows(inv: torch.Tensor, B: int, V: int, D: torch.Tensor, stre
     args = [_dev(inv, "inv", torch.int32, B * V), B, V, C, _dtype_code(D),
             _dev(D, "D", D.dtype, B * V * C), _stream(stream)]
     _check(load().shc_clear_inactive_rows(*args), "shc_clear_inactive_rows")
+
+
+def segment_group_norm(S: torch.Tensor, row_ptr: torch.Tensor, n_rows: int, B: int, G: int,
+                       out: torch.Tensor, eps: float = 1e-5, stream=None):
+    """shc_segment_group_norm: per body and channel group, over the active rows."""
+    C = S.shape[-1]
+    dt = _dtype_code(S)
+    args = [_dev(S, "S", S.dtype, n_rows * C) if n_rows > 0 else None,
+            _dev(row_ptr, "row_ptr", torch.int32, B + 1), n_rows, B, C, G, float(eps), dt,
+            _dev(out, "out", S.dtype, n_rows * C) if n_rows > 0 else None, _stream(stream)]
+    _check(load().shc_segment_group_norm(*args), "shc_segment_group_norm")
+
+
+def prepare_segment_group_norm(S, row_ptr, B, G, out, eps=1e-5, stream=None) -> Prepared:
+    C = S.shape[-1]
+    n_max = min(S.numel() // C, out.numel() // C)
+    args = [_dev(S, "S", S.dtype), _dev(row_ptr, "row_ptr", torch.int32, B + 1), 0, B, C, G,
+            float(eps), _dtype_code(S), _dev(out, "out", S.dtype), _stream(stream)]
+    return Prepared("shc_segment_group_norm", args, 2, n_max, (S, row_ptr, out))
 
 
 def segment_maxpool(S: torch.Tensor, row_ptr: torch.Tensor, n_rows: int, B: int,

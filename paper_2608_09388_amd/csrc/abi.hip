@@ -6,6 +6,8 @@
 #include <string.h>
 
 #include "../../include/shc.h"
+#include <cmath>
+
 #include "shc_internal.h"
 
 namespace {
@@ -420,6 +422,31 @@ int shc_clear_inactive_rows(const int32_t* inv, int32_t B, int32_t V, int32_t C,
   const int32_t row_bytes = C * (dtype == SHC_BF16 ? 2 : 4);
   return hip_status(shc::launch_clear_inactive(inv, B, V, row_bytes, D, stream),
                     "clear_inactive_rows launch");
+}
+
+int shc_segment_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
+                           int32_t C, int32_t G, float eps, int32_t dtype, void* out,
+                           hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (B <= 0) return fail(SHC_ERR_INVALID_ARG, "B = %d must be positive", B);
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("C", C));
+  if (G <= 0 || C % G != 0)
+    return fail(SHC_ERR_INVALID_ARG, "G = %d must be positive and divide C = %d", G, C);
+  if (!(eps > 0.f) || !std::isfinite(eps))
+    return fail(SHC_ERR_INVALID_ARG, "eps = %g must be positive and finite", (double)eps);
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(S, "S");
+  SHC_PTR(row_ptr, "row_ptr");
+  SHC_PTR(out, "out");
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_status(e, "segment_group_norm device query");
+  return hip_status(shc::launch_group_norm(S, row_ptr, n_rows, B, C, G, eps, dtype == SHC_BF16,
+                                           out, cus, stream),
+                    "segment_group_norm launch");
 }
 
 int shc_segment_maxpool(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,

@@ -1,0 +1,306 @@
+// Sparse group normalization (Eqs. 7-9): for every body b (a segment of the
+// active rows, [row_ptr[b], row_ptr[b+1])) and every group g of C/G
+// consecutive channels,
+//
+//   mu  = mean of the group's values over the body's rows          (Eq. 7)
+//   var = mean of (value - mu)^2 over the same values              (Eq. 8)
+//   out = (value - mu) / sqrt(var + eps)                           (Eq. 9)
+//
+// Only active rows enter the statistics (the rows of S are the active ones).
+//
+// Workgroups of 1024 threads, F per body: workgroup (b, f) takes the f-th
+// of F equal channel ranges (whole groups), so B * F workgroups fill the
+// chip even when bodies are few.  Thread (tx, ty) owns 16-byte channel
+// vector tx of its range in rows ty, ty + TY, ...; its partial sums are per
+// channel (4 fp32 or 8 bf16 channels), summed over the rows a wavefront holds
+// with lane shuffles, then through LDS over the wavefronts, then over the
+// channels of each group.  The statistics are
+// two-pass (the mean first, then the squared deviations from it) in fp32.
+// A body of up to kResident vectors per thread stays in registers, so HBM
+// sees one read and one write of every value; a larger body is streamed
+// three times (sums, deviations, output), the later passes mostly from L2.
+#include <algorithm>
+#include <mutex>
+
+#include "shc_internal.h"
+
+namespace shc {
+namespace {
+
+constexpr int kNormThreads = 1024;
+constexpr int kResident = 16;  // vectors per thread held in registers
+
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+template <bool BF16>
+struct NormVec;
+template <>
+struct NormVec<false> {
+  static constexpr int N = 4;
+  static __device__ __forceinline__ void widen(const i32x4& v, float* f) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) f[e] = __int_as_float(v[e]);
+  }
+  static __device__ __forceinline__ i32x4 narrow(const float* f) {
+    return i32x4{__float_as_int(f[0]), __float_as_int(f[1]), __float_as_int(f[2]),
+                 __float_as_int(f[3])};
+  }
+};
+template <>
+struct NormVec<true> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void widen(const i32x4& v, float* f) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {  // bf16 -> fp32 is exact: the bits move up
+      f[2 * e] = __int_as_float(v[e] << 16);
+      f[2 * e + 1] = __int_as_float(v[e] & (int)0xFFFF0000);
+    }
+  }
+  static __device__ __forceinline__ i32x4 narrow(const float* f) {
+    i32x4 out;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {  // hardware round-to-nearest-even conversion
+      const bf16x2 h = __builtin_convertvector(f32x2{f[2 * e], f[2 * e + 1]}, bf16x2);
+      out[e] = __builtin_bit_cast(int, h);
+    }
+    return out;
+  }
+};
+
+template <bool BF16>
+__global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
+    const i32x4* __restrict__ S, const int32_t* __restrict__ row_ptr, int64_t n_rows, int C,
+    int G, float eps, int vpr, i32x4* __restrict__ out) {
+  using NV = NormVec<BF16>;
+  constexpr int N = NV::N;
+  // part[slot][Cl]: channel partials (one slot per thread row, or per
+  // wavefront after the shuffles); then chan[Cl], then per-group mean /
+  // reciprocal deviation broadcast back per channel
+  extern __shared__ float smem[];
+  const int TX = blockDim.x, TY = blockDim.y;  // TX = vectors of this workgroup's range
+  const int ty = threadIdx.y;
+  const int tid = ty * TX + threadIdx.x;
+  const int Cl = TX * N;                       // channels of the range
+  const int tx = blockIdx.y * TX + threadIdx.x;  // vector within the row
+  // rows a wavefront holds: 64 / TX when TX divides 64 (then reduced by shuffles)
+  const int rw = (TX <= 64 && 64 % TX == 0) ? 64 / TX : 1;
+  const int slots = rw > 1 ? (TX * TY) / 64 : TY;
+  float* part = smem;                 // [slots][Cl]
+  float* chan = smem + slots * Cl;    // [Cl]
+  float* stat = chan + Cl;            // [Cl]: the group's mean, then 1/sqrt(var + eps)
+
+  int64_t lo = row_ptr[blockIdx.x], hi = row_ptr[blockIdx.x + 1];
+  lo = lo < 0 ? 0 : (lo > n_rows ? n_rows : lo);
+  hi = hi < lo ? lo : (hi > n_rows ? n_rows : hi);
+  const int rows = (int)(hi - lo);
+  if (rows == 0) return;  // uniform over the workgroup
+  const bool resident = rows <= TY * kResident;
+  const int cg = C / G;
+  const float count = (float)rows * (float)cg;  // exact below 2^24
+
+  // this thread's channel partials -> per-channel totals over the rows ->
+  // per group, into stat[] (the range's channels hold whole groups)
+  auto reduce = [&](float* acc, bool second) {
+    if (rw > 1) {
+      const int lane = tid & 63;
+#pragma unroll
+      for (int e = 0; e < N; ++e)
+        for (int d = TX; d < 64; d <<= 1) acc[e] += __shfl_xor(acc[e], d, 64);
+      if (lane < TX)
+#pragma unroll
+        for (int e = 0; e < N; ++e) part[(tid >> 6) * Cl + threadIdx.x * N + e] = acc[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < N; ++e) part[ty * Cl + threadIdx.x * N + e] = acc[e];
+    }
+    __syncthreads();
+    const int nt = TX * TY;
+    // groups line up with wavefront lanes: cg divides 64, or 64 divides cg
+    if (Cl <= nt && ((cg <= 64 && 64 % cg == 0) || cg % 64 == 0)) {
+      // thread c: channel total (four independent partial sums), then the
+      // group total by lane shuffles (cg <= 64) or per-wave partials (cg > 64)
+      const int c = tid;
+      float t = 0.f;
+      if (c < Cl) {
+        float q[4] = {0.f, 0.f, 0.f, 0.f};
+        int y = 0;
+        for (; y + 4 <= slots; y += 4)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) q[u] += part[(y + u) * Cl + c];
+        for (; y < slots; ++y) q[0] += part[y * Cl + c];
+        t = (q[0] + q[1]) + (q[2] + q[3]);
+      }
+      const int span = cg < 64 ? cg : 64;  // lanes summed by shuffles
+      for (int d = 1; d < span; d <<= 1) t += __shfl_xor(t, d, 64);
+      if (cg <= 64) {
+        if (c < Cl && c % cg == 0) {
+          const float v = t / count;  // correctly rounded: an exact mean stays exact
+          chan[c] = second ? 1.0f / sqrtf(v + eps) : v;  // the group's first channel
+        }
+      } else if (c < Cl && (c & 63) == 0) {
+        chan[c] = t;  // wave partial of the group, at the wave's first channel
+      }
+      __syncthreads();
+      if (cg > 64) {
+        for (int g = tid; g < Cl / cg; g += nt) {
+          float u = 0.f;
+          for (int w = g * cg; w < (g + 1) * cg; w += 64) u += chan[w];
+          const float v = u / count;
+          chan[g * cg] = second ? 1.0f / sqrtf(v + eps) : v;
+        }
+        __syncthreads();
+      }
+    } else {
+      for (int c = tid; c < Cl; c += nt) {
+        float t = 0.f;
+        for (int y = 0; y < slots; ++y) t += part[y * Cl + c];
+        chan[c] = t;
+      }
+      __syncthreads();
+      for (int g = tid; g < Cl / cg; g += nt) {
+        float t = 0.f;
+        for (int c = g * cg; c < (g + 1) * cg; ++c) t += chan[c];
+        const float v = t / count;  // correctly rounded: an exact mean stays exact
+        chan[g * cg] = second ? 1.0f / sqrtf(v + eps) : v;  // the group's first channel
+      }
+      __syncthreads();
+    }
+    for (int c = tid; c < Cl; c += nt) stat[c] = chan[(c / cg) * cg];
+    __syncthreads();
+  };
+
+  i32x4 keep[kResident];
+  float acc[N];
+  // ---- pass 1: sums ------------------------------------------------------------
+#pragma unroll
+  for (int e = 0; e < N; ++e) acc[e] = 0.f;
+  if (resident) {
+#pragma unroll
+    for (int k = 0; k < kResident; ++k) {
+      const int r = ty + k * TY;
+      keep[k] = r < rows ? S[(lo + r) * vpr + tx] : i32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int k = 0; k < kResident; ++k) {
+      float f[N];
+      NV::widen(keep[k], f);  // zeros past the rows add nothing
+#pragma unroll
+      for (int e = 0; e < N; ++e) acc[e] += f[e];
+    }
+  } else {
+    for (int r = ty; r < rows; r += TY) {
+      float f[N];
+      NV::widen(S[(lo + r) * vpr + tx], f);
+#pragma unroll
+      for (int e = 0; e < N; ++e) acc[e] += f[e];
+    }
+  }
+  reduce(acc, false);
+  float mu[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) mu[e] = stat[threadIdx.x * N + e];
+
+  // ---- pass 2: squared deviations from the group mean --------------------------
+#pragma unroll
+  for (int e = 0; e < N; ++e) acc[e] = 0.f;
+  if (resident) {
+#pragma unroll
+    for (int k = 0; k < kResident; ++k) {
+      if (ty + k * TY < rows) {
+        float f[N];
+        NV::widen(keep[k], f);
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+          const float d = f[e] - mu[e];
+          acc[e] += d * d;
+        }
+      }
+    }
+  } else {
+    for (int r = ty; r < rows; r += TY) {
+      float f[N];
+      NV::widen(S[(lo + r) * vpr + tx], f);
+#pragma unroll
+      for (int e = 0; e < N; ++e) {
+        const float d = f[e] - mu[e];
+        acc[e] += d * d;
+      }
+    }
+  }
+  reduce(acc, true);
+  float rs[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) rs[e] = stat[threadIdx.x * N + e];
+
+  // ---- pass 3: normalized values -----------------------------------------------
+  auto emit = [&](const i32x4& v, int r) {
+    float f[N];
+    NV::widen(v, f);
+#pragma unroll
+    for (int e = 0; e < N; ++e) f[e] = (f[e] - mu[e]) * rs[e];
+    __builtin_nontemporal_store(NV::narrow(f), out + (lo + r) * vpr + tx);
+  };
+  if (resident) {
+#pragma unroll
+    for (int k = 0; k < kResident; ++k)
+      if (ty + k * TY < rows) emit(keep[k], ty + k * TY);
+  } else {
+    for (int r = ty; r < rows; r += TY) emit(S[(lo + r) * vpr + tx], r);
+  }
+}
+
+}  // namespace
+
+// Channel ranges per body: the largest power of two F <= num_cus / B (one
+// 1024-thread workgroup fits a CU, so one wave of workgroups) that
+// splits the row's vectors evenly, keeps whole groups in every range and
+// leaves every workgroup at least 64 contiguous bytes of each row.
+int group_norm_split(int32_t B, int32_t C, int32_t G, int is_bf16, int num_cus) {
+  const int vpr = C * (is_bf16 ? 2 : 4) / 16;
+  const int cg = C / G;
+  const int want = std::max(1, num_cus / std::max(1, (int)B));
+  int f = 1;
+  while (2 * f <= want && vpr % (2 * f) == 0 && vpr / (2 * f) >= 4 && (C / (2 * f)) % cg == 0)
+    f *= 2;
+  return f;
+}
+
+size_t group_norm_lds_bytes(int32_t C, int is_bf16, int split) {
+  const int tx = C * (is_bf16 ? 2 : 4) / 16 / split;
+  const int ty = kNormThreads / tx;
+  const int cl = C / split;
+  return (size_t)(ty + 2) * (size_t)cl * sizeof(float);  // covers both reduction layouts
+}
+
+hipError_t launch_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
+                             int32_t C, int32_t G, float eps, int is_bf16, void* out,
+                             int num_cus, hipStream_t stream) {
+  const int vpr = C * (is_bf16 ? 2 : 4) / 16;  // <= 1024 for C <= 4096
+  const int split = group_norm_split(B, C, G, is_bf16, num_cus);
+  const dim3 block(vpr / split, kNormThreads / (vpr / split));
+  const size_t lds = group_norm_lds_bytes(C, is_bf16, split);
+  // up to 64 KB of dynamic LDS (C = 4096 bf16): allow it once per instantiation
+  static std::once_flag once;
+  static hipError_t attr_err = hipSuccess;
+  std::call_once(once, [&] {
+    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(group_norm_kernel<true>),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, 96 * 1024);
+    if (attr_err == hipSuccess)
+      attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(group_norm_kernel<false>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, 96 * 1024);
+  });
+  if (attr_err != hipSuccess) return attr_err;
+  if (B <= 0 || n_rows <= 0) return hipSuccess;
+  if (is_bf16)
+    hipLaunchKernelGGL(group_norm_kernel<true>, dim3(B, split), block, lds, stream,
+                       static_cast<const i32x4*>(S), row_ptr, n_rows, C, G, eps, vpr,
+                       static_cast<i32x4*>(out));
+  else
+    hipLaunchKernelGGL(group_norm_kernel<false>, dim3(B, split), block, lds, stream,
+                       static_cast<const i32x4*>(S), row_ptr, n_rows, C, G, eps, vpr,
+                       static_cast<i32x4*>(out));
+  return hipGetLastError();
+}
+
+}  // namespace shc

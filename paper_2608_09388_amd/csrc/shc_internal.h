@@ -49,6 +49,11 @@ hipError_t launch_compact(const uint8_t* mask, int32_t B, int32_t V, int32_t* co
 hipError_t launch_gather(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
                          int32_t V, int32_t row_bytes, void* S, hipStream_t stream);
 
+int group_norm_split(int32_t B, int32_t C, int32_t G, int is_bf16, int num_cus);
+size_t group_norm_lds_bytes(int32_t C, int is_bf16, int split);
+hipError_t launch_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
+                             int32_t C, int32_t G, float eps, int is_bf16, void* out,
+                             int num_cus, hipStream_t stream);
 hipError_t launch_clear_inactive(const int32_t* inv, int32_t B, int32_t V, int32_t row_bytes,
                                  void* D, hipStream_t stream);
 hipError_t launch_scatter(const void* S, const int32_t* inv, const int32_t* coords,

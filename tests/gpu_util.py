@@ -46,6 +46,28 @@ def assert_scaled_close(got, ref, scale, dtype, what=""):
                              f" got {got[tuple(idx[0])]}, ref {ref[tuple(idx[0])]}")
 
 
+# group normalization: sequential fp32 sums over at most ~280 terms (a
+# thread's rows, the threads of a channel, the channels of a group) bound the
+# error by about 1e-4 * (1 + |ref|) at these sizes; bf16 adds the output's
+# rounding, half an ulp: 2^-8 * |ref|
+GN_ATOL = 1e-4
+GN_RTOL = {"f32": 1e-4, "bf16": 2.0 ** -8 + 1e-4}
+
+
+def assert_gn_close(got, ref, dtype, what=""):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    err = np.abs(got - ref)
+    bound = GN_ATOL + GN_RTOL[dtype] * np.abs(ref)
+    bad = err > bound
+    if bad.any():
+        idx = np.argwhere(bad)[:3]
+        raise AssertionError(f"{what}: {int(bad.sum())} of {bad.size} outside the bound; worst "
+                             f"excess {np.max(err - bound):.3g}; first at {idx.tolist()}")
+
+
 def assert_normwise_close(got, ref, dtype, what=""):
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)

@@ -97,6 +97,24 @@ def test_clear_inactive_rows_validation(lib):
     assert call(B=0) == -1
 
 
+def test_group_norm_validation(lib):
+    def call(S=A, rp=A, n=100, B=4, C=128, G=32, eps=1e-5, dt=1, out=A):
+        return lib.shc_segment_group_norm(S, rp, n, B, C, G, eps, dt, out, None)
+
+    assert call(B=0) == -1
+    assert call(n=-1) == -1
+    assert call(C=8) == -4
+    assert call(dt=9) < 0
+    assert call(G=0) == -1 and "G = 0" in err(lib)
+    assert call(G=3) == -1 and "divide" in err(lib)
+    assert call(eps=0.0) == -1 and "eps" in err(lib)
+    assert call(eps=float("nan")) == -1
+    assert call(n=0, S=None, out=None) == 0        # no-op
+    assert call(S=None) == -1
+    assert call(rp=MIS) == -3
+    assert call(out=MIS) == -3
+
+
 def test_gather_scatter_pool_validation(lib):
     g = lib.shc_gather_rows
     assert g(A, A, 10, 4, 655, 24, 0, A, None) == -4

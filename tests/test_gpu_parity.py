@@ -12,8 +12,8 @@ import torch
 from oracle import shc_oracle as O
 from paper_2608_09388_amd import binding as shc
 from paper_2608_09388_amd import synth
-from tests.gpu_util import (Compaction, assert_normwise_close, assert_scaled_close, down,
-                            require_gpu, up)
+from tests.gpu_util import (Compaction, assert_gn_close, assert_normwise_close,
+                            assert_scaled_close, down, require_gpu, up)
 
 pytestmark = pytest.mark.gpu
 
@@ -333,6 +333,64 @@ def test_sparse_linear_zero_rows_is_noop(dev):
                       out)
     torch.cuda.synchronize()
     assert torch.all(out == 7.0)
+
+
+# ----------------------------------------------------------------------------
+# sparse group normalization (Eqs. 7-9)
+# ----------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("C,G,B,V,p", [
+    (16, 4, 9, 300, 0.3), (128, 32, 12, 2000, 0.05), (128, 1, 12, 2000, 0.05),
+    (48, 3, 6, 700, 0.4), (256, 8, 5, 1500, 0.2), (128, 16, 3, 3000, 0.9),
+    (4096, 64, 3, 200, 0.5), (2048, 2048, 2, 150, 0.6), (48, 1, 4, 500, 0.3),
+    (256, 1, 6, 900, 0.3), (1024, 4, 3, 400, 0.5)])
+def test_group_norm_oracle(dev, dtype, C, G, B, V, p):
+    """Bodies that are empty, of one row, register-resident and streamed (p =
+    0.9: 2700 rows, beyond the resident 1024), channel vectors that span
+    groups (C/G = 4) and groups that span vectors, G = 1 and G = C."""
+    rng = np.random.default_rng(C * 31 + G + B)
+    m = (rng.random((B, V)) < p).astype(np.uint8)
+    m[1] = 0
+    m[2 % B, :] = 0
+    m[2 % B, 5] = 1
+    coords, inv, rp, n = O.compact(m)
+    S = (rng.standard_normal((n, C)) * 2.0 + rng.standard_normal(C) * 3.0).astype(np.float32)
+    S = synth.as_dtype(S, dtype)[1]
+    Sd = up(S, dtype)
+    out = torch.full((n + 3, C), float("nan"), dtype=Sd.dtype, device=dev)
+    shc.segment_group_norm(Sd, up(rp), n, B, G, out)
+    got = down(out)
+    assert np.all(np.isnan(got[n:]))
+    ref = O.group_norm(S.astype(np.float64), rp, G)
+    assert_gn_close(got[:n], ref, dtype, f"group norm C={C} G={G} {dtype}")
+
+
+def test_group_norm_deterministic_and_edge_cases(dev):
+    rng = np.random.default_rng(77)
+    B, V, C, G = 8, 1000, 128, 32
+    m = (rng.random((B, V)) < 0.2).astype(np.uint8)
+    coords, inv, rp, n = O.compact(m)
+    S = up(rng.standard_normal((n, C)).astype(np.float32), "bf16")
+    o1 = torch.empty_like(S)
+    o2 = torch.empty_like(S)
+    shc.segment_group_norm(S, up(rp), n, B, G, o1)
+    shc.segment_group_norm(S, up(rp), n, B, G, o2)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    # a constant body: zero deviation everywhere, outputs exactly zero
+    Sc = torch.full((n, C), 3.25, dtype=torch.float32, device=dev)
+    oc = torch.empty_like(Sc)
+    shc.segment_group_norm(Sc, up(rp), n, B, G, oc)
+    assert torch.all(oc == 0)
+    # N' = 0 is a no-op; bad arguments are refused before any launch
+    shc.segment_group_norm(S[:0], up(np.zeros(B + 1, np.int32)), 0, B, G, o1[:0])
+    for kw, status in ((dict(G=3), -1), (dict(eps=0.0), -1), (dict(eps=float("inf")), -1)):
+        a = dict(G=G, eps=1e-5)
+        a.update(kw)
+        with pytest.raises(shc.ShcError) as e:
+            shc.segment_group_norm(S, up(rp), n, B, a["G"], o1, eps=a["eps"])
+        assert e.value.status == status
 
 
 # ----------------------------------------------------------------------------
