@@ -270,12 +270,17 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
       if (lane == 0) scnt[wave * kMaxSlots + j] = c;
     }
     __syncthreads();
-    uint32_t dense = 0;
-    for (int j = 0; j < K; ++j) {
+    // dense slots (present in at least half of the rows): lane j of wave 0
+    // sums slot j over the wavefronts, the mask goes out through LDS
+    if (wave == 0) {
       int c = 0;
-      for (int w = 0; w < kWaves; ++w) c += scnt[w * kMaxSlots + j];
-      if (2 * c >= nrows) dense |= 1u << j;
+      if (lane < K)
+        for (int w = 0; w < kWaves; ++w) c += scnt[w * kMaxSlots + lane];
+      const uint64_t d = __ballot(lane < K && 2 * c >= nrows);
+      if (lane == 0) scnt[kMaxSlots - 1] = (int32_t)(uint32_t)d;  // slot row of wave 0, K < kMaxSlots
     }
+    __syncthreads();
+    const uint32_t dense = (uint32_t)scnt[kMaxSlots - 1];
     // buckets: 0 = dense slots only, 1 + j = first sparse slot j, K + 1 = past
     // the end, -1 = no such row (t >= R)
     int bkt[kRPT], rank[kRPT];
