@@ -24,6 +24,13 @@ What it computes (Sec. 3.1-3.2 of the paper, arXiv 2608.09388):
 * Pooling is named alongside the other sparse layers but not defined; here
   it is the maximum over the active rows of each body / frame, 0 for a body
   with no active row.
+* Sec. 3.1 (several masks): each mask k of a set of kappa is applied to the
+  same input independently.  Stacked as a batch axis, body b under mask k is
+  body b' = k * B + b of a [kappa * B][V] mask whose rows read the input of
+  body b' mod B; the kappa outputs are then combined by a rule the paper
+  leaves open (sum, mean or maximum here).  A mask drawn per element
+  (vertex and channel) makes a vertex active when any of its channels is
+  kept, and multiplies the gathered row by the element mask.
 * Eqs. 7-9: sparse group normalization.  The channels are split into G
   groups of C/G; for every body / frame b and group g the mean and the
   (biased, 1/N) variance are taken over the group's values in the ACTIVE rows
@@ -258,6 +265,56 @@ def segment_max(S: np.ndarray, row_ptr: np.ndarray, empty_value: float = 0.0) ->
         if hi > lo:
             P[b] = np.fmax.reduce(S[lo:hi], axis=0)
     return P
+
+
+# ----------------------------------------------------------------------------
+# Sec. 3.1: several masks (stacked as a batch axis), per-element masks
+# ----------------------------------------------------------------------------
+
+
+def stack_masks(masks: np.ndarray) -> np.ndarray:
+    """[kappa][B][V] masks -> one [kappa * B][V] mask: row k * B + b is mask k
+    of body b."""
+    m = np.asarray(masks)
+    k, B, V = m.shape
+    return m.reshape(k * B, V)
+
+
+def gather_stacked(x: np.ndarray, coords: np.ndarray, B: int, V: int) -> np.ndarray:
+    """Rows of the stacked batch: row (b', v) reads the input of body b' mod B."""
+    b = coords[:, 0].astype(np.int64) % B
+    return np.asarray(x)[b * V + coords[:, 1].astype(np.int64)]
+
+
+def combine_stacked(Y: np.ndarray, kappa: int, op: str) -> np.ndarray:
+    """Combine kappa stacked outputs [kappa * R][C] -> [R][C], row by row and
+    channel by channel: 'sum', 'mean' or 'max' over k of Y[k * R + r]."""
+    Y = np.asarray(Y, dtype=np.float64)
+    R = Y.shape[0] // kappa
+    out = Y[:R].copy()
+    for k in range(1, kappa):
+        blk = Y[k * R:(k + 1) * R]
+        out = np.maximum(out, blk) if op == "max" else out + blk
+    if op == "mean":
+        out = out / kappa
+    elif op not in ("sum", "max"):
+        raise ValueError(op)
+    return out
+
+
+def row_mask_from_elements(me: np.ndarray) -> np.ndarray:
+    """Per-element mask [B][V][C] -> per-vertex activity [B][V]: a vertex is
+    active when any of its channels is kept."""
+    return (np.asarray(me) != 0).any(axis=2).astype(np.uint8)
+
+
+def gather_masked(x: np.ndarray, me: np.ndarray, coords: np.ndarray, V: int) -> np.ndarray:
+    """Active rows of the element-masked input: x[b, v, c] where the element
+    mask keeps (b, v, c), else 0."""
+    rows = coords[:, 0].astype(np.int64) * V + coords[:, 1].astype(np.int64)
+    C = np.asarray(x).shape[-1]
+    keep = (np.asarray(me).reshape(-1, C)[rows] != 0)
+    return np.where(keep, np.asarray(x)[rows], 0)
 
 
 # ----------------------------------------------------------------------------

@@ -351,6 +351,77 @@ def test_segment_max_ignores_nan_and_equals_dense_pool_after_relu():
 
 
 # ----------------------------------------------------------------------------
+# several masks stacked as a batch axis; per-element masks (Sec. 3.1)
+# ----------------------------------------------------------------------------
+
+
+def test_stacked_masks_equal_separate_runs():
+    """Mask k of body b as body k * B + b: the stacked compaction and gather
+    give, block by block, exactly what each mask gives on its own."""
+    rng = np.random.default_rng(21)
+    kappa, B, V, C = 3, 4, 30, 5
+    masks = (rng.random((kappa, B, V)) < 0.3).astype(np.uint8)
+    x = rng.standard_normal((B * V, C))
+    st = O.stack_masks(masks)
+    assert st.shape == (kappa * B, V)
+    coords, inv, rp, n = O.compact(st)
+    S = O.gather_stacked(x, coords, B, V)
+    for k in range(kappa):
+        ck, _, _, nk = O.compact(masks[k])
+        lo, hi = rp[k * B], rp[(k + 1) * B]
+        assert hi - lo == nk
+        np.testing.assert_array_equal(coords[lo:hi, 0] - k * B, ck[:, 0])
+        np.testing.assert_array_equal(coords[lo:hi, 1], ck[:, 1])
+        np.testing.assert_array_equal(S[lo:hi], O.gather(x, ck, V))
+    # brute force: every stacked row is the masked input of its body
+    for i in range(n):
+        bp, v = coords[i]
+        assert masks[bp // B, bp % B, v] == 1
+        np.testing.assert_array_equal(S[i], x[(bp % B) * V + v])
+
+
+def test_combine_stacked_brute_force_and_invariants():
+    rng = np.random.default_rng(22)
+    kappa, R, C = 3, 4, 3
+    Y = rng.standard_normal((kappa * R, C))
+    for op in ("sum", "mean", "max"):
+        got = O.combine_stacked(Y, kappa, op)
+        for r in range(R):
+            for c in range(C):
+                vals = [float(Y[k * R + r, c]) for k in range(kappa)]
+                exp = {"sum": sum(vals), "mean": sum(vals) / kappa, "max": max(vals)}[op]
+                assert abs(got[r, c] - exp) < 1e-12
+    Z = np.tile(Y[:R], (kappa, 1))       # kappa identical copies
+    np.testing.assert_allclose(O.combine_stacked(Z, kappa, "sum"), kappa * Y[:R], rtol=1e-15)
+    np.testing.assert_allclose(O.combine_stacked(Z, kappa, "mean"), Y[:R], rtol=1e-15)
+    np.testing.assert_array_equal(O.combine_stacked(Z, kappa, "max"), Y[:R])
+    np.testing.assert_array_equal(O.combine_stacked(Y, 1, "max"), Y)
+
+
+def test_element_masks_brute_force_and_broadcast_case():
+    rng = np.random.default_rng(23)
+    B, V, C = 3, 7, 4
+    me = (rng.random((B, V, C)) < 0.3).astype(np.uint8)
+    x = rng.standard_normal((B * V, C))
+    m = O.row_mask_from_elements(me)
+    for b in range(B):
+        for v in range(V):
+            assert m[b, v] == (1 if any(me[b, v, c] for c in range(C)) else 0)
+    coords, inv, rp, n = O.compact(m)
+    S = O.gather_masked(x, me, coords, V)
+    for i in range(n):
+        b, v = coords[i]
+        for c in range(C):
+            assert S[i, c] == (x[b * V + v, c] if me[b, v, c] else 0.0)
+    # a mask drawn per vertex and broadcast over channels is the vertex path
+    mv = (rng.random((B, V)) < 0.4).astype(np.uint8)
+    meb = np.repeat(mv[:, :, None], C, axis=2)
+    np.testing.assert_array_equal(O.row_mask_from_elements(meb), mv)
+    cv, _, _, _ = O.compact(mv)
+    np.testing.assert_array_equal(O.gather_masked(x, meb, cv, V), O.gather(x, cv, V))
+
+
+# ----------------------------------------------------------------------------
 # group normalization (Eqs. 7-9)
 # ----------------------------------------------------------------------------
 
