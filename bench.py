@@ -260,7 +260,8 @@ def main():
         "roofline": roof,
     }
 
-    out["next_rows"] = {"group_norm": group_norm_measure(st, shc, torch, args.reps)}
+    out["next_rows"] = {"group_norm": group_norm_measure(st, shc, torch, args.reps),
+                        "multi_mask": multi_mask_measure(st, w, shc, synth, torch, args.reps)}
     log("group norm measured")
 
     if not args.no_dense:
@@ -299,6 +300,66 @@ def group_norm_measure(st, shc, torch, reps, G=32):
                       f"{st.B} bodies", "launch_us": round(us, 2), "algorithmic_bytes": nbytes,
             "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(ach / HBM_PEAK_GBS, 4)}
+
+
+def _time_us(fn, torch, reps):
+    for _ in range(3):
+        fn()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(reps):
+        fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps * 1e3
+
+
+def multi_mask_measure(st, w, shc, synth, torch, reps, kappa=3):
+    """Several masks on the same input (kappa = 3 stacked as bodies k*B + b,
+    each Bernoulli at the workload's density) and a mask drawn per element:
+    HBM rates of the stacked gather, of the combination of the kappa dense
+    outputs, of the per-element row activity and of the masked gather."""
+    dev = st.device
+    B, V, C = w.B, w.V, st.x.shape[-1]
+    e = st.x.element_size()
+    rng = np.random.default_rng(4242)
+    masks = (rng.random((kappa * B, V)) < float(w.mask.mean())).astype(np.uint8)
+    md = torch.from_numpy(masks.reshape(-1)).to(dev)
+    Bs = kappa * B
+    coords = torch.empty((Bs * V, 2), dtype=torch.int32, device=dev)
+    inv = torch.empty(Bs * V, dtype=torch.int32, device=dev)
+    rp = torch.empty(Bs + 1, dtype=torch.int32, device=dev)
+    nd = torch.empty(4, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(shc.compact_mask_workspace(Bs, V), 16), dtype=torch.uint8, device=dev)
+    n = shc.compact_mask(md, Bs, V, coords, inv, rp, nd, ws)
+    S = torch.empty((n, C), dtype=st.x.dtype, device=dev)
+    res = {"config": f"kappa={kappa} masks at p={float(w.mask.mean()):.3f} stacked as "
+                     f"{Bs} bodies of V={V}, C={C}, N'={n}"}
+
+    def rate(name, us, nbytes):
+        ach = nbytes / (us * 1e-6) / 1e9
+        res[name] = {"launch_us": round(us, 2), "algorithmic_bytes": int(nbytes),
+                     "achieved": round(ach, 1), "unit": "GB/s",
+                     "frac": round(ach / HBM_PEAK_GBS, 4)}
+
+    us = _time_us(lambda: shc.gather_rows_stacked(st.x, coords, n, B, kappa, V, S), torch, reps)
+    rate("gather_stacked", us, n * (8 + 2 * C * e))
+    Y = torch.randn((Bs * V, C), device=dev).to(st.x.dtype)
+    Dc = torch.empty((B * V, C), dtype=st.x.dtype, device=dev)
+    us = _time_us(lambda: shc.combine_stacked(Y, kappa, B * V, Dc, "mean"), torch, reps)
+    rate("combine_dense_mean", us, (kappa + 1) * B * V * C * e)
+    del Y, Dc
+    me = (torch.rand((B * V, C), device=dev) < 0.002).to(torch.uint8)
+    m = torch.empty(B * V, dtype=torch.uint8, device=dev)
+    us = _time_us(lambda: shc.row_mask_from_elements(me, B, V, m), torch, reps)
+    rate("row_activity", us, B * V * (C + 1))
+    n2 = shc.compact_mask(m, B, V, coords, inv, rp, nd, ws)
+    S2 = torch.empty((n2, C), dtype=st.x.dtype, device=dev)
+    us = _time_us(lambda: shc.gather_rows_masked(st.x, me, coords, n2, B, V, S2), torch, reps)
+    rate("gather_masked", us, n2 * (8 + C + 2 * C * e))
+    res["masked_rows"] = n2
+    return res
 
 
 def dense_comparison(st, w, per_kernel_ms, torch, shc, synth):

@@ -140,6 +140,49 @@ int shc_gather_rows(const void* x, const int32_t* coords, int64_t n_rows, int32_
                     int32_t C, int32_t dtype, void* S, hipStream_t stream);
 
 /*
+ * Several masks applied to the same input (Sec. 3.1), stacked as a batch
+ * axis: mask k of body b is body b' = k * B + b of a [kappa * B][V] mask
+ * (compacted by shc_compact_mask like any other), and every layer call then
+ * takes kappa * B bodies unchanged.
+ *
+ * shc_gather_rows_stacked -- S[i] = x[(b'_i mod B) * V + v_i]: the rows of
+ *   the stacked batch read the input of their own body.  x [B*V][C]; coords
+ *   [n_rows][2] with b' in [0, kappa * B) (others read zeros).  An exact copy.
+ * shc_combine_stacked -- combines kappa stacked outputs, row by row and
+ *   channel by channel (the paper leaves the rule open):
+ *     out[r] = op over k < kappa of Y[k * rows + r],   r < rows,
+ *   op = SHC_COMBINE_SUM, SHC_COMBINE_MEAN (the sum divided by kappa) or
+ *   SHC_COMBINE_MAX.  Y [kappa * rows][C] (e.g. dense outputs with rows =
+ *   B*V, or pooled outputs with rows = B), out [rows][C].  Sums are taken in
+ *   fp32 in k order and rounded once; the maximum is exact (inputs are
+ *   numbers).
+ */
+int shc_gather_rows_stacked(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
+                            int32_t kappa, int32_t V, int32_t C, int32_t dtype, void* S,
+                            hipStream_t stream);
+#define SHC_COMBINE_SUM 0
+#define SHC_COMBINE_MEAN 1
+#define SHC_COMBINE_MAX 2
+int shc_combine_stacked(const void* Y, int32_t kappa, int64_t rows, int32_t C, int32_t dtype,
+                        int32_t op, void* out, hipStream_t stream);
+
+/*
+ * A mask drawn per element (vertex and channel) instead of per vertex:
+ *
+ * shc_row_mask_from_elements -- m[b*V + v] = 1 when any of the C bytes
+ *   me[(b*V + v)*C + c] is non-zero, else 0: the vertex activity that
+ *   shc_compact_mask then takes.  me [B*V][C] uint8, m [B*V] uint8.
+ * shc_gather_rows_masked -- S[i][c] = x[(b_i V + v_i)][c] where
+ *   me[(b_i V + v_i)][c] is non-zero, else 0: the gathered rows multiplied by
+ *   the element mask.  Arguments as for shc_gather_rows plus me.
+ */
+int shc_row_mask_from_elements(const uint8_t* me, int32_t B, int32_t V, int32_t C, uint8_t* m,
+                               hipStream_t stream);
+int shc_gather_rows_masked(const void* x, const uint8_t* me, const int32_t* coords,
+                           int64_t n_rows, int32_t B, int32_t V, int32_t C, int32_t dtype,
+                           void* S, hipStream_t stream);
+
+/*
  * Sparse linear layer -- Eq. 6 (+ Eq. 10): out[i] = act(S[i] W + bias).
  *
  *   S     [n_rows][Cin] active feature rows (coordinates unchanged, C' = C).

@@ -22,6 +22,8 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "shc.h")
 
 SHC_F32, SHC_BF16 = 0, 1
 SHC_ACT_NONE, SHC_ACT_RELU = 0, 1
+SHC_COMBINE_SUM, SHC_COMBINE_MEAN, SHC_COMBINE_MAX = 0, 1, 2
+COMBINE = {"sum": SHC_COMBINE_SUM, "mean": SHC_COMBINE_MEAN, "max": SHC_COMBINE_MAX}
 STATUS = {0: "SHC_OK", -1: "SHC_ERR_INVALID_ARG", -2: "SHC_ERR_CAPACITY",
           -3: "SHC_ERR_MISALIGNED", -4: "SHC_ERR_UNSUPPORTED", -5: "SHC_ERR_HIP"}
 
@@ -49,6 +51,14 @@ _SIGS = {
                                                _c_ptr]),
     "shc_gather_rows": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
                                        _c_ptr, _c_ptr]),
+    "shc_gather_rows_stacked": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32,
+                                               _c_i32, _c_i32, _c_ptr, _c_ptr]),
+    "shc_gather_rows_masked": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32,
+                                              _c_i32, _c_i32, _c_ptr, _c_ptr]),
+    "shc_row_mask_from_elements": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_i32, _c_ptr,
+                                                  _c_ptr]),
+    "shc_combine_stacked": (ctypes.c_int, [_c_ptr, _c_i32, _c_i64, _c_i32, _c_i32, _c_i32,
+                                           _c_ptr, _c_ptr]),
     "shc_sparse_linear": (ctypes.c_int, [_c_ptr, _c_i64, _c_ptr, _c_ptr, _c_i32, _c_i32, _c_i32,
                                          _c_i32, _c_ptr, _c_ptr]),
     "shc_gather_sparse_linear": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_ptr,
@@ -186,6 +196,44 @@ def gather_rows(x: torch.Tensor, coords: torch.Tensor, n_rows: int, B: int, V: i
     args = [_dev(x, "x", x.dtype, B * V * C), _dev(coords, "coords", torch.int32, 2 * n_rows),
             n_rows, B, V, C, dt, _dev(S, "S", x.dtype, n_rows * C), _stream(stream)]
     _check(load().shc_gather_rows(*args), "shc_gather_rows")
+
+
+def gather_rows_stacked(x: torch.Tensor, coords: torch.Tensor, n_rows: int, B: int,
+                        kappa: int, V: int, S: torch.Tensor, stream=None):
+    """shc_gather_rows_stacked: S[i] = x[(b'_i mod B) * V + v_i]."""
+    C = x.shape[-1]
+    args = [_dev(x, "x", x.dtype, B * V * C), _dev(coords, "coords", torch.int32, 2 * n_rows),
+            n_rows, B, kappa, V, C, _dtype_code(x), _dev(S, "S", x.dtype, n_rows * C),
+            _stream(stream)]
+    _check(load().shc_gather_rows_stacked(*args), "shc_gather_rows_stacked")
+
+
+def gather_rows_masked(x: torch.Tensor, me: torch.Tensor, coords: torch.Tensor, n_rows: int,
+                       B: int, V: int, S: torch.Tensor, stream=None):
+    """shc_gather_rows_masked: gathered rows times the per-element mask ``me`` [B*V][C]."""
+    C = x.shape[-1]
+    args = [_dev(x, "x", x.dtype, B * V * C), _dev(me, "me", torch.uint8, B * V * C),
+            _dev(coords, "coords", torch.int32, 2 * n_rows), n_rows, B, V, C, _dtype_code(x),
+            _dev(S, "S", x.dtype, n_rows * C), _stream(stream)]
+    _check(load().shc_gather_rows_masked(*args), "shc_gather_rows_masked")
+
+
+def row_mask_from_elements(me: torch.Tensor, B: int, V: int, m: torch.Tensor, stream=None):
+    """shc_row_mask_from_elements: m[b*V + v] = any(me[b*V + v, :])."""
+    C = me.numel() // (B * V)
+    args = [_dev(me, "me", torch.uint8, B * V * C), B, V, C, _dev(m, "m", torch.uint8, B * V),
+            _stream(stream)]
+    _check(load().shc_row_mask_from_elements(*args), "shc_row_mask_from_elements")
+
+
+def combine_stacked(Y: torch.Tensor, kappa: int, rows: int, out: torch.Tensor, op="mean",
+                    stream=None):
+    """shc_combine_stacked: out[r] = op over k of Y[k * rows + r] ('sum', 'mean', 'max')."""
+    C = Y.shape[-1]
+    args = [_dev(Y, "Y", Y.dtype, kappa * rows * C), kappa, rows, C, _dtype_code(Y),
+            COMBINE[op] if isinstance(op, str) else int(op), _dev(out, "out", Y.dtype, rows * C),
+            _stream(stream)]
+    _check(load().shc_combine_stacked(*args), "shc_combine_stacked")
 
 
 def sparse_linear(S: torch.Tensor, n_rows: int, W: torch.Tensor, bias: Optional[torch.Tensor],

@@ -226,6 +226,75 @@ int shc_gather_rows(const void* x, const int32_t* coords, int64_t n_rows, int32_
                     "gather_rows launch");
 }
 
+int shc_gather_rows_stacked(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
+                            int32_t kappa, int32_t V, int32_t C, int32_t dtype, void* S,
+                            hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (kappa <= 0) return fail(SHC_ERR_INVALID_ARG, "kappa = %d must be positive", kappa);
+  if ((int64_t)kappa * B > 0x7FFFFFFFLL)
+    return fail(SHC_ERR_UNSUPPORTED, "kappa * B = %lld bodies exceed int32", (long long)kappa * B);
+  SHC_TRY(check_bv(kappa * B, V));
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("C", C));
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(x, "x");
+  SHC_PTR(coords, "coords");
+  SHC_PTR(S, "S");
+  const int32_t row_bytes = C * (dtype == SHC_BF16 ? 2 : 4);
+  return hip_status(shc::launch_gather_ext(x, nullptr, 0, coords, n_rows, kappa * B, B, V,
+                                           row_bytes, S, stream),
+                    "gather_rows_stacked launch");
+}
+
+int shc_gather_rows_masked(const void* x, const uint8_t* me, const int32_t* coords,
+                           int64_t n_rows, int32_t B, int32_t V, int32_t C, int32_t dtype,
+                           void* S, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("C", C));
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(x, "x");
+  SHC_PTR(me, "me");
+  SHC_PTR(coords, "coords");
+  SHC_PTR(S, "S");
+  const int32_t row_bytes = C * (dtype == SHC_BF16 ? 2 : 4);
+  return hip_status(shc::launch_gather_ext(x, me, dtype == SHC_BF16 ? 1 : 2, coords, n_rows, B, B,
+                                           V, row_bytes, S, stream),
+                    "gather_rows_masked launch");
+}
+
+int shc_row_mask_from_elements(const uint8_t* me, int32_t B, int32_t V, int32_t C, uint8_t* m,
+                               hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_channels("C", C));
+  SHC_PTR(me, "me");
+  SHC_PTR(m, "m");
+  return hip_status(shc::launch_row_activity(me, B, V, C, m, stream),
+                    "row_mask_from_elements launch");
+}
+
+int shc_combine_stacked(const void* Y, int32_t kappa, int64_t rows, int32_t C, int32_t dtype,
+                        int32_t op, void* out, hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (kappa <= 0) return fail(SHC_ERR_INVALID_ARG, "kappa = %d must be positive", kappa);
+  SHC_TRY(check_rows(rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("C", C));
+  if (op != SHC_COMBINE_SUM && op != SHC_COMBINE_MEAN && op != SHC_COMBINE_MAX)
+    return fail(SHC_ERR_UNSUPPORTED, "unknown combination code %d", op);
+  if (rows == 0) return SHC_OK;
+  SHC_PTR(Y, "Y");
+  SHC_PTR(out, "out");
+  const int32_t row_bytes = C * (dtype == SHC_BF16 ? 2 : 4);
+  return hip_status(shc::launch_combine(Y, kappa, rows, row_bytes, op, dtype == SHC_BF16, out,
+                                        stream),
+                    "combine_stacked launch");
+}
+
 int shc_sparse_linear(const void* S, int64_t n_rows, const void* W, const float* bias, int32_t Cin,
                       int32_t Cout, int32_t dtype, int32_t act, void* out, hipStream_t stream) {
   g_last_error[0] = 0;

@@ -34,10 +34,17 @@ RowShape row_shape(int32_t row_bytes) {
 // reads row 0 and stores zeros.
 constexpr int kGatherRows = 4;
 
+// MASK: 0 = plain rows; 1 / 2 = rows multiplied by a per-element 0/1 mask
+// of bf16 / fp32 channels (8 / 4 mask bytes per 16-byte vector).  Coordinates
+// name bodies in [0, B); body b reads input body b mod Bx (Bx = B but for
+// several masks stacked as a batch axis).
+template <int MASK>
 __global__ __launch_bounds__(kThreads) void gather_kernel(const i32x4* __restrict__ x,
+                                                          const uint8_t* __restrict__ me,
                                                           const int2* __restrict__ coords,
-                                                          int64_t n_rows, int32_t B, int32_t V,
-                                                          int vpr, i32x4* __restrict__ S) {
+                                                          int64_t n_rows, int32_t B, int32_t Bx,
+                                                          int32_t V, int vpr,
+                                                          i32x4* __restrict__ S) {
   const int ty = blockDim.y;
   const int64_t i0 = (int64_t)blockIdx.x * kGatherRows * ty + threadIdx.y;
   int64_t src[kGatherRows];
@@ -47,18 +54,105 @@ __global__ __launch_bounds__(kThreads) void gather_kernel(const i32x4* __restric
     const int64_t i = min(i0 + (int64_t)k * ty, n_rows - 1);
     const int2 c = coords[i];
     ok[k] = c.x >= 0 && c.x < B && c.y >= 0 && c.y < V;
-    src[k] = ok[k] ? ((int64_t)c.x * V + c.y) * vpr : 0;
+    const int bx = c.x < Bx ? c.x : c.x % Bx;
+    src[k] = ok[k] ? ((int64_t)bx * V + c.y) * vpr : 0;
   }
   for (int q = threadIdx.x; q < vpr; q += blockDim.x) {
     i32x4 val[kGatherRows];
 #pragma unroll
     for (int k = 0; k < kGatherRows; ++k) val[k] = __builtin_nontemporal_load(x + src[k] + q);
+    if (MASK != 0) {
+      constexpr int kPer = MASK == 1 ? 8 : 4;  // channels (mask bytes) per vector
+#pragma unroll
+      for (int k = 0; k < kGatherRows; ++k) {
+        const uint8_t* mb = me + (src[k] + q) * kPer;  // element (row, channel) mask bytes
+        uint64_t bytes = MASK == 1 ? *reinterpret_cast<const uint64_t*>(mb)
+                                   : (uint64_t)*reinterpret_cast<const uint32_t*>(mb);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          uint32_t keep;
+          if (MASK == 1) {
+            keep = (((bytes >> (16 * e)) & 0xFFu) ? 0x0000FFFFu : 0u) |
+                   (((bytes >> (16 * e + 8)) & 0xFFu) ? 0xFFFF0000u : 0u);
+          } else {
+            keep = ((bytes >> (8 * e)) & 0xFFu) ? 0xFFFFFFFFu : 0u;
+          }
+          val[k][e] &= (int)keep;
+        }
+      }
+    }
 #pragma unroll
     for (int k = 0; k < kGatherRows; ++k) {
       const int64_t i = i0 + (int64_t)k * ty;
       if (i < n_rows) S[i * vpr + q] = ok[k] ? val[k] : i32x4{0, 0, 0, 0};
     }
   }
+}
+
+// out[v] = op over k < kappa of Y[k * n_vec + v], per channel of 16-byte
+// vector v (OP 0 sum, 1 mean, 2 max), accumulated in fp32 in k order.
+template <int OP, bool BF16>
+__global__ __launch_bounds__(kThreads) void combine_kernel(const i32x4* __restrict__ Y,
+                                                           int32_t kappa, int64_t n_vec,
+                                                           i32x4* __restrict__ out) {
+  const int64_t v = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (v >= n_vec) return;
+  constexpr int N = BF16 ? 8 : 4;
+  float acc[N];
+  auto widen = [&](const i32x4& w, float* f) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (BF16) {
+        f[2 * e] = __int_as_float(w[e] << 16);
+        f[2 * e + 1] = __int_as_float(w[e] & (int)0xFFFF0000);
+      } else {
+        f[e] = __int_as_float(w[e]);
+      }
+    }
+  };
+  widen(__builtin_nontemporal_load(Y + v), acc);
+  for (int k = 1; k < kappa; ++k) {
+    float f[N];
+    widen(__builtin_nontemporal_load(Y + (int64_t)k * n_vec + v), f);
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc[e] = OP == 2 ? (f[e] > acc[e] ? f[e] : acc[e]) : acc[e] + f[e];
+  }
+  if (OP == 1)
+#pragma unroll
+    for (int e = 0; e < N; ++e) acc[e] = acc[e] / (float)kappa;
+  i32x4 o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    if (BF16) {  // hardware round-to-nearest-even conversion, two channels at a time
+      typedef float f2 __attribute__((ext_vector_type(2)));
+      typedef __bf16 h2 __attribute__((ext_vector_type(2)));
+      o[e] = __builtin_bit_cast(int, __builtin_convertvector(f2{acc[2 * e], acc[2 * e + 1]}, h2));
+    } else {
+      o[e] = __float_as_int(acc[e]);
+    }
+  }
+  __builtin_nontemporal_store(o, out + v);
+}
+
+// m[b * V + v] = 1 when any of the C mask bytes of (b, v) is non-zero, else 0.
+// tx lanes (a power of two <= 64) share a vertex, each ORing every tx-th of
+// its C / 16 chunks, and a ballot over the wavefront ORs the vertex's lanes.
+__global__ __launch_bounds__(kThreads) void row_activity_kernel(const i32x4* __restrict__ me,
+                                                                int64_t n_vert, int vpr, int tx,
+                                                                uint8_t* __restrict__ m) {
+  const int lane = threadIdx.x & 63;
+  const int64_t vert = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / tx;
+  const int sub = lane % tx;
+  bool nz = false;
+  if (vert < n_vert)
+    for (int q = sub; q < vpr; q += tx) {
+      const i32x4 w = __builtin_nontemporal_load(me + vert * vpr + q);
+      nz |= (w[0] | w[1] | w[2] | w[3]) != 0;
+    }
+  const uint64_t bal = __ballot(nz);
+  const int slot = lane / tx;
+  const uint64_t lanes = (tx == 64 ? ~0ull : ((1ull << tx) - 1ull)) << (slot * tx);
+  if (vert < n_vert && sub == 0) m[vert] = (bal & lanes) ? 1 : 0;
 }
 
 // D[r] = S[inv[r]] or zeros, for every dense row r (COPY); or (!COPY) zeros
@@ -203,13 +297,58 @@ __global__ __launch_bounds__(kPoolThreads) void segment_max_kernel(
 
 hipError_t launch_gather(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
                          int32_t V, int32_t row_bytes, void* S, hipStream_t stream) {
+  return launch_gather_ext(x, nullptr, 0, coords, n_rows, B, B, V, row_bytes, S, stream);
+}
+
+hipError_t launch_gather_ext(const void* x, const uint8_t* me, int mask_mode,
+                             const int32_t* coords, int64_t n_rows, int32_t B, int32_t Bx,
+                             int32_t V, int32_t row_bytes, void* S, hipStream_t stream) {
   if (n_rows <= 0) return hipSuccess;
   const RowShape s = row_shape(row_bytes);
   const int64_t per_block = (int64_t)s.ty * kGatherRows;
   const int64_t blocks = (n_rows + per_block - 1) / per_block;
-  hipLaunchKernelGGL(gather_kernel, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0, stream,
-                     static_cast<const i32x4*>(x), reinterpret_cast<const int2*>(coords), n_rows,
-                     B, V, s.vpr, static_cast<i32x4*>(S));
+  const auto* xv = static_cast<const i32x4*>(x);
+  const auto* cv = reinterpret_cast<const int2*>(coords);
+  auto* sv = static_cast<i32x4*>(S);
+  if (mask_mode == 1)
+    hipLaunchKernelGGL(gather_kernel<1>, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0, stream, xv,
+                       me, cv, n_rows, B, Bx, V, s.vpr, sv);
+  else if (mask_mode == 2)
+    hipLaunchKernelGGL(gather_kernel<2>, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0, stream, xv,
+                       me, cv, n_rows, B, Bx, V, s.vpr, sv);
+  else
+    hipLaunchKernelGGL(gather_kernel<0>, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0, stream, xv,
+                       me, cv, n_rows, B, Bx, V, s.vpr, sv);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const void* Y, int32_t kappa, int64_t rows, int32_t row_bytes, int op,
+                          int is_bf16, void* out, hipStream_t stream) {
+  const int64_t n_vec = rows * (row_bytes / 16);
+  if (n_vec <= 0) return hipSuccess;
+  const int64_t blocks = (n_vec + kThreads - 1) / kThreads;
+  const auto* y = static_cast<const i32x4*>(Y);
+  auto* o = static_cast<i32x4*>(out);
+#define SHC_COMBINE(OPV, BF)                                                                \
+  if (op == OPV && (is_bf16 != 0) == BF)                                                    \
+    hipLaunchKernelGGL((combine_kernel<OPV, BF>), dim3((unsigned)blocks), dim3(kThreads), 0, \
+                       stream, y, kappa, n_vec, o);
+  SHC_COMBINE(0, true) SHC_COMBINE(1, true) SHC_COMBINE(2, true)
+  SHC_COMBINE(0, false) SHC_COMBINE(1, false) SHC_COMBINE(2, false)
+#undef SHC_COMBINE
+  return hipGetLastError();
+}
+
+hipError_t launch_row_activity(const uint8_t* me, int32_t B, int32_t V, int32_t C, uint8_t* m,
+                               hipStream_t stream) {
+  const int64_t n_vert = (int64_t)B * V;
+  const int vpr = C / 16;  // 16-byte chunks of mask bytes per vertex
+  int tx = 1;              // lanes per vertex: a power of two <= min(vpr, 64)
+  while (2 * tx <= vpr && 2 * tx <= 64) tx *= 2;
+  const int64_t threads = n_vert * tx;
+  const int64_t blocks = (threads + kThreads - 1) / kThreads;
+  hipLaunchKernelGGL(row_activity_kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream,
+                     reinterpret_cast<const i32x4*>(me), n_vert, vpr, tx, m);
   return hipGetLastError();
 }
 

@@ -56,6 +56,13 @@ hipError_t launch_group_norm(const void* S, const int32_t* row_ptr, int64_t n_ro
                              int num_cus, hipStream_t stream);
 hipError_t launch_clear_inactive(const int32_t* inv, int32_t B, int32_t V, int32_t row_bytes,
                                  void* D, hipStream_t stream);
+hipError_t launch_gather_ext(const void* x, const uint8_t* me, int mask_mode,
+                             const int32_t* coords, int64_t n_rows, int32_t B, int32_t Bx,
+                             int32_t V, int32_t row_bytes, void* S, hipStream_t stream);
+hipError_t launch_combine(const void* Y, int32_t kappa, int64_t rows, int32_t row_bytes, int op,
+                          int is_bf16, void* out, hipStream_t stream);
+hipError_t launch_row_activity(const uint8_t* me, int32_t B, int32_t V, int32_t C, uint8_t* m,
+                               hipStream_t stream);
 hipError_t launch_scatter(const void* S, const int32_t* inv, const int32_t* coords,
                           int64_t n_rows, int32_t B, int32_t V, int32_t row_bytes, int zero_fill,
                           void* D, hipStream_t stream);

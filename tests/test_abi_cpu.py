@@ -115,6 +115,39 @@ def test_group_norm_validation(lib):
     assert call(out=MIS) == -3
 
 
+def test_multi_mask_validation(lib):
+    def stacked(x=A, c=A, n=10, B=4, kappa=3, V=655, C=128, dt=1, S=A):
+        return lib.shc_gather_rows_stacked(x, c, n, B, kappa, V, C, dt, S, None)
+
+    assert stacked(kappa=0) == -1 and "kappa" in err(lib)
+    assert stacked(B=0) == -1
+    assert stacked(kappa=1 << 20, B=1 << 12) == -4
+    assert stacked(C=8) == -4
+    assert stacked(n=0, x=None, c=None, S=None) == 0
+    assert stacked(x=None) == -1
+    assert stacked(S=MIS) == -3
+
+    def combine(Y=A, kappa=3, rows=100, C=128, dt=1, op=1, out=A):
+        return lib.shc_combine_stacked(Y, kappa, rows, C, dt, op, out, None)
+
+    assert combine(kappa=0) == -1
+    assert combine(op=3) == -4 and "combination" in err(lib)
+    assert combine(rows=-1) == -1
+    assert combine(rows=0, Y=None, out=None) == 0
+    assert combine(Y=MIS) == -3
+
+    assert lib.shc_row_mask_from_elements(None, 4, 655, 128, A, None) == -1
+    assert lib.shc_row_mask_from_elements(A, 4, 655, 24, A, None) == -4
+    assert lib.shc_row_mask_from_elements(A, 0, 655, 128, A, None) == -1
+
+    def masked(x=A, me=A, c=A, n=10, B=4, V=655, C=128, dt=1, S=A):
+        return lib.shc_gather_rows_masked(x, me, c, n, B, V, C, dt, S, None)
+
+    assert masked(me=None) == -1 and "me" in err(lib)
+    assert masked(me=MIS) == -3
+    assert masked(n=0, x=None, me=None, c=None, S=None) == 0
+
+
 def test_gather_scatter_pool_validation(lib):
     g = lib.shc_gather_rows
     assert g(A, A, 10, 4, 655, 24, 0, A, None) == -4

@@ -336,6 +336,126 @@ def test_sparse_linear_zero_rows_is_noop(dev):
 
 
 # ----------------------------------------------------------------------------
+# several masks stacked as a batch axis; per-element masks (Sec. 3.1)
+# ----------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 128])
+def test_stacked_gather_exact(dev, dtype, C):
+    rng = np.random.default_rng(C + 3)
+    kappa, B, V = 3, 5, 600
+    masks = (rng.random((kappa, B, V)) < 0.2).astype(np.uint8)
+    x = synth.as_dtype(rng.standard_normal((B * V, C)).astype(np.float32), dtype)[1]
+    st = O.stack_masks(masks)
+    c = Compaction(st)
+    n = c.run()
+    S = torch.full((n + 4, C), float("nan"), dtype=synth_dtype(dtype), device=dev)
+    shc.gather_rows_stacked(up(x, dtype), c.coords, n, B, kappa, V, S)
+    ref_c, _, _, _ = O.compact(st)
+    got = down(S)
+    assert np.array_equal(got[:n], O.gather_stacked(x, ref_c, B, V))
+    assert np.all(np.isnan(got[n:]))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("op", ["sum", "mean", "max"])
+def test_combine_stacked(dev, dtype, op):
+    """Max is exact; sum and mean are fp32 sums in k order rounded once:
+    |err| <= (kappa + 1) 2^-24 sum_k |y_k| + (half an ulp of the output)."""
+    rng = np.random.default_rng(5)
+    kappa, R, C = 4, 1000, 48
+    Y = synth.as_dtype(rng.standard_normal((kappa * R, C)).astype(np.float32) * 3, dtype)[1]
+    out = torch.full((R + 2, C), float("nan"), dtype=synth_dtype(dtype), device=dev)
+    shc.combine_stacked(up(Y, dtype), kappa, R, out, op)
+    got = down(out)
+    assert np.all(np.isnan(got[R:]))
+    ref = O.combine_stacked(Y.astype(np.float64), kappa, op)
+    if op == "max":
+        assert np.array_equal(got[:R], ref)
+    else:
+        sa = np.abs(Y.astype(np.float64)).reshape(kappa, R, C).sum(0)
+        if op == "mean":
+            sa = sa / kappa
+        half_ulp = 2.0 ** -8 if dtype == "bf16" else 2.0 ** -24
+        bound = (kappa + 1) * 2.0 ** -24 * sa + half_ulp * np.abs(ref)
+        assert np.all(np.abs(got[:R] - ref) <= bound)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_multi_mask_stack_vs_oracle(dev, dtype):
+    """kappa = 3 masks as bodies k * B + b through the whole path (stacked
+    gather, linear, conv from the table, zero-fill scatter, pool), then the
+    kappa dense and pooled outputs combined; against the oracle run mask by
+    mask and combined the same way."""
+    rng = np.random.default_rng(31)
+    kappa, B, V, K, C = 3, 4, 400, 9, 64
+    pts = synth.sphere_points(V, rng)
+    nbr = synth.knn(pts, K)
+    masks = (rng.random((kappa, B, V)) < 0.15).astype(np.uint8)
+    x = synth.as_dtype(rng.standard_normal((B * V, C)).astype(np.float32), dtype)[1]
+    Wl = synth.as_dtype((rng.standard_normal((C, C)) / np.sqrt(C)).astype(np.float32), dtype)[1]
+    Wc = synth.as_dtype((rng.standard_normal((K, C, C)) / np.sqrt(K * C)).astype(np.float32),
+                        dtype)[1]
+    st = O.stack_masks(masks)
+    Bs = kappa * B
+    c = Compaction(st)
+    n = c.run()
+    td = synth_dtype(dtype)
+    S0 = torch.empty((n, C), dtype=td, device=dev)
+    shc.gather_rows_stacked(up(x, dtype), c.coords, n, B, kappa, V, S0)
+    S1 = torch.empty((n, C), dtype=td, device=dev)
+    shc.sparse_linear(S0, n, up(Wl, dtype), None, S1, shc.SHC_ACT_RELU)
+    table = torch.empty((K * n,), dtype=torch.int32, device=dev)
+    shc.build_neighbor_table(c.coords, c.inv, n, Bs, V, up(nbr), table)
+    S2 = torch.empty((n, C), dtype=td, device=dev)
+    shc.sparse_neighbor_conv_table(S1, table, n, up(Wc, dtype), None, S2, shc.SHC_ACT_RELU)
+    D = torch.empty((Bs * V, C), dtype=td, device=dev)
+    shc.scatter(S2, c.inv, c.coords, n, Bs, V, D, zero_fill=True)
+    P = torch.empty((Bs, C), dtype=td, device=dev)
+    shc.segment_maxpool(S2, c.row_ptr, n, Bs, P, 0.0)
+    spec = [("linear", Wl, None, True), ("conv", Wc, None, True)]
+    dense_k, pool_k = [], []
+    for k in range(kappa):
+        r = O.run_stack(x, masks[k], nbr, spec, dtype, pool=True)
+        dense_k.append(O.scatter(r["outs"][-1], r["inv"], zero_fill=True))
+        pool_k.append(r["pool"])
+    for op in ("sum", "mean", "max"):
+        Dc = torch.empty((B * V, C), dtype=td, device=dev)
+        shc.combine_stacked(D, kappa, B * V, Dc, op)
+        Pc = torch.empty((B, C), dtype=td, device=dev)
+        shc.combine_stacked(P, kappa, B, Pc, op)
+        assert_normwise_close(down(Dc), O.combine_stacked(np.concatenate(dense_k), kappa, op),
+                              dtype, f"dense {op}")
+        assert_normwise_close(down(Pc), O.combine_stacked(np.concatenate(pool_k), kappa, op),
+                              dtype, f"pool {op}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("C", [16, 48, 128, 2048])
+def test_element_masks_exact(dev, dtype, C):
+    rng = np.random.default_rng(C * 7 + 1)
+    B, V = 6, 300
+    me = (rng.random((B, V, C)) < 0.01 * (2048 / C) ** 0.5).astype(np.uint8)
+    me[0, :5, :] = 0
+    me[0, 3, C - 1] = 7                      # only the last channel of (0, 3)
+    mdev = torch.full((B * V,), 9, dtype=torch.uint8, device=dev)
+    shc.row_mask_from_elements(up(me.reshape(-1)), B, V, mdev)
+    m = down(mdev).reshape(B, V)
+    assert np.array_equal(m, O.row_mask_from_elements(me))
+    assert m[0, 3] == 1 and m[0, 2] == 0
+    x = synth.as_dtype(rng.standard_normal((B * V, C)).astype(np.float32), dtype)[1]
+    c = Compaction(m)
+    n = c.run()
+    S = torch.full((n + 1, C), float("nan"), dtype=synth_dtype(dtype), device=dev)
+    shc.gather_rows_masked(up(x, dtype), up(me.reshape(-1)), c.coords, n, B, V, S)
+    ref_c, _, _, _ = O.compact(m)
+    got = down(S)
+    assert np.array_equal(got[:n], O.gather_masked(x, me, ref_c, V))
+    assert np.all(np.isnan(got[n:]))
+
+
+# ----------------------------------------------------------------------------
 # sparse group normalization (Eqs. 7-9)
 # ----------------------------------------------------------------------------
 
