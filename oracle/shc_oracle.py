@@ -31,6 +31,11 @@ What it computes (Sec. 3.1-3.2 of the paper, arXiv 2608.09388):
   leaves open (sum, mean or maximum here).  A mask drawn per element
   (vertex and channel) makes a vertex active when any of its channels is
   kept, and multiplies the gathered row by the element mask.
+* Eq. 3: the mask score.  For K masks with aligned outputs O_k (one row per
+  vertex and body, C channels), the similarity of masks i and k is
+  ||O_i^T O_k||_F^2 / (||O_k^T O_k||_F ||O_i^T O_i||_F), and alpha_k grows by
+  the mean over i != k of (1 - similarity).  At inference the kappa masks of
+  largest alpha are kept (ties to the lower index).
 * Eqs. 7-9: sparse group normalization.  The channels are split into G
   groups of C/G; for every body / frame b and group g the mean and the
   (biased, 1/N) variance are taken over the group's values in the ACTIVE rows
@@ -315,6 +320,47 @@ def gather_masked(x: np.ndarray, me: np.ndarray, coords: np.ndarray, V: int) -> 
     C = np.asarray(x).shape[-1]
     keep = (np.asarray(me).reshape(-1, C)[rows] != 0)
     return np.where(keep, np.asarray(x)[rows], 0)
+
+
+# ----------------------------------------------------------------------------
+# Eq. 3: mask scores and top-kappa selection
+# ----------------------------------------------------------------------------
+
+
+def gram_frobenius(O: np.ndarray) -> np.ndarray:
+    """F[i][k] = ||O_i^T O_k||_F^2 for outputs O [K][N][C] (fp64)."""
+    O = np.asarray(O, dtype=np.float64)
+    K = O.shape[0]
+    F = np.empty((K, K))
+    for i in range(K):
+        for k in range(K):
+            G = O[i].T @ O[k]
+            F[i, k] = float((G * G).sum())
+    return F
+
+
+def mask_similarity(O: np.ndarray) -> np.ndarray:
+    """sim[i][k] = ||O_i^T O_k||_F^2 / (||O_k^T O_k||_F ||O_i^T O_i||_F) (Eq. 3)."""
+    F = gram_frobenius(O)
+    d = np.sqrt(np.diag(F))
+    return F / np.outer(d, d)
+
+
+def alpha_update(alpha: np.ndarray, O: np.ndarray) -> np.ndarray:
+    """One step of Eq. 3: alpha_k + 1/(K-1) sum_{i != k} (1 - sim[i][k])."""
+    sim = mask_similarity(O)
+    K = sim.shape[0]
+    out = np.array(alpha, dtype=np.float64, copy=True)
+    for k in range(K):
+        out[k] += sum(1.0 - sim[i, k] for i in range(K) if i != k) / (K - 1)
+    return out
+
+
+def top_kappa(alpha: np.ndarray, kappa: int) -> np.ndarray:
+    """Indices of the kappa largest scores, largest first; ties to the lower index."""
+    a = np.asarray(alpha, dtype=np.float64)
+    order = sorted(range(len(a)), key=lambda k: (-a[k], k))
+    return np.array(order[:kappa], dtype=np.int32)
 
 
 # ----------------------------------------------------------------------------

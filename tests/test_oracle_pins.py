@@ -422,6 +422,67 @@ def test_element_masks_brute_force_and_broadcast_case():
 
 
 # ----------------------------------------------------------------------------
+# mask scores (Eq. 3)
+# ----------------------------------------------------------------------------
+
+
+def test_mask_similarity_rank_one_closed_form():
+    """Y_k = u_k w_k^T: Y_i^T Y_k = (u_i . u_k) w_i w_k^T, so the similarity is
+    cos^2 of the row factors, whatever the channel factors."""
+    rng = np.random.default_rng(31)
+    K, N, C = 4, 50, 6
+    U = rng.standard_normal((K, N))
+    Wc = rng.standard_normal((K, C))
+    Y = np.einsum("kn,kc->knc", U, Wc)
+    sim = O.mask_similarity(Y)
+    for i in range(K):
+        for k in range(K):
+            cos = U[i] @ U[k] / (np.linalg.norm(U[i]) * np.linalg.norm(U[k]))
+            assert abs(sim[i, k] - cos * cos) < 1e-12
+
+
+def test_mask_scores_orthogonal_identical_and_invariances():
+    rng = np.random.default_rng(32)
+    N, C = 40, 5
+    # disjoint row supports: Y_i^T Y_k = 0, similarity 0, every score + 1
+    Y = np.zeros((3, N, C))
+    for k in range(3):
+        Y[k, 10 * k:10 * k + 10] = rng.standard_normal((10, C))
+    np.testing.assert_allclose(O.mask_similarity(Y), np.eye(3), atol=1e-15)
+    np.testing.assert_allclose(O.alpha_update(np.zeros(3), Y), np.ones(3), atol=1e-15)
+    # identical outputs: similarity 1, scores unchanged
+    X = rng.standard_normal((N, C))
+    np.testing.assert_allclose(O.alpha_update(np.array([0.5, -1.0, 2.0]), np.stack([X, X, X])),
+                               [0.5, -1.0, 2.0], atol=1e-12)
+    # scaling one output changes nothing; relabelling permutes; 0 <= sim <= 1
+    R = rng.standard_normal((4, N, C))
+    base = O.mask_similarity(R)
+    R2 = R.copy()
+    R2[2] *= -7.5
+    np.testing.assert_allclose(O.mask_similarity(R2), base, rtol=1e-12)
+    perm = [2, 0, 3, 1]
+    np.testing.assert_allclose(O.mask_similarity(R[perm]), base[np.ix_(perm, perm)], rtol=1e-12)
+    assert np.all(base <= 1 + 1e-12) and np.all(base >= 0)   # Cauchy-Schwarz
+
+
+def test_gram_frobenius_brute_force_and_top_kappa():
+    rng = np.random.default_rng(33)
+    K, N, C = 3, 4, 2
+    Y = rng.standard_normal((K, N, C))
+    F = O.gram_frobenius(Y)
+    for i in range(K):
+        for k in range(K):
+            tot = 0.0
+            for a in range(C):
+                for b in range(C):
+                    g = sum(float(Y[i, n, a]) * float(Y[k, n, b]) for n in range(N))
+                    tot += g * g
+            assert abs(F[i, k] - tot) < 1e-12 * max(1.0, tot)
+    assert list(O.top_kappa(np.array([0.3, 0.9, 0.3, 0.1, 0.9]), 3)) == [1, 4, 0]
+    assert list(O.top_kappa(np.array([2.0]), 1)) == [0]
+
+
+# ----------------------------------------------------------------------------
 # group normalization (Eqs. 7-9)
 # ----------------------------------------------------------------------------
 
