@@ -347,10 +347,15 @@ def mask_similarity(O: np.ndarray) -> np.ndarray:
 
 
 def alpha_update(alpha: np.ndarray, O: np.ndarray) -> np.ndarray:
-    """One step of Eq. 3: alpha_k + 1/(K-1) sum_{i != k} (1 - sim[i][k])."""
+    """One step of Eq. 3: alpha_k + 1/(K-1) sum_{i != k} (1 - sim[i][k]).
+
+    The paper always has several masks; with K = 1 the sum is empty and the
+    score is left as it is (the 1/(K-1) factor is not applied)."""
     sim = mask_similarity(O)
     K = sim.shape[0]
     out = np.array(alpha, dtype=np.float64, copy=True)
+    if K == 1:
+        return out
     for k in range(K):
         out[k] += sum(1.0 - sim[i, k] for i in range(K) if i != k) / (K - 1)
     return out

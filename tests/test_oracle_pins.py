@@ -479,6 +479,7 @@ def test_gram_frobenius_brute_force_and_top_kappa():
                     tot += g * g
             assert abs(F[i, k] - tot) < 1e-12 * max(1.0, tot)
     assert list(O.top_kappa(np.array([0.3, 0.9, 0.3, 0.1, 0.9]), 3)) == [1, 4, 0]
+    np.testing.assert_array_equal(O.alpha_update(np.array([1.25]), Y[:1]), [1.25])  # K = 1
     assert list(O.top_kappa(np.array([2.0]), 1)) == [0]
 
 
