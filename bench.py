@@ -261,7 +261,8 @@ def main():
     }
 
     out["next_rows"] = {"group_norm": group_norm_measure(st, shc, torch, args.reps),
-                        "multi_mask": multi_mask_measure(st, w, shc, synth, torch, args.reps)}
+                        "multi_mask": multi_mask_measure(st, w, shc, synth, torch, args.reps),
+                        "mask_scores": mask_scores_measure(w, shc, torch, args.reps)}
     log("group norm measured")
 
     if not args.no_dense:
@@ -360,6 +361,28 @@ def multi_mask_measure(st, w, shc, synth, torch, reps, kappa=3):
     rate("gather_masked", us, n2 * (8 + C + 2 * C * e))
     res["masked_rows"] = n2
     return res
+
+
+def mask_scores_measure(w, shc, torch, reps, K=10, bodies=16):
+    """Eq. 3 mask scores for K masks whose outputs are the dense per-vertex
+    outputs of `bodies` bodies of the workload's mesh (N = bodies * V rows,
+    C = 128, bf16): the whole call (Gram tiles, split reduction, scores and
+    top-3), and the MFMA rate of its useful work, K(K+1)/2 Gram blocks of
+    2 N C^2 flop each."""
+    N, C = bodies * w.V, 128
+    g = torch.Generator(device="cuda").manual_seed(7)
+    Y = torch.randn((K, N, C), device="cuda", generator=g).to(torch.bfloat16)
+    a_in = torch.zeros(K, dtype=torch.float64, device="cuda")
+    a_out = torch.empty_like(a_in)
+    top = torch.empty(3, dtype=torch.int32, device="cuda")
+    ws = shc.mask_scores(Y, a_in, a_out, 3, top)
+    us = _time_us(lambda: shc.mask_scores(Y, a_in, a_out, 3, top, None, ws), torch, reps)
+    flops = K * (K + 1) / 2 * 2.0 * N * C * C
+    ach = flops / (us * 1e-6) / 1e12
+    return {"config": f"K={K} masks, N={N} rows ({bodies} bodies x V={w.V}), C={C}, bf16",
+            "launch_us": round(us, 2), "useful_flops": flops, "achieved": round(ach, 1),
+            "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(ach / BF16_MFMA_PEAK_TFLOPS, 4), "bound": "mfma"}
 
 
 def dense_comparison(st, w, per_kernel_ms, torch, shc, synth):

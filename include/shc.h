@@ -321,6 +321,32 @@ int shc_segment_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows
                            hipStream_t stream);
 
 /*
+ * Mask scores -- Eq. 3 (Sec. 3.1) -- and the top-kappa masks kept at
+ * inference.  For K masks with aligned outputs O_k [N][C] (the same N rows,
+ * e.g. the dense per-vertex outputs of every body), stored mask-major as
+ * O [K][N][C] bf16:
+ *
+ *   F[i][k]      = || O_i^T O_k ||_F^2
+ *   sim[i][k]    = F[i][k] / sqrt(F[i][i] * F[k][k])      (0 where that is 0)
+ *   alpha_out[k] = alpha_in[k] + 1/(K-1) * sum_{i != k} (1 - sim[i][k])
+ *                  (alpha_in[k] itself when K = 1)
+ *   top[r]       = the mask of rank r by alpha_out, largest first, ties to
+ *                  the lower index, for r < kappa.
+ *
+ *   alpha_in [K] fp64 or NULL (zeros); alpha_out [K] fp64; sim [K][K] fp64
+ *   or NULL; top [kappa] int32 (may be NULL when kappa = 0); all device
+ *   memory.  K in [1, 64]; C a multiple of 64 in [64, 1024]; bf16 only.
+ *   ws, ws_bytes: device workspace of at least shc_mask_scores_workspace
+ *   bytes (0 for unsupported shapes); contents on entry do not matter.
+ * The Gram blocks are accumulated in fp32 by MFMA over row splits whose sums
+ * are combined in a fixed order in fp64: results repeat bit for bit.
+ */
+size_t shc_mask_scores_workspace(int32_t K, int64_t N, int32_t C);
+int shc_mask_scores(const void* O, int32_t K, int64_t N, int32_t C, int32_t dtype,
+                    const double* alpha_in, double* alpha_out, double* sim, int32_t kappa,
+                    int32_t* top, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * Segmented max-pool per body/frame -- the sparse pooling layer (Sec. 3.2):
  *
  *   P[b][c] = max over row_ptr[b] <= i < row_ptr[b+1] of S[i][c]

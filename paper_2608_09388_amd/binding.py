@@ -76,6 +76,9 @@ _SIGS = {
                                    _c_i32, _c_ptr, _c_ptr]),
     "shc_segment_group_norm": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32,
                                               _c_f, _c_i32, _c_ptr, _c_ptr]),
+    "shc_mask_scores_workspace": (_c_sz, [_c_i32, _c_i64, _c_i32]),
+    "shc_mask_scores": (ctypes.c_int, [_c_ptr, _c_i32, _c_i64, _c_i32, _c_i32, _c_ptr, _c_ptr,
+                                       _c_ptr, _c_i32, _c_ptr, _c_ptr, _c_sz, _c_ptr]),
     "shc_segment_maxpool": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_f,
                                            _c_ptr, _c_ptr]),
 }
@@ -357,6 +360,29 @@ def prepare_segment_group_norm(S, row_ptr, B, G, out, eps=1e-5, stream=None) -> 
     args = [_dev(S, "S", S.dtype), _dev(row_ptr, "row_ptr", torch.int32, B + 1), 0, B, C, G,
             float(eps), _dtype_code(S), _dev(out, "out", S.dtype), _stream(stream)]
     return Prepared("shc_segment_group_norm", args, 2, n_max, (S, row_ptr, out))
+
+
+def mask_scores_workspace(K: int, N: int, C: int) -> int:
+    return int(load().shc_mask_scores_workspace(K, N, C))
+
+
+def mask_scores(O: torch.Tensor, alpha_in: Optional[torch.Tensor], alpha_out: torch.Tensor,
+                kappa: int = 0, top: Optional[torch.Tensor] = None,
+                sim: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """shc_mask_scores on O [K][N][C] bf16; returns the workspace used."""
+    K, N, C = O.shape
+    need = mask_scores_workspace(K, N, C)
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=O.device)
+    args = [_dev(O, "O", torch.bfloat16, K * N * C), K, N, C, _dtype_code(O),
+            _opt_dev(alpha_in, "alpha_in", torch.float64, K),
+            _dev(alpha_out, "alpha_out", torch.float64, K),
+            _opt_dev(sim, "sim", torch.float64, K * K), kappa,
+            _opt_dev(top, "top", torch.int32, kappa), _dev(ws, "ws"),
+            ws.numel() * ws.element_size(), _stream(stream)]
+    _check(load().shc_mask_scores(*args), "shc_mask_scores")
+    return ws
 
 
 def segment_maxpool(S: torch.Tensor, row_ptr: torch.Tensor, n_rows: int, B: int,

@@ -518,6 +518,38 @@ int shc_segment_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows
                     "segment_group_norm launch");
 }
 
+size_t shc_mask_scores_workspace(int32_t K, int64_t N, int32_t C) {
+  if (K < 1 || K > shc::kMaxScoreMasks || N < 0 || C < 64 || C > 1024 || C % 64 != 0) return 0;
+  return shc::mask_scores_workspace_bytes(K, N, C);
+}
+
+int shc_mask_scores(const void* O, int32_t K, int64_t N, int32_t C, int32_t dtype,
+                    const double* alpha_in, double* alpha_out, double* sim, int32_t kappa,
+                    int32_t* top, void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (K < 1 || K > shc::kMaxScoreMasks)
+    return fail(SHC_ERR_UNSUPPORTED, "K = %d masks outside [1, %d]", K, shc::kMaxScoreMasks);
+  if (N < 1) return fail(SHC_ERR_INVALID_ARG, "N = %lld rows must be positive", (long long)N);
+  if (dtype != SHC_BF16) return fail(SHC_ERR_UNSUPPORTED, "mask scores take bf16 outputs");
+  if (C < 64 || C > 1024 || C % 64 != 0)
+    return fail(SHC_ERR_UNSUPPORTED, "C = %d must be a multiple of 64 in [64, 1024]", C);
+  if (kappa < 0 || kappa > K)
+    return fail(SHC_ERR_INVALID_ARG, "kappa = %d outside [0, K = %d]", kappa, K);
+  SHC_PTR(O, "O");
+  SHC_PTR(alpha_out, "alpha_out");
+  SHC_OPT_PTR(alpha_in, "alpha_in");
+  SHC_OPT_PTR(sim, "sim");
+  SHC_OPT_PTR(top, "top");
+  if (kappa > 0 && top == nullptr) return fail(SHC_ERR_INVALID_ARG, "kappa > 0 needs top");
+  SHC_PTR(ws, "ws");
+  const size_t need = shc_mask_scores_workspace(K, N, C);
+  if (ws_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "workspace of %zu bytes is below the %zu needed", ws_bytes, need);
+  return hip_status(shc::launch_mask_scores(O, K, N, C, alpha_in, alpha_out, sim, kappa, top, ws,
+                                            stream),
+                    "mask_scores launch");
+}
+
 int shc_segment_maxpool(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
                         int32_t C, int32_t dtype, float empty_value, void* P, hipStream_t stream) {
   g_last_error[0] = 0;

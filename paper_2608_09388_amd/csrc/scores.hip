@@ -1,0 +1,269 @@
+// Mask scores (Eq. 3).  For K masks with aligned outputs O_k [N][C] (bf16,
+// stored mask-major as O [K][N][C]):
+//
+//   F[i][k] = || O_i^T O_k ||_F^2,
+//   sim[i][k] = F[i][k] / sqrt(F[i][i] F[k][k]),
+//   alpha_out[k] = alpha_in[k] + 1/(K-1) * sum_{i != k} (1 - sim[i][k]),
+//
+// and the kappa masks of largest alpha_out (ties to the lower index).
+//
+// Three launches:
+//   1. tiles  -- workgroup (pair i <= k, T x T tile of O_i^T O_k, row split s)
+//                accumulates its rows' part of the tile with MFMAs.  Rows go
+//                through LDS 32 at a time (two stages, padded rows; the next
+//                step's loads in flight while a step is multiplied, and
+//                several workgroups per CU for the rest of the latency);
+//                both operands are read with transposing LDS reads, since the
+//                reduction runs over rows: lane (g, l) gets rows 8g .. 8g+7 of
+//                channel l.  Four wavefronts, each a (T/2) x (T/2) quarter.
+//                The fp32 partial tile goes to the workspace;
+//   2. reduce -- per (pair, tile): the splits summed in a fixed order in fp64,
+//                each entry squared, summed -> the tile's share of F;
+//   3. score  -- one workgroup: F per pair, similarities, alpha, ranks.
+// Every sum has a fixed order, so the results repeat bit for bit.
+#include <algorithm>
+
+#include "shc_internal.h"
+
+namespace shc {
+namespace {
+
+constexpr int kGramThreads = 256;
+constexpr int kRowsPerStep = 32;
+#define SHC_LDS __attribute__((address_space(3)))
+typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
+
+__host__ __device__ inline int tile_of(int C) { return C % 128 == 0 ? 128 : 64; }
+
+// T: tile edge (64 or 128).  Grid: (pairs * tiles, splits).
+template <int T>
+__global__ __launch_bounds__(kGramThreads) void gram_tile_kernel(const __bf16* __restrict__ O,
+                                                                 int32_t K, int64_t N, int32_t C,
+                                                                 int64_t rows_per_split,
+                                                                 float* __restrict__ part) {
+  constexpr int NB = T / 32;                // 16-column blocks per wavefront and side
+  constexpr int ROW = T * 2 + 16;           // padded LDS row (bytes)
+  constexpr int VPR = T * 2 / 16;           // 16-byte vectors per staged row
+  constexpr int LOADS = 2 * kRowsPerStep * VPR / kGramThreads;  // per thread per step
+  __shared__ __attribute__((aligned(16))) unsigned char stage[2][2][kRowsPerStep * ROW];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, l16 = lane & 15;
+  const int wa = wave >> 1, wb = wave & 1;  // the wave's quarter of the tile
+  const int tiles_side = C / T;
+  const int tiles = tiles_side * tiles_side;
+  const int pt = blockIdx.x;
+  const int p = pt / tiles, t = pt - p * tiles;
+  const int ta = t / tiles_side, tb = t - ta * tiles_side;
+  // pair p -> (i, k), i <= k, row-major over the upper triangle
+  int i = 0, rem = p;
+  while (rem >= K - i) {
+    rem -= K - i;
+    ++i;
+  }
+  const int k = i + rem;
+  const int64_t r0 = (int64_t)blockIdx.y * rows_per_split;
+  const int64_t r1 = min(r0 + rows_per_split, N);
+  const int steps = r1 > r0 ? (int)((r1 - r0 + kRowsPerStep - 1) / kRowsPerStep) : 0;
+
+  const __bf16* Oa = O + (int64_t)i * N * C + (int64_t)ta * T;
+  const __bf16* Ob = O + (int64_t)k * N * C + (int64_t)tb * T;
+
+  auto load = [&](int step, i32x4* v) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int e = tid + u * kGramThreads;  // [operand][row][vector]
+      const int op = e / (kRowsPerStep * VPR);
+      const int rr = (e / VPR) % kRowsPerStep;
+      const int q = e % VPR;
+      const int64_t r = r0 + (int64_t)step * kRowsPerStep + rr;
+      const __bf16* src = (op == 0 ? Oa : Ob) + (r < r1 ? r : r0) * C + q * 8;
+      v[u] = r < r1 ? *reinterpret_cast<const i32x4*>(src) : i32x4{0, 0, 0, 0};
+    }
+  };
+  auto store = [&](int buf, const i32x4* v) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int e = tid + u * kGramThreads;
+      const int op = e / (kRowsPerStep * VPR);
+      const int rr = (e / VPR) % kRowsPerStep;
+      const int q = e % VPR;
+      *reinterpret_cast<i32x4*>(&stage[buf][op][rr * ROW + q * 16]) = v[u];
+    }
+  };
+  // rows 8g .. 8g+7 of channel 16 cb + l16 of one staged operand
+  auto frag = [&](const unsigned char* base, int cb) -> bf16x8 {
+    const unsigned char* p0 = base + (8 * g + (l16 >> 2)) * ROW + cb * 32 + 8 * (l16 & 3);
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0)));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0 + 4 * ROW)));
+    return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  };
+
+  f32x4 acc[NB][NB];
+#pragma unroll
+  for (int x = 0; x < NB; ++x)
+#pragma unroll
+    for (int y = 0; y < NB; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // next step's rows in flight while this one is multiplied; two LDS stages
+  i32x4 v[LOADS];
+  if (steps > 0) {
+    load(0, v);
+    store(0, v);
+  }
+  __syncthreads();
+  for (int s = 0; s < steps; ++s) {
+    const int buf = s & 1;
+    if (s + 1 < steps) load(s + 1, v);
+    bf16x8 fa[NB], fb[NB];
+#pragma unroll
+    for (int x = 0; x < NB; ++x) fa[x] = frag(stage[buf][0], wa * NB + x);
+#pragma unroll
+    for (int y = 0; y < NB; ++y) fb[y] = frag(stage[buf][1], wb * NB + y);
+#pragma unroll
+    for (int x = 0; x < NB; ++x)
+#pragma unroll
+      for (int y = 0; y < NB; ++y)
+        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[x], fb[y], acc[x][y], 0, 0, 0);
+    if (s + 1 < steps) store(buf ^ 1, v);
+    __syncthreads();
+  }
+  // partial tile, row-major [T][T]: lane (g, l16) holds rows 4g .. 4g+3 of column l16
+  float* out = part + ((int64_t)pt * gridDim.y + blockIdx.y) * T * T;
+#pragma unroll
+  for (int x = 0; x < NB; ++x)
+#pragma unroll
+    for (int y = 0; y < NB; ++y)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int a = (wa * NB + x) * 16 + 4 * g + rr;
+        const int b = (wb * NB + y) * 16 + l16;
+        out[a * T + b] = acc[x][y][rr];
+      }
+}
+
+// One workgroup per (pair, tile): sum of the splits (fp64, split order),
+// squared and summed over the tile -> ft[pair * tiles + tile].
+__global__ __launch_bounds__(256) void gram_reduce_kernel(const float* __restrict__ part,
+                                                          int splits, int TT,
+                                                          double* __restrict__ ft) {
+  __shared__ double red[256];
+  const float* base = part + (int64_t)blockIdx.x * splits * TT;
+  double acc = 0.0;
+  for (int e = threadIdx.x; e < TT; e += 256) {
+    double s = 0.0;
+    for (int q = 0; q < splits; ++q) s += (double)base[(int64_t)q * TT + e];
+    acc += s * s;
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) ft[blockIdx.x] = red[0];
+}
+
+__device__ inline int pair_index(int i, int k, int K) {  // i <= k
+  return i * K - i * (i - 1) / 2 + (k - i);
+}
+
+// One workgroup of kMaxScoreMasks threads: thread k owns mask k.
+__global__ __launch_bounds__(kMaxScoreMasks) void score_kernel(
+    const double* __restrict__ ft, int tiles, int32_t K, const double* __restrict__ alpha_in,
+    double* __restrict__ alpha_out, double* __restrict__ sim, int32_t kappa,
+    int32_t* __restrict__ top) {
+  __shared__ double F[kMaxScoreMasks * (kMaxScoreMasks + 1) / 2];
+  __shared__ double a[kMaxScoreMasks];
+  const int P = K * (K + 1) / 2;
+  for (int p = threadIdx.x; p < P; p += blockDim.x) {
+    double s = 0.0;
+    for (int t = 0; t < tiles; ++t) s += ft[(int64_t)p * tiles + t];
+    F[p] = s;
+  }
+  __syncthreads();
+  const int k = threadIdx.x;
+  if (k < K) {
+    const double fkk = F[pair_index(k, k, K)];
+    double acc = 0.0;
+    for (int i = 0; i < K; ++i) {
+      const double fik = F[i <= k ? pair_index(i, k, K) : pair_index(k, i, K)];
+      const double fii = F[pair_index(i, i, K)];
+      const double den = sqrt(fii * fkk);
+      const double sk = den > 0.0 ? fik / den : 0.0;
+      if (sim != nullptr) sim[(int64_t)i * K + k] = sk;
+      if (i != k) acc += 1.0 - sk;
+    }
+    const double base = alpha_in != nullptr ? alpha_in[k] : 0.0;
+    a[k] = K > 1 ? base + acc / (double)(K - 1) : base;
+    alpha_out[k] = a[k];
+  }
+  __syncthreads();
+  if (k < K && top != nullptr) {
+    int rank = 0;
+    for (int j = 0; j < K; ++j) rank += (a[j] > a[k] || (a[j] == a[k] && j < k)) ? 1 : 0;
+    if (rank < kappa) top[rank] = k;
+  }
+}
+
+}  // namespace
+
+void mask_scores_plan(int32_t K, int64_t N, int32_t C, int* tile, int* tiles, int* splits,
+                      int64_t* rows_per_split) {
+  const int T = tile_of(C);
+  const int side = C / T;
+  const int P = K * (K + 1) / 2;
+  *tile = T;
+  *tiles = side * side;
+  const int64_t items = (int64_t)P * side * side;
+  int64_t s = (512 + items - 1) / items;  // about two workgroups per CU on 256 CUs
+  const int64_t max_s = std::max<int64_t>(1, (N + 255) / 256);
+  s = std::min<int64_t>(std::max<int64_t>(s, 1), std::min<int64_t>(64, max_s));
+  *splits = (int)s;
+  int64_t rps = (N + s - 1) / s;
+  rps = (rps + kRowsPerStep - 1) / kRowsPerStep * kRowsPerStep;
+  *rows_per_split = std::max<int64_t>(rps, kRowsPerStep);
+}
+
+size_t mask_scores_workspace_bytes(int32_t K, int64_t N, int32_t C) {
+  int T, tiles, splits;
+  int64_t rps;
+  mask_scores_plan(K, N, C, &T, &tiles, &splits, &rps);
+  const int64_t P = (int64_t)K * (K + 1) / 2;
+  const size_t part = (size_t)P * tiles * splits * T * T * sizeof(float);
+  const size_t ft = (size_t)P * tiles * sizeof(double);
+  return ((part + 255) & ~(size_t)255) + ((ft + 255) & ~(size_t)255);
+}
+
+hipError_t launch_mask_scores(const void* O, int32_t K, int64_t N, int32_t C,
+                              const double* alpha_in, double* alpha_out, double* sim,
+                              int32_t kappa, int32_t* top, void* ws, hipStream_t stream) {
+  int T, tiles, splits;
+  int64_t rps;
+  mask_scores_plan(K, N, C, &T, &tiles, &splits, &rps);
+  const int64_t P = (int64_t)K * (K + 1) / 2;
+  float* part = static_cast<float*>(ws);
+  const size_t part_bytes = (size_t)P * tiles * splits * T * T * sizeof(float);
+  double* ft = reinterpret_cast<double*>(static_cast<unsigned char*>(ws) +
+                                         ((part_bytes + 255) & ~(size_t)255));
+  const dim3 grid((unsigned)(P * tiles), (unsigned)splits);
+  if (T == 128)
+    hipLaunchKernelGGL(gram_tile_kernel<128>, grid, dim3(kGramThreads), 0, stream,
+                       static_cast<const __bf16*>(O), K, N, C, rps, part);
+  else
+    hipLaunchKernelGGL(gram_tile_kernel<64>, grid, dim3(kGramThreads), 0, stream,
+                       static_cast<const __bf16*>(O), K, N, C, rps, part);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(gram_reduce_kernel, dim3((unsigned)(P * tiles)), dim3(256), 0, stream, part,
+                     splits, T * T, ft);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(score_kernel, dim3(1), dim3(kMaxScoreMasks), 0, stream, ft, tiles, K,
+                     alpha_in, alpha_out, sim, kappa, top);
+  return hipGetLastError();
+}
+
+}  // namespace shc

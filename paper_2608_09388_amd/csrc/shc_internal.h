@@ -54,6 +54,14 @@ size_t group_norm_lds_bytes(int32_t C, int is_bf16, int split);
 hipError_t launch_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
                              int32_t C, int32_t G, float eps, int is_bf16, void* out,
                              int num_cus, hipStream_t stream);
+// mask scores (scores.hip)
+constexpr int kMaxScoreMasks = 64;
+void mask_scores_plan(int32_t K, int64_t N, int32_t C, int* tile, int* tiles, int* splits,
+                      int64_t* rows_per_split);
+size_t mask_scores_workspace_bytes(int32_t K, int64_t N, int32_t C);
+hipError_t launch_mask_scores(const void* O, int32_t K, int64_t N, int32_t C,
+                              const double* alpha_in, double* alpha_out, double* sim,
+                              int32_t kappa, int32_t* top, void* ws, hipStream_t stream);
 hipError_t launch_clear_inactive(const int32_t* inv, int32_t B, int32_t V, int32_t row_bytes,
                                  void* D, hipStream_t stream);
 hipError_t launch_gather_ext(const void* x, const uint8_t* me, int mask_mode,

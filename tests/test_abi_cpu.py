@@ -148,6 +148,29 @@ def test_multi_mask_validation(lib):
     assert masked(n=0, x=None, me=None, c=None, S=None) == 0
 
 
+def test_mask_scores_validation(lib):
+    assert lib.shc_mask_scores_workspace(10, 1000, 128) > 0
+    assert lib.shc_mask_scores_workspace(65, 1000, 128) == 0
+    assert lib.shc_mask_scores_workspace(10, 1000, 96) == 0
+    assert lib.shc_mask_scores_workspace(0, 1000, 128) == 0
+    need = lib.shc_mask_scores_workspace(4, 100, 128)
+
+    def call(O=A, K=4, N=100, C=128, dt=1, ain=None, aout=A, sim=None, kappa=0, top=None,
+             ws=A, nbytes=need):
+        return lib.shc_mask_scores(O, K, N, C, dt, ain, aout, sim, kappa, top, ws, nbytes, None)
+
+    assert call(K=0) == -4 and call(K=65) == -4
+    assert call(N=0) == -1
+    assert call(dt=0) == -4 and "bf16" in err(lib)
+    assert call(C=96) == -4
+    assert call(kappa=5) == -1
+    assert call(kappa=2) == -1 and "top" in err(lib)
+    assert call(O=None) == -1
+    assert call(aout=None) == -1
+    assert call(sim=MIS) == -3
+    assert call(nbytes=need - 1) == -2 and "workspace" in err(lib)
+
+
 def test_gather_scatter_pool_validation(lib):
     g = lib.shc_gather_rows
     assert g(A, A, 10, 4, 655, 24, 0, A, None) == -4

@@ -456,6 +456,105 @@ def test_element_masks_exact(dev, dtype, C):
 
 
 # ----------------------------------------------------------------------------
+# mask scores (Eq. 3) and top-kappa selection
+# ----------------------------------------------------------------------------
+
+
+def score_case(rng, K, N, C):
+    """bf16 outputs with a range of mutual similarities: a shared part with
+    mask-dependent weight plus mask-own noise, and one mask on its own rows."""
+    common = rng.standard_normal((N, C))
+    O_ = np.stack([(k / K) * common + rng.standard_normal((N, C)) * (1 + k % 3)
+                   for k in range(K)])
+    if K > 2:
+        O_[K - 1] = 0
+        O_[K - 1, : N // 7] = rng.standard_normal((N // 7, C))
+    return synth.as_dtype(O_.astype(np.float32), "bf16")[1].reshape(K, N, C)
+
+
+def similarity_bound(Y, sim, N):
+    """First-order bound of the GPU similarity's error: Gram entries summed in
+    fp32 over at most N/32 + 2 sequential MFMA accumulations err by
+    gamma |O_i|^T |O_k| entrywise; F = ||G||^2 and the normalisation follow."""
+    gamma = (N / 32 + 2) * 2.0 ** -24
+    K = Y.shape[0]
+    A = np.abs(Y).astype(np.float64)
+    F = O.gram_frobenius(Y)
+    dF = np.empty((K, K))
+    for i in range(K):
+        for k in range(K):
+            a = np.linalg.norm(A[i].T @ A[k]) * gamma
+            dF[i, k] = 2 * np.sqrt(F[i, k]) * a + a * a
+    d = np.diag(F)
+    rel = np.where(F > 0, dF / np.maximum(F, 1e-300), 0)
+    return 2 * (sim * (rel + 0.5 * (dF.diagonal()[:, None] / d[:, None]) +
+                       0.5 * (dF.diagonal()[None, :] / d[None, :])) + 1e-12)
+
+
+@pytest.mark.parametrize("K,N,C", [(3, 1000, 128), (10, 37, 64), (10, 20000, 128),
+                                   (4, 5000, 256), (5, 3000, 192), (1, 500, 64)])
+def test_mask_scores_vs_oracle(dev, K, N, C):
+    rng = np.random.default_rng(K * 1000 + C)
+    Y = score_case(rng, K, N, C)
+    alpha_in = rng.standard_normal(K)
+    kappa = min(3, K)
+    a_out = torch.full((K,), np.nan, dtype=torch.float64, device=dev)
+    simd = torch.full((K * K,), np.nan, dtype=torch.float64, device=dev)
+    top = torch.full((kappa + 1,), -9, dtype=torch.int32, device=dev)
+    ws = shc.mask_scores(up(Y.reshape(K * N, C), "bf16").reshape(K, N, C), up(alpha_in),
+                         a_out, kappa, top, simd)
+    sim = down(simd).reshape(K, K)
+    ref_sim = O.mask_similarity(Y)
+    assert np.all(np.abs(sim - ref_sim) <= similarity_bound(Y, ref_sim, N)), \
+        f"similarity off by {np.max(np.abs(sim - ref_sim)):.3g}"
+    ref_alpha = O.alpha_update(alpha_in, Y)
+    bound_a = (similarity_bound(Y, ref_sim, N).sum(0) / max(K - 1, 1))
+    assert np.all(np.abs(down(a_out) - ref_alpha) <= bound_a + 1e-12)
+    got_top = down(top)
+    assert got_top[kappa] == -9
+    # the selection is the device's own ranking of its scores; where the
+    # reference scores are farther apart than the bound it matches them
+    assert list(got_top[:kappa]) == list(O.top_kappa(down(a_out), kappa))
+    gap = np.min(np.diff(np.sort(ref_alpha))) if K > 1 else 1.0
+    if gap > 2 * bound_a.max():
+        assert list(got_top[:kappa]) == list(O.top_kappa(ref_alpha, kappa))
+    # bit-for-bit repeat, workspace reused
+    a2 = torch.empty_like(a_out)
+    shc.mask_scores(up(Y.reshape(K * N, C), "bf16").reshape(K, N, C), up(alpha_in), a2, 0,
+                    None, None, ws)
+    assert torch.equal(a2, a_out)
+
+
+def test_mask_scores_special_cases(dev):
+    """Disjoint row supports give exact zeros off the diagonal (every score
+    + 1); identical outputs give similarity 1 (scores unchanged); K = 1
+    leaves the score alone; no alpha_in means zeros."""
+    rng = np.random.default_rng(9)
+    N, C = 300, 64
+    Y = np.zeros((3, N, C), np.float32)
+    for k in range(3):
+        Y[k, 100 * k:100 * k + 100] = rng.standard_normal((100, C))
+    Y = synth.as_dtype(Y, "bf16")[1]
+    a = torch.empty(3, dtype=torch.float64, device=dev)
+    simd = torch.empty(9, dtype=torch.float64, device=dev)
+    shc.mask_scores(up(Y.reshape(-1, C), "bf16").reshape(3, N, C), None, a, 0, None, simd)
+    sim = down(simd).reshape(3, 3)
+    assert np.all(sim[~np.eye(3, dtype=bool)] == 0)
+    assert np.allclose(np.diag(sim), 1, atol=1e-12)
+    assert np.allclose(down(a), 1, atol=1e-12)
+    X = Y[0]
+    Yi = np.stack([X, X])
+    a = torch.empty(2, dtype=torch.float64, device=dev)
+    shc.mask_scores(up(Yi.reshape(-1, C), "bf16").reshape(2, N, C), up(np.array([0.25, -4.0])),
+                    a, 0)
+    assert np.allclose(down(a), [0.25, -4.0], atol=1e-9)
+    a1 = torch.empty(1, dtype=torch.float64, device=dev)
+    top1 = torch.empty(1, dtype=torch.int32, device=dev)
+    shc.mask_scores(up(X, "bf16").reshape(1, N, C), up(np.array([3.5])), a1, 1, top1)
+    assert float(a1[0]) == 3.5 and int(top1[0]) == 0
+
+
+# ----------------------------------------------------------------------------
 # sparse group normalization (Eqs. 7-9)
 # ----------------------------------------------------------------------------
 
