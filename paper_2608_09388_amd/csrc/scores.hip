@@ -10,15 +10,18 @@
 // Three launches:
 //   1. tiles  -- workgroup (pair i <= k, T x T tile of O_i^T O_k, row split s)
 //                accumulates its rows' part of the tile with MFMAs.  Rows go
-//                through LDS 32 at a time (two stages, padded rows; the next
-//                step's loads in flight while a step is multiplied, and
-//                several workgroups per CU for the rest of the latency);
+//                through one LDS stage (padded rows) 128 at a time; the next
+//                step's rows are loaded into registers while a step is
+//                multiplied, so each workgroup keeps 64 KB (T = 128) in
+//                flight.  Exactly the workgroups that fit at once are
+//                launched;
 //                both operands are read with transposing LDS reads, since the
 //                reduction runs over rows: lane (g, l) gets rows 8g .. 8g+7 of
 //                channel l.  Four wavefronts, each a (T/2) x (T/2) quarter.
 //                The fp32 partial tile goes to the workspace;
-//   2. reduce -- per (pair, tile): the splits summed in a fixed order in fp64,
-//                each entry squared, summed -> the tile's share of F;
+//   2. reduce -- per (pair, tile, chunk of entries): the splits summed in a
+//                fixed order in fp64, each entry squared, summed -> the
+//                chunk's share of F;
 //   3. score  -- one workgroup: F per pair, similarities, alpha, ranks.
 // Every sum has a fixed order, so the results repeat bit for bit.
 #include <algorithm>
@@ -29,30 +32,48 @@ namespace shc {
 namespace {
 
 constexpr int kGramThreads = 256;
-constexpr int kRowsPerStep = 32;
+constexpr int kXcds = 8;
+constexpr int kCus = 256;
+// Rows per step of the tile kernel (both tile edges) and the workgroups of it
+// that fit on one CU: at T = 128, 240 registers per lane and 68 KB of LDS
+// allow 2; at T = 64, 112 registers and 36 KB allow 4.
+constexpr int kRowsPerStep = 128;
+__host__ inline int tiles_per_cu(int T) { return T == 128 ? 2 : 4; }
+constexpr int kMaxSplits = 512;
+constexpr int kScoreThreads = 256;
 #define SHC_LDS __attribute__((address_space(3)))
 typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
 
 __host__ __device__ inline int tile_of(int C) { return C % 128 == 0 ? 128 : 64; }
 
-// T: tile edge (64 or 128).  Grid: (pairs * tiles, splits).
-template <int T>
+// T: tile edge (64 or 128).  Grid: pairs * tiles * splits workgroups, one
+// dimension.  Workgroups are dealt to the 8 XCDs in turn (block b to XCD
+// b % 8); the logical index gives each XCD a contiguous run, split-major, so
+// the workgroups that read the same rows of a mask share that XCD's L2.
+template <int T, int R>
 __global__ __launch_bounds__(kGramThreads) void gram_tile_kernel(const __bf16* __restrict__ O,
                                                                  int32_t K, int64_t N, int32_t C,
                                                                  int64_t rows_per_split,
+                                                                 int32_t splits,
                                                                  float* __restrict__ part) {
   constexpr int NB = T / 32;                // 16-column blocks per wavefront and side
   constexpr int ROW = T * 2 + 16;           // padded LDS row (bytes)
   constexpr int VPR = T * 2 / 16;           // 16-byte vectors per staged row
-  constexpr int LOADS = 2 * kRowsPerStep * VPR / kGramThreads;  // per thread per step
-  __shared__ __attribute__((aligned(16))) unsigned char stage[2][2][kRowsPerStep * ROW];
+  constexpr int LOADS = 2 * R * VPR / kGramThreads;  // per thread per step
+  __shared__ __attribute__((aligned(16))) unsigned char stage[2][R * ROW];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15;
   const int wa = wave >> 1, wb = wave & 1;  // the wave's quarter of the tile
   const int tiles_side = C / T;
   const int tiles = tiles_side * tiles_side;
-  const int pt = blockIdx.x;
+  const int n_wg = (int)gridDim.x;
+  const int xcd = (int)blockIdx.x % kXcds, slot = (int)blockIdx.x / kXcds;
+  const int q8 = n_wg / kXcds, r8 = n_wg % kXcds;
+  const int logical = (xcd < r8 ? xcd * (q8 + 1) : r8 * (q8 + 1) + (xcd - r8) * q8) + slot;
+  const int items = n_wg / splits;
+  const int split = logical / items;
+  const int pt = logical - split * items;
   const int p = pt / tiles, t = pt - p * tiles;
   const int ta = t / tiles_side, tb = t - ta * tiles_side;
   // pair p -> (i, k), i <= k, row-major over the upper triangle
@@ -62,9 +83,9 @@ __global__ __launch_bounds__(kGramThreads) void gram_tile_kernel(const __bf16* _
     ++i;
   }
   const int k = i + rem;
-  const int64_t r0 = (int64_t)blockIdx.y * rows_per_split;
+  const int64_t r0 = (int64_t)split * rows_per_split;
   const int64_t r1 = min(r0 + rows_per_split, N);
-  const int steps = r1 > r0 ? (int)((r1 - r0 + kRowsPerStep - 1) / kRowsPerStep) : 0;
+  const int steps = r1 > r0 ? (int)((r1 - r0 + R - 1) / R) : 0;
 
   const __bf16* Oa = O + (int64_t)i * N * C + (int64_t)ta * T;
   const __bf16* Ob = O + (int64_t)k * N * C + (int64_t)tb * T;
@@ -73,22 +94,22 @@ __global__ __launch_bounds__(kGramThreads) void gram_tile_kernel(const __bf16* _
 #pragma unroll
     for (int u = 0; u < LOADS; ++u) {
       const int e = tid + u * kGramThreads;  // [operand][row][vector]
-      const int op = e / (kRowsPerStep * VPR);
-      const int rr = (e / VPR) % kRowsPerStep;
+      const int op = e / (R * VPR);
+      const int rr = (e / VPR) % R;
       const int q = e % VPR;
-      const int64_t r = r0 + (int64_t)step * kRowsPerStep + rr;
+      const int64_t r = r0 + (int64_t)step * R + rr;
       const __bf16* src = (op == 0 ? Oa : Ob) + (r < r1 ? r : r0) * C + q * 8;
       v[u] = r < r1 ? *reinterpret_cast<const i32x4*>(src) : i32x4{0, 0, 0, 0};
     }
   };
-  auto store = [&](int buf, const i32x4* v) {
+  auto store = [&](const i32x4* v) {
 #pragma unroll
     for (int u = 0; u < LOADS; ++u) {
       const int e = tid + u * kGramThreads;
-      const int op = e / (kRowsPerStep * VPR);
-      const int rr = (e / VPR) % kRowsPerStep;
+      const int op = e / (R * VPR);
+      const int rr = (e / VPR) % R;
       const int q = e % VPR;
-      *reinterpret_cast<i32x4*>(&stage[buf][op][rr * ROW + q * 16]) = v[u];
+      *reinterpret_cast<i32x4*>(&stage[op][rr * ROW + q * 16]) = v[u];
     }
   };
   // rows 8g .. 8g+7 of channel 16 cb + l16 of one staged operand
@@ -107,31 +128,31 @@ __global__ __launch_bounds__(kGramThreads) void gram_tile_kernel(const __bf16* _
 #pragma unroll
     for (int y = 0; y < NB; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // next step's rows in flight while this one is multiplied; two LDS stages
+  // One LDS stage: the next step's rows are in flight in registers while
+  // this step's are multiplied.
   i32x4 v[LOADS];
-  if (steps > 0) {
-    load(0, v);
-    store(0, v);
-  }
-  __syncthreads();
+  if (steps > 0) load(0, v);
   for (int s = 0; s < steps; ++s) {
-    const int buf = s & 1;
+    store(v);
+    __syncthreads();
     if (s + 1 < steps) load(s + 1, v);
-    bf16x8 fa[NB], fb[NB];
 #pragma unroll
-    for (int x = 0; x < NB; ++x) fa[x] = frag(stage[buf][0], wa * NB + x);
+    for (int sub = 0; sub < R / 32; ++sub) {
+      bf16x8 fa[NB], fb[NB];
 #pragma unroll
-    for (int y = 0; y < NB; ++y) fb[y] = frag(stage[buf][1], wb * NB + y);
+      for (int x = 0; x < NB; ++x) fa[x] = frag(stage[0] + sub * 32 * ROW, wa * NB + x);
 #pragma unroll
-    for (int x = 0; x < NB; ++x)
+      for (int y = 0; y < NB; ++y) fb[y] = frag(stage[1] + sub * 32 * ROW, wb * NB + y);
 #pragma unroll
-      for (int y = 0; y < NB; ++y)
-        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[x], fb[y], acc[x][y], 0, 0, 0);
-    if (s + 1 < steps) store(buf ^ 1, v);
+      for (int x = 0; x < NB; ++x)
+#pragma unroll
+        for (int y = 0; y < NB; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[x], fb[y], acc[x][y], 0, 0, 0);
+    }
     __syncthreads();
   }
   // partial tile, row-major [T][T]: lane (g, l16) holds rows 4g .. 4g+3 of column l16
-  float* out = part + ((int64_t)pt * gridDim.y + blockIdx.y) * T * T;
+  float* out = part + ((int64_t)pt * splits + split) * T * T;
 #pragma unroll
   for (int x = 0; x < NB; ++x)
 #pragma unroll
@@ -144,16 +165,19 @@ __global__ __launch_bounds__(kGramThreads) void gram_tile_kernel(const __bf16* _
       }
 }
 
-// One workgroup per (pair, tile): sum of the splits (fp64, split order),
-// squared and summed over the tile -> ft[pair * tiles + tile].
+// Workgroup (pair-tile pt, chunk j): the entries e = j*256 + tid, + 256*chunks,
+// ... of tile pt, each summed over the splits (fp64, split order), squared, and
+// summed -> fq[pt * chunks + j].  One entry per thread at a time, so the loads
+// of consecutive splits are independent of each other and stay in flight.
 __global__ __launch_bounds__(256) void gram_reduce_kernel(const float* __restrict__ part,
-                                                          int splits, int TT,
-                                                          double* __restrict__ ft) {
+                                                          int splits, int TT, int chunks,
+                                                          double* __restrict__ fq) {
   __shared__ double red[256];
   const float* base = part + (int64_t)blockIdx.x * splits * TT;
   double acc = 0.0;
-  for (int e = threadIdx.x; e < TT; e += 256) {
+  for (int e = blockIdx.y * 256 + threadIdx.x; e < TT; e += 256 * chunks) {
     double s = 0.0;
+#pragma unroll 8
     for (int q = 0; q < splits; ++q) s += (double)base[(int64_t)q * TT + e];
     acc += s * s;
   }
@@ -163,25 +187,30 @@ __global__ __launch_bounds__(256) void gram_reduce_kernel(const float* __restric
     if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
-  if (threadIdx.x == 0) ft[blockIdx.x] = red[0];
+  if (threadIdx.x == 0) fq[(int64_t)blockIdx.x * chunks + blockIdx.y] = red[0];
 }
 
 __device__ inline int pair_index(int i, int k, int K) {  // i <= k
   return i * K - i * (i - 1) / 2 + (k - i);
 }
 
-// One workgroup of kMaxScoreMasks threads: thread k owns mask k.
-__global__ __launch_bounds__(kMaxScoreMasks) void score_kernel(
-    const double* __restrict__ ft, int tiles, int32_t K, const double* __restrict__ alpha_in,
+// One workgroup of kScoreThreads threads.  F of each pair: a wavefront per
+// pair sums its parts (lane j: parts j, j + 64, ...; then a fixed butterfly
+// over the lanes).  Then thread k < K owns mask k.
+__global__ __launch_bounds__(kScoreThreads) void score_kernel(
+    const double* __restrict__ fq, int parts, int32_t K, const double* __restrict__ alpha_in,
     double* __restrict__ alpha_out, double* __restrict__ sim, int32_t kappa,
     int32_t* __restrict__ top) {
   __shared__ double F[kMaxScoreMasks * (kMaxScoreMasks + 1) / 2];
   __shared__ double a[kMaxScoreMasks];
   const int P = K * (K + 1) / 2;
-  for (int p = threadIdx.x; p < P; p += blockDim.x) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int p = wave; p < P; p += kScoreThreads / 64) {
     double s = 0.0;
-    for (int t = 0; t < tiles; ++t) s += ft[(int64_t)p * tiles + t];
-    F[p] = s;
+    for (int t = lane; t < parts; t += 64) s += fq[(int64_t)p * parts + t];
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) s += __shfl_xor(s, m);
+    if (lane == 0) F[p] = s;
   }
   __syncthreads();
   const int k = threadIdx.x;
@@ -211,57 +240,65 @@ __global__ __launch_bounds__(kMaxScoreMasks) void score_kernel(
 }  // namespace
 
 void mask_scores_plan(int32_t K, int64_t N, int32_t C, int* tile, int* tiles, int* splits,
-                      int64_t* rows_per_split) {
+                      int64_t* rows_per_split, int* chunks) {
   const int T = tile_of(C);
   const int side = C / T;
   const int P = K * (K + 1) / 2;
   *tile = T;
   *tiles = side * side;
   const int64_t items = (int64_t)P * side * side;
-  int64_t s = (512 + items - 1) / items;  // about two workgroups per CU on 256 CUs
+  // As many row splits as keep every workgroup resident at once (a partial
+  // second wave of workgroups would double the time), at least 256 rows each.
+  // Each workgroup keeps one step of rows in flight, so the number resident
+  // sets the memory parallelism.
+  int64_t s = (int64_t)kCus * tiles_per_cu(T) / items;
   const int64_t max_s = std::max<int64_t>(1, (N + 255) / 256);
-  s = std::min<int64_t>(std::max<int64_t>(s, 1), std::min<int64_t>(64, max_s));
+  s = std::min<int64_t>(std::max<int64_t>(s, 1), std::min<int64_t>(kMaxSplits, max_s));
   *splits = (int)s;
   int64_t rps = (N + s - 1) / s;
   rps = (rps + kRowsPerStep - 1) / kRowsPerStep * kRowsPerStep;
   *rows_per_split = std::max<int64_t>(rps, kRowsPerStep);
+  // reduction: about 2048 workgroups, at most one 256-entry chunk each
+  int ch = 1;
+  while (ch * 256 < T * T && items * ch < 2048) ch *= 2;
+  *chunks = ch;
 }
 
 size_t mask_scores_workspace_bytes(int32_t K, int64_t N, int32_t C) {
-  int T, tiles, splits;
+  int T, tiles, splits, chunks;
   int64_t rps;
-  mask_scores_plan(K, N, C, &T, &tiles, &splits, &rps);
+  mask_scores_plan(K, N, C, &T, &tiles, &splits, &rps, &chunks);
   const int64_t P = (int64_t)K * (K + 1) / 2;
   const size_t part = (size_t)P * tiles * splits * T * T * sizeof(float);
-  const size_t ft = (size_t)P * tiles * sizeof(double);
+  const size_t ft = (size_t)P * tiles * chunks * sizeof(double);
   return ((part + 255) & ~(size_t)255) + ((ft + 255) & ~(size_t)255);
 }
 
 hipError_t launch_mask_scores(const void* O, int32_t K, int64_t N, int32_t C,
                               const double* alpha_in, double* alpha_out, double* sim,
                               int32_t kappa, int32_t* top, void* ws, hipStream_t stream) {
-  int T, tiles, splits;
+  int T, tiles, splits, chunks;
   int64_t rps;
-  mask_scores_plan(K, N, C, &T, &tiles, &splits, &rps);
+  mask_scores_plan(K, N, C, &T, &tiles, &splits, &rps, &chunks);
   const int64_t P = (int64_t)K * (K + 1) / 2;
   float* part = static_cast<float*>(ws);
   const size_t part_bytes = (size_t)P * tiles * splits * T * T * sizeof(float);
   double* ft = reinterpret_cast<double*>(static_cast<unsigned char*>(ws) +
                                          ((part_bytes + 255) & ~(size_t)255));
-  const dim3 grid((unsigned)(P * tiles), (unsigned)splits);
+  const dim3 grid((unsigned)(P * tiles * splits));
   if (T == 128)
-    hipLaunchKernelGGL(gram_tile_kernel<128>, grid, dim3(kGramThreads), 0, stream,
-                       static_cast<const __bf16*>(O), K, N, C, rps, part);
+    hipLaunchKernelGGL((gram_tile_kernel<128, kRowsPerStep>), grid, dim3(kGramThreads), 0, stream,
+                       static_cast<const __bf16*>(O), K, N, C, rps, splits, part);
   else
-    hipLaunchKernelGGL(gram_tile_kernel<64>, grid, dim3(kGramThreads), 0, stream,
-                       static_cast<const __bf16*>(O), K, N, C, rps, part);
+    hipLaunchKernelGGL((gram_tile_kernel<64, kRowsPerStep>), grid, dim3(kGramThreads), 0, stream,
+                       static_cast<const __bf16*>(O), K, N, C, rps, splits, part);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(gram_reduce_kernel, dim3((unsigned)(P * tiles)), dim3(256), 0, stream, part,
-                     splits, T * T, ft);
+  hipLaunchKernelGGL(gram_reduce_kernel, dim3((unsigned)(P * tiles), (unsigned)chunks), dim3(256),
+                     0, stream, part, splits, T * T, chunks, ft);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(score_kernel, dim3(1), dim3(kMaxScoreMasks), 0, stream, ft, tiles, K,
+  hipLaunchKernelGGL(score_kernel, dim3(1), dim3(kScoreThreads), 0, stream, ft, tiles * chunks, K,
                      alpha_in, alpha_out, sim, kappa, top);
   return hipGetLastError();
 }

@@ -57,7 +57,7 @@ hipError_t launch_group_norm(const void* S, const int32_t* row_ptr, int64_t n_ro
 // mask scores (scores.hip)
 constexpr int kMaxScoreMasks = 64;
 void mask_scores_plan(int32_t K, int64_t N, int32_t C, int* tile, int* tiles, int* splits,
-                      int64_t* rows_per_split);
+                      int64_t* rows_per_split, int* chunks);
 size_t mask_scores_workspace_bytes(int32_t K, int64_t N, int32_t C);
 hipError_t launch_mask_scores(const void* O, int32_t K, int64_t N, int32_t C,
                               const double* alpha_in, double* alpha_out, double* sim,
