@@ -36,6 +36,10 @@ What it computes (Sec. 3.1-3.2 of the paper, arXiv 2608.09388):
   ||O_i^T O_k||_F^2 / (||O_k^T O_k||_F ||O_i^T O_i||_F), and alpha_k grows by
   the mean over i != k of (1 - similarity).  At inference the kappa masks of
   largest alpha are kept (ties to the lower index).
+* Backward of the sparse linear and conv layers: the gradient of the dense
+  operator on x (.) m, restricted to the active rows (input rows, slot
+  weights, bias), with the activation's derivative taken from the stored
+  output.
 * Eqs. 7-9: sparse group normalization.  The channels are split into G
   groups of C/G; for every body / frame b and group g the mean and the
   (biased, 1/N) variance are taken over the group's values in the ACTIVE rows
@@ -366,6 +370,107 @@ def top_kappa(alpha: np.ndarray, kappa: int) -> np.ndarray:
     a = np.asarray(alpha, dtype=np.float64)
     order = sorted(range(len(a)), key=lambda k: (-a[k], k))
     return np.array(order[:kappa], dtype=np.int32)
+
+
+# ----------------------------------------------------------------------------
+# backward of the sparse linear and conv layers
+# ----------------------------------------------------------------------------
+#
+# A sparse layer is the dense layer applied to x (.) m and read at the active
+# rows: out = R L(P^T S), where P^T places the active rows S into a zero
+# dense tensor, L is the dense operator and R reads the active rows.  With the
+# upstream gradient dY at the output rows, the chain rule gives
+#   dZ = dY (.) f'(Z)                      (Eq. 10; for ReLU, [Y > 0])
+#   dS = P L^T(R^T dZ)                     (input rows)
+#   dW, db: the dense layer's weight gradients at R^T dZ,
+# i.e. the gradient of the dense operator on x (.) m, restricted to the
+# active rows.  The ReLU's derivative is taken from the layer's stored output
+# Y (derivative 0 at 0), so it is an input here, not recomputed.
+
+
+def relu_backward(dY: np.ndarray, Y: np.ndarray) -> np.ndarray:
+    """Gradient through Eq. 10's ReLU from the stored output: dY where Y > 0, else 0."""
+    dY = np.asarray(dY, dtype=np.float64)
+    return np.where(np.asarray(Y, dtype=np.float64) > 0, dY, 0.0)
+
+
+def dense_conv_transpose(dZd: np.ndarray, nbr: np.ndarray, W: np.ndarray, B: int,
+                         V: int) -> np.ndarray:
+    """Adjoint of :func:`dense_conv` in x: each output row (b, v) sends
+    dZ[b, v] W[j]^T back to its slot-j neighbour (b, nbr[v, j]), fp64."""
+    dZ = np.asarray(dZd, dtype=np.float64).reshape(B, V, -1)
+    W = np.asarray(W, dtype=np.float64)
+    K, Cin = W.shape[0], W.shape[1]
+    dX = np.zeros((B, V, Cin), dtype=np.float64)
+    for j in range(K):
+        n_j = nbr[:, j].astype(np.int64)
+        has = np.flatnonzero(n_j >= 0)
+        contrib = dZ[:, has, :] @ W[j].T                     # [B][|has|][C_in]
+        for b in range(B):
+            np.add.at(dX[b], n_j[has], contrib[b])
+    return dX.reshape(B * V, Cin)
+
+
+def sparse_linear_backward(S, W, dY, Y=None, act=False):
+    """Gradients of the sparse linear layer (Eq. 6 [+ Eq. 10]).
+
+    Rows are independent, so the dense gradient read at the active rows is
+    dZ = dY (.) [Y > 0] (with the activation), dS = dZ W^T, dW = S^T dZ,
+    db = sum of dZ over the rows.  Returns (dS, dW, db) in fp64."""
+    S = np.asarray(S, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    dZ = relu_backward(dY, Y) if act else np.asarray(dY, dtype=np.float64)
+    return dZ @ W.T, S.T @ dZ, dZ.sum(axis=0)
+
+
+def sparse_conv_backward(S, coords, B, V, nbr, W, dY, Y=None, act=False):
+    """Gradients of the sparse neighbourhood convolution (Eqs. 4-5 [+ Eq. 10]).
+
+    The output gradient is placed in a zero dense tensor (inactive output rows
+    receive none), sent back through the adjoint of the dense convolution and
+    read at the active rows; the slot weights' gradient is the dense one,
+    dW[j] = sum over dense rows (b, v) of x_m[b, nbr[v, j]]^T dZ[b, v], where
+    only active rows carry a non-zero x_m and dZ.  Returns (dS, dW, db)."""
+    S = np.asarray(S, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    dZ = relu_backward(dY, Y) if act else np.asarray(dY, dtype=np.float64)
+    dZd = densify(dZ, coords, B, V)
+    dS = restrict(dense_conv_transpose(dZd, nbr, W, B, V), coords, V)
+    xm = densify(S, coords, B, V).reshape(B, V, -1)
+    dZ3 = dZd.reshape(B, V, -1)
+    K = W.shape[0]
+    dW = np.zeros_like(W)
+    for j in range(K):
+        n_j = nbr[:, j].astype(np.int64)
+        has = n_j >= 0
+        xs = np.where(has[None, :, None], xm[:, np.where(has, n_j, 0), :], 0.0)
+        dW[j] = xs.reshape(B * V, -1).T @ dZ3.reshape(B * V, -1)
+    return dS, dW, dZ.sum(axis=0)
+
+
+def conv_backward_input_at(coords, B, V, nbr, W, dZ, rows, scale=False):
+    """dS of the sparse convolution at selected active rows only, from the
+    pre-activation gradient dZ of all active rows (for full-size checks).
+
+    Row r = (b, u) receives dZ[b, v] W[j]^T from every active (b, v) whose
+    slot j points at u.  With ``scale`` the abs-sum error scale is returned."""
+    rows = np.asarray(rows, dtype=np.int64)
+    dZ = np.asarray(dZ, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    if scale:
+        W, dZ = np.abs(W), np.abs(dZ)
+    n = dZ.shape[0]
+    where = np.full(B * V, -1, dtype=np.int64)
+    where[coords[:, 0].astype(np.int64) * V + coords[:, 1]] = np.arange(n)
+    out = np.zeros((rows.size, W.shape[1]), dtype=np.float64)
+    for q, r in enumerate(rows):
+        b, u = int(coords[r, 0]), int(coords[r, 1])
+        for j in range(W.shape[0]):
+            for v in np.flatnonzero(nbr[:, j] == u):
+                i = where[b * V + v]
+                if i >= 0:
+                    out[q] += dZ[i] @ W[j].T
+    return out
 
 
 # ----------------------------------------------------------------------------

@@ -484,6 +484,165 @@ def test_gram_frobenius_brute_force_and_top_kappa():
 
 
 # ----------------------------------------------------------------------------
+# backward of the sparse linear and conv layers
+# ----------------------------------------------------------------------------
+
+
+def bwd_case(rng, B=3, V=11, K=4, Ci=5, Co=6, p=0.5):
+    m = (rng.random((B, V)) < p).astype(np.uint8)
+    m[0, 0] = 1
+    coords, inv, rp, n = O.compact(m)
+    S = rng.standard_normal((n, Ci))
+    nbr = rand_nbr(V, K, rng)
+    nbr[1, 2] = nbr[2, 2] = 4                # two rows sending to one neighbour by one slot
+    W = rng.standard_normal((K, Ci, Co))
+    bias = rng.standard_normal(Co)
+    return m, coords, n, S, nbr, W, bias
+
+
+def torch_sparse_conv(S, coords, B, V, nbr, W, bias, act):
+    """The dense conv of x (.) m read at the active rows, written with torch
+    ops (an index_select per slot) so that autograd differentiates it."""
+    n = S.shape[0]
+    flat = torch.as_tensor(coords[:, 0].astype(np.int64) * V + coords[:, 1])
+    xd = torch.zeros((B * V, S.shape[1]), dtype=torch.float64).index_copy(0, flat, S)
+    xd = xd.view(B, V, -1)
+    y = torch.zeros((B, V, W.shape[2]), dtype=torch.float64)
+    for j in range(W.shape[0]):
+        idx = torch.as_tensor(np.maximum(nbr[:, j], 0).astype(np.int64))
+        has = torch.as_tensor(nbr[:, j] >= 0, dtype=torch.float64).view(1, V, 1)
+        y = y + has * (xd.index_select(1, idx) @ W[j])
+    y = y + bias
+    if act:
+        y = torch.relu(y)
+    return y.view(B * V, -1).index_select(0, flat)
+
+
+@pytest.mark.parametrize("act", [False, True])
+def test_conv_backward_matches_torch_autograd(act):
+    """dS, dW, db against autograd of an independently written dense conv."""
+    rng = np.random.default_rng(41 + act)
+    m, coords, n, S, nbr, W, bias = bwd_case(rng)
+    B, V = m.shape
+    St = torch.tensor(S, requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    bt = torch.tensor(bias, requires_grad=True)
+    Y = torch_sparse_conv(St, coords, B, V, nbr, Wt, bt, act)
+    dY = rng.standard_normal(Y.shape)
+    (Y * torch.as_tensor(dY)).sum().backward()
+    dS, dW, db = O.sparse_conv_backward(S, coords, B, V, nbr, W, dY,
+                                        Y.detach().numpy(), act)
+    np.testing.assert_allclose(dS, St.grad.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dW, Wt.grad.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(db, bt.grad.numpy(), rtol=1e-12, atol=1e-12)
+    if act:
+        assert np.any(Y.detach().numpy() == 0)   # the mask cut something
+
+
+@pytest.mark.parametrize("act", [False, True])
+def test_linear_backward_matches_torch_autograd(act):
+    rng = np.random.default_rng(43 + act)
+    S = rng.standard_normal((9, 5))
+    W = rng.standard_normal((5, 7))
+    bias = rng.standard_normal(7)
+    St, Wt, bt = (torch.tensor(a, requires_grad=True) for a in (S, W, bias))
+    Y = torch.nn.functional.linear(St, Wt.T, bt)
+    if act:
+        Y = torch.relu(Y)
+    dY = rng.standard_normal(Y.shape)
+    (Y * torch.as_tensor(dY)).sum().backward()
+    dS, dW, db = O.sparse_linear_backward(S, W, dY, Y.detach().numpy(), act)
+    np.testing.assert_allclose(dS, St.grad.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dW, Wt.grad.numpy(), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(db, bt.grad.numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_conv_backward_finite_differences_and_adjoint():
+    """Central differences of <dY, conv(S)> in a few entries of S and W, and
+    the dot-product test <conv(S), G> = <S, dS(G)> (no bias, no activation)."""
+    rng = np.random.default_rng(45)
+    m, coords, n, S, nbr, W, bias = bwd_case(rng)
+    B, V = m.shape
+    dY = rng.standard_normal((n, W.shape[2]))
+    dS, dW, db = O.sparse_conv_backward(S, coords, B, V, nbr, W, dY)
+
+    def loss(S_, W_, b_):
+        return float((O.sparse_conv(S_, coords, B, V, nbr, W_, b_) * dY).sum())
+
+    h = 1e-6
+    for (r, c) in [(0, 0), (n - 1, 3), (n // 2, 1)]:
+        Sp, Sm = S.copy(), S.copy()
+        Sp[r, c] += h
+        Sm[r, c] -= h
+        assert abs((loss(Sp, W, bias) - loss(Sm, W, bias)) / (2 * h) - dS[r, c]) < 1e-6
+    for (j, c, o) in [(0, 0, 0), (2, 4, 5), (3, 1, 2)]:
+        Wp, Wm = W.copy(), W.copy()
+        Wp[j, c, o] += h
+        Wm[j, c, o] -= h
+        assert abs((loss(S, Wp, bias) - loss(S, Wm, bias)) / (2 * h) - dW[j, c, o]) < 1e-6
+    bp = bias.copy()
+    bp[2] += 1.0
+    assert abs(loss(S, W, bp) - loss(S, W, bias) - db[2]) < 1e-9
+    G = rng.standard_normal((n, W.shape[2]))
+    dSG = O.sparse_conv_backward(S, coords, B, V, nbr, W, G)[0]
+    lhs = float((O.sparse_conv(S, coords, B, V, nbr, W) * G).sum())
+    assert abs(lhs - float((S * dSG).sum())) < 1e-10 * max(1.0, abs(lhs))
+
+
+def test_conv_backward_brute_force_tiny():
+    """Pure-Python loops over (row, slot) pairs."""
+    rng = np.random.default_rng(46)
+    m, coords, n, S, nbr, W, bias = bwd_case(rng, B=2, V=7, K=3, Ci=2, Co=3, p=0.6)
+    B, V = m.shape
+    Y = np.maximum(rng.standard_normal((n, 3)), 0.0)
+    dY = rng.standard_normal((n, 3))
+    dS, dW, db = O.sparse_conv_backward(S, coords, B, V, nbr, W, dY, Y, act=True)
+    row = {(int(b), int(v)): i for i, (b, v) in enumerate(coords)}
+    eS = [[0.0] * 2 for _ in range(n)]
+    eW = [[[0.0] * 3 for _ in range(2)] for _ in range(3)]
+    eb = [0.0] * 3
+    for i, (b, v) in enumerate(coords.tolist()):
+        for o in range(3):
+            g = float(dY[i, o]) if Y[i, o] > 0 else 0.0
+            eb[o] += g
+            for j in range(3):
+                u = int(nbr[v, j])
+                if u < 0 or (b, u) not in row:
+                    continue
+                src = row[(b, u)]
+                for c in range(2):
+                    eS[src][c] += g * float(W[j, c, o])
+                    eW[j][c][o] += float(S[src, c]) * g
+    np.testing.assert_allclose(dS, eS, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dW, eW, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(db, eb, rtol=1e-12, atol=1e-12)
+
+
+def test_conv_backward_special_cases_and_rows_at():
+    """A single self slot is the linear layer's backward; an inactive
+    neighbour receives nothing; the per-row evaluation agrees."""
+    rng = np.random.default_rng(47)
+    m, coords, n, S, nbr, W, bias = bwd_case(rng)
+    B, V = m.shape
+    dY = rng.standard_normal((n, W.shape[2]))
+    self_nbr = np.arange(V, dtype=np.int32)[:, None]
+    got = O.sparse_conv_backward(S, coords, B, V, self_nbr, W[:1], dY)
+    want = O.sparse_linear_backward(S, W[0], dY)
+    for a, b in zip(got, want):
+        np.testing.assert_allclose(a, np.reshape(b, a.shape), rtol=1e-12, atol=1e-12)
+    dS = O.sparse_conv_backward(S, coords, B, V, nbr, W, dY)[0]
+    rows = np.array([0, n // 3, n - 1])
+    np.testing.assert_allclose(O.conv_backward_input_at(coords, B, V, nbr, W, dY, rows),
+                               dS[rows], rtol=1e-12, atol=1e-12)
+    # a lone active vertex whose slots point elsewhere gets only its self term
+    m1 = np.zeros((1, V), np.uint8)
+    m1[0, 5] = 1
+    c1 = O.compact(m1)[0]
+    d1 = O.sparse_conv_backward(S[:1], c1, 1, V, nbr, W, dY[:1])
+    np.testing.assert_allclose(d1[0], dY[:1] @ W[0].T, rtol=1e-12, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
 # group normalization (Eqs. 7-9)
 # ----------------------------------------------------------------------------
 
