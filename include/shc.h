@@ -359,6 +359,104 @@ int shc_mask_scores(const void* O, int32_t K, int64_t N, int32_t C, int32_t dtyp
 int shc_segment_maxpool(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
                         int32_t C, int32_t dtype, float empty_value, void* P, hipStream_t stream);
 
+/* ------------------------------------------------------------------------ */
+/* Backward of the sparse linear layer (Eq. 6) and the sparse neighbourhood   */
+/* convolution (Eqs. 4-5), with the ReLU of Eq. 10.                           */
+/* ------------------------------------------------------------------------ */
+
+/* Virtual slots of a transposed neighbour list (see shc_transpose_neighbors). */
+#define SHC_MAX_VIRTUAL_SLOTS 64
+
+/*
+ * Transposed neighbour lists of a mesh, built once per mesh.  For vertex u
+ * and slot j, the vertices v with nbr[v][j] = u, ascending, are u's senders
+ * through slot j; the c-th of them sits in virtual slot s = off_j + c, where
+ * off_j = sum_{j' < j} m_j' and m_j is the largest number of senders any
+ * vertex has through slot j.  Kt = sum_j m_j.
+ *
+ *   nbr [V][K] int32 (entries outside [0, V) mean "no neighbour");
+ *   nbr_t [V][SHC_MAX_VIRTUAL_SLOTS] int32 out: the first V * Kt entries hold
+ *     [V][Kt] (sender vertex or -1), the rest -1;
+ *   slot_of [SHC_MAX_VIRTUAL_SLOTS] int32 out: the slot j of virtual slot s
+ *     (-1 past Kt);
+ *   *Kt_host out (host memory): Kt.  The call waits for the stream.
+ *   ws: device workspace of shc_transpose_neighbors_workspace(V, K) bytes.
+ * K <= 32; a mesh with Kt > SHC_MAX_VIRTUAL_SLOTS gets SHC_ERR_UNSUPPORTED.
+ */
+size_t shc_transpose_neighbors_workspace(int32_t V, int32_t K);
+int shc_transpose_neighbors(const int32_t* nbr, int32_t V, int32_t K, int32_t* nbr_t,
+                            int32_t* slot_of, int32_t* Kt_host, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/*
+ * Transposed table of an active set (the companion of
+ * shc_build_neighbor_table): for active row r = (b, u) and virtual slot s,
+ *
+ *   table_t[s * n_rows + r] = inv[b * V + nbr_t[u * Kt + s]], or -1,
+ *
+ * the active row that sends to r through s; row_slots[r] has bit s set when
+ * that entry is a row.  coords, inv: from shc_compact_mask; table_t
+ * [Kt][n_rows] int32 and row_slots [n_rows] uint64 out.  Kt <= 64.
+ */
+int shc_build_transposed_table(const int32_t* coords, const int32_t* inv, int64_t n_rows,
+                               int32_t B, int32_t V, const int32_t* nbr_t, int32_t Kt,
+                               int32_t* table_t, uint64_t* row_slots, hipStream_t stream);
+
+/*
+ * Gradients of the sparse linear layer out = act(S W + b) (Eq. 6, Eq. 10):
+ *
+ *   dZ = dY (.) [Y > 0] with act = SHC_ACT_RELU (dZ = dY without),
+ *   dS = dZ W^T,   dW = S^T dZ,   db = sum over rows of dZ,
+ *
+ * the dense layer's gradients at the active rows (rows are independent).
+ *   S [n_rows][Cin], W [Cin][Cout], Y = the layer's output [n_rows][Cout]
+ *   (read only with SHC_ACT_RELU), dY [n_rows][Cout]: bf16;
+ *   dS [n_rows][Cin] bf16 out, dW [Cin][Cout] fp32 out, db [Cout] fp32 out;
+ *   each output may be NULL (not computed).
+ *   ws: device workspace of shc_sparse_linear_backward_workspace bytes.
+ * Every sum has a fixed order: dS in fp32 over Cout, rounded once; dW in
+ * fp32 over chunks of rows, the chunks combined in fp64; db in fp32 over
+ * splits of rows, combined in fp64.  Results repeat bit for bit.
+ * bf16 only (SHC_ERR_UNSUPPORTED otherwise); Cout <= 256.
+ */
+size_t shc_sparse_linear_backward_workspace(int64_t n_rows, int32_t Cin, int32_t Cout,
+                                            int32_t dtype);
+int shc_sparse_linear_backward(const void* S, const void* W, const void* Y, const void* dY,
+                               int64_t n_rows, int32_t Cin, int32_t Cout, int32_t dtype,
+                               int32_t act, void* dS, float* dW, float* db, void* ws,
+                               size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Gradients of the sparse neighbourhood convolution (Eqs. 4-5, Eq. 10),
+ * i.e. of the dense convolution of x (.) m restricted to the active rows:
+ *
+ *   dZ = dY (.) [Y > 0] (SHC_ACT_RELU) or dY,
+ *   dW[j] = sum over rows i with table[j][i] >= 0 of S[table[j][i]]^T dZ[i],
+ *   db = sum over rows of dZ,
+ *   dS[r] = sum over (i, j) with table[j][i] = r of dZ[i] W[j]^T.
+ *
+ *   S [n_rows][Cin], W [K][Cin][Cout], Y, dY [n_rows][Cout]: bf16;
+ *   table [K][n_rows]: shc_build_neighbor_table of the active set;
+ *   table_t, row_slots: shc_build_transposed_table of the same active set;
+ *   slot_of, Kt: shc_transpose_neighbors of the mesh;
+ *   dS [n_rows][Cin] bf16 out, dW [K][Cin][Cout] fp32 out, db [Cout] fp32
+ *   out; each may be NULL (table_t, row_slots and slot_of are then only read
+ *   when dS is requested).
+ *   ws: device workspace of shc_sparse_neighbor_conv_backward_workspace bytes.
+ * dS sums its terms in ascending virtual slot order in fp32 and rounds once;
+ * dW and db as in shc_sparse_linear_backward.  bf16 only; K <= 32;
+ * Cout <= 256.
+ */
+size_t shc_sparse_neighbor_conv_backward_workspace(int64_t n_rows, int32_t K, int32_t Cin,
+                                                   int32_t Cout, int32_t dtype);
+int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table,
+                                      const int32_t* table_t, const uint64_t* row_slots,
+                                      const int32_t* slot_of, int32_t Kt, const void* W,
+                                      const void* Y, const void* dY, int64_t n_rows, int32_t K,
+                                      int32_t Cin, int32_t Cout, int32_t dtype, int32_t act,
+                                      void* dS, float* dW, float* db, void* ws, size_t ws_bytes,
+                                      hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -81,6 +81,22 @@ _SIGS = {
                                        _c_ptr, _c_i32, _c_ptr, _c_ptr, _c_sz, _c_ptr]),
     "shc_segment_maxpool": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_f,
                                            _c_ptr, _c_ptr]),
+    "shc_transpose_neighbors_workspace": (_c_sz, [_c_i32, _c_i32]),
+    "shc_transpose_neighbors": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr,
+                                               _c_ptr, _c_sz, _c_ptr]),
+    "shc_build_transposed_table": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_ptr,
+                                                  _c_i32, _c_ptr, _c_ptr, _c_ptr]),
+    "shc_sparse_linear_backward_workspace": (_c_sz, [_c_i64, _c_i32, _c_i32, _c_i32]),
+    "shc_sparse_linear_backward": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i32,
+                                                  _c_i32, _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr,
+                                                  _c_ptr, _c_sz, _c_ptr]),
+    "shc_sparse_neighbor_conv_backward_workspace": (_c_sz, [_c_i64, _c_i32, _c_i32, _c_i32,
+                                                            _c_i32]),
+    "shc_sparse_neighbor_conv_backward": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
+                                                         _c_i32, _c_ptr, _c_ptr, _c_ptr, _c_i64,
+                                                         _c_i32, _c_i32, _c_i32, _c_i32, _c_i32,
+                                                         _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_sz,
+                                                         _c_ptr]),
 }
 
 
@@ -394,6 +410,90 @@ def segment_maxpool(S: torch.Tensor, row_ptr: torch.Tensor, n_rows: int, B: int,
             _dev(row_ptr, "row_ptr", torch.int32, B + 1), n_rows, B, C, dt, float(empty_value),
             _dev(P, "P", P.dtype, B * C), _stream(stream)]
     _check(load().shc_segment_maxpool(*args), "shc_segment_maxpool")
+
+
+# ----------------------------------------------------------------------------
+# backward of the linear and conv layers
+# ----------------------------------------------------------------------------
+
+SHC_MAX_VIRTUAL_SLOTS = 64
+
+
+def transpose_neighbors(nbr: torch.Tensor, stream=None):
+    """shc_transpose_neighbors on nbr [V][K] int32 (device).  Returns
+    (nbr_t [V][64] int32, slot_of [64] int32, Kt); waits for the stream."""
+    V, K = nbr.shape
+    need = int(load().shc_transpose_neighbors_workspace(V, K))
+    ws = torch.empty(max(need, 16), dtype=torch.uint8, device=nbr.device)
+    nbr_t = torch.empty((V, SHC_MAX_VIRTUAL_SLOTS), dtype=torch.int32, device=nbr.device)
+    slot_of = torch.empty(SHC_MAX_VIRTUAL_SLOTS, dtype=torch.int32, device=nbr.device)
+    kt = ctypes.c_int32(0)
+    args = [_dev(nbr, "nbr", torch.int32, V * K), V, K, _dev(nbr_t, "nbr_t"),
+            _dev(slot_of, "slot_of"), ctypes.addressof(kt), _dev(ws, "ws"),
+            ws.numel(), _stream(stream)]
+    _check(load().shc_transpose_neighbors(*args), "shc_transpose_neighbors")
+    return nbr_t, slot_of, int(kt.value)
+
+
+def build_transposed_table(coords: torch.Tensor, inv: torch.Tensor, n_rows: int, B: int, V: int,
+                           nbr_t: torch.Tensor, Kt: int, table_t: torch.Tensor,
+                           row_slots: torch.Tensor, stream=None):
+    """shc_build_transposed_table: table_t [Kt][n_rows] int32, row_slots [n_rows] int64."""
+    args = [_dev(coords, "coords", torch.int32, 2 * n_rows), _dev(inv, "inv", torch.int32, B * V),
+            n_rows, B, V, _dev(nbr_t, "nbr_t", torch.int32, V * Kt), Kt,
+            _dev(table_t, "table_t", torch.int32, Kt * n_rows),
+            _dev(row_slots, "row_slots", torch.int64, n_rows), _stream(stream)]
+    _check(load().shc_build_transposed_table(*args), "shc_build_transposed_table")
+
+
+def sparse_linear_backward_workspace(n_rows: int, Cin: int, Cout: int, dtype: int = SHC_BF16):
+    return int(load().shc_sparse_linear_backward_workspace(n_rows, Cin, Cout, dtype))
+
+
+def sparse_linear_backward(S, W, Y, dY, n_rows: int, dS=None, dW=None, db=None,
+                           act: int = SHC_ACT_RELU, ws=None, stream=None):
+    """shc_sparse_linear_backward; W [Cin][Cout] bf16, dW / db fp32.  Returns the workspace."""
+    Cin, Cout = W.shape
+    need = sparse_linear_backward_workspace(n_rows, Cin, Cout, _dtype_code(W))
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=W.device)
+    dt = W.dtype
+    args = [_opt_dev(S, "S", dt, n_rows * Cin), _dev(W, "W", dt, Cin * Cout),
+            _opt_dev(Y, "Y", dt, n_rows * Cout), _dev(dY, "dY", dt, n_rows * Cout), n_rows, Cin,
+            Cout, _dtype_code(W), act, _opt_dev(dS, "dS", dt, n_rows * Cin),
+            _opt_dev(dW, "dW", torch.float32, Cin * Cout),
+            _opt_dev(db, "db", torch.float32, Cout), _dev(ws, "ws"),
+            ws.numel() * ws.element_size(), _stream(stream)]
+    _check(load().shc_sparse_linear_backward(*args), "shc_sparse_linear_backward")
+    return ws
+
+
+def sparse_neighbor_conv_backward_workspace(n_rows: int, K: int, Cin: int, Cout: int,
+                                            dtype: int = SHC_BF16):
+    return int(load().shc_sparse_neighbor_conv_backward_workspace(n_rows, K, Cin, Cout, dtype))
+
+
+def sparse_neighbor_conv_backward(S, table, table_t, row_slots, slot_of, Kt: int, W, Y, dY,
+                                  n_rows: int, dS=None, dW=None, db=None,
+                                  act: int = SHC_ACT_RELU, ws=None, stream=None):
+    """shc_sparse_neighbor_conv_backward; W [K][Cin][Cout] bf16, dW [K][Cin][Cout] and db fp32.
+    Returns the workspace."""
+    K, Cin, Cout = W.shape
+    need = sparse_neighbor_conv_backward_workspace(n_rows, K, Cin, Cout, _dtype_code(W))
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=W.device)
+    dt = W.dtype
+    args = [_opt_dev(S, "S", dt, n_rows * Cin), _opt_dev(table, "table", torch.int32, K * n_rows),
+            _opt_dev(table_t, "table_t", torch.int32, Kt * n_rows),
+            _opt_dev(row_slots, "row_slots", torch.int64, n_rows),
+            _opt_dev(slot_of, "slot_of", torch.int32, Kt), Kt, _dev(W, "W", dt, K * Cin * Cout),
+            _opt_dev(Y, "Y", dt, n_rows * Cout), _dev(dY, "dY", dt, n_rows * Cout), n_rows, K,
+            Cin, Cout, _dtype_code(W), act, _opt_dev(dS, "dS", dt, n_rows * Cin),
+            _opt_dev(dW, "dW", torch.float32, K * Cin * Cout),
+            _opt_dev(db, "db", torch.float32, Cout), _dev(ws, "ws"),
+            ws.numel() * ws.element_size(), _stream(stream)]
+    _check(load().shc_sparse_neighbor_conv_backward(*args), "shc_sparse_neighbor_conv_backward")
+    return ws
 
 
 # ----------------------------------------------------------------------------

@@ -550,6 +550,155 @@ int shc_mask_scores(const void* O, int32_t K, int64_t N, int32_t C, int32_t dtyp
                     "mask_scores launch");
 }
 
+size_t shc_transpose_neighbors_workspace(int32_t V, int32_t K) {
+  if (V <= 0 || K <= 0 || K > kMaxSlots) return 0;
+  return shc::transpose_neighbors_ws_bytes(V, K);
+}
+
+int shc_transpose_neighbors(const int32_t* nbr, int32_t V, int32_t K, int32_t* nbr_t,
+                            int32_t* slot_of, int32_t* Kt_host, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (V <= 0) return fail(SHC_ERR_INVALID_ARG, "V = %d must be positive", V);
+  if (K <= 0) return fail(SHC_ERR_INVALID_ARG, "K = %d must be positive", K);
+  if (K > kMaxSlots) return fail(SHC_ERR_UNSUPPORTED, "K = %d exceeds %d slots", K, kMaxSlots);
+  if ((int64_t)V * SHC_MAX_VIRTUAL_SLOTS > INT32_MAX)
+    return fail(SHC_ERR_UNSUPPORTED, "V = %d is too large for the transposed lists", V);
+  SHC_PTR(nbr, "nbr");
+  SHC_PTR(nbr_t, "nbr_t");
+  SHC_PTR(slot_of, "slot_of");
+  SHC_PTR(ws, "ws");
+  if (Kt_host == nullptr) return fail(SHC_ERR_INVALID_ARG, "Kt_host is NULL");
+  const size_t need = shc_transpose_neighbors_workspace(V, K);
+  if (ws_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "workspace of %zu bytes is below the %zu needed", ws_bytes, need);
+  // the slot offsets follow the two count arrays in the workspace
+  int32_t* off = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(ws) + need -
+                                            (((size_t)(K + 1) * 4 + 255) & ~(size_t)255));
+  SHC_TRY(hip_status(shc::launch_transpose_neighbors(nbr, V, K, nbr_t, slot_of, off, ws, stream),
+                     "transpose_neighbors launch"));
+  int32_t kt = 0;
+  SHC_TRY(hip_status(hipMemcpyAsync(&kt, off + K, sizeof(int32_t), hipMemcpyDeviceToHost, stream),
+                     "transpose_neighbors Kt copy"));
+  SHC_TRY(hip_status(hipStreamSynchronize(stream), "transpose_neighbors stream sync"));
+  *Kt_host = kt;
+  if (kt > SHC_MAX_VIRTUAL_SLOTS)
+    return fail(SHC_ERR_UNSUPPORTED, "the mesh needs Kt = %d virtual slots, above %d", kt,
+                SHC_MAX_VIRTUAL_SLOTS);
+  return SHC_OK;
+}
+
+int shc_build_transposed_table(const int32_t* coords, const int32_t* inv, int64_t n_rows,
+                               int32_t B, int32_t V, const int32_t* nbr_t, int32_t Kt,
+                               int32_t* table_t, uint64_t* row_slots, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_rows(n_rows));
+  if (Kt < 1 || Kt > SHC_MAX_VIRTUAL_SLOTS)
+    return fail(SHC_ERR_INVALID_ARG, "Kt = %d outside [1, %d]", Kt, SHC_MAX_VIRTUAL_SLOTS);
+  if ((int64_t)Kt * n_rows > INT32_MAX)
+    return fail(SHC_ERR_UNSUPPORTED, "Kt * n_rows exceeds 2^31 - 1");
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(coords, "coords");
+  SHC_PTR(inv, "inv");
+  SHC_PTR(nbr_t, "nbr_t");
+  SHC_PTR(table_t, "table_t");
+  SHC_PTR(row_slots, "row_slots");
+  return hip_status(shc::launch_transposed_table(coords, inv, n_rows, B, V, nbr_t, Kt, table_t,
+                                                 row_slots, stream),
+                    "build_transposed_table launch");
+}
+
+// Shared checks of the two layer backward calls.
+static int check_backward(const void* S, const void* W, const void* Y, const void* dY,
+                          int64_t n_rows, int32_t Kw, int32_t Cin, int32_t Cout, int32_t dtype,
+                          int32_t act, const void* dS, const float* dW, const float* db,
+                          const void* ws, size_t ws_bytes, size_t need) {
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_dtype(dtype));
+  if (dtype != SHC_BF16) return fail(SHC_ERR_UNSUPPORTED, "the backward takes bf16 tensors");
+  SHC_TRY(check_channels("Cin", Cin));
+  SHC_TRY(check_channels("Cout", Cout));
+  if (Cout > 256) return fail(SHC_ERR_UNSUPPORTED, "Cout = %d above 256", Cout);
+  if (act != SHC_ACT_NONE && act != SHC_ACT_RELU)
+    return fail(SHC_ERR_UNSUPPORTED, "unknown activation code %d", act);
+  if (n_rows * (int64_t)(Cin > Cout ? Cin : Cout) * 2 > INT32_MAX)
+    return fail(SHC_ERR_UNSUPPORTED, "a feature tensor of %lld rows exceeds 2 GiB",
+                (long long)n_rows);
+  if (dS != nullptr && !shc::backward_dgrad_supported(Kw, Cin, Cout))
+    return fail(SHC_ERR_UNSUPPORTED, "input gradient for K = %d, Cin = %d, Cout = %d does not fit",
+                Kw, Cin, Cout);
+  SHC_OPT_PTR(dS, "dS");
+  SHC_OPT_PTR(dW, "dW");
+  SHC_OPT_PTR(db, "db");
+  if (n_rows > 0) {
+    SHC_PTR(dY, "dY");
+    if (act == SHC_ACT_RELU) SHC_PTR(Y, "Y");
+    if (dW != nullptr) SHC_PTR(S, "S");
+  }
+  if (dS != nullptr || dW != nullptr) SHC_PTR(W, "W");
+  if (n_rows > 0 || dW != nullptr || db != nullptr) SHC_PTR(ws, "ws");
+  if (ws_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "workspace of %zu bytes is below the %zu needed", ws_bytes, need);
+  return SHC_OK;
+}
+
+size_t shc_sparse_linear_backward_workspace(int64_t n_rows, int32_t Cin, int32_t Cout,
+                                            int32_t dtype) {
+  if (n_rows < 0 || Cin <= 0 || Cout <= 0 || dtype != SHC_BF16) return 0;
+  shc::BwdPlan pl;
+  shc::backward_plan(n_rows, 1, Cin, Cout, 1, 0, &pl);
+  return pl.total;
+}
+
+int shc_sparse_linear_backward(const void* S, const void* W, const void* Y, const void* dY,
+                               int64_t n_rows, int32_t Cin, int32_t Cout, int32_t dtype,
+                               int32_t act, void* dS, float* dW, float* db, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_backward(S, W, Y, dY, n_rows, 1, Cin, Cout, dtype, act, dS, dW, db, ws, ws_bytes,
+                         shc_sparse_linear_backward_workspace(n_rows, Cin, Cout, dtype)));
+  return hip_status(shc::launch_layer_backward(0, S, nullptr, nullptr, nullptr, nullptr, W, Y, dY,
+                                               n_rows, 1, Cin, Cout, act, dS, dW, db, ws, stream),
+                    "sparse_linear_backward launch");
+}
+
+size_t shc_sparse_neighbor_conv_backward_workspace(int64_t n_rows, int32_t K, int32_t Cin,
+                                                   int32_t Cout, int32_t dtype) {
+  if (n_rows < 0 || K <= 0 || K > kMaxSlots || Cin <= 0 || Cout <= 0 || dtype != SHC_BF16)
+    return 0;
+  shc::BwdPlan pl;
+  shc::backward_plan(n_rows, K, Cin, Cout, 1, 1, &pl);
+  return pl.total;
+}
+
+int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table,
+                                      const int32_t* table_t, const uint64_t* row_slots,
+                                      const int32_t* slot_of, int32_t Kt, const void* W,
+                                      const void* Y, const void* dY, int64_t n_rows, int32_t K,
+                                      int32_t Cin, int32_t Cout, int32_t dtype, int32_t act,
+                                      void* dS, float* dW, float* db, void* ws, size_t ws_bytes,
+                                      hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (K <= 0) return fail(SHC_ERR_INVALID_ARG, "K = %d must be positive", K);
+  if (K > kMaxSlots) return fail(SHC_ERR_UNSUPPORTED, "K = %d exceeds %d slots", K, kMaxSlots);
+  SHC_TRY(check_backward(S, W, Y, dY, n_rows, K, Cin, Cout, dtype, act, dS, dW, db, ws, ws_bytes,
+                         shc_sparse_neighbor_conv_backward_workspace(n_rows, K, Cin, Cout, dtype)));
+  if ((int64_t)K * n_rows > INT32_MAX)
+    return fail(SHC_ERR_UNSUPPORTED, "K * n_rows exceeds 2^31 - 1");
+  if (n_rows > 0 && dW != nullptr) SHC_PTR(table, "table");
+  if (n_rows > 0 && dS != nullptr) {
+    if (Kt < 1 || Kt > SHC_MAX_VIRTUAL_SLOTS)
+      return fail(SHC_ERR_INVALID_ARG, "Kt = %d outside [1, %d]", Kt, SHC_MAX_VIRTUAL_SLOTS);
+    SHC_PTR(table_t, "table_t");
+    SHC_PTR(row_slots, "row_slots");
+    SHC_PTR(slot_of, "slot_of");
+  }
+  return hip_status(shc::launch_layer_backward(1, S, table, table_t, row_slots, slot_of, W, Y, dY,
+                                               n_rows, K, Cin, Cout, act, dS, dW, db, ws, stream),
+                    "sparse_neighbor_conv_backward launch");
+}
+
 int shc_segment_maxpool(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
                         int32_t C, int32_t dtype, float empty_value, void* P, hipStream_t stream) {
   g_last_error[0] = 0;

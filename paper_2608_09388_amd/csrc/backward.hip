@@ -1,0 +1,824 @@
+// Backward of the sparse linear layer (Eq. 6) and the sparse neighbourhood
+// convolution (Eqs. 4-5), with the ReLU of Eq. 10.  The gradients are those
+// of the dense operator on x (.) m restricted to the active rows:
+//
+//   dZ = dY (.) [Y > 0]                       (Y: the layer's stored output)
+//   db[o]       = sum_i dZ[i][o]
+//   dW[j][c][o] = sum_{i : r_ij >= 0} S[r_ij][c] dZ[i][o]
+//   dS[r][c]    = sum_{(i, j) : r_ij = r} sum_o dZ[i][o] W[j][c][o]
+//
+// with r_ij the row that slot j of row i reads (the neighbour-row table;
+// r_i0 = i and K = 1 for the linear layer).
+//
+// Kernels:
+//   * relu_bwd     -- dZ, and per-split column sums of dZ (db, fixed order);
+//   * transposed neighbour lists, once per mesh: for vertex u and slot j, the
+//     vertices v whose slot j points at u, ascending.  The c-th of them is
+//     "virtual slot" (j, c); a mesh has Kt = sum_j max_u |list(u, j)| of them;
+//   * transposed table, once per active set: for active row r and virtual
+//     slot s = (j, c), the active row that sends to r through it (or -1),
+//     plus a 64-bit mask of the virtual slots present in the row;
+//   * dgrad (dS)   -- the transposed table makes dS a gathered contraction
+//     like the forward one: rows of dZ gathered per virtual slot, times
+//     W[j]^T.  A B fragment of W[j]^T (8 consecutive reduction entries o of
+//     one output column c) is 16 contiguous bytes of W[j][c][.], so the
+//     weights go to LDS in fragment order with plain copies;
+//   * wgrad (dW)   -- per slot, the Gram-type contraction S[r_ij]^T dZ[i] over
+//     the rows i where slot j is present.  Those rows come from a compaction
+//     of the [K][N'] presence mask (slot-major lists, ascending i); each list
+//     is cut into chunks of a fixed number of rows, a workgroup multiplies one
+//     chunk into a fp32 partial tile, and the partials of a slot are summed in
+//     chunk order in fp64.
+// Every sum has a fixed order, so results repeat bit for bit.
+#include <algorithm>
+
+#include "shc_internal.h"
+
+namespace shc {
+namespace {
+
+constexpr int kThreads = 256;
+#define SHC_LDS __attribute__((address_space(3)))
+typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
+typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+constexpr int kBufferWord3 = 0x00020000;
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr int kMaxSlotsBwd = 32;
+constexpr int kWgradRows = 128;      // rows per step of the wgrad tile kernel
+constexpr int kDgradLds = 160 * 1024;
+
+// ---------------------------------------------------------------------------
+// dZ and the column sums of db
+// ---------------------------------------------------------------------------
+
+// Workgroup s takes rows [s * rps, (s + 1) * rps).  A thread owns one 16-byte
+// vector column q of rows y, y + ty, ...; its sums, then the ty row groups in
+// order, give colpart[s][c].  With act == 0, dZ = dY and nothing is written.
+template <bool BF16>
+__global__ __launch_bounds__(kThreads) void relu_bwd_kernel(const i32x4* __restrict__ dY,
+                                                            const i32x4* __restrict__ Y,
+                                                            int64_t n, int32_t C, int act,
+                                                            int64_t rps, i32x4* __restrict__ dZ,
+                                                            float* __restrict__ colpart) {
+  constexpr int PER = BF16 ? 8 : 4;
+  __shared__ float red[kThreads * 8];
+  const int vpr = C / PER;
+  const int ty = kThreads / vpr;
+  const int q = threadIdx.x % vpr, y = threadIdx.x / vpr;
+  const int64_t r0 = (int64_t)blockIdx.x * rps;
+  const int64_t r1 = min(r0 + rps, n);
+  float s[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) s[e] = 0.f;
+  if (y < ty) {
+    for (int64_t r = r0 + y; r < r1; r += ty) {
+      const int64_t idx = r * vpr + q;
+      i32x4 g = dY[idx];
+      if (act) {
+        const i32x4 yv = Y[idx];
+        if (BF16) {
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const uint32_t gw = (uint32_t)g[w], yw = (uint32_t)yv[w];
+            const uint32_t lo = bf16_bits_to_f32(yw & 0xFFFFu) > 0.f ? (gw & 0xFFFFu) : 0u;
+            const uint32_t hi = bf16_bits_to_f32(yw >> 16) > 0.f ? (gw & 0xFFFF0000u) : 0u;
+            g[w] = (int)(lo | hi);
+          }
+        } else {
+#pragma unroll
+          for (int w = 0; w < 4; ++w) g[w] = __int_as_float(yv[w]) > 0.f ? g[w] : 0;
+        }
+        dZ[idx] = g;
+      }
+      if (BF16) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          s[2 * w] += bf16_bits_to_f32((uint32_t)g[w] & 0xFFFFu);
+          s[2 * w + 1] += bf16_bits_to_f32((uint32_t)g[w] >> 16);
+        }
+      } else {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) s[w] += __int_as_float(g[w]);
+      }
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < PER; ++e) red[threadIdx.x * 8 + e] = s[e];
+  __syncthreads();
+  for (int c = threadIdx.x; c < C; c += kThreads) {
+    const int qq = c / PER, e = c % PER;
+    float t = 0.f;
+    for (int yy = 0; yy < ty; ++yy) t += red[(yy * vpr + qq) * 8 + e];
+    colpart[(int64_t)blockIdx.x * C + c] = t;
+  }
+}
+
+// db[c] = sum over splits of colpart[s][c], fp64 in split order, one rounding.
+__global__ __launch_bounds__(kThreads) void colsum_kernel(const float* __restrict__ colpart,
+                                                          int splits, int32_t C,
+                                                          float* __restrict__ db) {
+  const int c = blockIdx.x * kThreads + threadIdx.x;
+  if (c >= C) return;
+  double t = 0.0;
+  for (int s = 0; s < splits; ++s) t += (double)colpart[(int64_t)s * C + c];
+  db[c] = (float)t;
+}
+
+// ---------------------------------------------------------------------------
+// transposed neighbour lists (once per mesh)
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kThreads) void fill_i32_kernel(int32_t* __restrict__ p, int64_t n,
+                                                            int32_t v) {
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kThreads)
+    p[i] = v;
+}
+
+// cnt[u * K + j] = number of v with nbr[v][j] = u
+__global__ __launch_bounds__(kThreads) void tv_count_kernel(const int32_t* __restrict__ nbr,
+                                                            int32_t V, int32_t K,
+                                                            int32_t* __restrict__ cnt) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= (int64_t)V * K) return;
+  const int j = (int)(e % K);
+  const int32_t u = nbr[e];
+  if (u >= 0 && u < V) atomicAdd(&cnt[(int64_t)u * K + j], 1);
+}
+
+// One workgroup: m_j = max_u cnt[u][j]; off[j] = sum_{j' < j} m_j'; off[K] = Kt;
+// slot_of[s] = j for the virtual slots s of slot j.
+__global__ __launch_bounds__(kThreads) void tv_layout_kernel(const int32_t* __restrict__ cnt,
+                                                             int32_t V, int32_t K,
+                                                             int32_t* __restrict__ off,
+                                                             int32_t* __restrict__ slot_of,
+                                                             int32_t max_kt) {
+  __shared__ int32_t mx[kThreads];
+  __shared__ int32_t mj[kMaxSlotsBwd];
+  for (int j = 0; j < K; ++j) {
+    int32_t m = 0;
+    for (int32_t u = threadIdx.x; u < V; u += kThreads) m = max(m, cnt[(int64_t)u * K + j]);
+    mx[threadIdx.x] = m;
+    __syncthreads();
+    for (int w = kThreads / 2; w > 0; w >>= 1) {
+      if (threadIdx.x < w) mx[threadIdx.x] = max(mx[threadIdx.x], mx[threadIdx.x + w]);
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) mj[j] = mx[0];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    int32_t o = 0;
+    for (int j = 0; j < K; ++j) {
+      off[j] = o;
+      for (int c = 0; c < mj[j]; ++c)
+        if (o + c < max_kt) slot_of[o + c] = j;
+      o += mj[j];
+    }
+    off[K] = o;
+  }
+}
+
+// tv[u * Kt + off[j] + c] = v for the c-th (arrival order) v with nbr[v][j] = u
+__global__ __launch_bounds__(kThreads) void tv_fill_kernel(const int32_t* __restrict__ nbr,
+                                                           int32_t V, int32_t K,
+                                                           const int32_t* __restrict__ off,
+                                                           int32_t* __restrict__ cur,
+                                                           int32_t* __restrict__ tv,
+                                                           int32_t max_kt) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= (int64_t)V * K) return;
+  const int32_t Kt = off[K];
+  if (Kt > max_kt) return;  // does not fit: the caller reports it
+  const int j = (int)(e % K);
+  const int32_t v = (int32_t)(e / K);
+  const int32_t u = nbr[e];
+  if (u < 0 || u >= V) return;
+  const int c = atomicAdd(&cur[(int64_t)u * K + j], 1);
+  tv[(int64_t)u * Kt + off[j] + c] = v;
+}
+
+// sort each (u, j) run ascending, so the order does not depend on arrival
+__global__ __launch_bounds__(kThreads) void tv_sort_kernel(const int32_t* __restrict__ cnt,
+                                                           int32_t V, int32_t K,
+                                                           const int32_t* __restrict__ off,
+                                                           int32_t* __restrict__ tv,
+                                                           int32_t max_kt) {
+  const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (e >= (int64_t)V * K) return;
+  const int32_t Kt = off[K];
+  if (Kt > max_kt) return;
+  const int j = (int)(e % K);
+  const int64_t u = e / K;
+  const int m = cnt[e];
+  int32_t* p = tv + u * Kt + off[j];
+  for (int a = 1; a < m; ++a) {
+    const int32_t x = p[a];
+    int b = a - 1;
+    while (b >= 0 && p[b] > x) {
+      p[b + 1] = p[b];
+      --b;
+    }
+    p[b + 1] = x;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// transposed table of an active set
+// ---------------------------------------------------------------------------
+
+// table_t[s * n + i] = inv[b_i * V + tv[v_i * Kt + s]] or -1; row_slots[i] has
+// bit s set when that entry is a row.
+__global__ __launch_bounds__(kThreads) void tt_kernel(const int2* __restrict__ coords,
+                                                      const int32_t* __restrict__ inv, int64_t n,
+                                                      int32_t B, int32_t V,
+                                                      const int32_t* __restrict__ tv, int32_t Kt,
+                                                      int32_t* __restrict__ table_t,
+                                                      uint64_t* __restrict__ row_slots) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n) return;
+  const int2 c = coords[i];
+  const bool ok = c.x >= 0 && c.x < B && c.y >= 0 && c.y < V;
+  const int32_t* trow = tv + (int64_t)(ok ? c.y : 0) * Kt;
+  const int32_t* irow = inv + (int64_t)(ok ? c.x : 0) * V;
+  uint64_t bits = 0;
+  for (int s0 = 0; s0 < Kt; s0 += 16) {
+    int32_t v[16], r[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) v[u] = s0 + u < Kt ? trow[s0 + u] : -1;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const bool live = ok && v[u] >= 0 && v[u] < V;
+      r[u] = irow[live ? v[u] : 0];
+      r[u] = (live && r[u] >= 0 && (int64_t)r[u] < n) ? r[u] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (s0 + u < Kt) {
+        table_t[(int64_t)(s0 + u) * n + i] = r[u];
+        if (r[u] >= 0) bits |= 1ull << (s0 + u);
+      }
+  }
+  row_slots[i] = bits;
+}
+
+// ---------------------------------------------------------------------------
+// wgrad: presence mask, chunk schedule, partial tiles, reduction
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kThreads) void presence_kernel(const int32_t* __restrict__ table,
+                                                            int64_t total,
+                                                            uint8_t* __restrict__ m) {
+  for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * kThreads)
+    m[e] = table[e] >= 0 ? 1 : 0;
+}
+
+// cs[j] = first chunk of slot j (chunks of L rows of its list); cs[K] = total
+__global__ void chunk_schedule_kernel(const int32_t* __restrict__ row_ptr, int32_t K, int32_t L,
+                                      int32_t* __restrict__ cs) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  int32_t c = 0;
+  for (int j = 0; j < K; ++j) {
+    cs[j] = c;
+    const int32_t cnt = row_ptr[j + 1] - row_ptr[j];
+    c += (cnt + L - 1) / L;
+  }
+  cs[K] = c;
+}
+
+// Partial tile of dW[j] over one chunk of slot j's rows.  Workgroup
+// (chunk w, tile t); chunks past the last exit.  Pair t of the list is
+// (slot j, row i) = pairs[t]; the A row is S[table[j * n + i]], the B row
+// dZ[i].  Without a list (linear layer): one slot, row t itself on both sides.
+// Layout and MFMA scheme as the Gram tiles of the mask scores: R rows through
+// one padded LDS stage, both operands read with transposing reads, four
+// wavefronts each a (T/2) x (T/2) quarter.
+template <int T, int R>
+__global__ __launch_bounds__(kThreads) void wgrad_tile_kernel(
+    const __bf16* __restrict__ S, const __bf16* __restrict__ dZ, const int32_t* __restrict__ table,
+    const int2* __restrict__ pairs, const int32_t* __restrict__ row_ptr,
+    const int32_t* __restrict__ cs, int32_t K, int64_t n, int32_t L, int32_t Cin, int32_t Cout,
+    float* __restrict__ part) {
+  constexpr int NB = T / 32;
+  constexpr int ROW = T * 2 + 16;
+  constexpr int VPR = T * 2 / 16;
+  constexpr int LOADS = 2 * R * VPR / kThreads;
+  constexpr int kMaxL = 512;
+  __shared__ __attribute__((aligned(16))) unsigned char stage[2][R * ROW];
+  __shared__ int32_t ia[kMaxL], ib[kMaxL];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, l16 = lane & 15;
+  const int wa = wave >> 1, wb = wave & 1;
+  const int tA = (Cin + T - 1) / T, tB = (Cout + T - 1) / T;
+  const int tiles = tA * tB;
+  const int w = blockIdx.x / tiles, t = blockIdx.x - w * tiles;
+  const int ta = t / tB, tb = t - ta * tB;
+  int j = 0;
+  int64_t t0, t1;
+  if (pairs != nullptr) {
+    if (w >= cs[K]) return;
+    while (j + 1 < K && cs[j + 1] <= w) ++j;
+    const int64_t base = row_ptr[j] + (int64_t)(w - cs[j]) * L;
+    t0 = base;
+    t1 = min(base + L, (int64_t)row_ptr[j + 1]);
+  } else {
+    t0 = (int64_t)w * L;
+    if (t0 >= n) return;
+    t1 = min(t0 + L, n);
+  }
+  const int rows = (int)(t1 - t0);
+  // the chunk's row indices, once
+  for (int q = tid; q < rows; q += kThreads) {
+    if (pairs != nullptr) {
+      const int2 p = pairs[t0 + q];
+      const int32_t i = p.y;
+      const int32_t a = table[(int64_t)j * n + i];
+      ia[q] = a;
+      ib[q] = i;
+    } else {
+      ia[q] = (int32_t)(t0 + q);
+      ib[q] = (int32_t)(t0 + q);
+    }
+  }
+  __syncthreads();
+  const int steps = (rows + R - 1) / R;
+
+  auto load = [&](int step, i32x4* v) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int e = tid + u * kThreads;
+      const int op = e / (R * VPR);
+      const int rr = (e / VPR) % R;
+      const int q = e % VPR;
+      const int local = step * R + rr;
+      const int col = (op == 0 ? ta : tb) * T + q * 8;
+      const int C = op == 0 ? Cin : Cout;
+      v[u] = i32x4{0, 0, 0, 0};
+      if (local < rows && col < C) {
+        const int32_t row = op == 0 ? ia[local] : ib[local];
+        if (row >= 0)
+          v[u] = *reinterpret_cast<const i32x4*>((op == 0 ? S : dZ) + (int64_t)row * C + col);
+      }
+    }
+  };
+  auto store = [&](const i32x4* v) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int e = tid + u * kThreads;
+      const int op = e / (R * VPR);
+      const int rr = (e / VPR) % R;
+      const int q = e % VPR;
+      *reinterpret_cast<i32x4*>(&stage[op][rr * ROW + q * 16]) = v[u];
+    }
+  };
+  auto frag = [&](const unsigned char* base, int cb) -> bf16x8 {
+    const unsigned char* p0 = base + (8 * g + (l16 >> 2)) * ROW + cb * 32 + 8 * (l16 & 3);
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0)));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0 + 4 * ROW)));
+    return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  };
+
+  f32x4 acc[NB][NB];
+#pragma unroll
+  for (int x = 0; x < NB; ++x)
+#pragma unroll
+    for (int y = 0; y < NB; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+  i32x4 v[LOADS];
+  if (steps > 0) load(0, v);
+  for (int s = 0; s < steps; ++s) {
+    store(v);
+    __syncthreads();
+    if (s + 1 < steps) load(s + 1, v);
+#pragma unroll
+    for (int sub = 0; sub < R / 32; ++sub) {
+      bf16x8 fa[NB], fb[NB];
+#pragma unroll
+      for (int x = 0; x < NB; ++x) fa[x] = frag(stage[0] + sub * 32 * ROW, wa * NB + x);
+#pragma unroll
+      for (int y = 0; y < NB; ++y) fb[y] = frag(stage[1] + sub * 32 * ROW, wb * NB + y);
+#pragma unroll
+      for (int x = 0; x < NB; ++x)
+#pragma unroll
+        for (int y = 0; y < NB; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[x], fb[y], acc[x][y], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  float* out = part + ((int64_t)w * tiles + t) * T * T;
+#pragma unroll
+  for (int x = 0; x < NB; ++x)
+#pragma unroll
+    for (int y = 0; y < NB; ++y)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int a = (wa * NB + x) * 16 + 4 * g + rr;
+        const int b = (wb * NB + y) * 16 + l16;
+        out[a * T + b] = acc[x][y][rr];
+      }
+}
+
+// dW[j][c][o]: sum of the partial tiles of slot j's chunks, fp64 in chunk
+// order.  Workgroup (slot j, tile, entry chunk); a slot without chunks gets 0.
+template <int T>
+__global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __restrict__ part,
+                                                                const int32_t* __restrict__ cs,
+                                                                int32_t K, int32_t Cin,
+                                                                int32_t Cout, int single,
+                                                                int32_t n_chunks,
+                                                                float* __restrict__ dW) {
+  const int tA = (Cin + T - 1) / T, tB = (Cout + T - 1) / T;
+  const int tiles = tA * tB;
+  const int j = blockIdx.x / tiles, t = blockIdx.x - j * tiles;
+  const int ta = t / tB, tb = t - ta * tB;
+  const int c0 = single ? 0 : cs[j];
+  const int c1 = single ? n_chunks : cs[j + 1];
+  for (int e = blockIdx.y * kThreads + threadIdx.x; e < T * T; e += gridDim.y * kThreads) {
+    const int a = e / T, b = e - a * T;
+    const int c = ta * T + a, o = tb * T + b;
+    if (c >= Cin || o >= Cout) continue;
+    double s = 0.0;
+#pragma unroll 4
+    for (int q = c0; q < c1; ++q) s += (double)part[((int64_t)q * tiles + t) * T * T + e];
+    dW[((int64_t)j * Cin + c) * Cout + o] = (float)s;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// dgrad: dS through the transposed table
+// ---------------------------------------------------------------------------
+
+// Grid: (row groups of R rows) x (column slices of WS input channels).
+// Workgroup: the fragments of W[j]^T for every slot j, k-step and 16-column
+// block of its slice go to LDS once (frag f = (j * KS + ks) * NCB + cb, one
+// 1 KB run of 64 lanes x 16 bytes).  Each wavefront takes 16-row blocks
+// b = wave, wave + 4, ...; the block's virtual slots (or of the rows' 64-bit
+// masks) are visited in ascending order, each a job: the rows' sources
+// through table_t, their dZ rows as A fragments (raw buffer loads, an absent
+// row reading zeros), and NCB x KS MFMAs against W[slot_of[s]]^T.  The next
+// job's loads are issued before the current job is multiplied.  Without a
+// transposed table (linear layer) every row is its own source, one slot.
+template <int WS>
+__global__ __launch_bounds__(kThreads) void dgrad_kernel(
+    const __bf16* __restrict__ dZ, const __bf16* __restrict__ W,
+    const int32_t* __restrict__ table_t, const uint64_t* __restrict__ row_slots,
+    const int32_t* __restrict__ slot_of, int64_t n, int32_t K, int32_t Cin, int32_t Cout,
+    int32_t R, __bf16* __restrict__ dS) {
+  constexpr int NCB = WS / 16;
+  constexpr int KSM = 8;  // k-steps of 32 reduction entries held per job (Cout <= 256)
+  constexpr int WROW = WS * 2 + 16;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int KS = (Cout + 31) / 32;
+  unsigned char* wl = smem;                                   // [K][KS][NCB][64][16]
+  unsigned char* scratch = smem + (size_t)K * KS * NCB * 1024;  // [waves][16][WROW]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, l16 = lane & 15;
+  const int64_t row0 = (int64_t)blockIdx.x * R;
+  const int nrows = (int)min((int64_t)R, n - row0);
+  const int n0 = blockIdx.y * WS;
+
+  // weights: lane (g, l16) of fragment (j, ks, cb) holds W[j][n0 + 16 cb + l16][32 ks + 8 g .. + 7]
+  const int nfrag = K * KS * NCB * 64;
+  for (int f = tid; f < nfrag; f += kThreads) {
+    const int ln = f & 63;
+    const int fr = f >> 6;
+    const int cb = fr % NCB;
+    const int ks = (fr / NCB) % KS;
+    const int j = fr / (NCB * KS);
+    const int c = n0 + cb * 16 + (ln & 15);
+    const int o = ks * 32 + 8 * (ln >> 4);
+    i32x4 v = i32x4{0, 0, 0, 0};
+    if (c < Cin && o < Cout)
+      v = *reinterpret_cast<const i32x4*>(W + ((int64_t)j * Cin + c) * Cout + o);
+    *reinterpret_cast<i32x4*>(wl + (size_t)f * 16) = v;
+  }
+  __syncthreads();
+
+  const __amdgpu_buffer_rsrc_t z_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<__bf16*>(dZ), (short)0, (int)(n * Cout * 2), kBufferWord3);
+  const uint32_t row_bytes = (uint32_t)Cout * 2u;
+  unsigned char* my = scratch + wave * 16 * WROW;
+
+  for (int blk = wave; blk * 16 < nrows; blk += kThreads / 64) {
+    const int64_t r = row0 + blk * 16 + l16;
+    const bool rin = blk * 16 + l16 < nrows;
+    uint64_t m = 1;
+    if (table_t != nullptr) {
+      m = rin ? row_slots[r] : 0ull;
+#pragma unroll
+      for (int d = 1; d < 16; d <<= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)m, d, 64);
+        const uint32_t hi = __shfl_xor((uint32_t)(m >> 32), d, 64);
+        m |= ((uint64_t)hi << 32) | lo;
+      }
+      // every lane group g holds the same union; make it wave-uniform
+      m = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(m >> 32)) << 32) |
+          (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)m);
+    }
+    f32x4 acc[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto issue = [&](int s, i32x4* a) {
+      int32_t src = -1;
+      if (s >= 0 && rin) src = table_t != nullptr ? table_t[(int64_t)s * n + r] : (int32_t)r;
+      const uint32_t off =
+          src >= 0 ? (uint32_t)src * row_bytes + (uint32_t)g * 16u : kOutOfRange;
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks)
+        a[ks] = __builtin_bit_cast(
+            i32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                       z_rsrc, (ks < KS && ks * 32 + 8 * g < Cout) ? off + (uint32_t)ks * 64u
+                                                                   : kOutOfRange,
+                       0, 0));
+    };
+    auto compute = [&](int s, const i32x4* a) {
+      const int j = table_t != nullptr ? slot_of[s] : 0;
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks) {
+        if (ks >= KS) break;
+        const bf16x8 af = __builtin_bit_cast(bf16x8, a[ks]);
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) {
+          const bf16x8 bfr = *reinterpret_cast<const bf16x8*>(
+              wl + ((size_t)((j * KS + ks) * NCB + cb) * 64 + lane) * 16);
+          acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr, acc[cb], 0, 0, 0);
+        }
+      }
+    };
+    // the block's virtual slots in ascending order, one job each
+    uint64_t rest = m;
+    int s_cur = rest ? __builtin_ctzll(rest) : -1;
+    if (rest) rest &= rest - 1;
+    i32x4 a_cur[KSM], a_nxt[KSM];
+    issue(s_cur, a_cur);
+    while (s_cur >= 0) {
+      const int s_nxt = rest ? __builtin_ctzll(rest) : -1;
+      if (rest) rest &= rest - 1;
+      if (s_nxt >= 0) issue(s_nxt, a_nxt);
+      compute(s_cur, a_cur);
+#pragma unroll
+      for (int ks = 0; ks < KSM; ++ks) a_cur[ks] = a_nxt[ks];
+      s_cur = s_nxt;
+    }
+    // rounding, then 16-byte row stores through the wave's scratch
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<uint16_t*>(my + (4 * g + q) * WROW + (cb * 16 + l16) * 2) =
+            (uint16_t)f32_to_bf16_bits(acc[cb][q]);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    constexpr int VPRW = WS * 2 / 16;
+#pragma unroll
+    for (int idx0 = 0; idx0 < 16 * VPRW; idx0 += 64) {
+      const int idx = idx0 + lane;
+      const int rr = idx / VPRW, q = idx % VPRW;
+      const int64_t row = row0 + blk * 16 + rr;
+      const int c = n0 + q * 8;
+      if (idx < 16 * VPRW && blk * 16 + rr < nrows && c < Cin)
+        *reinterpret_cast<i32x4*>(dS + row * Cin + c) =
+            *reinterpret_cast<const i32x4*>(my + rr * WROW + q * 16);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+}
+
+}  // namespace
+// ---------------------------------------------------------------------------
+// host side
+// ---------------------------------------------------------------------------
+
+namespace {
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n + kThreads - 1) / kThreads); }
+
+// column slice of the dgrad kernel: the widest of 128 / 64 / 32 / 16 input
+// channels (not above Cin) whose weight fragments and scratch fit in LDS
+int dgrad_ws(int32_t Kw, int32_t Cin, int32_t Cout) {
+  const int KS = (Cout + 31) / 32;
+  for (int ws = 128; ws >= 16; ws /= 2) {
+    if (ws > Cin && ws > 16) continue;
+    const size_t lds = (size_t)Kw * KS * (ws / 16) * 1024 + 4 * 16 * (ws * 2 + 16);
+    if (lds <= (size_t)kDgradLds) return ws;
+  }
+  return 0;
+}
+
+size_t dgrad_lds(int ws, int32_t Kw, int32_t Cout) {
+  const int KS = (Cout + 31) / 32;
+  return (size_t)Kw * KS * (ws / 16) * 1024 + 4 * 16 * (ws * 2 + 16);
+}
+
+template <int WS>
+hipError_t launch_dgrad_ws(const void* dZ, const void* W, const int32_t* table_t,
+                           const uint64_t* row_slots, const int32_t* slot_of, int64_t n,
+                           int32_t Kw, int32_t Cin, int32_t Cout, void* dS, hipStream_t stream) {
+  auto kern = dgrad_kernel<WS>;
+  const hipError_t a = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kDgradLds);
+  if (a != hipSuccess) return a;
+  const int slices = (Cin + WS - 1) / WS;
+  // about 384 workgroups in all, whole 16-row blocks, at least 64 rows each
+  int64_t R = (n * slices + 383) / 384;
+  R = std::max<int64_t>(64, (R + 15) / 16 * 16);
+  const unsigned gx = (unsigned)((n + R - 1) / R);
+  hipLaunchKernelGGL(kern, dim3(gx, (unsigned)slices), dim3(kThreads), dgrad_lds(WS, Kw, Cout),
+                     stream, static_cast<const __bf16*>(dZ), static_cast<const __bf16*>(W),
+                     table_t, row_slots, slot_of, n, Kw, Cin, Cout, (int32_t)R,
+                     static_cast<__bf16*>(dS));
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int backward_dgrad_supported(int32_t Kw, int32_t Cin, int32_t Cout) {
+  return Cout <= 256 && Kw <= kMaxSlotsBwd && dgrad_ws(Kw, Cin, Cout) > 0;
+}
+
+void backward_plan(int64_t n, int32_t K, int32_t Cin, int32_t Cout, int is_bf16, int conv,
+                   BwdPlan* p) {
+  const int e = is_bf16 ? 2 : 4;
+  p->T = (Cin % 128 == 0 && Cout % 128 == 0) ? 128 : 64;
+  p->tiles = ((Cin + p->T - 1) / p->T) * ((Cout + p->T - 1) / p->T);
+  const int64_t per = conv ? (int64_t)K * ((n + 255) / 256) : (n + 255) / 256;
+  p->L = per > 8192 ? 512 : 256;
+  p->max_chunks = conv ? (int64_t)K * ((n + p->L - 1) / p->L) : (n + p->L - 1) / p->L;
+  p->splits = (int)std::min<int64_t>(2048, std::max<int64_t>(1, (n + 63) / 64));
+  p->rps = std::max<int64_t>(1, (n + p->splits - 1) / p->splits);
+  size_t o = 0;
+  p->off_dz = o;
+  o += align256((size_t)n * Cout * e);
+  p->off_colpart = o;
+  o += align256((size_t)p->splits * Cout * sizeof(float));
+  const int64_t kn = conv ? (int64_t)K * n : 0;
+  p->off_mask = o;
+  o += align256((size_t)kn);
+  p->off_pairs = o;
+  o += align256((size_t)kn * 8);
+  p->off_inv = o;
+  o += align256((size_t)kn * 4);
+  p->off_rowptr = o;
+  o += align256((size_t)(K + 1) * 4);
+  p->off_nact = o;
+  o += align256(16);
+  p->off_bc = o;
+  int32_t nb = 0;
+  int64_t per_block = 0;
+  if (kn > 0) compact_plan(kn, &nb, &per_block);
+  o += align256((size_t)nb * 4);
+  p->off_cs = o;
+  o += align256((size_t)(K + 1) * 4);
+  p->off_part = o;
+  o += align256((size_t)p->max_chunks * p->tiles * p->T * p->T * sizeof(float));
+  p->total = o;
+}
+
+size_t transpose_neighbors_ws_bytes(int32_t V, int32_t K) {
+  return align256((size_t)V * K * 4) * 2 + align256((size_t)(K + 1) * 4);
+}
+
+hipError_t launch_transpose_neighbors(const int32_t* nbr, int32_t V, int32_t K, int32_t* nbr_t,
+                                      int32_t* slot_of, int32_t* off_dev, void* ws,
+                                      hipStream_t stream) {
+  unsigned char* w = static_cast<unsigned char*>(ws);
+  int32_t* cnt = reinterpret_cast<int32_t*>(w);
+  int32_t* cur = reinterpret_cast<int32_t*>(w + align256((size_t)V * K * 4));
+  const int64_t vk = (int64_t)V * K;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(std::min<unsigned>(grid_for(vk), 4096)), dim3(kThreads),
+                     0, stream, cnt, vk, 0);
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(std::min<unsigned>(grid_for(vk), 4096)), dim3(kThreads),
+                     0, stream, cur, vk, 0);
+  const int64_t cap = (int64_t)V * kMaxVirtualSlots;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(std::min<unsigned>(grid_for(cap), 4096)),
+                     dim3(kThreads), 0, stream, nbr_t, cap, -1);
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(kThreads), 0, stream, slot_of,
+                     (int64_t)kMaxVirtualSlots, -1);
+  hipLaunchKernelGGL(tv_count_kernel, dim3(grid_for(vk)), dim3(kThreads), 0, stream, nbr, V, K, cnt);
+  hipLaunchKernelGGL(tv_layout_kernel, dim3(1), dim3(kThreads), 0, stream, cnt, V, K, off_dev,
+                     slot_of, (int32_t)kMaxVirtualSlots);
+  hipLaunchKernelGGL(tv_fill_kernel, dim3(grid_for(vk)), dim3(kThreads), 0, stream, nbr, V, K,
+                     off_dev, cur, nbr_t, (int32_t)kMaxVirtualSlots);
+  hipLaunchKernelGGL(tv_sort_kernel, dim3(grid_for(vk)), dim3(kThreads), 0, stream, cnt, V, K,
+                     off_dev, nbr_t, (int32_t)kMaxVirtualSlots);
+  return hipGetLastError();
+}
+
+hipError_t launch_transposed_table(const int32_t* coords, const int32_t* inv, int64_t n, int32_t B,
+                                   int32_t V, const int32_t* nbr_t, int32_t Kt, int32_t* table_t,
+                                   uint64_t* row_slots, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(tt_kernel, dim3(grid_for(n)), dim3(kThreads), 0, stream,
+                     reinterpret_cast<const int2*>(coords), inv, n, B, V, nbr_t, Kt, table_t,
+                     row_slots);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
+                                 const int32_t* table_t, const uint64_t* row_slots,
+                                 const int32_t* slot_of, const void* W, const void* Y,
+                                 const void* dY, int64_t n, int32_t K, int32_t Cin, int32_t Cout,
+                                 int act, void* dS, float* dW, float* db, void* ws,
+                                 hipStream_t stream) {
+  BwdPlan pl;
+  backward_plan(n, K, Cin, Cout, 1, conv, &pl);
+  unsigned char* w = static_cast<unsigned char*>(ws);
+  const int Kw = conv ? K : 1;
+  if (n == 0) {  // no rows: zero weight and bias gradients
+    if (dW != nullptr)
+      hipLaunchKernelGGL(fill_i32_kernel, dim3(64), dim3(kThreads), 0, stream,
+                         reinterpret_cast<int32_t*>(dW), (int64_t)Kw * Cin * Cout, 0);
+    if (db != nullptr)
+      hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(kThreads), 0, stream,
+                         reinterpret_cast<int32_t*>(db), (int64_t)Cout, 0);
+    return hipGetLastError();
+  }
+  // dZ (through the ReLU) and the bias gradient
+  const void* dZ = dY;
+  if (act || db != nullptr) {
+    float* colpart = reinterpret_cast<float*>(w + pl.off_colpart);
+    void* dz_out = act ? static_cast<void*>(w + pl.off_dz) : nullptr;
+    hipLaunchKernelGGL(relu_bwd_kernel<true>, dim3(pl.splits), dim3(kThreads), 0, stream,
+                       static_cast<const i32x4*>(dY), static_cast<const i32x4*>(Y), n, Cout, act,
+                       pl.rps, static_cast<i32x4*>(dz_out), colpart);
+    if (act) dZ = dz_out;
+    if (db != nullptr)
+      hipLaunchKernelGGL(colsum_kernel, dim3((Cout + kThreads - 1) / kThreads), dim3(kThreads), 0,
+                         stream, colpart, pl.splits, Cout, db);
+  }
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  // weight gradient
+  if (dW != nullptr) {
+    float* part = reinterpret_cast<float*>(w + pl.off_part);
+    const int2* pairs = nullptr;
+    const int32_t* rp = nullptr;
+    const int32_t* cs = nullptr;
+    int64_t grid_chunks = pl.max_chunks;
+    if (conv) {
+      uint8_t* mask = w + pl.off_mask;
+      int32_t* pr = reinterpret_cast<int32_t*>(w + pl.off_pairs);
+      int32_t* inv_p = reinterpret_cast<int32_t*>(w + pl.off_inv);
+      int32_t* rowp = reinterpret_cast<int32_t*>(w + pl.off_rowptr);
+      int32_t* nact = reinterpret_cast<int32_t*>(w + pl.off_nact);
+      int32_t* bc = reinterpret_cast<int32_t*>(w + pl.off_bc);
+      int32_t* csw = reinterpret_cast<int32_t*>(w + pl.off_cs);
+      const int64_t kn = (int64_t)K * n;
+      hipLaunchKernelGGL(presence_kernel, dim3(std::min<unsigned>(grid_for(kn), 8192)),
+                         dim3(kThreads), 0, stream, table, kn, mask);
+      err = launch_compact(mask, K, (int32_t)n, pr, inv_p, rowp, nact, nullptr, kn, bc, stream);
+      if (err != hipSuccess) return err;
+      hipLaunchKernelGGL(chunk_schedule_kernel, dim3(1), dim3(64), 0, stream, rowp, K, pl.L, csw);
+      pairs = reinterpret_cast<const int2*>(pr);
+      rp = rowp;
+      cs = csw;
+    }
+    const unsigned gt = (unsigned)(grid_chunks * pl.tiles);
+    if (pl.T == 128)
+      hipLaunchKernelGGL((wgrad_tile_kernel<128, kWgradRows>), dim3(gt), dim3(kThreads), 0, stream,
+                         static_cast<const __bf16*>(S), static_cast<const __bf16*>(dZ), table,
+                         pairs, rp, cs, Kw, n, pl.L, Cin, Cout, part);
+    else
+      hipLaunchKernelGGL((wgrad_tile_kernel<64, kWgradRows>), dim3(gt), dim3(kThreads), 0, stream,
+                         static_cast<const __bf16*>(S), static_cast<const __bf16*>(dZ), table,
+                         pairs, rp, cs, Kw, n, pl.L, Cin, Cout, part);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    const dim3 rg((unsigned)(Kw * pl.tiles), (unsigned)std::max(1, pl.T * pl.T / (kThreads * 4)));
+    if (pl.T == 128)
+      hipLaunchKernelGGL(wgrad_reduce_kernel<128>, rg, dim3(kThreads), 0, stream, part, cs, Kw,
+                         Cin, Cout, conv ? 0 : 1, (int32_t)grid_chunks, dW);
+    else
+      hipLaunchKernelGGL(wgrad_reduce_kernel<64>, rg, dim3(kThreads), 0, stream, part, cs, Kw,
+                         Cin, Cout, conv ? 0 : 1, (int32_t)grid_chunks, dW);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  // input gradient
+  if (dS != nullptr) {
+    const int wsl = dgrad_ws(Kw, Cin, Cout);
+    const int32_t* tt = conv ? table_t : nullptr;
+    const uint64_t* rs = conv ? row_slots : nullptr;
+    const int32_t* so = conv ? slot_of : nullptr;
+    switch (wsl) {
+      case 128: err = launch_dgrad_ws<128>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+      case 64: err = launch_dgrad_ws<64>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+      case 32: err = launch_dgrad_ws<32>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+      default: err = launch_dgrad_ws<16>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+    }
+    if (err != hipSuccess) return err;
+  }
+  return hipSuccess;
+}
+
+}  // namespace shc

@@ -62,6 +62,30 @@ size_t mask_scores_workspace_bytes(int32_t K, int64_t N, int32_t C);
 hipError_t launch_mask_scores(const void* O, int32_t K, int64_t N, int32_t C,
                               const double* alpha_in, double* alpha_out, double* sim,
                               int32_t kappa, int32_t* top, void* ws, hipStream_t stream);
+// backward of the linear and conv layers (backward.hip)
+constexpr int kMaxVirtualSlots = 64;
+struct BwdPlan {
+  int T, tiles, L, splits;
+  int64_t max_chunks, rps;
+  size_t off_dz, off_colpart, off_mask, off_pairs, off_inv, off_rowptr, off_nact, off_bc, off_cs,
+      off_part, total;
+};
+void backward_plan(int64_t n, int32_t K, int32_t Cin, int32_t Cout, int is_bf16, int conv,
+                   BwdPlan* p);
+int backward_dgrad_supported(int32_t Kw, int32_t Cin, int32_t Cout);
+size_t transpose_neighbors_ws_bytes(int32_t V, int32_t K);
+hipError_t launch_transpose_neighbors(const int32_t* nbr, int32_t V, int32_t K, int32_t* nbr_t,
+                                      int32_t* slot_of, int32_t* off_dev, void* ws,
+                                      hipStream_t stream);
+hipError_t launch_transposed_table(const int32_t* coords, const int32_t* inv, int64_t n, int32_t B,
+                                   int32_t V, const int32_t* nbr_t, int32_t Kt, int32_t* table_t,
+                                   uint64_t* row_slots, hipStream_t stream);
+hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
+                                 const int32_t* table_t, const uint64_t* row_slots,
+                                 const int32_t* slot_of, const void* W, const void* Y,
+                                 const void* dY, int64_t n, int32_t K, int32_t Cin, int32_t Cout,
+                                 int act, void* dS, float* dW, float* db, void* ws,
+                                 hipStream_t stream);
 hipError_t launch_clear_inactive(const int32_t* inv, int32_t B, int32_t V, int32_t row_bytes,
                                  void* D, hipStream_t stream);
 hipError_t launch_gather_ext(const void* x, const uint8_t* me, int mask_mode,

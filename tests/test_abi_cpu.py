@@ -171,6 +171,65 @@ def test_mask_scores_validation(lib):
     assert call(nbytes=need - 1) == -2 and "workspace" in err(lib)
 
 
+def test_backward_validation(lib):
+    """The transposed lists, the transposed table and both layer backward
+    calls reject bad arguments before any launch."""
+    assert lib.shc_transpose_neighbors_workspace(100, 9) > 0
+    assert lib.shc_transpose_neighbors_workspace(100, 33) == 0
+    kt = ctypes.c_int32(0)
+    tn = lib.shc_transpose_neighbors
+    need_t = lib.shc_transpose_neighbors_workspace(100, 9)
+    assert tn(A, 0, 9, A, A, ctypes.addressof(kt), A, need_t, None) == -1
+    assert tn(A, 100, 33, A, A, ctypes.addressof(kt), A, need_t, None) == -4
+    assert tn(A, 100, 9, A, A, None, A, need_t, None) == -1
+    assert tn(MIS, 100, 9, A, A, ctypes.addressof(kt), A, need_t, None) == -3
+    assert tn(A, 100, 9, A, A, ctypes.addressof(kt), A, need_t - 1, None) == -2
+    tt = lib.shc_build_transposed_table
+    assert tt(A, A, 10, 4, 100, A, 0, A, A, None) == -1
+    assert tt(A, A, 10, 4, 100, A, 65, A, A, None) == -1
+    assert tt(A, A, 10, 4, 100, A, 20, A, MIS, None) == -3
+    assert tt(A, A, 10, 0, 100, A, 20, A, A, None) == -1
+
+    assert lib.shc_sparse_linear_backward_workspace(1000, 128, 128, 1) > 0
+    assert lib.shc_sparse_linear_backward_workspace(1000, 128, 128, 0) == 0
+    need = lib.shc_sparse_linear_backward_workspace(1000, 128, 128, 1)
+
+    def lin(S=A, W=A, Y=A, dY=A, n=1000, Cin=128, Cout=128, dt=1, act=1, dS=A, dW=A, db=A,
+            ws=A, nbytes=need):
+        return lib.shc_sparse_linear_backward(S, W, Y, dY, n, Cin, Cout, dt, act, dS, dW, db, ws,
+                                              nbytes, None)
+
+    assert lin(dt=0) == -4 and "bf16" in err(lib)
+    assert lin(Cin=24) == -4
+    assert lin(Cout=512) == -4
+    assert lin(act=7) == -4
+    assert lin(n=-1) == -1
+    assert lin(Y=None) == -1                       # the ReLU needs the stored output
+    assert lin(dY=None) == -1
+    assert lin(S=None) == -1                       # dW needs S
+    assert lin(W=None) == -1
+    assert lin(dS=MIS) == -3
+    assert lin(nbytes=need - 1) == -2 and "workspace" in err(lib)
+
+    needc = lib.shc_sparse_neighbor_conv_backward_workspace(1000, 9, 128, 128, 1)
+    assert needc > need
+    assert lib.shc_sparse_neighbor_conv_backward_workspace(1000, 33, 128, 128, 1) == 0
+
+    def conv(S=A, table=A, table_t=A, rs=A, so=A, Kt=56, W=A, Y=A, dY=A, n=1000, K=9, Cin=128,
+             Cout=128, dt=1, act=1, dS=A, dW=A, db=A, ws=A, nbytes=needc):
+        return lib.shc_sparse_neighbor_conv_backward(S, table, table_t, rs, so, Kt, W, Y, dY, n,
+                                                     K, Cin, Cout, dt, act, dS, dW, db, ws,
+                                                     nbytes, None)
+
+    assert conv(K=0) == -1 and conv(K=33) == -4
+    assert conv(dt=0) == -4
+    assert conv(table=None) == -1                  # dW needs the neighbour-row table
+    assert conv(table_t=None) == -1                # dS needs the transposed table
+    assert conv(Kt=0) == -1 and conv(Kt=65) == -1
+    assert conv(rs=MIS) == -3
+    assert conv(nbytes=needc - 1) == -2
+
+
 def test_gather_scatter_pool_validation(lib):
     g = lib.shc_gather_rows
     assert g(A, A, 10, 4, 655, 24, 0, A, None) == -4
