@@ -45,7 +45,8 @@ constexpr int kBufferWord3 = 0x00020000;
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr int kMaxSlotsBwd = 32;
 constexpr int kWgradRows = 128;      // rows per step of the wgrad tile kernel
-constexpr int kDgradLds = 160 * 1024;
+// dynamic LDS of the dgrad kernel: 160 KB less room for its static arrays
+constexpr int kDgradLds = 159 * 1024;
 
 // ---------------------------------------------------------------------------
 // dZ and the column sums of db
@@ -113,15 +114,26 @@ __global__ __launch_bounds__(kThreads) void relu_bwd_kernel(const i32x4* __restr
   }
 }
 
-// db[c] = sum over splits of colpart[s][c], fp64 in split order, one rounding.
+// db[c]: workgroup of 8 columns x 32 split groups; group y sums splits y,
+// y + 32, ... in fp64, then the 32 group sums are added in order; one rounding.
 __global__ __launch_bounds__(kThreads) void colsum_kernel(const float* __restrict__ colpart,
                                                           int splits, int32_t C,
                                                           float* __restrict__ db) {
-  const int c = blockIdx.x * kThreads + threadIdx.x;
-  if (c >= C) return;
+  __shared__ double red[32][8];
+  const int cx = threadIdx.x & 7, y = threadIdx.x >> 3;
+  const int c = blockIdx.x * 8 + cx;
   double t = 0.0;
-  for (int s = 0; s < splits; ++s) t += (double)colpart[(int64_t)s * C + c];
-  db[c] = (float)t;
+  if (c < C) {
+#pragma unroll 4
+    for (int s = y; s < splits; s += 32) t += (double)colpart[(int64_t)s * C + c];
+  }
+  red[y][cx] = t;
+  __syncthreads();
+  if (y == 0 && c < C) {
+    double u = 0.0;
+    for (int yy = 0; yy < 32; ++yy) u += red[yy][cx];
+    db[c] = (float)u;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -421,8 +433,10 @@ __global__ __launch_bounds__(kThreads) void wgrad_tile_kernel(
       }
 }
 
-// dW[j][c][o]: sum of the partial tiles of slot j's chunks, fp64 in chunk
-// order.  Workgroup (slot j, tile, entry chunk); a slot without chunks gets 0.
+// dW[j][c][o]: sum of the partial tiles of slot j's chunks in fp64.
+// Workgroup (slot j and tile, 32 consecutive entries) of 8 chunk groups:
+// group y sums chunks y, y + 8, ... of the slot in order, then the 8 group
+// sums are added in order.  A slot without chunks gets 0.
 template <int T>
 __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __restrict__ part,
                                                                 const int32_t* __restrict__ cs,
@@ -430,20 +444,26 @@ __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __r
                                                                 int32_t Cout, int single,
                                                                 int32_t n_chunks,
                                                                 float* __restrict__ dW) {
+  __shared__ double red[8][32];
   const int tA = (Cin + T - 1) / T, tB = (Cout + T - 1) / T;
   const int tiles = tA * tB;
   const int j = blockIdx.x / tiles, t = blockIdx.x - j * tiles;
   const int ta = t / tB, tb = t - ta * tB;
   const int c0 = single ? 0 : cs[j];
   const int c1 = single ? n_chunks : cs[j + 1];
-  for (int e = blockIdx.y * kThreads + threadIdx.x; e < T * T; e += gridDim.y * kThreads) {
+  const int ex = threadIdx.x & 31, y = threadIdx.x >> 5;
+  const int e = blockIdx.y * 32 + ex;
+  double s = 0.0;
+#pragma unroll 4
+  for (int q = c0 + y; q < c1; q += 8) s += (double)part[((int64_t)q * tiles + t) * T * T + e];
+  red[y][ex] = s;
+  __syncthreads();
+  if (y == 0) {
+    double u = 0.0;
+    for (int yy = 0; yy < 8; ++yy) u += red[yy][ex];
     const int a = e / T, b = e - a * T;
     const int c = ta * T + a, o = tb * T + b;
-    if (c >= Cin || o >= Cout) continue;
-    double s = 0.0;
-#pragma unroll 4
-    for (int q = c0; q < c1; ++q) s += (double)part[((int64_t)q * tiles + t) * T * T + e];
-    dW[((int64_t)j * Cin + c) * Cout + o] = (float)s;
+    if (c < Cin && o < Cout) dW[((int64_t)j * Cin + c) * Cout + o] = (float)u;
   }
 }
 
@@ -454,26 +474,33 @@ __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __r
 // Grid: (row groups of R rows) x (column slices of WS input channels).
 // Workgroup: the fragments of W[j]^T for every slot j, k-step and 16-column
 // block of its slice go to LDS once (frag f = (j * KS + ks) * NCB + cb, one
-// 1 KB run of 64 lanes x 16 bytes).  Each wavefront takes 16-row blocks
-// b = wave, wave + 4, ...; the block's virtual slots (or of the rows' 64-bit
-// masks) are visited in ascending order, each a job: the rows' sources
-// through table_t, their dZ rows as A fragments (raw buffer loads, an absent
-// row reading zeros), and NCB x KS MFMAs against W[slot_of[s]]^T.  The next
-// job's loads are issued before the current job is multiplied.  Without a
-// transposed table (linear layer) every row is its own source, one slot.
-template <int WS>
+// 1 KB run of 64 lanes x 16 bytes).  Each wavefront walks its 16-row blocks
+// b = wave, wave + 4, ...; a block's jobs are its virtual slots (the or of
+// its rows' 64-bit masks) in ascending order, or one empty job when it has
+// none.  A job loads the rows' sources through table_t, their dZ rows as A
+// fragments (raw buffer loads, an absent row reading zeros), and runs
+// NCB x KS MFMAs against W[slot_of[s]]^T.  The blocks' slot masks are
+// formed in LDS up front; jobs go through a ring of register sets in two
+// stages (source rows, then data); after a block's last job its 16 rows are rounded
+// and stored through the wavefront's LDS scratch.  Without a transposed
+// table (linear layer) every row is its own source through one slot.
+template <int WS, int KSM, bool TBL>
 __global__ __launch_bounds__(kThreads) void dgrad_kernel(
     const __bf16* __restrict__ dZ, const __bf16* __restrict__ W,
     const int32_t* __restrict__ table_t, const uint64_t* __restrict__ row_slots,
     const int32_t* __restrict__ slot_of, int64_t n, int32_t K, int32_t Cin, int32_t Cout,
     int32_t R, __bf16* __restrict__ dS) {
   constexpr int NCB = WS / 16;
-  constexpr int KSM = 8;  // k-steps of 32 reduction entries held per job (Cout <= 256)
+  constexpr int DA = KSM <= 4 ? 4 : 2;  // jobs with data loads in flight
+  constexpr int D = 2 * DA;              // ring: as many again with only the source loaded
+  constexpr int kWaves = kThreads / 64;
   constexpr int WROW = WS * 2 + 16;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int KS = (Cout + 31) / 32;
-  unsigned char* wl = smem;                                   // [K][KS][NCB][64][16]
+  unsigned char* wl = smem;                                     // [K][KS][NCB][64][16]
   unsigned char* scratch = smem + (size_t)K * KS * NCB * 1024;  // [waves][16][WROW]
+  uint64_t* blkmask = reinterpret_cast<uint64_t*>(scratch + kWaves * 16 * WROW);  // [R / 16]
+  __shared__ int32_t slot_lds[kMaxVirtualSlots];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15;
@@ -496,6 +523,21 @@ __global__ __launch_bounds__(kThreads) void dgrad_kernel(
       v = *reinterpret_cast<const i32x4*>(W + ((int64_t)j * Cin + c) * Cout + o);
     *reinterpret_cast<i32x4*>(wl + (size_t)f * 16) = v;
   }
+  // block masks: the or of the 16 rows' virtual-slot masks, one per block;
+  // the virtual slots' weight slots
+  if (TBL) {
+    if (tid < kMaxVirtualSlots) slot_lds[tid] = slot_of[tid];
+    for (int base = wave * 64; base < nrows; base += kThreads) {
+      uint64_t m = base + lane < nrows ? row_slots[row0 + base + lane] : 0ull;
+#pragma unroll
+      for (int d = 1; d < 16; d <<= 1) {
+        const uint32_t lo = __shfl_xor((uint32_t)m, d, 64);
+        const uint32_t hi = __shfl_xor((uint32_t)(m >> 32), d, 64);
+        m |= ((uint64_t)hi << 32) | lo;
+      }
+      if (l16 == 0 && base + lane < nrows) blkmask[(base + lane) >> 4] = m;
+    }
+  }
   __syncthreads();
 
   const __amdgpu_buffer_rsrc_t z_rsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -503,45 +545,62 @@ __global__ __launch_bounds__(kThreads) void dgrad_kernel(
   const uint32_t row_bytes = (uint32_t)Cout * 2u;
   unsigned char* my = scratch + wave * 16 * WROW;
 
-  for (int blk = wave; blk * 16 < nrows; blk += kThreads / 64) {
-    const int64_t r = row0 + blk * 16 + l16;
-    const bool rin = blk * 16 + l16 < nrows;
-    uint64_t m = 1;
-    if (table_t != nullptr) {
-      m = rin ? row_slots[r] : 0ull;
-#pragma unroll
-      for (int d = 1; d < 16; d <<= 1) {
-        const uint32_t lo = __shfl_xor((uint32_t)m, d, 64);
-        const uint32_t hi = __shfl_xor((uint32_t)(m >> 32), d, 64);
-        m |= ((uint64_t)hi << 32) | lo;
-      }
-      // every lane group g holds the same union; make it wave-uniform
-      m = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(m >> 32)) << 32) |
-          (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)m);
+  struct Job {
+    int blk;    // block, or -1 past the end
+    int s;      // virtual slot, or -1 for a block without any
+    bool last;  // last job of its block
+  };
+  // the wavefront's job sequence, generated block by block from the block
+  // masks in LDS (wave-uniform state, no memory loads)
+  int cur_blk = wave - kWaves;
+  uint64_t rest = 0;
+  auto next_job = [&]() -> Job {
+    if (rest == 0) {
+      cur_blk += kWaves;
+      if (cur_blk * 16 >= nrows) return Job{-1, -1, true};
+      const uint64_t m = TBL ? blkmask[cur_blk] : 1ull;
+      if (m == 0) return Job{cur_blk, -1, true};
+      rest = m;
     }
-    f32x4 acc[NCB];
+    const int sl = __builtin_ctzll(rest);
+    rest &= rest - 1;
+    return Job{cur_blk, sl, rest == 0};
+  };
+  struct Frags {
+    i32x4 v[KSM];
+  };
+  // a job's source row (one lane per row), loaded ahead of its data; the
+  // load is issued on every path (a clamped address when there is none) and
+  // its value is only looked at when the data loads go out
+  auto live_of = [&](const Job& jb) -> bool {
+    return jb.blk >= 0 && jb.s >= 0 && jb.blk * 16 + l16 < nrows;
+  };
+  auto load_src = [&](const Job& jb, bool live) -> int32_t {
+    const int64_t r = row0 + (live ? jb.blk * 16 + l16 : 0);
+    if (!TBL) return (int32_t)r;
+    return table_t[(live ? (int64_t)jb.s * n : 0) + r];
+  };
+  auto issue = [&](int32_t raw, bool live, Frags& f) {
+    const int32_t src = live ? raw : -1;
+    const uint32_t off = src >= 0 ? (uint32_t)src * row_bytes + (uint32_t)g * 16u : kOutOfRange;
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    auto issue = [&](int s, i32x4* a) {
-      int32_t src = -1;
-      if (s >= 0 && rin) src = table_t != nullptr ? table_t[(int64_t)s * n + r] : (int32_t)r;
-      const uint32_t off =
-          src >= 0 ? (uint32_t)src * row_bytes + (uint32_t)g * 16u : kOutOfRange;
+    for (int ks = 0; ks < KSM; ++ks)
+      f.v[ks] = __builtin_bit_cast(
+          i32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     z_rsrc, (ks < KS && ks * 32 + 8 * g < Cout) ? off + (uint32_t)ks * 64u
+                                                                 : kOutOfRange,
+                     0, 0));
+  };
+  f32x4 acc[NCB];
 #pragma unroll
-      for (int ks = 0; ks < KSM; ++ks)
-        a[ks] = __builtin_bit_cast(
-            i32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                       z_rsrc, (ks < KS && ks * 32 + 8 * g < Cout) ? off + (uint32_t)ks * 64u
-                                                                   : kOutOfRange,
-                       0, 0));
-    };
-    auto compute = [&](int s, const i32x4* a) {
-      const int j = table_t != nullptr ? slot_of[s] : 0;
+  for (int cb = 0; cb < NCB; ++cb) acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](const Job& jb, const Frags& f) {
+    if (jb.blk < 0 || jb.s < 0) return;
+    const int j = TBL ? slot_lds[jb.s] : 0;
 #pragma unroll
-      for (int ks = 0; ks < KSM; ++ks) {
-        if (ks >= KS) break;
-        const bf16x8 af = __builtin_bit_cast(bf16x8, a[ks]);
+    for (int ks = 0; ks < KSM; ++ks) {
+      if (ks < KS) {
+        const bf16x8 af = __builtin_bit_cast(bf16x8, f.v[ks]);
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
           const bf16x8 bfr = *reinterpret_cast<const bf16x8*>(
@@ -549,29 +608,17 @@ __global__ __launch_bounds__(kThreads) void dgrad_kernel(
           acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr, acc[cb], 0, 0, 0);
         }
       }
-    };
-    // the block's virtual slots in ascending order, one job each
-    uint64_t rest = m;
-    int s_cur = rest ? __builtin_ctzll(rest) : -1;
-    if (rest) rest &= rest - 1;
-    i32x4 a_cur[KSM], a_nxt[KSM];
-    issue(s_cur, a_cur);
-    while (s_cur >= 0) {
-      const int s_nxt = rest ? __builtin_ctzll(rest) : -1;
-      if (rest) rest &= rest - 1;
-      if (s_nxt >= 0) issue(s_nxt, a_nxt);
-      compute(s_cur, a_cur);
-#pragma unroll
-      for (int ks = 0; ks < KSM; ++ks) a_cur[ks] = a_nxt[ks];
-      s_cur = s_nxt;
     }
-    // rounding, then 16-byte row stores through the wave's scratch
+  };
+  auto epilogue = [&](int blk) {
 #pragma unroll
-    for (int cb = 0; cb < NCB; ++cb)
+    for (int cb = 0; cb < NCB; ++cb) {
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         *reinterpret_cast<uint16_t*>(my + (4 * g + q) * WROW + (cb * 16 + l16) * 2) =
             (uint16_t)f32_to_bf16_bits(acc[cb][q]);
+      acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -589,10 +636,38 @@ __global__ __launch_bounds__(kThreads) void dgrad_kernel(
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+
+  // Ring of D = DA + DS jobs in sequence order: slot u holds job t D + u.
+  // Processing job k issues the data loads of job k + DA (its source row was
+  // loaded DS jobs earlier) and takes job k + D, whose source load it issues.
+  Job jobs[D];
+  int32_t srcv[D];
+  bool live[D];
+  Frags fr[D];
+#pragma unroll
+  for (int u = 0; u < D; ++u) {
+    jobs[u] = next_job();
+    live[u] = live_of(jobs[u]);
+    srcv[u] = load_src(jobs[u], live[u]);
+  }
+#pragma unroll
+  for (int u = 0; u < DA; ++u) issue(srcv[u], live[u], fr[u]);
+  while (jobs[0].blk >= 0) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      compute(jobs[u], fr[u]);
+      if (jobs[u].blk >= 0 && jobs[u].last) epilogue(jobs[u].blk);
+      issue(srcv[(u + DA) % D], live[(u + DA) % D], fr[(u + DA) % D]);
+      jobs[u] = next_job();
+      live[u] = live_of(jobs[u]);
+      srcv[u] = load_src(jobs[u], live[u]);
+    }
   }
 }
 
 }  // namespace
+
 // ---------------------------------------------------------------------------
 // host side
 // ---------------------------------------------------------------------------
@@ -604,40 +679,60 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n + kThreads - 1) / kThreads); }
 
 // column slice of the dgrad kernel: the widest of 128 / 64 / 32 / 16 input
-// channels (not above Cin) whose weight fragments and scratch fit in LDS
-int dgrad_ws(int32_t Kw, int32_t Cin, int32_t Cout) {
-  const int KS = (Cout + 31) / 32;
-  for (int ws = 128; ws >= 16; ws /= 2) {
-    if (ws > Cin && ws > 16) continue;
-    const size_t lds = (size_t)Kw * KS * (ws / 16) * 1024 + 4 * 16 * (ws * 2 + 16);
-    if (lds <= (size_t)kDgradLds) return ws;
-  }
-  return 0;
-}
+// channels (not above Cin) whose weight fragments and scratch leave room for
+// two workgroups per CU, else the widest that fits one
+constexpr int kDgradMaxRows = 4096;  // rows per workgroup (block masks in LDS)
 
 size_t dgrad_lds(int ws, int32_t Kw, int32_t Cout) {
   const int KS = (Cout + 31) / 32;
-  return (size_t)Kw * KS * (ws / 16) * 1024 + 4 * 16 * (ws * 2 + 16);
+  return (size_t)Kw * KS * (ws / 16) * 1024 + (kThreads / 64) * 16 * (ws * 2 + 16) +
+         kDgradMaxRows / 16 * sizeof(uint64_t);
 }
 
-template <int WS>
+int dgrad_ws(int32_t Kw, int32_t Cin, int32_t Cout) {
+  for (size_t budget : {(size_t)kDgradLds / 2, (size_t)kDgradLds})
+    for (int ws = 128; ws >= 16; ws /= 2) {
+      if (ws > Cin && ws > 16) continue;
+      if (dgrad_lds(ws, Kw, Cout) <= budget) return ws;
+    }
+  return 0;
+}
+
+template <int WS, int KSM, bool TBL>
 hipError_t launch_dgrad_ws(const void* dZ, const void* W, const int32_t* table_t,
                            const uint64_t* row_slots, const int32_t* slot_of, int64_t n,
                            int32_t Kw, int32_t Cin, int32_t Cout, void* dS, hipStream_t stream) {
-  auto kern = dgrad_kernel<WS>;
+  auto kern = dgrad_kernel<WS, KSM, TBL>;
+  const size_t lds = dgrad_lds(WS, Kw, Cout);
   const hipError_t a = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, kDgradLds);
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (a != hipSuccess) return a;
   const int slices = (Cin + WS - 1) / WS;
-  // about 384 workgroups in all, whole 16-row blocks, at least 64 rows each
-  int64_t R = (n * slices + 383) / 384;
-  R = std::max<int64_t>(64, (R + 15) / 16 * 16);
+  // about 512 workgroups in all, whole 16-row blocks, at least 64 rows each
+  int64_t R = (n * slices + 511) / 512;
+  R = std::min<int64_t>(kDgradMaxRows, std::max<int64_t>(64, (R + 15) / 16 * 16));
   const unsigned gx = (unsigned)((n + R - 1) / R);
-  hipLaunchKernelGGL(kern, dim3(gx, (unsigned)slices), dim3(kThreads), dgrad_lds(WS, Kw, Cout),
+  hipLaunchKernelGGL(kern, dim3(gx, (unsigned)slices), dim3(kThreads), lds,
                      stream, static_cast<const __bf16*>(dZ), static_cast<const __bf16*>(W),
                      table_t, row_slots, slot_of, n, Kw, Cin, Cout, (int32_t)R,
                      static_cast<__bf16*>(dS));
   return hipGetLastError();
+}
+
+template <int WS>
+hipError_t launch_dgrad_k(const void* dZ, const void* W, const int32_t* table_t,
+                          const uint64_t* row_slots, const int32_t* slot_of, int64_t n,
+                          int32_t Kw, int32_t Cin, int32_t Cout, void* dS, hipStream_t stream) {
+  const bool tbl = table_t != nullptr;
+  if (Cout <= 128)
+    return tbl ? launch_dgrad_ws<WS, 4, true>(dZ, W, table_t, row_slots, slot_of, n, Kw, Cin,
+                                              Cout, dS, stream)
+               : launch_dgrad_ws<WS, 4, false>(dZ, W, table_t, row_slots, slot_of, n, Kw, Cin,
+                                               Cout, dS, stream);
+  return tbl ? launch_dgrad_ws<WS, 8, true>(dZ, W, table_t, row_slots, slot_of, n, Kw, Cin, Cout,
+                                            dS, stream)
+             : launch_dgrad_ws<WS, 8, false>(dZ, W, table_t, row_slots, slot_of, n, Kw, Cin, Cout,
+                                             dS, stream);
 }
 
 }  // namespace
@@ -753,8 +848,8 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
                        pl.rps, static_cast<i32x4*>(dz_out), colpart);
     if (act) dZ = dz_out;
     if (db != nullptr)
-      hipLaunchKernelGGL(colsum_kernel, dim3((Cout + kThreads - 1) / kThreads), dim3(kThreads), 0,
-                         stream, colpart, pl.splits, Cout, db);
+      hipLaunchKernelGGL(colsum_kernel, dim3((Cout + 7) / 8), dim3(kThreads), 0, stream, colpart,
+                         pl.splits, Cout, db);
   }
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
@@ -794,7 +889,7 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
                          pairs, rp, cs, Kw, n, pl.L, Cin, Cout, part);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
-    const dim3 rg((unsigned)(Kw * pl.tiles), (unsigned)std::max(1, pl.T * pl.T / (kThreads * 4)));
+    const dim3 rg((unsigned)(Kw * pl.tiles), (unsigned)(pl.T * pl.T / 32));
     if (pl.T == 128)
       hipLaunchKernelGGL(wgrad_reduce_kernel<128>, rg, dim3(kThreads), 0, stream, part, cs, Kw,
                          Cin, Cout, conv ? 0 : 1, (int32_t)grid_chunks, dW);
@@ -811,10 +906,10 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
     const uint64_t* rs = conv ? row_slots : nullptr;
     const int32_t* so = conv ? slot_of : nullptr;
     switch (wsl) {
-      case 128: err = launch_dgrad_ws<128>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
-      case 64: err = launch_dgrad_ws<64>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
-      case 32: err = launch_dgrad_ws<32>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
-      default: err = launch_dgrad_ws<16>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+      case 128: err = launch_dgrad_k<128>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+      case 64: err = launch_dgrad_k<64>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+      case 32: err = launch_dgrad_k<32>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+      default: err = launch_dgrad_k<16>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
     }
     if (err != hipSuccess) return err;
   }
