@@ -262,7 +262,8 @@ def main():
 
     out["next_rows"] = {"group_norm": group_norm_measure(st, shc, torch, args.reps),
                         "multi_mask": multi_mask_measure(st, w, shc, synth, torch, args.reps),
-                        "mask_scores": mask_scores_measure(w, shc, torch, args.reps)}
+                        "mask_scores": mask_scores_measure(w, shc, torch, args.reps),
+                        "backward": backward_measure(st, w, shc, torch, args.reps)}
     log("group norm measured")
 
     if not args.no_dense:
@@ -301,6 +302,62 @@ def group_norm_measure(st, shc, torch, reps, G=32):
                       f"{st.B} bodies", "launch_us": round(us, 2), "algorithmic_bytes": nbytes,
             "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(ach / HBM_PEAK_GBS, 4)}
+
+
+def backward_measure(st, w, shc, torch, reps):
+    """Backward of the step's two layers (sparse linear + ReLU, then sparse
+    conv + ReLU) on the density-sweep workload, with a seeded upstream
+    gradient at the conv's output: the conv's input, weight and bias
+    gradients, then the linear layer's from the conv's input gradient.  The
+    transposed neighbour lists are built once per mesh and the transposed
+    table once per active set (shared by every conv layer on it); each is
+    timed on its own.  Prepared calls, back to back between HIP events.
+
+    Roofline figure of the conv backward: algorithmic bytes (dY and the
+    stored output Y read once, S and the input rows read once, the table,
+    the row masks and the live transposed-table entries, dS and dW written
+    once) over its time; flops 4 P C_in C_out for P present (row, slot)
+    pairs (dW and dS each 2 P C_in C_out)."""
+    n = st.n
+    st.gather()                       # the step fuses it into the linear; the backward reads it
+    K = w.K
+    nbr_t, slot_of, Kt = shc.transpose_neighbors(st.nbr)
+    table_t = torch.empty((Kt, n), dtype=torch.int32, device=st.device)
+    row_slots = torch.empty(n, dtype=torch.int64, device=st.device)
+    tt = shc.prepare_build_transposed_table(st.coords, st.inv, st.B, st.V, nbr_t, Kt, table_t,
+                                            row_slots)
+    tt(n)
+    C0, C1, C2 = st.acts[0].shape[-1], st.acts[1].shape[-1], st.acts[2].shape[-1]
+    g = torch.Generator(device=st.device).manual_seed(5)
+    dY2 = torch.randn((n, C2), device=st.device, generator=g).to(st.dtype)
+    dS1 = torch.empty((n, C1), dtype=st.dtype, device=st.device)
+    dW1 = torch.empty(tuple(st.weights[1].shape), dtype=torch.float32, device=st.device)
+    db1 = torch.empty(C2, dtype=torch.float32, device=st.device)
+    dS0 = torch.empty((n, C0), dtype=st.dtype, device=st.device)
+    dW0 = torch.empty(tuple(st.weights[0].shape), dtype=torch.float32, device=st.device)
+    db0 = torch.empty(C1, dtype=torch.float32, device=st.device)
+    conv = shc.prepare_sparse_neighbor_conv_backward(st.acts[1], st.table, table_t, row_slots,
+                                                     slot_of, Kt, st.weights[1], st.acts[2], dY2,
+                                                     dS1, dW1, db1)
+    lin = shc.prepare_sparse_linear_backward(st.acts[0], st.weights[0], st.acts[1], dS1, dS0,
+                                             dW0, db0)
+    t_tt = _time_us(lambda: tt(n), torch, reps)
+    t_conv = _time_us(lambda: conv(n), torch, reps)
+    t_lin = _time_us(lambda: lin(n), torch, reps)
+    t_both = _time_us(lambda: (conv(n), lin(n)), torch, reps)
+    P = int((st.table.view(-1)[: K * n] >= 0).sum().item())
+    e = st.weights[1].element_size()
+    nbytes = (2 * n * C2 * e + n * C1 * e + K * C1 * C2 * e + 4 * K * n + 8 * n + 4 * P
+              + n * C1 * e + 4 * K * C1 * C2 + 4 * C2)
+    flops = 4.0 * P * C1 * C2
+    ach = nbytes / (t_conv * 1e-6) / 1e9
+    return {"config": f"{w.name}: N'={n}, K={K}, C={C1}, bf16, "
+                      f"{Kt} virtual slots, {P} present (row, slot) pairs",
+            "transposed_table_us": round(t_tt, 2), "conv_backward_us": round(t_conv, 2),
+            "linear_backward_us": round(t_lin, 2), "both_layers_us": round(t_both, 2),
+            "conv_algorithmic_bytes": nbytes, "conv_achieved": round(ach, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "conv_frac": round(ach / HBM_PEAK_GBS, 4),
+            "conv_tflops": round(flops / (t_conv * 1e-6) / 1e12, 1)}
 
 
 def _time_us(fn, torch, reps):

@@ -584,6 +584,57 @@ def prepare_sparse_linear(S, W, bias, out, act=SHC_ACT_RELU, stream=None) -> Pre
     return Prepared("shc_sparse_linear", args, 1, n_max, (S, W, bias, out))
 
 
+def prepare_build_transposed_table(coords, inv, B, V, nbr_t, Kt, table_t, row_slots,
+                                   stream=None) -> Prepared:
+    n_max = min(coords.numel() // 2, table_t.numel() // Kt, row_slots.numel())
+    args = [_dev(coords, "coords", torch.int32), _dev(inv, "inv", torch.int32, B * V), 0, B, V,
+            _dev(nbr_t, "nbr_t", torch.int32, V * Kt), Kt, _dev(table_t, "table_t", torch.int32),
+            _dev(row_slots, "row_slots", torch.int64), _stream(stream)]
+    return Prepared("shc_build_transposed_table", args, 2, n_max,
+                    (coords, inv, nbr_t, table_t, row_slots))
+
+
+def prepare_sparse_linear_backward(S, W, Y, dY, dS, dW, db, act=SHC_ACT_RELU, ws=None,
+                                   stream=None) -> Prepared:
+    """shc_sparse_linear_backward for any row count up to the buffers' capacity."""
+    Cin, Cout = W.shape
+    n_max = min(dY.numel() // Cout, S.numel() // Cin if S is not None else 1 << 62,
+                dS.numel() // Cin if dS is not None else 1 << 62)
+    if ws is None:
+        need = sparse_linear_backward_workspace(n_max, Cin, Cout, _dtype_code(W))
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=W.device)
+    dt = W.dtype
+    args = [_opt_dev(S, "S", dt), _dev(W, "W", dt, Cin * Cout), _opt_dev(Y, "Y", dt),
+            _dev(dY, "dY", dt), 0, Cin, Cout, _dtype_code(W), act, _opt_dev(dS, "dS", dt),
+            _opt_dev(dW, "dW", torch.float32, Cin * Cout), _opt_dev(db, "db", torch.float32, Cout),
+            _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)]
+    return Prepared("shc_sparse_linear_backward", args, 4, n_max, (S, W, Y, dY, dS, dW, db, ws))
+
+
+def prepare_sparse_neighbor_conv_backward(S, table, table_t, row_slots, slot_of, Kt, W, Y, dY,
+                                          dS, dW, db, act=SHC_ACT_RELU, ws=None,
+                                          stream=None) -> Prepared:
+    """shc_sparse_neighbor_conv_backward for any row count up to the buffers' capacity."""
+    K, Cin, Cout = W.shape
+    n_max = min(dY.numel() // Cout, S.numel() // Cin if S is not None else 1 << 62,
+                dS.numel() // Cin if dS is not None else 1 << 62,
+                table.numel() // K if table is not None else 1 << 62,
+                table_t.numel() // Kt if table_t is not None else 1 << 62)
+    if ws is None:
+        need = sparse_neighbor_conv_backward_workspace(n_max, K, Cin, Cout, _dtype_code(W))
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=W.device)
+    dt = W.dtype
+    args = [_opt_dev(S, "S", dt), _opt_dev(table, "table", torch.int32),
+            _opt_dev(table_t, "table_t", torch.int32), _opt_dev(row_slots, "row_slots", torch.int64),
+            _opt_dev(slot_of, "slot_of", torch.int32), Kt, _dev(W, "W", dt, K * Cin * Cout),
+            _opt_dev(Y, "Y", dt), _dev(dY, "dY", dt), 0, K, Cin, Cout, _dtype_code(W), act,
+            _opt_dev(dS, "dS", dt), _opt_dev(dW, "dW", torch.float32, K * Cin * Cout),
+            _opt_dev(db, "db", torch.float32, Cout), _dev(ws, "ws"),
+            ws.numel() * ws.element_size(), _stream(stream)]
+    return Prepared("shc_sparse_neighbor_conv_backward", args, 9, n_max,
+                    (S, table, table_t, row_slots, slot_of, W, Y, dY, dS, dW, db, ws))
+
+
 def prepare_gather_sparse_linear(x, coords, B, V, W, bias, out, act=SHC_ACT_RELU,
                                  stream=None) -> Prepared:
     Cin, Cout = W.shape

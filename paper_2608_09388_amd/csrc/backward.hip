@@ -774,8 +774,12 @@ void backward_plan(int64_t n, int32_t K, int32_t Cin, int32_t Cout, int is_bf16,
   o += align256((size_t)nb * 4);
   p->off_cs = o;
   o += align256((size_t)(K + 1) * 4);
+  // partial tiles: sized for chunks of 256 rows whatever L is, so the
+  // workspace never shrinks as n grows
+  const int64_t cap_chunks = conv ? (int64_t)K * ((n + 255) / 256) : (n + 255) / 256;
   p->off_part = o;
-  o += align256((size_t)p->max_chunks * p->tiles * p->T * p->T * sizeof(float));
+  o += align256((size_t)std::max<int64_t>(cap_chunks, p->max_chunks) * p->tiles * p->T * p->T *
+                sizeof(float));
   p->total = o;
 }
 
