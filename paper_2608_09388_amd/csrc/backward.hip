@@ -41,12 +41,17 @@ constexpr int kThreads = 256;
 #define SHC_LDS __attribute__((address_space(3)))
 typedef __bf16 bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
 typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 constexpr int kBufferWord3 = 0x00020000;
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr int kMaxSlotsBwd = 32;
 constexpr int kWgradRows = 128;      // rows per step of the wgrad tile kernel
 // dynamic LDS of the dgrad kernel: 160 KB less room for its static arrays
 constexpr int kDgradLds = 159 * 1024;
+constexpr int kDgradThreads = 512;
+constexpr int kDgradMaxRows = 1536;  // rows per workgroup (sorted in LDS)
+constexpr int kWBatch = 8;           // weight vectors per thread in flight while staging
 
 // ---------------------------------------------------------------------------
 // dZ and the column sums of db
@@ -471,21 +476,29 @@ __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __r
 // dgrad: dS through the transposed table
 // ---------------------------------------------------------------------------
 
-// Grid: (row groups of R rows) x (column slices of WS input channels).
-// Workgroup: the fragments of W[j]^T for every slot j, k-step and 16-column
-// block of its slice go to LDS once (frag f = (j * KS + ks) * NCB + cb, one
-// 1 KB run of 64 lanes x 16 bytes).  Each wavefront walks its 16-row blocks
-// b = wave, wave + 4, ...; a block's jobs are its virtual slots (the or of
-// its rows' 64-bit masks) in ascending order, or one empty job when it has
-// none.  A job loads the rows' sources through table_t, their dZ rows as A
-// fragments (raw buffer loads, an absent row reading zeros), and runs
-// NCB x KS MFMAs against W[slot_of[s]]^T.  The blocks' slot masks are
-// formed in LDS up front; jobs go through a ring of register sets in two
-// stages (source rows, then data); after a block's last job its 16 rows are rounded
-// and stored through the wavefront's LDS scratch.  Without a transposed
-// table (linear layer) every row is its own source through one slot.
+// Grid: (row groups of R rows) x (column slices of WS input channels);
+// kDgradThreads threads.  Workgroup:
+//   * the fragments of W[j]^T for every slot j, k-step and 16-column block of
+//     its slice go to LDS once (frag f = (j * KS + ks) * NCB + cb, one 1 KB
+//     run of 64 lanes x 16 bytes);
+//   * with a transposed table, its rows are bucketed (LDS histogram and
+//     cursors) by their first sparse virtual slot -- one present in fewer
+//     than half of the rows -- so 16-row blocks hold rows that share it;
+//     each block's slot mask is the or of its rows' masks;
+//   * each wavefront walks its blocks b = wave, wave + 8, ...; a block's
+//     jobs are its virtual slots in ascending order (one empty job when it
+//     has none).  A job loads the rows' sources through table_t, their dZ
+//     rows as A fragments (raw buffer loads, an absent row reading zeros),
+//     and runs NCB x KS MFMAs against W[slot_of[s]]^T.  Jobs go through a
+//     ring of register sets in two stages (source rows, then data); after a
+//     block's last job its 16 rows are rounded and stored, through the
+//     wavefront's LDS scratch, at their original positions.
+// Every row is accumulated over its virtual slots in ascending order whatever
+// block it lands in (absent slots add exact zeros), so the result does not
+// depend on the sort.  Without a transposed table (linear layer) every row is
+// its own source through one slot, unsorted.
 template <int WS, int KSM, bool TBL>
-__global__ __launch_bounds__(kThreads) void dgrad_kernel(
+__global__ __launch_bounds__(kDgradThreads) void dgrad_kernel(
     const __bf16* __restrict__ dZ, const __bf16* __restrict__ W,
     const int32_t* __restrict__ table_t, const uint64_t* __restrict__ row_slots,
     const int32_t* __restrict__ slot_of, int64_t n, int32_t K, int32_t Cin, int32_t Cout,
@@ -493,14 +506,20 @@ __global__ __launch_bounds__(kThreads) void dgrad_kernel(
   constexpr int NCB = WS / 16;
   constexpr int DA = KSM <= 4 ? 4 : 2;  // jobs with data loads in flight
   constexpr int D = 2 * DA;              // ring: as many again with only the source loaded
-  constexpr int kWaves = kThreads / 64;
+  constexpr int kWaves = kDgradThreads / 64;
+  constexpr int RPT = kDgradMaxRows / kDgradThreads;  // rows per thread in the sort
+  constexpr int NBK = kMaxVirtualSlots + 1;            // sort buckets
   constexpr int WROW = WS * 2 + 16;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int KS = (Cout + 31) / 32;
   unsigned char* wl = smem;                                     // [K][KS][NCB][64][16]
   unsigned char* scratch = smem + (size_t)K * KS * NCB * 1024;  // [waves][16][WROW]
   uint64_t* blkmask = reinterpret_cast<uint64_t*>(scratch + kWaves * 16 * WROW);  // [R / 16]
+  int32_t* perm = reinterpret_cast<int32_t*>(blkmask + kDgradMaxRows / 16);         // [R]
+  int32_t* hist = perm + kDgradMaxRows;                       // [NBK]: counts, then cursors
   __shared__ int32_t slot_lds[kMaxVirtualSlots];
+  __shared__ int32_t scnt[kMaxVirtualSlots];
+  __shared__ uint64_t dense_lds;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, l16 = lane & 15;
@@ -508,42 +527,122 @@ __global__ __launch_bounds__(kThreads) void dgrad_kernel(
   const int nrows = (int)min((int64_t)R, n - row0);
   const int n0 = blockIdx.y * WS;
 
-  // weights: lane (g, l16) of fragment (j, ks, cb) holds W[j][n0 + 16 cb + l16][32 ks + 8 g .. + 7]
-  const int nfrag = K * KS * NCB * 64;
-  for (int f = tid; f < nfrag; f += kThreads) {
-    const int ln = f & 63;
-    const int fr = f >> 6;
-    const int cb = fr % NCB;
-    const int ks = (fr / NCB) % KS;
-    const int j = fr / (NCB * KS);
-    const int c = n0 + cb * 16 + (ln & 15);
-    const int o = ks * 32 + 8 * (ln >> 4);
-    i32x4 v = i32x4{0, 0, 0, 0};
-    if (c < Cin && o < Cout)
-      v = *reinterpret_cast<const i32x4*>(W + ((int64_t)j * Cin + c) * Cout + o);
-    *reinterpret_cast<i32x4*>(wl + (size_t)f * 16) = v;
-  }
-  // block masks: the or of the 16 rows' virtual-slot masks, one per block;
-  // the virtual slots' weight slots
+  // sort keys' inputs go out with the weights
+  uint64_t mrow[RPT];
   if (TBL) {
-    if (tid < kMaxVirtualSlots) slot_lds[tid] = slot_of[tid];
-    for (int base = wave * 64; base < nrows; base += kThreads) {
-      uint64_t m = base + lane < nrows ? row_slots[row0 + base + lane] : 0ull;
 #pragma unroll
-      for (int d = 1; d < 16; d <<= 1) {
-        const uint32_t lo = __shfl_xor((uint32_t)m, d, 64);
-        const uint32_t hi = __shfl_xor((uint32_t)(m >> 32), d, 64);
-        m |= ((uint64_t)hi << 32) | lo;
-      }
-      if (l16 == 0 && base + lane < nrows) blkmask[(base + lane) >> 4] = m;
+    for (int rr = 0; rr < RPT; ++rr) {
+      const int t = tid + rr * kDgradThreads;
+      mrow[rr] = t < nrows ? row_slots[row0 + t] : 0ull;
+    }
+    if (tid < kMaxVirtualSlots) {
+      slot_lds[tid] = slot_of[tid];
+      scnt[tid] = 0;
+    }
+    for (int q = tid; q < NBK; q += kDgradThreads) hist[q] = 0;
+    for (int b = tid; b < kDgradMaxRows / 16; b += kDgradThreads) blkmask[b] = 0ull;
+  }
+  // weights: lane (g, l16) of fragment (j, ks, cb) holds W[j][n0 + 16 cb + l16][32 ks + 8 g .. + 7];
+  // kWBatch vectors per thread in flight at a time
+  const int nfrag = K * KS * NCB * 64;
+  for (int f0 = 0; f0 < nfrag; f0 += kWBatch * kDgradThreads) {
+    i32x4 v[kWBatch];
+#pragma unroll
+    for (int u = 0; u < kWBatch; ++u) {
+      const int f = f0 + u * kDgradThreads + tid;
+      const int ln = f & 63;
+      const int fr = f >> 6;
+      const int cb = fr % NCB;
+      const int ks = (fr / NCB) % KS;
+      const int j = fr / (NCB * KS);
+      const int c = n0 + cb * 16 + (ln & 15);
+      const int o = ks * 32 + 8 * (ln >> 4);
+      const bool ok = f < nfrag && c < Cin && o < Cout;
+      v[u] = *reinterpret_cast<const i32x4*>(W + (ok ? ((int64_t)j * Cin + c) * Cout + o : 0));
+      if (!ok) v[u] = i32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < kWBatch; ++u) {
+      const int f = f0 + u * kDgradThreads + tid;
+      if (f < nfrag) *reinterpret_cast<i32x4*>(wl + (size_t)f * 16) = v[u];
     }
   }
   __syncthreads();
+
+  if (TBL) {
+    // rows per virtual slot (only the slots some row of the wavefront has)
+    uint64_t wor = 0;
+#pragma unroll
+    for (int rr = 0; rr < RPT; ++rr) wor |= mrow[rr];
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t lo = __shfl_xor((uint32_t)wor, d, 64);
+      const uint32_t hi = __shfl_xor((uint32_t)(wor >> 32), d, 64);
+      wor |= ((uint64_t)hi << 32) | lo;
+    }
+    wor = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(wor >> 32)) << 32) |
+          (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)wor);
+    for (uint64_t bits = wor; bits != 0; bits &= bits - 1) {
+      const int sl = __builtin_ctzll(bits);
+      int c = 0;
+#pragma unroll
+      for (int rr = 0; rr < RPT; ++rr) c += __popcll(__ballot((mrow[rr] >> sl) & 1ull));
+      if (lane == 0) atomicAdd(&scnt[sl], c);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      const uint64_t d = __ballot(lane < kMaxVirtualSlots && 2 * scnt[lane] >= nrows);
+      if (lane == 0) dense_lds = d;
+    }
+    __syncthreads();
+    const uint64_t dense = dense_lds;
+    // buckets: 0 = dense slots only, 1 + s = first sparse virtual slot s; -1 = no row.
+    // A histogram, its exclusive scan, then a position per row from the
+    // bucket's cursor.  The order inside a bucket is whatever the atomics
+    // give: every row is accumulated over its virtual slots in ascending
+    // order whichever block it lands in, so results do not depend on it.
+    int bkt[RPT];
+#pragma unroll
+    for (int rr = 0; rr < RPT; ++rr) {
+      const int t = tid + rr * kDgradThreads;
+      const uint64_t key = mrow[rr] & ~dense;
+      bkt[rr] = t >= nrows ? -1 : (key ? 1 + __builtin_ctzll(key) : 0);
+      if (bkt[rr] >= 0) atomicAdd(&hist[bkt[rr]], 1);
+    }
+    __syncthreads();
+    if (wave == 0) {  // exclusive scan of NBK <= 128 counts, two per lane
+      const int c0 = 2 * lane < NBK ? hist[2 * lane] : 0;
+      const int c1 = 2 * lane + 1 < NBK ? hist[2 * lane + 1] : 0;
+      const int local = c0 + c1;
+      int inc = local;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int y = __shfl_up(inc, d, 64);
+        if (lane >= d) inc += y;
+      }
+      const int run = inc - local;
+      if (2 * lane < NBK) hist[2 * lane] = run;
+      if (2 * lane + 1 < NBK) hist[2 * lane + 1] = run + c0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int rr = 0; rr < RPT; ++rr) {
+      if (bkt[rr] >= 0) {
+        const int pos = atomicAdd(&hist[bkt[rr]], 1);
+        perm[pos] = tid + rr * kDgradThreads;
+        if (mrow[rr]) atomicOr(reinterpret_cast<unsigned long long*>(&blkmask[pos >> 4]),
+                               (unsigned long long)mrow[rr]);
+      }
+    }
+    __syncthreads();
+  }
 
   const __amdgpu_buffer_rsrc_t z_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<__bf16*>(dZ), (short)0, (int)(n * Cout * 2), kBufferWord3);
   const uint32_t row_bytes = (uint32_t)Cout * 2u;
   unsigned char* my = scratch + wave * 16 * WROW;
+  // the row of the workgroup at sorted position p
+  auto row_at = [&](int p) -> int { return TBL ? perm[p] : p; };
 
   struct Job {
     int blk;    // block, or -1 past the end
@@ -576,7 +675,7 @@ __global__ __launch_bounds__(kThreads) void dgrad_kernel(
     return jb.blk >= 0 && jb.s >= 0 && jb.blk * 16 + l16 < nrows;
   };
   auto load_src = [&](const Job& jb, bool live) -> int32_t {
-    const int64_t r = row0 + (live ? jb.blk * 16 + l16 : 0);
+    const int64_t r = row0 + (live ? row_at(jb.blk * 16 + l16) : 0);
     if (!TBL) return (int32_t)r;
     return table_t[(live ? (int64_t)jb.s * n : 0) + r];
   };
@@ -613,10 +712,13 @@ __global__ __launch_bounds__(kThreads) void dgrad_kernel(
   auto epilogue = [&](int blk) {
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
+      // hardware round-to-nearest-even conversion, two rows per instruction
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        *reinterpret_cast<uint16_t*>(my + (4 * g + q) * WROW + (cb * 16 + l16) * 2) =
-            (uint16_t)f32_to_bf16_bits(acc[cb][q]);
+      for (int q = 0; q < 4; q += 2) {
+        const bf16x2 h = __builtin_convertvector(f32x2{acc[cb][q], acc[cb][q + 1]}, bf16x2);
+        *reinterpret_cast<__bf16*>(my + (4 * g + q) * WROW + (cb * 16 + l16) * 2) = h[0];
+        *reinterpret_cast<__bf16*>(my + (4 * g + q + 1) * WROW + (cb * 16 + l16) * 2) = h[1];
+      }
       acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -627,11 +729,12 @@ __global__ __launch_bounds__(kThreads) void dgrad_kernel(
     for (int idx0 = 0; idx0 < 16 * VPRW; idx0 += 64) {
       const int idx = idx0 + lane;
       const int rr = idx / VPRW, q = idx % VPRW;
-      const int64_t row = row0 + blk * 16 + rr;
       const int c = n0 + q * 8;
-      if (idx < 16 * VPRW && blk * 16 + rr < nrows && c < Cin)
+      if (idx < 16 * VPRW && blk * 16 + rr < nrows && c < Cin) {
+        const int64_t row = row0 + row_at(blk * 16 + rr);
         *reinterpret_cast<i32x4*>(dS + row * Cin + c) =
             *reinterpret_cast<const i32x4*>(my + rr * WROW + q * 16);
+      }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -679,22 +782,20 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n + kThreads - 1) / kThreads); }
 
 // column slice of the dgrad kernel: the widest of 128 / 64 / 32 / 16 input
-// channels (not above Cin) whose weight fragments and scratch leave room for
-// two workgroups per CU, else the widest that fits one
-constexpr int kDgradMaxRows = 4096;  // rows per workgroup (block masks in LDS)
-
+// channels (not above Cin) whose weight fragments, scratch and sort arrays
+// fit in LDS (a workgroup of eight wavefronts keeps two per SIMD)
 size_t dgrad_lds(int ws, int32_t Kw, int32_t Cout) {
   const int KS = (Cout + 31) / 32;
-  return (size_t)Kw * KS * (ws / 16) * 1024 + (kThreads / 64) * 16 * (ws * 2 + 16) +
-         kDgradMaxRows / 16 * sizeof(uint64_t);
+  return (size_t)Kw * KS * (ws / 16) * 1024 + (kDgradThreads / 64) * 16 * (ws * 2 + 16) +
+         kDgradMaxRows / 16 * sizeof(uint64_t) + kDgradMaxRows * sizeof(int32_t) +
+         (size_t)(kMaxVirtualSlots + 1) * sizeof(int32_t);
 }
 
 int dgrad_ws(int32_t Kw, int32_t Cin, int32_t Cout) {
-  for (size_t budget : {(size_t)kDgradLds / 2, (size_t)kDgradLds})
-    for (int ws = 128; ws >= 16; ws /= 2) {
-      if (ws > Cin && ws > 16) continue;
-      if (dgrad_lds(ws, Kw, Cout) <= budget) return ws;
-    }
+  for (int ws = 128; ws >= 16; ws /= 2) {
+    if (ws > Cin && ws > 16) continue;
+    if (dgrad_lds(ws, Kw, Cout) <= (size_t)kDgradLds) return ws;
+  }
   return 0;
 }
 
@@ -708,11 +809,15 @@ hipError_t launch_dgrad_ws(const void* dZ, const void* W, const int32_t* table_t
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (a != hipSuccess) return a;
   const int slices = (Cin + WS - 1) / WS;
-  // about 512 workgroups in all, whole 16-row blocks, at least 64 rows each
-  int64_t R = (n * slices + 511) / 512;
+  // one wave of workgroups: as many row groups as the CUs hold workgroups
+  // (all slices), whole 16-row blocks, 64 to kDgradMaxRows rows each; past
+  // that many rows, more groups of the largest size
+  const int64_t per_cu = std::max<int64_t>(1, (int64_t)(160 * 1024) / (int64_t)(lds + 1024));
+  const int64_t groups = std::max<int64_t>(1, 256 * per_cu / slices);
+  int64_t R = (n + groups - 1) / groups;
   R = std::min<int64_t>(kDgradMaxRows, std::max<int64_t>(64, (R + 15) / 16 * 16));
   const unsigned gx = (unsigned)((n + R - 1) / R);
-  hipLaunchKernelGGL(kern, dim3(gx, (unsigned)slices), dim3(kThreads), lds,
+  hipLaunchKernelGGL(kern, dim3(gx, (unsigned)slices), dim3(kDgradThreads), lds,
                      stream, static_cast<const __bf16*>(dZ), static_cast<const __bf16*>(W),
                      table_t, row_slots, slot_of, n, Kw, Cin, Cout, (int32_t)R,
                      static_cast<__bf16*>(dS));
