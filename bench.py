@@ -309,9 +309,10 @@ def backward_measure(st, w, shc, torch, reps):
     conv + ReLU) on the density-sweep workload, with a seeded upstream
     gradient at the conv's output: the conv's input, weight and bias
     gradients, then the linear layer's from the conv's input gradient.  The
-    transposed neighbour lists are built once per mesh and the transposed
-    table once per active set (shared by every conv layer on it); each is
-    timed on its own.  Prepared calls, back to back between HIP events.
+    transposed neighbour lists are built once per mesh, the transposed table
+    and the slot pair lists once per active set (shared by every conv layer
+    on it); each is timed on its own.  Prepared calls, back to back between
+    HIP events.
 
     Roofline figure of the conv backward: algorithmic bytes (dY and the
     stored output Y read once, S and the input rows read once, the table,
@@ -327,6 +328,10 @@ def backward_measure(st, w, shc, torch, reps):
     tt = shc.prepare_build_transposed_table(st.coords, st.inv, st.B, st.V, nbr_t, Kt, table_t,
                                             row_slots)
     tt(n)
+    pairs = torch.empty((K * n, 2), dtype=torch.int32, device=st.device)
+    pair_ptr = torch.empty(K + 1, dtype=torch.int32, device=st.device)
+    sp = shc.prepare_build_slot_pairs(st.table, K, pairs, pair_ptr, n)
+    sp(n)
     C0, C1, C2 = st.acts[0].shape[-1], st.acts[1].shape[-1], st.acts[2].shape[-1]
     g = torch.Generator(device=st.device).manual_seed(5)
     dY2 = torch.randn((n, C2), device=st.device, generator=g).to(st.dtype)
@@ -338,10 +343,12 @@ def backward_measure(st, w, shc, torch, reps):
     db0 = torch.empty(C1, dtype=torch.float32, device=st.device)
     conv = shc.prepare_sparse_neighbor_conv_backward(st.acts[1], st.table, table_t, row_slots,
                                                      slot_of, Kt, st.weights[1], st.acts[2], dY2,
-                                                     dS1, dW1, db1)
+                                                     dS1, dW1, db1, pairs=pairs,
+                                                     pair_ptr=pair_ptr)
     lin = shc.prepare_sparse_linear_backward(st.acts[0], st.weights[0], st.acts[1], dS1, dS0,
                                              dW0, db0)
     t_tt = _time_us(lambda: tt(n), torch, reps)
+    t_sp = _time_us(lambda: sp(n), torch, reps)
     t_conv = _time_us(lambda: conv(n), torch, reps)
     t_lin = _time_us(lambda: lin(n), torch, reps)
     t_both = _time_us(lambda: (conv(n), lin(n)), torch, reps)
@@ -353,7 +360,8 @@ def backward_measure(st, w, shc, torch, reps):
     ach = nbytes / (t_conv * 1e-6) / 1e9
     return {"config": f"{w.name}: N'={n}, K={K}, C={C1}, bf16, "
                       f"{Kt} virtual slots, {P} present (row, slot) pairs",
-            "transposed_table_us": round(t_tt, 2), "conv_backward_us": round(t_conv, 2),
+            "transposed_table_us": round(t_tt, 2), "slot_pairs_us": round(t_sp, 2),
+            "conv_backward_us": round(t_conv, 2),
             "linear_backward_us": round(t_lin, 2), "both_layers_us": round(t_both, 2),
             "conv_algorithmic_bytes": nbytes, "conv_achieved": round(ach, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "conv_frac": round(ach / HBM_PEAK_GBS, 4),

@@ -427,6 +427,19 @@ int shc_sparse_linear_backward(const void* S, const void* W, const void* Y, cons
                                size_t ws_bytes, hipStream_t stream);
 
 /*
+ * Slot pair lists of an active set, for the weight gradient of the sparse
+ * convolution: every (slot j, row i) with table[j][i] >= 0, slot-major with
+ * rows ascending, as int32 pairs[t][2] = (j, i), and pair_ptr[K + 1] with
+ * slot j's pairs at [pair_ptr[j], pair_ptr[j + 1]).  table [K][n_rows] from
+ * shc_build_neighbor_table; pairs capacity K * n_rows pairs.  Built once per
+ * active set and shared by every conv layer on it.
+ * ws: device workspace of shc_build_slot_pairs_workspace bytes.
+ */
+size_t shc_build_slot_pairs_workspace(int64_t n_rows, int32_t K);
+int shc_build_slot_pairs(const int32_t* table, int64_t n_rows, int32_t K, int32_t* pairs,
+                         int32_t* pair_ptr, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * Gradients of the sparse neighbourhood convolution (Eqs. 4-5, Eq. 10),
  * i.e. of the dense convolution of x (.) m restricted to the active rows:
  *
@@ -437,6 +450,8 @@ int shc_sparse_linear_backward(const void* S, const void* W, const void* Y, cons
  *
  *   S [n_rows][Cin], W [K][Cin][Cout], Y, dY [n_rows][Cout]: bf16;
  *   table [K][n_rows]: shc_build_neighbor_table of the active set;
+ *   pairs, pair_ptr: shc_build_slot_pairs of the same table, or both NULL
+ *     (then built inside the call, in the workspace);
  *   table_t, row_slots: shc_build_transposed_table of the same active set;
  *   slot_of, Kt: shc_transpose_neighbors of the mesh;
  *   dS [n_rows][Cin] bf16 out, dW [K][Cin][Cout] fp32 out, db [Cout] fp32
@@ -449,13 +464,13 @@ int shc_sparse_linear_backward(const void* S, const void* W, const void* Y, cons
  */
 size_t shc_sparse_neighbor_conv_backward_workspace(int64_t n_rows, int32_t K, int32_t Cin,
                                                    int32_t Cout, int32_t dtype);
-int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table,
-                                      const int32_t* table_t, const uint64_t* row_slots,
-                                      const int32_t* slot_of, int32_t Kt, const void* W,
-                                      const void* Y, const void* dY, int64_t n_rows, int32_t K,
-                                      int32_t Cin, int32_t Cout, int32_t dtype, int32_t act,
-                                      void* dS, float* dW, float* db, void* ws, size_t ws_bytes,
-                                      hipStream_t stream);
+int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table, const int32_t* pairs,
+                                      const int32_t* pair_ptr, const int32_t* table_t,
+                                      const uint64_t* row_slots, const int32_t* slot_of,
+                                      int32_t Kt, const void* W, const void* Y, const void* dY,
+                                      int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout,
+                                      int32_t dtype, int32_t act, void* dS, float* dW, float* db,
+                                      void* ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -92,11 +92,14 @@ _SIGS = {
                                                   _c_ptr, _c_sz, _c_ptr]),
     "shc_sparse_neighbor_conv_backward_workspace": (_c_sz, [_c_i64, _c_i32, _c_i32, _c_i32,
                                                             _c_i32]),
+    "shc_build_slot_pairs_workspace": (_c_sz, [_c_i64, _c_i32]),
+    "shc_build_slot_pairs": (ctypes.c_int, [_c_ptr, _c_i64, _c_i32, _c_ptr, _c_ptr, _c_ptr, _c_sz,
+                                            _c_ptr]),
     "shc_sparse_neighbor_conv_backward": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
-                                                         _c_i32, _c_ptr, _c_ptr, _c_ptr, _c_i64,
-                                                         _c_i32, _c_i32, _c_i32, _c_i32, _c_i32,
-                                                         _c_ptr, _c_ptr, _c_ptr, _c_ptr, _c_sz,
-                                                         _c_ptr]),
+                                                         _c_ptr, _c_ptr, _c_i32, _c_ptr, _c_ptr,
+                                                         _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32,
+                                                         _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr,
+                                                         _c_ptr, _c_sz, _c_ptr]),
 }
 
 
@@ -473,9 +476,24 @@ def sparse_neighbor_conv_backward_workspace(n_rows: int, K: int, Cin: int, Cout:
     return int(load().shc_sparse_neighbor_conv_backward_workspace(n_rows, K, Cin, Cout, dtype))
 
 
+def build_slot_pairs(table: torch.Tensor, n_rows: int, K: int, pairs: torch.Tensor,
+                     pair_ptr: torch.Tensor, ws=None, stream=None):
+    """shc_build_slot_pairs: pairs [K * n_rows][2] int32, pair_ptr [K + 1] int32."""
+    need = int(load().shc_build_slot_pairs_workspace(n_rows, K))
+    if ws is None:
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=table.device)
+    args = [_dev(table, "table", torch.int32, K * n_rows), n_rows, K,
+            _dev(pairs, "pairs", torch.int32, 2 * K * n_rows),
+            _dev(pair_ptr, "pair_ptr", torch.int32, K + 1), _dev(ws, "ws"),
+            ws.numel() * ws.element_size(), _stream(stream)]
+    _check(load().shc_build_slot_pairs(*args), "shc_build_slot_pairs")
+    return ws
+
+
 def sparse_neighbor_conv_backward(S, table, table_t, row_slots, slot_of, Kt: int, W, Y, dY,
                                   n_rows: int, dS=None, dW=None, db=None,
-                                  act: int = SHC_ACT_RELU, ws=None, stream=None):
+                                  act: int = SHC_ACT_RELU, ws=None, stream=None, pairs=None,
+                                  pair_ptr=None):
     """shc_sparse_neighbor_conv_backward; W [K][Cin][Cout] bf16, dW [K][Cin][Cout] and db fp32.
     Returns the workspace."""
     K, Cin, Cout = W.shape
@@ -484,6 +502,8 @@ def sparse_neighbor_conv_backward(S, table, table_t, row_slots, slot_of, Kt: int
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=W.device)
     dt = W.dtype
     args = [_opt_dev(S, "S", dt, n_rows * Cin), _opt_dev(table, "table", torch.int32, K * n_rows),
+            _opt_dev(pairs, "pairs", torch.int32, 2 * K * n_rows),
+            _opt_dev(pair_ptr, "pair_ptr", torch.int32, K + 1),
             _opt_dev(table_t, "table_t", torch.int32, Kt * n_rows),
             _opt_dev(row_slots, "row_slots", torch.int64, n_rows),
             _opt_dev(slot_of, "slot_of", torch.int32, Kt), Kt, _dev(W, "W", dt, K * Cin * Cout),
@@ -611,9 +631,19 @@ def prepare_sparse_linear_backward(S, W, Y, dY, dS, dW, db, act=SHC_ACT_RELU, ws
     return Prepared("shc_sparse_linear_backward", args, 4, n_max, (S, W, Y, dY, dS, dW, db, ws))
 
 
+def prepare_build_slot_pairs(table, K, pairs, pair_ptr, n_max, ws=None, stream=None) -> Prepared:
+    if ws is None:
+        need = int(load().shc_build_slot_pairs_workspace(n_max, K))
+        ws = torch.empty(max(need, 16), dtype=torch.uint8, device=table.device)
+    args = [_dev(table, "table", torch.int32), 0, K, _dev(pairs, "pairs", torch.int32),
+            _dev(pair_ptr, "pair_ptr", torch.int32, K + 1), _dev(ws, "ws"),
+            ws.numel() * ws.element_size(), _stream(stream)]
+    return Prepared("shc_build_slot_pairs", args, 1, n_max, (table, pairs, pair_ptr, ws))
+
+
 def prepare_sparse_neighbor_conv_backward(S, table, table_t, row_slots, slot_of, Kt, W, Y, dY,
                                           dS, dW, db, act=SHC_ACT_RELU, ws=None,
-                                          stream=None) -> Prepared:
+                                          stream=None, pairs=None, pair_ptr=None) -> Prepared:
     """shc_sparse_neighbor_conv_backward for any row count up to the buffers' capacity."""
     K, Cin, Cout = W.shape
     n_max = min(dY.numel() // Cout, S.numel() // Cin if S is not None else 1 << 62,
@@ -625,14 +655,16 @@ def prepare_sparse_neighbor_conv_backward(S, table, table_t, row_slots, slot_of,
         ws = torch.empty(max(need, 16), dtype=torch.uint8, device=W.device)
     dt = W.dtype
     args = [_opt_dev(S, "S", dt), _opt_dev(table, "table", torch.int32),
+            _opt_dev(pairs, "pairs", torch.int32), _opt_dev(pair_ptr, "pair_ptr", torch.int32, K + 1),
             _opt_dev(table_t, "table_t", torch.int32), _opt_dev(row_slots, "row_slots", torch.int64),
             _opt_dev(slot_of, "slot_of", torch.int32), Kt, _dev(W, "W", dt, K * Cin * Cout),
             _opt_dev(Y, "Y", dt), _dev(dY, "dY", dt), 0, K, Cin, Cout, _dtype_code(W), act,
             _opt_dev(dS, "dS", dt), _opt_dev(dW, "dW", torch.float32, K * Cin * Cout),
             _opt_dev(db, "db", torch.float32, Cout), _dev(ws, "ws"),
             ws.numel() * ws.element_size(), _stream(stream)]
-    return Prepared("shc_sparse_neighbor_conv_backward", args, 9, n_max,
-                    (S, table, table_t, row_slots, slot_of, W, Y, dY, dS, dW, db, ws))
+    return Prepared("shc_sparse_neighbor_conv_backward", args, 11, n_max,
+                    (S, table, pairs, pair_ptr, table_t, row_slots, slot_of, W, Y, dY, dS, dW, db,
+                     ws))
 
 
 def prepare_gather_sparse_linear(x, coords, B, V, W, bias, out, act=SHC_ACT_RELU,

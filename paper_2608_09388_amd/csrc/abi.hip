@@ -658,8 +658,9 @@ int shc_sparse_linear_backward(const void* S, const void* W, const void* Y, cons
   g_last_error[0] = 0;
   SHC_TRY(check_backward(S, W, Y, dY, n_rows, 1, Cin, Cout, dtype, act, dS, dW, db, ws, ws_bytes,
                          shc_sparse_linear_backward_workspace(n_rows, Cin, Cout, dtype)));
-  return hip_status(shc::launch_layer_backward(0, S, nullptr, nullptr, nullptr, nullptr, W, Y, dY,
-                                               n_rows, 1, Cin, Cout, act, dS, dW, db, ws, stream),
+  return hip_status(shc::launch_layer_backward(0, S, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                               nullptr, W, Y, dY, n_rows, 1, Cin, Cout, act, dS,
+                                               dW, db, ws, stream),
                     "sparse_linear_backward launch");
 }
 
@@ -672,13 +673,40 @@ size_t shc_sparse_neighbor_conv_backward_workspace(int64_t n_rows, int32_t K, in
   return pl.total;
 }
 
-int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table,
-                                      const int32_t* table_t, const uint64_t* row_slots,
-                                      const int32_t* slot_of, int32_t Kt, const void* W,
-                                      const void* Y, const void* dY, int64_t n_rows, int32_t K,
-                                      int32_t Cin, int32_t Cout, int32_t dtype, int32_t act,
-                                      void* dS, float* dW, float* db, void* ws, size_t ws_bytes,
-                                      hipStream_t stream) {
+size_t shc_build_slot_pairs_workspace(int64_t n_rows, int32_t K) {
+  if (n_rows < 0 || K <= 0 || K > kMaxSlots) return 0;
+  return shc::slot_pairs_ws_bytes(n_rows, K);
+}
+
+int shc_build_slot_pairs(const int32_t* table, int64_t n_rows, int32_t K, int32_t* pairs,
+                         int32_t* pair_ptr, void* ws, size_t ws_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_rows(n_rows));
+  if (K <= 0) return fail(SHC_ERR_INVALID_ARG, "K = %d must be positive", K);
+  if (K > kMaxSlots) return fail(SHC_ERR_UNSUPPORTED, "K = %d exceeds %d slots", K, kMaxSlots);
+  if ((int64_t)K * n_rows > INT32_MAX)
+    return fail(SHC_ERR_UNSUPPORTED, "K * n_rows exceeds 2^31 - 1");
+  SHC_PTR(pair_ptr, "pair_ptr");
+  if (n_rows == 0)
+    return hip_status(shc::launch_fill_i32(pair_ptr, K + 1, 0, stream),
+                      "build_slot_pairs empty offsets");
+  SHC_PTR(table, "table");
+  SHC_PTR(pairs, "pairs");
+  SHC_PTR(ws, "ws");
+  const size_t need = shc_build_slot_pairs_workspace(n_rows, K);
+  if (ws_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "workspace of %zu bytes is below the %zu needed", ws_bytes, need);
+  return hip_status(shc::launch_slot_pairs(table, n_rows, K, pairs, pair_ptr, ws, stream),
+                    "build_slot_pairs launch");
+}
+
+int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table, const int32_t* pairs,
+                                      const int32_t* pair_ptr, const int32_t* table_t,
+                                      const uint64_t* row_slots, const int32_t* slot_of,
+                                      int32_t Kt, const void* W, const void* Y, const void* dY,
+                                      int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout,
+                                      int32_t dtype, int32_t act, void* dS, float* dW, float* db,
+                                      void* ws, size_t ws_bytes, hipStream_t stream) {
   g_last_error[0] = 0;
   if (K <= 0) return fail(SHC_ERR_INVALID_ARG, "K = %d must be positive", K);
   if (K > kMaxSlots) return fail(SHC_ERR_UNSUPPORTED, "K = %d exceeds %d slots", K, kMaxSlots);
@@ -686,6 +714,10 @@ int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table,
                          shc_sparse_neighbor_conv_backward_workspace(n_rows, K, Cin, Cout, dtype)));
   if ((int64_t)K * n_rows > INT32_MAX)
     return fail(SHC_ERR_UNSUPPORTED, "K * n_rows exceeds 2^31 - 1");
+  if ((pairs == nullptr) != (pair_ptr == nullptr))
+    return fail(SHC_ERR_INVALID_ARG, "pairs and pair_ptr go together");
+  SHC_OPT_PTR(pairs, "pairs");
+  SHC_OPT_PTR(pair_ptr, "pair_ptr");
   if (n_rows > 0 && dW != nullptr) SHC_PTR(table, "table");
   if (n_rows > 0 && dS != nullptr) {
     if (Kt < 1 || Kt > SHC_MAX_VIRTUAL_SLOTS)
@@ -694,8 +726,9 @@ int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table,
     SHC_PTR(row_slots, "row_slots");
     SHC_PTR(slot_of, "slot_of");
   }
-  return hip_status(shc::launch_layer_backward(1, S, table, table_t, row_slots, slot_of, W, Y, dY,
-                                               n_rows, K, Cin, Cout, act, dS, dW, db, ws, stream),
+  return hip_status(shc::launch_layer_backward(1, S, table, pairs, pair_ptr, table_t, row_slots,
+                                               slot_of, W, Y, dY, n_rows, K, Cin, Cout, act, dS,
+                                               dW, db, ws, stream),
                     "sparse_neighbor_conv_backward launch");
 }
 

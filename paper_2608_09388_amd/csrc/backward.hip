@@ -291,17 +291,13 @@ __global__ __launch_bounds__(kThreads) void presence_kernel(const int32_t* __res
     m[e] = table[e] >= 0 ? 1 : 0;
 }
 
-// cs[j] = first chunk of slot j (chunks of L rows of its list); cs[K] = total
-__global__ void chunk_schedule_kernel(const int32_t* __restrict__ row_ptr, int32_t K, int32_t L,
-                                      int32_t* __restrict__ cs) {
-  if (threadIdx.x != 0 || blockIdx.x != 0) return;
-  int32_t c = 0;
-  for (int j = 0; j < K; ++j) {
-    cs[j] = c;
-    const int32_t cnt = row_ptr[j + 1] - row_ptr[j];
-    c += (cnt + L - 1) / L;
-  }
-  cs[K] = c;
+// chunks of L rows of slot j's list: the first one's index and the count
+__device__ inline void slot_chunks(const int32_t* __restrict__ row_ptr, int j, int32_t L,
+                                   int* first, int* count) {
+  int c = 0;
+  for (int q = 0; q < j; ++q) c += (row_ptr[q + 1] - row_ptr[q] + L - 1) / L;
+  *first = c;
+  *count = (row_ptr[j + 1] - row_ptr[j] + L - 1) / L;
 }
 
 // Partial tile of dW[j] over one chunk of slot j's rows.  Workgroup
@@ -314,9 +310,8 @@ __global__ void chunk_schedule_kernel(const int32_t* __restrict__ row_ptr, int32
 template <int T, int R>
 __global__ __launch_bounds__(kThreads) void wgrad_tile_kernel(
     const __bf16* __restrict__ S, const __bf16* __restrict__ dZ, const int32_t* __restrict__ table,
-    const int2* __restrict__ pairs, const int32_t* __restrict__ row_ptr,
-    const int32_t* __restrict__ cs, int32_t K, int64_t n, int32_t L, int32_t Cin, int32_t Cout,
-    float* __restrict__ part) {
+    const int2* __restrict__ pairs, const int32_t* __restrict__ row_ptr, int32_t K, int64_t n,
+    int32_t L, int32_t Cin, int32_t Cout, float* __restrict__ part) {
   constexpr int NB = T / 32;
   constexpr int ROW = T * 2 + 16;
   constexpr int VPR = T * 2 / 16;
@@ -335,9 +330,18 @@ __global__ __launch_bounds__(kThreads) void wgrad_tile_kernel(
   int j = 0;
   int64_t t0, t1;
   if (pairs != nullptr) {
-    if (w >= cs[K]) return;
-    while (j + 1 < K && cs[j + 1] <= w) ++j;
-    const int64_t base = row_ptr[j] + (int64_t)(w - cs[j]) * L;
+    // chunk w: slot j and the chunk's place in slot j's list
+    int c = 0, wc = -1;
+    for (j = 0; j < K; ++j) {
+      const int nch = (row_ptr[j + 1] - row_ptr[j] + L - 1) / L;
+      if (w < c + nch) {
+        wc = w - c;
+        break;
+      }
+      c += nch;
+    }
+    if (wc < 0) return;  // past the last chunk
+    const int64_t base = row_ptr[j] + (int64_t)wc * L;
     t0 = base;
     t1 = min(base + L, (int64_t)row_ptr[j + 1]);
   } else {
@@ -444,8 +448,8 @@ __global__ __launch_bounds__(kThreads) void wgrad_tile_kernel(
 // sums are added in order.  A slot without chunks gets 0.
 template <int T>
 __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __restrict__ part,
-                                                                const int32_t* __restrict__ cs,
-                                                                int32_t K, int32_t Cin,
+                                                                const int32_t* __restrict__ row_ptr,
+                                                                int32_t L, int32_t Cin,
                                                                 int32_t Cout, int single,
                                                                 int32_t n_chunks,
                                                                 float* __restrict__ dW) {
@@ -454,8 +458,12 @@ __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __r
   const int tiles = tA * tB;
   const int j = blockIdx.x / tiles, t = blockIdx.x - j * tiles;
   const int ta = t / tB, tb = t - ta * tB;
-  const int c0 = single ? 0 : cs[j];
-  const int c1 = single ? n_chunks : cs[j + 1];
+  int c0 = 0, c1 = n_chunks;
+  if (!single) {
+    int cnt;
+    slot_chunks(row_ptr, j, L, &c0, &cnt);
+    c1 = c0 + cnt;
+  }
   const int ex = threadIdx.x & 31, y = threadIdx.x >> 5;
   const int e = blockIdx.y * 32 + ex;
   double s = 0.0;
@@ -862,23 +870,12 @@ void backward_plan(int64_t n, int32_t K, int32_t Cin, int32_t Cout, int is_bf16,
   p->off_colpart = o;
   o += align256((size_t)p->splits * Cout * sizeof(float));
   const int64_t kn = conv ? (int64_t)K * n : 0;
-  p->off_mask = o;
-  o += align256((size_t)kn);
   p->off_pairs = o;
   o += align256((size_t)kn * 8);
-  p->off_inv = o;
-  o += align256((size_t)kn * 4);
   p->off_rowptr = o;
   o += align256((size_t)(K + 1) * 4);
-  p->off_nact = o;
-  o += align256(16);
-  p->off_bc = o;
-  int32_t nb = 0;
-  int64_t per_block = 0;
-  if (kn > 0) compact_plan(kn, &nb, &per_block);
-  o += align256((size_t)nb * 4);
-  p->off_cs = o;
-  o += align256((size_t)(K + 1) * 4);
+  p->off_mask = o;  // the pair build's own workspace
+  o += conv ? slot_pairs_ws_bytes(n, K) : 0;
   // partial tiles: sized for chunks of 256 rows whatever L is, so the
   // workspace never shrinks as n grows
   const int64_t cap_chunks = conv ? (int64_t)K * ((n + 255) / 256) : (n + 255) / 256;
@@ -928,7 +925,42 @@ hipError_t launch_transposed_table(const int32_t* coords, const int32_t* inv, in
   return hipGetLastError();
 }
 
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3(std::min<unsigned>(grid_for(n), 4096)), dim3(kThreads),
+                     0, stream, p, n, v);
+  return hipGetLastError();
+}
+
+size_t slot_pairs_ws_bytes(int64_t n, int32_t K) {
+  int32_t nb = 0;
+  int64_t per_block = 0;
+  const int64_t kn = (int64_t)K * n;
+  if (kn > 0) compact_plan(kn, &nb, &per_block);
+  return align256((size_t)kn) + align256((size_t)kn * 4) + align256(16) + align256((size_t)nb * 4);
+}
+
+// Pair lists of an active set: (slot j, row i) for every table[j][i] >= 0,
+// slot-major with rows ascending (a compaction of the [K][n] presence
+// mask), and the slot offsets pair_ptr[K + 1].  ws: slot_pairs_ws_bytes.
+hipError_t launch_slot_pairs(const int32_t* table, int64_t n, int32_t K, int32_t* pairs,
+                             int32_t* pair_ptr, void* ws, hipStream_t stream) {
+  unsigned char* w = static_cast<unsigned char*>(ws);
+  const int64_t kn = (int64_t)K * n;
+  uint8_t* mask = w;
+  int32_t* inv_p = reinterpret_cast<int32_t*>(w + align256((size_t)kn));
+  int32_t* nact = reinterpret_cast<int32_t*>(w + align256((size_t)kn) + align256((size_t)kn * 4));
+  int32_t* bc = nact + 64;
+  hipLaunchKernelGGL(presence_kernel, dim3(std::min<unsigned>(grid_for(kn), 8192)), dim3(kThreads),
+                     0, stream, table, kn, mask);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  return launch_compact(mask, K, (int32_t)n, pairs, inv_p, pair_ptr, nact, nullptr, kn, bc,
+                        stream);
+}
+
 hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
+                                 const int32_t* pairs, const int32_t* pair_ptr,
                                  const int32_t* table_t, const uint64_t* row_slots,
                                  const int32_t* slot_of, const void* W, const void* Y,
                                  const void* dY, int64_t n, int32_t K, int32_t Cin, int32_t Cout,
@@ -965,46 +997,39 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
   // weight gradient
   if (dW != nullptr) {
     float* part = reinterpret_cast<float*>(w + pl.off_part);
-    const int2* pairs = nullptr;
+    const int2* pr = nullptr;
     const int32_t* rp = nullptr;
-    const int32_t* cs = nullptr;
-    int64_t grid_chunks = pl.max_chunks;
     if (conv) {
-      uint8_t* mask = w + pl.off_mask;
-      int32_t* pr = reinterpret_cast<int32_t*>(w + pl.off_pairs);
-      int32_t* inv_p = reinterpret_cast<int32_t*>(w + pl.off_inv);
-      int32_t* rowp = reinterpret_cast<int32_t*>(w + pl.off_rowptr);
-      int32_t* nact = reinterpret_cast<int32_t*>(w + pl.off_nact);
-      int32_t* bc = reinterpret_cast<int32_t*>(w + pl.off_bc);
-      int32_t* csw = reinterpret_cast<int32_t*>(w + pl.off_cs);
-      const int64_t kn = (int64_t)K * n;
-      hipLaunchKernelGGL(presence_kernel, dim3(std::min<unsigned>(grid_for(kn), 8192)),
-                         dim3(kThreads), 0, stream, table, kn, mask);
-      err = launch_compact(mask, K, (int32_t)n, pr, inv_p, rowp, nact, nullptr, kn, bc, stream);
-      if (err != hipSuccess) return err;
-      hipLaunchKernelGGL(chunk_schedule_kernel, dim3(1), dim3(64), 0, stream, rowp, K, pl.L, csw);
-      pairs = reinterpret_cast<const int2*>(pr);
-      rp = rowp;
-      cs = csw;
+      if (pairs != nullptr) {
+        pr = reinterpret_cast<const int2*>(pairs);
+        rp = pair_ptr;
+      } else {
+        int32_t* prw = reinterpret_cast<int32_t*>(w + pl.off_pairs);
+        int32_t* rpw = reinterpret_cast<int32_t*>(w + pl.off_rowptr);
+        err = launch_slot_pairs(table, n, K, prw, rpw, w + pl.off_mask, stream);
+        if (err != hipSuccess) return err;
+        pr = reinterpret_cast<const int2*>(prw);
+        rp = rpw;
+      }
     }
-    const unsigned gt = (unsigned)(grid_chunks * pl.tiles);
+    const unsigned gt = (unsigned)(pl.max_chunks * pl.tiles);
     if (pl.T == 128)
       hipLaunchKernelGGL((wgrad_tile_kernel<128, kWgradRows>), dim3(gt), dim3(kThreads), 0, stream,
-                         static_cast<const __bf16*>(S), static_cast<const __bf16*>(dZ), table,
-                         pairs, rp, cs, Kw, n, pl.L, Cin, Cout, part);
+                         static_cast<const __bf16*>(S), static_cast<const __bf16*>(dZ), table, pr,
+                         rp, Kw, n, pl.L, Cin, Cout, part);
     else
       hipLaunchKernelGGL((wgrad_tile_kernel<64, kWgradRows>), dim3(gt), dim3(kThreads), 0, stream,
-                         static_cast<const __bf16*>(S), static_cast<const __bf16*>(dZ), table,
-                         pairs, rp, cs, Kw, n, pl.L, Cin, Cout, part);
+                         static_cast<const __bf16*>(S), static_cast<const __bf16*>(dZ), table, pr,
+                         rp, Kw, n, pl.L, Cin, Cout, part);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     const dim3 rg((unsigned)(Kw * pl.tiles), (unsigned)(pl.T * pl.T / 32));
     if (pl.T == 128)
-      hipLaunchKernelGGL(wgrad_reduce_kernel<128>, rg, dim3(kThreads), 0, stream, part, cs, Kw,
-                         Cin, Cout, conv ? 0 : 1, (int32_t)grid_chunks, dW);
+      hipLaunchKernelGGL(wgrad_reduce_kernel<128>, rg, dim3(kThreads), 0, stream, part, rp, pl.L,
+                         Cin, Cout, conv ? 0 : 1, (int32_t)pl.max_chunks, dW);
     else
-      hipLaunchKernelGGL(wgrad_reduce_kernel<64>, rg, dim3(kThreads), 0, stream, part, cs, Kw,
-                         Cin, Cout, conv ? 0 : 1, (int32_t)grid_chunks, dW);
+      hipLaunchKernelGGL(wgrad_reduce_kernel<64>, rg, dim3(kThreads), 0, stream, part, rp, pl.L,
+                         Cin, Cout, conv ? 0 : 1, (int32_t)pl.max_chunks, dW);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
   }

@@ -67,8 +67,7 @@ constexpr int kMaxVirtualSlots = 64;
 struct BwdPlan {
   int T, tiles, L, splits;
   int64_t max_chunks, rps;
-  size_t off_dz, off_colpart, off_mask, off_pairs, off_inv, off_rowptr, off_nact, off_bc, off_cs,
-      off_part, total;
+  size_t off_dz, off_colpart, off_pairs, off_rowptr, off_mask, off_part, total;
 };
 void backward_plan(int64_t n, int32_t K, int32_t Cin, int32_t Cout, int is_bf16, int conv,
                    BwdPlan* p);
@@ -80,7 +79,12 @@ hipError_t launch_transpose_neighbors(const int32_t* nbr, int32_t V, int32_t K, 
 hipError_t launch_transposed_table(const int32_t* coords, const int32_t* inv, int64_t n, int32_t B,
                                    int32_t V, const int32_t* nbr_t, int32_t Kt, int32_t* table_t,
                                    uint64_t* row_slots, hipStream_t stream);
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t stream);
+size_t slot_pairs_ws_bytes(int64_t n, int32_t K);
+hipError_t launch_slot_pairs(const int32_t* table, int64_t n, int32_t K, int32_t* pairs,
+                             int32_t* pair_ptr, void* ws, hipStream_t stream);
 hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
+                                 const int32_t* pairs, const int32_t* pair_ptr,
                                  const int32_t* table_t, const uint64_t* row_slots,
                                  const int32_t* slot_of, const void* W, const void* Y,
                                  const void* dY, int64_t n, int32_t K, int32_t Cin, int32_t Cout,

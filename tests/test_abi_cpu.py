@@ -215,11 +215,11 @@ def test_backward_validation(lib):
     assert needc > need
     assert lib.shc_sparse_neighbor_conv_backward_workspace(1000, 33, 128, 128, 1) == 0
 
-    def conv(S=A, table=A, table_t=A, rs=A, so=A, Kt=56, W=A, Y=A, dY=A, n=1000, K=9, Cin=128,
-             Cout=128, dt=1, act=1, dS=A, dW=A, db=A, ws=A, nbytes=needc):
-        return lib.shc_sparse_neighbor_conv_backward(S, table, table_t, rs, so, Kt, W, Y, dY, n,
-                                                     K, Cin, Cout, dt, act, dS, dW, db, ws,
-                                                     nbytes, None)
+    def conv(S=A, table=A, pairs=None, pp=None, table_t=A, rs=A, so=A, Kt=56, W=A, Y=A, dY=A,
+             n=1000, K=9, Cin=128, Cout=128, dt=1, act=1, dS=A, dW=A, db=A, ws=A, nbytes=needc):
+        return lib.shc_sparse_neighbor_conv_backward(S, table, pairs, pp, table_t, rs, so, Kt, W,
+                                                     Y, dY, n, K, Cin, Cout, dt, act, dS, dW, db,
+                                                     ws, nbytes, None)
 
     assert conv(K=0) == -1 and conv(K=33) == -4
     assert conv(dt=0) == -4
@@ -228,6 +228,15 @@ def test_backward_validation(lib):
     assert conv(Kt=0) == -1 and conv(Kt=65) == -1
     assert conv(rs=MIS) == -3
     assert conv(nbytes=needc - 1) == -2
+    assert conv(pairs=A) == -1 and "together" in err(lib)   # pairs without their offsets
+    assert conv(pairs=MIS, pp=A) == -3
+    sp = lib.shc_build_slot_pairs
+    need_p = lib.shc_build_slot_pairs_workspace(1000, 9)
+    assert need_p > 0 and lib.shc_build_slot_pairs_workspace(1000, 33) == 0
+    assert sp(A, 1000, 0, A, A, A, need_p, None) == -1
+    assert sp(A, 1000, 33, A, A, A, need_p, None) == -4
+    assert sp(None, 1000, 9, A, A, A, need_p, None) == -1
+    assert sp(A, 1000, 9, A, A, A, need_p - 1, None) == -2
 
 
 def test_gather_scatter_pool_validation(lib):

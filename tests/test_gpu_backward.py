@@ -86,7 +86,7 @@ def conv_inputs(rng, n, K, Cin, Cout):
     return S, W, Y, dY
 
 
-def run_conv_backward(st, S, W, Y, dY, act, want=("dS", "dW", "db")):
+def run_conv_backward(st, S, W, Y, dY, act, want=("dS", "dW", "db"), with_pairs=False):
     n, K = st.n, st.K
     Cin, Cout = W.shape[1], W.shape[2]
     dS = torch.full((max(n, 1), Cin), float("nan"), dtype=torch.bfloat16, device="cuda")
@@ -95,17 +95,23 @@ def run_conv_backward(st, S, W, Y, dY, act, want=("dS", "dW", "db")):
     Sd = up(S if n else np.zeros((1, Cin)), "bf16")
     Yd = up(Y if n else np.zeros((1, Cout)), "bf16")
     dYd = up(dY if n else np.zeros((1, Cout)), "bf16")
+    pairs = pair_ptr = None
+    if with_pairs:
+        pairs = torch.full((max(K * n, 1), 2), -7, dtype=torch.int32, device="cuda")
+        pair_ptr = torch.full((K + 1,), -7, dtype=torch.int32, device="cuda")
+        shc.build_slot_pairs(st.table, n, K, pairs, pair_ptr)
     shc.sparse_neighbor_conv_backward(
         Sd, st.table, st.table_t, st.row_slots, st.slot_of, st.Kt, up(W, "bf16"), Yd, dYd, n,
         dS if "dS" in want else None, dW if "dW" in want else None,
-        db if "db" in want else None, act=shc.SHC_ACT_RELU if act else shc.SHC_ACT_NONE)
+        db if "db" in want else None, act=shc.SHC_ACT_RELU if act else shc.SHC_ACT_NONE,
+        pairs=pairs, pair_ptr=pair_ptr)
     torch.cuda.synchronize()
     return down(dS)[:n], down(dW), down(db)
 
 
-def check_conv(st, nbr, S, W, Y, dY, act):
+def check_conv(st, nbr, S, W, Y, dY, act, with_pairs=False):
     B, V = st.B, st.V
-    gS, gW, gb = run_conv_backward(st, S, W, Y, dY, act)
+    gS, gW, gb = run_conv_backward(st, S, W, Y, dY, act, with_pairs=with_pairs)
     rS, rW, rb = O.sparse_conv_backward(S, st.coords, B, V, nbr, W, dY, Y, act)
     dZ = O.relu_backward(dY, Y) if act else np.asarray(dY, np.float64)
     sS, sW, sb = O.sparse_conv_backward(np.abs(S), st.coords, B, V, nbr, np.abs(W), np.abs(dZ))
@@ -184,7 +190,8 @@ def test_conv_backward_vs_oracle(dev, B, V, K, Cin, Cout, p, act):
     st = ConvSetup(mask, nbr)
     assert st.n > 0
     S, W, Y, dY = conv_inputs(rng, st.n, K, Cin, Cout)
-    check_conv(st, nbr, S, W, Y, dY, act)
+    # half of the cases take slot pairs built once beforehand, as a stack would
+    check_conv(st, nbr, S, W, Y, dY, act, with_pairs=(Cin + Cout) % 3 == 0)
 
 
 @pytest.mark.parametrize("n,Cin,Cout,act", [(1000, 128, 128, True), (37, 64, 32, False),
@@ -235,6 +242,32 @@ def test_conv_backward_self_slot_is_linear_and_repeats(dev):
     only = run_conv_backward(st, S, W, Y, dY, True, want=("db",))
     assert np.all(np.isnan(only[0])) and np.all(np.isnan(only[1]))
     assert np.array_equal(only[2], a[2])
+
+
+def test_slot_pairs_exact_and_shared(dev):
+    """Slot pair lists are the slot-major (j, i) of every present table entry;
+    a conv backward given them equals one that builds its own, bit for bit."""
+    rng = np.random.default_rng(13)
+    B, V, K = 3, 90, 6
+    nbr = rand_nbr(V, K, rng)
+    mask = (rng.random((B, V)) < 0.35).astype(np.uint8)
+    st = ConvSetup(mask, nbr)
+    n = st.n
+    pairs = torch.full((K * n, 2), -7, dtype=torch.int32, device="cuda")
+    pair_ptr = torch.full((K + 1,), -7, dtype=torch.int32, device="cuda")
+    shc.build_slot_pairs(st.table, n, K, pairs, pair_ptr)
+    torch.cuda.synchronize()
+    tab = down(st.table).reshape(-1)[: K * n].reshape(K, n)
+    want = np.array([(j, i) for j in range(K) for i in range(n) if tab[j, i] >= 0], np.int32)
+    ptr = down(pair_ptr)
+    assert ptr[0] == 0 and ptr[-1] == len(want)
+    assert np.array_equal(down(pairs)[: len(want)], want)
+    assert np.array_equal(np.diff(ptr), [(tab[j] >= 0).sum() for j in range(K)])
+    S, W, Y, dY = conv_inputs(rng, n, K, 64, 64)
+    a = run_conv_backward(st, S, W, Y, dY, True)
+    b = run_conv_backward(st, S, W, Y, dY, True, with_pairs=True)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
 
 
 def test_conv_backward_empty_active_set(dev):
