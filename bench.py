@@ -186,7 +186,9 @@ def main():
         copy_calibration(torch, args.copy_calibration)
         return
     w = synth.workload_c4(args.density)
-    st = SparseStack(w, device="cuda:0")
+    # the next batch's compaction and neighbour table run on a second stream
+    # beside the current batch's scatter and pool
+    st = SparseStack(w, device="cuda:0", side_stream=True)
     n = st.compact()
     log(f"workload ready: N'={n} active rows of {w.B * w.V}")
     L = len(w.layers)
@@ -196,7 +198,8 @@ def main():
     torch.cuda.synchronize()
 
     # timed region: K whole steps over consecutive batches (each step's
-    # compaction overlapped with the previous step's scatter and pool); HIP
+    # compaction and table on the side stream, overlapped with the previous
+    # step's scatter and pool); HIP
     # events around the conv launch of every EVENT_EVERY-th step, on the
     # stream it runs on (a pair of timing events costs the step a few us)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))

@@ -65,10 +65,19 @@ class _IndexSet:
         # full capacity, so each call only takes the row count
         self.compact = shc.PreparedCompact(st.mask, B, V, self.coords, self.inv, self.row_ptr,
                                            self.n_active, self.ws)
+        # the same compaction and table build on the side stream (run() with
+        # side_stream: they overlap the previous batch's scatter and pool)
+        self.compact_side = (shc.PreparedCompact(st.mask, B, V, self.coords, self.inv,
+                                                 self.row_ptr, self.n_active, self.ws,
+                                                 stream=st.side)
+                             if st.side is not None else None)
         self.gather = shc.prepare_gather_rows(st.x, self.coords, B, V, st.acts[0])
         self.table_call = (shc.prepare_build_neighbor_table(self.coords, self.inv, B, V, st.nbr,
                                                             self.table)
                            if self.table is not None else None)
+        self.table_side = (shc.prepare_build_neighbor_table(self.coords, self.inv, B, V, st.nbr,
+                                                            self.table, stream=st.side)
+                           if self.table is not None and st.side is not None else None)
         self.layers = []
         for l, spec in enumerate(st.w.layers):
             src, dst = st.acts[l], st.acts[l + 1]
@@ -90,9 +99,13 @@ class _IndexSet:
 
 
 class SparseStack:
-    def __init__(self, w: Workload, device: str = "cuda", act: int = shc.SHC_ACT_RELU):
+    def __init__(self, w: Workload, device: str = "cuda", act: int = shc.SHC_ACT_RELU,
+                 side_stream: bool = False):
         self.w = w
         self.device = torch.device(device)
+        # second stream (default priority) for the next batch's compaction and
+        # table in run(); None: everything on the current stream
+        self.side = torch.cuda.Stream(device=self.device) if side_stream else None
         self.dtype = TORCH_DTYPE[w.dtype]
         self.B, self.V, self.K = w.B, w.V, w.K
         self.act = act
@@ -172,10 +185,10 @@ class SparseStack:
         if s.pool is not None:
             s.pool(s.n)
 
-    def _front(self, s: _IndexSet, around=None):
+    def _front(self, s: _IndexSet, around=None, table_done: bool = False):
         """Everything of a batch after its compaction, up to its last layer;
         ``around = (l, ev_a, ev_b)`` records the events around layer l."""
-        if s.table_call is not None:
+        if s.table_call is not None and not table_done:
             s.table_call(s.n)
         if not self.fused_gather:
             s.gather(s.n)
@@ -209,6 +222,8 @@ class SparseStack:
         last batch's.  Returns its N'."""
         if steps <= 0:
             return self.n or 0
+        if self.side is not None:
+            return self._run_two_streams(steps, around_layer, feed)
         s = self._set
         if feed is not None:
             feed(0)
@@ -233,6 +248,60 @@ class SparseStack:
             if nxt is not None:
                 nxt.n = nxt.compact.wait()
                 s = nxt
+        return s.n
+
+    def _run_two_streams(self, steps: int, around_layer, feed) -> int:
+        """run() with batch k + 1's compaction and neighbour table on the side
+        stream, beside batch k's scatter and pool on the current stream.
+
+        Events order the two streams: the side stream starts on an index set
+        only after the current stream's last reader of it (the pool of batch
+        k - 1) and after ``feed``'s writes; the current stream starts batch
+        k + 1's layers only after its table.  Every batch runs the whole path."""
+        main = torch.cuda.current_stream(self.device)
+        side = self.side
+        free = [torch.cuda.Event(), torch.cuda.Event()]   # set i released by its last reader
+        used = [False, False]
+        ready = torch.cuda.Event()
+        fed = torch.cuda.Event()
+        cur = self._cur
+        s = self._sets[cur]
+        if feed is not None:
+            feed(0)
+        s.compact.start()
+        s.n = s.compact.wait()
+        table_done = False
+        for k in range(steps):
+            ev = None
+            if around_layer is not None and around_layer[1][k][0] is not None:
+                ev = (around_layer[0], *around_layer[1][k])
+            self._front(s, ev, table_done=table_done)
+            nxt_i = cur ^ 1
+            nxt = self._sets[nxt_i] if k + 1 < steps else None
+            if nxt is not None:
+                if feed is not None:
+                    feed(k + 1)
+                    fed.record(main)
+                    side.wait_event(fed)
+                if used[nxt_i]:
+                    side.wait_event(free[nxt_i])
+                nxt.compact_side.start()
+            if s.scatter is not None:
+                s.scatter(s.n)
+            if s.pool is not None:
+                s.pool(s.n)
+            free[cur].record(main)
+            used[cur] = True
+            if nxt is not None:
+                nxt.n = nxt.compact_side.wait()
+                table_done = nxt.table_side is not None
+                if table_done:
+                    nxt.table_side(nxt.n)
+                ready.record(side)
+                main.wait_event(ready)
+                cur = nxt_i
+                s = nxt
+        self._cur = cur
         return s.n
 
     # -- results on the host --------------------------------------------------

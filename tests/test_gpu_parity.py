@@ -855,19 +855,21 @@ def test_full_size_workloads_sampled(dev, name):
             assert np.array_equal(P[b], seg.max(0) if len(seg) else np.zeros(last.shape[1]))
 
 
+@pytest.mark.parametrize("side", [False, True])
 @pytest.mark.parametrize("steps", [1, 2, 3])
-def test_overlapped_run_new_mask_per_batch(dev, steps):
+def test_overlapped_run_new_mask_per_batch(dev, steps, side):
     """SparseStack.run: each batch's compaction (into the other index set) is
-    enqueued before the previous batch's scatter and pool.  Every batch gets
-    its own mask and features; the outputs left behind must be the oracle's
-    for the last batch, with index sets that last held another mask."""
+    enqueued before the previous batch's scatter and pool -- with ``side``, on
+    a second stream beside them, ordered by events.  Every batch gets its own
+    mask and features; the outputs left behind must be the oracle's for the
+    last batch, with index sets that last held another mask."""
     from paper_2608_09388_amd.pipeline import SparseStack, to_device
     w = synth.workload_c4(0.05, B=6, V=655)
     rng = np.random.default_rng(400 + steps)
     masks = [(rng.random((w.B, w.V)) < p).astype(np.uint8) for p in (0.3, 0.05, 0.2)][:steps]
     xs = [synth.as_dtype(rng.standard_normal(w.x.shape).astype(np.float32), w.dtype)[1]
           for _ in range(steps)]
-    st = SparseStack(w, device=str(dev))
+    st = SparseStack(w, device=str(dev), side_stream=side)
     st.run(2)                               # both index sets hold the workload's own mask
 
     def feed(k):
