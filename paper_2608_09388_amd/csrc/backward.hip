@@ -245,38 +245,48 @@ __global__ __launch_bounds__(kThreads) void tv_sort_kernel(const int32_t* __rest
 // ---------------------------------------------------------------------------
 
 // table_t[s * n + i] = inv[b_i * V + tv[v_i * Kt + s]] or -1; row_slots[i] has
-// bit s set when that entry is a row.
+// bit s set when that entry is a row.  Four lanes per row, lane q taking the
+// virtual slots 16 q .. 16 q + 15 (both load rounds of all four in flight at
+// once); the row's mask is or-ed over the four lanes by shuffles.
 __global__ __launch_bounds__(kThreads) void tt_kernel(const int2* __restrict__ coords,
                                                       const int32_t* __restrict__ inv, int64_t n,
                                                       int32_t B, int32_t V,
                                                       const int32_t* __restrict__ tv, int32_t Kt,
                                                       int32_t* __restrict__ table_t,
                                                       uint64_t* __restrict__ row_slots) {
-  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (i >= n) return;
-  const int2 c = coords[i];
-  const bool ok = c.x >= 0 && c.x < B && c.y >= 0 && c.y < V;
+  const int64_t gid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t i = gid >> 2;
+  const int q = (int)(gid & 3);
+  const bool in = i < n;
+  const int2 c = coords[in ? i : 0];
+  const bool ok = in && c.x >= 0 && c.x < B && c.y >= 0 && c.y < V;
   const int32_t* trow = tv + (int64_t)(ok ? c.y : 0) * Kt;
   const int32_t* irow = inv + (int64_t)(ok ? c.x : 0) * V;
-  uint64_t bits = 0;
-  for (int s0 = 0; s0 < Kt; s0 += 16) {
-    int32_t v[16], r[16];
+  const int s0 = q * 16;
+  int32_t v[16], r[16];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) v[u] = s0 + u < Kt ? trow[s0 + u] : -1;
+  for (int u = 0; u < 16; ++u) v[u] = s0 + u < Kt ? trow[s0 + u] : -1;
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const bool live = ok && v[u] >= 0 && v[u] < V;
-      r[u] = irow[live ? v[u] : 0];
-      r[u] = (live && r[u] >= 0 && (int64_t)r[u] < n) ? r[u] : -1;
-    }
-#pragma unroll
-    for (int u = 0; u < 16; ++u)
-      if (s0 + u < Kt) {
-        table_t[(int64_t)(s0 + u) * n + i] = r[u];
-        if (r[u] >= 0) bits |= 1ull << (s0 + u);
-      }
+  for (int u = 0; u < 16; ++u) {
+    const bool live = ok && v[u] >= 0 && v[u] < V;
+    r[u] = irow[live ? v[u] : 0];
+    r[u] = (live && r[u] >= 0 && (int64_t)r[u] < n) ? r[u] : -1;
   }
-  row_slots[i] = bits;
+  uint64_t bits = 0;
+#pragma unroll
+  for (int u = 0; u < 16; ++u)
+    if (in && s0 + u < Kt) {
+      table_t[(int64_t)(s0 + u) * n + i] = r[u];
+      if (r[u] >= 0) bits |= 1ull << (s0 + u);
+    }
+  // or over the row's four lanes (lanes 4k .. 4k + 3 of the wavefront)
+#pragma unroll
+  for (int d = 1; d < 4; d <<= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)bits, d, 64);
+    const uint32_t hi = __shfl_xor((uint32_t)(bits >> 32), d, 64);
+    bits |= ((uint64_t)hi << 32) | lo;
+  }
+  if (in && q == 0) row_slots[i] = bits;
 }
 
 // ---------------------------------------------------------------------------
@@ -919,7 +929,7 @@ hipError_t launch_transposed_table(const int32_t* coords, const int32_t* inv, in
                                    int32_t V, const int32_t* nbr_t, int32_t Kt, int32_t* table_t,
                                    uint64_t* row_slots, hipStream_t stream) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(tt_kernel, dim3(grid_for(n)), dim3(kThreads), 0, stream,
+  hipLaunchKernelGGL(tt_kernel, dim3(grid_for(4 * n)), dim3(kThreads), 0, stream,
                      reinterpret_cast<const int2*>(coords), inv, n, B, V, nbr_t, Kt, table_t,
                      row_slots);
   return hipGetLastError();
