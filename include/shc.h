@@ -410,14 +410,14 @@ int shc_build_transposed_table(const int32_t* coords, const int32_t* inv, int64_
  *
  * the dense layer's gradients at the active rows (rows are independent).
  *   S [n_rows][Cin], W [Cin][Cout], Y = the layer's output [n_rows][Cout]
- *   (read only with SHC_ACT_RELU), dY [n_rows][Cout]: bf16;
- *   dS [n_rows][Cin] bf16 out, dW [Cin][Cout] fp32 out, db [Cout] fp32 out;
+ *   (read only with SHC_ACT_RELU), dY [n_rows][Cout]: all of `dtype`;
+ *   dS [n_rows][Cin] `dtype` out, dW [Cin][Cout] fp32 out, db [Cout] fp32 out;
  *   each output may be NULL (not computed).
  *   ws: device workspace of shc_sparse_linear_backward_workspace bytes.
  * Every sum has a fixed order: dS in fp32 over Cout, rounded once; dW in
  * fp32 over chunks of rows, the chunks combined in fp64; db in fp32 over
  * splits of rows, combined in fp64.  Results repeat bit for bit.
- * bf16 only (SHC_ERR_UNSUPPORTED otherwise); Cout <= 256.
+ * dtype SHC_BF16 or SHC_F32; Cout <= 256.
  */
 size_t shc_sparse_linear_backward_workspace(int64_t n_rows, int32_t Cin, int32_t Cout,
                                             int32_t dtype);
@@ -448,19 +448,19 @@ int shc_build_slot_pairs(const int32_t* table, int64_t n_rows, int32_t K, int32_
  *   db = sum over rows of dZ,
  *   dS[r] = sum over (i, j) with table[j][i] = r of dZ[i] W[j]^T.
  *
- *   S [n_rows][Cin], W [K][Cin][Cout], Y, dY [n_rows][Cout]: bf16;
+ *   S [n_rows][Cin], W [K][Cin][Cout], Y, dY [n_rows][Cout]: all of `dtype`;
  *   table [K][n_rows]: shc_build_neighbor_table of the active set;
  *   pairs, pair_ptr: shc_build_slot_pairs of the same table, or both NULL
  *     (then built inside the call, in the workspace);
  *   table_t, row_slots: shc_build_transposed_table of the same active set;
  *   slot_of, Kt: shc_transpose_neighbors of the mesh;
- *   dS [n_rows][Cin] bf16 out, dW [K][Cin][Cout] fp32 out, db [Cout] fp32
+ *   dS [n_rows][Cin] `dtype` out, dW [K][Cin][Cout] fp32 out, db [Cout] fp32
  *   out; each may be NULL (table_t, row_slots and slot_of are then only read
  *   when dS is requested).
  *   ws: device workspace of shc_sparse_neighbor_conv_backward_workspace bytes.
  * dS sums its terms in ascending virtual slot order in fp32 and rounds once;
- * dW and db as in shc_sparse_linear_backward.  bf16 only; K <= 32;
- * Cout <= 256.
+ * dW and db as in shc_sparse_linear_backward.  dtype SHC_BF16 or SHC_F32;
+ * K <= 32; Cout <= 256.
  */
 size_t shc_sparse_neighbor_conv_backward_workspace(int64_t n_rows, int32_t K, int32_t Cin,
                                                    int32_t Cout, int32_t dtype);

@@ -616,16 +616,16 @@ static int check_backward(const void* S, const void* W, const void* Y, const voi
                           const void* ws, size_t ws_bytes, size_t need) {
   SHC_TRY(check_rows(n_rows));
   SHC_TRY(check_dtype(dtype));
-  if (dtype != SHC_BF16) return fail(SHC_ERR_UNSUPPORTED, "the backward takes bf16 tensors");
   SHC_TRY(check_channels("Cin", Cin));
   SHC_TRY(check_channels("Cout", Cout));
   if (Cout > 256) return fail(SHC_ERR_UNSUPPORTED, "Cout = %d above 256", Cout);
   if (act != SHC_ACT_NONE && act != SHC_ACT_RELU)
     return fail(SHC_ERR_UNSUPPORTED, "unknown activation code %d", act);
-  if (n_rows * (int64_t)(Cin > Cout ? Cin : Cout) * 2 > INT32_MAX)
+  const int64_t e = dtype == SHC_BF16 ? 2 : 4;
+  if (n_rows * (int64_t)(Cin > Cout ? Cin : Cout) * e > INT32_MAX)
     return fail(SHC_ERR_UNSUPPORTED, "a feature tensor of %lld rows exceeds 2 GiB",
                 (long long)n_rows);
-  if (dS != nullptr && !shc::backward_dgrad_supported(Kw, Cin, Cout))
+  if (dS != nullptr && !shc::backward_dgrad_supported(Kw, Cin, Cout, dtype == SHC_BF16))
     return fail(SHC_ERR_UNSUPPORTED, "input gradient for K = %d, Cin = %d, Cout = %d does not fit",
                 Kw, Cin, Cout);
   SHC_OPT_PTR(dS, "dS");
@@ -645,9 +645,9 @@ static int check_backward(const void* S, const void* W, const void* Y, const voi
 
 size_t shc_sparse_linear_backward_workspace(int64_t n_rows, int32_t Cin, int32_t Cout,
                                             int32_t dtype) {
-  if (n_rows < 0 || Cin <= 0 || Cout <= 0 || dtype != SHC_BF16) return 0;
+  if (n_rows < 0 || Cin <= 0 || Cout <= 0 || (dtype != SHC_BF16 && dtype != SHC_F32)) return 0;
   shc::BwdPlan pl;
-  shc::backward_plan(n_rows, 1, Cin, Cout, 1, 0, &pl);
+  shc::backward_plan(n_rows, 1, Cin, Cout, dtype == SHC_BF16, 0, &pl);
   return pl.total;
 }
 
@@ -659,17 +659,18 @@ int shc_sparse_linear_backward(const void* S, const void* W, const void* Y, cons
   SHC_TRY(check_backward(S, W, Y, dY, n_rows, 1, Cin, Cout, dtype, act, dS, dW, db, ws, ws_bytes,
                          shc_sparse_linear_backward_workspace(n_rows, Cin, Cout, dtype)));
   return hip_status(shc::launch_layer_backward(0, S, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                               nullptr, W, Y, dY, n_rows, 1, Cin, Cout, act, dS,
-                                               dW, db, ws, stream),
+                                               nullptr, W, Y, dY, n_rows, 1, Cin, Cout,
+                                               dtype == SHC_BF16, act, dS, dW, db, ws, stream),
                     "sparse_linear_backward launch");
 }
 
 size_t shc_sparse_neighbor_conv_backward_workspace(int64_t n_rows, int32_t K, int32_t Cin,
                                                    int32_t Cout, int32_t dtype) {
-  if (n_rows < 0 || K <= 0 || K > kMaxSlots || Cin <= 0 || Cout <= 0 || dtype != SHC_BF16)
+  if (n_rows < 0 || K <= 0 || K > kMaxSlots || Cin <= 0 || Cout <= 0 ||
+      (dtype != SHC_BF16 && dtype != SHC_F32))
     return 0;
   shc::BwdPlan pl;
-  shc::backward_plan(n_rows, K, Cin, Cout, 1, 1, &pl);
+  shc::backward_plan(n_rows, K, Cin, Cout, dtype == SHC_BF16, 1, &pl);
   return pl.total;
 }
 
@@ -727,8 +728,8 @@ int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table, const
     SHC_PTR(slot_of, "slot_of");
   }
   return hip_status(shc::launch_layer_backward(1, S, table, pairs, pair_ptr, table_t, row_slots,
-                                               slot_of, W, Y, dY, n_rows, K, Cin, Cout, act, dS,
-                                               dW, db, ws, stream),
+                                               slot_of, W, Y, dY, n_rows, K, Cin, Cout,
+                                               dtype == SHC_BF16, act, dS, dW, db, ws, stream),
                     "sparse_neighbor_conv_backward launch");
 }
 

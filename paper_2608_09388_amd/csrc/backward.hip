@@ -452,6 +452,136 @@ __global__ __launch_bounds__(kThreads) void wgrad_tile_kernel(
       }
 }
 
+// fp32 version of the partial tiles: T = 64, R = 32 rows per step, one LDS
+// stage (rows padded by 64 bytes, so the four row groups of a read sit in
+// different banks), the next step in registers.  MFMA 16x16x4 (fp32): lane
+// (g, i) gives row g of the k-step at channel i on both sides; the output
+// layout is that of the bf16 tiles.
+template <int T, int R>
+__global__ __launch_bounds__(kThreads) void wgrad_tile_f32_kernel(
+    const float* __restrict__ S, const float* __restrict__ dZ, const int32_t* __restrict__ table,
+    const int2* __restrict__ pairs, const int32_t* __restrict__ row_ptr, int32_t K, int64_t n,
+    int32_t L, int32_t Cin, int32_t Cout, float* __restrict__ part) {
+  constexpr int NB = T / 32;
+  constexpr int ROW = T * 4 + 64;  // bytes
+  constexpr int VPR = T * 4 / 16;
+  constexpr int LOADS = 2 * R * VPR / kThreads;
+  constexpr int kMaxL = 512;
+  __shared__ __attribute__((aligned(16))) unsigned char stage[2][R * ROW];
+  __shared__ int32_t ia[kMaxL], ib[kMaxL];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, l16 = lane & 15;
+  const int wa = wave >> 1, wb = wave & 1;
+  const int tA = (Cin + T - 1) / T, tB = (Cout + T - 1) / T;
+  const int tiles = tA * tB;
+  const int w = blockIdx.x / tiles, t = blockIdx.x - w * tiles;
+  const int ta = t / tB, tb = t - ta * tB;
+  int j = 0;
+  int64_t t0, t1;
+  if (pairs != nullptr) {
+    int c = 0, wc = -1;
+    for (j = 0; j < K; ++j) {
+      const int nch = (row_ptr[j + 1] - row_ptr[j] + L - 1) / L;
+      if (w < c + nch) {
+        wc = w - c;
+        break;
+      }
+      c += nch;
+    }
+    if (wc < 0) return;  // past the last chunk
+    const int64_t base = row_ptr[j] + (int64_t)wc * L;
+    t0 = base;
+    t1 = min(base + L, (int64_t)row_ptr[j + 1]);
+  } else {
+    t0 = (int64_t)w * L;
+    if (t0 >= n) return;
+    t1 = min(t0 + L, n);
+  }
+  const int rows = (int)(t1 - t0);
+  for (int q = tid; q < rows; q += kThreads) {
+    if (pairs != nullptr) {
+      const int2 pq = pairs[t0 + q];
+      ia[q] = table[(int64_t)j * n + pq.y];
+      ib[q] = pq.y;
+    } else {
+      ia[q] = (int32_t)(t0 + q);
+      ib[q] = (int32_t)(t0 + q);
+    }
+  }
+  __syncthreads();
+  const int steps = (rows + R - 1) / R;
+  auto load = [&](int step, i32x4* v) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int e = tid + u * kThreads;
+      const int op = e / (R * VPR);
+      const int rr = (e / VPR) % R;
+      const int q = e % VPR;
+      const int local = step * R + rr;
+      const int col = (op == 0 ? ta : tb) * T + q * 4;
+      const int C = op == 0 ? Cin : Cout;
+      v[u] = i32x4{0, 0, 0, 0};
+      if (local < rows && col < C) {
+        const int32_t row = op == 0 ? ia[local] : ib[local];
+        if (row >= 0)
+          v[u] = *reinterpret_cast<const i32x4*>((op == 0 ? S : dZ) + (int64_t)row * C + col);
+      }
+    }
+  };
+  auto store = [&](const i32x4* v) {
+#pragma unroll
+    for (int u = 0; u < LOADS; ++u) {
+      const int e = tid + u * kThreads;
+      const int op = e / (R * VPR);
+      const int rr = (e / VPR) % R;
+      const int q = e % VPR;
+      *reinterpret_cast<i32x4*>(&stage[op][rr * ROW + q * 16]) = v[u];
+    }
+  };
+  f32x4 acc[NB][NB];
+#pragma unroll
+  for (int x = 0; x < NB; ++x)
+#pragma unroll
+    for (int y = 0; y < NB; ++y) acc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+  i32x4 v[LOADS];
+  if (steps > 0) load(0, v);
+  for (int st = 0; st < steps; ++st) {
+    store(v);
+    __syncthreads();
+    if (st + 1 < steps) load(st + 1, v);
+#pragma unroll
+    for (int k0 = 0; k0 < R; k0 += 4) {
+      float fa[NB], fb[NB];
+#pragma unroll
+      for (int x = 0; x < NB; ++x)
+        fa[x] = *reinterpret_cast<const float*>(
+            &stage[0][(k0 + g) * ROW + ((wa * NB + x) * 16 + l16) * 4]);
+#pragma unroll
+      for (int y = 0; y < NB; ++y)
+        fb[y] = *reinterpret_cast<const float*>(
+            &stage[1][(k0 + g) * ROW + ((wb * NB + y) * 16 + l16) * 4]);
+#pragma unroll
+      for (int x = 0; x < NB; ++x)
+#pragma unroll
+        for (int y = 0; y < NB; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x4f32(fa[x], fb[y], acc[x][y], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+  float* out = part + ((int64_t)w * tiles + t) * T * T;
+#pragma unroll
+  for (int x = 0; x < NB; ++x)
+#pragma unroll
+    for (int y = 0; y < NB; ++y)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int a = (wa * NB + x) * 16 + 4 * g + rr;
+        const int b = (wb * NB + y) * 16 + l16;
+        out[a * T + b] = acc[x][y][rr];
+      }
+}
+
 // dW[j][c][o]: sum of the partial tiles of slot j's chunks in fp64.
 // Workgroup (slot j and tile, 32 consecutive entries) of 8 chunk groups:
 // group y sums chunks y, y + 8, ... of the slot in order, then the 8 group
@@ -515,21 +645,23 @@ __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __r
 // block it lands in (absent slots add exact zeros), so the result does not
 // depend on the sort.  Without a transposed table (linear layer) every row is
 // its own source through one slot, unsorted.
-template <int WS, int KSM, bool TBL>
+template <int WS, int KSM, bool TBL, bool BF16>
 __global__ __launch_bounds__(kDgradThreads) void dgrad_kernel(
-    const __bf16* __restrict__ dZ, const __bf16* __restrict__ W,
+    const unsigned char* __restrict__ dZ, const unsigned char* __restrict__ W,
     const int32_t* __restrict__ table_t, const uint64_t* __restrict__ row_slots,
     const int32_t* __restrict__ slot_of, int64_t n, int32_t K, int32_t Cin, int32_t Cout,
-    int32_t R, __bf16* __restrict__ dS) {
+    int32_t R, unsigned char* __restrict__ dS) {
+  constexpr int E = BF16 ? 2 : 4;          // bytes per element
+  constexpr int KW = BF16 ? 32 : 16;       // reduction entries per k-step (64 bytes)
   constexpr int NCB = WS / 16;
-  constexpr int DA = KSM <= 4 ? 4 : 2;  // jobs with data loads in flight
+  constexpr int DA = KSM <= 4 ? 4 : (KSM <= 8 ? 2 : 1);  // jobs with data loads in flight
   constexpr int D = 2 * DA;              // ring: as many again with only the source loaded
   constexpr int kWaves = kDgradThreads / 64;
   constexpr int RPT = kDgradMaxRows / kDgradThreads;  // rows per thread in the sort
   constexpr int NBK = kMaxVirtualSlots + 1;            // sort buckets
-  constexpr int WROW = WS * 2 + 16;
+  constexpr int WROW = WS * E + 16;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int KS = (Cout + 31) / 32;
+  const int KS = (Cout + KW - 1) / KW;
   unsigned char* wl = smem;                                     // [K][KS][NCB][64][16]
   unsigned char* scratch = smem + (size_t)K * KS * NCB * 1024;  // [waves][16][WROW]
   uint64_t* blkmask = reinterpret_cast<uint64_t*>(scratch + kWaves * 16 * WROW);  // [R / 16]
@@ -560,7 +692,8 @@ __global__ __launch_bounds__(kDgradThreads) void dgrad_kernel(
     for (int q = tid; q < NBK; q += kDgradThreads) hist[q] = 0;
     for (int b = tid; b < kDgradMaxRows / 16; b += kDgradThreads) blkmask[b] = 0ull;
   }
-  // weights: lane (g, l16) of fragment (j, ks, cb) holds W[j][n0 + 16 cb + l16][32 ks + 8 g .. + 7];
+  // weights: lane (g, l16) of fragment (j, ks, cb) holds the 16 bytes
+  // W[j][n0 + 16 cb + l16][KW ks + (KW / 4) g ...] (8 bf16 or 4 fp32 entries);
   // kWBatch vectors per thread in flight at a time
   const int nfrag = K * KS * NCB * 64;
   for (int f0 = 0; f0 < nfrag; f0 += kWBatch * kDgradThreads) {
@@ -574,9 +707,9 @@ __global__ __launch_bounds__(kDgradThreads) void dgrad_kernel(
       const int ks = (fr / NCB) % KS;
       const int j = fr / (NCB * KS);
       const int c = n0 + cb * 16 + (ln & 15);
-      const int o = ks * 32 + 8 * (ln >> 4);
+      const int o = ks * KW + (KW / 4) * (ln >> 4);
       const bool ok = f < nfrag && c < Cin && o < Cout;
-      v[u] = *reinterpret_cast<const i32x4*>(W + (ok ? ((int64_t)j * Cin + c) * Cout + o : 0));
+      v[u] = *reinterpret_cast<const i32x4*>(W + (ok ? (((int64_t)j * Cin + c) * Cout + o) * E : 0));
       if (!ok) v[u] = i32x4{0, 0, 0, 0};
     }
 #pragma unroll
@@ -656,8 +789,8 @@ __global__ __launch_bounds__(kDgradThreads) void dgrad_kernel(
   }
 
   const __amdgpu_buffer_rsrc_t z_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<__bf16*>(dZ), (short)0, (int)(n * Cout * 2), kBufferWord3);
-  const uint32_t row_bytes = (uint32_t)Cout * 2u;
+      const_cast<unsigned char*>(dZ), (short)0, (int)(n * Cout * E), kBufferWord3);
+  const uint32_t row_bytes = (uint32_t)Cout * E;
   unsigned char* my = scratch + wave * 16 * WROW;
   // the row of the workgroup at sorted position p
   auto row_at = [&](int p) -> int { return TBL ? perm[p] : p; };
@@ -704,8 +837,8 @@ __global__ __launch_bounds__(kDgradThreads) void dgrad_kernel(
     for (int ks = 0; ks < KSM; ++ks)
       f.v[ks] = __builtin_bit_cast(
           i32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                     z_rsrc, (ks < KS && ks * 32 + 8 * g < Cout) ? off + (uint32_t)ks * 64u
-                                                                 : kOutOfRange,
+                     z_rsrc, (ks < KS && ks * KW + (KW / 4) * g < Cout) ? off + (uint32_t)ks * 64u
+                                                                         : kOutOfRange,
                      0, 0));
   };
   f32x4 acc[NCB];
@@ -717,12 +850,23 @@ __global__ __launch_bounds__(kDgradThreads) void dgrad_kernel(
 #pragma unroll
     for (int ks = 0; ks < KSM; ++ks) {
       if (ks < KS) {
-        const bf16x8 af = __builtin_bit_cast(bf16x8, f.v[ks]);
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) {
-          const bf16x8 bfr = *reinterpret_cast<const bf16x8*>(
+          const i32x4 bw = *reinterpret_cast<const i32x4*>(
               wl + ((size_t)((j * KS + ks) * NCB + cb) * 64 + lane) * 16);
-          acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bfr, acc[cb], 0, 0, 0);
+          if constexpr (BF16) {
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, f.v[ks]),
+                                                             __builtin_bit_cast(bf16x8, bw),
+                                                             acc[cb], 0, 0, 0);
+          } else {
+            // lane group g holds reduction entries 4 g .. 4 g + 3 of the
+            // k-step on both sides; MFMA s contracts component s
+#pragma unroll
+            for (int s2 = 0; s2 < 4; ++s2)
+              acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__int_as_float(f.v[ks][s2]),
+                                                             __int_as_float(bw[s2]), acc[cb], 0,
+                                                             0, 0);
+          }
         }
       }
     }
@@ -730,27 +874,33 @@ __global__ __launch_bounds__(kDgradThreads) void dgrad_kernel(
   auto epilogue = [&](int blk) {
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) {
-      // hardware round-to-nearest-even conversion, two rows per instruction
+      if constexpr (BF16) {
+        // hardware round-to-nearest-even conversion, two rows per instruction
 #pragma unroll
-      for (int q = 0; q < 4; q += 2) {
-        const bf16x2 h = __builtin_convertvector(f32x2{acc[cb][q], acc[cb][q + 1]}, bf16x2);
-        *reinterpret_cast<__bf16*>(my + (4 * g + q) * WROW + (cb * 16 + l16) * 2) = h[0];
-        *reinterpret_cast<__bf16*>(my + (4 * g + q + 1) * WROW + (cb * 16 + l16) * 2) = h[1];
+        for (int q = 0; q < 4; q += 2) {
+          const bf16x2 h = __builtin_convertvector(f32x2{acc[cb][q], acc[cb][q + 1]}, bf16x2);
+          *reinterpret_cast<__bf16*>(my + (4 * g + q) * WROW + (cb * 16 + l16) * 2) = h[0];
+          *reinterpret_cast<__bf16*>(my + (4 * g + q + 1) * WROW + (cb * 16 + l16) * 2) = h[1];
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<float*>(my + (4 * g + q) * WROW + (cb * 16 + l16) * 4) = acc[cb][q];
       }
       acc[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    constexpr int VPRW = WS * 2 / 16;
+    constexpr int VPRW = WS * E / 16;
 #pragma unroll
     for (int idx0 = 0; idx0 < 16 * VPRW; idx0 += 64) {
       const int idx = idx0 + lane;
       const int rr = idx / VPRW, q = idx % VPRW;
-      const int c = n0 + q * 8;
+      const int c = n0 + q * (16 / E);
       if (idx < 16 * VPRW && blk * 16 + rr < nrows && c < Cin) {
         const int64_t row = row0 + row_at(blk * 16 + rr);
-        *reinterpret_cast<i32x4*>(dS + row * Cin + c) =
+        *reinterpret_cast<i32x4*>(dS + (row * Cin + c) * E) =
             *reinterpret_cast<const i32x4*>(my + rr * WROW + q * 16);
       }
     }
@@ -802,27 +952,28 @@ unsigned grid_for(int64_t n) { return (unsigned)std::max<int64_t>(1, (n + kThrea
 // column slice of the dgrad kernel: the widest of 128 / 64 / 32 / 16 input
 // channels (not above Cin) whose weight fragments, scratch and sort arrays
 // fit in LDS (a workgroup of eight wavefronts keeps two per SIMD)
-size_t dgrad_lds(int ws, int32_t Kw, int32_t Cout) {
-  const int KS = (Cout + 31) / 32;
-  return (size_t)Kw * KS * (ws / 16) * 1024 + (kDgradThreads / 64) * 16 * (ws * 2 + 16) +
+size_t dgrad_lds(int ws, int32_t Kw, int32_t Cout, int e) {
+  const int kw = e == 2 ? 32 : 16;
+  const int KS = (Cout + kw - 1) / kw;
+  return (size_t)Kw * KS * (ws / 16) * 1024 + (kDgradThreads / 64) * 16 * (ws * e + 16) +
          kDgradMaxRows / 16 * sizeof(uint64_t) + kDgradMaxRows * sizeof(int32_t) +
          (size_t)(kMaxVirtualSlots + 1) * sizeof(int32_t);
 }
 
-int dgrad_ws(int32_t Kw, int32_t Cin, int32_t Cout) {
+int dgrad_ws(int32_t Kw, int32_t Cin, int32_t Cout, int e) {
   for (int ws = 128; ws >= 16; ws /= 2) {
     if (ws > Cin && ws > 16) continue;
-    if (dgrad_lds(ws, Kw, Cout) <= (size_t)kDgradLds) return ws;
+    if (dgrad_lds(ws, Kw, Cout, e) <= (size_t)kDgradLds) return ws;
   }
   return 0;
 }
 
-template <int WS, int KSM, bool TBL>
+template <int WS, int KSM, bool TBL, bool BF16>
 hipError_t launch_dgrad_ws(const void* dZ, const void* W, const int32_t* table_t,
                            const uint64_t* row_slots, const int32_t* slot_of, int64_t n,
                            int32_t Kw, int32_t Cin, int32_t Cout, void* dS, hipStream_t stream) {
-  auto kern = dgrad_kernel<WS, KSM, TBL>;
-  const size_t lds = dgrad_lds(WS, Kw, Cout);
+  auto kern = dgrad_kernel<WS, KSM, TBL, BF16>;
+  const size_t lds = dgrad_lds(WS, Kw, Cout, BF16 ? 2 : 4);
   const hipError_t a = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (a != hipSuccess) return a;
@@ -835,39 +986,47 @@ hipError_t launch_dgrad_ws(const void* dZ, const void* W, const int32_t* table_t
   int64_t R = (n + groups - 1) / groups;
   R = std::min<int64_t>(kDgradMaxRows, std::max<int64_t>(64, (R + 15) / 16 * 16));
   const unsigned gx = (unsigned)((n + R - 1) / R);
-  hipLaunchKernelGGL(kern, dim3(gx, (unsigned)slices), dim3(kDgradThreads), lds,
-                     stream, static_cast<const __bf16*>(dZ), static_cast<const __bf16*>(W),
+  hipLaunchKernelGGL(kern, dim3(gx, (unsigned)slices), dim3(kDgradThreads), lds, stream,
+                     static_cast<const unsigned char*>(dZ), static_cast<const unsigned char*>(W),
                      table_t, row_slots, slot_of, n, Kw, Cin, Cout, (int32_t)R,
-                     static_cast<__bf16*>(dS));
+                     static_cast<unsigned char*>(dS));
   return hipGetLastError();
 }
 
-template <int WS>
+template <int WS, bool BF16>
 hipError_t launch_dgrad_k(const void* dZ, const void* W, const int32_t* table_t,
                           const uint64_t* row_slots, const int32_t* slot_of, int64_t n,
                           int32_t Kw, int32_t Cin, int32_t Cout, void* dS, hipStream_t stream) {
   const bool tbl = table_t != nullptr;
-  if (Cout <= 128)
-    return tbl ? launch_dgrad_ws<WS, 4, true>(dZ, W, table_t, row_slots, slot_of, n, Kw, Cin,
-                                              Cout, dS, stream)
-               : launch_dgrad_ws<WS, 4, false>(dZ, W, table_t, row_slots, slot_of, n, Kw, Cin,
-                                               Cout, dS, stream);
-  return tbl ? launch_dgrad_ws<WS, 8, true>(dZ, W, table_t, row_slots, slot_of, n, Kw, Cin, Cout,
-                                            dS, stream)
-             : launch_dgrad_ws<WS, 8, false>(dZ, W, table_t, row_slots, slot_of, n, Kw, Cin, Cout,
-                                             dS, stream);
+  const int ks = BF16 ? (Cout + 31) / 32 : (Cout + 15) / 16;  // k-steps: at most 8 / 16
+  if (ks <= 4)
+    return tbl ? launch_dgrad_ws<WS, 4, true, BF16>(dZ, W, table_t, row_slots, slot_of, n, Kw,
+                                                    Cin, Cout, dS, stream)
+               : launch_dgrad_ws<WS, 4, false, BF16>(dZ, W, table_t, row_slots, slot_of, n, Kw,
+                                                     Cin, Cout, dS, stream);
+  if (ks <= 8)
+    return tbl ? launch_dgrad_ws<WS, 8, true, BF16>(dZ, W, table_t, row_slots, slot_of, n, Kw,
+                                                    Cin, Cout, dS, stream)
+               : launch_dgrad_ws<WS, 8, false, BF16>(dZ, W, table_t, row_slots, slot_of, n, Kw,
+                                                     Cin, Cout, dS, stream);
+  if constexpr (!BF16)
+    return tbl ? launch_dgrad_ws<WS, 16, true, false>(dZ, W, table_t, row_slots, slot_of, n, Kw,
+                                                      Cin, Cout, dS, stream)
+               : launch_dgrad_ws<WS, 16, false, false>(dZ, W, table_t, row_slots, slot_of, n,
+                                                       Kw, Cin, Cout, dS, stream);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-int backward_dgrad_supported(int32_t Kw, int32_t Cin, int32_t Cout) {
-  return Cout <= 256 && Kw <= kMaxSlotsBwd && dgrad_ws(Kw, Cin, Cout) > 0;
+int backward_dgrad_supported(int32_t Kw, int32_t Cin, int32_t Cout, int is_bf16) {
+  return Cout <= 256 && Kw <= kMaxSlotsBwd && dgrad_ws(Kw, Cin, Cout, is_bf16 ? 2 : 4) > 0;
 }
 
 void backward_plan(int64_t n, int32_t K, int32_t Cin, int32_t Cout, int is_bf16, int conv,
                    BwdPlan* p) {
   const int e = is_bf16 ? 2 : 4;
-  p->T = (Cin % 128 == 0 && Cout % 128 == 0) ? 128 : 64;
+  p->T = (is_bf16 && Cin % 128 == 0 && Cout % 128 == 0) ? 128 : 64;
   p->tiles = ((Cin + p->T - 1) / p->T) * ((Cout + p->T - 1) / p->T);
   const int64_t per = conv ? (int64_t)K * ((n + 255) / 256) : (n + 255) / 256;
   p->L = per > 8192 ? 512 : 256;
@@ -974,10 +1133,10 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
                                  const int32_t* table_t, const uint64_t* row_slots,
                                  const int32_t* slot_of, const void* W, const void* Y,
                                  const void* dY, int64_t n, int32_t K, int32_t Cin, int32_t Cout,
-                                 int act, void* dS, float* dW, float* db, void* ws,
+                                 int is_bf16, int act, void* dS, float* dW, float* db, void* ws,
                                  hipStream_t stream) {
   BwdPlan pl;
-  backward_plan(n, K, Cin, Cout, 1, conv, &pl);
+  backward_plan(n, K, Cin, Cout, is_bf16, conv, &pl);
   unsigned char* w = static_cast<unsigned char*>(ws);
   const int Kw = conv ? K : 1;
   if (n == 0) {  // no rows: zero weight and bias gradients
@@ -994,9 +1153,14 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
   if (act || db != nullptr) {
     float* colpart = reinterpret_cast<float*>(w + pl.off_colpart);
     void* dz_out = act ? static_cast<void*>(w + pl.off_dz) : nullptr;
-    hipLaunchKernelGGL(relu_bwd_kernel<true>, dim3(pl.splits), dim3(kThreads), 0, stream,
-                       static_cast<const i32x4*>(dY), static_cast<const i32x4*>(Y), n, Cout, act,
-                       pl.rps, static_cast<i32x4*>(dz_out), colpart);
+    if (is_bf16)
+      hipLaunchKernelGGL(relu_bwd_kernel<true>, dim3(pl.splits), dim3(kThreads), 0, stream,
+                         static_cast<const i32x4*>(dY), static_cast<const i32x4*>(Y), n, Cout,
+                         act, pl.rps, static_cast<i32x4*>(dz_out), colpart);
+    else
+      hipLaunchKernelGGL(relu_bwd_kernel<false>, dim3(pl.splits), dim3(kThreads), 0, stream,
+                         static_cast<const i32x4*>(dY), static_cast<const i32x4*>(Y), n, Cout,
+                         act, pl.rps, static_cast<i32x4*>(dz_out), colpart);
     if (act) dZ = dz_out;
     if (db != nullptr)
       hipLaunchKernelGGL(colsum_kernel, dim3((Cout + 7) / 8), dim3(kThreads), 0, stream, colpart,
@@ -1023,7 +1187,11 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
       }
     }
     const unsigned gt = (unsigned)(pl.max_chunks * pl.tiles);
-    if (pl.T == 128)
+    if (!is_bf16)
+      hipLaunchKernelGGL((wgrad_tile_f32_kernel<64, 32>), dim3(gt), dim3(kThreads), 0, stream,
+                         static_cast<const float*>(S), static_cast<const float*>(dZ), table, pr,
+                         rp, Kw, n, pl.L, Cin, Cout, part);
+    else if (pl.T == 128)
       hipLaunchKernelGGL((wgrad_tile_kernel<128, kWgradRows>), dim3(gt), dim3(kThreads), 0, stream,
                          static_cast<const __bf16*>(S), static_cast<const __bf16*>(dZ), table, pr,
                          rp, Kw, n, pl.L, Cin, Cout, part);
@@ -1045,15 +1213,24 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
   }
   // input gradient
   if (dS != nullptr) {
-    const int wsl = dgrad_ws(Kw, Cin, Cout);
+    const int wsl = dgrad_ws(Kw, Cin, Cout, is_bf16 ? 2 : 4);
     const int32_t* tt = conv ? table_t : nullptr;
     const uint64_t* rs = conv ? row_slots : nullptr;
     const int32_t* so = conv ? slot_of : nullptr;
-    switch (wsl) {
-      case 128: err = launch_dgrad_k<128>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
-      case 64: err = launch_dgrad_k<64>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
-      case 32: err = launch_dgrad_k<32>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
-      default: err = launch_dgrad_k<16>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+    if (is_bf16) {
+      switch (wsl) {
+        case 128: err = launch_dgrad_k<128, true>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+        case 64: err = launch_dgrad_k<64, true>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+        case 32: err = launch_dgrad_k<32, true>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+        default: err = launch_dgrad_k<16, true>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+      }
+    } else {
+      switch (wsl) {
+        case 128: err = launch_dgrad_k<128, false>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+        case 64: err = launch_dgrad_k<64, false>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+        case 32: err = launch_dgrad_k<32, false>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+        default: err = launch_dgrad_k<16, false>(dZ, W, tt, rs, so, n, Kw, Cin, Cout, dS, stream); break;
+      }
     }
     if (err != hipSuccess) return err;
   }

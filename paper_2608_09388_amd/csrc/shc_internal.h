@@ -71,7 +71,7 @@ struct BwdPlan {
 };
 void backward_plan(int64_t n, int32_t K, int32_t Cin, int32_t Cout, int is_bf16, int conv,
                    BwdPlan* p);
-int backward_dgrad_supported(int32_t Kw, int32_t Cin, int32_t Cout);
+int backward_dgrad_supported(int32_t Kw, int32_t Cin, int32_t Cout, int is_bf16);
 size_t transpose_neighbors_ws_bytes(int32_t V, int32_t K);
 hipError_t launch_transpose_neighbors(const int32_t* nbr, int32_t V, int32_t K, int32_t* nbr_t,
                                       int32_t* slot_of, int32_t* off_dev, void* ws,
@@ -88,7 +88,7 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
                                  const int32_t* table_t, const uint64_t* row_slots,
                                  const int32_t* slot_of, const void* W, const void* Y,
                                  const void* dY, int64_t n, int32_t K, int32_t Cin, int32_t Cout,
-                                 int act, void* dS, float* dW, float* db, void* ws,
+                                 int is_bf16, int act, void* dS, float* dW, float* db, void* ws,
                                  hipStream_t stream);
 hipError_t launch_clear_inactive(const int32_t* inv, int32_t B, int32_t V, int32_t row_bytes,
                                  void* D, hipStream_t stream);

@@ -191,7 +191,8 @@ def test_backward_validation(lib):
     assert tt(A, A, 10, 0, 100, A, 20, A, A, None) == -1
 
     assert lib.shc_sparse_linear_backward_workspace(1000, 128, 128, 1) > 0
-    assert lib.shc_sparse_linear_backward_workspace(1000, 128, 128, 0) == 0
+    assert lib.shc_sparse_linear_backward_workspace(1000, 128, 128, 0) > 0     # fp32
+    assert lib.shc_sparse_linear_backward_workspace(1000, 128, 128, 7) == 0
     need = lib.shc_sparse_linear_backward_workspace(1000, 128, 128, 1)
 
     def lin(S=A, W=A, Y=A, dY=A, n=1000, Cin=128, Cout=128, dt=1, act=1, dS=A, dW=A, db=A,
@@ -199,7 +200,7 @@ def test_backward_validation(lib):
         return lib.shc_sparse_linear_backward(S, W, Y, dY, n, Cin, Cout, dt, act, dS, dW, db, ws,
                                               nbytes, None)
 
-    assert lin(dt=0) == -4 and "bf16" in err(lib)
+    assert lin(dt=7) == -4 and "dtype" in err(lib)
     assert lin(Cin=24) == -4
     assert lin(Cout=512) == -4
     assert lin(act=7) == -4
@@ -222,7 +223,10 @@ def test_backward_validation(lib):
                                                      ws, nbytes, None)
 
     assert conv(K=0) == -1 and conv(K=33) == -4
-    assert conv(dt=0) == -4
+    assert conv(dt=7) == -4
+    # fp32 weight fragments of 9 slots x 256 outputs do not fit in LDS: refused up front
+    need_big = lib.shc_sparse_neighbor_conv_backward_workspace(1000, 9, 64, 256, 0)
+    assert conv(dt=0, Cin=64, Cout=256, nbytes=need_big) == -4 and "fit" in err(lib)
     assert conv(table=None) == -1                  # dW needs the neighbour-row table
     assert conv(table_t=None) == -1                # dS needs the transposed table
     assert conv(Kt=0) == -1 and conv(Kt=65) == -1

@@ -2,8 +2,8 @@
 
 Integer structures (transposed neighbour lists, transposed table) are checked
 bit-exactly against a numpy construction.  Gradients against the oracle's
-fp64 backward on the same bf16 inputs: dS (bf16) within 2e-2 of the abs-sum
-scale of its terms, dW and db (fp32) within 1e-5 of theirs.  The stored
+fp64 backward on the same inputs: dS within 2e-2 (bf16) or 1e-5 (fp32) of the
+abs-sum scale of its terms, dW and db (fp32) within 1e-5 of theirs.  The stored
 output Y that decides the ReLU's derivative is a seeded input on both sides.
 """
 import numpy as np
@@ -55,6 +55,14 @@ def bf16(a):
     return synth.as_dtype(np.asarray(a, np.float32), "bf16")[1]
 
 
+def exact(a, dtype):
+    """Values exactly representable in dtype ('bf16' or 'f32')."""
+    return synth.as_dtype(np.asarray(a, np.float32), dtype)[1]
+
+
+TDT = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+
 class ConvSetup:
     """Active set, neighbour-row table and transposed table on the GPU."""
 
@@ -78,30 +86,31 @@ class ConvSetup:
                                        self.nbr_t, self.Kt, self.table_t, self.row_slots)
 
 
-def conv_inputs(rng, n, K, Cin, Cout):
-    S = bf16(rng.standard_normal((n, Cin)))
-    W = bf16(rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin))
-    Y = bf16(np.maximum(rng.standard_normal((n, Cout)), 0.0))   # half exact zeros
-    dY = bf16(rng.standard_normal((n, Cout)))
+def conv_inputs(rng, n, K, Cin, Cout, dtype="bf16"):
+    S = exact(rng.standard_normal((n, Cin)), dtype)
+    W = exact(rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin), dtype)
+    Y = exact(np.maximum(rng.standard_normal((n, Cout)), 0.0), dtype)   # half exact zeros
+    dY = exact(rng.standard_normal((n, Cout)), dtype)
     return S, W, Y, dY
 
 
-def run_conv_backward(st, S, W, Y, dY, act, want=("dS", "dW", "db"), with_pairs=False):
+def run_conv_backward(st, S, W, Y, dY, act, want=("dS", "dW", "db"), with_pairs=False,
+                      dtype="bf16"):
     n, K = st.n, st.K
     Cin, Cout = W.shape[1], W.shape[2]
-    dS = torch.full((max(n, 1), Cin), float("nan"), dtype=torch.bfloat16, device="cuda")
+    dS = torch.full((max(n, 1), Cin), float("nan"), dtype=TDT[dtype], device="cuda")
     dW = torch.full((K, Cin, Cout), float("nan"), dtype=torch.float32, device="cuda")
     db = torch.full((Cout,), float("nan"), dtype=torch.float32, device="cuda")
-    Sd = up(S if n else np.zeros((1, Cin)), "bf16")
-    Yd = up(Y if n else np.zeros((1, Cout)), "bf16")
-    dYd = up(dY if n else np.zeros((1, Cout)), "bf16")
+    Sd = up(S if n else np.zeros((1, Cin)), dtype)
+    Yd = up(Y if n else np.zeros((1, Cout)), dtype)
+    dYd = up(dY if n else np.zeros((1, Cout)), dtype)
     pairs = pair_ptr = None
     if with_pairs:
         pairs = torch.full((max(K * n, 1), 2), -7, dtype=torch.int32, device="cuda")
         pair_ptr = torch.full((K + 1,), -7, dtype=torch.int32, device="cuda")
         shc.build_slot_pairs(st.table, n, K, pairs, pair_ptr)
     shc.sparse_neighbor_conv_backward(
-        Sd, st.table, st.table_t, st.row_slots, st.slot_of, st.Kt, up(W, "bf16"), Yd, dYd, n,
+        Sd, st.table, st.table_t, st.row_slots, st.slot_of, st.Kt, up(W, dtype), Yd, dYd, n,
         dS if "dS" in want else None, dW if "dW" in want else None,
         db if "db" in want else None, act=shc.SHC_ACT_RELU if act else shc.SHC_ACT_NONE,
         pairs=pairs, pair_ptr=pair_ptr)
@@ -109,13 +118,13 @@ def run_conv_backward(st, S, W, Y, dY, act, want=("dS", "dW", "db"), with_pairs=
     return down(dS)[:n], down(dW), down(db)
 
 
-def check_conv(st, nbr, S, W, Y, dY, act, with_pairs=False):
+def check_conv(st, nbr, S, W, Y, dY, act, with_pairs=False, dtype="bf16"):
     B, V = st.B, st.V
-    gS, gW, gb = run_conv_backward(st, S, W, Y, dY, act, with_pairs=with_pairs)
+    gS, gW, gb = run_conv_backward(st, S, W, Y, dY, act, with_pairs=with_pairs, dtype=dtype)
     rS, rW, rb = O.sparse_conv_backward(S, st.coords, B, V, nbr, W, dY, Y, act)
     dZ = O.relu_backward(dY, Y) if act else np.asarray(dY, np.float64)
     sS, sW, sb = O.sparse_conv_backward(np.abs(S), st.coords, B, V, nbr, np.abs(W), np.abs(dZ))
-    assert_scaled_close(gS, rS, sS, "bf16", "dS")
+    assert_scaled_close(gS, rS, sS, dtype, "dS")
     assert_scaled_close(gW, rW, sW, "f32", "dW")
     assert_scaled_close(gb, rb, sb, "f32", "db")
     return gS, gW, gb
@@ -175,43 +184,49 @@ def test_transposed_table_exact(dev):
 # ----------------------------------------------------------------------------
 
 
-@pytest.mark.parametrize("B,V,K,Cin,Cout,p,act", [
-    (3, 200, 9, 128, 128, 0.3, True),      # both tile edges at 128
-    (4, 150, 9, 64, 128, 0.5, True),
-    (2, 333, 5, 16, 64, 0.2, False),       # narrow input, no activation
-    (5, 97, 3, 48, 32, 0.7, True),         # ragged channel tiles
-    (2, 700, 9, 128, 256, 0.05, True),     # sparse, wide output
-    (1, 50, 9, 32, 16, 1.0, True),         # every vertex active
+@pytest.mark.parametrize("B,V,K,Cin,Cout,p,act,dtype", [
+    (3, 200, 9, 128, 128, 0.3, True, "bf16"),      # both tile edges at 128
+    (4, 150, 9, 64, 128, 0.5, True, "bf16"),
+    (2, 333, 5, 16, 64, 0.2, False, "bf16"),       # narrow input, no activation
+    (5, 97, 3, 48, 32, 0.7, True, "bf16"),         # ragged channel tiles
+    (2, 700, 9, 128, 256, 0.05, True, "bf16"),     # sparse, wide output
+    (1, 50, 9, 32, 16, 1.0, True, "bf16"),         # every vertex active
+    (3, 200, 9, 128, 128, 0.3, True, "f32"),
+    (2, 333, 5, 16, 64, 0.2, False, "f32"),
+    (2, 400, 9, 64, 192, 0.1, True, "f32"),        # 12 fp32 k-steps (the 16-step path)
+    (5, 97, 3, 48, 32, 0.7, True, "f32"),
 ])
-def test_conv_backward_vs_oracle(dev, B, V, K, Cin, Cout, p, act):
+def test_conv_backward_vs_oracle(dev, B, V, K, Cin, Cout, p, act, dtype):
     rng = np.random.default_rng(B * 1000 + V + K + Cin)
     nbr = rand_nbr(V, K, rng)
     mask = (rng.random((B, V)) < p).astype(np.uint8)
     st = ConvSetup(mask, nbr)
     assert st.n > 0
-    S, W, Y, dY = conv_inputs(rng, st.n, K, Cin, Cout)
+    S, W, Y, dY = conv_inputs(rng, st.n, K, Cin, Cout, dtype)
     # half of the cases take slot pairs built once beforehand, as a stack would
-    check_conv(st, nbr, S, W, Y, dY, act, with_pairs=(Cin + Cout) % 3 == 0)
+    check_conv(st, nbr, S, W, Y, dY, act, with_pairs=(Cin + Cout) % 3 == 0, dtype=dtype)
 
 
-@pytest.mark.parametrize("n,Cin,Cout,act", [(1000, 128, 128, True), (37, 64, 32, False),
-                                            (5000, 16, 256, True), (1, 128, 64, True)])
-def test_linear_backward_vs_oracle(dev, n, Cin, Cout, act):
+@pytest.mark.parametrize("n,Cin,Cout,act,dtype", [
+    (1000, 128, 128, True, "bf16"), (37, 64, 32, False, "bf16"), (5000, 16, 256, True, "bf16"),
+    (1, 128, 64, True, "bf16"), (1000, 128, 128, True, "f32"), (37, 64, 32, False, "f32"),
+    (3000, 48, 256, True, "f32")])
+def test_linear_backward_vs_oracle(dev, n, Cin, Cout, act, dtype):
     rng = np.random.default_rng(n + Cin + Cout)
-    S = bf16(rng.standard_normal((n, Cin)))
-    W = bf16(rng.standard_normal((Cin, Cout)) / np.sqrt(Cin))
-    Y = bf16(np.maximum(rng.standard_normal((n, Cout)), 0.0))
-    dY = bf16(rng.standard_normal((n, Cout)))
-    dS = torch.empty((n, Cin), dtype=torch.bfloat16, device="cuda")
+    S = exact(rng.standard_normal((n, Cin)), dtype)
+    W = exact(rng.standard_normal((Cin, Cout)) / np.sqrt(Cin), dtype)
+    Y = exact(np.maximum(rng.standard_normal((n, Cout)), 0.0), dtype)
+    dY = exact(rng.standard_normal((n, Cout)), dtype)
+    dS = torch.empty((n, Cin), dtype=TDT[dtype], device="cuda")
     dW = torch.empty((Cin, Cout), dtype=torch.float32, device="cuda")
     db = torch.empty(Cout, dtype=torch.float32, device="cuda")
-    shc.sparse_linear_backward(up(S, "bf16"), up(W, "bf16"), up(Y, "bf16"), up(dY, "bf16"), n,
+    shc.sparse_linear_backward(up(S, dtype), up(W, dtype), up(Y, dtype), up(dY, dtype), n,
                                dS, dW, db, act=shc.SHC_ACT_RELU if act else shc.SHC_ACT_NONE)
     torch.cuda.synchronize()
     rS, rW, rb = O.sparse_linear_backward(S, W, dY, Y, act)
     dZ = O.relu_backward(dY, Y) if act else np.asarray(dY, np.float64)
     sS, sW, sb = O.sparse_linear_backward(np.abs(S), np.abs(W), np.abs(dZ))
-    assert_scaled_close(down(dS), rS, sS, "bf16", "dS")
+    assert_scaled_close(down(dS), rS, sS, dtype, "dS")
     assert_scaled_close(down(dW), rW, sW, "f32", "dW")
     assert_scaled_close(down(db), rb, sb, "f32", "db")
 
