@@ -12,7 +12,7 @@ import torch
 from oracle import shc_oracle as O
 from paper_2608_09388_amd import binding as shc
 from paper_2608_09388_amd import synth
-from tests.gpu_util import (Compaction, assert_gn_close, assert_normwise_close,
+from tests.gpu_util import (TORCH, Compaction, assert_gn_close, assert_normwise_close,
                             assert_scaled_close, down, require_gpu, up)
 
 pytestmark = pytest.mark.gpu
@@ -678,6 +678,36 @@ def test_sparse_conv_full_oracle(dev, dtype, B, V, K, Cin, Cout, p, path):
         ref = O.sparse_conv(S, coords, B, V, nbr, W, b, act == shc.SHC_ACT_RELU)
         scale = O.sparse_conv_scale(S, coords, B, V, nbr, W, b)
         assert_scaled_close(got, ref, scale, dtype, f"conv K={K} {Cin}->{Cout} p={p}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind,K,Cin,Cout", [("linear", 1, 4096, 4096), ("linear", 1, 4096, 16),
+                                             ("conv", 9, 1024, 512), ("conv", 3, 4096, 64)])
+def test_max_channels(dev, dtype, kind, K, Cin, Cout):
+    """Channel counts at the library's limit (4096) and wide convs whose weight
+    slices do not fit in LDS, on a few dozen rows (a ragged last tile)."""
+    rng = np.random.default_rng(Cin + Cout + K)
+    B, V = 2, 40
+    m = (rng.random((B, V)) < 0.6).astype(np.uint8)
+    coords, inv, rp, n = O.compact(m)
+    S = synth.as_dtype(rng.standard_normal((n, Cin)).astype(np.float32), dtype)[1]
+    W = synth.as_dtype((rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin))
+                       .astype(np.float32), dtype)[1]
+    bias = rng.standard_normal(Cout).astype(np.float32)
+    if kind == "linear":
+        out = torch.full((n, Cout), float("nan"), dtype=TORCH[dtype], device=dev)
+        shc.sparse_linear(up(S, dtype), n, up(W[0], dtype), up(bias), out, shc.SHC_ACT_RELU)
+        torch.cuda.synchronize()
+        ref = O.relu(np.asarray(S, np.float64) @ W[0] + bias)
+        scale = np.abs(np.asarray(S, np.float64)) @ np.abs(W[0]) + np.abs(bias)
+        assert_scaled_close(down(out), ref, scale, dtype, f"linear {Cin}->{Cout}")
+    else:
+        nbr = rand_nbr(V, K, rng)
+        got, n2 = run_conv(dev, m, nbr, S, W, bias, dtype, shc.SHC_ACT_RELU, "table")
+        assert n2 == n
+        ref = O.sparse_conv(S, coords, B, V, nbr, W, bias, True)
+        scale = O.sparse_conv_scale(S, coords, B, V, nbr, W, bias)
+        assert_scaled_close(got, ref, scale, dtype, f"conv K={K} {Cin}->{Cout}")
 
 
 @pytest.mark.parametrize("path", ["direct", "table"])
