@@ -16,7 +16,7 @@
 //   * it builds the index lists of its whole row range with three rounds of
 //     loads (coordinates, neighbour vertices, inverse-map rows), each round
 //     fully in flight, while the weight slice streams in alongside;
-//   * the rows are counting-sorted (wavefront ballots, stable) by their first
+//   * the rows are bucketed (LDS histogram and cursors) by their first
 //     sparse slot -- a slot present in fewer than half of the rows.  16-row
 //     blocks then hold rows with only dense slots, or rows sharing a sparse
 //     slot, and each block carries the set of slots any of its rows has;
@@ -185,9 +185,9 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   load_w(0, wv);
 
   for (int q = tid; q < R / 16; q += kThreads) blkmask[q] = 0;
+  for (int q = tid; q < kBuckets; q += kThreads) bcnt[q] = 0;  // the sort's histogram
   for (int q = tid; q < E::kstep * WROWW / 16; q += kThreads)
     reinterpret_cast<i32x4*>(zrows)[q] = i32x4{0, 0, 0, 0};
-  const uint64_t lt = (1ull << lane) - 1ull;
 
   // ---- index lists, sorted by first sparse slot ---------------------------------
   // thread tid handles rows t = tid + rr * kThreads (rr < kRPT) of this workgroup
@@ -282,48 +282,35 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
     __syncthreads();
     const uint32_t dense = (uint32_t)scnt[kMaxSlots - 1];
     // buckets: 0 = dense slots only, 1 + j = first sparse slot j, K + 1 = past
-    // the end, -1 = no such row (t >= R)
-    int bkt[kRPT], rank[kRPT];
+    // the end, -1 = no such row (t >= R).  A histogram (LDS atomics), its
+    // exclusive scan, then a position per row from its bucket's cursor; the
+    // order inside a bucket is whatever the atomics give, which no result
+    // depends on (see the header).
+    int* hist = bcnt;  // [kBuckets]: counts, then cursors
+    int bkt[kRPT];
 #pragma unroll
     for (int rr = 0; rr < kRPT; ++rr) {
       const int t = tid + rr * kThreads;
       const uint32_t key = rmask[rr] & ~dense;
       bkt[rr] = t >= R ? -1 : (t >= nrows ? K + 1 : (key ? 1 + __builtin_ctz(key) : 0));
-      rank[rr] = 0;
-    }
-    for (int bk = 0; bk <= K + 1; ++bk) {
-#pragma unroll
-      for (int rr = 0; rr < kRPT; ++rr) {
-        const uint64_t bal = __ballot(bkt[rr] == bk);
-        if (bkt[rr] == bk) rank[rr] = __popcll(bal & lt);
-        if (lane == 0) bcnt[(bk * kRPT + rr) * kWaves + wave] = __popcll(bal);
-      }
+      if (bkt[rr] >= 0) atomicAdd(&hist[bkt[rr]], 1);
     }
     __syncthreads();
-    if (wave == 0) {  // exclusive scan in (bucket, rr, wave) order: stable in row order
-      const int ne = (K + 2) * kRPT * kWaves;
-      const int per = (ne + 63) / 64;
-      const int e0 = lane * per;
-      int local = 0;
-      for (int e = e0; e < e0 + per && e < ne; ++e) local += bcnt[e];
-      int inc = local;
+    if (wave == 0) {  // exclusive scan of the K + 2 <= 34 counts, one per lane
+      const int c = lane < K + 2 ? hist[lane] : 0;
+      int inc = c;
 #pragma unroll
       for (int d = 1; d < 64; d <<= 1) {
         const int y = __shfl_up(inc, d, 64);
         if (lane >= d) inc += y;
       }
-      int run = inc - local;
-      for (int e = e0; e < e0 + per && e < ne; ++e) {
-        const int n = bcnt[e];
-        bcnt[e] = run;
-        run += n;
-      }
+      if (lane < K + 2) hist[lane] = inc - c;
     }
     __syncthreads();
 #pragma unroll
     for (int rr = 0; rr < kRPT; ++rr) {
       if (bkt[rr] >= 0) {
-        const int pos = bcnt[(bkt[rr] * kRPT + rr) * kWaves + wave] + rank[rr];
+        const int pos = atomicAdd(&hist[bkt[rr]], 1);
         perm[pos] = tid + rr * kThreads;
 #pragma unroll
         for (int j = 0; j < KM; ++j)
