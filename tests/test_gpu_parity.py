@@ -491,8 +491,12 @@ def similarity_bound(Y, sim, N):
                        0.5 * (dF.diagonal()[None, :] / d[None, :])) + 1e-12)
 
 
+# pair tiles: (3, 128), (10, 64), (5, 192), (1, 64); 256-column blocks of the
+# concatenated outputs: (10, 128), (4, 256), (11, 128) with a padded last
+# block, (16, 64) with four masks per block, (7, 256)
 @pytest.mark.parametrize("K,N,C", [(3, 1000, 128), (10, 37, 64), (10, 20000, 128),
-                                   (4, 5000, 256), (5, 3000, 192), (1, 500, 64)])
+                                   (4, 5000, 256), (5, 3000, 192), (1, 500, 64),
+                                   (11, 3001, 128), (16, 2500, 64), (7, 777, 256)])
 def test_mask_scores_vs_oracle(dev, K, N, C):
     rng = np.random.default_rng(K * 1000 + C)
     Y = score_case(rng, K, N, C)
