@@ -31,6 +31,7 @@
 //     chunk order in fp64.
 // Every sum has a fixed order, so results repeat bit for bit.
 #include <algorithm>
+#include <mutex>
 
 #include "shc_internal.h"
 
@@ -974,9 +975,14 @@ hipError_t launch_dgrad_ws(const void* dZ, const void* W, const int32_t* table_t
                            int32_t Kw, int32_t Cin, int32_t Cout, void* dS, hipStream_t stream) {
   auto kern = dgrad_kernel<WS, KSM, TBL, BF16>;
   const size_t lds = dgrad_lds(WS, Kw, Cout, BF16 ? 2 : 4);
-  const hipError_t a = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (a != hipSuccess) return a;
+  // allow the large dynamic LDS allocation (up to kDgradLds); once per instantiation
+  static std::once_flag once;
+  static hipError_t attr_err = hipSuccess;
+  std::call_once(once, [&] {
+    attr_err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, kDgradLds);
+  });
+  if (attr_err != hipSuccess) return attr_err;
   const int slices = (Cin + WS - 1) / WS;
   // one wave of workgroups: as many row groups as the CUs hold workgroups
   // (all slices), whole 16-row blocks, 64 to kDgradMaxRows rows each; past
