@@ -79,6 +79,31 @@ def algorithmic_conv(w, coords, inv, n, e):
     return bytes_, flops, present / (n * K)
 
 
+def algorithmic_step_bytes(w, n, e, conv_bytes):
+    """Bytes each kernel of the step must move for N' = n active rows, from
+    the per-unit figures of the path (Sec. 3 operators): compaction reads the
+    mask byte and writes the inverse-map entry of every dense vertex, plus a
+    coordinate pair per active row and an offset per body; the neighbour-row
+    table reads a coordinate pair and K neighbour and inverse-map entries and
+    writes K table entries per row; the fused gather + linear reads a
+    coordinate pair and C_in features and writes C_out per row, plus the
+    weights once; the zero-fill scatter reads each active row and writes
+    every dense row (reading its inverse-map entry); the pool reads each
+    active row and writes a row per body (reading its offset)."""
+    B, V, K = w.B, w.V, w.K
+    Cin, Cout = w.layers[0].W.shape[-2:]
+    C = w.layers[-1].W.shape[-1]
+    BV = B * V
+    return {
+        "compact": BV * (1 + 4) + n * 8 + (B + 1) * 4,
+        "table": n * (8 + 3 * 4 * K),
+        "gather+linear": n * (8 + Cin * e + Cout * e) + Cin * Cout * e,
+        "conv": conv_bytes,
+        "scatter": n * C * e + BV * (4 + C * e),
+        "pool": n * C * e + B * (4 + C * e),
+    }
+
+
 def kernel_source_digest():
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
@@ -246,6 +271,17 @@ def main():
     roof["launch_us"] = round(per_kernel_ms["conv"] * 1e3, 2)
     roof["launch_us_in_step_events"] = round(conv_in_step_ms * 1e3, 2)
 
+    # every kernel of the step against HBM: algorithmic bytes / back-to-back
+    # duration (compaction and table are latency-bound at this size)
+    step_bytes = algorithmic_step_bytes(w, n, e, cbytes)
+    kernel_rooflines = {}
+    for name, b in step_bytes.items():
+        if name in per_kernel_ms:
+            t = per_kernel_ms[name] / 1e3
+            kernel_rooflines[name] = {"algorithmic_bytes": int(b), "us": round(t * 1e6, 2),
+                                      "GB/s": round(b / t / 1e9, 1),
+                                      "frac_hbm": round(b / t / 1e9 / HBM_PEAK_GBS, 4)}
+
     out = {
         "metric": "active-vertex rows/sec per sparse contact layer; speed-up vs dense layer",
         "value": round(value, 1),
@@ -261,6 +297,7 @@ def main():
                    "n_active": n, "sparse_layers": L, "parallelism": "single GPU"},
         "per_kernel_us": {k: round(v * 1e3, 2) for k, v in per_kernel_ms.items()},
         "roofline": roof,
+        "kernel_rooflines": kernel_rooflines,
     }
 
     out["next_rows"] = {"group_norm": group_norm_measure(st, shc, torch, args.reps),

@@ -19,7 +19,8 @@
  * - All array arguments are DEVICE pointers (memory on the current HIP device)
  *   unless the comment says "host".  The caller owns every buffer; the library
  *   keeps no pointer after the work it enqueues has run, allocates nothing and
- *   holds no state between calls.
+ *   holds no state between calls (the one exception: the stream-ordering
+ *   events of shc_event_create, which the caller creates and destroys).
  * - Every call validates its arguments on the host, then enqueues its kernels
  *   on `stream` and returns without waiting (the one exception is the optional
  *   host count of shc_compact_mask).  Calls are thread-safe.
@@ -471,6 +472,38 @@ int shc_sparse_neighbor_conv_backward(const void* S, const int32_t* table, const
                                       int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout,
                                       int32_t dtype, int32_t act, void* dS, float* dW, float* db,
                                       void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Stream-ordering events -- a runtime helper, not an operator of the paper.
+ *
+ * An event orders work between streams of one device and lets the host wait
+ * for that work, like a HIP event made with hipEventDisableTiming, except that
+ * its record carries no system-scope fence.  A default HIP event's record
+ * writes back and invalidates the device caches for the host's sake; between
+ * two streams of one device that costs the stream microseconds per record.
+ * Work enqueued after a wait on this event sees every device-memory write of
+ * the work recorded before it (a device-scope release and acquire).  The host
+ * learns only that the work has finished: its writes to host-visible memory
+ * need not be visible to the host yet when shc_event_synchronize returns.
+ *
+ * shc_event_create      -- *event receives a new event of the current device;
+ *                          the caller releases it with shc_event_destroy.
+ * shc_event_record      -- records the event on stream: it completes when the
+ *                          work enqueued on stream before the record has
+ *                          finished.  A new record replaces the last one.
+ * shc_stream_wait_event -- work enqueued on stream after this call starts
+ *                          only after the event's last record has completed
+ *                          (at once if it was never recorded).
+ * shc_event_synchronize -- the host waits until the last record has completed.
+ * shc_event_destroy     -- releases the event; NULL is accepted and ignored.
+ * A NULL event is SHC_ERR_INVALID_ARG (except for destroy); runtime failures
+ * are SHC_ERR_HIP.
+ */
+int shc_event_create(void** event);
+int shc_event_record(void* event, hipStream_t stream);
+int shc_stream_wait_event(hipStream_t stream, void* event);
+int shc_event_synchronize(void* event);
+int shc_event_destroy(void* event);
 
 #ifdef __cplusplus
 }

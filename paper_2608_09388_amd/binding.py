@@ -100,6 +100,11 @@ _SIGS = {
                                                          _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32,
                                                          _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr,
                                                          _c_ptr, _c_sz, _c_ptr]),
+    "shc_event_create": (ctypes.c_int, [ctypes.POINTER(_c_ptr)]),
+    "shc_event_record": (ctypes.c_int, [_c_ptr, _c_ptr]),
+    "shc_stream_wait_event": (ctypes.c_int, [_c_ptr, _c_ptr]),
+    "shc_event_synchronize": (ctypes.c_int, [_c_ptr]),
+    "shc_event_destroy": (ctypes.c_int, [_c_ptr]),
 }
 
 
@@ -413,6 +418,35 @@ def segment_maxpool(S: torch.Tensor, row_ptr: torch.Tensor, n_rows: int, B: int,
             _dev(row_ptr, "row_ptr", torch.int32, B + 1), n_rows, B, C, dt, float(empty_value),
             _dev(P, "P", P.dtype, B * C), _stream(stream)]
     _check(load().shc_segment_maxpool(*args), "shc_segment_maxpool")
+
+
+class StreamEvent:
+    """shc_event_*: orders work between streams of one device, and lets the
+    host wait for it, without a system-scope fence at each record.  Created on
+    the current device."""
+
+    def __init__(self):
+        lib = load()
+        h = _c_ptr()
+        _check(lib.shc_event_create(ctypes.byref(h)), "shc_event_create")
+        self._h = h
+        self._destroy = lib.shc_event_destroy
+
+    def record(self, stream=None):
+        _check(load().shc_event_record(self._h, _stream(stream)), "shc_event_record")
+
+    def wait(self, stream=None):
+        """Work enqueued on ``stream`` after this call waits for the last record."""
+        _check(load().shc_stream_wait_event(_stream(stream), self._h), "shc_stream_wait_event")
+
+    def synchronize(self):
+        _check(load().shc_event_synchronize(self._h), "shc_event_synchronize")
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._destroy(h)
+            self._h = None
 
 
 # ----------------------------------------------------------------------------

@@ -748,4 +748,42 @@ int shc_segment_maxpool(const void* S, const int32_t* row_ptr, int64_t n_rows, i
                     "segment_maxpool launch");
 }
 
+// -- stream-ordering events ---------------------------------------------------
+
+int shc_event_create(void** event) {
+  g_last_error[0] = 0;
+  if (event == nullptr) return fail(SHC_ERR_INVALID_ARG, "event is NULL");
+  *event = nullptr;
+  hipEvent_t ev = nullptr;
+  SHC_TRY(hip_status(hipEventCreateWithFlags(&ev, hipEventDisableTiming | hipEventDisableSystemFence),
+                     "event create"));
+  *event = ev;
+  return SHC_OK;
+}
+
+int shc_event_record(void* event, hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (event == nullptr) return fail(SHC_ERR_INVALID_ARG, "event is NULL");
+  return hip_status(hipEventRecord(static_cast<hipEvent_t>(event), stream), "event record");
+}
+
+int shc_stream_wait_event(hipStream_t stream, void* event) {
+  g_last_error[0] = 0;
+  if (event == nullptr) return fail(SHC_ERR_INVALID_ARG, "event is NULL");
+  return hip_status(hipStreamWaitEvent(stream, static_cast<hipEvent_t>(event), 0),
+                    "stream wait event");
+}
+
+int shc_event_synchronize(void* event) {
+  g_last_error[0] = 0;
+  if (event == nullptr) return fail(SHC_ERR_INVALID_ARG, "event is NULL");
+  return hip_status(hipEventSynchronize(static_cast<hipEvent_t>(event)), "event synchronize");
+}
+
+int shc_event_destroy(void* event) {
+  g_last_error[0] = 0;
+  if (event == nullptr) return SHC_OK;
+  return hip_status(hipEventDestroy(static_cast<hipEvent_t>(event)), "event destroy");
+}
+
 }  // extern "C"

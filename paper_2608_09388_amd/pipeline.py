@@ -16,11 +16,11 @@ The active set never changes across layers (C'_k = C_k, Sec. 3.2), so the
 active count is read back once per mask and passed to every layer call.
 
 The index buffers of a mask (coords, inv, row_ptr, the neighbour-row table)
-exist twice.  ``run(steps)`` uses this for consecutive batches: the
-compaction of batch k + 1 goes into the other set and is enqueued before the
-scatter and pool of batch k, so the host learns the next active count while
-the GPU still has batch k's tail to run, and the stream never idles on that
-wait.  Every batch still runs the whole path.
+exist twice (three times with a side stream).  ``run(steps)`` uses this for
+consecutive batches: the compaction of batch k + 1 goes into another set and
+is enqueued before the scatter and pool of batch k, so the host learns the
+next active count while the GPU still has batch k's tail to run, and the
+stream never idles on that wait.  Every batch still runs the whole path.
 
 This module only moves buffers and issues calls; all arithmetic runs in the
 library's kernels.
@@ -106,6 +106,11 @@ class SparseStack:
         # second stream (default priority) for the next batch's compaction and
         # table in run(); None: everything on the current stream
         self.side = torch.cuda.Stream(device=self.device) if side_stream else None
+        self._events = None
+        if side_stream:
+            with torch.cuda.device(self.device):
+                self._events = ([shc.StreamEvent() for _ in range(3)], shc.StreamEvent(),
+                                shc.StreamEvent())
         self.dtype = TORCH_DTYPE[w.dtype]
         self.B, self.V, self.K = w.B, w.V, w.K
         self.act = act
@@ -126,7 +131,9 @@ class SparseStack:
         # A first linear layer reads its rows straight from x (gather fused in);
         # otherwise the active rows are gathered into acts[0] first.
         self.fused_gather = len(w.layers) > 0 and w.layers[0].kind == "linear"
-        self._sets = [_IndexSet(self), _IndexSet(self)]
+        # two index sets, or three with a side stream (run() then keeps the
+        # side stream off the current stream's events; see _run_two_streams)
+        self._sets = [_IndexSet(self) for _ in range(3 if side_stream else 2)]
         self._cur = 0
 
     # -- the index set of the current mask -------------------------------------
@@ -236,7 +243,7 @@ class SparseStack:
             self._front(s, ev)
             nxt = None
             if k + 1 < steps:
-                self._cur ^= 1
+                self._cur = (self._cur + 1) % len(self._sets)
                 nxt = self._set
                 if feed is not None:
                     feed(k + 1)
@@ -254,16 +261,25 @@ class SparseStack:
         """run() with batch k + 1's compaction and neighbour table on the side
         stream, beside batch k's scatter and pool on the current stream.
 
-        Events order the two streams: the side stream starts on an index set
-        only after the current stream's last reader of it (the pool of batch
-        k - 1) and after ``feed``'s writes; the current stream starts batch
-        k + 1's layers only after its table.  Every batch runs the whole path."""
+        The three index sets rotate, so batch k + 1's compaction writes the set
+        whose last reader was the pool of batch k - 2.  The host checks that
+        this pool has finished (an event on the current stream, synchronised
+        from the host; the host runs at most about two batches ahead, so it has
+        almost always finished) instead of making the side stream wait for it
+        on the GPU: a side stream that waits on the current stream's events
+        and is waited on by it costs the current stream several microseconds a
+        batch, while a wait in one direction only (current on side) costs
+        nothing measurable.  The current stream starts batch k + 1's layers
+        only after its table (an event on the side stream).  With ``feed``,
+        the side stream also waits on the GPU for the writes of ``feed``.
+        The events carry no system-scope fence (shc_event_create): a default
+        event's cache write-back at every record costs the step a few
+        microseconds more.  Every batch runs the whole path."""
         main = torch.cuda.current_stream(self.device)
         side = self.side
-        free = [torch.cuda.Event(), torch.cuda.Event()]   # set i released by its last reader
-        used = [False, False]
-        ready = torch.cuda.Event()
-        fed = torch.cuda.Event()
+        ns = len(self._sets)
+        free, ready, fed = self._events    # free[i]: set i released by its last reader
+        used = [False] * ns
         cur = self._cur
         s = self._sets[cur]
         if feed is not None:
@@ -276,15 +292,15 @@ class SparseStack:
             if around_layer is not None and around_layer[1][k][0] is not None:
                 ev = (around_layer[0], *around_layer[1][k])
             self._front(s, ev, table_done=table_done)
-            nxt_i = cur ^ 1
+            nxt_i = (cur + 1) % ns
             nxt = self._sets[nxt_i] if k + 1 < steps else None
             if nxt is not None:
                 if feed is not None:
                     feed(k + 1)
                     fed.record(main)
-                    side.wait_event(fed)
+                    fed.wait(side)
                 if used[nxt_i]:
-                    side.wait_event(free[nxt_i])
+                    free[nxt_i].synchronize()
                 nxt.compact_side.start()
             if s.scatter is not None:
                 s.scatter(s.n)
@@ -298,7 +314,7 @@ class SparseStack:
                 if table_done:
                     nxt.table_side(nxt.n)
                 ready.record(side)
-                main.wait_event(ready)
+                ready.wait(main)
                 cur = nxt_i
                 s = nxt
         self._cur = cur

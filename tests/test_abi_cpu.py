@@ -348,3 +348,13 @@ def test_binding_refuses_cpu_tensors():
     x = torch.zeros(4 * 655, 16)
     with pytest.raises(ValueError):
         shc.gather_rows(x, torch.zeros(10, 2, dtype=torch.int32), 10, 4, 655, torch.zeros(10, 16))
+
+
+def test_event_helpers_validation(lib):
+    """The stream-ordering event helpers refuse a NULL event before any HIP
+    call (destroy accepts it)."""
+    assert lib.shc_event_create(None) == -1 and "event" in err(lib)
+    assert lib.shc_event_record(None, None) == -1
+    assert lib.shc_stream_wait_event(None, None) == -1
+    assert lib.shc_event_synchronize(None) == -1
+    assert lib.shc_event_destroy(None) == 0

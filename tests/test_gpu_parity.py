@@ -890,21 +890,23 @@ def test_full_size_workloads_sampled(dev, name):
 
 
 @pytest.mark.parametrize("side", [False, True])
-@pytest.mark.parametrize("steps", [1, 2, 3])
+@pytest.mark.parametrize("steps", [1, 2, 3, 5])
 def test_overlapped_run_new_mask_per_batch(dev, steps, side):
-    """SparseStack.run: each batch's compaction (into the other index set) is
+    """SparseStack.run: each batch's compaction (into another index set) is
     enqueued before the previous batch's scatter and pool -- with ``side``, on
-    a second stream beside them, ordered by events.  Every batch gets its own
-    mask and features; the outputs left behind must be the oracle's for the
-    last batch, with index sets that last held another mask."""
+    a second stream beside them, ordered by events and, for an index set's
+    reuse, by a host-side check of its last reader (five batches rotate the
+    three sets past it).  Every batch gets its own mask and features; the
+    outputs left behind must be the oracle's for the last batch, with index
+    sets that last held another mask."""
     from paper_2608_09388_amd.pipeline import SparseStack, to_device
     w = synth.workload_c4(0.05, B=6, V=655)
     rng = np.random.default_rng(400 + steps)
-    masks = [(rng.random((w.B, w.V)) < p).astype(np.uint8) for p in (0.3, 0.05, 0.2)][:steps]
+    masks = [(rng.random((w.B, w.V)) < p).astype(np.uint8) for p in (0.3, 0.05, 0.2, 0.6, 0.1)][:steps]
     xs = [synth.as_dtype(rng.standard_normal(w.x.shape).astype(np.float32), w.dtype)[1]
           for _ in range(steps)]
     st = SparseStack(w, device=str(dev), side_stream=side)
-    st.run(2)                               # both index sets hold the workload's own mask
+    st.run(2)                               # two index sets hold the workload's own mask
 
     def feed(k):
         st.mask.copy_(up(masks[k].reshape(-1)))
@@ -965,3 +967,37 @@ def test_empty_mask_path(dev):
     res = st.results()
     assert res["n"] == 0 and np.all(res["row_ptr"] == 0) and np.all(res["inv"] == -1)
     assert np.all(res["dense"] == 0) and np.all(res["pool"] == 0)
+
+
+def test_stream_events_order_streams(dev):
+    """shc_event_*: a wait on the event holds the second stream until the work
+    recorded on the first has finished (its device writes visible), a wait on
+    a never-recorded event passes, and the host wait returns only after the
+    recorded work."""
+    a = torch.cuda.Stream(device=dev)
+    b = torch.cuda.Stream(device=dev)
+    x = torch.zeros(1 << 24, dtype=torch.float32, device=dev)
+    y = torch.empty_like(x)
+    ev, fresh = shc.StreamEvent(), shc.StreamEvent()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        with torch.cuda.stream(a):
+            for _ in range(30):
+                x.add_(1.0)
+        ev.record(a)
+        fresh.wait(b)
+        ev.wait(b)
+        with torch.cuda.stream(b):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        assert torch.all(y == 30.0 * (rep + 1))
+    done = torch.cuda.Event()
+    with torch.cuda.stream(a):
+        for _ in range(30):
+            x.add_(1.0)
+        done.record(a)
+    ev.record(a)
+    ev.synchronize()
+    assert done.query()          # everything recorded before the event has finished
+    torch.cuda.synchronize()
+    assert torch.all(x == 120.0)
