@@ -85,7 +85,9 @@ def algorithmic_step_bytes(w, n, e, conv_bytes):
     mask byte and writes the inverse-map entry of every dense vertex, plus a
     coordinate pair per active row and an offset per body; the neighbour-row
     table reads a coordinate pair and K neighbour and inverse-map entries and
-    writes K table entries per row; the fused gather + linear reads a
+    writes K table entries per row (K neighbour entries and K table entries
+    when the compaction writes it, the row numbering staying on chip); the
+    fused gather + linear reads a
     coordinate pair and C_in features and writes C_out per row, plus the
     weights once; the zero-fill scatter reads each active row and writes
     every dense row (reading its inverse-map entry); the pool reads each
@@ -97,6 +99,8 @@ def algorithmic_step_bytes(w, n, e, conv_bytes):
     return {
         "compact": BV * (1 + 4) + n * 8 + (B + 1) * 4,
         "table": n * (8 + 3 * 4 * K),
+        # in one pass: the table reads only the neighbour lists
+        "compact+table": BV * (1 + 4) + n * 8 + (B + 1) * 4 + n * 2 * 4 * K,
         "gather+linear": n * (8 + Cin * e + Cout * e) + Cin * Cout * e,
         "conv": conv_bytes,
         "scatter": n * C * e + BV * (4 + C * e),
@@ -159,12 +163,17 @@ def kernel_times(st, shc, torch, reps):
                          want_host_count=False)
 
     calls = {"compact": (compact_async, main), "table": (st.build_table, main),
+             # the step's compaction: with the table written in the same pass
+             # when the set is built that way (no host wait: start only)
+             "compact+table": (st._set.compact.start, main),
              "gather": (st.gather, main),
              ("gather+linear" if st.fused_gather else "linear"): (lambda: st.layer(0), main),
              "conv": (lambda: st.layer(1), main), "scatter": (st.scatter, main),
              "pool": (st.pool, main)}
     if st.fused_gather:  # the step has no separate gather kernel
         del calls["gather"]
+    if not st._set.fused:
+        del calls["compact+table"]
     out = {}
     for name, (fn, stream) in calls.items():
         for _ in range(3):

@@ -130,6 +130,25 @@ int shc_compact_mask_start(const uint8_t* mask, int32_t B, int32_t V, int32_t* c
 int shc_compact_mask_wait(int64_t* n_active_host, int64_t cap, hipStream_t stream);
 
 /*
+ * shc_compact_mask_table_start -- shc_compact_mask_start that also writes the
+ *   neighbour-row table of the active set (shc_build_neighbor_table's output
+ *   for the N' rows it produces) in the same pass, so the table needs no
+ *   launch of its own and no host knowledge of N':
+ *     nbr    [V][K] int32 neighbour lists, -1 = none (as for the table call);
+ *     table  [K][N'] int32 out, slot-major with row stride N'; written only
+ *            when N' <= cap, so it must hold K * cap entries (may be NULL when
+ *            cap = 0).
+ *   K in [1, 32]; V <= 19456 (a body's row numbering is kept on chip),
+ *   else SHC_ERR_UNSUPPORTED.  Finish with shc_compact_mask_wait.  Other
+ *   arguments, outputs and errors as for shc_compact_mask_start.
+ */
+int shc_compact_mask_table_start(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
+                                 int32_t* inv, int32_t* row_ptr, int32_t* n_active_dev,
+                                 int64_t* n_active_host, int64_t cap, const int32_t* nbr,
+                                 int32_t K, int32_t* table, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+/*
  * Gather of the active feature rows -- S' of Eq. 2: S[i] = x[b_i * V + v_i].
  *
  *   x       [B*V][C] dense per-vertex features.

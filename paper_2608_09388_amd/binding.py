@@ -23,6 +23,8 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "shc.h")
 SHC_F32, SHC_BF16 = 0, 1
 SHC_ACT_NONE, SHC_ACT_RELU = 0, 1
 SHC_COMBINE_SUM, SHC_COMBINE_MEAN, SHC_COMBINE_MAX = 0, 1, 2
+# largest V shc_compact_mask_table_start takes
+COMPACT_TABLE_MAX_V = 19456
 COMBINE = {"sum": SHC_COMBINE_SUM, "mean": SHC_COMBINE_MEAN, "max": SHC_COMBINE_MAX}
 STATUS = {0: "SHC_OK", -1: "SHC_ERR_INVALID_ARG", -2: "SHC_ERR_CAPACITY",
           -3: "SHC_ERR_MISALIGNED", -4: "SHC_ERR_UNSUPPORTED", -5: "SHC_ERR_HIP"}
@@ -47,6 +49,9 @@ _SIGS = {
     "shc_compact_mask_start": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr,
                                               _c_ptr, _c_ptr, _c_i64, _c_ptr, _c_sz, _c_ptr]),
     "shc_compact_mask_wait": (ctypes.c_int, [_c_ptr, _c_i64, _c_ptr]),
+    "shc_compact_mask_table_start": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr,
+                                                    _c_ptr, _c_ptr, _c_ptr, _c_i64, _c_ptr,
+                                                    _c_i32, _c_ptr, _c_ptr, _c_sz, _c_ptr]),
     "shc_clear_inactive_rows": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_i32, _c_i32, _c_ptr,
                                                _c_ptr]),
     "shc_gather_rows": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
@@ -590,10 +595,14 @@ class PreparedCompact:
 
     ``start()`` and ``wait()`` are the two halves (shc_compact_mask_start /
     shc_compact_mask_wait): work that needs only ``inv`` can be enqueued
-    between them, while the count is on its way.
+    between them, while the count is on its way.  Given ``nbr`` [V][K] and
+    ``table``, ``start()`` is shc_compact_mask_table_start: the neighbour-row
+    table of the active set ([K][N'], row stride N') is written in the same
+    pass, for up to ``cap`` = coords rows (the table holds K * cap entries).
     """
 
-    def __init__(self, mask, B, V, coords, inv, row_ptr, n_active, ws, stream=None):
+    def __init__(self, mask, B, V, coords, inv, row_ptr, n_active, ws, stream=None,
+                 nbr=None, table=None):
         self.host = torch.zeros(1, dtype=torch.int64, pin_memory=True)
         self._host_view = self.host.numpy()
         cap = coords.numel() // 2
@@ -603,9 +612,16 @@ class PreparedCompact:
                 _dev(row_ptr, "row_ptr", torch.int32, B + 1),
                 _dev(n_active, "n_active", torch.int32, 1), self.host.data_ptr(), cap,
                 _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)]
-        keep = (mask, coords, inv, row_ptr, n_active, ws, self.host)
+        keep = (mask, coords, inv, row_ptr, n_active, ws, self.host, nbr, table)
         self._call = Prepared("shc_compact_mask", args, None, 0, keep)
-        self._start = Prepared("shc_compact_mask_start", args, None, 0, keep)
+        if nbr is not None:
+            K = nbr.shape[-1]
+            targs = args[:9] + [_dev(nbr, "nbr", torch.int32, V * K), K,
+                                _dev(table, "table", torch.int32, K * cap) if cap > 0 else None]
+            targs += args[9:]
+            self._start = Prepared("shc_compact_mask_table_start", targs, None, 0, keep)
+        else:
+            self._start = Prepared("shc_compact_mask_start", args, None, 0, keep)
         self._wait = Prepared("shc_compact_mask_wait", [self.host.data_ptr(), cap, args[-1]],
                               None, 0, keep)
 

@@ -119,10 +119,12 @@ static int64_t* mapped_host_count(int64_t* host) {
 // Validation and launch shared by shc_compact_mask and shc_compact_mask_start.
 // *mapped receives the device address of a page-locked host count, or null
 // (no host count, or pageable memory: refused when require_mapped).
+// With nbr != NULL the neighbour-row table is written too (compact + table).
 static int compact_launch(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords, int32_t* inv,
                           int32_t* row_ptr, int32_t* n_active_dev, int64_t* n_active_host,
                           bool require_mapped, int64_t** mapped_out, int64_t cap, void* ws,
-                          size_t ws_bytes, hipStream_t stream) {
+                          size_t ws_bytes, hipStream_t stream, const int32_t* nbr = nullptr,
+                          int32_t K = 0, int32_t* table = nullptr) {
   *mapped_out = nullptr;
   if (require_mapped && n_active_host == nullptr)
     return fail(SHC_ERR_INVALID_ARG, "n_active_host is NULL");
@@ -143,6 +145,11 @@ static int compact_launch(const uint8_t* mask, int32_t B, int32_t V, int32_t* co
                                      "into the device");
   *mapped_out = mapped;
   if (mapped != nullptr) *reinterpret_cast<volatile int64_t*>(n_active_host) = -1;  // set by the kernel
+  if (nbr != nullptr)
+    return hip_status(shc::launch_compact_table(mask, B, V, coords, inv, row_ptr, n_active_dev,
+                                                mapped, cap, nbr, K, table,
+                                                static_cast<int32_t*>(ws), stream),
+                      "compact_mask_table launch");
   return hip_status(shc::launch_compact(mask, B, V, coords, inv, row_ptr, n_active_dev, mapped,
                                         cap, static_cast<int32_t*>(ws), stream),
                     "compact_mask launch");
@@ -156,6 +163,24 @@ int shc_compact_mask_start(const uint8_t* mask, int32_t B, int32_t V, int32_t* c
   int64_t* mapped = nullptr;
   return compact_launch(mask, B, V, coords, inv, row_ptr, n_active_dev, n_active_host, true,
                         &mapped, cap, ws, ws_bytes, stream);
+}
+
+int shc_compact_mask_table_start(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
+                                 int32_t* inv, int32_t* row_ptr, int32_t* n_active_dev,
+                                 int64_t* n_active_host, int64_t cap, const int32_t* nbr,
+                                 int32_t K, int32_t* table, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  g_last_error[0] = 0;
+  if (K <= 0) return fail(SHC_ERR_INVALID_ARG, "K = %d must be positive", K);
+  if (K > kMaxSlots) return fail(SHC_ERR_UNSUPPORTED, "K = %d exceeds %d slots", K, kMaxSlots);
+  if (V > shc::kCompactTableMaxV)
+    return fail(SHC_ERR_UNSUPPORTED, "V = %d exceeds the %d vertices of a body this call keeps",
+                V, shc::kCompactTableMaxV);
+  SHC_PTR(nbr, "nbr");
+  if (cap > 0) SHC_PTR(table, "table");
+  int64_t* mapped = nullptr;
+  return compact_launch(mask, B, V, coords, inv, row_ptr, n_active_dev, n_active_host, true,
+                        &mapped, cap, ws, ws_bytes, stream, nbr, K, cap > 0 ? table : nullptr);
 }
 
 int shc_compact_mask_wait(int64_t* n_active_host, int64_t cap, hipStream_t stream) {

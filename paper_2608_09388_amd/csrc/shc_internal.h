@@ -46,6 +46,16 @@ hipError_t launch_compact(const uint8_t* mask, int32_t B, int32_t V, int32_t* co
                           int32_t* row_ptr, int32_t* n_active, int64_t* n_host, int64_t cap,
                           int32_t* block_counts, hipStream_t stream);
 
+// compaction that also writes the neighbour-row table of the active set
+// (table[j * N' + i], as launch_neighbor_table), one block per body: the body's
+// row numbering lives in LDS, 8 bytes per vertex
+constexpr int32_t kCompactTableMaxV = 19456;
+bool compact_table_supported(int32_t V, int32_t K);
+hipError_t launch_compact_table(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
+                                int32_t* inv, int32_t* row_ptr, int32_t* n_active,
+                                int64_t* n_host, int64_t cap, const int32_t* nbr, int32_t K,
+                                int32_t* table, int32_t* block_counts, hipStream_t stream);
+
 hipError_t launch_gather(const void* x, const int32_t* coords, int64_t n_rows, int32_t B,
                          int32_t V, int32_t row_bytes, void* S, hipStream_t stream);
 

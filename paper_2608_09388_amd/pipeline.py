@@ -10,7 +10,9 @@ as a sequence of library calls:
     per layer -> shc_scatter / shc_segment_maxpool
 
 with the gather fused into the first layer (shc_gather_sparse_linear) when
-that layer is linear.
+that layer is linear, and a conv layer's neighbour-row table written by the
+compaction itself (shc_compact_mask_table_start) when a body's vertices fit
+its on-chip row numbering.
 
 The active set never changes across layers (C'_k = C_k, Sec. 3.2), so the
 active count is read back once per mask and passed to every layer call.
@@ -62,14 +64,18 @@ class _IndexSet:
                       if has_conv else None)
         self.n: Optional[int] = None
         # every call marshalled once, on the current stream; the buffers are at
-        # full capacity, so each call only takes the row count
+        # full capacity, so each call only takes the row count.  compact.start()
+        # also writes the neighbour-row table when one is needed and a body's
+        # row numbering fits on chip (shc_compact_mask_table_start): `fused`
+        self.fused = self.table is not None and V <= shc.COMPACT_TABLE_MAX_V and K <= 32
+        tbl = dict(nbr=st.nbr, table=self.table) if self.fused else {}
         self.compact = shc.PreparedCompact(st.mask, B, V, self.coords, self.inv, self.row_ptr,
-                                           self.n_active, self.ws)
-        # the same compaction and table build on the side stream (run() with
-        # side_stream: they overlap the previous batch's scatter and pool)
+                                           self.n_active, self.ws, **tbl)
+        # the same compaction (and table build) on the side stream (run() with
+        # side_stream: they overlap the previous batch's layers, scatter and pool)
         self.compact_side = (shc.PreparedCompact(st.mask, B, V, self.coords, self.inv,
                                                  self.row_ptr, self.n_active, self.ws,
-                                                 stream=st.side)
+                                                 stream=st.side, **tbl)
                              if st.side is not None else None)
         self.gather = shc.prepare_gather_rows(st.x, self.coords, B, V, st.acts[0])
         self.table_call = (shc.prepare_build_neighbor_table(self.coords, self.inv, B, V, st.nbr,
@@ -77,7 +83,8 @@ class _IndexSet:
                            if self.table is not None else None)
         self.table_side = (shc.prepare_build_neighbor_table(self.coords, self.inv, B, V, st.nbr,
                                                             self.table, stream=st.side)
-                           if self.table is not None and st.side is not None else None)
+                           if self.table is not None and st.side is not None and not self.fused
+                           else None)
         self.layers = []
         for l, spec in enumerate(st.w.layers):
             src, dst = st.acts[l], st.acts[l + 1]
@@ -240,7 +247,7 @@ class SparseStack:
             ev = None
             if around_layer is not None and around_layer[1][k][0] is not None:
                 ev = (around_layer[0], *around_layer[1][k])
-            self._front(s, ev)
+            self._front(s, ev, table_done=s.fused)
             nxt = None
             if k + 1 < steps:
                 self._cur = (self._cur + 1) % len(self._sets)
@@ -286,7 +293,7 @@ class SparseStack:
             feed(0)
         s.compact.start()
         s.n = s.compact.wait()
-        table_done = False
+        table_done = s.fused
         for k in range(steps):
             ev = None
             if around_layer is not None and around_layer[1][k][0] is not None:
@@ -310,9 +317,9 @@ class SparseStack:
             used[cur] = True
             if nxt is not None:
                 nxt.n = nxt.compact_side.wait()
-                table_done = nxt.table_side is not None
-                if table_done:
+                if nxt.table_side is not None:
                     nxt.table_side(nxt.n)
+                table_done = nxt.table is not None    # built on the side stream
                 ready.record(side)
                 ready.wait(main)
                 cur = nxt_i

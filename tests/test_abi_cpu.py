@@ -358,3 +358,28 @@ def test_event_helpers_validation(lib):
     assert lib.shc_stream_wait_event(None, None) == -1
     assert lib.shc_event_synchronize(None) == -1
     assert lib.shc_event_destroy(None) == 0
+
+
+def test_compact_table_start_validation(lib):
+    ws = lib.shc_compact_mask_workspace(4, 655)
+    host = ctypes.c_int64(0)
+    ok = dict(mask=A, B=4, V=655, coords=A, inv=A, row_ptr=A, n_dev=A,
+              n_host=ctypes.addressof(host), cap=2620, nbr=A, K=9, table=A, ws=A, ws_bytes=ws)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return lib.shc_compact_mask_table_start(a["mask"], a["B"], a["V"], a["coords"], a["inv"],
+                                                a["row_ptr"], a["n_dev"], a["n_host"], a["cap"],
+                                                a["nbr"], a["K"], a["table"], a["ws"],
+                                                a["ws_bytes"], None)
+
+    assert call(K=0) == -1 and "K" in err(lib)
+    assert call(K=33) == -4
+    assert call(V=19457, ws_bytes=1 << 30) == -4 and "19456" in err(lib)
+    assert call(nbr=None) == -1 and "nbr" in err(lib)
+    assert call(nbr=MIS) == -3
+    assert call(table=None) == -1 and "table" in err(lib)
+    assert call(n_host=None) == -1
+    assert call(ws_bytes=ws - 1) == -2
+    # pageable host memory cannot receive the kernel's count
+    assert call() == -1 and "page-locked" in err(lib)

@@ -1001,3 +1001,52 @@ def test_stream_events_order_streams(dev):
     assert done.query()          # everything recorded before the event has finished
     torch.cuda.synchronize()
     assert torch.all(x == 120.0)
+
+
+@pytest.mark.parametrize("B,V,K,p,cap_delta", [
+    (5, 655, 9, 0.1, None),       # 256-thread blocks, one pass
+    (3, 4096, 9, 0.3, None),      # 256-thread blocks, two passes
+    (4, 4097, 9, 0.05, None),     # 1024-thread blocks, odd body starts
+    (3, 10475, 9, 0.05, None),    # 1024-thread blocks, the mesh size of the 10,475-vertex bodies
+    (2, 19456, 5, 0.5, None),     # the largest V, two passes
+    (7, 333, 32, 0.4, None),      # 32 slots
+    (6, 97, 1, 0.9, None),        # one slot
+    (9, 211, 9, 0.0, None),       # empty mask
+    (4, 300, 9, 1.0, None),       # every vertex active
+    (3, 1000, 9, 0.2, 0),         # cap = N' exactly
+    (3, 1000, 9, 0.2, -5),        # cap below N': capacity error, table untouched
+    (1, 5, 3, 0.6, None),         # tiny body, last bytes of the mask
+])
+def test_compact_table_start(dev, B, V, K, p, cap_delta):
+    """shc_compact_mask_table_start: the lists of the compaction (Eq. 2), bit
+    for bit as the oracle's, and the neighbour-row table of its active set
+    (the rows each slot of Eqs. 4-5 reads, written out from the oracle's
+    compaction), with row stride N'."""
+    rng = np.random.default_rng(B * 1000 + V + K)
+    m = (rng.random((B, V)) < p).astype(np.uint8)
+    nbr = rand_nbr(V, K, rng)
+    nbr[rng.random((V, K)) < 0.05] = V + 3          # out-of-range entries read as absent
+    ref_c, ref_inv, ref_rp, ref_n = O.compact(m)
+    cap = B * V if cap_delta is None else max(ref_n + cap_delta, 0)
+    c = Compaction(m, cap)
+    table = torch.full((K * max(cap, 1) + 5,), -7, dtype=torch.int32, device=dev)
+    pc = shc.PreparedCompact(c.mask, B, V, c.coords, c.inv, c.row_ptr, c.n_dev, c.ws,
+                             nbr=up(nbr), table=table)
+    pc.start()
+    if cap < ref_n:
+        with pytest.raises(shc.ShcError, match="exceed"):
+            pc.wait()
+        torch.cuda.synchronize()
+        assert np.all(down(table) == -7)
+        assert np.array_equal(down(c.inv), ref_inv)
+        assert np.array_equal(down(c.coords)[:cap], ref_c[:cap])
+        return
+    n = pc.wait()
+    torch.cuda.synchronize()
+    assert n == ref_n == int(down(c.n_dev)[0])
+    assert np.array_equal(down(c.coords)[:n], ref_c)
+    assert np.array_equal(down(c.inv), ref_inv)
+    assert np.array_equal(down(c.row_ptr), ref_rp)
+    got_t = down(table)
+    assert np.array_equal(got_t[:K * n].reshape(K, n), table_reference(m, nbr))
+    assert np.all(got_t[K * n:] == -7)
