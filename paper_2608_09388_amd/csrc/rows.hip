@@ -234,27 +234,33 @@ struct PoolVec<true> {  // 8 bf16 channels
   }
 };
 
-// One block of kPoolThreads threads per segment: tx threads span a row, ty
-// row slots; each thread folds kPoolRows rows per batch, all loaded before the
-// first maximum.  A row index past the segment clamps to its last row:
-// repeating a row leaves a maximum unchanged, so no select is needed.
+// Blocks (segment b, channel part): a part is a run of vpp of the row's vpr
+// 16-byte vectors (all of them when there is one part); tx threads span it,
+// ty row slots; each thread folds kPoolRows rows per batch, all loaded before
+// the first maximum.  A row index past the segment clamps to its last row:
+// repeating a row leaves a maximum unchanged, so no select is needed.  The
+// parts split few, long segments over more CUs; each part's maximum is its
+// own, so no block combines another's.
 constexpr int kPoolThreads = 1024;
 constexpr int kPoolRows = 8;
+constexpr int kPoolMinBlocks = 512;   // split channels until about this many blocks
+constexpr int kPoolMinPartVecs = 4;   // ... keeping at least 64 bytes of a row per part
 
 template <bool BF16>
 __global__ __launch_bounds__(kPoolThreads) void segment_max_kernel(
     const i32x4* __restrict__ S, const int32_t* __restrict__ row_ptr, int64_t n_rows, int vpr,
-    float empty_value, i32x4* __restrict__ P) {
+    int vpp, float empty_value, i32x4* __restrict__ P) {
   using PV = PoolVec<BF16>;
   extern __shared__ float part[];  // [ty][tx][N]
   const int b = blockIdx.x;
+  const int qp = blockIdx.y * vpp;  // first vector of this block's channel part
   int64_t lo = row_ptr[b], hi = row_ptr[b + 1];
   lo = lo < 0 ? 0 : (lo > n_rows ? n_rows : lo);
   hi = hi < lo ? lo : (hi > n_rows ? n_rows : hi);
   const int tx = blockDim.x, ty = blockDim.y, y = threadIdx.y;
   const float nanv = __builtin_nanf("");
-  for (int q0 = 0; q0 < vpr; q0 += tx) {
-    const int q = min(q0 + (int)threadIdx.x, vpr - 1);
+  for (int q0 = 0; q0 < vpp; q0 += tx) {
+    const int q = qp + min(q0 + (int)threadIdx.x, vpp - 1);
     float m[PV::N];
     for (int k = 0; k < PV::N; ++k) m[k] = nanv;
     for (int64_t i0 = lo + y; i0 < hi; i0 += (int64_t)kPoolRows * ty) {
@@ -280,7 +286,7 @@ __global__ __launch_bounds__(kPoolThreads) void segment_max_kernel(
       for (int k = 0; k < PV::N; ++k) mine[k] = m[k];
     }
     __syncthreads();
-    if (y == 0 && q0 + (int)threadIdx.x < vpr) {
+    if (y == 0 && q0 + (int)threadIdx.x < vpp) {
       for (int yy = 1; yy < 8 && yy < ty; ++yy) {
         const float* o = part + ((size_t)yy * tx + threadIdx.x) * PV::N;
         for (int k = 0; k < PV::N; ++k) m[k] = fmaxf(m[k], o[k]);
@@ -387,17 +393,25 @@ hipError_t launch_segment_max(const void* S, const int32_t* row_ptr, int64_t n_r
                               int32_t C, int is_bf16, float empty_value, void* P,
                               hipStream_t stream) {
   const int32_t row_bytes = C * (is_bf16 ? 2 : 4);
-  RowShape s = row_shape(row_bytes);
-  s.ty = kPoolThreads / s.tx;
+  const int vpr = row_bytes / 16;
+  int parts = 1;
+  while ((int64_t)B * parts < kPoolMinBlocks && vpr % (2 * parts) == 0 &&
+         vpr / (2 * parts) >= kPoolMinPartVecs)
+    parts *= 2;
+  const int vpp = vpr / parts;
+  RowShape s = row_shape(vpp * 16);
+  // a split segment's rows are spread over 4x fewer threads per block
+  s.ty = (parts > 1 ? kPoolThreads / 4 : kPoolThreads) / s.tx;
+  if (s.ty < 1) s.ty = 1;
   const int n_per_vec = is_bf16 ? 8 : 4;
   const size_t lds = (size_t)s.tx * s.ty * n_per_vec * sizeof(float);
   if (is_bf16)
-    hipLaunchKernelGGL(segment_max_kernel<true>, dim3(B), dim3(s.tx, s.ty), lds, stream,
-                       static_cast<const i32x4*>(S), row_ptr, n_rows, s.vpr, empty_value,
+    hipLaunchKernelGGL(segment_max_kernel<true>, dim3(B, parts), dim3(s.tx, s.ty), lds, stream,
+                       static_cast<const i32x4*>(S), row_ptr, n_rows, vpr, vpp, empty_value,
                        static_cast<i32x4*>(P));
   else
-    hipLaunchKernelGGL(segment_max_kernel<false>, dim3(B), dim3(s.tx, s.ty), lds, stream,
-                       static_cast<const i32x4*>(S), row_ptr, n_rows, s.vpr, empty_value,
+    hipLaunchKernelGGL(segment_max_kernel<false>, dim3(B, parts), dim3(s.tx, s.ty), lds, stream,
+                       static_cast<const i32x4*>(S), row_ptr, n_rows, vpr, vpp, empty_value,
                        static_cast<i32x4*>(P));
   return hipGetLastError();
 }
