@@ -37,7 +37,7 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_conv_c4_5pct.txt")
 # sources of the conv launch (dispatch and kernel): the counter summary is
 # only used while they are unchanged
-EVENT_EVERY = 10  # steps between two sampled conv launches in the timed region
+EVENT_EVERY = 50  # steps between two sampled conv launches in the timed region
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_09388_amd", "csrc", f)
                   for f in ("gemm.hip", "conv_ws.hip", "shc_internal.h")]
 
@@ -49,8 +49,8 @@ def log(msg):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=1000)
+    p.add_argument("--warmup", type=int, default=50)
     p.add_argument("--density", type=float, default=0.05)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-dense", action="store_true", help="skip the dense-layer comparison")

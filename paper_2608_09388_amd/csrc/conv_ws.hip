@@ -112,7 +112,7 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   constexpr int WROWW = BF16 ? WS * 2 : WROW;      // weight-slice row
   constexpr int VPR = WS * E::bytes / 16;  // 16-byte vectors per slice row
   // jobs in flight (fewer when the linear layer keeps its B fragments in registers)
-  constexpr int D = (BF16 && !CONV && KSM * NCB <= 32) ? 8 / KSM : 16 / KSM;
+  constexpr int D = (BF16 && !CONV && KSM * NCB <= 32) ? 12 / KSM : 16 / KSM;
 
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int K = CONV ? a.K : 1;
@@ -143,6 +143,15 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   const int nblk = (nrows + 15) / 16;
   const int n0 = blockIdx.y * WS;
   const unsigned char* W = static_cast<const unsigned char*>(a.W);
+  // bias of this lane's columns, loaded now so the prologue hides the latency
+  // (the selection below waits until after it)
+  float bias_raw[NCB];
+#pragma unroll
+  for (int cb = 0; cb < NCB; ++cb) {
+    const int col = n0 + cb * 16 + l16;
+    const float* bp = a.bias != nullptr ? a.bias : reinterpret_cast<const float*>(a.W);
+    bias_raw[cb] = bp[(a.bias != nullptr && col < Cout) ? col : 0];
+  }
 
   // Byte offset of 16-byte vector q in weight-slice row k.  For bf16 the
   // 32-byte column chunk (16 output columns) is XOR-ed with bit 1 ^ bit 3 of
@@ -352,10 +361,7 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
     const int col = n0 + cb * 16 + l16;
-    const bool ok = a.bias != nullptr && col < Cout;
-    const float* bp = a.bias != nullptr ? a.bias : reinterpret_cast<const float*>(a.W);
-    const float bvl = bp[ok ? col : 0];
-    bias_v[cb] = ok ? bvl : 0.f;
+    bias_v[cb] = (a.bias != nullptr && col < Cout) ? bias_raw[cb] : 0.f;
   }
   const bool relu = a.relu != 0;
   unsigned char* my_scratch = scratch + wave * 16 * WROW;
@@ -457,11 +463,6 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   // wavefront keeps their B fragments in registers for the whole loop.
   constexpr bool kResidentB = BF16 && !CONV && KSM * NCB <= 32;  // at most 128 VGPRs
   bf16x8 wres[kResidentB ? KSM : 1][kResidentB ? NCB : 1];
-  if constexpr (kResidentB) {
-#pragma unroll
-    for (int ks = 0; ks < KSM; ++ks)
-      read_b(ks < KS ? wl + ks * E::kstep * WROWW : zrows, wres[kResidentB ? ks : 0]);
-  }
 
   // Branch-free contraction of one job: every B fragment of the job is read
   // from LDS before the first MFMA (the scheduling barrier keeps the reads
@@ -544,7 +545,11 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
     for (int cb = 0; cb < NCB; ++cb) {
       float v[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = (!relu || acc[cb][r] > 0.f) ? acc[cb][r] : 0.f;
+      for (int r = 0; r < 4; ++r) {
+        const float x = acc[cb][r];
+        const float rx = x > 0.f ? x : 0.f;  // selects, no branch
+        v[r] = relu ? rx : x;
+      }
       unsigned char* pp = my_scratch + (g * 4) * WROW + (cb * 16 + l16) * E::bytes;
       if (BF16) {  // hardware round-to-nearest-even conversion, two rows per instruction
 #pragma unroll
@@ -562,19 +567,33 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // every LDS read of the stores first (row positions, then the staged
+    // vectors), then the stores: two LDS round trips, not one per store
+    constexpr int NST = (16 * VPR + 63) / 64;
+    int prow[NST];
+    i32x4 sv[NST];
 #pragma unroll
-    for (int idx0 = 0; idx0 < 16 * VPR; idx0 += 64) {
-      const int idx = idx0 + lane;
-      const int r = (idx / VPR) & 15;
-      const int q = idx % VPR;
-      const int pos = blk * 16 + r;
-      const int n = n0 + q * E::per_vec;
+    for (int t = 0; t < NST; ++t) {
+      const int idx = t * 64 + lane;
+      const int pos = blk * 16 + ((idx / VPR) & 15);
+      prow[t] = perm[pos < nrows ? pos : 0];
+    }
+#pragma unroll
+    for (int t = 0; t < NST; ++t) {
+      const int idx = t * 64 + lane;
+      sv[t] = *reinterpret_cast<const i32x4*>(my_scratch + ((idx / VPR) & 15) * WROW +
+                                              (idx % VPR) * 16);
+    }
+#pragma unroll
+    for (int t = 0; t < NST; ++t) {
+      const int idx = t * 64 + lane;
+      const int pos = blk * 16 + ((idx / VPR) & 15);
+      const int n = n0 + (idx % VPR) * E::per_vec;
       const bool ok = idx < 16 * VPR && pos < nrows && n < Cout;
       const uint32_t off =
-          ok ? ((uint32_t)(row0 + perm[pos]) * (uint32_t)Cout + (uint32_t)n) * E::bytes
+          ok ? ((uint32_t)(row0 + prow[t]) * (uint32_t)Cout + (uint32_t)n) * E::bytes
              : kOutOfRange;
-      const i32x4 v = *reinterpret_cast<const i32x4*>(my_scratch + r * WROW + q * 16);
-      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, v), o_rsrc, off, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u32, sv[t]), o_rsrc, off, 0, 0);
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -588,6 +607,12 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   for (int u = 0; u < D; ++u) {
     jobs[u] = next_job();
     issue(jobs[u], fr[u]);
+  }
+  // the resident B fragments are read once the first A loads are in flight
+  if constexpr (kResidentB) {
+#pragma unroll
+    for (int ks = 0; ks < KSM; ++ks)
+      read_b(ks < KS ? wl + ks * E::kstep * WROWW : zrows, wres[kResidentB ? ks : 0]);
   }
   // Every ring slot is processed on every trip (an exhausted job computes
   // nothing and reloads a dummy address), so the loads of the other D - 1
