@@ -22,7 +22,10 @@ exist twice (three times with a side stream).  ``run(steps)`` uses this for
 consecutive batches: the compaction of batch k + 1 goes into another set and
 is enqueued before the scatter and pool of batch k, so the host learns the
 next active count while the GPU still has batch k's tail to run, and the
-stream never idles on that wait.  Every batch still runs the whole path.
+stream never idles on that wait.  With a side stream the compaction runs on
+it, and the scatter and pool of batch k run on a third stream beside batch
+k + 1's layers (the last layer's output alternates between two buffers).
+Every batch still runs the whole path.
 
 This module only moves buffers and issues calls; all arithmetic runs in the
 library's kernels.
@@ -85,24 +88,38 @@ class _IndexSet:
                                                             self.table, stream=st.side)
                            if self.table is not None and st.side is not None and not self.fused
                            else None)
-        self.layers = []
-        for l, spec in enumerate(st.w.layers):
-            src, dst = st.acts[l], st.acts[l + 1]
-            a = st.act if spec.relu else shc.SHC_ACT_NONE
-            if spec.kind == "conv":
-                call = shc.prepare_sparse_neighbor_conv_table(src, self.table, st.weights[l],
-                                                              st.biases[l], dst, a)
-            elif l == 0 and st.fused_gather:
-                call = shc.prepare_gather_sparse_linear(st.x, self.coords, B, V, st.weights[l],
-                                                        st.biases[l], dst, a)
-            else:
-                call = shc.prepare_sparse_linear(src, st.weights[l], st.biases[l], dst, a)
-            self.layers.append(call)
+        self.layers = [self._layer_call(st, l, st.acts[l + 1]) for l in range(len(st.w.layers))]
         last = st.acts[-1]
         self.scatter = (shc.prepare_scatter(last, self.inv, self.coords, B, V, st.dense_out)
                         if st.dense_out is not None else None)
         self.pool = (shc.prepare_segment_maxpool(last, self.row_ptr, B, st.pooled, 0.0)
                      if st.pooled is not None else None)
+        # run() with a side stream: the last layer writes one of two buffers
+        # (acts[-1] or st.last_alt), and the scatter and pool of that buffer
+        # run on the tail stream
+        self.last_into = self.scatter_tail = self.pool_tail = None
+        if st.tail is not None and st.w.layers:
+            L = (st.acts[-1], st.last_alt)
+            self.last_into = [self._layer_call(st, len(st.w.layers) - 1, L[i]) for i in range(2)]
+            self.scatter_tail = [shc.prepare_scatter(L[i], self.inv, self.coords, B, V,
+                                                     st.dense_out, stream=st.tail)
+                                 if st.dense_out is not None else None for i in range(2)]
+            self.pool_tail = [shc.prepare_segment_maxpool(L[i], self.row_ptr, B, st.pooled, 0.0,
+                                                          stream=st.tail)
+                              if st.pooled is not None else None for i in range(2)]
+
+    def _layer_call(self, st: "SparseStack", l: int, dst: torch.Tensor):
+        """Layer l of the stack on this index set, writing dst."""
+        spec = st.w.layers[l]
+        src = st.acts[l]
+        a = st.act if spec.relu else shc.SHC_ACT_NONE
+        if spec.kind == "conv":
+            return shc.prepare_sparse_neighbor_conv_table(src, self.table, st.weights[l],
+                                                          st.biases[l], dst, a)
+        if l == 0 and st.fused_gather:
+            return shc.prepare_gather_sparse_linear(st.x, self.coords, st.B, st.V, st.weights[l],
+                                                    st.biases[l], dst, a)
+        return shc.prepare_sparse_linear(src, st.weights[l], st.biases[l], dst, a)
 
 
 class SparseStack:
@@ -110,14 +127,18 @@ class SparseStack:
                  side_stream: bool = False):
         self.w = w
         self.device = torch.device(device)
-        # second stream (default priority) for the next batch's compaction and
-        # table in run(); None: everything on the current stream
+        # with side_stream, run() uses two more streams (default priority): the
+        # side stream for the next batch's compaction and table, the tail stream
+        # for each batch's scatter and pool; None: everything on the current one
         self.side = torch.cuda.Stream(device=self.device) if side_stream else None
+        self.tail = torch.cuda.Stream(device=self.device) if side_stream else None
         self._events = None
         if side_stream:
             with torch.cuda.device(self.device):
-                self._events = ([shc.StreamEvent() for _ in range(3)], shc.StreamEvent(),
-                                shc.StreamEvent())
+                ev = shc.StreamEvent
+                self._events = dict(set_free=[ev() for _ in range(3)], ready=ev(), fed=ev(),
+                                    last_done=[ev() for _ in range(2)],
+                                    tail_done=[ev() for _ in range(2)], tail_end=ev())
         self.dtype = TORCH_DTYPE[w.dtype]
         self.B, self.V, self.K = w.B, w.V, w.K
         self.act = act
@@ -132,6 +153,8 @@ class SparseStack:
         # activations: gathered input + one buffer per layer
         chans = [w.C0] + [l.Cout for l in w.layers]
         self.acts = [torch.empty((BV, c), dtype=self.dtype, device=dev) for c in chans]
+        # second buffer of the last layer's output (run() with side_stream)
+        self.last_alt = torch.empty_like(self.acts[-1]) if side_stream else None
         Cl = chans[-1]
         self.dense_out = torch.empty((BV, Cl), dtype=self.dtype, device=dev) if w.scatter else None
         self.pooled = torch.empty((self.B, Cl), dtype=self.dtype, device=dev) if w.pool else None
@@ -225,7 +248,8 @@ class SparseStack:
             feed: Optional[Callable[[int], None]] = None) -> int:
         """`steps` passes of the whole path over consecutive batches, the
         compaction of each batch overlapped with the scatter and pool of the
-        one before (module docstring).
+        one before (module docstring); with a side stream, each batch's scatter
+        and pool also run beside the next batch's layers (_run_two_streams).
 
         ``feed(k)``, if given, is called just before batch k's compaction is
         enqueued and may write batch k's mask and features into ``mask`` and
@@ -236,7 +260,7 @@ class SparseStack:
         last batch's.  Returns its N'."""
         if steps <= 0:
             return self.n or 0
-        if self.side is not None:
+        if self.side is not None and self.w.layers:
             return self._run_two_streams(steps, around_layer, feed)
         s = self._set
         if feed is not None:
@@ -265,28 +289,35 @@ class SparseStack:
         return s.n
 
     def _run_two_streams(self, steps: int, around_layer, feed) -> int:
-        """run() with batch k + 1's compaction and neighbour table on the side
-        stream, beside batch k's scatter and pool on the current stream.
+        """run() over three streams: the current stream runs each batch's
+        layers; the side stream the next batch's compaction (which also
+        writes its neighbour-row table); the tail stream each batch's scatter
+        and pool, beside the next batch's layers.
 
-        The three index sets rotate, so batch k + 1's compaction writes the set
-        whose last reader was the pool of batch k - 2.  The host checks that
-        this pool has finished (an event on the current stream, synchronised
-        from the host; the host runs at most about two batches ahead, so it has
-        almost always finished) instead of making the side stream wait for it
-        on the GPU: a side stream that waits on the current stream's events
-        and is waited on by it costs the current stream several microseconds a
-        batch, while a wait in one direction only (current on side) costs
-        nothing measurable.  The current stream starts batch k + 1's layers
-        only after its table (an event on the side stream).  With ``feed``,
-        the side stream also waits on the GPU for the writes of ``feed``.
-        The events carry no system-scope fence (shc_event_create): a default
-        event's cache write-back at every record costs the step a few
-        microseconds more.  Every batch runs the whole path."""
+        The last layer writes one of two buffers (acts[-1], last_alt) in turn,
+        the last batch into acts[-1], so the scatter and pool of batch k read
+        theirs while batch k + 1's layers write the other.  Three index sets
+        rotate: batch k + 1's compaction writes the set last read by batch
+        k - 2's scatter and pool, and the host checks that they have finished
+        (an event on the tail stream, synchronised from the host; the host
+        runs at most about two batches ahead, so it has almost always fired)
+        instead of making the side stream wait for it on the GPU.  GPU waits:
+        the current stream on the side stream's table before a batch's layers
+        and on the tail stream before it overwrites a buffer the tail still
+        reads; the tail stream on the current stream's last layer of its
+        batch; the side stream on ``feed``'s writes.  At the end the current
+        stream waits for the tail stream, so work the caller enqueues after
+        run() sees the last batch's scatter and pool.  The events carry no
+        system-scope fence (shc_event_create): a default event's cache
+        write-back at every record costs the step microseconds.  Every batch
+        runs the whole path."""
         main = torch.cuda.current_stream(self.device)
-        side = self.side
+        side, tail = self.side, self.tail
+        ev = self._events
         ns = len(self._sets)
-        free, ready, fed = self._events    # free[i]: set i released by its last reader
-        used = [False] * ns
+        set_used = [False] * ns
+        buf_used = [False, False]
+        nl = len(self.w.layers)
         cur = self._cur
         s = self._sets[cur]
         if feed is not None:
@@ -295,35 +326,59 @@ class SparseStack:
         s.n = s.compact.wait()
         table_done = s.fused
         for k in range(steps):
-            ev = None
+            i = (steps - 1 - k) % 2        # the last batch writes acts[-1]
+            around = None
             if around_layer is not None and around_layer[1][k][0] is not None:
-                ev = (around_layer[0], *around_layer[1][k])
-            self._front(s, ev, table_done=table_done)
+                around = (around_layer[0], *around_layer[1][k])
+            # layers of batch k (current stream)
+            if s.table_call is not None and not table_done:
+                s.table_call(s.n)
+            if not self.fused_gather:
+                s.gather(s.n)
+            for l in range(nl):
+                call = s.layers[l]
+                if l == nl - 1:
+                    if buf_used[i]:
+                        ev["tail_done"][i].wait(main)
+                    call = s.last_into[i]
+                if around is not None and around[0] == l:
+                    around[1].record()
+                call(s.n)
+                if around is not None and around[0] == l:
+                    around[2].record()
+            ev["last_done"][i].record(main)
+            buf_used[i] = True
+            # compaction of batch k + 1 (side stream)
             nxt_i = (cur + 1) % ns
             nxt = self._sets[nxt_i] if k + 1 < steps else None
             if nxt is not None:
                 if feed is not None:
                     feed(k + 1)
-                    fed.record(main)
-                    fed.wait(side)
-                if used[nxt_i]:
-                    free[nxt_i].synchronize()
+                    ev["fed"].record(main)
+                    ev["fed"].wait(side)
+                if set_used[nxt_i]:
+                    ev["set_free"][nxt_i].synchronize()
                 nxt.compact_side.start()
-            if s.scatter is not None:
-                s.scatter(s.n)
-            if s.pool is not None:
-                s.pool(s.n)
-            free[cur].record(main)
-            used[cur] = True
+            # scatter and pool of batch k (tail stream)
+            ev["last_done"][i].wait(tail)
+            if s.scatter_tail[i] is not None:
+                s.scatter_tail[i](s.n)
+            if s.pool_tail[i] is not None:
+                s.pool_tail[i](s.n)
+            ev["tail_done"][i].record(tail)
+            ev["set_free"][cur].record(tail)
+            set_used[cur] = True
             if nxt is not None:
                 nxt.n = nxt.compact_side.wait()
                 if nxt.table_side is not None:
                     nxt.table_side(nxt.n)
                 table_done = nxt.table is not None    # built on the side stream
-                ready.record(side)
-                ready.wait(main)
+                ev["ready"].record(side)
+                ev["ready"].wait(main)
                 cur = nxt_i
                 s = nxt
+        ev["tail_end"].record(tail)
+        ev["tail_end"].wait(main)
         self._cur = cur
         return s.n
 

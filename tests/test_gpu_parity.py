@@ -1050,3 +1050,35 @@ def test_compact_table_start(dev, B, V, K, p, cap_delta):
     got_t = down(table)
     assert np.array_equal(got_t[:K * n].reshape(K, n), table_reference(m, nbr))
     assert np.all(got_t[K * n:] == -7)
+
+
+@pytest.mark.parametrize("steps", [1, 4])
+def test_overlapped_run_conv_only_stack(dev, steps):
+    """SparseStack.run with a side stream on a stack of four convs that ends in
+    the pool (no fused gather, several layers before the double-buffered last
+    one): a new mask and new features per batch; the outputs left behind must
+    be the oracle's for the last batch."""
+    from paper_2608_09388_amd.pipeline import SparseStack, to_device
+    w = synth.workload_c2()
+    w.B = 12
+    w.mask = w.mask[:12]
+    w.x = w.x[: 12 * w.V]
+    rng = np.random.default_rng(700 + steps)
+    masks = [(rng.random((w.B, w.V)) < p).astype(np.uint8) for p in (0.1, 0.3, 0.05, 0.2)][:steps]
+    xs = [synth.as_dtype(rng.standard_normal(w.x.shape).astype(np.float32), w.dtype)[1]
+          for _ in range(steps)]
+    st = SparseStack(w, device=str(dev), side_stream=True)
+    st.run(3)
+
+    def feed(k):
+        st.mask.copy_(up(masks[k].reshape(-1)))
+        st.x.copy_(to_device(xs[k], w.dtype, st.device))
+
+    n = st.run(steps, feed=feed)
+    spec = [(l.kind, l.W, l.bias, l.relu) for l in w.layers]
+    ref = O.run_stack(xs[-1], masks[-1], w.nbr, spec, w.dtype, pool=True)
+    got = st.results()
+    assert n == ref["n"] == got["n"]
+    for l in range(len(w.layers)):
+        assert_normwise_close(got["outs"][l], ref["outs"][l], w.dtype, f"layer {l}")
+    assert_normwise_close(got["pool"], ref["pool"], w.dtype, "pool")
