@@ -1082,3 +1082,35 @@ def test_overlapped_run_conv_only_stack(dev, steps):
     for l in range(len(w.layers)):
         assert_normwise_close(got["outs"][l], ref["outs"][l], w.dtype, f"layer {l}")
     assert_normwise_close(got["pool"], ref["pool"], w.dtype, "pool")
+
+
+def test_overlapped_run_table_on_its_own(dev):
+    """Bodies of more vertices than the compaction keeps on chip (V = 20000):
+    the side stream builds the neighbour-row table with its own call after the
+    compaction.  A new mask and new features per batch over three batches;
+    the outputs left behind must be the oracle's for the last batch."""
+    from paper_2608_09388_amd.pipeline import SparseStack, to_device
+    w = synth.workload_c4(0.05, B=2, V=20000)
+    rng = np.random.default_rng(901)
+    masks = [(rng.random((w.B, w.V)) < p).astype(np.uint8) for p in (0.05, 0.2, 0.1)]
+    xs = [synth.as_dtype(rng.standard_normal(w.x.shape).astype(np.float32), w.dtype)[1]
+          for _ in range(3)]
+    st = SparseStack(w, device=str(dev), side_stream=True)
+    assert not st._set.fused and st._set.table_side is not None
+    st.run(2)
+
+    def feed(k):
+        st.mask.copy_(up(masks[k].reshape(-1)))
+        st.x.copy_(to_device(xs[k], w.dtype, st.device))
+
+    n = st.run(3, feed=feed)
+    spec = [(l.kind, l.W, l.bias, l.relu) for l in w.layers]
+    ref = O.run_stack(xs[-1], masks[-1], w.nbr, spec, w.dtype, pool=True)
+    got = st.results()
+    assert n == ref["n"] == got["n"]
+    assert np.array_equal(got["coords"], ref["coords"])
+    for l in range(len(w.layers)):
+        assert_normwise_close(got["outs"][l], ref["outs"][l], w.dtype, f"layer {l}")
+    assert_normwise_close(got["dense"], O.scatter(ref["outs"][-1], ref["inv"], zero_fill=True),
+                          w.dtype, "dense")
+    assert_normwise_close(got["pool"], ref["pool"], w.dtype, "pool")
