@@ -1114,3 +1114,35 @@ def test_overlapped_run_table_on_its_own(dev):
     assert_normwise_close(got["dense"], O.scatter(ref["outs"][-1], ref["inv"], zero_fill=True),
                           w.dtype, "dense")
     assert_normwise_close(got["pool"], ref["pool"], w.dtype, "pool")
+
+
+@pytest.mark.parametrize("B,V,K,Cout,p", [
+    (4, 3000, 9, 128, 0.05),     # few rows per workgroup
+    (6, 2000, 10, 64, 0.3),      # ten slots, Cout 64
+    (3, 1000, 1, 128, 0.5),      # one slot
+    (5, 1500, 4, 16, 0.9),       # four slots, Cout 16, dense mask
+    (90, 10475, 9, 128, 0.1),    # about 94 K rows
+    (128, 10475, 9, 128, 0.05),  # the density-sweep batch at 5%
+])
+def test_conv_cin128_table_parity(dev, B, V, K, Cout, p):
+    """The bf16 conv from a table with C_in = 128, at row counts from one small
+    workgroup per CU to the density-sweep batch, against the oracle on sampled
+    rows plus the first and last 400 rows, and bit for bit against the direct
+    path (index lists built from coords, inv and nbr inside the kernel)."""
+    rng = np.random.default_rng(B * 17 + V + K * 3 + Cout)
+    m = (rng.random((B, V)) < p).astype(np.uint8)
+    nbr = rand_nbr(V, K, rng)
+    coords, inv, rp, n = O.compact(m)
+    S = synth.as_dtype(rng.standard_normal((n, 128)).astype(np.float32), "bf16")[1]
+    W = synth.as_dtype((rng.standard_normal((K, 128, Cout)) / np.sqrt(K * 128))
+                       .astype(np.float32), "bf16")[1]
+    bias = rng.standard_normal(Cout).astype(np.float32)
+    g_tab, n2 = run_conv(dev, m, nbr, S, W, bias, "bf16", shc.SHC_ACT_RELU, "table")
+    g_dir, _ = run_conv(dev, m, nbr, S, W, bias, "bf16", shc.SHC_ACT_RELU, "direct")
+    assert n2 == n
+    assert np.array_equal(g_tab, g_dir)
+    rows = np.unique(np.concatenate([np.arange(min(n, 400)), np.arange(max(0, n - 400), n),
+                                     rng.choice(n, size=min(n, 600), replace=False)]))
+    ref = O.conv_at(S, coords, B, V, nbr, W, rows, bias, act=True)
+    scale = O.conv_at(S, coords, B, V, nbr, W, rows, bias, scale=True)
+    assert_scaled_close(g_tab[rows], ref, scale, "bf16", f"conv K={K} 128->{Cout} p={p}")
