@@ -161,8 +161,8 @@ class SparseStack:
         # A first linear layer reads its rows straight from x (gather fused in);
         # otherwise the active rows are gathered into acts[0] first.
         self.fused_gather = len(w.layers) > 0 and w.layers[0].kind == "linear"
-        # two index sets, or three with a side stream (run() then keeps the
-        # side stream off the current stream's events; see _run_two_streams)
+        # two index sets, or three with a side stream (run() then checks an
+        # index set's reuse from the host; see _run_pipelined)
         self._sets = [_IndexSet(self) for _ in range(3 if side_stream else 2)]
         self._cur = 0
 
@@ -249,7 +249,7 @@ class SparseStack:
         """`steps` passes of the whole path over consecutive batches, the
         compaction of each batch overlapped with the scatter and pool of the
         one before (module docstring); with a side stream, each batch's scatter
-        and pool also run beside the next batch's layers (_run_two_streams).
+        and pool also run beside the next batch's layers (_run_pipelined).
 
         ``feed(k)``, if given, is called just before batch k's compaction is
         enqueued and may write batch k's mask and features into ``mask`` and
@@ -261,7 +261,7 @@ class SparseStack:
         if steps <= 0:
             return self.n or 0
         if self.side is not None and self.w.layers:
-            return self._run_two_streams(steps, around_layer, feed)
+            return self._run_pipelined(steps, around_layer, feed)
         s = self._set
         if feed is not None:
             feed(0)
@@ -288,7 +288,7 @@ class SparseStack:
                 s = nxt
         return s.n
 
-    def _run_two_streams(self, steps: int, around_layer, feed) -> int:
+    def _run_pipelined(self, steps: int, around_layer, feed) -> int:
         """run() over three streams: the current stream runs each batch's
         layers; the side stream the next batch's compaction (which also
         writes its neighbour-row table); the tail stream each batch's scatter
