@@ -309,6 +309,8 @@ def main():
         "kernel_rooflines": kernel_rooflines,
     }
 
+    out["gather_scatter"] = gather_scatter_measure(shc, synth, torch, args.reps)
+    log("gather and scatter measured")
     out["next_rows"] = {"group_norm": group_norm_measure(st, shc, torch, args.reps),
                         "multi_mask": multi_mask_measure(st, w, shc, synth, torch, args.reps),
                         "mask_scores": mask_scores_measure(w, shc, torch, args.reps),
@@ -428,6 +430,53 @@ def _time_us(fn, torch, reps):
     b.record()
     torch.cuda.synchronize()
     return a.elapsed_time(b) / reps * 1e3
+
+
+def gather_scatter_measure(shc, synth, torch, reps):
+    """The row gather (S' of Eq. 2) and the zero-fill scatter on their own, on
+    the masks of the full-mesh (B = 256, V = 10475, C = 64: the cap as written
+    and its 5% variant, fp32 and bf16), density-sweep (B = 128, C = 128 bf16,
+    5%) and sequence (2048 frames of V = 655, C = 256 bf16, Markov runs)
+    workloads: HBM rates against the algorithmic bytes, 8 + 2 C e per active
+    row for the gather and C e per active row + (4 + C e) per dense vertex for
+    the scatter.  Features are N(0, 1) made on the device."""
+    dev = torch.device("cuda:0")
+    pts3, _ = synth.mesh("ellipsoid", 10475, 9, 3)
+    cases = [("full mesh, cap y<-0.6", lambda: synth.cap_mask(pts3, 256, -0.6, 0.02, synth._rng(3, 1)), 64, "f32"),
+             ("full mesh, 5% cap", lambda: synth.cap_mask(pts3, 256, -0.845, 0.02, synth._rng(3, 1)), 64, "f32"),
+             ("full mesh, 5% cap", lambda: synth.cap_mask(pts3, 256, -0.845, 0.02, synth._rng(3, 1)), 64, "bf16"),
+             ("density sweep 5%", lambda: synth.bernoulli_mask(128, 10475, 0.05, synth._rng(4, 1)), 128, "bf16"),
+             ("sequences", lambda: synth.markov_mask(32, 64, 655, 0.10, 8.0, synth._rng(5, 1)), 256, "bf16")]
+    out = []
+    for name, mk, C, dt in cases:
+        m = mk()
+        B, V = m.shape
+        td = torch.float32 if dt == "f32" else torch.bfloat16
+        e = 4 if dt == "f32" else 2
+        md = torch.from_numpy(np.ascontiguousarray(m.reshape(-1))).to(dev)
+        coords = torch.empty((B * V, 2), dtype=torch.int32, device=dev)
+        inv = torch.empty(B * V, dtype=torch.int32, device=dev)
+        rp = torch.empty(B + 1, dtype=torch.int32, device=dev)
+        nd = torch.empty(4, dtype=torch.int32, device=dev)
+        ws = torch.empty(max(shc.compact_mask_workspace(B, V), 16), dtype=torch.uint8, device=dev)
+        n = shc.compact_mask(md, B, V, coords, inv, rp, nd, ws)
+        x = torch.randn((B * V, C), device=dev).to(td)
+        S = torch.empty((max(n, 1), C), dtype=td, device=dev)
+        D = torch.empty((B * V, C), dtype=td, device=dev)
+        # prepared calls: one ctypes call per launch, so the host keeps ahead
+        gather = shc.prepare_gather_rows(x, coords, B, V, S)
+        scatter = shc.prepare_scatter(S, inv, coords, B, V, D)
+        g_us = _time_us(lambda: gather(n), torch, reps)
+        s_us = _time_us(lambda: scatter(n), torch, reps)
+        g_b = n * (8 + 2 * C * e)
+        s_b = n * C * e + B * V * (4 + C * e)
+        out.append({"workload": name, "B": B, "V": V, "C": C, "dtype": dt, "n_active": n,
+                    "gather_us": round(g_us, 2),
+                    "gather_frac_hbm": round(g_b / (g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                    "scatter_us": round(s_us, 2),
+                    "scatter_frac_hbm": round(s_b / (s_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
+        del gather, scatter, x, S, D, coords, inv
+    return out
 
 
 def multi_mask_measure(st, w, shc, synth, torch, reps, kappa=3):
