@@ -100,7 +100,15 @@ __host__ __device__ inline int ws_scratch(int ws, int e, int waves) {
 
 // KM: slots held per row in registers during the index build (>= K).
 // KSM: k-steps per slot held per job (>= Cin / kstep); D jobs in flight.
-template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM>
+// 16 bytes per lane from global memory straight into LDS: lane i's vector
+// lands at dst + 16 i (dst is the wavefront's LDS base)
+__device__ __forceinline__ void lds_direct_load16(const void* src, SHC_LDS void* dst) {
+  __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+}
+
+// DW: the weight slice goes straight into LDS with 16-byte direct loads, all
+// issued first (bf16, full column slices, a multiple of 64 vectors).
+template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM, bool DW = false>
 __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kernel(GemmArgs a,
                                                                                    int R) {
   constexpr int kThreads = CONV ? kThreadsConv : kThreadsLin;
@@ -191,7 +199,23 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
     }
   };
   i32x4 wv[kWBatch];
-  load_w(0, wv);
+  if constexpr (DW) {
+    // LDS vector v = 64 c + lane of the slice is row k = v / VPR, position
+    // p = v % VPR; it holds source vector q with w_col(k, q) = 16 p (the
+    // chunk swizzle is its own inverse).  A wavefront's direct load writes
+    // 64 consecutive vectors; the waits come before the prologue's last barrier.
+    for (int c = wave; c < wvecs / 64; c += kWaves) {
+      const int v = c * 64 + lane;
+      const int k = v / VPR;
+      const int p = v - k * VPR;
+      const int h = ((k >> 1) ^ (k >> 3)) & 1;
+      const int q = NCB >= 2 ? 2 * ((p >> 1) ^ h) + (p & 1) : p;
+      lds_direct_load16(W + ((int64_t)k * Cout + n0 + q * E::per_vec) * E::bytes,
+                        (SHC_LDS void*)(wl + c * 1024));
+    }
+  } else {
+    load_w(0, wv);
+  }
 
   for (int q = tid; q < R / 16; q += kThreads) blkmask[q] = 0;
   for (int q = tid; q < kBuckets; q += kThreads) bcnt[q] = 0;  // the sort's histogram
@@ -212,14 +236,16 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
         for (int j = 0; j < KM; ++j)
           sv[rr][j] = a.table[(int64_t)(j < K ? j : K - 1) * a.n_rows + i];
       }
-      store_w(0, wv);
-      load_w(kWBatch * kThreads, wv);  // possibly all dummies: kept unconditional
+      if constexpr (!DW) {
+        store_w(0, wv);
+        load_w(kWBatch * kThreads, wv);  // possibly all dummies: kept unconditional
+      }
 #pragma unroll
       for (int rr = 0; rr < kRPT; ++rr)
 #pragma unroll
         for (int j = 0; j < KM; ++j)
           if (j >= K || tid + rr * kThreads >= nrows) sv[rr][j] = -1;
-      store_w(kWBatch * kThreads, wv);
+      if constexpr (!DW) store_w(kWBatch * kThreads, wv);
     } else {
       int rb[kRPT], rv[kRPT];
 #pragma unroll
@@ -267,9 +293,11 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
       }
     }
     // weight vectors past the first two batches (large slices only)
-    for (int base = 2 * kWBatch * kThreads; base < wvecs; base += kWBatch * kThreads) {
-      load_w(base, wv);
-      store_w(base, wv);
+    if constexpr (!DW) {
+      for (int base = 2 * kWBatch * kThreads; base < wvecs; base += kWBatch * kThreads) {
+        load_w(base, wv);
+        store_w(base, wv);
+      }
     }
     // rows per slot, then the dense slots
     for (int j = 0; j < K; ++j) {
@@ -354,6 +382,7 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
     }
     for (int q = tid; q < R / 16; q += kThreads) blkmask[q] = (16 * q < nrows) ? 1u : 0u;
   }
+  if constexpr (DW) __builtin_amdgcn_s_waitcnt(0);  // this wavefront's direct loads are in LDS
   __syncthreads();
 
   // ---- per-wave job loop -----------------------------------------------------------
@@ -628,11 +657,11 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   }
 }
 
-template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM>
+template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM, bool DW = false>
 hipError_t launch_ws(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) {
   const unsigned gx = (unsigned)((a.n_rows + pl.rows - 1) / pl.rows);
   const unsigned gy = (unsigned)((a.Cout + WS - 1) / WS);
-  auto kern = ws_kernel<BF16, WS, CONV, TBL, KM, KSM>;
+  auto kern = ws_kernel<BF16, WS, CONV, TBL, KM, KSM, DW>;
   // allow the large dynamic LDS allocation; once per instantiation
   static std::once_flag once;
   static hipError_t attr_err = hipSuccess;
@@ -655,8 +684,13 @@ hipError_t launch_ws_k(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) 
     return launch_ws<BF16, WS, false, false, 1, 8>(a, pl, stream);
   }
   if (a.table != nullptr) {
-    if (ks <= 4) return launch_ws<BF16, WS, true, true, 10, 4>(a, pl, stream);
-    return launch_ws<BF16, WS, true, true, 10, 8>(a, pl, stream);
+    // direct weight loads: full column slices, whole 64-vector chunks
+    const bool dw = BF16 && a.Cout % WS == 0 && ((int64_t)a.K * a.Cin * (WS * 2 / 16)) % 64 == 0;
+    if (ks <= 4)
+      return dw ? launch_ws<BF16, WS, true, true, 10, 4, BF16>(a, pl, stream)
+                : launch_ws<BF16, WS, true, true, 10, 4>(a, pl, stream);
+    return dw ? launch_ws<BF16, WS, true, true, 10, 8, BF16>(a, pl, stream)
+              : launch_ws<BF16, WS, true, true, 10, 8>(a, pl, stream);
   }
   if (ks <= 4) return launch_ws<BF16, WS, true, false, 10, 4>(a, pl, stream);
   return launch_ws<BF16, WS, true, false, 10, 8>(a, pl, stream);
