@@ -107,7 +107,8 @@ __device__ __forceinline__ void lds_direct_load16(const void* src, SHC_LDS void*
 }
 
 // DW: the weight slice goes straight into LDS with 16-byte direct loads, all
-// issued first (bf16, full column slices, a multiple of 64 vectors).
+// issued first (bf16, full column slices, a multiple of 64 vectors; conv from
+// a table, or linear).
 template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM, bool DW = false>
 __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kernel(GemmArgs a,
                                                                                    int R) {
@@ -366,9 +367,11 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
       cr[rr] = a.gather ? reinterpret_cast<const int2*>(a.coords)[row0 + (t < nrows ? t : 0)]
                         : int2{0, 0};
     }
-    for (int base = 0; base < wvecs; base += kWBatch * kThreads) {
-      if (base > 0) load_w(base, wv);
-      store_w(base, wv);
+    if constexpr (!DW) {
+      for (int base = 0; base < wvecs; base += kWBatch * kThreads) {
+        if (base > 0) load_w(base, wv);
+        store_w(base, wv);
+      }
     }
 #pragma unroll
     for (int rr = 0; rr < kRPT; ++rr) {
@@ -680,8 +683,13 @@ hipError_t launch_ws_k(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) 
   constexpr int kstep = BF16 ? 32 : 16;
   const int ks = a.Cin / kstep;
   if (!CONV) {
-    if (ks <= 4) return launch_ws<BF16, WS, false, false, 1, 4>(a, pl, stream);
-    return launch_ws<BF16, WS, false, false, 1, 8>(a, pl, stream);
+    // direct weight loads: full column slices, whole 64-vector chunks
+    const bool dw = BF16 && a.Cout % WS == 0 && ((int64_t)a.Cin * (WS * 2 / 16)) % 64 == 0;
+    if (ks <= 4)
+      return dw ? launch_ws<BF16, WS, false, false, 1, 4, BF16>(a, pl, stream)
+                : launch_ws<BF16, WS, false, false, 1, 4>(a, pl, stream);
+    return dw ? launch_ws<BF16, WS, false, false, 1, 8, BF16>(a, pl, stream)
+              : launch_ws<BF16, WS, false, false, 1, 8>(a, pl, stream);
   }
   if (a.table != nullptr) {
     // direct weight loads: full column slices, whole 64-vector chunks
