@@ -1010,6 +1010,7 @@ def test_stream_events_order_streams(dev):
     (3, 10475, 9, 0.05, None),    # 1024-thread blocks, the mesh size of the 10,475-vertex bodies
     (2, 19456, 5, 0.5, None),     # the largest V, two passes
     (7, 333, 32, 0.4, None),      # 32 slots
+    (2, 5000, 32, 0.3, None),     # 32 slots, 1024-thread blocks
     (6, 97, 1, 0.9, None),        # one slot
     (9, 211, 9, 0.0, None),       # empty mask
     (4, 300, 9, 1.0, None),       # every vertex active
