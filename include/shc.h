@@ -333,8 +333,9 @@ int shc_clear_inactive_rows(const int32_t* inv, int32_t B, int32_t V, int32_t C,
  *   S [n_rows][C], row_ptr [B+1] (bounds clamped to [0, n_rows]), out
  *   [n_rows][C] of the same dtype, must not overlap S.  G must divide C; eps
  *   must be positive and finite (1e-5 is the usual value).
- * Statistics are accumulated in fp32 (two passes: the mean, then the squared
- * deviations from it); bf16 outputs are rounded to nearest even.
+ * Statistics are accumulated in fp64 (two passes: the mean, then the squared
+ * deviations from it); each output is evaluated in fp64 and rounded once to
+ * fp32, then (bf16 outputs) to bf16, to nearest even.
  */
 int shc_segment_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
                            int32_t C, int32_t G, float eps, int32_t dtype, void* out,
@@ -347,7 +348,9 @@ int shc_segment_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows
  * O [K][N][C] bf16:
  *
  *   F[i][k]      = || O_i^T O_k ||_F^2
- *   sim[i][k]    = F[i][k] / sqrt(F[i][i] * F[k][k])      (0 where that is 0)
+ *   sim[i][k]    = F[i][k] / sqrt(F[i][i] * F[k][k]), or 1 where that
+ *                  denominator is 0 (a mask whose output is all zero earns
+ *                  no dissimilarity credit, so it ranks last among equals)
  *   alpha_out[k] = alpha_in[k] + 1/(K-1) * sum_{i != k} (1 - sim[i][k])
  *                  (alpha_in[k] itself when K = 1)
  *   top[r]       = the mask of rank r by alpha_out, largest first, ties to

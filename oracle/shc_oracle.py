@@ -180,12 +180,6 @@ def sparse_conv(S, coords, B, V, nbr, W, bias=None, act=False):
     return restrict(y, coords, V)
 
 
-def sparse_linear_scale(S, coords, B, V, W, bias=None):
-    """Abs-sum of every output's dot product: sum |s_t||w_t| + |b| (error scale)."""
-    return sparse_linear(np.abs(np.asarray(S, np.float64)), coords, B, V, np.abs(W),
-                         None if bias is None else np.abs(bias))
-
-
 def sparse_conv_scale(S, coords, B, V, nbr, W, bias=None):
     """Abs-sum of every output's dot product over all slots (error scale)."""
     return sparse_conv(np.abs(np.asarray(S, np.float64)), coords, B, V, nbr, np.abs(W),
@@ -344,10 +338,16 @@ def gram_frobenius(O: np.ndarray) -> np.ndarray:
 
 
 def mask_similarity(O: np.ndarray) -> np.ndarray:
-    """sim[i][k] = ||O_i^T O_k||_F^2 / (||O_k^T O_k||_F ||O_i^T O_i||_F) (Eq. 3)."""
+    """sim[i][k] = ||O_i^T O_k||_F^2 / (||O_k^T O_k||_F ||O_i^T O_i||_F) (Eq. 3).
+
+    Eq. 3 leaves the quotient undefined when one of the two outputs is all
+    zero.  Such a mask adds nothing beyond the others, so it is given no
+    dissimilarity credit: the similarity of a pair with a zero output is 1
+    (which is also every output's similarity with itself)."""
     F = gram_frobenius(O)
     d = np.sqrt(np.diag(F))
-    return F / np.outer(d, d)
+    den = np.outer(d, d)
+    return np.where(den > 0, F / np.where(den > 0, den, 1.0), 1.0)
 
 
 def alpha_update(alpha: np.ndarray, O: np.ndarray) -> np.ndarray:
@@ -448,6 +448,33 @@ def sparse_conv_backward(S, coords, B, V, nbr, W, dY, Y=None, act=False):
     return dS, dW, dZ.sum(axis=0)
 
 
+def conv_backward_weight_bias(S, coords, B, V, nbr, dZ, K, scale=False):
+    """dW and db of the sparse convolution from the pre-activation gradient dZ
+    of all active rows (for full-size checks, without the dense tensors).
+
+    Slot j's weight gradient sums, over the active rows i = (b, v) whose slot-j
+    neighbour u = nbr[v, j] is an active row r of the same body, the outer
+    product S[r]^T dZ[i]; rows with an absent neighbour add nothing.  db sums
+    dZ over the active rows.  With ``scale`` the abs-sum error scales
+    (sums of |S[r]|^T |dZ[i]| and of |dZ[i]|) are returned instead."""
+    S = np.asarray(S, dtype=np.float64)
+    dZ = np.asarray(dZ, dtype=np.float64)
+    if scale:
+        S, dZ = np.abs(S), np.abs(dZ)
+    n = dZ.shape[0]
+    where = np.full(B * V, -1, dtype=np.int64)         # coordinate -> row of C'
+    where[coords[:, 0].astype(np.int64) * V + coords[:, 1]] = np.arange(n)
+    b = coords[:, 0].astype(np.int64)
+    v = coords[:, 1].astype(np.int64)
+    dW = np.zeros((K, S.shape[1], dZ.shape[1]), dtype=np.float64)
+    for j in range(K):
+        u = nbr[v, j].astype(np.int64)
+        r = np.where(u >= 0, where[b * V + np.maximum(u, 0)], -1)
+        has = r >= 0
+        dW[j] = S[r[has]].T @ dZ[has]
+    return dW, dZ.sum(axis=0)
+
+
 def conv_backward_input_at(coords, B, V, nbr, W, dZ, rows, scale=False):
     """dS of the sparse convolution at selected active rows only, from the
     pre-activation gradient dZ of all active rows (for full-size checks).
@@ -542,8 +569,10 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
 
 
 def round_f32(x: np.ndarray) -> np.ndarray:
-    """Round fp64 values to fp32 storage (IEEE conversion), returned as fp64."""
-    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+    """Round fp64 values to fp32 storage (IEEE conversion, to nearest with ties
+    to even; past the largest finite value to +-inf), returned as fp64."""
+    with np.errstate(over="ignore"):
+        return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
 
 
 def store(x: np.ndarray, dtype: str) -> np.ndarray:

@@ -15,7 +15,11 @@
 // channel (4 fp32 or 8 bf16 channels), summed over the rows a wavefront holds
 // with lane shuffles, then through LDS over the wavefronts, then over the
 // channels of each group.  The statistics are
-// two-pass (the mean first, then the squared deviations from it) in fp32.
+// two-pass (the mean first, then the squared deviations from it) and held in
+// fp64 from the first addition on, so their rounding error (about n * 2^-53
+// relative for n values) stays far below the output's own rounding; every
+// output is (value - mu) * rsqrt(var + eps) evaluated in fp64 and rounded once
+// to fp32 (then to bf16 for bf16 outputs).
 // A body of up to kResident vectors per thread stays in registers, so HBM
 // sees one read and one write of every value; a larger body is streamed
 // three times (sums, deviations, output), the later passes mostly from L2.
@@ -75,9 +79,12 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
   using NV = NormVec<BF16>;
   constexpr int N = NV::N;
   // part[slot][Cl]: channel partials (one slot per thread row, or per
-  // wavefront after the shuffles); then chan[Cl], then per-group mean /
-  // reciprocal deviation broadcast back per channel
-  extern __shared__ float smem[];
+  // wavefront after the shuffles); then chan[Cl]; then stat[Cl], the group's
+  // mean / reciprocal deviation broadcast back per channel, which reuses the
+  // partials' space (every read of part precedes a barrier before stat is
+  // written, and a barrier at the start of each reduction keeps the next
+  // partials from overwriting stat while it is still being read)
+  extern __shared__ double smem[];
   const int TX = blockDim.x, TY = blockDim.y;  // TX = vectors of this workgroup's range
   const int ty = threadIdx.y;
   const int tid = ty * TX + threadIdx.x;
@@ -86,9 +93,9 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
   // rows a wavefront holds: 64 / TX when TX divides 64 (then reduced by shuffles)
   const int rw = (TX <= 64 && 64 % TX == 0) ? 64 / TX : 1;
   const int slots = rw > 1 ? (TX * TY) / 64 : TY;
-  float* part = smem;                 // [slots][Cl]
-  float* chan = smem + slots * Cl;    // [Cl]
-  float* stat = chan + Cl;            // [Cl]: the group's mean, then 1/sqrt(var + eps)
+  double* part = smem;                // [slots][Cl]
+  double* chan = smem + slots * Cl;   // [Cl]
+  double* stat = smem;                // [Cl]: the group's mean, then 1/sqrt(var + eps)
 
   int64_t lo = row_ptr[blockIdx.x], hi = row_ptr[blockIdx.x + 1];
   lo = lo < 0 ? 0 : (lo > n_rows ? n_rows : lo);
@@ -97,11 +104,13 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
   if (rows == 0) return;  // uniform over the workgroup
   const bool resident = rows <= TY * kResident;
   const int cg = C / G;
-  const float count = (float)rows * (float)cg;  // exact below 2^24
+  const double count = (double)rows * (double)cg;  // exact
+  const double deps = (double)eps;
 
   // this thread's channel partials -> per-channel totals over the rows ->
   // per group, into stat[] (the range's channels hold whole groups)
-  auto reduce = [&](float* acc, bool second) {
+  auto reduce = [&](double* acc, bool second) {
+    __syncthreads();  // the previous reduction's stat has been read
     if (rw > 1) {
       const int lane = tid & 63;
 #pragma unroll
@@ -121,9 +130,9 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
       // thread c: channel total (four independent partial sums), then the
       // group total by lane shuffles (cg <= 64) or per-wave partials (cg > 64)
       const int c = tid;
-      float t = 0.f;
+      double t = 0.0;
       if (c < Cl) {
-        float q[4] = {0.f, 0.f, 0.f, 0.f};
+        double q[4] = {0.0, 0.0, 0.0, 0.0};
         int y = 0;
         for (; y + 4 <= slots; y += 4)
 #pragma unroll
@@ -135,8 +144,8 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
       for (int d = 1; d < span; d <<= 1) t += __shfl_xor(t, d, 64);
       if (cg <= 64) {
         if (c < Cl && c % cg == 0) {
-          const float v = t / count;  // correctly rounded: an exact mean stays exact
-          chan[c] = second ? 1.0f / sqrtf(v + eps) : v;  // the group's first channel
+          const double v = t / count;  // correctly rounded: an exact mean stays exact
+          chan[c] = second ? 1.0 / sqrt(v + deps) : v;  // the group's first channel
         }
       } else if (c < Cl && (c & 63) == 0) {
         chan[c] = t;  // wave partial of the group, at the wave's first channel
@@ -144,25 +153,25 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
       __syncthreads();
       if (cg > 64) {
         for (int g = tid; g < Cl / cg; g += nt) {
-          float u = 0.f;
+          double u = 0.0;
           for (int w = g * cg; w < (g + 1) * cg; w += 64) u += chan[w];
-          const float v = u / count;
-          chan[g * cg] = second ? 1.0f / sqrtf(v + eps) : v;
+          const double v = u / count;
+          chan[g * cg] = second ? 1.0 / sqrt(v + deps) : v;
         }
         __syncthreads();
       }
     } else {
       for (int c = tid; c < Cl; c += nt) {
-        float t = 0.f;
+        double t = 0.0;
         for (int y = 0; y < slots; ++y) t += part[y * Cl + c];
         chan[c] = t;
       }
       __syncthreads();
       for (int g = tid; g < Cl / cg; g += nt) {
-        float t = 0.f;
+        double t = 0.0;
         for (int c = g * cg; c < (g + 1) * cg; ++c) t += chan[c];
-        const float v = t / count;  // correctly rounded: an exact mean stays exact
-        chan[g * cg] = second ? 1.0f / sqrtf(v + eps) : v;  // the group's first channel
+        const double v = t / count;  // correctly rounded: an exact mean stays exact
+        chan[g * cg] = second ? 1.0 / sqrt(v + deps) : v;  // the group's first channel
       }
       __syncthreads();
     }
@@ -171,10 +180,10 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
   };
 
   i32x4 keep[kResident];
-  float acc[N];
+  double acc[N];
   // ---- pass 1: sums ------------------------------------------------------------
 #pragma unroll
-  for (int e = 0; e < N; ++e) acc[e] = 0.f;
+  for (int e = 0; e < N; ++e) acc[e] = 0.0;
   if (resident) {
 #pragma unroll
     for (int k = 0; k < kResident; ++k) {
@@ -186,24 +195,24 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
       float f[N];
       NV::widen(keep[k], f);  // zeros past the rows add nothing
 #pragma unroll
-      for (int e = 0; e < N; ++e) acc[e] += f[e];
+      for (int e = 0; e < N; ++e) acc[e] += (double)f[e];
     }
   } else {
     for (int r = ty; r < rows; r += TY) {
       float f[N];
       NV::widen(S[(lo + r) * vpr + tx], f);
 #pragma unroll
-      for (int e = 0; e < N; ++e) acc[e] += f[e];
+      for (int e = 0; e < N; ++e) acc[e] += (double)f[e];
     }
   }
   reduce(acc, false);
-  float mu[N];
+  double mu[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) mu[e] = stat[threadIdx.x * N + e];
 
   // ---- pass 2: squared deviations from the group mean --------------------------
 #pragma unroll
-  for (int e = 0; e < N; ++e) acc[e] = 0.f;
+  for (int e = 0; e < N; ++e) acc[e] = 0.0;
   if (resident) {
 #pragma unroll
     for (int k = 0; k < kResident; ++k) {
@@ -212,7 +221,7 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
         NV::widen(keep[k], f);
 #pragma unroll
         for (int e = 0; e < N; ++e) {
-          const float d = f[e] - mu[e];
+          const double d = (double)f[e] - mu[e];
           acc[e] += d * d;
         }
       }
@@ -223,13 +232,13 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
       NV::widen(S[(lo + r) * vpr + tx], f);
 #pragma unroll
       for (int e = 0; e < N; ++e) {
-        const float d = f[e] - mu[e];
+        const double d = (double)f[e] - mu[e];
         acc[e] += d * d;
       }
     }
   }
   reduce(acc, true);
-  float rs[N];
+  double rs[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) rs[e] = stat[threadIdx.x * N + e];
 
@@ -238,7 +247,7 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
     float f[N];
     NV::widen(v, f);
 #pragma unroll
-    for (int e = 0; e < N; ++e) f[e] = (f[e] - mu[e]) * rs[e];
+    for (int e = 0; e < N; ++e) f[e] = (float)(((double)f[e] - mu[e]) * rs[e]);
     __builtin_nontemporal_store(NV::narrow(f), out + (lo + r) * vpr + tx);
   };
   if (resident) {
@@ -270,7 +279,8 @@ size_t group_norm_lds_bytes(int32_t C, int is_bf16, int split) {
   const int tx = C * (is_bf16 ? 2 : 4) / 16 / split;
   const int ty = kNormThreads / tx;
   const int cl = C / split;
-  return (size_t)(ty + 2) * (size_t)cl * sizeof(float);  // covers both reduction layouts
+  // partials (at most ty slots in either layout; stat reuses them) + chan
+  return (size_t)(ty + 1) * (size_t)cl * sizeof(double);
 }
 
 hipError_t launch_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
@@ -280,7 +290,7 @@ hipError_t launch_group_norm(const void* S, const int32_t* row_ptr, int64_t n_ro
   const int split = group_norm_split(B, C, G, is_bf16, num_cus);
   const dim3 block(vpr / split, kNormThreads / (vpr / split));
   const size_t lds = group_norm_lds_bytes(C, is_bf16, split);
-  // up to 64 KB of dynamic LDS (C = 4096 bf16): allow it once per instantiation
+  // up to 96 KB of dynamic LDS (C = 4096 bf16): allow it once per instantiation
   static std::once_flag once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(once, [&] {

@@ -386,7 +386,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(
       const double fik = F[i <= k ? pair_index(i, k, K) : pair_index(k, i, K)];
       const double fii = F[pair_index(i, i, K)];
       const double den = sqrt(fii * fkk);
-      const double sk = den > 0.0 ? fik / den : 0.0;
+      const double sk = den > 0.0 ? fik / den : 1.0;
       if (sim != nullptr) sim[(int64_t)i * K + k] = sk;
       if (i != k) acc += 1.0 - sk;
     }

@@ -13,7 +13,7 @@ from oracle import shc_oracle as O
 from paper_2608_09388_amd import binding as shc
 from paper_2608_09388_amd import synth
 from tests.gpu_util import (TORCH, Compaction, assert_gn_close, assert_normwise_close,
-                            assert_scaled_close, down, require_gpu, up)
+                            assert_scaled_close, down, gn_floor, require_gpu, up)
 
 pytestmark = pytest.mark.gpu
 
@@ -268,7 +268,7 @@ def test_sparse_linear(dev, dtype, Cin, Cout):
         got = down(out)
         ref = O.linear_at(S, W, rows, b, act == shc.SHC_ACT_RELU)
         scale = O.linear_at(S, W, rows, b, scale=True)
-        assert_scaled_close(got[:n], ref, scale, dtype, f"linear {Cin}->{Cout}")
+        assert_scaled_close(got[:n], ref, scale, dtype, f"linear {Cin}->{Cout}", n_terms=Cin)
         assert np.all(np.isnan(got[n:]))
 
 
@@ -304,7 +304,8 @@ def test_gather_sparse_linear(dev, dtype, Cin, Cout):
     S_ref = O.gather(x, ref_c, V)
     ref = O.linear_at(S_ref, W, np.arange(n), bias, act=True)
     scale = O.linear_at(S_ref, W, np.arange(n), bias, scale=True)
-    assert_scaled_close(got[:n], ref, scale, dtype, f"gather+linear {Cin}->{Cout}")
+    assert_scaled_close(got[:n], ref, scale, dtype, f"gather+linear {Cin}->{Cout}",
+                        n_terms=Cin)
 
 
 def test_gather_sparse_linear_bad_coords_read_zeros(dev):
@@ -556,6 +557,24 @@ def test_mask_scores_special_cases(dev):
     top1 = torch.empty(1, dtype=torch.int32, device=dev)
     shc.mask_scores(up(X, "bf16").reshape(1, N, C), up(np.array([3.5])), a1, 1, top1)
     assert float(a1[0]) == 3.5 and int(top1[0]) == 0
+    # an all-zero output: similarity 1 with every mask, score unchanged,
+    # nothing added to the others, ranked last
+    Z = np.stack([Y[0], np.zeros_like(Y[0]), Y[2], Y[0] + Y[1]])
+    Z = synth.as_dtype(Z.astype(np.float32), "bf16")[1]
+    az = torch.empty(4, dtype=torch.float64, device=dev)
+    simz = torch.empty(16, dtype=torch.float64, device=dev)
+    topz = torch.empty(4, dtype=torch.int32, device=dev)
+    alpha0 = np.full(4, 0.5)
+    shc.mask_scores(up(Z.reshape(-1, C), "bf16").reshape(4, N, C), up(alpha0), az, 4, topz,
+                    simz)
+    sz = down(simz).reshape(4, 4)
+    ref = O.mask_similarity(Z)
+    assert np.all(sz[1] == 1.0) and np.all(sz[:, 1] == 1.0)
+    live = np.ix_([0, 2, 3], [0, 2, 3])
+    assert np.all(np.abs(sz - ref)[live] <= similarity_bound(Z[[0, 2, 3]], ref[live], N))
+    assert float(az[1]) == 0.5
+    assert np.allclose(down(az), O.alpha_update(alpha0, Z), atol=1e-6)
+    assert int(down(topz)[-1]) == 1
 
 
 # ----------------------------------------------------------------------------
@@ -587,7 +606,7 @@ def test_group_norm_oracle(dev, dtype, C, G, B, V, p):
     got = down(out)
     assert np.all(np.isnan(got[n:]))
     ref = O.group_norm(S.astype(np.float64), rp, G)
-    assert_gn_close(got[:n], ref, dtype, f"group norm C={C} G={G} {dtype}")
+    assert_gn_close(got[:n], ref, dtype, gn_floor(S, rp, G), f"group norm C={C} G={G} {dtype}")
 
 
 def test_group_norm_deterministic_and_edge_cases(dev):
@@ -681,7 +700,8 @@ def test_sparse_conv_full_oracle(dev, dtype, B, V, K, Cin, Cout, p, path):
         assert n2 == n
         ref = O.sparse_conv(S, coords, B, V, nbr, W, b, act == shc.SHC_ACT_RELU)
         scale = O.sparse_conv_scale(S, coords, B, V, nbr, W, b)
-        assert_scaled_close(got, ref, scale, dtype, f"conv K={K} {Cin}->{Cout} p={p}")
+        assert_scaled_close(got, ref, scale, dtype, f"conv K={K} {Cin}->{Cout} p={p}",
+                            n_terms=K * Cin)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -704,14 +724,14 @@ def test_max_channels(dev, dtype, kind, K, Cin, Cout):
         torch.cuda.synchronize()
         ref = O.relu(np.asarray(S, np.float64) @ W[0] + bias)
         scale = np.abs(np.asarray(S, np.float64)) @ np.abs(W[0]) + np.abs(bias)
-        assert_scaled_close(down(out), ref, scale, dtype, f"linear {Cin}->{Cout}")
+        assert_scaled_close(down(out), ref, scale, dtype, f"linear {Cin}->{Cout}", n_terms=Cin)
     else:
         nbr = rand_nbr(V, K, rng)
         got, n2 = run_conv(dev, m, nbr, S, W, bias, dtype, shc.SHC_ACT_RELU, "table")
         assert n2 == n
         ref = O.sparse_conv(S, coords, B, V, nbr, W, bias, True)
         scale = O.sparse_conv_scale(S, coords, B, V, nbr, W, bias)
-        assert_scaled_close(got, ref, scale, dtype, f"conv K={K} {Cin}->{Cout}")
+        assert_scaled_close(got, ref, scale, dtype, f"conv K={K} {Cin}->{Cout}", n_terms=K * Cin)
 
 
 @pytest.mark.parametrize("path", ["direct", "table"])
@@ -819,7 +839,8 @@ def test_c2_full_stack_bf16(dev):
     S0 = O.gather(w.x, ref["coords"], w.V)
     scale = O.sparse_conv_scale(S0, ref["coords"], w.B, w.V, w.nbr, w.layers[0].W)
     ref0 = O.sparse_conv(S0, ref["coords"], w.B, w.V, w.nbr, w.layers[0].W, None, True)
-    assert_scaled_close(res["outs"][0], ref0, scale, "bf16", "C2 layer 0")
+    assert_scaled_close(res["outs"][0], ref0, scale, "bf16", "C2 layer 0",
+                        n_terms=w.K * w.layers[0].W.shape[1])
     for l in range(len(w.layers)):
         assert_normwise_close(res["outs"][l], ref["outs"][l], "bf16", f"C2 layer {l}")
     assert_normwise_close(res["pool"], ref["pool"], "bf16", "C2 pool")
@@ -838,14 +859,16 @@ def sampled_layer_check(res_rows_in, got, w, layer, coords, rows, dtype, what):
                         layer.relu)
         sc = O.conv_at(res_rows_in, coords, w.B, w.V, w.nbr, layer.W, rows, layer.bias,
                        scale=True)
+        n_terms = layer.W.shape[0] * layer.W.shape[1]
     else:
         ref = O.linear_at(res_rows_in, layer.W, rows, layer.bias, layer.relu)
         sc = O.linear_at(res_rows_in, layer.W, rows, layer.bias, scale=True)
-    assert_scaled_close(got[rows], ref, sc, dtype, what)
+        n_terms = layer.W.shape[0]
+    assert_scaled_close(got[rows], ref, sc, dtype, what, n_terms=n_terms)
 
 
 @pytest.mark.parametrize("name", ["c3_f32", "c3_bf16", "c3_5pct_bf16", "c4_0.01", "c4_0.05",
-                                  "c4_0.2", "c4_1.0"])
+                                  "c4_0.2", "c4_0.5", "c4_1.0"])
 def test_full_size_workloads_sampled(dev, name):
     from paper_2608_09388_amd.pipeline import SparseStack
     if name.startswith("c3"):
@@ -1146,4 +1169,5 @@ def test_conv_cin128_table_parity(dev, B, V, K, Cout, p):
                                      rng.choice(n, size=min(n, 600), replace=False)]))
     ref = O.conv_at(S, coords, B, V, nbr, W, rows, bias, act=True)
     scale = O.conv_at(S, coords, B, V, nbr, W, rows, bias, scale=True)
-    assert_scaled_close(g_tab[rows], ref, scale, "bf16", f"conv K={K} 128->{Cout} p={p}")
+    assert_scaled_close(g_tab[rows], ref, scale, "bf16", f"conv K={K} 128->{Cout} p={p}",
+                        n_terms=K * 128)

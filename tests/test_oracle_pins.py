@@ -465,6 +465,34 @@ def test_mask_scores_orthogonal_identical_and_invariances():
     assert np.all(base <= 1 + 1e-12) and np.all(base >= 0)   # Cauchy-Schwarz
 
 
+def test_mask_scores_zero_output_earns_no_credit():
+    """Eq. 3 divides by the Frobenius norms of the two Gram matrices, which
+    vanish for an all-zero output.  Reading: such a pair counts as similar
+    (sim = 1), so the zero mask's score is unchanged, it adds nothing to the
+    others' scores, and it ranks after every mask whose score grew."""
+    rng = np.random.default_rng(34)
+    N, C = 30, 4
+    Y = rng.standard_normal((4, N, C))
+    Y[1] = 0.0
+    sim = O.mask_similarity(Y)
+    assert np.all(np.isfinite(sim))
+    np.testing.assert_array_equal(sim[1], np.ones(4))
+    np.testing.assert_array_equal(sim[:, 1], np.ones(4))
+    live = [0, 2, 3]
+    np.testing.assert_allclose(sim[np.ix_(live, live)], O.mask_similarity(Y[live]),
+                               rtol=1e-14)
+    a0 = np.array([0.25, 0.25, 0.25, 0.25])
+    a1 = O.alpha_update(a0, Y)
+    assert a1[1] == a0[1]
+    # the live masks' increments are those of the three-mask problem scaled by
+    # (3 - 1) / (4 - 1): the zero mask contributes 1 - 1 = 0 to each sum
+    inc3 = O.alpha_update(np.zeros(3), Y[live])
+    np.testing.assert_allclose(a1[live] - 0.25, inc3 * 2.0 / 3.0, rtol=1e-13)
+    assert O.top_kappa(a1, 4)[-1] == 1
+    # every output zero: all pairs similar, nothing changes
+    np.testing.assert_array_equal(O.alpha_update(a0, np.zeros((4, N, C))), a0)
+
+
 def test_gram_frobenius_brute_force_and_top_kappa():
     rng = np.random.default_rng(33)
     K, N, C = 3, 4, 2
@@ -640,6 +668,34 @@ def test_conv_backward_special_cases_and_rows_at():
     c1 = O.compact(m1)[0]
     d1 = O.sparse_conv_backward(S[:1], c1, 1, V, nbr, W, dY[:1])
     np.testing.assert_allclose(d1[0], dY[:1] @ W[0].T, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("seed,p", [(48, 0.5), (49, 0.15), (50, 1.0)])
+def test_conv_backward_weight_bias_matches_full_backward(seed, p):
+    """The slot-by-slot weight and bias gradient from dZ equals the full
+    backward's dW and db (no activation, so dZ = dY), and its scale form
+    equals the full backward of the absolute values."""
+    rng = np.random.default_rng(seed)
+    m, coords, n, S, nbr, W, bias = bwd_case(rng, B=3, V=23, K=5, Ci=4, Co=6, p=p)
+    B, V = m.shape
+    dZ = rng.standard_normal((n, W.shape[2]))
+    _, dW, db = O.sparse_conv_backward(S, coords, B, V, nbr, W, dZ)
+    gW, gb = O.conv_backward_weight_bias(S, coords, B, V, nbr, dZ, W.shape[0])
+    np.testing.assert_allclose(gW, dW, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(gb, db, rtol=1e-12, atol=1e-12)
+    _, aW, ab = O.sparse_conv_backward(np.abs(S), coords, B, V, nbr, np.abs(W), np.abs(dZ))
+    sW, sb = O.conv_backward_weight_bias(S, coords, B, V, nbr, dZ, W.shape[0], scale=True)
+    np.testing.assert_allclose(sW, aW, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(sb, ab, rtol=1e-12, atol=1e-12)
+    # brute force of one slot's gradient: rows whose slot-j neighbour is active
+    row = {(int(b), int(v)): i for i, (b, v) in enumerate(coords)}
+    j = 2
+    e = np.zeros((S.shape[1], dZ.shape[1]))
+    for i, (b, v) in enumerate(coords.tolist()):
+        u = int(nbr[v, j])
+        if u >= 0 and (b, u) in row:
+            e += np.outer(S[row[(b, u)]], dZ[i])
+    np.testing.assert_allclose(gW[j], e, rtol=1e-12, atol=1e-12)
 
 
 # ----------------------------------------------------------------------------
@@ -831,6 +887,86 @@ def test_stack_matches_chained_brute_force_bf16():
         seg = h2[rp[b]:rp[b + 1]]
         ref = seg.max(0) if len(seg) else np.zeros(2)
         np.testing.assert_array_equal(res["pool"][b], ref)
+
+
+def f32_exact_rne(x: float) -> float:
+    """Nearest binary32 value (24 significant bits, exponents from -126,
+    largest finite (2 - 2^-23) 2^127), ties to even, by exact rational
+    comparison of the two bracketing values."""
+    if x == 0 or not np.isfinite(x):
+        return x
+    fx = abs(Fraction(x))
+    e = 0
+    ax = fx
+    while ax >= 2:
+        ax /= 2
+        e += 1
+    while ax < 1:
+        ax *= 2
+        e -= 1
+    spacing = Fraction(2) ** (max(e, -126) - 23)
+    lo = (fx // spacing) * spacing
+    hi = lo + spacing
+    if fx - lo < hi - fx:
+        r = lo
+    elif hi - fx < fx - lo:
+        r = hi
+    else:
+        r = lo if (lo / spacing) % 2 == 0 else hi
+    if r > (2 - Fraction(1, 2 ** 23)) * Fraction(2) ** 127:
+        return float(np.copysign(np.inf, x))
+    return float(r) if x > 0 else -float(r)
+
+
+def test_round_f32_exact_rational_and_store():
+    vals = list(RNG.standard_normal(3000) * 10.0 ** RNG.integers(-45, 38, 3000))
+    for k in range(200):
+        t = float(np.float32(RNG.standard_normal() * 10.0 ** RNG.integers(-30, 30)))
+        spacing = 2.0 ** (max(np.frexp(abs(t))[1] - 1, -126) - 23)
+        tie = t + spacing / 2
+        vals += [tie, np.nextafter(tie, np.inf), np.nextafter(tie, -np.inf)]
+    vals += [3.4028235677973366e38, 3.4028235e38 * 1.0000001, 2.0 ** -149, 2.0 ** -150,
+             1.5 * 2.0 ** -149, -0.0]
+    got = O.round_f32(np.array(vals))
+    ref = np.array([f32_exact_rne(v) for v in vals])
+    assert np.array_equal(got, ref)
+    np.testing.assert_array_equal(O.store(np.array(vals), "f32"), ref)
+    np.testing.assert_array_equal(O.store(np.array(vals[:50]), "bf16"),
+                                  [bf16_exact_rne(v) for v in vals[:50]])
+    with pytest.raises(ValueError):
+        O.store(np.zeros(2), "f16")
+
+
+def test_stack_matches_chained_brute_force_f32():
+    """An fp32 stack: every layer's output is rounded to binary32 (torch's
+    conversion here) before it feeds the next layer."""
+    B, V, K = 2, 16, 5
+    rng = np.random.default_rng(78)
+    m = (rng.random((B, V)) < 0.55).astype(np.uint8)
+    nbr = rand_nbr(V, K, rng)
+    x = rng.standard_normal((B * V, 3)).astype(np.float32).astype(np.float64)
+    W1 = rng.standard_normal((K, 3, 4))
+    b1 = rng.standard_normal(4)
+    W2 = rng.standard_normal((K, 4, 4))
+    W3 = rng.standard_normal((4, 2))
+    layers = [("conv", W1, b1, True), ("conv", W2, None, False), ("linear", W3, None, True)]
+    res = O.run_stack(x, m, nbr, layers, "f32", pool=True)
+    to32 = lambda a: torch.from_numpy(a).to(torch.float32).double().numpy()   # noqa: E731
+    h1 = to32(brute_conv(x, m, nbr, W1, b1, B, V, True))
+    # the second conv reads the first layer's rows scattered back (x (.) m)
+    coords = res["coords"]
+    d1 = np.zeros((B * V, 4))
+    d1[coords[:, 0] * V + coords[:, 1]] = h1
+    h2 = to32(brute_conv(d1, m, nbr, W2, None, B, V, False))
+    h3 = to32(np.maximum(h2 @ W3, 0))
+    for got, want in zip(res["outs"], (h1, h2, h3)):
+        np.testing.assert_array_equal(got, want)
+    rp = res["row_ptr"]
+    for b in range(B):
+        seg = h3[rp[b]:rp[b + 1]]
+        np.testing.assert_array_equal(res["pool"][b], seg.max(0) if len(seg) else np.zeros(2))
+    # the rounding matters: the same stack in fp64 storage differs somewhere
+    assert not np.array_equal(to32(h2), brute_conv(d1, m, nbr, W2, None, B, V, False))
 
 
 def test_density_reading_matches_table4(request):
