@@ -109,6 +109,26 @@ int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
                      void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
+ * shc_compact_mask without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The compaction's per-span counts go to a
+ * scratch array of 64 KB that the library holds in device memory, one copy
+ * per GPU, kept until the process ends; a B x V mask needs
+ * shc_compact_mask_workspace(B, V) bytes of it (at most 4 KB for any mask the
+ * library takes), and a mask that needed more would get SHC_ERR_CAPACITY.
+ * The call makes no allocation of its own (no hipMalloc, hipFree or
+ * allocating library routine); for none at all, pass n_active_host as NULL
+ * or in page-locked memory (pageable memory goes through a HIP copy).
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (concurrent streams, or host threads) race and must be ordered by the
+ * caller.  Nothing in the array needs to start at any value.  Arguments,
+ * outputs, waiting and errors otherwise as for shc_compact_mask.
+ */
+int shc_compact_mask_noalloc(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
+                             int32_t* inv, int32_t* row_ptr, int32_t* n_active_dev,
+                             int64_t* n_active_host, int64_t cap, hipStream_t stream);
+
+/*
  * shc_compact_mask in two halves, for a caller with work to enqueue before it
  * needs N' (work that reads only inv, such as shc_clear_inactive_rows):
  *

@@ -46,6 +46,8 @@ _SIGS = {
     "shc_compact_mask_workspace": (_c_sz, [_c_i32, _c_i32]),
     "shc_compact_mask": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr, _c_ptr,
                                         _c_ptr, _c_i64, _c_ptr, _c_sz, _c_ptr]),
+    "shc_compact_mask_noalloc": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr,
+                                                _c_ptr, _c_ptr, _c_i64, _c_ptr]),
     "shc_compact_mask_start": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr, _c_ptr,
                                               _c_ptr, _c_ptr, _c_i64, _c_ptr, _c_sz, _c_ptr]),
     "shc_compact_mask_wait": (ctypes.c_int, [_c_ptr, _c_i64, _c_ptr]),
@@ -215,6 +217,30 @@ def compact_mask(mask: torch.Tensor, B: int, V: int, coords: torch.Tensor, inv: 
         hp = ctypes.addressof(host) if want_host_count else None
     args += [hp, cap, _dev(ws, "ws"), ws.numel() * ws.element_size(), _stream(stream)]
     _check(lib.shc_compact_mask(*args), "shc_compact_mask")
+    if host_count is not None:
+        return int(host_count[0])
+    return int(host.value) if want_host_count else None
+
+
+def compact_mask_noalloc(mask: torch.Tensor, B: int, V: int, coords: torch.Tensor,
+                         inv: torch.Tensor, row_ptr: torch.Tensor, n_active: torch.Tensor,
+                         want_host_count: bool = True, stream=None,
+                         host_count: Optional[torch.Tensor] = None) -> Optional[int]:
+    """shc_compact_mask_noalloc: shc_compact_mask with the library's own scratch
+    instead of a workspace.  Arguments and result as for compact_mask."""
+    lib = load()
+    cap = coords.numel() // 2
+    args = [_dev(mask, "mask", torch.uint8, B * V), B, V,
+            _dev(coords, "coords", torch.int32) if cap > 0 else None,
+            _dev(inv, "inv", torch.int32, B * V), _dev(row_ptr, "row_ptr", torch.int32, B + 1),
+            _dev(n_active, "n_active", torch.int32, 1)]
+    host = ctypes.c_int64(-1)
+    if host_count is not None:
+        hp = _host_count_ptr(host_count)
+    else:
+        hp = ctypes.addressof(host) if want_host_count else None
+    args += [hp, cap, _stream(stream)]
+    _check(lib.shc_compact_mask_noalloc(*args), "shc_compact_mask_noalloc")
     if host_count is not None:
         return int(host_count[0])
     return int(host.value) if want_host_count else None

@@ -7,6 +7,7 @@
 
 #include "../../include/shc.h"
 #include <cmath>
+#include <mutex>
 
 #include "shc_internal.h"
 
@@ -233,6 +234,71 @@ int shc_compact_mask(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
     return fail(SHC_ERR_CAPACITY, "N' = %lld active rows exceed cap = %lld", (long long)n32,
                 (long long)cap);
   return SHC_OK;
+}
+
+}  // extern "C"
+
+// Scratch of shc_compact_mask_noalloc: the compaction's per-span counts, in
+// device memory the library owns instead of a caller's workspace.  Every GPU
+// the library runs on holds its own copy of the array until the process
+// ends.  Host code never passes the array's name to a kernel (on the host it
+// names a stand-in, not the device copy): scratch_address() resolves the
+// current device's copy once and every use goes through that pointer.
+static constexpr size_t kNoAllocScratchBytes = 64 * 1024;
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices];  // device copy of `scratch`, per device
+
+// Device address of the current device's `scratch`, resolved on the first
+// call on that device (with the device current) and kept.
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, "compact_mask_noalloc device query");
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(SHC_ERR_UNSUPPORTED, "device %d is beyond the %d this library serves", dev,
+                kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "compact_mask_noalloc scratch address");
+    if (p == nullptr) return fail(SHC_ERR_HIP, "compact_mask_noalloc: scratch address is NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SHC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int shc_compact_mask_noalloc(const uint8_t* mask, int32_t B, int32_t V, int32_t* coords,
+                             int32_t* inv, int32_t* row_ptr, int32_t* n_active_dev,
+                             int64_t* n_active_host, int64_t cap, hipStream_t stream) {
+  g_last_error[0] = 0;
+  // the arguments are checked before the scratch address is looked up, so
+  // a bad call touches no device
+  SHC_TRY(check_bv(B, V));
+  SHC_PTR(mask, "mask");
+  SHC_PTR(inv, "inv");
+  SHC_PTR(row_ptr, "row_ptr");
+  SHC_PTR(n_active_dev, "n_active_dev");
+  if (cap < 0) return fail(SHC_ERR_INVALID_ARG, "cap = %lld is negative", (long long)cap);
+  if (cap > 0) SHC_PTR(coords, "coords");
+  const size_t need = shc_compact_mask_workspace(B, V);
+  if (need > kNoAllocScratchBytes)
+    return fail(SHC_ERR_CAPACITY, "a %d x %d mask needs %zu bytes of scratch, above the %zu "
+                "this call holds", B, V, need, kNoAllocScratchBytes);
+  void* ws = nullptr;
+  SHC_TRY(scratch_address(&ws));
+  return shc_compact_mask(mask, B, V, coords, inv, row_ptr, n_active_dev, n_active_host, cap, ws,
+                          kNoAllocScratchBytes, stream);
 }
 
 int shc_gather_rows(const void* x, const int32_t* coords, int64_t n_rows, int32_t B, int32_t V,

@@ -72,6 +72,28 @@ def test_compact_mask_validation(lib):
     assert call(ws_bytes=ws - 1) == -2 and "workspace" in err(lib)
 
 
+def test_compact_mask_noalloc_validation(lib):
+    """The allocation-free compaction checks its arguments before it looks up
+    its scratch array, so none of these touches a device."""
+    ok = dict(mask=A, B=4, V=655, coords=A, inv=A, row_ptr=A, n_dev=A, n_host=None, cap=2620)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return lib.shc_compact_mask_noalloc(a["mask"], a["B"], a["V"], a["coords"], a["inv"],
+                                            a["row_ptr"], a["n_dev"], a["n_host"], a["cap"], None)
+
+    assert call(B=0) == -1 and "B = 0" in err(lib)
+    assert call(B=1 << 16, V=1 << 16) == -4
+    assert call(mask=None) == -1 and "mask" in err(lib)
+    assert call(inv=MIS) == -3 and "inv" in err(lib)
+    assert call(row_ptr=None) == -1
+    assert call(n_dev=MIS) == -3
+    assert call(cap=-1) == -1
+    assert call(coords=None) == -1
+    # the largest mask the library takes needs 4 KB of the 64 KB scratch
+    assert lib.shc_compact_mask_workspace(1 << 15, (1 << 16) - 1) <= 4096
+
+
 def test_compact_mask_start_wait_validation(lib):
     ws = lib.shc_compact_mask_workspace(4, 655)
 
