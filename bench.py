@@ -131,8 +131,23 @@ def traffic_from_profile():
     return float(kv["hbm_bytes_per_launch"])
 
 
+def cpu_model():
+    """The host CPU's model name (first 'model name' line of /proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, layers_spec, budget_s):
-    """The oracle as it stands on a bounded sample of bodies of the same workload."""
+    """The oracle as it stands on a bounded sample of bodies of the same
+    workload: one warm-up run, then the median of three timed runs, once with
+    the BLAS pool on every core this process may use and once limited to one
+    thread (threadpoolctl), each on its own body sample sized for about
+    budget_s / 8 seconds per run."""
     import threadpoolctl
     from oracle import shc_oracle as O
 
@@ -142,14 +157,34 @@ def cpu_baseline(w, layers_spec, budget_s):
         O.scatter(r["outs"][-1], r["inv"], zero_fill=True)
         return time.perf_counter() - t, r["n"]
 
-    t1, _ = run(1)
-    nb = int(max(1, min(w.B, budget_s / max(t1, 1e-3))))
-    t, n = run(nb)
-    info = threadpoolctl.threadpool_info()
-    cores = max([i.get("num_threads", 1) for i in info] + [1])
-    return {"value": n * len(layers_spec) / t, "unit": "active-vertex rows/s per sparse layer",
-            "cores": cores, "kind": "oracle",
-            "sample": f"{nb} of {w.B} bodies ({n} active rows), full step, {t:.1f} s, fp64 numpy"}
+    def leg(threads):
+        with threadpoolctl.threadpool_limits(limits=threads):
+            t1, _ = run(1)                                  # sizing run
+            nb = int(max(1, min(w.B, budget_s / 8 / max(t1, 1e-3))))
+            run(nb)                                         # warm-up
+            times = []
+            for _ in range(3):
+                t, n = run(nb)
+                times.append(t)
+        t = float(np.median(times))
+        return nb, n, t, n * len(layers_spec) / t
+
+    affinity = len(os.sched_getaffinity(0))
+    nb, n, t, rate = leg(affinity)
+    nb1, n1, t1, rate1 = leg(1)
+    return {"value": rate, "unit": "active-vertex rows/s per sparse layer",
+            "cores": affinity, "kind": "oracle",
+            "sample": (f"{nb} of {w.B} bodies ({n} active rows), full step; median of 3 runs "
+                       f"after a warm-up, {t:.2f} s each; fp64 numpy"),
+            "value_1thread": rate1,
+            "sample_1thread": (f"{nb1} of {w.B} bodies ({n1} active rows), median of 3 after "
+                               f"a warm-up, {t1:.2f} s each"),
+            "nproc": os.cpu_count(), "cpu_model": cpu_model(),
+            "paper_context": ("the paper reports 0.009 s per sample for its whole network on one "
+                              "NVIDIA Tesla V100, 12 times faster than the next-best method, and "
+                              "0.28 s -> 0.009 s when one mask cuts the processed vertices from "
+                              "655 to 66 (Table 4); a whole-model latency on other hardware, not "
+                              "comparable with this per-layer throughput")}
 
 
 def kernel_times(st, shc, torch, reps):

@@ -353,9 +353,11 @@ int shc_clear_inactive_rows(const int32_t* inv, int32_t B, int32_t V, int32_t C,
  *   S [n_rows][C], row_ptr [B+1] (bounds clamped to [0, n_rows]), out
  *   [n_rows][C] of the same dtype, must not overlap S.  G must divide C; eps
  *   must be positive and finite (1e-5 is the usual value).
- * Statistics are accumulated in fp64 (two passes: the mean, then the squared
- * deviations from it); each output is evaluated in fp64 and rounded once to
- * fp32, then (bf16 outputs) to bf16, to nearest even.
+ * Two passes: the mean, accumulated in fp64, then the squared deviations
+ * from it, summed in fp32 over at most 16 rows per thread and in fp64 beyond.
+ * Each output is computed in fp32 from the mean as two fp32 terms (about
+ * 12 * 2^-24 relative error in all); bf16 outputs are then rounded to
+ * nearest even.
  */
 int shc_segment_group_norm(const void* S, const int32_t* row_ptr, int64_t n_rows, int32_t B,
                            int32_t C, int32_t G, float eps, int32_t dtype, void* out,

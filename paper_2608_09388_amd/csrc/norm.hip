@@ -15,11 +15,15 @@
 // channel (4 fp32 or 8 bf16 channels), summed over the rows a wavefront holds
 // with lane shuffles, then through LDS over the wavefronts, then over the
 // channels of each group.  The statistics are
-// two-pass (the mean first, then the squared deviations from it) and held in
-// fp64 from the first addition on, so their rounding error (about n * 2^-53
-// relative for n values) stays far below the output's own rounding; every
-// output is (value - mu) * rsqrt(var + eps) evaluated in fp64 and rounded once
-// to fp32 (then to bf16 for bf16 outputs).
+// two-pass: the mean, held in fp64 from the first addition on, then the
+// squared deviations from it, summed in fp32 over a thread's rows (at most 16
+// positive terms) and in fp64 from there; the variance errs by at most about
+// 16 * 2^-24 relative and the mean by n * 2^-53 of the values' magnitude.  Every
+// output is ((value - mu_hi) - mu_lo) * rs in fp32, with the fp64 mean split
+// into two fp32 terms and rs = 1/sqrt(var + eps) rounded to fp32: four
+// roundings of about 2^-24 of the output each (then bf16's for bf16 outputs).
+// The in-wavefront row sums use DPP rotations and the row/half swaps of
+// v_permlane16_swap / v_permlane32_swap (VALU, no LDS traffic).
 // A body of up to kResident vectors per thread stays in registers, so HBM
 // sees one read and one write of every value; a larger body is streamed
 // three times (sums, deviations, output), the later passes mostly from L2.
@@ -72,6 +76,43 @@ struct NormVec<true> {
   }
 };
 
+// Sum of v over the lanes of a wavefront that share lane % tx (tx a power of
+// two below 64): rotations within each 16-lane row (DPP), then the swaps of
+// rows 16 apart and halves 32 apart (v_permlane16_swap / v_permlane32_swap).
+// All VALU; every lane ends with its sum.
+__device__ __forceinline__ double rot_row(double v, int d) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  int lo = (int)(uint32_t)u, hi = (int)(uint32_t)(u >> 32);
+  switch (d) {
+    case 1: lo = __builtin_amdgcn_update_dpp(0, lo, 0x121, 0xF, 0xF, false);
+            hi = __builtin_amdgcn_update_dpp(0, hi, 0x121, 0xF, 0xF, false); break;
+    case 2: lo = __builtin_amdgcn_update_dpp(0, lo, 0x122, 0xF, 0xF, false);
+            hi = __builtin_amdgcn_update_dpp(0, hi, 0x122, 0xF, 0xF, false); break;
+    case 4: lo = __builtin_amdgcn_update_dpp(0, lo, 0x124, 0xF, 0xF, false);
+            hi = __builtin_amdgcn_update_dpp(0, hi, 0x124, 0xF, 0xF, false); break;
+    default: lo = __builtin_amdgcn_update_dpp(0, lo, 0x128, 0xF, 0xF, false);
+             hi = __builtin_amdgcn_update_dpp(0, hi, 0x128, 0xF, 0xF, false); break;
+  }
+  return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+__device__ __forceinline__ double lanes_sum(double v, int tx) {
+  for (int d = tx; d < 16; d <<= 1) v += rot_row(v, d);
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)u, hi = (uint32_t)(u >> 32);
+  if (tx <= 16) {
+    const auto a = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto b = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    v = __builtin_bit_cast(double, ((uint64_t)b[0] << 32) | a[0]) +
+        __builtin_bit_cast(double, ((uint64_t)b[1] << 32) | a[1]);
+  }
+  const uint64_t w = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo2 = (uint32_t)w, hi2 = (uint32_t)(w >> 32);
+  const auto c = __builtin_amdgcn_permlane32_swap(lo2, lo2, false, false);
+  const auto d2 = __builtin_amdgcn_permlane32_swap(hi2, hi2, false, false);
+  return __builtin_bit_cast(double, ((uint64_t)d2[0] << 32) | c[0]) +
+         __builtin_bit_cast(double, ((uint64_t)d2[1] << 32) | c[1]);
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
     const i32x4* __restrict__ S, const int32_t* __restrict__ row_ptr, int64_t n_rows, int C,
@@ -114,8 +155,7 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
     if (rw > 1) {
       const int lane = tid & 63;
 #pragma unroll
-      for (int e = 0; e < N; ++e)
-        for (int d = TX; d < 64; d <<= 1) acc[e] += __shfl_xor(acc[e], d, 64);
+      for (int e = 0; e < N; ++e) acc[e] = lanes_sum(acc[e], TX);
       if (lane < TX)
 #pragma unroll
         for (int e = 0; e < N; ++e) part[(tid >> 6) * Cl + threadIdx.x * N + e] = acc[e];
@@ -188,14 +228,17 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
 #pragma unroll
     for (int k = 0; k < kResident; ++k) {
       const int r = ty + k * TY;
-      keep[k] = r < rows ? S[(lo + r) * vpr + tx] : i32x4{0, 0, 0, 0};
+      keep[k] = i32x4{0, 0, 0, 0};
+      if (k * TY < rows && r < rows) keep[k] = S[(lo + r) * vpr + tx];
     }
 #pragma unroll
     for (int k = 0; k < kResident; ++k) {
-      float f[N];
-      NV::widen(keep[k], f);  // zeros past the rows add nothing
+      if (k * TY < rows) {  // uniform: register slots no thread of the body uses are skipped
+        float f[N];
+        NV::widen(keep[k], f);  // zeros past the rows add nothing
 #pragma unroll
-      for (int e = 0; e < N; ++e) acc[e] += (double)f[e];
+        for (int e = 0; e < N; ++e) acc[e] += (double)f[e];
+      }
     }
   } else {
     for (int r = ty; r < rows; r += TY) {
@@ -209,32 +252,56 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
   double mu[N];
 #pragma unroll
   for (int e = 0; e < N; ++e) mu[e] = stat[threadIdx.x * N + e];
+  // the mean as two fp32 terms (hi + lo): centred values (value - mu_hi) - mu_lo
+  // err by 2^-24 of themselves, not of the mean
+  float mu_hi[N], mu_lo[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    mu_hi[e] = (float)mu[e];
+    mu_lo[e] = (float)(mu[e] - (double)mu_hi[e]);
+  }
 
   // ---- pass 2: squared deviations from the group mean --------------------------
+  // A thread's squares (positive terms) are summed in fp32 over at most
+  // kResident rows at a time (relative error at most 15 * 2^-24), then the
+  // sums go on in fp64.
 #pragma unroll
   for (int e = 0; e < N; ++e) acc[e] = 0.0;
   if (resident) {
+    float sq[N];
+#pragma unroll
+    for (int e = 0; e < N; ++e) sq[e] = 0.f;
 #pragma unroll
     for (int k = 0; k < kResident; ++k) {
-      if (ty + k * TY < rows) {
+      if (k * TY < rows) {  // uniform skip, then the rows of this slot
+        const bool in = ty + k * TY < rows;
         float f[N];
         NV::widen(keep[k], f);
 #pragma unroll
         for (int e = 0; e < N; ++e) {
-          const double d = (double)f[e] - mu[e];
-          acc[e] += d * d;
+          const float d = in ? (f[e] - mu_hi[e]) - mu_lo[e] : 0.f;
+          sq[e] = __builtin_fmaf(d, d, sq[e]);
         }
       }
     }
-  } else {
-    for (int r = ty; r < rows; r += TY) {
-      float f[N];
-      NV::widen(S[(lo + r) * vpr + tx], f);
 #pragma unroll
-      for (int e = 0; e < N; ++e) {
-        const double d = (double)f[e] - mu[e];
-        acc[e] += d * d;
+    for (int e = 0; e < N; ++e) acc[e] = (double)sq[e];
+  } else {
+    for (int r0 = ty; r0 < rows; r0 += kResident * TY) {
+      float sq[N];
+#pragma unroll
+      for (int e = 0; e < N; ++e) sq[e] = 0.f;
+      for (int r = r0; r < rows && r < r0 + kResident * TY; r += TY) {
+        float f[N];
+        NV::widen(S[(lo + r) * vpr + tx], f);
+#pragma unroll
+        for (int e = 0; e < N; ++e) {
+          const float d = (f[e] - mu_hi[e]) - mu_lo[e];
+          sq[e] = __builtin_fmaf(d, d, sq[e]);
+        }
       }
+#pragma unroll
+      for (int e = 0; e < N; ++e) acc[e] += (double)sq[e];
     }
   }
   reduce(acc, true);
@@ -243,17 +310,20 @@ __global__ __launch_bounds__(kNormThreads) void group_norm_kernel(
   for (int e = 0; e < N; ++e) rs[e] = stat[threadIdx.x * N + e];
 
   // ---- pass 3: normalized values -----------------------------------------------
+  float rs_f[N];
+#pragma unroll
+  for (int e = 0; e < N; ++e) rs_f[e] = (float)rs[e];
   auto emit = [&](const i32x4& v, int r) {
     float f[N];
     NV::widen(v, f);
 #pragma unroll
-    for (int e = 0; e < N; ++e) f[e] = (float)(((double)f[e] - mu[e]) * rs[e]);
+    for (int e = 0; e < N; ++e) f[e] = ((f[e] - mu_hi[e]) - mu_lo[e]) * rs_f[e];
     __builtin_nontemporal_store(NV::narrow(f), out + (lo + r) * vpr + tx);
   };
   if (resident) {
 #pragma unroll
     for (int k = 0; k < kResident; ++k)
-      if (ty + k * TY < rows) emit(keep[k], ty + k * TY);
+      if (k * TY < rows && ty + k * TY < rows) emit(keep[k], ty + k * TY);
   } else {
     for (int r = ty; r < rows; r += TY) emit(S[(lo + r) * vpr + tx], r);
   }

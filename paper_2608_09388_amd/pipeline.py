@@ -127,6 +127,11 @@ class SparseStack:
                  side_stream: bool = False):
         self.w = w
         self.device = torch.device(device)
+        # every prepared call below launches on the stream current now; step()
+        # and run() order that stream after the caller's stream when they
+        # are called under another one (and the caller's stream after them)
+        self.main = torch.cuda.current_stream(self.device)
+        self._bracket = None
         # with side_stream, run() uses two more streams (default priority): the
         # side stream for the next batch's compaction and table, the tail stream
         # for each batch's scatter and pool; None: everything on the current one
@@ -236,12 +241,34 @@ class SparseStack:
             if around is not None and around[0] == l:
                 around[2].record()
 
+    def _enter(self):
+        """If the caller's current stream is not the stack's own, make the
+        stack's stream wait for the caller's work so far; returns the
+        caller's stream, or None when they are the same."""
+        cur = torch.cuda.current_stream(self.device)
+        if cur == self.main:
+            return None
+        if self._bracket is None:
+            with torch.cuda.device(self.device):
+                self._bracket = (shc.StreamEvent(), shc.StreamEvent())
+        self._bracket[0].record(cur)
+        self._bracket[0].wait(self.main)
+        return cur
+
+    def _leave(self, cur):
+        """The caller's stream waits for the stack's work (see _enter)."""
+        if cur is not None:
+            self._bracket[1].record(self.main)
+            self._bracket[1].wait(cur)
+
     def step(self) -> int:
         """One pass of the whole path over the workload's batch, on its own."""
+        cur = self._enter()
         s = self._set
         s.n = s.compact()
         self._front(s)
         self.finish()
+        self._leave(cur)
         return s.n
 
     def run(self, steps: int, around_layer: Optional[Tuple[int, Sequence]] = None,
@@ -260,8 +287,17 @@ class SparseStack:
         last batch's.  Returns its N'."""
         if steps <= 0:
             return self.n or 0
-        if self.side is not None and self.w.layers:
-            return self._run_pipelined(steps, around_layer, feed)
+        cur = self._enter()
+        try:
+            with torch.cuda.stream(self.main):
+                if self.side is not None and self.w.layers:
+                    return self._run_pipelined(steps, around_layer, feed)
+                return self._run_serial(steps, around_layer, feed)
+        finally:
+            self._leave(cur)
+
+    def _run_serial(self, steps: int, around_layer, feed) -> int:
+        """run() on the stack's own stream alone."""
         s = self._set
         if feed is not None:
             feed(0)
@@ -311,7 +347,7 @@ class SparseStack:
         system-scope fence (shc_event_create): a default event's cache
         write-back at every record costs the step microseconds.  Every batch
         runs the whole path."""
-        main = torch.cuda.current_stream(self.device)
+        main = self.main
         side, tail = self.side, self.tail
         ev = self._events
         ns = len(self._sets)

@@ -951,6 +951,49 @@ def test_overlapped_run_new_mask_per_batch(dev, steps, side):
     assert_normwise_close(got["pool"], ref["pool"], w.dtype, "pool")
 
 
+@pytest.mark.parametrize("side", [False, True])
+def test_run_under_another_stream(dev, side):
+    """A stack built on the default stream and run (and stepped) under
+    ``torch.cuda.stream(other)``: the inputs are written on the other stream
+    just before, the results read on it just after, and they must be bit for
+    bit those of the same run on the default stream."""
+    from paper_2608_09388_amd.pipeline import SparseStack, to_device
+    w = synth.workload_c4(0.05, B=6, V=655)
+    rng = np.random.default_rng(77)
+    masks = [(rng.random((w.B, w.V)) < p).astype(np.uint8) for p in (0.2, 0.4, 0.1)]
+    xs = [synth.as_dtype(rng.standard_normal(w.x.shape).astype(np.float32), w.dtype)[1]
+          for _ in range(3)]
+
+    def go(st, stream):
+        def feed(k):
+            st.mask.copy_(up(masks[k].reshape(-1)))
+            st.x.copy_(to_device(xs[k], w.dtype, st.device))
+        with torch.cuda.stream(stream):
+            n = st.run(3, feed=feed)
+            outs = [a.clone() for a in (st.acts[-1][:n], st.dense_out, st.pooled)]
+        torch.cuda.synchronize()
+        return [o.view(torch.int16).cpu().numpy() for o in outs]
+
+    ref_st = SparseStack(w, device=str(dev), side_stream=side)
+    ref = go(ref_st, torch.cuda.current_stream())
+    st = SparseStack(w, device=str(dev), side_stream=side)
+    other = torch.cuda.Stream(device=dev)
+    got = go(st, other)
+    for a, b in zip(got, ref):
+        assert np.array_equal(a, b)
+    # step() under the other stream, with its input written there just before
+    with torch.cuda.stream(other):
+        st.mask.copy_(up(masks[0].reshape(-1)))
+        st.x.copy_(to_device(xs[0], w.dtype, st.device))
+        n = st.step()
+        pooled = st.pooled.clone()
+    torch.cuda.synchronize()
+    spec = [(l.kind, l.W, l.bias, l.relu) for l in w.layers]
+    oref = O.run_stack(xs[0], masks[0], w.nbr, spec, w.dtype, pool=True)
+    assert n == oref["n"]
+    assert_normwise_close(pooled.float().cpu().numpy(), oref["pool"], w.dtype, "pool")
+
+
 def test_c5_sequences_stack(dev):
     """C5 shape (V=655, C=256 bf16, Markov masks, 3 convs + per-frame pool) on one of
     the 32 sequences end to end against the full oracle stack; all 32 sequences for
