@@ -54,6 +54,8 @@ def parse():
     p.add_argument("--density", type=float, default=0.05)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-dense", action="store_true", help="skip the dense-layer comparison")
+    p.add_argument("--no-sweep", action="store_true",
+                   help="skip the density sweep and the full-mesh layers")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--reps", type=int, default=50,
                    help="back-to-back launches per kernel for the per-kernel times")
@@ -62,9 +64,10 @@ def parse():
     return p.parse_args()
 
 
-def algorithmic_conv(w, coords, inv, n, e):
-    """Bytes and useful flops the conv must move/do for N' rows (per launch)."""
-    K, Cin, Cout = w.layers[1].W.shape
+def algorithmic_conv(w, coords, inv, n, e, layer=1):
+    """Bytes and useful flops the conv (layer `layer`) must move/do for N'
+    rows (per launch)."""
+    K, Cin, Cout = w.layers[layer].W.shape
     b = coords[:, 0].astype(np.int64)
     v = coords[:, 1].astype(np.int64)
     present = 0
@@ -346,6 +349,13 @@ def main():
 
     out["gather_scatter"] = gather_scatter_measure(shc, synth, torch, args.reps)
     log("gather and scatter measured")
+    out["cold_warm"] = cold_warm_measure(st, torch)
+    log("cold and warm launches measured")
+    if not args.no_sweep:
+        out["density_sweep"] = density_sweep(w, shc, synth, torch, args.reps)
+        log("density sweep measured")
+        out["c3_layers"] = c3_layers(shc, synth, torch, args.reps)
+        log("full-mesh layers measured")
     out["next_rows"] = {"group_norm": group_norm_measure(st, shc, torch, args.reps),
                         "multi_mask": multi_mask_measure(st, w, shc, synth, torch, args.reps),
                         "mask_scores": mask_scores_measure(w, shc, torch, args.reps),
@@ -581,6 +591,175 @@ def mask_scores_measure(w, shc, torch, reps, K=10, bodies=16):
             "launch_us": round(us, 2), "useful_flops": flops, "achieved": round(ach, 1),
             "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": round(ach / BF16_MFMA_PEAK_TFLOPS, 4), "bound": "mfma"}
+
+
+def _time_each(fn, torch, reps, flush=None):
+    """Durations (us) of `reps` launches of fn, each between its own pair of
+    HIP events on the current stream; with `flush`, it runs before each
+    launch (outside the events)."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    for a, b in evs:
+        if flush is not None:
+            flush()
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
+
+
+def _pct(t):
+    return {"p10": round(float(np.percentile(t, 10)), 2), "p50": round(float(np.median(t)), 2),
+            "p90": round(float(np.percentile(t, 90)), 2), "reps": int(len(t))}
+
+
+def cold_warm_measure(st, torch, reps=100):
+    """The gather + linear layer, the conv and the zero-fill scatter of the
+    step, each launched `reps` times on its own: warm (back to back, inputs
+    left in the caches by the launch before) and cold (a 512 MiB write between
+    launches evicts the 256 MiB Infinity Cache and the L2s), with p10 / p50 /
+    p90 of the per-launch event times.  The flush reads its 512 MiB (a sum),
+    so it leaves no dirty lines whose write-back would run during the next
+    launch.  A per-launch event pair adds a few us of its own to short
+    kernels, so the back-to-back averages of `per_kernel_us` stay the
+    reference figures."""
+    junk = torch.ones(512 * 1024 * 1024 // 4, dtype=torch.float32, device=st.device)
+    acc = torch.zeros((), dtype=torch.float32, device=st.device)
+
+    def flush():
+        torch.sum(junk, dim=(0,), out=acc)
+
+    lin = "gather+linear" if st.fused_gather else "linear"
+    calls = {lin: lambda: st.layer(0), "conv": lambda: st.layer(1), "scatter": st.scatter,
+             # reference: a plain write of the same dense output (PyTorch's fill)
+             "fill_dense_output": lambda: st.dense_out.zero_()}
+    out = {}
+    for name, fn in calls.items():
+        out[name] = {"warm": _pct(_time_each(fn, torch, reps)),
+                     "cold": _pct(_time_each(fn, torch, reps, flush))}
+    nb = st.dense_out.numel() * st.dense_out.element_size()
+    out["fill_dense_output"]["bytes"] = nb
+    out["fill_dense_output"]["cold_frac_hbm"] = round(
+        nb / (out["fill_dense_output"]["cold"]["p50"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+    n = st.n
+    sb = n * st.dense_out.shape[1] * st.dense_out.element_size() + st.B * st.V * (
+        4 + st.dense_out.shape[1] * st.dense_out.element_size())
+    out["scatter"]["cold_frac_hbm"] = round(sb / (out["scatter"]["cold"]["p50"] * 1e-6) / 1e9
+                                            / HBM_PEAK_GBS, 4)
+    del junk
+    return out
+
+
+def density_sweep(w0, shc, synth, torch, reps):
+    """The density-sweep workload at every density it names (B = 128,
+    V = 10475, K = 9, C = 128 bf16, i.i.d. Bernoulli(p)): the sparse linear
+    layer (with the gather fused in) and the sparse conv, back to back on one
+    stack per density, against the same layers at p = 1 (every vertex active:
+    this library's dense run) and against PyTorch's dense layers (hipBLASLt
+    matmul, an index_select per slot for the conv).  The crossover is the
+    density where a sparse layer's time reaches its dense time (linear
+    interpolation between sweep points)."""
+    import copy
+    from paper_2608_09388_amd.pipeline import SparseStack
+
+    dens = [0.01, 0.05, 0.20, 0.50, 1.00]
+    rows = []
+    for p in dens:
+        w = copy.copy(w0)
+        w.mask = synth.bernoulli_mask(w0.B, w0.V, p, synth._rng(4, 1))
+        st = SparseStack(w, device="cuda:0")
+        n = st.compact()
+        st.gather()
+        st.layer(0)
+        t_lin = _time_us(lambda: st.layer(0), torch, reps)
+        t_conv = _time_us(lambda: st.layer(1), torch, reps)
+        coords = st.coords[:n].cpu().numpy()
+        inv = st.inv.cpu().numpy()
+        cb, cf, a = algorithmic_conv(w, coords, inv, n, 2)
+        lb = n * (8 + 2 * 128 * 2) + 128 * 128 * 2
+        rows.append({"p": p, "n_active": n,
+                     "linear_us": round(t_lin, 2), "conv_us": round(t_conv, 2),
+                     "linear_rows_per_s": round(n / (t_lin * 1e-6), 1),
+                     "conv_rows_per_s": round(n / (t_conv * 1e-6), 1),
+                     "linear_frac_hbm": round(lb / (t_lin * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "conv_frac_hbm": round(cb / (t_conv * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                     "conv_useful_tflops": round(cf / (t_conv * 1e-6) / 1e12, 1),
+                     "present_slot_fraction": round(a, 4)})
+        if p == 1.0:
+            # PyTorch's dense layers on the same all-rows input
+            x = st.acts[1]
+            Wl = st.weights[0]
+            Wc = st.weights[1].reshape(-1, st.weights[1].shape[-1]).contiguous()
+            nbr_flat = st.nbr.long().view(-1)
+            BV = w.B * w.V
+            t_lt = _time_us(lambda: torch.relu(st.x @ Wl), torch, 5)
+            t_ct = _time_us(lambda: torch.relu(
+                x.view(w.B, w.V, -1)[:, nbr_flat].reshape(BV, -1) @ Wc), torch, 3)
+        del st
+        torch.cuda.empty_cache()
+    dense_lin, dense_conv = rows[-1]["linear_us"], rows[-1]["conv_us"]
+    for r in rows:
+        r["linear_speedup_vs_own_dense"] = round(dense_lin / r["linear_us"], 2)
+        r["conv_speedup_vs_own_dense"] = round(dense_conv / r["conv_us"], 2)
+        r["linear_speedup_vs_torch_dense"] = round(t_lt / r["linear_us"], 2)
+        r["conv_speedup_vs_torch_dense"] = round(t_ct / r["conv_us"], 2)
+
+    def crossover(key, dense):
+        """Lowest density where the sparse layer takes as long as the dense
+        one (interpolated), or None when it stays faster up to p < 1 (at
+        p = 1 the sparse path is the dense run itself)."""
+        prev = None
+        for r in rows:
+            if r["p"] < 1.0 and r[key] >= dense:
+                if prev is None:
+                    return r["p"]
+                f = (dense - prev[key]) / (r[key] - prev[key])
+                return round(prev["p"] + f * (r["p"] - prev["p"]), 3)
+            prev = r
+        return None
+
+    return {"workload": "B=128, V=10475 ellipsoid, K=9, C=128->128 bf16, Bernoulli(p)",
+            "points": rows, "dense_torch_linear_us": round(t_lt, 2),
+            "dense_torch_conv_us": round(t_ct, 2),
+            "crossover_vs_own_dense": {"linear": crossover("linear_us", dense_lin),
+                                       "conv": crossover("conv_us", dense_conv)},
+            "crossover_vs_torch_dense": {"linear": crossover("linear_us", t_lt),
+                                         "conv": crossover("conv_us", t_ct)}}
+
+
+def c3_layers(shc, synth, torch, reps):
+    """The full-mesh workload's conv layer (B = 256, V = 10475, K = 9,
+    C = 64 -> 64 + ReLU) in fp32 and bf16, with the cap mask as written and
+    its 5% variant: rows/s, HBM fraction of the algorithmic bytes, and the
+    useful MFMA rate against the dtype's peak (fp32 157.3, bf16 2500 TFLOP/s)."""
+    from paper_2608_09388_amd.pipeline import SparseStack
+
+    out = []
+    for dt, five in (("f32", False), ("bf16", False), ("f32", True), ("bf16", True)):
+        w = synth.workload_c3(dt, five_percent=five)
+        st = SparseStack(w, device="cuda:0")
+        n = st.compact()
+        st.gather()
+        t = _time_us(lambda: st.layer(0), torch, reps)
+        e = 4 if dt == "f32" else 2
+        coords = st.coords[:n].cpu().numpy()
+        inv = st.inv.cpu().numpy()
+        cb, cf, a = algorithmic_conv(w, coords, inv, n, e, layer=0)
+        peak = 157.3 if dt == "f32" else BF16_MFMA_PEAK_TFLOPS
+        out.append({"mask": "5% cap" if five else "cap y<-0.6", "dtype": dt, "n_active": n,
+                    "conv_us": round(t, 2), "rows_per_s": round(n / (t * 1e-6), 1),
+                    "algorithmic_bytes": int(cb),
+                    "frac_hbm": round(cb / (t * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                    "useful_tflops": round(cf / (t * 1e-6) / 1e12, 1),
+                    "useful_frac_mfma": round(cf / (t * 1e-6) / 1e12 / peak, 4),
+                    "present_slot_fraction": round(a, 4)})
+        del st
+        torch.cuda.empty_cache()
+    return out
 
 
 def dense_comparison(st, w, per_kernel_ms, torch, shc, synth):
