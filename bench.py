@@ -515,7 +515,9 @@ def gather_scatter_measure(shc, synth, torch, reps):
         s_us = _time_us(lambda: scatter(n), torch, reps)
         g_b = n * (8 + 2 * C * e)
         s_b = n * C * e + B * V * (4 + C * e)
-        out.append({"workload": name, "B": B, "V": V, "C": C, "dtype": dt, "n_active": n,
+        out.append({"workload": name, "timing": "warm: back to back, inputs and part of the "
+                                                 "output left in the caches by the launch before",
+                    "B": B, "V": V, "C": C, "dtype": dt, "n_active": n,
                     "gather_us": round(g_us, 2),
                     "gather_frac_hbm": round(g_b / (g_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
                     "scatter_us": round(s_us, 2),
