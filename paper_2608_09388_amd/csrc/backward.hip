@@ -584,19 +584,43 @@ __global__ __launch_bounds__(kThreads) void wgrad_tile_f32_kernel(
 }
 
 // dW[j][c][o]: sum of the partial tiles of slot j's chunks in fp64.
-// Workgroup (slot j and tile, 32 consecutive entries) of 8 chunk groups:
-// group y sums chunks y, y + 8, ... of the slot in order, then the 8 group
-// sums are added in order.  A slot without chunks gets 0.
-template <int T>
-__global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __restrict__ part,
-                                                                const int32_t* __restrict__ row_ptr,
-                                                                int32_t L, int32_t Cin,
-                                                                int32_t Cout, int single,
-                                                                int32_t n_chunks,
-                                                                float* __restrict__ dW) {
-  __shared__ double red[8][32];
+// Workgroup (slot j and tile, 32 consecutive entries) of G chunk groups:
+// group y sums chunks y, y + G, ... of the slot in order, then the G group
+// sums are added in order.  A slot without chunks gets 0.  G = 32 for the
+// linear layer (one slot with all the chunks), 8 for a conv (whose sparse
+// slots have few chunks each).  With colpart, the workgroups of one more x
+// index reduce the bias gradient in colsum_kernel's order (32 groups: group y
+// sums splits y, y + 32, ..., whatever G is).
+template <int T, int G>
+__global__ __launch_bounds__(32 * G) void wgrad_reduce_kernel(
+    const float* __restrict__ part, const int32_t* __restrict__ row_ptr, int32_t L, int32_t Cin,
+    int32_t Cout, int single, int32_t n_chunks, float* __restrict__ dW,
+    const float* __restrict__ colpart, int32_t splits, float* __restrict__ db) {
+  __shared__ double red[32][33];
+  static_assert(G == 8 || G == 32, "chunk groups");
   const int tA = (Cin + T - 1) / T, tB = (Cout + T - 1) / T;
   const int tiles = tA * tB;
+  const int ex = threadIdx.x & 31, y = threadIdx.x >> 5;
+  const int e = blockIdx.y * 32 + ex;
+  // the last x index is the bias gradient's when colpart is given
+  if (colpart != nullptr && (int)blockIdx.x == (int)gridDim.x - 1) {
+    // 32 split groups over the G * 32 threads (G = 8: four groups per thread)
+    for (int yg = y; yg < 32; yg += G) {
+      double t = 0.0;
+      if (e < Cout) {
+#pragma unroll 4
+        for (int q = yg; q < splits; q += 32) t += (double)colpart[(int64_t)q * Cout + e];
+      }
+      red[yg][ex] = t;
+    }
+    __syncthreads();
+    if (y == 0 && e < Cout) {
+      double u = 0.0;
+      for (int yy = 0; yy < 32; ++yy) u += red[yy][ex];
+      db[e] = (float)u;
+    }
+    return;
+  }
   const int j = blockIdx.x / tiles, t = blockIdx.x - j * tiles;
   const int ta = t / tB, tb = t - ta * tB;
   int c0 = 0, c1 = n_chunks;
@@ -605,16 +629,14 @@ __global__ __launch_bounds__(kThreads) void wgrad_reduce_kernel(const float* __r
     slot_chunks(row_ptr, j, L, &c0, &cnt);
     c1 = c0 + cnt;
   }
-  const int ex = threadIdx.x & 31, y = threadIdx.x >> 5;
-  const int e = blockIdx.y * 32 + ex;
   double s = 0.0;
 #pragma unroll 4
-  for (int q = c0 + y; q < c1; q += 8) s += (double)part[((int64_t)q * tiles + t) * T * T + e];
+  for (int q = c0 + y; q < c1; q += G) s += (double)part[((int64_t)q * tiles + t) * T * T + e];
   red[y][ex] = s;
   __syncthreads();
   if (y == 0) {
     double u = 0.0;
-    for (int yy = 0; yy < 8; ++yy) u += red[yy][ex];
+    for (int yy = 0; yy < G; ++yy) u += red[yy][ex];
     const int a = e / T, b = e - a * T;
     const int c = ta * T + a, o = tb * T + b;
     if (c < Cin && o < Cout) dW[((int64_t)j * Cin + c) * Cout + o] = (float)u;
@@ -1168,7 +1190,9 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
                          static_cast<const i32x4*>(dY), static_cast<const i32x4*>(Y), n, Cout,
                          act, pl.rps, static_cast<i32x4*>(dz_out), colpart);
     if (act) dZ = dz_out;
-    if (db != nullptr)
+    // the bias gradient's column sums: in the weight gradient's reduction
+    // launch when there is one, else on their own
+    if (db != nullptr && dW == nullptr)
       hipLaunchKernelGGL(colsum_kernel, dim3((Cout + 7) / 8), dim3(kThreads), 0, stream, colpart,
                          pl.splits, Cout, db);
   }
@@ -1207,13 +1231,19 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
                          rp, Kw, n, pl.L, Cin, Cout, part);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
-    const dim3 rg((unsigned)(Kw * pl.tiles), (unsigned)(pl.T * pl.T / 32));
-    if (pl.T == 128)
-      hipLaunchKernelGGL(wgrad_reduce_kernel<128>, rg, dim3(kThreads), 0, stream, part, rp, pl.L,
-                         Cin, Cout, conv ? 0 : 1, (int32_t)pl.max_chunks, dW);
-    else
-      hipLaunchKernelGGL(wgrad_reduce_kernel<64>, rg, dim3(kThreads), 0, stream, part, rp, pl.L,
-                         Cin, Cout, conv ? 0 : 1, (int32_t)pl.max_chunks, dW);
+    // one more column of workgroups reduces the bias gradient (T * T / 32 >= Cout / 32)
+    const float* cp = db != nullptr ? reinterpret_cast<const float*>(w + pl.off_colpart) : nullptr;
+    const dim3 rg((unsigned)(Kw * pl.tiles + (db != nullptr ? 1 : 0)),
+                  (unsigned)(pl.T * pl.T / 32));
+#define SHC_REDUCE(TT, GG)                                                                     \
+  hipLaunchKernelGGL((wgrad_reduce_kernel<TT, GG>), rg, dim3(32 * GG), 0, stream, part, rp, pl.L, \
+                     Cin, Cout, conv ? 0 : 1, (int32_t)pl.max_chunks, dW, cp, pl.splits, db)
+    if (pl.T == 128) {
+      if (conv) SHC_REDUCE(128, 8); else SHC_REDUCE(128, 32);
+    } else {
+      if (conv) SHC_REDUCE(64, 8); else SHC_REDUCE(64, 32);
+    }
+#undef SHC_REDUCE
     err = hipGetLastError();
     if (err != hipSuccess) return err;
   }
