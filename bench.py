@@ -56,6 +56,9 @@ def parse():
     p.add_argument("--no-dense", action="store_true", help="skip the dense-layer comparison")
     p.add_argument("--no-sweep", action="store_true",
                    help="skip the density sweep and the full-mesh layers")
+    p.add_argument("--step-only", action="store_true",
+                   help="the step, its per-kernel times and roofline only (one workload, "
+                        "for kernel traces of the density-sweep batch alone)")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--reps", type=int, default=50,
                    help="back-to-back launches per kernel for the per-kernel times")
@@ -347,10 +350,15 @@ def main():
         "kernel_rooflines": kernel_rooflines,
     }
 
+    if args.step_only:
+        print(json.dumps(out))
+        return
     out["gather_scatter"] = gather_scatter_measure(shc, synth, torch, args.reps)
     log("gather and scatter measured")
     out["cold_warm"] = cold_warm_measure(st, torch)
     log("cold and warm launches measured")
+    out["conv_plan"] = conv_plan_measure(st, shc, torch, args.reps)
+    log("conv plan measured")
     if not args.no_sweep:
         out["density_sweep"] = density_sweep(w, shc, synth, torch, args.reps)
         log("density sweep measured")
@@ -370,6 +378,45 @@ def main():
         out["cpu_baseline"] = cpu_baseline(w, spec, args.cpu_seconds)
         log("cpu baseline done")
     print(json.dumps(out))
+
+
+def conv_plan_measure(st, shc, torch, reps):
+    """The conv layer of the step from its table against the same layer from
+    a plan of the active set (index lists, sort and job lists built once by
+    shc_build_conv_plan): the plan build, a planned layer, and three layers
+    of that shape chained on the set -- from the table each, or one build
+    and three planned layers.  Back-to-back prepared calls between HIP
+    events; outputs checked equal."""
+    n = st.n
+    W, bias = st.weights[1], st.biases[1]
+    K, Cin, Cout = W.shape
+    nb = shc.conv_plan_bytes(n, K, Cin, Cout)
+    if nb == 0:
+        return {"config": f"N'={n}: no plan for this row count"}
+    plan = torch.empty(nb, dtype=torch.uint8, device=st.device)
+    src = st.acts[1]
+    y = [torch.empty((n, Cout), dtype=src.dtype, device=st.device) for _ in range(4)]
+    build = shc.prepare_build_conv_plan(st.table, K, Cin, Cout, plan)
+    tab = [shc.prepare_sparse_neighbor_conv_table(a, st.table, W, bias, b)
+           for a, b in ((src, y[0]), (y[0], y[1]), (y[1], y[2]))]
+    pl = [shc.prepare_sparse_neighbor_conv_planned(a, plan, W, bias, b)
+          for a, b in ((src, y[3]), (y[3], y[1]), (y[1], y[2]))]
+    build(n)
+    tab[0](n)
+    pl[0](n)
+    torch.cuda.synchronize()
+    same = bool(torch.equal(y[0], y[3]))
+    t_tab = _time_us(lambda: tab[0](n), torch, reps)
+    t_build = _time_us(lambda: build(n), torch, reps)
+    t_pl = _time_us(lambda: pl[0](n), torch, reps)
+    t_tab3 = _time_us(lambda: [c(n) for c in tab], torch, reps)
+    t_pl3 = _time_us(lambda: (build(n), [c(n) for c in pl]), torch, reps)
+    return {"config": f"N'={n} rows of the density-sweep set, K={K}, C={Cin}->{Cout} bf16, "
+                      f"plan {nb} bytes",
+            "planned_equals_table": same, "table_conv_us": round(t_tab, 2),
+            "plan_build_us": round(t_build, 2), "planned_conv_us": round(t_pl, 2),
+            "three_layers_table_us": round(t_tab3, 2),
+            "three_layers_build_and_planned_us": round(t_pl3, 2)}
 
 
 def group_norm_measure(st, shc, torch, reps, G=32):

@@ -311,6 +311,58 @@ int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t 
                                    hipStream_t stream);
 
 /*
+ * Conv plan of an active set.  The weight-stationary conv splits the active
+ * rows into row groups (one workgroup each, per column slice of W) and, in
+ * every workgroup, first builds the group's index lists from the table: the
+ * rows sorted by their first sparse slot, each wavefront's list of
+ * (16-row block, slot) jobs.  These depend only on the table and the shape,
+ * so one plan, built once, serves every column slice and every conv layer of
+ * the same shape on that active set (the layers of Eqs. 4-5 stacked on one
+ * mask).  A planned layer computes the same per-row sums in the same order as
+ * shc_sparse_neighbor_conv_table, so its output is identical to that call's.
+ *
+ * shc_conv_plan_max_rows: the largest active-row count whose conv with K
+ *   slots and Cin -> Cout channels of dtype takes a plan on the current
+ *   device (every smaller count does too); 0 when none does (fp32, a shape
+ *   the weight-stationary kernel does not run, invalid arguments, no
+ *   device).  Past it the conv runs on the tiled kernel, which builds no
+ *   index lists: use shc_sparse_neighbor_conv_table there.
+ *
+ * shc_conv_plan_bytes: bytes of a plan buffer that holds the plan of any
+ *   active set of at most n_rows rows (those up to shc_conv_plan_max_rows),
+ *   for that shape on the current device; 0 when none takes a plan.  A
+ *   multiple of 1024.
+ *
+ * shc_build_conv_plan: writes the plan of `table` (from
+ *   shc_build_neighbor_table or shc_compact_mask_table_start, [K][n_rows])
+ *   for layers of shape (n_rows, K, Cin, Cout, dtype) into `plan`, a device
+ *   buffer of plan_bytes >= shc_conv_plan_bytes(n_rows, ...) bytes
+ *   (caller-owned, 16-byte aligned; the plan of n_rows rows may take fewer:
+ *   the bytes past it are not touched).  Stream-ordered; reads only `table`.
+ *
+ * shc_sparse_neighbor_conv_planned: the conv of shc_sparse_neighbor_conv_table
+ *   with the index lists taken from `plan` (built by shc_build_conv_plan for
+ *   the same active set and the same n_rows, K, Cin, Cout, dtype; the table
+ *   itself is not read).  Other arguments as there.
+ *
+ * Errors: the calls' shape errors are those of shc_sparse_neighbor_conv_table;
+ * SHC_ERR_UNSUPPORTED when the shape (n_rows included) takes no plan,
+ * SHC_ERR_CAPACITY when plan_bytes is below that plan's size.  A plan of another active set or shape is not
+ * detected: the result is then wrong, but every access stays inside S, W,
+ * bias, out and the plan.
+ */
+int64_t shc_conv_plan_max_rows(int32_t K, int32_t Cin, int32_t Cout, int32_t dtype);
+size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype);
+int shc_build_conv_plan(const int32_t* table, int64_t n_rows, int32_t K, int32_t Cin,
+                        int32_t Cout, int32_t dtype, void* plan, size_t plan_bytes,
+                        hipStream_t stream);
+int shc_sparse_neighbor_conv_planned(const void* S, const void* plan, size_t plan_bytes,
+                                     int64_t n_rows, int32_t K, const void* W,
+                                     const float* bias, int32_t Cin, int32_t Cout,
+                                     int32_t dtype, int32_t act, void* out,
+                                     hipStream_t stream);
+
+/*
  * Scatter back to the dense per-vertex layout (C' = C, so row i returns to
  * (b_i, v_i)):
  *

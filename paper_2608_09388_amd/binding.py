@@ -79,6 +79,13 @@ _SIGS = {
     "shc_sparse_neighbor_conv_table": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_ptr,
                                                       _c_ptr, _c_i32, _c_i32, _c_i32, _c_i32,
                                                       _c_ptr, _c_ptr]),
+    "shc_conv_plan_max_rows": (_c_i64, [_c_i32, _c_i32, _c_i32, _c_i32]),
+    "shc_conv_plan_bytes": (_c_sz, [_c_i64, _c_i32, _c_i32, _c_i32, _c_i32]),
+    "shc_build_conv_plan": (ctypes.c_int, [_c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
+                                           _c_ptr, _c_sz, _c_ptr]),
+    "shc_sparse_neighbor_conv_planned": (ctypes.c_int, [_c_ptr, _c_ptr, _c_sz, _c_i64, _c_i32,
+                                                        _c_ptr, _c_ptr, _c_i32, _c_i32, _c_i32,
+                                                        _c_i32, _c_ptr, _c_ptr]),
     "shc_scatter": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
                                    _c_i32, _c_ptr, _c_ptr]),
     "shc_segment_group_norm": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32,
@@ -354,6 +361,38 @@ def sparse_neighbor_conv_table(S: torch.Tensor, table: torch.Tensor, n_rows: int
             _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, dt, act,
             _dev(out, "out", S.dtype, n_rows * Cout), _stream(stream)]
     _check(load().shc_sparse_neighbor_conv_table(*args), "shc_sparse_neighbor_conv_table")
+
+
+def conv_plan_max_rows(K: int, Cin: int, Cout: int, dtype: int = SHC_BF16) -> int:
+    """shc_conv_plan_max_rows: largest active-row count with a plan (0: none)."""
+    return int(load().shc_conv_plan_max_rows(K, Cin, Cout, dtype))
+
+
+def conv_plan_bytes(n_rows: int, K: int, Cin: int, Cout: int, dtype: int = SHC_BF16) -> int:
+    """shc_conv_plan_bytes: a buffer for the plan of any set of <= n_rows rows
+    (0 when none takes a plan)."""
+    return int(load().shc_conv_plan_bytes(n_rows, K, Cin, Cout, dtype))
+
+
+def build_conv_plan(table: torch.Tensor, n_rows: int, K: int, Cin: int, Cout: int,
+                    plan: torch.Tensor, dtype: int = SHC_BF16, stream=None):
+    """shc_build_conv_plan: table [K][n_rows] (int32), plan a device byte buffer."""
+    args = [_dev(table, "table", torch.int32, K * n_rows), n_rows, K, Cin, Cout, dtype,
+            _dev(plan, "plan"), plan.numel() * plan.element_size(), _stream(stream)]
+    _check(load().shc_build_conv_plan(*args), "shc_build_conv_plan")
+
+
+def sparse_neighbor_conv_planned(S: torch.Tensor, plan: torch.Tensor, n_rows: int,
+                                 W: torch.Tensor, bias: Optional[torch.Tensor], out: torch.Tensor,
+                                 act: int = SHC_ACT_RELU, stream=None):
+    """shc_sparse_neighbor_conv_planned: W [K][Cin][Cout], plan from build_conv_plan."""
+    K, Cin, Cout = W.shape
+    args = [_dev(S, "S", S.dtype, n_rows * Cin), _dev(plan, "plan"),
+            plan.numel() * plan.element_size(), n_rows, K,
+            _dev(W, "W", S.dtype, K * Cin * Cout), _opt_dev(bias, "bias", torch.float32, Cout),
+            Cin, Cout, _dtype_code(S), act, _dev(out, "out", S.dtype, n_rows * Cout),
+            _stream(stream)]
+    _check(load().shc_sparse_neighbor_conv_planned(*args), "shc_sparse_neighbor_conv_planned")
 
 
 def scatter(S: torch.Tensor, inv: torch.Tensor, coords: torch.Tensor, n_rows: int, B: int,
@@ -782,6 +821,24 @@ def prepare_sparse_neighbor_conv_table(S, table, W, bias, out, act=SHC_ACT_RELU,
             _dev(W, "W", S.dtype, K * Cin * Cout), _opt_dev(bias, "bias", torch.float32, Cout),
             Cin, Cout, _dtype_code(S), act, _dev(out, "out", S.dtype), _stream(stream)]
     return Prepared("shc_sparse_neighbor_conv_table", args, 2, n_max, (S, table, W, bias, out))
+
+
+def prepare_build_conv_plan(table, K, Cin, Cout, plan, dtype=SHC_BF16, stream=None) -> Prepared:
+    """shc_build_conv_plan with n_rows given per call (table [K][n_rows] of
+    the call's n_rows, plan sized for the largest n_rows called with)."""
+    args = [_dev(table, "table", torch.int32), 0, K, Cin, Cout, dtype, _dev(plan, "plan"),
+            plan.numel() * plan.element_size(), _stream(stream)]
+    return Prepared("shc_build_conv_plan", args, 1, table.numel() // K, (table, plan))
+
+
+def prepare_sparse_neighbor_conv_planned(S, plan, W, bias, out, act=SHC_ACT_RELU,
+                                         stream=None) -> Prepared:
+    K, Cin, Cout = W.shape
+    n_max = min(S.numel() // Cin, out.numel() // Cout)
+    args = [_dev(S, "S", S.dtype), _dev(plan, "plan"), plan.numel() * plan.element_size(), 0, K,
+            _dev(W, "W", S.dtype, K * Cin * Cout), _opt_dev(bias, "bias", torch.float32, Cout),
+            Cin, Cout, _dtype_code(S), act, _dev(out, "out", S.dtype), _stream(stream)]
+    return Prepared("shc_sparse_neighbor_conv_planned", args, 3, n_max, (S, plan, W, bias, out))
 
 
 def prepare_scatter(S, inv, coords, B, V, D, zero_fill=True, stream=None) -> Prepared:

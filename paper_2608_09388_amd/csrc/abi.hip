@@ -510,11 +510,13 @@ int shc_build_neighbor_table(const int32_t* coords, const int32_t* inv, int64_t 
                     "build_neighbor_table launch");
 }
 
-int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t n_rows,
-                                   int32_t K, const void* W, const float* bias, int32_t Cin,
-                                   int32_t Cout, int32_t dtype, int32_t act, void* out,
-                                   hipStream_t stream) {
-  g_last_error[0] = 0;
+}  // extern "C"
+
+namespace {
+
+// Shape checks shared by the table conv, its plan and the planned conv.
+int check_conv_shape(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype,
+                     int32_t act) {
   SHC_TRY(check_rows(n_rows));
   SHC_TRY(check_dtype(dtype));
   SHC_TRY(check_channels("Cin", Cin));
@@ -523,6 +525,70 @@ int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t 
   if (K > kMaxSlots) return fail(SHC_ERR_UNSUPPORTED, "K = %d exceeds %d slots", K, kMaxSlots);
   if (act != SHC_ACT_NONE && act != SHC_ACT_RELU)
     return fail(SHC_ERR_UNSUPPORTED, "unknown activation code %d", act);
+  return SHC_OK;
+}
+
+// A conv shape on the current device for the plan queries (false: no device).
+bool plan_shape(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, shc::GemmArgs* a,
+                int* cus) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return false;
+  *a = shc::GemmArgs{};
+  a->n_rows = n_rows;
+  a->B = 1;
+  a->V = 1;
+  a->K = K;
+  a->Cin = Cin;
+  a->Cout = Cout;
+  return true;
+}
+
+// Plan size and row-group stride of a conv of exactly n_rows rows (0: no
+// plan for this shape, or no device).
+int64_t plan_size(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype,
+                  int64_t* stride) {
+  *stride = 0;
+  shc::GemmArgs a;
+  int cus = 0;
+  if (!plan_shape(n_rows, K, Cin, Cout, &a, &cus)) return 0;
+  return shc::conv_plan_bytes(a, dtype == SHC_BF16, cus, stride);
+}
+
+bool plan_query_args_ok(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype) {
+  return n_rows > 0 && n_rows <= INT32_MAX && K > 0 && K <= kMaxSlots && Cin > 0 &&
+         Cin % 16 == 0 && Cin <= kMaxChannels && Cout > 0 && Cout % 16 == 0 &&
+         Cout <= kMaxChannels && (dtype == SHC_F32 || dtype == SHC_BF16);
+}
+
+// The plan buffer of a build or planned call: present, and large enough for
+// this shape's plan.
+int check_plan(const void* plan, size_t plan_bytes, int64_t n_rows, int32_t K, int32_t Cin,
+               int32_t Cout, int32_t dtype, int64_t* stride) {
+  SHC_PTR(plan, "plan");
+  const int64_t need = plan_size(n_rows, K, Cin, Cout, dtype, stride);
+  if (need == 0)
+    return fail(SHC_ERR_UNSUPPORTED,
+                "no conv plan for n_rows = %lld, K = %d, Cin = %d, Cout = %d, dtype %d on "
+                "this device",
+                (long long)n_rows, K, Cin, Cout, dtype);
+  if ((int64_t)plan_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "plan_bytes = %zu is below the %lld bytes of this plan",
+                plan_bytes, (long long)need);
+  return SHC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t n_rows,
+                                   int32_t K, const void* W, const float* bias, int32_t Cin,
+                                   int32_t Cout, int32_t dtype, int32_t act, void* out,
+                                   hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_conv_shape(n_rows, K, Cin, Cout, dtype, act));
   if (n_rows == 0) return SHC_OK;
   SHC_PTR(S, "S");
   SHC_PTR(table, "table");
@@ -544,6 +610,77 @@ int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t 
   a.relu = act == SHC_ACT_RELU;
   return hip_status(shc::launch_gather_gemm(a, true, dtype == SHC_BF16, stream),
                     "sparse_neighbor_conv_table launch");
+}
+
+size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype) {
+  if (!plan_query_args_ok(n_rows, K, Cin, Cout, dtype)) return 0;
+  shc::GemmArgs a;
+  int cus = 0;
+  if (!plan_shape(n_rows, K, Cin, Cout, &a, &cus)) return 0;
+  return (size_t)shc::conv_plan_bytes_upto(a, dtype == SHC_BF16, cus);
+}
+
+int64_t shc_conv_plan_max_rows(int32_t K, int32_t Cin, int32_t Cout, int32_t dtype) {
+  if (!plan_query_args_ok(1, K, Cin, Cout, dtype)) return 0;
+  shc::GemmArgs a;
+  int cus = 0;
+  if (!plan_shape(1, K, Cin, Cout, &a, &cus)) return 0;
+  return shc::conv_plan_max_rows(a, dtype == SHC_BF16, cus);
+}
+
+int shc_build_conv_plan(const int32_t* table, int64_t n_rows, int32_t K, int32_t Cin,
+                        int32_t Cout, int32_t dtype, void* plan, size_t plan_bytes,
+                        hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_conv_shape(n_rows, K, Cin, Cout, dtype, SHC_ACT_NONE));
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(table, "table");
+  int64_t stride;
+  SHC_TRY(check_plan(plan, plan_bytes, n_rows, K, Cin, Cout, dtype, &stride));
+  shc::GemmArgs a{};
+  a.table = table;
+  a.n_rows = n_rows;
+  a.B = 1;
+  a.V = 1;
+  a.K = K;
+  a.Cin = Cin;
+  a.Cout = Cout;
+  a.plan_out = plan;
+  a.plan_stride = stride;
+  return hip_status(shc::launch_gather_gemm(a, true, dtype == SHC_BF16, stream),
+                    "build_conv_plan launch");
+}
+
+int shc_sparse_neighbor_conv_planned(const void* S, const void* plan, size_t plan_bytes,
+                                     int64_t n_rows, int32_t K, const void* W,
+                                     const float* bias, int32_t Cin, int32_t Cout,
+                                     int32_t dtype, int32_t act, void* out,
+                                     hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_conv_shape(n_rows, K, Cin, Cout, dtype, act));
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(S, "S");
+  SHC_PTR(W, "W");
+  SHC_OPT_PTR(bias, "bias");
+  SHC_PTR(out, "out");
+  int64_t stride;
+  SHC_TRY(check_plan(plan, plan_bytes, n_rows, K, Cin, Cout, dtype, &stride));
+  shc::GemmArgs a{};
+  a.S = S;
+  a.W = W;
+  a.bias = bias;
+  a.out = out;
+  a.n_rows = n_rows;
+  a.B = 1;
+  a.V = 1;
+  a.K = K;
+  a.Cin = Cin;
+  a.Cout = Cout;
+  a.relu = act == SHC_ACT_RELU;
+  a.plan = plan;
+  a.plan_stride = stride;
+  return hip_status(shc::launch_gather_gemm(a, true, dtype == SHC_BF16, stream),
+                    "sparse_neighbor_conv_planned launch");
 }
 
 int shc_scatter(const void* S, const int32_t* inv, const int32_t* coords, int64_t n_rows,

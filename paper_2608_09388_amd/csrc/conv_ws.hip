@@ -34,6 +34,7 @@
 // Every output row is accumulated over the same (slot, k-step) sequence
 // whatever block it lands in (absent slots contribute exact zeros), so the
 // result does not depend on the order the sort produced.
+#include <algorithm>
 #include <mutex>
 
 #include "shc_internal.h"
@@ -109,9 +110,20 @@ __device__ __forceinline__ void lds_direct_load16(const void* src, SHC_LDS void*
 // DW: the weight slice goes straight into LDS with 16-byte direct loads, all
 // issued first (bf16, full column slices, a multiple of 64 vectors; conv from
 // a table, or linear).
-template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM, bool DW = false>
+// MODE (conv from a table, bf16, direct weight loads only):
+//   kFull    -- everything in one launch;
+//   kPlanOut -- the index lists, sort and job lists of one row group, without
+//               the weights, copied from LDS to plan + blockIdx.x * plan_stride
+//               (the "plan" of the active set: the same for every column slice
+//               and every layer of the same shape on it);
+//   kPlanned -- the index lists come from such a plan (16-byte direct loads
+//               into LDS beside the weight slice) instead of the table.
+constexpr int kFull = 0, kPlanOut = 1, kPlanned = 2;
+template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM, bool DW = false,
+          int MODE = kFull>
 __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kernel(GemmArgs a,
                                                                                    int R) {
+  static_assert(MODE == kFull || (BF16 && CONV && TBL && DW), "plans: bf16 table conv only");
   constexpr int kThreads = CONV ? kThreadsConv : kThreadsLin;
   constexpr int kWaves = kThreads / 64;
   constexpr int kRPT = kMaxRows / kThreads;  // rows per thread in the index build
@@ -130,8 +142,8 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   const int Ktot = K * Cin;
   const int KS = Cin / E::kstep;  // k-steps per slot (Cin * e is a multiple of 64)
 
-  unsigned char* wl = smem;  // [Ktot][WROWW]
-  const int wbytes = (Ktot * WROWW + 15) & ~15;
+  unsigned char* wl = smem;  // [Ktot][WROWW] (none in a plan build)
+  const int wbytes = MODE == kPlanOut ? 0 : (Ktot * WROWW + 15) & ~15;
   int32_t* srcs = reinterpret_cast<int32_t*>(smem + wbytes);    // [R][K], sorted order
   int32_t* perm = srcs + R * K;                                 // [R] position -> row
   uint32_t* blkmask = reinterpret_cast<uint32_t*>(perm + R);    // [R/16]
@@ -154,12 +166,13 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   const unsigned char* W = static_cast<const unsigned char*>(a.W);
   // bias of this lane's columns, loaded now so the prologue hides the latency
   // (the selection below waits until after it)
+  // (a plan build has neither weights nor bias)
   float bias_raw[NCB];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
     const int col = n0 + cb * 16 + l16;
     const float* bp = a.bias != nullptr ? a.bias : reinterpret_cast<const float*>(a.W);
-    bias_raw[cb] = bp[(a.bias != nullptr && col < Cout) ? col : 0];
+    bias_raw[cb] = MODE == kPlanOut ? 0.f : bp[(a.bias != nullptr && col < Cout) ? col : 0];
   }
 
   // Byte offset of 16-byte vector q in weight-slice row k.  For bf16 the
@@ -200,7 +213,9 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
     }
   };
   i32x4 wv[kWBatch];
-  if constexpr (DW) {
+  if constexpr (MODE == kPlanOut) {
+    // no weights in a plan
+  } else if constexpr (DW) {
     // LDS vector v = 64 c + lane of the slice is row k = v / VPR, position
     // p = v % VPR; it holds source vector q with w_col(k, q) = 16 p (the
     // chunk swizzle is its own inverse).  A wavefront's direct load writes
@@ -218,14 +233,30 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
     load_w(0, wv);
   }
 
-  for (int q = tid; q < R / 16; q += kThreads) blkmask[q] = 0;
-  for (int q = tid; q < kBuckets; q += kThreads) bcnt[q] = 0;  // the sort's histogram
-  for (int q = tid; q < E::kstep * WROWW / 16; q += kThreads)
-    reinterpret_cast<i32x4*>(zrows)[q] = i32x4{0, 0, 0, 0};
+  if constexpr (MODE == kPlanned) {
+    // the row group's index lists, sort and job lists: the plan's image of
+    // this LDS region, 64 vectors of 16 bytes per wavefront instruction (the
+    // image is padded to whole 1 KB runs in the plan)
+    const int ivecs = (ws_idx_bytes(R, K, kWaves, kRPT) + 1023) / 1024 * 64;
+    const unsigned char* img = static_cast<const unsigned char*>(a.plan) +
+                               (int64_t)blockIdx.x * a.plan_stride;
+    unsigned char* ldst = smem + wbytes;
+    for (int c = wave; c < ivecs / 64; c += kWaves)
+      lds_direct_load16(img + (int64_t)c * 1024 + lane * 16, (SHC_LDS void*)(ldst + c * 1024));
+  } else {
+    for (int q = tid; q < R / 16; q += kThreads) blkmask[q] = 0;
+    for (int q = tid; q < kBuckets; q += kThreads) bcnt[q] = 0;  // the sort's histogram
+  }
+  if constexpr (MODE != kPlanOut) {
+    for (int q = tid; q < E::kstep * WROWW / 16; q += kThreads)
+      reinterpret_cast<i32x4*>(zrows)[q] = i32x4{0, 0, 0, 0};
+  }
 
   // ---- index lists, sorted by first sparse slot ---------------------------------
   // thread tid handles rows t = tid + rr * kThreads (rr < kRPT) of this workgroup
-  if (CONV) {
+  if constexpr (MODE == kPlanned) {
+    // from the plan (loaded above)
+  } else if (CONV) {
     int32_t sv[kRPT][KM];
     if (TBL) {
       // one round: slot-major table rows, coalesced across the wavefront
@@ -407,7 +438,11 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   // in order, each with one job per live slot (ascending) or a single
   // bias-only job; packed as b << 8 | (slot + 1) << 1 | last.
   int njobs = 0;
-  {
+  if constexpr (MODE == kPlanned) {
+    // the plan's job count of this wavefront (at most kMaxJobs: a plan that
+    // is not this shape's cannot run the loop past its list)
+    njobs = min(scnt[wave], kMaxJobs);
+  } else {
     const int nb = nblk > wave ? (nblk - wave + kWaves - 1) / kWaves : 0;
     int32_t* mine = jobl + wave * kMaxJobs;
     for (int i0 = 0; i0 < nb; i0 += 64) {
@@ -440,6 +475,20 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   njobs = __builtin_amdgcn_readfirstlane(njobs);
+  if constexpr (MODE == kPlanOut) {
+    // every wavefront's job count beside its list (scnt is free after the
+    // sort), then the whole region -- index lists, positions, block masks,
+    // job lists -- to this row group's plan image
+    if (lane == 0) scnt[wave] = njobs;
+    __syncthreads();
+    const int ibytes = ws_idx_bytes(R, K, kWaves, kRPT);
+    const unsigned char* src = smem + wbytes;
+    unsigned char* img = static_cast<unsigned char*>(a.plan_out) +
+                         (int64_t)blockIdx.x * a.plan_stride;
+    for (int q = tid; q < ibytes / 16; q += kThreads)
+      *reinterpret_cast<i32x4*>(img + q * 16) = *reinterpret_cast<const i32x4*>(src + q * 16);
+    return;
+  }
   // lane l holds job (jt & ~63) + l; refilled every 64 jobs
   int jt = 0;
   int jreg = jobl[wave * kMaxJobs + lane];
@@ -448,6 +497,8 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
     if ((jt & 63) == 0 && jt > 0) jreg = jobl[wave * kMaxJobs + ((jt + lane) & (kMaxJobs - 1))];
     const int w = __builtin_amdgcn_readlane(jreg, jt & 63);
     ++jt;
+    if (MODE == kPlanned && ((w >> 8) >= nblk || (w >> 8) < 0 || ((w >> 1) & 127) > K))
+      return Job{-1, -1, true};
     return Job{w >> 8, ((w >> 1) & 127) - 1, (w & 1) != 0};
   };
 
@@ -660,11 +711,13 @@ __global__ __launch_bounds__(CONV ? kThreadsConv : kThreadsLin, 1) void ws_kerne
   }
 }
 
-template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM, bool DW = false>
+template <bool BF16, int WS, bool CONV, bool TBL, int KM, int KSM, bool DW = false,
+          int MODE = kFull>
 hipError_t launch_ws(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) {
   const unsigned gx = (unsigned)((a.n_rows + pl.rows - 1) / pl.rows);
-  const unsigned gy = (unsigned)((a.Cout + WS - 1) / WS);
-  auto kern = ws_kernel<BF16, WS, CONV, TBL, KM, KSM, DW>;
+  // a plan is one image per row group, shared by the column slices
+  const unsigned gy = MODE == kPlanOut ? 1u : (unsigned)((a.Cout + WS - 1) / WS);
+  auto kern = ws_kernel<BF16, WS, CONV, TBL, KM, KSM, DW, MODE>;
   // allow the large dynamic LDS allocation; once per instantiation
   static std::once_flag once;
   static hipError_t attr_err = hipSuccess;
@@ -673,8 +726,10 @@ hipError_t launch_ws(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) {
                                    hipFuncAttributeMaxDynamicSharedMemorySize, kLdsLimit);
   });
   if (attr_err != hipSuccess) return attr_err;
-  hipLaunchKernelGGL(kern, dim3(gx, gy), dim3(CONV ? kThreadsConv : kThreadsLin), (size_t)pl.total,
-                     stream, a, pl.rows);
+  // a plan build holds only the index region in LDS
+  const size_t lds = MODE == kPlanOut ? (size_t)pl.idx_bytes : (size_t)pl.total;
+  hipLaunchKernelGGL(kern, dim3(gx, gy), dim3(CONV ? kThreadsConv : kThreadsLin), lds, stream, a,
+                     pl.rows);
   return hipGetLastError();
 }
 
@@ -691,9 +746,18 @@ hipError_t launch_ws_k(const GemmArgs& a, const WsPlan& pl, hipStream_t stream) 
     return dw ? launch_ws<BF16, WS, false, false, 1, 8, BF16>(a, pl, stream)
               : launch_ws<BF16, WS, false, false, 1, 8>(a, pl, stream);
   }
-  if (a.table != nullptr) {
+  if (a.table != nullptr || a.plan != nullptr) {
     // direct weight loads: full column slices, whole 64-vector chunks
     const bool dw = BF16 && a.Cout % WS == 0 && ((int64_t)a.K * a.Cin * (WS * 2 / 16)) % 64 == 0;
+    if constexpr (BF16) {
+      if (dw && a.plan_out != nullptr)
+        return ks <= 4 ? launch_ws<true, WS, true, true, 10, 4, true, kPlanOut>(a, pl, stream)
+                       : launch_ws<true, WS, true, true, 10, 8, true, kPlanOut>(a, pl, stream);
+      if (dw && a.plan != nullptr)
+        return ks <= 4 ? launch_ws<true, WS, true, true, 10, 4, true, kPlanned>(a, pl, stream)
+                       : launch_ws<true, WS, true, true, 10, 8, true, kPlanned>(a, pl, stream);
+    }
+    if (a.plan_out != nullptr || a.table == nullptr) return hipErrorInvalidValue;
     if (ks <= 4)
       return dw ? launch_ws<BF16, WS, true, true, 10, 4, BF16>(a, pl, stream)
                 : launch_ws<BF16, WS, true, true, 10, 4>(a, pl, stream);
@@ -722,7 +786,8 @@ bool ws_plan(const GemmArgs& a, bool conv, bool bf16, int num_cus, WsPlan* pl) {
   if ((int64_t)a.n_rows * a.Cout * e > 0x7FFF0000LL) return false;
   // sparse inputs only: at high density the tiled kernel (gemm.hip) is faster
   // than building the index lists here (with a prebuilt table there is none)
-  if (conv && a.table == nullptr && (double)a.n_rows > 0.3 * (double)a.B * (double)a.V)
+  if (conv && a.table == nullptr && a.plan == nullptr && a.plan_out == nullptr &&
+      (double)a.n_rows > 0.3 * (double)a.B * (double)a.V)
     return false;
   int ws = 0;
   for (int cand : {128, 64, 32}) {
@@ -755,6 +820,60 @@ bool ws_plan(const GemmArgs& a, bool conv, bool bf16, int num_cus, WsPlan* pl) {
   pl->scratch = ws_scratch(ws, e, waves);
   pl->total = wb + pl->idx_bytes + pl->scratch;
   return true;
+}
+
+int64_t conv_plan_bytes(const GemmArgs& a_in, bool bf16, int num_cus, int64_t* stride) {
+  *stride = 0;
+  // sized as the conv from a table that builds it (the pointer is never read)
+  GemmArgs a = a_in;
+  a.plan_out = &a;
+  WsPlan pl;
+  if (!bf16 || a.n_rows <= 0 || !ws_plan(a, true, true, num_cus, &pl)) return 0;
+  // the same condition as the launch's direct weight loads
+  if (a.Cout % pl.ws != 0 || ((int64_t)a.K * a.Cin * (pl.ws * 2 / 16)) % 64 != 0) return 0;
+  const int waves = kThreadsConv / 64, rpt = kMaxRows / kThreadsConv;
+  *stride = ((int64_t)ws_idx_bytes(pl.rows, a.K, waves, rpt) + 1023) / 1024 * 1024;
+  return ((a.n_rows + pl.rows - 1) / pl.rows) * *stride;
+}
+
+int64_t conv_plan_max_rows(const GemmArgs& a_in, bool bf16, int num_cus) {
+  // A plan exists for every row count up to a limit (the one-wave and 32-bit
+  // offset bounds of ws_plan grow with n, the rest does not depend on it).
+  GemmArgs a = a_in;
+  int64_t st;
+  a.n_rows = 1;
+  if (conv_plan_bytes(a, bf16, num_cus, &st) == 0) return 0;
+  int64_t lo = 1, hi = INT32_MAX;  // plan at lo; find the last n with one
+  a.n_rows = hi;
+  if (conv_plan_bytes(a, bf16, num_cus, &st) > 0) return hi;
+  while (hi - lo > 1) {
+    const int64_t mid = lo + (hi - lo) / 2;
+    a.n_rows = mid;
+    if (conv_plan_bytes(a, bf16, num_cus, &st) > 0) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+int64_t conv_plan_bytes_upto(const GemmArgs& a_in, bool bf16, int num_cus) {
+  // Rows per group R(n) rise in steps of 16 with n, and within a step the plan
+  // (row groups x image stride) only grows; so the largest plan of any n <=
+  // n_rows is at the end of a step or at the last n that takes a plan.
+  const int64_t nmax = std::min<int64_t>(a_in.n_rows, conv_plan_max_rows(a_in, bf16, num_cus));
+  if (nmax <= 0) return 0;
+  GemmArgs a = a_in;
+  a.n_rows = 1;
+  a.plan_out = &a;
+  WsPlan pl;
+  if (!ws_plan(a, true, true, num_cus, &pl)) return 0;
+  const int64_t slices = (a.Cout + pl.ws - 1) / pl.ws;
+  int64_t best = 0, st;
+  for (int r = 64; r <= kMaxRows + 16; r += 16) {
+    const int64_t n = r > kMaxRows ? nmax : std::min(nmax, (int64_t)r * num_cus / slices);
+    if (n <= 0) continue;
+    a.n_rows = n;
+    best = std::max(best, conv_plan_bytes(a, bf16, num_cus, &st));
+  }
+  return best;
 }
 
 hipError_t launch_ws_gemm(const GemmArgs& a, bool conv, bool bf16, const WsPlan& pl,

@@ -626,6 +626,8 @@ hipError_t launch_gather_gemm(const GemmArgs& a, bool conv, bool bf16, hipStream
   if (e != hipSuccess) return e;
   WsPlan plan;
   if (ws_plan(a, conv, bf16, cus, &plan)) return launch_ws_gemm(a, conv, bf16, plan, stream);
+  // a conv plan exists only for the weight-stationary kernel
+  if (a.plan != nullptr || a.plan_out != nullptr) return hipErrorInvalidValue;
   if (bf16) return conv ? launch_typed<true, true>(a, stream) : launch_typed<true, false>(a, stream);
   return conv ? launch_typed<false, true>(a, stream) : launch_typed<false, false>(a, stream);
 }

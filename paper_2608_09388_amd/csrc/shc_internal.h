@@ -137,6 +137,12 @@ struct GemmArgs {
   int32_t relu;
   int32_t gather;       // linear only: input row i is S[coords b_i * V + v_i] (S = dense x)
   uint32_t cin_magic;   // ceil(2^32 / Cin), filled in by the launcher
+  // conv from a table, weight-stationary kernel only: write the active set's
+  // plan (index lists, sort, job lists per row group) to plan_out instead of
+  // computing, or read it from plan; images plan_stride bytes apart
+  void* plan_out;
+  const void* plan;
+  int64_t plan_stride;
 };
 
 hipError_t launch_gather_gemm(const GemmArgs& a, bool conv, bool bf16, hipStream_t stream);
@@ -152,6 +158,13 @@ struct WsPlan {
   int total;
 };
 bool ws_plan(const GemmArgs& a, bool conv, bool bf16, int num_cus, WsPlan* plan);
+// Bytes of the plan of a conv from a table with this shape (0: the shape
+// takes no plan), and the distance between two row groups' images.
+int64_t conv_plan_bytes(const GemmArgs& a, bool bf16, int num_cus, int64_t* stride);
+// The largest row count whose conv takes a plan (0: none), and the largest
+// plan of any row count up to a.n_rows.
+int64_t conv_plan_max_rows(const GemmArgs& a, bool bf16, int num_cus);
+int64_t conv_plan_bytes_upto(const GemmArgs& a, bool bf16, int num_cus);
 hipError_t launch_ws_gemm(const GemmArgs& a, bool conv, bool bf16, const WsPlan& plan,
                           hipStream_t stream);
 

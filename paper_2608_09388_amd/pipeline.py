@@ -15,7 +15,11 @@ compaction itself (shc_compact_mask_table_start) when a body's vertices fit
 its on-chip row numbering.
 
 The active set never changes across layers (C'_k = C_k, Sec. 3.2), so the
-active count is read back once per mask and passed to every layer call.
+active count is read back once per mask and passed to every layer call.  For
+the same reason the conv's index lists can be built once per mask and conv
+shape (shc_build_conv_plan) and read by every layer of that shape
+(shc_sparse_neighbor_conv_planned); by default this is done for shapes shared
+by two or more conv layers.
 
 The index buffers of a mask (coords, inv, row_ptr, the neighbour-row table)
 exist twice (three times with a side stream).  ``run(steps)`` uses this for
@@ -88,6 +92,19 @@ class _IndexSet:
                                                             self.table, stream=st.side)
                            if self.table is not None and st.side is not None and not self.fused
                            else None)
+        # conv plans (shc_build_conv_plan): one per conv shape that takes one,
+        # built after the table, read by every conv layer of that shape while
+        # the batch's row count is within the shape's limit
+        self.plans = {}
+        for key, n_lim in st.plan_shapes.items():
+            K_, Cin, Cout = key
+            nb = shc.conv_plan_bytes(min(BV, n_lim), K_, Cin, Cout)
+            buf = torch.empty(nb, dtype=torch.uint8, device=dev)
+            build = shc.prepare_build_conv_plan(self.table, K_, Cin, Cout, buf)
+            build_side = (shc.prepare_build_conv_plan(self.table, K_, Cin, Cout, buf,
+                                                      stream=st.side)
+                          if st.side is not None else None)
+            self.plans[key] = (buf, n_lim, build, build_side)
         self.layers = [self._layer_call(st, l, st.acts[l + 1]) for l in range(len(st.w.layers))]
         last = st.acts[-1]
         self.scatter = (shc.prepare_scatter(last, self.inv, self.coords, B, V, st.dense_out)
@@ -108,23 +125,46 @@ class _IndexSet:
                                                           stream=st.tail)
                               if st.pooled is not None else None for i in range(2)]
 
+    def build_plans(self, n: int, side: bool = False):
+        """The conv plans of this set's n rows (on the side stream: side)."""
+        for buf, n_lim, build, build_side in self.plans.values():
+            if 0 < n <= n_lim:
+                (build_side if side else build)(n)
+
     def _layer_call(self, st: "SparseStack", l: int, dst: torch.Tensor):
         """Layer l of the stack on this index set, writing dst."""
         spec = st.w.layers[l]
         src = st.acts[l]
         a = st.act if spec.relu else shc.SHC_ACT_NONE
         if spec.kind == "conv":
-            return shc.prepare_sparse_neighbor_conv_table(src, self.table, st.weights[l],
-                                                          st.biases[l], dst, a)
+            table = shc.prepare_sparse_neighbor_conv_table(src, self.table, st.weights[l],
+                                                           st.biases[l], dst, a)
+            plan = self.plans.get(tuple(st.weights[l].shape))
+            if plan is None:
+                return table
+            planned = shc.prepare_sparse_neighbor_conv_planned(src, plan[0], st.weights[l],
+                                                               st.biases[l], dst, a)
+            return _PlannedConv(table, planned, plan[1])
         if l == 0 and st.fused_gather:
             return shc.prepare_gather_sparse_linear(st.x, self.coords, st.B, st.V, st.weights[l],
                                                     st.biases[l], dst, a)
         return shc.prepare_sparse_linear(src, st.weights[l], st.biases[l], dst, a)
 
 
+class _PlannedConv:
+    """A conv layer that reads its set's plan when the batch's row count has
+    one (the plan was built for it), else the table."""
+
+    def __init__(self, table, planned, n_lim: int):
+        self.table, self.planned, self.n_lim = table, planned, n_lim
+
+    def __call__(self, n: int):
+        return self.planned(n) if 0 < n <= self.n_lim else self.table(n)
+
+
 class SparseStack:
     def __init__(self, w: Workload, device: str = "cuda", act: int = shc.SHC_ACT_RELU,
-                 side_stream: bool = False):
+                 side_stream: bool = False, conv_plans: Optional[bool] = None):
         self.w = w
         self.device = torch.device(device)
         # every prepared call below launches on the stream current now; step()
@@ -166,6 +206,24 @@ class SparseStack:
         # A first linear layer reads its rows straight from x (gather fused in);
         # otherwise the active rows are gathered into acts[0] first.
         self.fused_gather = len(w.layers) > 0 and w.layers[0].kind == "linear"
+        # Conv shapes that read a plan of the active set instead of sorting
+        # the table's rows in every layer and column slice.  A plan costs a
+        # launch of its own (7.7 us for 67 K rows at K = 9, C = 128, against
+        # 4.4 us saved per planned layer), so by default a shape takes one
+        # only when two or more conv layers share it; conv_plans = True /
+        # False forces plans on / off for every conv shape that can take one.
+        self.plan_shapes: Dict[Tuple[int, int, int], int] = {}
+        if w.dtype == "bf16":
+            shapes: Dict[Tuple[int, int, int], int] = {}
+            for l, spec in enumerate(w.layers):
+                if spec.kind == "conv":
+                    key = tuple(self.weights[l].shape)
+                    shapes[key] = shapes.get(key, 0) + 1
+            for key, count in shapes.items():
+                use = conv_plans if conv_plans is not None else count >= 2
+                n_lim = shc.conv_plan_max_rows(*key) if use else 0
+                if n_lim > 0:
+                    self.plan_shapes[key] = n_lim
         # two index sets, or three with a side stream (run() then checks an
         # index set's reuse from the host; see _run_pipelined)
         self._sets = [_IndexSet(self) for _ in range(3 if side_stream else 2)]
@@ -200,10 +258,13 @@ class SparseStack:
         s.n = s.compact()
         if s.table_call is not None:
             s.table_call(s.n)
+        s.build_plans(s.n)
         return s.n
 
     def build_table(self):
+        """The neighbour-row table (and the conv plans) of the current set."""
         self._set.table_call(self.n)
+        self._set.build_plans(self.n)
 
     def gather(self):
         """Gather the active rows into acts[0] (not needed by the step when
@@ -227,11 +288,14 @@ class SparseStack:
         if s.pool is not None:
             s.pool(s.n)
 
-    def _front(self, s: _IndexSet, around=None, table_done: bool = False):
+    def _front(self, s: _IndexSet, around=None, table_done: bool = False,
+               plans_done: bool = False):
         """Everything of a batch after its compaction, up to its last layer;
         ``around = (l, ev_a, ev_b)`` records the events around layer l."""
         if s.table_call is not None and not table_done:
             s.table_call(s.n)
+        if not plans_done:
+            s.build_plans(s.n)
         if not self.fused_gather:
             s.gather(s.n)
         for l, call in enumerate(s.layers):
@@ -361,6 +425,7 @@ class SparseStack:
         s.compact.start()
         s.n = s.compact.wait()
         table_done = s.fused
+        plans_done = False
         for k in range(steps):
             i = (steps - 1 - k) % 2        # the last batch writes acts[-1]
             around = None
@@ -369,6 +434,8 @@ class SparseStack:
             # layers of batch k (current stream)
             if s.table_call is not None and not table_done:
                 s.table_call(s.n)
+            if not plans_done:
+                s.build_plans(s.n)
             if not self.fused_gather:
                 s.gather(s.n)
             for l in range(nl):
@@ -408,7 +475,9 @@ class SparseStack:
                 nxt.n = nxt.compact_side.wait()
                 if nxt.table_side is not None:
                     nxt.table_side(nxt.n)
+                nxt.build_plans(nxt.n, side=True)
                 table_done = nxt.table is not None    # built on the side stream
+                plans_done = True
                 ev["ready"].record(side)
                 ev["ready"].wait(main)
                 cur = nxt_i

@@ -365,6 +365,55 @@ def test_neighbor_table_validation(lib):
     assert conv(n=0, S=None, table=None, out=None) == 0
 
 
+def test_conv_plan_validation(lib):
+    Q = lib.shc_conv_plan_bytes
+    bf = shc.SHC_BF16
+    assert Q(0, 9, 128, 128, bf) == 0
+    assert Q(-1, 9, 128, 128, bf) == 0
+    assert Q(1 << 31, 9, 128, 128, bf) == 0
+    assert Q(100, 0, 128, 128, bf) == 0
+    assert Q(100, 33, 128, 128, bf) == 0
+    assert Q(100, 9, 20, 128, bf) == 0
+    assert Q(100, 9, 128, 0, bf) == 0
+    assert Q(100, 9, 128, 128, 7) == 0
+    P = lib.shc_build_conv_plan
+
+    def plan(**kw):
+        a = dict(table=A, n=10, K=9, Cin=128, Cout=128, dt=bf, plan=A, nb=1 << 20)
+        a.update(kw)
+        return P(a["table"], a["n"], a["K"], a["Cin"], a["Cout"], a["dt"], a["plan"], a["nb"],
+                 None)
+
+    assert plan(table=None) == -1 and "table" in err(lib)
+    assert plan(table=MIS) == -3
+    assert plan(plan=None) == -1 and "plan" in err(lib)
+    assert plan(plan=MIS) == -3
+    assert plan(K=0) == -1
+    assert plan(K=40) == -4
+    assert plan(Cout=24) == -4
+    assert plan(dt=5) == -4
+    assert plan(n=-2) == -1
+    assert plan(n=0, table=None, plan=None) == 0     # N' = 0 is a no-op
+    C = lib.shc_sparse_neighbor_conv_planned
+
+    def conv(**kw):
+        a = dict(S=A, plan=A, nb=1 << 20, n=10, K=9, W=A, bias=None, Cin=128, Cout=128, dt=bf,
+                 act=1, out=A)
+        a.update(kw)
+        return C(a["S"], a["plan"], a["nb"], a["n"], a["K"], a["W"], a["bias"], a["Cin"],
+                 a["Cout"], a["dt"], a["act"], a["out"], None)
+
+    assert conv(plan=None) == -1 and "plan" in err(lib)
+    assert conv(plan=MIS) == -3
+    assert conv(S=None) == -1 and "S" in err(lib)
+    assert conv(W=MIS) == -3
+    assert conv(out=None) == -1
+    assert conv(bias=MIS) == -3
+    assert conv(act=3) == -4
+    assert conv(K=33) == -4
+    assert conv(n=0, S=None, plan=None, out=None) == 0
+
+
 def test_binding_refuses_cpu_tensors():
     torch = pytest.importorskip("torch")
     x = torch.zeros(4 * 655, 16)
