@@ -513,7 +513,9 @@ int shc_build_transposed_table(const int32_t* coords, const int32_t* inv, int64_
  *   ws: device workspace of shc_sparse_linear_backward_workspace bytes.
  * Every sum has a fixed order: dS in fp32 over Cout, rounded once; dW in
  * fp32 over chunks of rows, the chunks combined in fp64; db in fp32 over
- * splits of rows, combined in fp64.  Results repeat bit for bit.
+ * splits of rows, combined in fp64.  Results repeat bit for bit on one
+ * device (the chunks of the bf16 layer with Cin, Cout in {64, 128}, which
+ * runs in one pass over the rows, are sized by the device's CU count).
  * dtype SHC_BF16 or SHC_F32; Cout <= 256.
  */
 size_t shc_sparse_linear_backward_workspace(int64_t n_rows, int32_t Cin, int32_t Cout,

@@ -11,6 +11,8 @@
 // r_i0 = i and K = 1 for the linear layer).
 //
 // Kernels:
+//   * linear_bwd_fused -- the bf16 linear layer of 64 or 128 channels in one
+//     pass over the rows (dZ in registers, dS, partial dW and column sums);
 //   * relu_bwd     -- dZ, and per-split column sums of dZ (db, fixed order);
 //   * transposed neighbour lists, once per mesh: for vertex u and slot j, the
 //     vertices v whose slot j points at u, ascending.  The c-th of them is
@@ -1021,6 +1023,257 @@ hipError_t launch_dgrad_ws(const void* dZ, const void* W, const int32_t* table_t
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// the bf16 linear layer's backward in one pass over the rows
+// ---------------------------------------------------------------------------
+
+// C_in, C_out in {64, 128}.  Workgroup w takes rows [w L, w L + L), 32 rows
+// per step, with the loads of the next kLinRing - 1 steps in flight in
+// registers.  Per step:
+//   * dZ = dY (.) [Y > 0] of the step's rows, formed from the loaded dY and Y
+//     vectors (rows past n read as zeros), its column sums added per thread
+//     in fp32 (the bias gradient), and staged in LDS with the S rows;
+//   * dS rows = dZ W^T: A fragments are 16 contiguous bytes of a dZ row, the
+//     B fragments of W^T (W[c][o .. o + 7], 16 contiguous bytes) stay in
+//     registers for the whole launch; the rounded rows go out as whole
+//     16-byte vectors through an LDS tile;
+//   * the workgroup's partial dW += S^T dZ over the step's 32 rows, both
+//     operands read with transposing LDS reads (wgrad_tile's scheme).
+// At the end the partial tile (fp32, in wgrad_tile's chunk layout, chunk w)
+// and the column sums (colpart[w]) go to the workspace; wgrad_reduce_kernel
+// then sums them over the chunks in a fixed order.
+constexpr int kLinThreads = 512;
+constexpr int kLinRing = 3;
+template <int CI, int CO>
+__global__ __launch_bounds__(kLinThreads) void linear_bwd_fused_kernel(
+    const __bf16* __restrict__ S, const __bf16* __restrict__ W, const __bf16* __restrict__ Y,
+    const __bf16* __restrict__ dY, int64_t n, int32_t L, int act, int32_t T,
+    __bf16* __restrict__ dS, float* __restrict__ part, float* __restrict__ colpart) {
+  constexpr int R = 32;
+  constexpr int NCI = CI / 16, NCO = CO / 16, KSO = CO / 32;
+  constexpr int ROWI = CI * 2 + 16, ROWO = CO * 2 + 16;  // padded LDS rows
+  constexpr int VPI = CI / 8, VPO = CO / 8;              // 16-byte vectors per row
+  constexpr int NVI = (R * VPI + kLinThreads - 1) / kLinThreads;
+  constexpr int NVO = (R * VPO + kLinThreads - 1) / kLinThreads;
+  // dgrad: 2 row blocks x NCI column blocks, DCB column blocks per wavefront
+  constexpr int DCB = NCI / 4;
+  // wgrad: wavefront (wa, wb) of 2 x 4 takes NBA x NBB blocks of 16 x 16
+  constexpr int NBA = NCI / 2, NBB = NCO / 4;
+  static_assert((CI == 64 || CI == 128) && (CO == 64 || CO == 128), "C_in, C_out in {64, 128}");
+  static_assert(kLinThreads % VPI == 0 && kLinThreads % VPO == 0, "column of a thread");
+  __shared__ __attribute__((aligned(16))) unsigned char st_s[R * ROWI];
+  __shared__ __attribute__((aligned(16))) unsigned char st_z[R * ROWO];
+  __shared__ __attribute__((aligned(16))) unsigned char st_d[R * ROWI];
+  __shared__ float csum[kLinThreads * 8];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 4, l16 = lane & 15;
+  const int64_t row0 = (int64_t)blockIdx.x * L;
+  const int rows = (int)min((int64_t)L, n - row0);
+  const int steps = (rows + R - 1) / R;
+
+  // B fragments of W^T for this wavefront's dgrad blocks: row block rb,
+  // column blocks cb0 .. cb0 + DCB - 1
+  // (each output optional: W is read only for dS, S only for dW)
+  const bool do_ds = dS != nullptr, do_dw = part != nullptr;
+  const int rb = wave & 1, cb0 = (wave >> 1) * DCB;
+  bf16x8 wt[DCB][KSO];
+#pragma unroll
+  for (int x = 0; x < DCB; ++x)
+#pragma unroll
+    for (int ks = 0; ks < KSO; ++ks)
+      wt[x][ks] = do_ds ? *reinterpret_cast<const bf16x8*>(
+                              W + (int64_t)((cb0 + x) * 16 + l16) * CO + ks * 32 + 8 * g)
+                        : bf16x8{};
+
+  struct Regs {
+    i32x4 dy[NVO], y[NVO], s[NVI];
+  };
+  // the loads of step st (rows past n, or steps past the last, clamped to
+  // row 0 of the workgroup and zeroed when used)
+  auto load = [&](int st, Regs& r) {
+#pragma unroll
+    for (int u = 0; u < NVO; ++u) {
+      const int e = tid + u * kLinThreads;
+      const int rr = e / VPO, q = e % VPO;
+      const int64_t row = row0 + (int64_t)st * R + rr;
+      const int64_t idx = (row < n && e < R * VPO ? row : row0) * CO + q * 8;
+      r.dy[u] = *reinterpret_cast<const i32x4*>(dY + idx);
+      r.y[u] = *reinterpret_cast<const i32x4*>(Y + idx);  // Y = dY when there is no ReLU
+    }
+#pragma unroll
+    for (int u = 0; u < NVI; ++u) {
+      const int e = tid + u * kLinThreads;
+      const int rr = e / VPI, q = e % VPI;
+      const int64_t row = row0 + (int64_t)st * R + rr;
+      const int64_t idx = (row < n && e < R * VPI ? row : row0) * CI + q * 8;
+      r.s[u] = do_dw ? *reinterpret_cast<const i32x4*>(S + idx) : i32x4{0, 0, 0, 0};
+    }
+  };
+
+  // transposing read of 32 rows x 16 columns (block cb) of a staged tile
+  auto frag = [&](const unsigned char* base, int row_bytes, int cb) -> bf16x8 {
+    const unsigned char* p0 = base + (8 * g + (l16 >> 2)) * row_bytes + cb * 32 + 8 * (l16 & 3);
+    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0)));
+    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (SHC_LDS bf16x4*)(const_cast<unsigned char*>(p0 + 4 * row_bytes)));
+    return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  };
+
+  const int wa = wave >> 2, wb = wave & 3;
+  f32x4 wacc[NBA][NBB];
+#pragma unroll
+  for (int x = 0; x < NBA; ++x)
+#pragma unroll
+    for (int y = 0; y < NBB; ++y) wacc[x][y] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float cs[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) cs[k] = 0.f;
+
+  auto body = [&](int st, Regs& r) {
+    if (st >= steps) return;
+    const int64_t rbase = row0 + (int64_t)st * R;
+    // dZ and its column sums, staged with the S rows
+#pragma unroll
+    for (int u = 0; u < NVO; ++u) {
+      const int e = tid + u * kLinThreads;
+      const int rr = e / VPO, q = e % VPO;
+      const bool live = e < R * VPO && rbase + rr < n;
+      i32x4 z = r.dy[u];
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t gw = live ? (uint32_t)z[w] : 0u;
+        const uint32_t yv = (uint32_t)r.y[u][w];
+        const uint32_t lo = (!act || bf16_bits_to_f32(yv & 0xFFFFu) > 0.f) ? (gw & 0xFFFFu) : 0u;
+        const uint32_t hi = (!act || bf16_bits_to_f32(yv >> 16) > 0.f) ? (gw & 0xFFFF0000u) : 0u;
+        z[w] = (int)(lo | hi);
+        cs[2 * w] += bf16_bits_to_f32(lo);
+        cs[2 * w + 1] += bf16_bits_to_f32(hi >> 16);
+      }
+      if (e < R * VPO) *reinterpret_cast<i32x4*>(st_z + rr * ROWO + q * 16) = z;
+    }
+#pragma unroll
+    for (int u = 0; u < NVI; ++u) {
+      const int e = tid + u * kLinThreads;
+      const int rr = e / VPI, q = e % VPI;
+      const bool live = e < R * VPI && rbase + rr < n;
+      if (e < R * VPI)
+        *reinterpret_cast<i32x4*>(st_s + rr * ROWI + q * 16) = live ? r.s[u] : i32x4{0, 0, 0, 0};
+    }
+    __syncthreads();
+    // the registers are free: the loads of step st + kLinRing
+    load(st + kLinRing, r);
+    // dS rows of the step (zeros, never stored, without dS)
+    f32x4 dacc[DCB];
+#pragma unroll
+    for (int x = 0; x < DCB; ++x) dacc[x] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < KSO; ++ks) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(st_z + (16 * rb + l16) * ROWO +
+                                                        (32 * ks + 8 * g) * 2);
+#pragma unroll
+      for (int x = 0; x < DCB; ++x)
+        dacc[x] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, wt[x][ks], dacc[x], 0, 0, 0);
+    }
+    // partial dW over the step's rows (always run: S reads as zeros without
+    // dW, and no branch separates the dgrad MFMAs above from the reads of
+    // their results below)
+    {
+      bf16x8 fa[NBA], fb[NBB];
+#pragma unroll
+      for (int x = 0; x < NBA; ++x) fa[x] = frag(st_s, ROWI, wa * NBA + x);
+#pragma unroll
+      for (int y = 0; y < NBB; ++y) fb[y] = frag(st_z, ROWO, wb * NBB + y);
+#pragma unroll
+      for (int x = 0; x < NBA; ++x)
+#pragma unroll
+        for (int y = 0; y < NBB; ++y)
+          wacc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[x], fb[y], wacc[x][y], 0, 0, 0);
+    }
+    // dS tile: rows 16 rb + 4 g + i, columns 16 (cb0 + x) + l16, rounded to
+    // nearest even by the hardware conversion
+#pragma unroll
+    for (int x = 0; x < DCB; ++x) {
+      unsigned char* pp = st_d + (16 * rb + 4 * g) * ROWI + ((cb0 + x) * 16 + l16) * 2;
+#pragma unroll
+      for (int i = 0; i < 4; i += 2) {
+        const bf16x2 h = __builtin_convertvector(f32x2{dacc[x][i], dacc[x][i + 1]}, bf16x2);
+        *reinterpret_cast<__bf16*>(pp + i * ROWI) = h[0];
+        *reinterpret_cast<__bf16*>(pp + (i + 1) * ROWI) = h[1];
+      }
+    }
+    __syncthreads();
+    if (do_ds) {
+#pragma unroll
+      for (int u = 0; u < NVI; ++u) {
+        const int e = tid + u * kLinThreads;
+        const int rr = e / VPI, q = e % VPI;
+        if (e < R * VPI && rbase + rr < n)
+          *reinterpret_cast<i32x4*>(dS + (rbase + rr) * CI + q * 8) =
+              *reinterpret_cast<const i32x4*>(st_d + rr * ROWI + q * 16);
+      }
+    }
+  };
+
+  Regs r0, r1, r2;
+  static_assert(kLinRing == 3, "three register sets");
+  load(0, r0);
+  load(1, r1);
+  load(2, r2);
+  for (int st = 0; st < steps; st += kLinRing) {
+    body(st, r0);
+    body(st + 1, r1);
+    body(st + 2, r2);
+  }
+
+  // partial tile of chunk w (wgrad_tile's layout: tile (ta, tb) of T x T)
+  if (part != nullptr) {
+    const int tB = CO / T;
+    const int tiles = (CI / T) * tB;
+#pragma unroll
+    for (int x = 0; x < NBA; ++x)
+#pragma unroll
+      for (int y = 0; y < NBB; ++y)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int c = (wa * NBA + x) * 16 + 4 * g + i;
+          const int o = (wb * NBB + y) * 16 + l16;
+          const int ta = c / T, tb = o / T;
+          part[((int64_t)blockIdx.x * tiles + ta * tB + tb) * T * T + (c - ta * T) * T +
+               (o - tb * T)] = wacc[x][y][i];
+        }
+  }
+  // column sums: threads with the same 16-byte column vector, in thread order
+  if (colpart != nullptr) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) csum[tid * 8 + k] = cs[k];
+    __syncthreads();
+    for (int c = tid; c < CO; c += kLinThreads) {
+      const int q = c / 8, k = c % 8;
+      float t = 0.f;
+      for (int th = q; th < kLinThreads; th += VPO) t += csum[th * 8 + k];
+      colpart[(int64_t)blockIdx.x * CO + c] = t;
+    }
+  }
+}
+
+struct LinBwdArgs {
+  const __bf16 *S, *W, *Y, *dY;
+  int64_t n;
+  int32_t L;
+  int act;
+  int32_t T;
+  __bf16* dS;
+  float *part, *colpart;
+};
+
+template <int CI, int CO>
+void launch_linear_bwd_fused(const LinBwdArgs& a, unsigned grid, hipStream_t stream) {
+  hipLaunchKernelGGL((linear_bwd_fused_kernel<CI, CO>), dim3(grid), dim3(kLinThreads), 0, stream,
+                     a.S, a.W, a.Y, a.dY, a.n, a.L, a.act, a.T, a.dS, a.part, a.colpart);
+}
+
 template <int WS, bool BF16>
 hipError_t launch_dgrad_k(const void* dZ, const void* W, const int32_t* table_t,
                           const uint64_t* row_slots, const int32_t* slot_of, int64_t n,
@@ -1174,6 +1427,48 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
     if (db != nullptr)
       hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(kThreads), 0, stream,
                          reinterpret_cast<int32_t*>(db), (int64_t)Cout, 0);
+    return hipGetLastError();
+  }
+  // the bf16 linear layer of 64 or 128 channels: one pass over the rows,
+  // then the reduction of its per-workgroup partials
+  if (!conv && is_bf16 && (Cin == 64 || Cin == 128) && (Cout == 64 || Cout == 128)) {
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    // about one workgroup per CU, at least 256 rows each (the workspace holds
+    // partials for chunks of 256 rows)
+    int64_t L = (n + cus - 1) / cus;
+    L = std::max<int64_t>(256, (L + 31) / 32 * 32);
+    const int64_t G = (n + L - 1) / L;
+    float* part = dW != nullptr ? reinterpret_cast<float*>(w + pl.off_part) : nullptr;
+    float* colpart = db != nullptr ? reinterpret_cast<float*>(w + pl.off_colpart) : nullptr;
+    const LinBwdArgs la{static_cast<const __bf16*>(S), static_cast<const __bf16*>(W),
+                        static_cast<const __bf16*>(act ? Y : dY), static_cast<const __bf16*>(dY),
+                        n, (int32_t)L, act, pl.T, static_cast<__bf16*>(dS), part, colpart};
+    if (Cin == 128) {
+      if (Cout == 128) launch_linear_bwd_fused<128, 128>(la, (unsigned)G, stream);
+      else launch_linear_bwd_fused<128, 64>(la, (unsigned)G, stream);
+    } else {
+      if (Cout == 128) launch_linear_bwd_fused<64, 128>(la, (unsigned)G, stream);
+      else launch_linear_bwd_fused<64, 64>(la, (unsigned)G, stream);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (dW != nullptr) {
+      const dim3 rg((unsigned)(pl.tiles + (db != nullptr ? 1 : 0)), (unsigned)(pl.T * pl.T / 32));
+      if (pl.T == 128)
+        hipLaunchKernelGGL((wgrad_reduce_kernel<128, 32>), rg, dim3(32 * 32), 0, stream, part,
+                           nullptr, (int32_t)L, Cin, Cout, 1, (int32_t)G, dW, colpart, (int32_t)G,
+                           db);
+      else
+        hipLaunchKernelGGL((wgrad_reduce_kernel<64, 32>), rg, dim3(32 * 32), 0, stream, part,
+                           nullptr, (int32_t)L, Cin, Cout, 1, (int32_t)G, dW, colpart, (int32_t)G,
+                           db);
+    } else if (db != nullptr) {
+      hipLaunchKernelGGL(colsum_kernel, dim3((Cout + 7) / 8), dim3(kThreads), 0, stream, colpart,
+                         (int)G, Cout, db);
+    }
     return hipGetLastError();
   }
   // dZ (through the ReLU) and the bias gradient

@@ -211,7 +211,11 @@ def test_conv_backward_vs_oracle(dev, B, V, K, Cin, Cout, p, act, dtype):
 @pytest.mark.parametrize("n,Cin,Cout,act,dtype", [
     (1000, 128, 128, True, "bf16"), (37, 64, 32, False, "bf16"), (5000, 16, 256, True, "bf16"),
     (1, 128, 64, True, "bf16"), (1000, 128, 128, True, "f32"), (37, 64, 32, False, "f32"),
-    (3000, 48, 256, True, "f32")])
+    (3000, 48, 256, True, "f32"),
+    # the one-pass bf16 kernel (C_in, C_out in {64, 128}): several workgroups
+    # with a ragged last one, a single short one, no ReLU
+    (70001, 128, 128, True, "bf16"), (300, 64, 64, False, "bf16"), (2049, 64, 128, True, "bf16"),
+    (513, 128, 64, False, "bf16"), (31, 64, 64, True, "bf16")])
 def test_linear_backward_vs_oracle(dev, n, Cin, Cout, act, dtype):
     rng = np.random.default_rng(n + Cin + Cout)
     S = exact(rng.standard_normal((n, Cin)), dtype)
@@ -230,6 +234,40 @@ def test_linear_backward_vs_oracle(dev, n, Cin, Cout, act, dtype):
     assert_scaled_close(down(dS), rS, sS, dtype, "dS", n_terms=Cout)
     assert_scaled_close(down(dW), rW, sW, "f32", "dW")
     assert_scaled_close(down(db), rb, sb, "f32", "db")
+
+
+@pytest.mark.parametrize("Cin,Cout", [(128, 128), (64, 128)])
+def test_linear_backward_outputs_one_at_a_time(dev, Cin, Cout):
+    """Each output of the linear backward asked for alone equals the same
+    output of the call that asks for all three, bit for bit, and the outputs
+    not asked for stay untouched; two full calls agree bit for bit."""
+    rng = np.random.default_rng(Cin + 3 * Cout)
+    n = 9001
+    S = bf16(rng.standard_normal((n, Cin)))
+    W = bf16(rng.standard_normal((Cin, Cout)) / np.sqrt(Cin))
+    Y = bf16(np.maximum(rng.standard_normal((n, Cout)), 0.0))
+    dY = bf16(rng.standard_normal((n, Cout)))
+    args = [up(S, "bf16"), up(W, "bf16"), up(Y, "bf16"), up(dY, "bf16"), n]
+
+    def run(want):
+        dS = torch.full((n, Cin), float("nan"), dtype=torch.bfloat16, device="cuda")
+        dW = torch.full((Cin, Cout), float("nan"), dtype=torch.float32, device="cuda")
+        db = torch.full((Cout,), float("nan"), dtype=torch.float32, device="cuda")
+        shc.sparse_linear_backward(*args, dS if "dS" in want else None,
+                                   dW if "dW" in want else None, db if "db" in want else None)
+        torch.cuda.synchronize()
+        return down(dS), down(dW), down(db)
+
+    full = run(("dS", "dW", "db"))
+    again = run(("dS", "dW", "db"))
+    for x, y in zip(full, again):
+        assert np.array_equal(x, y)
+    for k, name in enumerate(("dS", "dW", "db")):
+        got = run((name,))
+        assert np.array_equal(got[k], full[k]), name
+        for m in range(3):
+            if m != k:
+                assert np.all(np.isnan(got[m])), (name, m)
 
 
 def test_conv_backward_self_slot_is_linear_and_repeats(dev):
@@ -253,8 +291,10 @@ def test_conv_backward_self_slot_is_linear_and_repeats(dev):
                                n, dS, dW, db)
     torch.cuda.synchronize()
     assert np.array_equal(down(dS), a[0])
+    # the linear layer's one-pass kernel sums dW and db over its own row
+    # chunks: the same values up to the order of the fp32 partial sums
     np.testing.assert_allclose(down(dW), a[1][0], rtol=0, atol=1e-6 * np.abs(a[1]).max())
-    assert np.array_equal(down(db), a[2])
+    np.testing.assert_allclose(down(db), a[2], rtol=0, atol=1e-6 * np.abs(a[2]).max())
     only = run_conv_backward(st, S, W, Y, dY, True, want=("db",))
     assert np.all(np.isnan(only[0])) and np.all(np.isnan(only[1]))
     assert np.array_equal(only[2], a[2])
