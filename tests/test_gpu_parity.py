@@ -1083,6 +1083,9 @@ def test_stream_events_order_streams(dev):
     (3, 1000, 9, 0.2, 0),         # cap = N' exactly
     (3, 1000, 9, 0.2, -5),        # cap below N': capacity error, table untouched
     (1, 5, 3, 0.6, None),         # tiny body, last bytes of the mask
+    (128, 10475, 9, 0.05, None),  # the density-sweep batch
+    (200, 655, 9, 0.1, None),     # 200 small bodies
+    (3000, 40, 9, 0.3, None),     # many tiny bodies
 ])
 def test_compact_table_start(dev, B, V, K, p, cap_delta):
     """shc_compact_mask_table_start: the lists of the compaction (Eq. 2), bit
@@ -1117,6 +1120,33 @@ def test_compact_table_start(dev, B, V, K, p, cap_delta):
     got_t = down(table)
     assert np.array_equal(got_t[:K * n].reshape(K, n), table_reference(m, nbr))
     assert np.all(got_t[K * n:] == -7)
+
+
+@pytest.mark.parametrize("B,V", [(128, 10475), (300, 655)])
+def test_compact_table_start_any_workspace(dev, B, V):
+    """The compaction with its table: exact whatever the workspace held
+    before (random bytes, then the counts of earlier calls on other masks),
+    over calls in a row."""
+    K = 9
+    rng = np.random.default_rng(B + V)
+    nbr = rand_nbr(V, K, rng)
+    masks = [(rng.random((B, V)) < p).astype(np.uint8) for p in (0.05, 0.3, 0.0, 0.05)]
+    c = Compaction(masks[0])
+    table = torch.full((K * B * V,), -7, dtype=torch.int32, device=dev)
+    c.ws.copy_(torch.from_numpy(rng.integers(0, 256, c.ws.numel(), dtype=np.uint8)).to(dev))
+    pc = shc.PreparedCompact(c.mask, B, V, c.coords, c.inv, c.row_ptr, c.n_dev, c.ws,
+                             nbr=up(nbr), table=table)
+    for m in masks:
+        c.mask.copy_(up(m.reshape(-1)))
+        ref_c, ref_inv, ref_rp, ref_n = O.compact(m)
+        pc.start()
+        n = pc.wait()
+        torch.cuda.synchronize()
+        assert n == ref_n
+        assert np.array_equal(down(c.coords)[:n], ref_c)
+        assert np.array_equal(down(c.inv), ref_inv)
+        assert np.array_equal(down(c.row_ptr), ref_rp)
+        assert np.array_equal(down(table)[:K * n].reshape(K, n), table_reference(m, nbr))
 
 
 @pytest.mark.parametrize("steps", [1, 4])
