@@ -631,9 +631,24 @@ __global__ __launch_bounds__(32 * G) void wgrad_reduce_kernel(
     slot_chunks(row_ptr, j, L, &c0, &cnt);
     c1 = c0 + cnt;
   }
+  // NU chunks' loads in flight at once (clamped addresses, past-the-end
+  // values dropped), then added in chunk order; NU covers about a thread's
+  // share (the linear layer's one slot has all the chunks)
+  constexpr int NU = G >= 32 ? 8 : 4;
   double s = 0.0;
-#pragma unroll 4
-  for (int q = c0 + y; q < c1; q += G) s += (double)part[((int64_t)q * tiles + t) * T * T + e];
+  const int64_t stride = (int64_t)tiles * T * T;
+  const float* pe = part + (int64_t)t * T * T + e;
+  for (int q0 = c0 + y; q0 < c1; q0 += NU * G) {
+    float v[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int q = q0 + u * G;
+      v[u] = pe[(int64_t)(q < c1 ? q : q0) * stride];
+    }
+#pragma unroll
+    for (int u = 0; u < NU; ++u)
+      if (q0 + u * G < c1) s += (double)v[u];
+  }
   red[y][ex] = s;
   __syncthreads();
   if (y == 0) {
