@@ -359,6 +359,8 @@ def main():
     log("cold and warm launches measured")
     out["conv_plan"] = conv_plan_measure(st, shc, torch, args.reps)
     log("conv plan measured")
+    out["measured_peaks"] = measured_peaks(torch)
+    log("measured peaks done")
     if not args.no_sweep:
         out["density_sweep"] = density_sweep(w, shc, synth, torch, args.reps)
         log("density sweep measured")
@@ -378,6 +380,28 @@ def main():
         out["cpu_baseline"] = cpu_baseline(w, spec, args.cpu_seconds)
         log("cpu baseline done")
     print(json.dumps(out))
+
+
+def measured_peaks(torch, reps=20):
+    """What this GPU reaches on plain work, beside the published peaks: a
+    device-to-device copy of 1 GiB (PyTorch's copy kernel; read + write bytes
+    over its time) and an 8192^3 bf16 GEMM (PyTorch's matmul, hipBLASLt)."""
+    n = 1 << 29                                   # 1 GiB of bf16
+    x = torch.empty(n, dtype=torch.bfloat16, device="cuda:0").normal_()
+    y = torch.empty_like(x)
+    t_copy = _time_us(lambda: y.copy_(x), torch, reps)
+    copy_gbs = 2 * n * 2 / (t_copy * 1e-6) / 1e9
+    del x, y
+    m = 8192
+    a = torch.randn((m, m), device="cuda:0").to(torch.bfloat16)
+    b = torch.randn((m, m), device="cuda:0").to(torch.bfloat16)
+    t_mm = _time_us(lambda: torch.mm(a, b), torch, reps)
+    tflops = 2.0 * m ** 3 / (t_mm * 1e-6) / 1e12
+    del a, b
+    torch.cuda.empty_cache()
+    return {"copy_1GiB_GBs": round(copy_gbs, 1), "copy_frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4),
+            "gemm_bf16_8192_TFLOPs": round(tflops, 1),
+            "gemm_frac_of_peak": round(tflops / BF16_MFMA_PEAK_TFLOPS, 4)}
 
 
 def conv_plan_measure(st, shc, torch, reps):
