@@ -243,3 +243,32 @@ def test_stack_with_plans_matches_without(dev, side):
     assert outs[False][0] == outs[True][0]
     for a, b in zip(outs[False][1:], outs[True][1:]):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("side", [False, True])
+def test_encoder_stack_mixed_plans(dev, side):
+    """The 4-layer encoder (conv 16 -> 64 -> 64 -> 128 -> 128 on 64 small
+    bodies, max-pool): with plans forced on, the layers whose shape takes one
+    read it and the first (C_in = 16) runs from the table; every output
+    identical to the stack without plans, over three batches."""
+    from paper_2608_09388_amd.pipeline import SparseStack
+    w = synth.workload_c2()
+    outs = {}
+    for use in (False, True):
+        st = SparseStack(w, device=dev, side_stream=side, conv_plans=use)
+        if use:
+            assert (9, 16, 64) not in st.plan_shapes
+            assert {(9, 64, 64), (9, 64, 128), (9, 128, 128)} <= set(st.plan_shapes)
+        masks = [np.random.default_rng(70 + k).random(w.B * w.V) < 0.06 + 0.04 * k
+                 for k in range(3)]
+
+        def feed(k):
+            st.mask.copy_(torch.from_numpy(masks[k].astype(np.uint8)).to(dev))
+
+        n = st.run(3, feed=feed)
+        torch.cuda.synchronize()
+        outs[use] = (n, [a[:n].clone() for a in st.acts[1:]], st.pooled.clone())
+    assert outs[False][0] == outs[True][0]
+    for a, b in zip(outs[False][1], outs[True][1]):
+        assert torch.equal(a, b)
+    assert torch.equal(outs[False][2], outs[True][2])
