@@ -359,6 +359,8 @@ def main():
     log("cold and warm launches measured")
     out["conv_plan"] = conv_plan_measure(st, shc, torch, args.reps)
     log("conv plan measured")
+    out["incremental_scatter"] = incremental_scatter_measure(w, shc, synth, torch, args.reps)
+    log("incremental scatter measured")
     out["measured_peaks"] = measured_peaks(torch)
     log("measured peaks done")
     if not args.no_sweep:
@@ -441,6 +443,90 @@ def conv_plan_measure(st, shc, torch, reps):
             "plan_build_us": round(t_build, 2), "planned_conv_us": round(t_pl, 2),
             "three_layers_table_us": round(t_tab3, 2),
             "three_layers_build_and_planned_us": round(t_pl3, 2)}
+
+
+def incremental_scatter_measure(w, shc, synth, torch, reps, steps=300, warmup=30):
+    """The zero-fill scatter against shc_scatter_update on consecutive batches
+    whose masks differ: two independent Bernoulli(p) masks of the density-
+    sweep workload, alternated.  The update kernel alone (back to back,
+    A -> B then B -> A, each checked equal to the zero-fill scatter of its
+    set), and the whole step with either scatter when the masks alternate
+    (the mask of each batch copied into place on the device first, in both
+    runs).  Algorithmic bytes of an update: the current rows read and written
+    (2 C e + 8 each), the previous coordinates and their inv entries read
+    (12 each) and the previous rows inactive now written (C e each)."""
+    from paper_2608_09388_amd.pipeline import SparseStack
+    dev = torch.device("cuda:0")
+    B, V, C = w.B, w.V, 128
+    e = 2
+    m_host = [w.mask.reshape(-1), synth.bernoulli_mask(B, V, float(w.mask.mean()),
+                                                       synth._rng(11, 2)).reshape(-1)]
+    md = [torch.from_numpy(np.ascontiguousarray(m.astype(np.uint8))).to(dev) for m in m_host]
+    sets = []
+    for m in md:
+        coords = torch.empty((B * V, 2), dtype=torch.int32, device=dev)
+        inv = torch.empty(B * V, dtype=torch.int32, device=dev)
+        rp = torch.empty(B + 1, dtype=torch.int32, device=dev)
+        nd = torch.empty(4, dtype=torch.int32, device=dev)
+        ws = torch.empty(max(shc.compact_mask_workspace(B, V), 16), dtype=torch.uint8, device=dev)
+        n = shc.compact_mask(m, B, V, coords, inv, rp, nd, ws)
+        S = torch.randn((max(n, 1), C), device=dev).to(torch.bfloat16)
+        sets.append((n, coords, inv, S))
+    (na, ca, ia, Sa), (nb, cb, ib, Sb) = sets
+    D = torch.zeros((B * V, C), dtype=torch.bfloat16, device=dev)
+    ref = [torch.empty_like(D), torch.empty_like(D)]
+    zf = shc.prepare_scatter(Sa, ia, ca, B, V, ref[0])
+    shc.scatter(Sb, ib, cb, nb, B, V, ref[1], zero_fill=True)
+    to_b = shc.prepare_scatter_update(Sb, ib, cb, ca, B, V, D)
+    to_a = shc.prepare_scatter_update(Sa, ia, ca, cb, B, V, D)
+    zf(na)
+    shc.scatter(Sa, ia, ca, na, B, V, D, zero_fill=True)
+    to_b(nb, na)
+    torch.cuda.synchronize()
+    same = bool(torch.equal(D, ref[1]))
+    to_a(na, nb)
+    torch.cuda.synchronize()
+    same = same and bool(torch.equal(D, ref[0]))
+    t_zf = _time_us(lambda: zf(na), torch, reps)
+    t_pair = _time_us(lambda: (to_b(nb, na), to_a(na, nb)), torch, reps)
+    torch.cuda.synchronize()
+    same = same and bool(torch.equal(D, ref[0]))
+    both = set(map(tuple, ca[:na].cpu().numpy().tolist())) & set(
+        map(tuple, cb[:nb].cpu().numpy().tolist()))
+    kept = len(both)
+    upd_bytes = ((na + nb) * (2 * C * e + 8) + (na + nb) * 12
+                 + (na - kept + nb - kept) * C * e) / 2
+    zf_bytes = na * C * e + B * V * (4 + C * e)
+    t_upd = t_pair / 2
+    res = {"config": f"two Bernoulli masks of the density-sweep batch alternated "
+                     f"(N'={na} and {nb}, {kept} rows in both), C={C} bf16",
+           "update_equals_zero_fill": same,
+           "zero_fill_scatter_us": round(t_zf, 2),
+           "zero_fill_frac_hbm": round(zf_bytes / (t_zf * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+           "update_us": round(t_upd, 2),
+           "update_algorithmic_bytes": int(upd_bytes),
+           "update_frac_hbm": round(upd_bytes / (t_upd * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    del to_a, to_b, zf, D, ref, sets
+    # the whole step, masks alternating, with each scatter
+    for inc in (False, True):
+        st = SparseStack(w, device="cuda:0", side_stream=True, incremental_scatter=inc)
+
+        def feed(k, st=st):
+            st.mask.copy_(md[k % 2])
+
+        st.run(warmup, feed=feed)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        n_last = st.run(steps, feed=feed)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        key = "step_ms_update" if inc else "step_ms_zero_fill"
+        res[key] = round(ms, 4)
+        res[key.replace("step_ms", "rows_per_s_per_layer")] = round(
+            (na + nb) / 2 * len(w.layers) / (ms / 1e3), 1)
+        del st
+    res["steps"] = steps
+    return res
 
 
 def group_norm_measure(st, shc, torch, reps, G=32):

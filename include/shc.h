@@ -19,8 +19,9 @@
  * - All array arguments are DEVICE pointers (memory on the current HIP device)
  *   unless the comment says "host".  The caller owns every buffer; the library
  *   keeps no pointer after the work it enqueues has run, allocates nothing and
- *   holds no state between calls (the one exception: the stream-ordering
- *   events of shc_event_create, which the caller creates and destroys).
+ *   holds no state between calls (the exceptions: the stream-ordering events
+ *   of shc_event_create and the stack executors of shc_stack_create, which
+ *   the caller creates and destroys).
  * - Every call validates its arguments on the host, then enqueues its kernels
  *   on `stream` and returns without waiting (the one exception is the optional
  *   host count of shc_compact_mask).  Calls are thread-safe.
@@ -377,6 +378,27 @@ int shc_scatter(const void* S, const int32_t* inv, const int32_t* coords, int64_
                 hipStream_t stream);
 
 /*
+ * The zero-filled scatter (D = y (.) m, Sec. 3.2) as an update of a dense
+ * output that holds the previous batch's: when D holds the zero_fill = 1
+ * result of shc_scatter for a previous active set whose coordinates are
+ * prev_coords [prev_rows][2], this call leaves D holding the zero_fill = 1
+ * result for this set (S, inv, coords, n_rows):
+ *
+ *   D[b * V + v] = 0   for every (b, v) of prev_coords with inv[b * V + v] < 0,
+ *   D[b_i * V + v_i] = S[i]   for every i < n_rows,
+ *
+ * every other row untouched.  It touches only the rows of the two active
+ * sets (about 2 N' rows instead of B * V).  A dense output kept resident from
+ * batch to batch starts as all zeros with prev_rows = 0.  prev_coords must
+ * not be this call's coords buffer (SHC_ERR_INVALID_ARG); the caller keeps a
+ * copy of the coordinates for the next call.  Coordinates out of range are
+ * skipped.  Other arguments as for shc_scatter; an exact copy.
+ */
+int shc_scatter_update(const void* S, const int32_t* inv, const int32_t* coords, int64_t n_rows,
+                       const int32_t* prev_coords, int64_t prev_rows, int32_t B, int32_t V,
+                       int32_t C, int32_t dtype, void* D, hipStream_t stream);
+
+/*
  * The zeros of the zero-filled scatter (D = y (.) m, Sec. 3.2), which need
  * only the inverse map:
  *
@@ -602,6 +624,133 @@ int shc_event_record(void* event, hipStream_t stream);
 int shc_stream_wait_event(hipStream_t stream, void* event);
 int shc_event_synchronize(void* event);
 int shc_event_destroy(void* event);
+
+/* ------------------------------------------------------------------------ */
+/* Stack executor: the whole path over consecutive batches from native code  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * A stack is the path of Sec. 3.2 applied to one batch after another: the
+ * mask of a batch is compacted once (Eq. 2, with the neighbour-row table of
+ * the active set when a conv layer reads it), and because the active set is
+ * the same for every layer (C'_k = C_k), its N' rows run through every layer
+ * (Eq. 6 linear or Eqs. 4-5 conv, each with the activation of Eq. 10)
+ * before the last layer's rows are scattered back to the dense layout (the
+ * zero-filled y (.) m, by shc_scatter or by shc_scatter_update from the
+ * previous batch's output) and/or max-pooled per body.  shc_stack_run issues
+ * exactly the calls of this header that a caller would issue for the same
+ * work, in the same order per stream, from a native loop: results are
+ * bit-identical to those calls'.
+ *
+ * The caller owns every buffer (device memory unless marked host) and
+ * describes them once in an shc_stack_desc; shc_stack_create copies the
+ * description, checks it and creates the executor's stream-ordering events
+ * (device-scope, like shc_event_create's) on the current device.  Buffers
+ * must stay allocated until shc_stack_destroy.
+ *
+ * Streams: with side and tail both NULL the stack is serial: everything
+ * runs on the stream given to shc_stack_run, the compaction of batch k + 1
+ * enqueued before the scatter and pool of batch k (so the host learns N'
+ * while the stream still has work).  With both set (default-priority
+ * streams of the same device, distinct from each other and from the run's
+ * stream) it is pipelined: the side stream runs batch k + 1's compaction,
+ * table and conv plans beside batch k's layers, and the tail stream runs
+ * batch k's scatter and pool beside batch k + 1's layers; the last layer's
+ * output then alternates between acts[n_layers] and last_alt (the last
+ * batch of a run writes acts[n_layers]), and the index sets rotate over
+ * three (the host waits for a set's previous scatter and pool to finish
+ * before compacting into it).  At the end of a run the run's stream waits
+ * for the other two, so work enqueued on it afterwards sees every output.
+ */
+#define SHC_STACK_MAX_LAYERS 16
+#define SHC_LAYER_LINEAR 0 /* Eq. 6 */
+#define SHC_LAYER_CONV 1   /* Eqs. 4-5 */
+
+typedef struct shc_stack_layer {
+  int32_t kind;      /* SHC_LAYER_LINEAR or SHC_LAYER_CONV */
+  int32_t Cin, Cout; /* channels (Cin of layer l = Cout of layer l - 1) */
+  int32_t act;       /* SHC_ACT_* */
+  const void* W;     /* [Cin][Cout] (linear) or [K][Cin][Cout] (conv), dtype */
+  const float* bias; /* [Cout] fp32, or NULL */
+  int64_t plan_rows; /* conv: read plan[l] of the index set when 0 < N' <= plan_rows
+                        (at most shc_conv_plan_max_rows of the shape); 0: never */
+} shc_stack_layer;
+
+typedef struct shc_stack_index_set {
+  int32_t* coords;      /* [B*V][2] */
+  int32_t* inv;         /* [B*V] */
+  int32_t* row_ptr;     /* [B+1] */
+  int32_t* n_active;    /* [1] device copy of N' */
+  int64_t* host_count;  /* host: page-locked and mapped (receives N') */
+  void* ws;             /* compaction workspace (shc_compact_mask_workspace) */
+  size_t ws_bytes;
+  int32_t* table;       /* [K][B*V] neighbour-row table, or NULL without conv layers */
+  void* plan[SHC_STACK_MAX_LAYERS]; /* per conv layer with plan_rows > 0: its plan buffer
+                                       (layers of one shape may share one; it is built
+                                       once per batch), else NULL */
+  size_t plan_bytes[SHC_STACK_MAX_LAYERS];
+} shc_stack_index_set;
+
+typedef struct shc_stack_desc {
+  int32_t B, V, K;         /* bodies, vertices per body, neighbour slots (0: no conv) */
+  int32_t dtype;           /* SHC_F32 or SHC_BF16, every feature buffer and weight */
+  int32_t C0;              /* input channels = layers[0].Cin */
+  const uint8_t* mask;     /* [B*V], read by each batch's compaction */
+  const void* x;           /* [B*V][C0] dense input features */
+  const int32_t* nbr;      /* [V][K] neighbour lists (conv layers), else NULL */
+  int32_t table_in_compaction; /* 1: the compaction writes the table
+                                  (shc_compact_mask_table_start), else a
+                                  shc_build_neighbor_table call after it */
+  int32_t n_layers;        /* 1 .. SHC_STACK_MAX_LAYERS */
+  shc_stack_layer layers[SHC_STACK_MAX_LAYERS];
+  void* acts[SHC_STACK_MAX_LAYERS + 1]; /* acts[0]: gathered input rows [B*V][C0]
+                                           (unused, may be NULL, when layer 0 is linear:
+                                           the gather is fused into it); acts[l + 1]:
+                                           layer l's output rows [B*V][Cout] */
+  void* last_alt;          /* pipelined: second buffer of the last layer's output */
+  void* dense_out;         /* [B*V][C_last] scatter output, or NULL for none */
+  int32_t incremental;     /* 1: shc_scatter_update from the previous batch's output
+                              (dense_out then holds the last scattered batch's y (.) m
+                              between runs and is written by nothing else) */
+  int32_t* prev_coords;    /* incremental: [B*V][2], the last scattered batch's coords */
+  void* pooled;            /* [B][C_last] per-body max-pool output, or NULL for none */
+  float pool_empty;        /* pooled value of a body without active rows */
+  int32_t n_sets;          /* index sets: 2 (serial) or 3 (pipelined) */
+  shc_stack_index_set sets[3];
+  hipStream_t side, tail;  /* both NULL (serial) or both set (pipelined) */
+} shc_stack_desc;
+
+/* Batch-input callback of shc_stack_run: called just before the compaction
+ * of batch `batch` (0-based within the run) is enqueued; it may write that
+ * batch's mask and x with work on `stream` (in a pipelined run the side
+ * stream, ordered after the gather of batch - 1; the run's stream
+ * otherwise).  A nonzero return ends the run with SHC_ERR_INVALID_ARG. */
+typedef int (*shc_stack_feed_fn)(void* user, int64_t batch, hipStream_t stream);
+
+/*
+ * shc_stack_create  -- *stack receives a new executor for `desc` (copied).
+ *   SHC_ERR_INVALID_ARG / _MISALIGNED / _UNSUPPORTED for a description the
+ *   calls above would refuse (checked here so that a run does not stop
+ *   half-way), SHC_ERR_HIP if an event cannot be created.
+ * shc_stack_run     -- `steps` batches on `stream` (and the side and tail
+ *   streams).  *cur_set (in/out) is the index set the first batch compacts
+ *   into and, on return, the set of the last batch; *prev_rows (in/out,
+ *   incremental scatter) the row count of the batch dense_out holds (0 for a
+ *   dense_out of zeros).  *n_last receives the last batch's N'.
+ *   time_events (may be NULL): 2 * steps caller-owned events, a pair per
+ *   batch, recorded on `stream` just before and just after layer time_layer
+ *   of that batch (NULL entries: none for that batch).  Returns the first
+ *   failing call's status; work enqueued before it stays enqueued (the caller
+ *   synchronises the streams before reusing the buffers).  Only one run at a
+ *   time per executor.
+ * shc_stack_destroy -- releases the executor (NULL is ignored); runs that
+ *   used it must have finished.
+ */
+int shc_stack_create(const shc_stack_desc* desc, void** stack);
+int shc_stack_run(void* stack, int64_t steps, hipStream_t stream, shc_stack_feed_fn feed,
+                  void* user, int32_t time_layer, void* const* time_events, int32_t* cur_set,
+                  int64_t* prev_rows, int64_t* n_last);
+int shc_stack_destroy(void* stack);
 
 #ifdef __cplusplus
 }

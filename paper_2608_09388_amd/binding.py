@@ -40,6 +40,35 @@ _lib = None
 
 _c_i32, _c_i64, _c_ptr, _c_sz, _c_f = (ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p,
                                         ctypes.c_size_t, ctypes.c_float)
+
+# stack executor (shc_stack_*): mirrors of the C structs, same field order
+STACK_MAX_LAYERS = 16
+SHC_LAYER_LINEAR, SHC_LAYER_CONV = 0, 1
+
+
+class StackLayer(ctypes.Structure):
+    _fields_ = [("kind", _c_i32), ("Cin", _c_i32), ("Cout", _c_i32), ("act", _c_i32),
+                ("W", _c_ptr), ("bias", _c_ptr), ("plan_rows", _c_i64)]
+
+
+class StackIndexSet(ctypes.Structure):
+    _fields_ = [("coords", _c_ptr), ("inv", _c_ptr), ("row_ptr", _c_ptr), ("n_active", _c_ptr),
+                ("host_count", _c_ptr), ("ws", _c_ptr), ("ws_bytes", _c_sz), ("table", _c_ptr),
+                ("plan", _c_ptr * STACK_MAX_LAYERS), ("plan_bytes", _c_sz * STACK_MAX_LAYERS)]
+
+
+class StackDesc(ctypes.Structure):
+    _fields_ = [("B", _c_i32), ("V", _c_i32), ("K", _c_i32), ("dtype", _c_i32), ("C0", _c_i32),
+                ("mask", _c_ptr), ("x", _c_ptr), ("nbr", _c_ptr),
+                ("table_in_compaction", _c_i32), ("n_layers", _c_i32),
+                ("layers", StackLayer * STACK_MAX_LAYERS),
+                ("acts", _c_ptr * (STACK_MAX_LAYERS + 1)), ("last_alt", _c_ptr),
+                ("dense_out", _c_ptr), ("incremental", _c_i32), ("prev_coords", _c_ptr),
+                ("pooled", _c_ptr), ("pool_empty", _c_f), ("n_sets", _c_i32),
+                ("sets", StackIndexSet * 3), ("side", _c_ptr), ("tail", _c_ptr)]
+
+
+STACK_FEED_FN = ctypes.CFUNCTYPE(ctypes.c_int, _c_ptr, _c_i64, _c_ptr)
 _SIGS = {
     "shc_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "shc_last_error": (ctypes.c_char_p, []),
@@ -54,6 +83,8 @@ _SIGS = {
     "shc_compact_mask_table_start": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_ptr, _c_ptr,
                                                     _c_ptr, _c_ptr, _c_ptr, _c_i64, _c_ptr,
                                                     _c_i32, _c_ptr, _c_ptr, _c_sz, _c_ptr]),
+    "shc_scatter_update": (ctypes.c_int, [_c_ptr, _c_ptr, _c_ptr, _c_i64, _c_ptr, _c_i64, _c_i32,
+                                          _c_i32, _c_i32, _c_i32, _c_ptr, _c_ptr]),
     "shc_clear_inactive_rows": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_i32, _c_i32, _c_ptr,
                                                _c_ptr]),
     "shc_gather_rows": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
@@ -119,6 +150,11 @@ _SIGS = {
     "shc_stream_wait_event": (ctypes.c_int, [_c_ptr, _c_ptr]),
     "shc_event_synchronize": (ctypes.c_int, [_c_ptr]),
     "shc_event_destroy": (ctypes.c_int, [_c_ptr]),
+    "shc_stack_create": (ctypes.c_int, [ctypes.POINTER(StackDesc), ctypes.POINTER(_c_ptr)]),
+    "shc_stack_run": (ctypes.c_int, [_c_ptr, _c_i64, _c_ptr, STACK_FEED_FN, _c_ptr, _c_i32,
+                                     _c_ptr, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i64),
+                                     ctypes.POINTER(_c_i64)]),
+    "shc_stack_destroy": (ctypes.c_int, [_c_ptr]),
 }
 
 
@@ -408,6 +444,31 @@ def scatter(S: torch.Tensor, inv: torch.Tensor, coords: torch.Tensor, n_rows: in
     _check(load().shc_scatter(*args), "shc_scatter")
 
 
+def scatter_update(S: torch.Tensor, inv: torch.Tensor, coords: torch.Tensor, n_rows: int,
+                   prev_coords: torch.Tensor, prev_rows: int, B: int, V: int, D: torch.Tensor,
+                   stream=None):
+    """shc_scatter_update: D held the zero-fill scatter of prev_coords[:prev_rows];
+    afterwards it holds this set's."""
+    C = D.shape[-1]
+    args = [_dev(S, "S", D.dtype, n_rows * C) if n_rows else None,
+            _dev(inv, "inv", torch.int32, B * V),
+            _dev(coords, "coords", torch.int32, 2 * n_rows) if n_rows else None, n_rows,
+            _dev(prev_coords, "prev_coords", torch.int32, 2 * prev_rows) if prev_rows else None,
+            prev_rows, B, V, C, _dtype_code(D), _dev(D, "D", D.dtype, B * V * C), _stream(stream)]
+    _check(load().shc_scatter_update(*args), "shc_scatter_update")
+
+
+def prepare_scatter_update(S, inv, coords, prev_coords, B, V, D, stream=None) -> "Prepared":
+    """shc_scatter_update with (n_rows, prev_rows) given per call."""
+    C = D.shape[-1]
+    args = [_dev(S, "S", D.dtype), _dev(inv, "inv", torch.int32, B * V),
+            _dev(coords, "coords", torch.int32), 0, _dev(prev_coords, "prev_coords", torch.int32),
+            0, B, V, C, _dtype_code(D), _dev(D, "D", D.dtype, B * V * C), _stream(stream)]
+    return PreparedScatterUpdate(args, (S, inv, coords, prev_coords, D),
+                                 min(S.numel() // C, coords.numel() // 2),
+                                 prev_coords.numel() // 2)
+
+
 def compact_mask_start(mask: torch.Tensor, B: int, V: int, coords: torch.Tensor,
                        inv: torch.Tensor, row_ptr: torch.Tensor, n_active: torch.Tensor,
                        ws: torch.Tensor, host_count: torch.Tensor, stream=None):
@@ -488,6 +549,59 @@ def segment_maxpool(S: torch.Tensor, row_ptr: torch.Tensor, n_rows: int, B: int,
             _dev(row_ptr, "row_ptr", torch.int32, B + 1), n_rows, B, C, dt, float(empty_value),
             _dev(P, "P", P.dtype, B * C), _stream(stream)]
     _check(load().shc_segment_maxpool(*args), "shc_segment_maxpool")
+
+
+class StackExecutor:
+    """shc_stack_create / shc_stack_run / shc_stack_destroy.  ``desc`` is a
+    filled StackDesc; ``keep`` holds the tensors it points into (alive as
+    long as the executor)."""
+
+    def __init__(self, desc: StackDesc, keep=()):
+        lib = load()
+        h = _c_ptr()
+        self._desc, self._keep = desc, keep
+        _check(lib.shc_stack_create(ctypes.byref(desc), ctypes.byref(h)), "shc_stack_create")
+        self._h = h
+        self._destroy = lib.shc_stack_destroy
+
+    def run(self, steps: int, stream=None, feed=None, time_layer: int = 0, time_events=None,
+            cur_set: int = 0, prev_rows: int = 0):
+        """shc_stack_run; returns (n_last, cur_set, prev_rows).  ``feed(k,
+        stream_handle)`` is called for every batch; an exception it raises
+        ends the run and is raised here.  ``time_events``: 2 * steps HIP event
+        handles (int, 0 for none) or None."""
+        err = []
+
+        def _feed(user, k, st):
+            try:
+                feed(int(k), st or 0)
+                return 0
+            except BaseException as e:  # noqa: BLE001 -- re-raised below
+                err.append(e)
+                return 1
+
+        cb = STACK_FEED_FN(_feed) if feed is not None else ctypes.cast(None, STACK_FEED_FN)
+        ev = None
+        if time_events is not None:
+            if len(time_events) != 2 * steps:
+                raise ValueError(f"time_events holds {len(time_events)} handles, "
+                                 f"not 2 * steps = {2 * steps}")
+            ev = (_c_ptr * (2 * steps))(*[int(e) if e else None for e in time_events])
+        cur = _c_i32(cur_set)
+        prev = _c_i64(prev_rows)
+        n = _c_i64(0)
+        rc = load().shc_stack_run(self._h, steps, _stream(stream), cb, None, time_layer, ev,
+                                  ctypes.byref(cur), ctypes.byref(prev), ctypes.byref(n))
+        if err:
+            raise err[0]
+        _check(rc, "shc_stack_run")
+        return int(n.value), int(cur.value), int(prev.value)
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            self._destroy(h)
+            self._h = None
 
 
 class StreamEvent:
@@ -652,6 +766,27 @@ class Prepared:
         rc = self._fn(*self._args)
         if rc != 0:
             _check(rc, self._where)
+        return rc
+
+
+class PreparedScatterUpdate:
+    """shc_scatter_update marshalled once; call with (n_rows, prev_rows)."""
+
+    def __init__(self, args, keep, n_max: int, prev_max: int):
+        self._fn = load().shc_scatter_update
+        self._args = list(args)
+        self._keep = keep
+        self.n_max, self.prev_max = int(n_max), int(prev_max)
+
+    def __call__(self, n_rows: int, prev_rows: int) -> int:
+        if not (0 <= n_rows <= self.n_max and 0 <= prev_rows <= self.prev_max):
+            raise ValueError(f"shc_scatter_update: n_rows = {n_rows}, prev_rows = {prev_rows} "
+                             f"outside [0, {self.n_max}] x [0, {self.prev_max}]")
+        self._args[3] = n_rows
+        self._args[5] = prev_rows
+        rc = self._fn(*self._args)
+        if rc != 0:
+            _check(rc, "shc_scatter_update")
         return rc
 
 

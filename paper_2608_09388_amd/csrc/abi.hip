@@ -81,6 +81,18 @@ int check_rows(int64_t n_rows) {
 
 }  // namespace
 
+namespace shc {
+// The thread's last-error message, for entry points defined in other files.
+int set_error(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return code;
+}
+void clear_error() { g_last_error[0] = 0; }
+}  // namespace shc
+
 extern "C" {
 
 const char* shc_status_string(int status) {
@@ -706,6 +718,31 @@ int shc_scatter(const void* S, const int32_t* inv, const int32_t* coords, int64_
   return hip_status(
       shc::launch_scatter(S, inv, coords, n_rows, B, V, row_bytes, zero_fill, D, stream),
       "scatter launch");
+}
+
+int shc_scatter_update(const void* S, const int32_t* inv, const int32_t* coords, int64_t n_rows,
+                       const int32_t* prev_coords, int64_t prev_rows, int32_t B, int32_t V,
+                       int32_t C, int32_t dtype, void* D, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_bv(B, V));
+  SHC_TRY(check_rows(n_rows));
+  SHC_TRY(check_rows(prev_rows));
+  SHC_TRY(check_dtype(dtype));
+  SHC_TRY(check_channels("C", C));
+  if (n_rows + prev_rows == 0) return SHC_OK;
+  SHC_PTR(D, "D");
+  SHC_PTR(inv, "inv");
+  if (n_rows > 0) {
+    SHC_PTR(S, "S");
+    SHC_PTR(coords, "coords");
+  }
+  if (prev_rows > 0) SHC_PTR(prev_coords, "prev_coords");
+  if (prev_coords != nullptr && prev_coords == coords)
+    return fail(SHC_ERR_INVALID_ARG, "prev_coords and coords are the same buffer");
+  const int32_t row_bytes = C * (dtype == SHC_BF16 ? 2 : 4);
+  return hip_status(shc::launch_scatter_update(S, inv, coords, n_rows, prev_coords, prev_rows, B,
+                                               V, row_bytes, D, stream),
+                    "scatter_update launch");
 }
 
 int shc_clear_inactive_rows(const int32_t* inv, int32_t B, int32_t V, int32_t C, int32_t dtype,

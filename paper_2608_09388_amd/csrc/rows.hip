@@ -178,6 +178,31 @@ __global__ __launch_bounds__(kThreads) void scatter_fill_kernel(const i32x4* __r
   }
 }
 
+// D holding the zero-fill scatter of the previous active set (prev) updated
+// to this set's: threads t < prev_rows zero the rows of the previous set that
+// are inactive now, the others write this set's rows.  The two parts touch
+// different rows (a row is zeroed only when inactive now), so one launch
+// does both in any order.
+__global__ __launch_bounds__(kThreads) void scatter_update_kernel(
+    const i32x4* __restrict__ S, const int32_t* __restrict__ inv, const int2* __restrict__ coords,
+    int64_t n_rows, const int2* __restrict__ prev, int64_t prev_rows, int32_t B, int32_t V,
+    int vpr, i32x4* __restrict__ D) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.y + threadIdx.y;
+  if (t >= prev_rows + n_rows) return;
+  const bool clear = t < prev_rows;
+  const int64_t i = t - prev_rows;  // this set's row (when !clear)
+  const int2 c = clear ? prev[t] : coords[i];
+  if (!(c.x >= 0 && c.x < B && c.y >= 0 && c.y < V)) return;
+  const int64_t r = (int64_t)c.x * V + c.y;
+  if (clear && inv[r] >= 0) return;
+  i32x4* dst = D + r * vpr;
+  for (int q = threadIdx.x; q < vpr; q += blockDim.x) {
+    i32x4 val = {0, 0, 0, 0};
+    if (!clear) val = S[i * vpr + q];
+    __builtin_nontemporal_store(val, dst + q);
+  }
+}
+
 // D[b_i * V + v_i] = S[i] for every active row i; other rows untouched.
 __global__ __launch_bounds__(kThreads) void scatter_active_kernel(const i32x4* __restrict__ S,
                                                                   const int2* __restrict__ coords,
@@ -376,6 +401,21 @@ hipError_t launch_scatter(const void* S, const int32_t* inv, const int32_t* coor
                        reinterpret_cast<const int2*>(coords), n_rows, B, V, s.vpr,
                        static_cast<i32x4*>(D));
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_update(const void* S, const int32_t* inv, const int32_t* coords,
+                                 int64_t n_rows, const int32_t* prev_coords, int64_t prev_rows,
+                                 int32_t B, int32_t V, int32_t row_bytes, void* D,
+                                 hipStream_t stream) {
+  const RowShape s = row_shape(row_bytes);
+  const int64_t rows = prev_rows + n_rows;
+  if (rows == 0) return hipSuccess;
+  const int64_t blocks = (rows + s.ty - 1) / s.ty;
+  hipLaunchKernelGGL(scatter_update_kernel, dim3((unsigned)blocks), dim3(s.tx, s.ty), 0, stream,
+                     static_cast<const i32x4*>(S), inv, reinterpret_cast<const int2*>(coords),
+                     n_rows, reinterpret_cast<const int2*>(prev_coords), prev_rows, B, V, s.vpr,
+                     static_cast<i32x4*>(D));
   return hipGetLastError();
 }
 

@@ -39,6 +39,11 @@ __device__ __forceinline__ T ceil_div(T a, T b) {
 // launchers (host side, enqueue only; arguments already validated)
 // ---------------------------------------------------------------------------
 
+// the calling thread's last-error message (shc_last_error), for entry points
+// defined outside the file that owns it; set_error returns `code`
+int set_error(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+
 // compaction: number of blocks and per-block element span for a mask of `total` entries
 void compact_plan(int64_t total, int32_t* nblocks, int64_t* per_block);
 
@@ -102,6 +107,10 @@ hipError_t launch_layer_backward(int conv, const void* S, const int32_t* table,
                                  hipStream_t stream);
 hipError_t launch_clear_inactive(const int32_t* inv, int32_t B, int32_t V, int32_t row_bytes,
                                  void* D, hipStream_t stream);
+hipError_t launch_scatter_update(const void* S, const int32_t* inv, const int32_t* coords,
+                                 int64_t n_rows, const int32_t* prev_coords, int64_t prev_rows,
+                                 int32_t B, int32_t V, int32_t row_bytes, void* D,
+                                 hipStream_t stream);
 hipError_t launch_gather_ext(const void* x, const uint8_t* me, int mask_mode,
                              const int32_t* coords, int64_t n_rows, int32_t B, int32_t Bx,
                              int32_t V, int32_t row_bytes, void* S, hipStream_t stream);

@@ -29,7 +29,15 @@ next active count while the GPU still has batch k's tail to run, and the
 stream never idles on that wait.  With a side stream the compaction runs on
 it, and the scatter and pool of batch k run on a third stream beside batch
 k + 1's layers (the last layer's output alternates between two buffers).
-Every batch still runs the whole path.
+Every batch still runs the whole path.  ``run`` issues these calls from the
+library's own loop (shc_stack_run, one call for all the batches) unless the
+stack is made with executor="python", which issues the same calls one by one
+from this module.
+
+With ``incremental_scatter`` the dense output is kept from batch to batch and
+each scatter is shc_scatter_update: the rows of the previous batch that are
+inactive now are zeroed and this batch's rows written, instead of all B*V
+rows; the result is the zero-fill scatter's, bit for bit.
 
 This module only moves buffers and issues calls; all arithmetic runs in the
 library's kernels.
@@ -107,8 +115,7 @@ class _IndexSet:
             self.plans[key] = (buf, n_lim, build, build_side)
         self.layers = [self._layer_call(st, l, st.acts[l + 1]) for l in range(len(st.w.layers))]
         last = st.acts[-1]
-        self.scatter = (shc.prepare_scatter(last, self.inv, self.coords, B, V, st.dense_out)
-                        if st.dense_out is not None else None)
+        self.scatter = self._scatter_call(st, last, None)
         self.pool = (shc.prepare_segment_maxpool(last, self.row_ptr, B, st.pooled, 0.0)
                      if st.pooled is not None else None)
         # run() with a side stream: the last layer writes one of two buffers
@@ -118,12 +125,24 @@ class _IndexSet:
         if st.tail is not None and st.w.layers:
             L = (st.acts[-1], st.last_alt)
             self.last_into = [self._layer_call(st, len(st.w.layers) - 1, L[i]) for i in range(2)]
-            self.scatter_tail = [shc.prepare_scatter(L[i], self.inv, self.coords, B, V,
-                                                     st.dense_out, stream=st.tail)
-                                 if st.dense_out is not None else None for i in range(2)]
+            self.scatter_tail = [self._scatter_call(st, L[i], st.tail) for i in range(2)]
             self.pool_tail = [shc.prepare_segment_maxpool(L[i], self.row_ptr, B, st.pooled, 0.0,
                                                           stream=st.tail)
                               if st.pooled is not None else None for i in range(2)]
+
+    def _scatter_call(self, st: "SparseStack", src: torch.Tensor, stream):
+        """The scatter of src into the dense output (on `stream`, None: the
+        stack's own): a zero-fill scatter, or with incremental_scatter an
+        update of the previous batch's output."""
+        if st.dense_out is None:
+            return None
+        B, V = st.B, st.V
+        if not st.incremental_scatter:
+            return shc.prepare_scatter(src, self.inv, self.coords, B, V, st.dense_out,
+                                       stream=stream)
+        upd = shc.prepare_scatter_update(src, self.inv, self.coords, st.prev_coords, B, V,
+                                         st.dense_out, stream=stream)
+        return _IncrementalScatter(st, upd, self.coords, stream)
 
     def build_plans(self, n: int, side: bool = False):
         """The conv plans of this set's n rows (on the side stream: side)."""
@@ -151,6 +170,23 @@ class _IndexSet:
         return shc.prepare_sparse_linear(src, st.weights[l], st.biases[l], dst, a)
 
 
+class _IncrementalScatter:
+    """shc_scatter_update from the previous scattered batch's coordinates
+    (kept in the stack's prev_coords), then this batch's coordinates copied
+    there, both on the scatter's stream."""
+
+    def __init__(self, st: "SparseStack", upd, coords: torch.Tensor, stream):
+        self.st, self.upd, self.coords = st, upd, coords
+        self.stream = stream if stream is not None else st.main
+
+    def __call__(self, n: int):
+        st = self.st
+        self.upd(n, st.prev_n)
+        with torch.cuda.stream(self.stream):
+            st.prev_coords[:n].copy_(self.coords[:n])
+        st.prev_n = n
+
+
 class _PlannedConv:
     """A conv layer that reads its set's plan when the batch's row count has
     one (the plan was built for it), else the table."""
@@ -164,7 +200,10 @@ class _PlannedConv:
 
 class SparseStack:
     def __init__(self, w: Workload, device: str = "cuda", act: int = shc.SHC_ACT_RELU,
-                 side_stream: bool = False, conv_plans: Optional[bool] = None):
+                 side_stream: bool = False, conv_plans: Optional[bool] = None,
+                 incremental_scatter: bool = False, executor: str = "native"):
+        if executor not in ("native", "python"):
+            raise ValueError(f"executor = {executor!r}: 'native' or 'python'")
         self.w = w
         self.device = torch.device(device)
         # every prepared call below launches on the stream current now; step()
@@ -181,7 +220,7 @@ class SparseStack:
         if side_stream:
             with torch.cuda.device(self.device):
                 ev = shc.StreamEvent
-                self._events = dict(set_free=[ev() for _ in range(3)], ready=ev(), fed=ev(),
+                self._events = dict(set_free=[ev() for _ in range(3)], ready=ev(), x_read=ev(),
                                     last_done=[ev() for _ in range(2)],
                                     tail_done=[ev() for _ in range(2)], tail_end=ev())
         self.dtype = TORCH_DTYPE[w.dtype]
@@ -201,7 +240,17 @@ class SparseStack:
         # second buffer of the last layer's output (run() with side_stream)
         self.last_alt = torch.empty_like(self.acts[-1]) if side_stream else None
         Cl = chans[-1]
-        self.dense_out = torch.empty((BV, Cl), dtype=self.dtype, device=dev) if w.scatter else None
+        # With incremental_scatter the dense output stays resident from batch
+        # to batch: it starts as zeros and each scatter only zeroes the rows
+        # the previous batch wrote that are inactive now and writes this
+        # batch's rows (shc_scatter_update); it then must not be written by
+        # anything else.  Otherwise every scatter writes all B*V rows.
+        self.incremental_scatter = bool(incremental_scatter and w.scatter)
+        self.dense_out = ((torch.zeros if self.incremental_scatter else torch.empty)(
+            (BV, Cl), dtype=self.dtype, device=dev) if w.scatter else None)
+        self.prev_coords = (torch.empty((BV, 2), dtype=torch.int32, device=dev)
+                            if self.incremental_scatter else None)
+        self.prev_n = 0
         self.pooled = torch.empty((self.B, Cl), dtype=self.dtype, device=dev) if w.pool else None
         # A first linear layer reads its rows straight from x (gather fused in);
         # otherwise the active rows are gathered into acts[0] first.
@@ -228,6 +277,61 @@ class SparseStack:
         # index set's reuse from the host; see _run_pipelined)
         self._sets = [_IndexSet(self) for _ in range(3 if side_stream else 2)]
         self._cur = 0
+        # run() issues its calls from the library's native loop
+        # (shc_stack_run) unless executor = "python" (the same calls, issued
+        # from this module); a stack without layers always takes the latter
+        self.executor = executor if w.layers else "python"
+        self._native = self._make_native() if self.executor == "native" else None
+
+    def _make_native(self) -> shc.StackExecutor:
+        """The shc_stack_desc of this stack's buffers, and its executor."""
+        w = self.w
+        d = shc.StackDesc()
+        has_conv = any(l.kind == "conv" for l in w.layers)
+        d.B, d.V, d.K = self.B, self.V, self.K if has_conv else 0
+        d.dtype = shc.SHC_BF16 if w.dtype == "bf16" else shc.SHC_F32
+        d.C0 = w.C0
+        d.mask, d.x = self.mask.data_ptr(), self.x.data_ptr()
+        d.nbr = self.nbr.data_ptr() if has_conv else None
+        d.table_in_compaction = int(self._sets[0].fused)
+        d.n_layers = len(w.layers)
+        BV = self.B * self.V
+        for l, spec in enumerate(w.layers):
+            L = d.layers[l]
+            W = self.weights[l]
+            L.kind = shc.SHC_LAYER_CONV if spec.kind == "conv" else shc.SHC_LAYER_LINEAR
+            L.Cin, L.Cout = W.shape[-2], W.shape[-1]
+            L.act = self.act if spec.relu else shc.SHC_ACT_NONE
+            L.W = W.data_ptr()
+            L.bias = self.biases[l].data_ptr() if self.biases[l] is not None else None
+            n_lim = self.plan_shapes.get(tuple(W.shape), 0) if spec.kind == "conv" else 0
+            L.plan_rows = min(BV, n_lim)
+        for i, a in enumerate(self.acts):
+            d.acts[i] = a.data_ptr()
+        d.last_alt = self.last_alt.data_ptr() if self.last_alt is not None else None
+        d.dense_out = self.dense_out.data_ptr() if self.dense_out is not None else None
+        d.incremental = int(self.incremental_scatter)
+        d.prev_coords = self.prev_coords.data_ptr() if self.prev_coords is not None else None
+        d.pooled = self.pooled.data_ptr() if self.pooled is not None else None
+        d.pool_empty = 0.0
+        d.n_sets = len(self._sets)
+        keep = []
+        for i, s in enumerate(self._sets):
+            S = d.sets[i]
+            host = torch.zeros(1, dtype=torch.int64, pin_memory=True)
+            keep.append(host)
+            S.coords, S.inv = s.coords.data_ptr(), s.inv.data_ptr()
+            S.row_ptr, S.n_active = s.row_ptr.data_ptr(), s.n_active.data_ptr()
+            S.host_count = host.data_ptr()
+            S.ws, S.ws_bytes = s.ws.data_ptr(), s.ws.numel()
+            S.table = s.table.data_ptr() if s.table is not None else None
+            for l, spec in enumerate(w.layers):
+                plan = s.plans.get(tuple(self.weights[l].shape)) if spec.kind == "conv" else None
+                if plan is not None:
+                    S.plan[l], S.plan_bytes[l] = plan[0].data_ptr(), plan[0].numel()
+        d.side = self.side.cuda_stream if self.side is not None else None
+        d.tail = self.tail.cuda_stream if self.tail is not None else None
+        return shc.StackExecutor(d, keep)
 
     # -- the index set of the current mask -------------------------------------
     @property
@@ -344,8 +448,9 @@ class SparseStack:
 
         ``feed(k)``, if given, is called just before batch k's compaction is
         enqueued and may write batch k's mask and features into ``mask`` and
-        ``x`` with work on the current stream (without it every batch reuses
-        them).  ``around_layer = (l, [(ev_a, ev_b), ...])`` records one pair of
+        ``x`` with work on the stream current when it is called (the side
+        stream in a pipelined run, after the gather of batch k - 1; without
+        it every batch reuses them).  ``around_layer = (l, [(ev_a, ev_b), ...])`` records one pair of
         events around layer l of every batch (a pair of None: none for that
         batch).  The outputs left behind are the
         last batch's.  Returns its N'."""
@@ -354,11 +459,42 @@ class SparseStack:
         cur = self._enter()
         try:
             with torch.cuda.stream(self.main):
+                if self._native is not None:
+                    return self._run_native(steps, around_layer, feed)
                 if self.side is not None and self.w.layers:
                     return self._run_pipelined(steps, around_layer, feed)
                 return self._run_serial(steps, around_layer, feed)
         finally:
             self._leave(cur)
+
+    def _run_native(self, steps: int, around_layer, feed) -> int:
+        """run() through shc_stack_run: the schedule of _run_serial or
+        _run_pipelined, issued from the library."""
+        tl, ev = 0, None
+        if around_layer is not None:
+            tl, pairs = around_layer
+            ev = []
+            for pair in pairs[:steps]:
+                if pair[0] is None:
+                    ev += [0, 0]
+                    continue
+                for e in pair:
+                    if not e.cuda_event:    # torch creates the HIP event at its first record
+                        e.record(self.main)
+                ev += [pair[0].cuda_event, pair[1].cuda_event]
+        fd = None
+        if feed is not None:
+            side_h = self.side.cuda_stream if self.side is not None else None
+
+            def fd(k: int, h: int):
+                with torch.cuda.stream(self.side if side_h is not None and h == side_h
+                                       else self.main):
+                    feed(k)
+        n, cur, prev = self._native.run(steps, self.main, fd, tl, ev, self._cur, self.prev_n)
+        self._cur = cur
+        self._set.n = n
+        self.prev_n = prev
+        return n
 
     def _run_serial(self, steps: int, around_layer, feed) -> int:
         """run() on the stack's own stream alone."""
@@ -405,7 +541,10 @@ class SparseStack:
         the current stream on the side stream's table before a batch's layers
         and on the tail stream before it overwrites a buffer the tail still
         reads; the tail stream on the current stream's last layer of its
-        batch; the side stream on ``feed``'s writes.  At the end the current
+        batch; the side stream on the gather of the batch before (the read
+        of ``x``) ahead of ``feed``, which runs with the side stream current
+        so that the next batch's inputs are written and compacted beside the
+        current batch's later layers.  At the end the current
         stream waits for the tail stream, so work the caller enqueues after
         run() sees the last batch's scatter and pool.  The events carry no
         system-scope fence (shc_event_create): a default event's cache
@@ -438,6 +577,8 @@ class SparseStack:
                 s.build_plans(s.n)
             if not self.fused_gather:
                 s.gather(s.n)
+                if feed is not None:
+                    ev["x_read"].record(main)
             for l in range(nl):
                 call = s.layers[l]
                 if l == nl - 1:
@@ -449,6 +590,8 @@ class SparseStack:
                 call(s.n)
                 if around is not None and around[0] == l:
                     around[2].record()
+                if l == 0 and self.fused_gather and feed is not None:
+                    ev["x_read"].record(main)
             ev["last_done"][i].record(main)
             buf_used[i] = True
             # compaction of batch k + 1 (side stream)
@@ -456,9 +599,12 @@ class SparseStack:
             nxt = self._sets[nxt_i] if k + 1 < steps else None
             if nxt is not None:
                 if feed is not None:
-                    feed(k + 1)
-                    ev["fed"].record(main)
-                    ev["fed"].wait(side)
+                    # batch k + 1's inputs may be written once batch k's
+                    # gather has read x (its compaction read the mask
+                    # earlier on the side stream)
+                    ev["x_read"].wait(side)
+                    with torch.cuda.stream(side):
+                        feed(k + 1)
                 if set_used[nxt_i]:
                     ev["set_free"][nxt_i].synchronize()
                 nxt.compact_side.start()

@@ -1,6 +1,7 @@
 /*
  * Host-side fuzz of the C ABI, built with AddressSanitizer and
- * UndefinedBehaviorSanitizer around the library's host code (abi.hip).
+ * UndefinedBehaviorSanitizer around the library's host code (abi.hip and
+ * the stack executor, stack.hip).
  *
  * Every entry point is called many times with arguments drawn from small
  * sets of edge values: NULL, aligned and misaligned stand-in device
@@ -66,6 +67,135 @@ static void check(int rc, const char* fn) {
   }
 }
 
+/* A stack description: with probability 1/2 a coherent one (two bf16 conv
+ * layers on a 4 x 655 batch, pipelined) with one to three fields then
+ * replaced by edge values, else every field an edge value. */
+static const int32_t kLayers[] = {-1, 0, 1, 2, 3, 16, 17};
+static const int32_t kSets[] = {-1, 0, 1, 2, 3, 4};
+static int64_t g_counts[3];
+
+static void random_layer(shc_stack_layer* L) {
+  L->kind = CODE();
+  L->Cin = I32();
+  L->Cout = I32();
+  L->act = CODE();
+  L->W = P();
+  L->bias = P();
+  L->plan_rows = I64();
+}
+
+static void random_set(shc_stack_index_set* x, int s) {
+  x->coords = P();
+  x->inv = P();
+  x->row_ptr = P();
+  x->n_active = P();
+  x->host_count = (next_u64() & 1) ? &g_counts[s] : NULL;
+  x->ws = P();
+  x->ws_bytes = SZ();
+  x->table = P();
+  for (int l = 0; l < SHC_STACK_MAX_LAYERS; ++l) {
+    x->plan[l] = P();
+    x->plan_bytes[l] = SZ();
+  }
+}
+
+static void stack_desc(shc_stack_desc* d) {
+  memset(d, 0, sizeof *d);
+  if (next_u64() & 1) {
+    d->B = I32();
+    d->V = I32();
+    d->K = I32();
+    d->dtype = CODE();
+    d->C0 = I32();
+    d->mask = P();
+    d->x = P();
+    d->nbr = P();
+    d->table_in_compaction = CODE();
+    d->n_layers = PICK(kLayers);
+    for (int l = 0; l < SHC_STACK_MAX_LAYERS; ++l) random_layer(&d->layers[l]);
+    for (int l = 0; l <= SHC_STACK_MAX_LAYERS; ++l) d->acts[l] = P();
+    d->last_alt = P();
+    d->dense_out = P();
+    d->incremental = CODE();
+    d->prev_coords = P();
+    d->pooled = P();
+    d->pool_empty = PICK(kF);
+    d->n_sets = PICK(kSets);
+    for (int s = 0; s < 3; ++s) random_set(&d->sets[s], s);
+    d->side = (hipStream_t)P();
+    d->tail = (hipStream_t)P();
+    return;
+  }
+  /* coherent base; buffers at distinct aligned stand-in addresses */
+  uintptr_t a = 0x100000;
+#define NEXT() ((void*)(a += 0x1000))
+  d->B = 4;
+  d->V = 655;
+  d->K = 9;
+  d->dtype = SHC_BF16;
+  d->C0 = 64;
+  d->mask = NEXT();
+  d->x = NEXT();
+  d->nbr = NEXT();
+  d->table_in_compaction = 1;
+  d->n_layers = 2;
+  for (int l = 0; l < 2; ++l) {
+    shc_stack_layer* L = &d->layers[l];
+    L->kind = SHC_LAYER_CONV;
+    L->Cin = 64;
+    L->Cout = 64;
+    L->act = SHC_ACT_RELU;
+    L->W = NEXT();
+    L->bias = NULL;
+    L->plan_rows = 1000;
+  }
+  for (int l = 0; l <= 2; ++l) d->acts[l] = NEXT();
+  d->last_alt = NEXT();
+  d->dense_out = NEXT();
+  d->incremental = 1;
+  d->prev_coords = NEXT();
+  d->pooled = NEXT();
+  d->n_sets = 3;
+  for (int s = 0; s < 3; ++s) {
+    shc_stack_index_set* x = &d->sets[s];
+    x->coords = NEXT();
+    x->inv = NEXT();
+    x->row_ptr = NEXT();
+    x->n_active = NEXT();
+    x->host_count = &g_counts[s];
+    x->ws = NEXT();
+    x->ws_bytes = (size_t)1 << 20;
+    x->table = NEXT();
+    x->plan[0] = x->plan[1] = NEXT();
+    x->plan_bytes[0] = x->plan_bytes[1] = (size_t)1 << 30;
+  }
+  d->side = (hipStream_t)NEXT();
+  d->tail = (hipStream_t)NEXT();
+#undef NEXT
+  const int changes = 1 + (int)(next_u64() % 3);
+  for (int c = 0; c < changes; ++c) {
+    const int s = (int)(next_u64() % 3), l = (int)(next_u64() % 2);
+    switch (next_u64() % 16) {
+      case 0: d->B = I32(); break;
+      case 1: d->V = I32(); break;
+      case 2: d->K = I32(); break;
+      case 3: d->dtype = CODE(); break;
+      case 4: d->C0 = I32(); break;
+      case 5: d->n_layers = PICK(kLayers); break;
+      case 6: random_layer(&d->layers[l]); break;
+      case 7: d->acts[next_u64() % 3] = P(); break;
+      case 8: d->incremental = CODE(); d->prev_coords = P(); break;
+      case 9: d->n_sets = PICK(kSets); break;
+      case 10: random_set(&d->sets[s], s); break;
+      case 11: d->sets[s].plan[l] = P(); d->sets[s].plan_bytes[l] = SZ(); break;
+      case 12: d->side = (hipStream_t)P(); break;
+      case 13: d->tail = d->side; break;
+      case 14: d->table_in_compaction = CODE(); d->nbr = P(); break;
+      default: d->sets[s].coords = d->sets[(s + 1) % 3].coords; break;
+    }
+  }
+}
+
 int main(void) {
   int ndev = 0;
   if (hipGetDeviceCount(&ndev) == hipSuccess && ndev > 0) {
@@ -128,6 +258,9 @@ int main(void) {
           "sparse_neighbor_conv_planned");
     check(shc_scatter(P(), P(), P(), I64(), I32(), I32(), I32(), CODE(), CODE(), P(), NULL),
           "scatter");
+    check(shc_scatter_update(P(), P(), P(), I64(), P(), I64(), I32(), I32(), I32(), CODE(), P(),
+                             NULL),
+          "scatter_update");
     check(shc_clear_inactive_rows(P(), I32(), I32(), I32(), CODE(), P(), NULL),
           "clear_inactive_rows");
     check(shc_segment_group_norm(P(), P(), I64(), I32(), I32(), I32(), PICK(kF), CODE(), P(), NULL),
@@ -155,6 +288,22 @@ int main(void) {
     check(shc_stream_wait_event(NULL, NULL), "stream_wait_event");
     check(shc_event_synchronize(NULL), "event_synchronize");
     check(shc_event_destroy(NULL), "event_destroy");
+    shc_stack_desc desc;
+    stack_desc(&desc);
+    void* stk = NULL;
+    check(shc_stack_create((next_u64() & 7) ? &desc : NULL, (next_u64() & 7) ? &stk : NULL),
+          "stack_create");
+    if (stk != NULL) {
+      fprintf(stderr, "stack_create succeeded without a GPU\n");
+      g_bad = 1;
+      shc_stack_destroy(stk);
+    }
+    int32_t cur = (int32_t)(next_u64() % 5) - 1;
+    int64_t prev = I64(), nl = 0;
+    check(shc_stack_run(NULL, I64(), NULL, NULL, NULL, I32(), NULL, (next_u64() & 1) ? &cur : NULL,
+                        &prev, &nl),
+          "stack_run");
+    check(shc_stack_destroy(NULL), "stack_destroy");
   }
   printf("calls %ld ok %ld bad %d\n", g_calls, g_ok, g_bad);
   return g_bad;

@@ -6,6 +6,7 @@ launch), so no device is touched.  Fake "device pointers" are plain integers
 with the alignment each case needs; validation never dereferences them.
 """
 import ctypes
+import os
 import subprocess
 
 import pytest
@@ -280,6 +281,24 @@ def test_gather_scatter_pool_validation(lib):
     assert s(A, None, A, 10, 4, 655, 16, 0, 1, A, None) == -1       # zero-fill needs inv
     assert s(A, A, None, 10, 4, 655, 16, 0, 0, A, None) == -1       # active-only needs coords
     assert s(A, A, A, 10, 4, 655, 16, 0, 1, MIS, None) == -3
+    u = lib.shc_scatter_update
+    A2 = 0x20000         # a second aligned fake address (prev_coords != coords)
+    assert u(A, A, A, -1, A2, 0, 4, 655, 16, 0, A, None) == -1
+    assert u(A, A, A, 0, A2, -1, 4, 655, 16, 0, A, None) == -1
+    assert u(A, A, A, 10, A2, 0, 4, 655, 16, 7, A, None) == -4
+    assert u(A, A, A, 10, A2, 0, 4, 655, 24, 0, A, None) == -4
+    assert u(A, A, A, 10, A2, 0, 0, 655, 16, 0, A, None) == -1
+    assert u(None, None, None, 0, None, 0, 4, 655, 16, 0, None, None) == 0   # nothing to do
+    assert u(A, A, A, 10, A2, 0, 4, 655, 16, 0, None, None) == -1 and "D" in err(lib)
+    assert u(A, None, A, 10, A2, 0, 4, 655, 16, 0, A, None) == -1 and "inv" in err(lib)
+    assert u(None, A, A, 10, A2, 0, 4, 655, 16, 0, A, None) == -1 and "S" in err(lib)
+    assert u(A, A, None, 10, A2, 0, 4, 655, 16, 0, A, None) == -1 and "coords" in err(lib)
+    assert u(None, A, None, 0, None, 10, 4, 655, 16, 0, A, None) == -1
+    assert "prev_coords" in err(lib)
+    assert u(A, A, A, 10, A, 10, 4, 655, 16, 0, A, None) == -1 and "same" in err(lib)
+    assert u(A, A, A, 10, A2, 0, 4, 655, 16, 0, MIS, None) == -3
+    assert u(A, A, A, 10, MIS, 10, 4, 655, 16, 0, A, None) == -3
+    assert u(A, A, A, 1 << 31, A2, 0, 4, 655, 16, 0, A, None) == -1
     p = lib.shc_segment_maxpool
     assert p(A, A, 10, 0, 16, 0, 0.0, A, None) == -1
     assert p(A, None, 10, 4, 16, 0, 0.0, A, None) == -1
@@ -454,3 +473,128 @@ def test_compact_table_start_validation(lib):
     assert call(ws_bytes=ws - 1) == -2
     # pageable host memory cannot receive the kernel's count
     assert call() == -1 and "page-locked" in err(lib)
+
+
+def _c_layout(tmp_path, struct, fields):
+    """offsetof of each field and sizeof of `struct`, from the C compiler."""
+    src = tmp_path / f"{struct}.c"
+    lines = ["#include <stddef.h>", "#include <stdio.h>", '#include "shc.h"', "int main(void) {",
+             f'  printf("%zu\\n", sizeof({struct}));']
+    lines += [f'  printf("%zu\\n", offsetof({struct}, {f}));' for f in fields]
+    lines += ["  return 0;", "}"]
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / f"{struct}_layout"
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    subprocess.run(["gcc", "-D__HIP_PLATFORM_AMD__", "-I", os.path.dirname(shc.HEADER), "-I",
+                    os.path.join(rocm, "include"), str(src), "-o", str(exe)], check=True,
+                   capture_output=True)
+    vals = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                           check=True).stdout.split()]
+    return vals[0], vals[1:]
+
+
+@pytest.mark.parametrize("py,c", [(shc.StackLayer, "shc_stack_layer"),
+                                  (shc.StackIndexSet, "shc_stack_index_set"),
+                                  (shc.StackDesc, "shc_stack_desc")])
+def test_stack_struct_layout_matches_header(tmp_path, py, c):
+    """The binding's ctypes mirrors of the stack structs have the header's
+    size and field offsets."""
+    names = [f[0] for f in py._fields_]
+    size, offs = _c_layout(tmp_path, c, names)
+    assert ctypes.sizeof(py) == size
+    for name, off in zip(names, offs):
+        assert getattr(py, name).offset == off, name
+
+
+def test_stack_validation(lib):
+    """shc_stack_create refuses a description the path's calls would refuse,
+    before any HIP call; shc_stack_run and _destroy take NULL safely.  (Without
+    a device no shape takes a conv plan, so the plan buffers' checks are in
+    the GPU tests.)"""
+    B, V, K = 4, 655, 9
+    ws = lib.shc_compact_mask_workspace(B, V)
+
+    def desc(**kw):
+        d = shc.StackDesc()
+        d.B, d.V, d.K, d.dtype, d.C0 = B, V, K, shc.SHC_BF16, 64
+        d.mask, d.x, d.nbr = A, A + 0x100, A + 0x200
+        d.table_in_compaction = 1
+        d.n_layers = 2
+        for l in range(2):
+            L = d.layers[l]
+            L.kind, L.Cin, L.Cout, L.act = shc.SHC_LAYER_CONV, 64, 64, shc.SHC_ACT_RELU
+            L.W, L.bias, L.plan_rows = A + 0x300 + 0x100 * l, None, 0
+        for i in range(3):
+            d.acts[i] = A + 0x1000 * (i + 1)
+        d.last_alt, d.dense_out, d.pooled = A + 0x5000, A + 0x6000, A + 0x7000
+        d.incremental, d.prev_coords = 1, A + 0x8000
+        d.n_sets = 3
+        for s in range(3):
+            S = d.sets[s]
+            base = A + 0x100000 * (s + 1)
+            S.coords, S.inv, S.row_ptr, S.n_active = base, base + 0x100, base + 0x200, base + 0x300
+            S.host_count, S.ws, S.ws_bytes, S.table = base + 0x400, base + 0x500, ws, base + 0x600
+        d.side, d.tail = 0x1111, 0x2222
+        for k, v in kw.items():
+            obj, _, name = k.rpartition("__")
+            tgt = d
+            for part in filter(None, obj.split("__")):
+                tgt = getattr(tgt, part[:-1])[int(part[-1])] if part[-1].isdigit() else \
+                    getattr(tgt, part)
+            setattr(tgt, name, v)
+        return d
+
+    def create(d):
+        h = ctypes.c_void_p()
+        rc = lib.shc_stack_create(ctypes.byref(d), ctypes.byref(h))
+        assert not h.value
+        return rc
+
+    assert lib.shc_stack_create(None, ctypes.byref(ctypes.c_void_p())) == -1
+    assert lib.shc_stack_create(ctypes.byref(desc()), None) == -1
+    assert create(desc(B=0)) == -1
+    assert create(desc(dtype=5)) == -4
+    assert create(desc(n_layers=0)) == -1
+    assert create(desc(n_layers=17)) == -1
+    assert create(desc(mask=MIS)) == -3
+    assert create(desc(C0=48)) == -1 and "Cin = 64" in err(lib)
+    assert create(desc(layers0__Cout=40)) == -4
+    assert create(desc(layers1__act=7)) == -4
+    assert create(desc(layers0__kind=3)) == -4
+    assert create(desc(layers0__plan_rows=1 << 40)) == -4 and "plan_rows" in err(lib)
+    assert create(desc(layers1__W=None)) == -1
+    assert create(desc(K=0)) == -1
+    assert create(desc(K=33)) == -4
+    assert create(desc(nbr=None)) == -1
+    d = desc()
+    d.acts[0] = None                  # layer 0 is a conv: the gathered rows are needed
+    assert create(d) == -1 and "acts[0]" in err(lib)
+    d = desc()
+    d.acts[2] = MIS
+    assert create(d) == -3
+    assert create(desc(last_alt=None)) == -1 and "last_alt" in err(lib)
+    assert create(desc(tail=0)) == -1 and "both" in err(lib)
+    assert create(desc(tail=0x1111)) == -1 and "different" in err(lib)
+    assert create(desc(n_sets=2)) == -1
+    assert create(desc(prev_coords=None)) == -1
+    assert create(desc(incremental=1, dense_out=None)) == -1
+    assert create(desc(table_in_compaction=2)) == -1
+    assert create(desc(V=20000)) == -4 and "table" in err(lib)
+    assert create(desc(sets0__ws_bytes=ws - 1)) == -2
+    assert create(desc(sets1__table=None)) == -1
+    assert create(desc(sets2__host_count=None)) == -1
+    assert create(desc(sets1__coords=A + 0x100000)) == -1 and "share" in err(lib)
+    d = desc()
+    d.sets[1].plan[1] = A + 0x9000    # a plan buffer for a layer without plan rows
+    assert create(d) == -1 and "plan_rows = 0" in err(lib)
+    # a linear layer with a plan row limit
+    d = desc()
+    d.layers[0].kind = shc.SHC_LAYER_LINEAR
+    d.layers[0].plan_rows = 10
+    assert create(d) == -1 and "linear" in err(lib)
+    # prev_coords aliasing an index set's coords
+    assert create(desc(prev_coords=A + 0x200000)) == -1
+    assert lib.shc_stack_destroy(None) == 0
+    cur, prev, n = ctypes.c_int32(0), ctypes.c_int64(0), ctypes.c_int64(0)
+    assert lib.shc_stack_run(None, 1, None, ctypes.cast(None, shc.STACK_FEED_FN), None, 0, None,
+                             ctypes.byref(cur), ctypes.byref(prev), ctypes.byref(n)) == -1

@@ -1,7 +1,8 @@
 """The library's host code under AddressSanitizer and UndefinedBehaviorSanitizer.
 
-abi.hip (argument validation, workspace sizing, launch set-up) is rebuilt
-with both sanitizers on its host side only, linked with the other objects of
+abi.hip (argument validation, workspace sizing, launch set-up) and
+stack.hip (the stack executor) are rebuilt with both sanitizers on their host
+side only, linked with the other objects of
 the library build and with tests/sanitize/abi_fuzz.c, which calls every entry
 point with edge-value arguments (see that file).  Runs only where no GPU is
 present: there no call gets past its first HIP call, so the stand-in device
@@ -22,23 +23,27 @@ CLANGXX = os.path.join(ROCM, "llvm", "bin", "clang++")
 
 
 def test_abi_host_code_under_asan_ubsan(tmp_path):
+    host = ("abi", "stack")    # sources whose host code is rebuilt with the sanitizers
     objs = [o for o in sorted(glob.glob(os.path.join(BUILD, "*.o")))
-            if os.path.basename(o) != "abi.o"]
+            if os.path.splitext(os.path.basename(o))[0] not in host]
     if not objs:
         pytest.skip("library objects not built (python -m paper_2608_09388_amd.build)")
     for tool in (HIPCC, CLANG, CLANGXX):
         if not os.path.exists(tool):
             pytest.skip(f"{tool} not found")
     inc = os.path.join(ROOT, "include")
-    abi = str(tmp_path / "abi_san.o")
-    # host-side sanitizers only: each -fsanitize flag goes to the host compile
-    subprocess.run([HIPCC, "--offload-arch=gfx950", "-O1", "-g", "-fPIC", "-std=c++17", "-I", inc,
-                    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-                    "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
-                    "-Xarch_host", "-fno-sanitize-recover=undefined",
-                    "-Xarch_host", "-fno-omit-frame-pointer",
-                    "-c", os.path.join(ROOT, "paper_2608_09388_amd", "csrc", "abi.hip"),
-                    "-o", abi], check=True, capture_output=True)
+    san = []
+    for name in host:
+        o = str(tmp_path / f"{name}_san.o")
+        # host-side sanitizers only: each -fsanitize flag goes to the host compile
+        subprocess.run([HIPCC, "--offload-arch=gfx950", "-O1", "-g", "-fPIC", "-std=c++17", "-I",
+                        inc, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                        "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                        "-Xarch_host", "-fno-sanitize-recover=undefined",
+                        "-Xarch_host", "-fno-omit-frame-pointer",
+                        "-c", os.path.join(ROOT, "paper_2608_09388_amd", "csrc", f"{name}.hip"),
+                        "-o", o], check=True, capture_output=True)
+        san.append(o)
     fuzz_o = str(tmp_path / "fuzz.o")
     subprocess.run([CLANG, "-O1", "-g", "-fsanitize=address,undefined",
                     "-fno-sanitize-recover=undefined", "-D__HIP_PLATFORM_AMD__", "-I", inc,
@@ -46,7 +51,7 @@ def test_abi_host_code_under_asan_ubsan(tmp_path):
                     "-c", os.path.join(ROOT, "tests", "sanitize", "abi_fuzz.c"), "-o", fuzz_o],
                    check=True, capture_output=True)
     exe = str(tmp_path / "abi_fuzz")
-    subprocess.run([CLANGXX, "-fsanitize=address,undefined", fuzz_o, abi, *objs,
+    subprocess.run([CLANGXX, "-fsanitize=address,undefined", fuzz_o, *san, *objs,
                     "-L", os.path.join(ROCM, "lib"), "-lamdhip64",
                     "-Wl,-rpath," + os.path.join(ROCM, "lib"), "-o", exe],
                    check=True, capture_output=True)
