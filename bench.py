@@ -350,9 +350,22 @@ def main():
         "kernel_rooflines": kernel_rooflines,
     }
 
+    # the step's kernels back to back, against the pipelined step; and the
+    # per-layer rate (N' / one layer's launch)
+    sum_keys = ["compact+table" if "compact+table" in per_kernel_ms else "compact",
+                "gather+linear", "conv", "scatter", "pool"]
+    ksum = sum(per_kernel_ms[k] for k in sum_keys if k in per_kernel_ms)
+    out["step_breakdown"] = {
+        "kernels": sum_keys, "kernel_sum_us": round(ksum * 1e3, 2),
+        "step_over_kernel_sum": round(ms_per_step / ksum, 4),
+        "per_layer_rows_per_s": {
+            "gather+linear": round(n / (per_kernel_ms["gather+linear"] / 1e3), 1),
+            "conv": round(n / (per_kernel_ms["conv"] / 1e3), 1)}}
     if args.step_only:
         print(json.dumps(out))
         return
+    out["chains"] = chain_measure(w, torch, args.steps, args.warmup)
+    log("scatter-only and pool-only chains measured")
     out["gather_scatter"] = gather_scatter_measure(shc, synth, torch, args.reps)
     log("gather and scatter measured")
     out["cold_warm"] = cold_warm_measure(st, torch)
@@ -443,6 +456,29 @@ def conv_plan_measure(st, shc, torch, reps):
             "plan_build_us": round(t_build, 2), "planned_conv_us": round(t_pl, 2),
             "three_layers_table_us": round(t_tab3, 2),
             "three_layers_build_and_planned_us": round(t_pl3, 2)}
+
+
+def chain_measure(w, torch, steps, warmup):
+    """The same pipelined step ending in the scatter alone or the pool alone
+    (the path ends in "a scatter or a segmented pool"; the headline step does
+    both): ms per step and rows/s per sparse layer for each ending."""
+    import dataclasses
+    from paper_2608_09388_amd.pipeline import SparseStack
+    res = {}
+    for name, scatter, pool in (("scatter_only", True, False), ("pool_only", False, True)):
+        wv = dataclasses.replace(w, scatter=scatter, pool=pool)
+        st = SparseStack(wv, device="cuda:0", side_stream=True)
+        n = st.compact()
+        st.run(warmup)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        st.run(steps)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        res[name] = {"ms_per_step": round(ms, 4),
+                     "rows_per_s_per_layer": round(n * len(w.layers) / (ms / 1e3), 1)}
+        del st
+    return res
 
 
 def incremental_scatter_measure(w, shc, synth, torch, reps, steps=300, warmup=30):

@@ -562,7 +562,7 @@ bool plan_shape(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, shc::GemmA
 int64_t plan_size(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype,
                   int64_t* stride) {
   *stride = 0;
-  shc::GemmArgs a;
+  shc::GemmArgs a{};
   int cus = 0;
   if (!plan_shape(n_rows, K, Cin, Cout, &a, &cus)) return 0;
   return shc::conv_plan_bytes(a, dtype == SHC_BF16, cus, stride);
@@ -626,7 +626,7 @@ int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t 
 
 size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype) {
   if (!plan_query_args_ok(n_rows, K, Cin, Cout, dtype)) return 0;
-  shc::GemmArgs a;
+  shc::GemmArgs a{};
   int cus = 0;
   if (!plan_shape(n_rows, K, Cin, Cout, &a, &cus)) return 0;
   return (size_t)shc::conv_plan_bytes_upto(a, dtype == SHC_BF16, cus);
@@ -634,7 +634,7 @@ size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout,
 
 int64_t shc_conv_plan_max_rows(int32_t K, int32_t Cin, int32_t Cout, int32_t dtype) {
   if (!plan_query_args_ok(1, K, Cin, Cout, dtype)) return 0;
-  shc::GemmArgs a;
+  shc::GemmArgs a{};
   int cus = 0;
   if (!plan_shape(1, K, Cin, Cout, &a, &cus)) return 0;
   return shc::conv_plan_max_rows(a, dtype == SHC_BF16, cus);

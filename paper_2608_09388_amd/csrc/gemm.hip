@@ -624,6 +624,18 @@ hipError_t launch_gather_gemm(const GemmArgs& a, bool conv, bool bf16, hipStream
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) return e;
+  // The slot-major conv (every output column per workgroup, the slots in
+  // turn) against the weight-stationary one (column slices of W resident,
+  // jobs of 16 rows x slot), measured at K = 9 (the same results bit for
+  // bit): faster from about 1000 rows per CU (the density-sweep batch at
+  // 20 / 50 / 100%: 112 / 282 / 612 us against 138 / 347 / 659 us; the
+  // full-mesh cap at 64 channels 54 against 95 us) and for 64 input
+  // channels within one round of 128-row groups (6.6 against 10.6 us at
+  // 4,200 rows); slower for 128 input channels at a few hundred rows per CU
+  // (36 against 26 us at 5% of the density-sweep batch).
+  if (conv && conv_sm_supported(a, bf16) &&
+      (a.n_rows >= 1000LL * cus || (a.Cin == 64 && a.n_rows <= 128LL * cus)))
+    return launch_conv_sm(a, cus, stream);
   WsPlan plan;
   if (ws_plan(a, conv, bf16, cus, &plan)) return launch_ws_gemm(a, conv, bf16, plan, stream);
   // a conv plan exists only for the weight-stationary kernel

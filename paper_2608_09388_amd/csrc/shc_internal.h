@@ -176,5 +176,9 @@ int64_t conv_plan_max_rows(const GemmArgs& a, bool bf16, int num_cus);
 int64_t conv_plan_bytes_upto(const GemmArgs& a, bool bf16, int num_cus);
 hipError_t launch_ws_gemm(const GemmArgs& a, bool conv, bool bf16, const WsPlan& plan,
                           hipStream_t stream);
+// slot-major conv from a neighbour-row table (conv_sm.hip): bf16, C_in and
+// C_out in {64, 128}, K <= 32, no plan
+bool conv_sm_supported(const GemmArgs& a, bool bf16);
+hipError_t launch_conv_sm(const GemmArgs& a, int num_cus, hipStream_t stream);
 
 }  // namespace shc
