@@ -366,6 +366,8 @@ def main():
         return
     out["chains"] = chain_measure(w, torch, args.steps, args.warmup)
     log("scatter-only and pool-only chains measured")
+    out["config_stacks"] = config_stacks_measure(torch)
+    log("the other configurations' stacks measured")
     out["gather_scatter"] = gather_scatter_measure(shc, synth, torch, args.reps)
     log("gather and scatter measured")
     out["cold_warm"] = cold_warm_measure(st, torch)
@@ -456,6 +458,42 @@ def conv_plan_measure(st, shc, torch, reps):
             "plan_build_us": round(t_build, 2), "planned_conv_us": round(t_pl, 2),
             "three_layers_table_us": round(t_tab3, 2),
             "three_layers_build_and_planned_us": round(t_pl3, 2)}
+
+
+def config_stacks_measure(torch, steps=500, warmup=30, reps=50):
+    """The other configurations' whole stacks (the tiny fp32 layer, the
+    4-layer encoder, the sequence workload), pipelined as the headline step:
+    ms per step, rows/s per sparse layer, and each layer's launch on its own
+    (back to back between HIP events)."""
+    from paper_2608_09388_amd import synth
+    from paper_2608_09388_amd.pipeline import SparseStack
+    out = []
+    for name, mk in (("tiny spiral-conv layer", synth.workload_c1),
+                     ("4-layer encoder", synth.workload_c2),
+                     ("sequences", synth.workload_c5)):
+        w = mk()
+        st = SparseStack(w, device="cuda:0", side_stream=True)
+        n = st.compact()
+        st.run(warmup)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        st.run(steps)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        n = st.n
+        if st.table is not None:
+            st.build_table()
+        layer_us = [round(_time_us(lambda l=l: st.layer(l), torch, reps), 2)
+                    for l in range(len(w.layers))]
+        out.append({"workload": w.name, "dtype": w.dtype, "B": w.B, "V": w.V, "n_active": n,
+                    "layers": [f"{l.kind} {l.Cin}->{l.Cout}" for l in w.layers],
+                    "ends_in": ("scatter" if w.scatter else "") + (" pool" if w.pool else ""),
+                    "ms_per_step": round(ms, 4),
+                    "rows_per_s_per_layer": round(n * len(w.layers) / (ms / 1e3), 1),
+                    "layer_us": layer_us,
+                    "layer_rows_per_s": [round(n / (u * 1e-6), 1) for u in layer_us]})
+        del st
+    return out
 
 
 def chain_measure(w, torch, steps, warmup):
