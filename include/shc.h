@@ -352,6 +352,47 @@ int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t 
  * detected: the result is then wrong, but every access stays inside S, W,
  * bias, out and the plan.
  */
+/*
+ * The conv of shc_sparse_neighbor_conv_table with slot 0 and the other slots
+ * computed apart (Eqs. 4-5 with Eq. 10's activation; the slots of a row are
+ * summed in a different order, so results agree to rounding, not bit for
+ * bit):
+ *
+ *   P[j][i] = S[table[j][i]] W[j]   for every present (i, j >= 1), in fp32,
+ *   out[i]  = act( P[j1][i] + bias + P[j2][i] + ... + S[table[0][i]] W[0] ),
+ *
+ * j1 < j2 < ... the row's present slots j >= 1, slot 0's product accumulated
+ * last.  Two launches: one multiplies the present (row, slot) pairs of every
+ * slot j >= 1 by W[j], 16 pairs per matrix-core job, into the workspace; the
+ * other computes slot 0 for every row and adds the row's partial rows.  Each
+ * weight matrix and each neighbour row then reaches a compute unit once for
+ * all output columns, which pays when few pairs are present (sparse masks)
+ * and rows are wide: for 256 channels the table conv re-reads the weights for
+ * every 128-row tile.  Slot 0 should be the vertex itself (spiral and k-NN
+ * neighbourhoods); any other table is still computed correctly.
+ *
+ * shc_conv_split_workspace_bytes: bytes of the workspace of a call with up
+ *   to n_rows rows: (K - 1) * n_rows * Cout * 4 (at least 16); 0 when the
+ *   shape takes no split conv (dtype other than bf16, Cin or Cout outside
+ *   {64, 128, 256}, K outside [1, 32], or a workspace of 2^31 bytes or more).
+ * shc_sparse_neighbor_conv_split: S, table, W, bias, out, act as for
+ *   shc_sparse_neighbor_conv_table; workspace: device memory of at least
+ *   shc_conv_split_workspace_bytes(n_rows, ...) bytes, 16-byte aligned,
+ *   owned by the caller; its contents on entry do not matter and on return
+ *   are unspecified.  Stream-ordered; calls that share a workspace must not
+ *   overlap.
+ *
+ * Errors: those of shc_sparse_neighbor_conv_table; SHC_ERR_UNSUPPORTED for a
+ * shape without a split conv, SHC_ERR_CAPACITY when workspace_bytes is too
+ * small.
+ */
+size_t shc_conv_split_workspace_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout,
+                                      int32_t dtype);
+int shc_sparse_neighbor_conv_split(const void* S, const int32_t* table, int64_t n_rows,
+                                   int32_t K, const void* W, const float* bias, int32_t Cin,
+                                   int32_t Cout, int32_t dtype, int32_t act, void* out,
+                                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 int64_t shc_conv_plan_max_rows(int32_t K, int32_t Cin, int32_t Cout, int32_t dtype);
 size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype);
 int shc_build_conv_plan(const int32_t* table, int64_t n_rows, int32_t K, int32_t Cin,
@@ -674,6 +715,9 @@ typedef struct shc_stack_layer {
   const float* bias; /* [Cout] fp32, or NULL */
   int64_t plan_rows; /* conv: read plan[l] of the index set when 0 < N' <= plan_rows
                         (at most shc_conv_plan_max_rows of the shape); 0: never */
+  int64_t split_rows; /* conv: shc_sparse_neighbor_conv_split, with the description's
+                         split workspace, when 0 < N' <= split_rows; 0: never.  A layer
+                         takes a plan or the split conv, not both. */
 } shc_stack_layer;
 
 typedef struct shc_stack_index_set {
@@ -718,6 +762,10 @@ typedef struct shc_stack_desc {
   int32_t n_sets;          /* index sets: 2 (serial) or 3 (pipelined) */
   shc_stack_index_set sets[3];
   hipStream_t side, tail;  /* both NULL (serial) or both set (pipelined) */
+  void* split_ws;          /* workspace of the layers with split_rows > 0, at least
+                              shc_conv_split_workspace_bytes of each at its split_rows
+                              (the layers run one after another and share it), else NULL */
+  size_t split_ws_bytes;
 } shc_stack_desc;
 
 /* Batch-input callback of shc_stack_run: called just before the compaction

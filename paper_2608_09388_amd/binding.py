@@ -48,7 +48,7 @@ SHC_LAYER_LINEAR, SHC_LAYER_CONV = 0, 1
 
 class StackLayer(ctypes.Structure):
     _fields_ = [("kind", _c_i32), ("Cin", _c_i32), ("Cout", _c_i32), ("act", _c_i32),
-                ("W", _c_ptr), ("bias", _c_ptr), ("plan_rows", _c_i64)]
+                ("W", _c_ptr), ("bias", _c_ptr), ("plan_rows", _c_i64), ("split_rows", _c_i64)]
 
 
 class StackIndexSet(ctypes.Structure):
@@ -65,7 +65,8 @@ class StackDesc(ctypes.Structure):
                 ("acts", _c_ptr * (STACK_MAX_LAYERS + 1)), ("last_alt", _c_ptr),
                 ("dense_out", _c_ptr), ("incremental", _c_i32), ("prev_coords", _c_ptr),
                 ("pooled", _c_ptr), ("pool_empty", _c_f), ("n_sets", _c_i32),
-                ("sets", StackIndexSet * 3), ("side", _c_ptr), ("tail", _c_ptr)]
+                ("sets", StackIndexSet * 3), ("side", _c_ptr), ("tail", _c_ptr),
+                ("split_ws", _c_ptr), ("split_ws_bytes", _c_sz)]
 
 
 STACK_FEED_FN = ctypes.CFUNCTYPE(ctypes.c_int, _c_ptr, _c_i64, _c_ptr)
@@ -110,6 +111,10 @@ _SIGS = {
     "shc_sparse_neighbor_conv_table": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_ptr,
                                                       _c_ptr, _c_i32, _c_i32, _c_i32, _c_i32,
                                                       _c_ptr, _c_ptr]),
+    "shc_conv_split_workspace_bytes": (_c_sz, [_c_i64, _c_i32, _c_i32, _c_i32, _c_i32]),
+    "shc_sparse_neighbor_conv_split": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_ptr,
+                                                      _c_ptr, _c_i32, _c_i32, _c_i32, _c_i32,
+                                                      _c_ptr, _c_ptr, _c_sz, _c_ptr]),
     "shc_conv_plan_max_rows": (_c_i64, [_c_i32, _c_i32, _c_i32, _c_i32]),
     "shc_conv_plan_bytes": (_c_sz, [_c_i64, _c_i32, _c_i32, _c_i32, _c_i32]),
     "shc_build_conv_plan": (ctypes.c_int, [_c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
@@ -397,6 +402,28 @@ def sparse_neighbor_conv_table(S: torch.Tensor, table: torch.Tensor, n_rows: int
             _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, dt, act,
             _dev(out, "out", S.dtype, n_rows * Cout), _stream(stream)]
     _check(load().shc_sparse_neighbor_conv_table(*args), "shc_sparse_neighbor_conv_table")
+
+
+def conv_split_workspace_bytes(n_rows: int, K: int, Cin: int, Cout: int,
+                               dtype: int = SHC_BF16) -> int:
+    """shc_conv_split_workspace_bytes: workspace of a split conv of up to
+    n_rows rows (0 when the shape takes none)."""
+    return int(load().shc_conv_split_workspace_bytes(n_rows, K, Cin, Cout, dtype))
+
+
+def sparse_neighbor_conv_split(S: torch.Tensor, table: torch.Tensor, n_rows: int,
+                               W: torch.Tensor, bias: Optional[torch.Tensor], out: torch.Tensor,
+                               workspace: torch.Tensor, act: int = SHC_ACT_RELU, stream=None):
+    """shc_sparse_neighbor_conv_split: the conv of sparse_neighbor_conv_table
+    with slot 0 and the other slots apart; workspace a device byte buffer of at
+    least conv_split_workspace_bytes(n_rows, ...) bytes."""
+    K, Cin, Cout = W.shape
+    args = [_dev(S, "S", S.dtype, n_rows * Cin), _dev(table, "table", torch.int32, K * n_rows),
+            n_rows, K, _dev(W, "W", S.dtype, K * Cin * Cout),
+            _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, _dtype_code(S), act,
+            _dev(out, "out", S.dtype, n_rows * Cout), _dev(workspace, "workspace"),
+            workspace.numel() * workspace.element_size(), _stream(stream)]
+    _check(load().shc_sparse_neighbor_conv_split(*args), "shc_sparse_neighbor_conv_split")
 
 
 def conv_plan_max_rows(K: int, Cin: int, Cout: int, dtype: int = SHC_BF16) -> int:
@@ -956,6 +983,18 @@ def prepare_sparse_neighbor_conv_table(S, table, W, bias, out, act=SHC_ACT_RELU,
             _dev(W, "W", S.dtype, K * Cin * Cout), _opt_dev(bias, "bias", torch.float32, Cout),
             Cin, Cout, _dtype_code(S), act, _dev(out, "out", S.dtype), _stream(stream)]
     return Prepared("shc_sparse_neighbor_conv_table", args, 2, n_max, (S, table, W, bias, out))
+
+
+def prepare_sparse_neighbor_conv_split(S, table, W, bias, out, workspace, act=SHC_ACT_RELU,
+                                       stream=None) -> Prepared:
+    K, Cin, Cout = W.shape
+    n_max = min(S.numel() // Cin, table.numel() // K, out.numel() // Cout)
+    args = [_dev(S, "S", S.dtype), _dev(table, "table", torch.int32), 0, K,
+            _dev(W, "W", S.dtype, K * Cin * Cout), _opt_dev(bias, "bias", torch.float32, Cout),
+            Cin, Cout, _dtype_code(S), act, _dev(out, "out", S.dtype), _dev(workspace, "workspace"),
+            workspace.numel() * workspace.element_size(), _stream(stream)]
+    return Prepared("shc_sparse_neighbor_conv_split", args, 2, n_max,
+                    (S, table, W, bias, out, workspace))
 
 
 def prepare_build_conv_plan(table, K, Cin, Cout, plan, dtype=SHC_BF16, stream=None) -> Prepared:

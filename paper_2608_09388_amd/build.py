@@ -18,7 +18,8 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libshc.so")
 SOURCES = ["compact.hip", "neighbors.hip", "rows.hip", "norm.hip", "scores.hip", "backward.hip",
-           "gemm.hip", "conv_ws.hip", "conv_sm.hip", "abi.hip", "stack.hip"]
+           "gemm.hip", "conv_ws.hip", "conv_sm.hip", "conv_split.hip", "abi.hip",
+           "stack.hip"]
 ARCH = os.environ.get("SHC_OFFLOAD_ARCH", "gfx950")
 
 # Packed fp32 VALU instructions are disabled for all device code.

@@ -624,6 +624,50 @@ int shc_sparse_neighbor_conv_table(const void* S, const int32_t* table, int64_t 
                     "sparse_neighbor_conv_table launch");
 }
 
+size_t shc_conv_split_workspace_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout,
+                                      int32_t dtype) {
+  if (n_rows < 0 || n_rows > INT32_MAX || dtype != SHC_BF16 ||
+      !shc::conv_split_supported(n_rows, K, Cin, Cout))
+    return 0;
+  const int64_t b = shc::conv_split_workspace_bytes(n_rows, K, Cout);
+  return (size_t)(b > 16 ? b : 16);
+}
+
+int shc_sparse_neighbor_conv_split(const void* S, const int32_t* table, int64_t n_rows,
+                                   int32_t K, const void* W, const float* bias, int32_t Cin,
+                                   int32_t Cout, int32_t dtype, int32_t act, void* out,
+                                   void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_conv_shape(n_rows, K, Cin, Cout, dtype, act));
+  if (dtype != SHC_BF16)
+    return fail(SHC_ERR_UNSUPPORTED, "the split conv runs bf16 only (dtype %d)", dtype);
+  if (!shc::conv_split_supported(n_rows, K, Cin, Cout))
+    return fail(SHC_ERR_UNSUPPORTED,
+                "no split conv for n_rows = %lld, K = %d, Cin = %d, Cout = %d (channels in "
+                "{64, 128, 256}, (K - 1) * n_rows * Cout * 4 below 2^31)",
+                (long long)n_rows, K, Cin, Cout);
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(S, "S");
+  SHC_PTR(table, "table");
+  SHC_PTR(W, "W");
+  SHC_OPT_PTR(bias, "bias");
+  SHC_PTR(out, "out");
+  SHC_PTR(workspace, "workspace");
+  const int64_t need = shc::conv_split_workspace_bytes(n_rows, K, Cout);
+  if ((int64_t)workspace_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "workspace_bytes = %zu is below the %lld bytes this call needs",
+                workspace_bytes, (long long)need);
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_status(e, "sparse_neighbor_conv_split device query");
+  return hip_status(shc::launch_conv_split(S, table, n_rows, K, W, bias, Cin, Cout,
+                                           act == SHC_ACT_RELU, out,
+                                           static_cast<float*>(workspace), cus, stream),
+                    "sparse_neighbor_conv_split launch");
+}
+
 size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype) {
   if (!plan_query_args_ok(n_rows, K, Cin, Cout, dtype)) return 0;
   shc::GemmArgs a{};

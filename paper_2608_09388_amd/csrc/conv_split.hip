@@ -1,0 +1,580 @@
+// Sparse neighbourhood convolution from a neighbour-row table (Eqs. 4-5,
+// with the activation of Eq. 10), bf16, with slot 0 and the other slots
+// computed apart:
+//
+//   out[i] = act( bias + sum_{1 <= j < K} P[j][i] + S[table[0][i]] W[0] ),
+//   P[j][i] = S[table[j][i]] W[j]   where table[j][i] >= 0 (else no term).
+//
+// Slot 0 of a spiral or k-NN neighbourhood is the vertex itself, present in
+// every row; under a sparse mask the other slots are mostly absent (at 10%
+// density about one row in ten has a given one).  Two launches:
+//
+//   pair launch: a workgroup owns one slot j >= 1 and a chunk of rows.  It
+//     holds W[j] (every output column) in LDS, lists the chunk's rows whose
+//     slot j is present, and multiplies their neighbour rows by W[j] in jobs
+//     of 16 (row, slot) pairs, writing each P[j][i] in fp32 to a workspace
+//     [K - 1][n_rows][Cout] (absent pairs are neither written nor read);
+//   row launch: a workgroup holds W[0] in LDS and its wavefronts walk groups
+//     of rows.  A row's accumulators start at its first present P[j][i] plus
+//     the bias, then take its other present P[j][i] in slot order, and the
+//     slot-0 product is accumulated onto them on the matrix cores; then the
+//     activation and the rounding to bf16.
+//
+// Every weight matrix reaches a CU once per workgroup and every gathered
+// neighbour row once for all output columns, where the tiled kernel re-reads
+// the weights per 128-row tile and the weight-stationary one the rows per
+// column slice.  The price is the fp32 round trip of the present pairs'
+// partial rows through the workspace, so the split pays at low density and
+// wide rows.  The order of the sums is fixed (the present slots j >= 1
+// ascending, with the bias added after the first, then slot 0's k-steps), so
+// the result does not depend on how rows or pairs are spread over
+// workgroups.
+//
+// MFMAs run transposed (D^T = W^T S^T): the A operand is a 16-column block of
+// W read with the transposing LDS load, the B operand 16 gathered rows of S
+// (16 contiguous bytes per lane), and lane (g, i) of the 16 x 16 result holds
+// output columns 4g .. 4g+3 of row i: 16 contiguous fp32 bytes of a partial
+// row, or 8 of an output row, per lane and column block.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+
+#include "shc_internal.h"
+
+namespace shc {
+namespace {
+
+constexpr int kSpLdsLimit = 160 * 1024;
+constexpr int kSpBufferWord3 = 0x00020000;  // raw buffer resource, 32-bit data
+constexpr uint32_t kSpOutOfRange = 0x80000000u;
+constexpr int kPairThreads = 256;
+constexpr int kPairLoads = 16;                               // table loads per thread
+constexpr int kMaxChunkRows = kPairLoads * kPairThreads;     // one pass over a chunk
+constexpr int kRowsBlocks = 2;                               // 16-row blocks per wavefront
+#define SHC_SP_LDS __attribute__((address_space(3)))
+
+typedef __bf16 sp_bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
+typedef __bf16 sp_bf16x2 __attribute__((ext_vector_type(2)));
+typedef float sp_f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t sp_v4u32 __attribute__((ext_vector_type(4)));
+typedef uint32_t sp_v2u32 __attribute__((ext_vector_type(2)));
+
+struct SplitArgs {
+  const void* S;         // [n_rows][Cin] bf16
+  const int32_t* table;  // [K][n_rows]
+  const void* W;         // [K][Cin][Cout] bf16
+  const float* bias;     // [Cout] or null
+  void* out;             // [n_rows][Cout] bf16
+  float* P;              // [K - 1][n_rows][Cout] fp32
+  int64_t n_rows;
+  int32_t K;
+  int32_t relu;
+  int32_t chunk_rows;    // pair launch: rows per workgroup
+};
+
+// A workgroup barrier that orders LDS only (global loads stay in flight).
+__device__ __forceinline__ void sp_lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Weights of one slot in LDS, [Cin][Cout] bf16 rows of 2 Cout bytes whose
+// 32-byte column chunk c sits at c ^ swz(r).  A transposing read touches
+// rows 8g + i (+ 4) for g, i < 4, each half-wavefront 8 of them; with rows of
+// 256 or 512 bytes every row starts on bank 0, and the three bits of the XOR
+// put those 8 rows on 8 different bank groups; with 128-byte rows (two to a
+// bank cycle) two bits do it.
+template <int NCT>
+__device__ __forceinline__ int sp_swz(int r) {
+  if constexpr (NCT >= 8) return (r & 3) | (((r >> 3) & 1) << 2);
+  else return ((r >> 1) & 1) | (((r >> 3) & 1) << 1);
+}
+
+template <int KS, int NCT, int NT>
+struct SlotWeights {
+  static constexpr int Cin = KS * 32;
+  static constexpr int Cout = NCT * 16;
+  static constexpr int WROW = Cout * 2;
+  static constexpr int VPR = WROW / 16;
+  static constexpr int VECS = Cin * VPR;  // 16-byte vectors
+  static_assert(VECS % 64 == 0, "whole wavefront loads");
+  static constexpr int bytes = Cin * WROW;
+
+  // W[j] straight into LDS with 16-byte direct loads: LDS vector v (row
+  // k = v / VPR, position p = v % VPR) receives source vector q of row k with
+  // q's chunk swizzled to p's (the XOR is its own inverse).  A wavefront's
+  // load writes 64 consecutive vectors; the caller waits for its own loads
+  // (s_waitcnt) before the barrier that publishes them.
+  __device__ static void load(const void* W, int j, int tid, unsigned char* wbuf) {
+    const unsigned char* src = static_cast<const unsigned char*>(W) + (int64_t)j * bytes;
+    const int lane = tid & 63;
+    for (int c = tid >> 6; c < VECS / 64; c += NT / 64) {
+      const int v = c * 64 + lane;
+      const int k = v / VPR;
+      const int p = v - k * VPR;
+      const int q = 2 * ((p >> 1) ^ sp_swz<NCT>(k)) + (p & 1);
+      __builtin_amdgcn_global_load_lds(src + (k * VPR + q) * 16,
+                                       (SHC_SP_LDS void*)(wbuf + c * 1024), 16, 0, 0);
+    }
+  }
+  // the A operand of k-step ks and column block ct: lane (g, i) gets W rows
+  // 32 ks + 8g .. +7 of column 16 ct + i (two transposing reads)
+  __device__ static bf16x8 read(const unsigned char* wbuf, int ks, int ct, int g, int l16) {
+    const int swz = sp_swz<NCT>(8 * g + (l16 >> 2));
+    const unsigned char* p0 = wbuf + (ks * 32 + 8 * g + (l16 >> 2)) * WROW + 8 * (l16 & 3) +
+                              ((ct ^ swz) << 5);
+    const sp_bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (SHC_SP_LDS sp_bf16x4*)(const_cast<unsigned char*>(p0)));
+    const sp_bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+        (SHC_SP_LDS sp_bf16x4*)(const_cast<unsigned char*>(p0 + 4 * WROW)));
+    return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  }
+};
+
+__device__ __forceinline__ int sp_lanes_below(uint64_t bal) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+}
+
+// ---------------------------------------------------------------------------
+// pair launch: grid (chunks, K - 1), workgroup (chunk c, slot j = 1 + y)
+// ---------------------------------------------------------------------------
+// (MINW: wavefronts per SIMD the registers must allow; one when a slot's
+// weights take most of the LDS, so that only one workgroup fits a CU anyway)
+template <int KS, int NCT, int MINW>
+__global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const SplitArgs a) {
+  constexpr int NT = kPairThreads;
+  constexpr int NW = NT / 64;
+  using SW = SlotWeights<KS, NCT, NT>;
+  constexpr int Cin = SW::Cin;
+  constexpr int Cout = SW::Cout;
+
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int rc = a.chunk_rows;
+  unsigned char* wbuf = smem;                                        // W[j]
+  int32_t* srcl = reinterpret_cast<int32_t*>(smem + SW::bytes);     // [rc] neighbour rows
+  int32_t* dstl = srcl + rc;                                         // [rc] their rows
+  int32_t* cnt = dstl + rc;                                          // pairs listed
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int g = lane >> 4;
+  const int l16 = lane & 15;
+  const int j = blockIdx.y + 1;
+  const int64_t n = a.n_rows;
+  const int64_t row0 = (int64_t)blockIdx.x * rc;
+  const int nrows = (int)min((int64_t)rc, n - row0);
+
+  SW::load(a.W, j, tid, wbuf);
+  if (tid == 0) *cnt = 0;
+  // the chunk's slot-j entries, all in flight at once (rc <= kMaxChunkRows)
+  const int32_t* tj = a.table + (int64_t)j * n + row0;
+  int32_t s[kPairLoads];
+#pragma unroll
+  for (int u = 0; u < kPairLoads; ++u) {
+    const int t = u * NT + tid;
+    s[u] = t < nrows ? tj[t] : -1;
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // the direct weight loads and the entries are in
+  sp_lds_barrier();
+
+  // the present pairs (list order is immaterial: every pair's partial row is
+  // computed on its own and stored by row)
+#pragma unroll
+  for (int u = 0; u < kPairLoads; ++u) {
+    const int t = u * NT + tid;
+    const bool ok = (uint32_t)s[u] < (uint32_t)n;  // t >= nrows gives s = -1
+    const uint64_t bal = __ballot(ok);
+    if (bal == 0) continue;
+    int base = 0;
+    if (lane == 0) base = atomicAdd(cnt, (int)__popcll(bal));
+    base = __shfl(base, 0);
+    if (ok) {
+      const int pos = base + sp_lanes_below(bal);
+      srcl[pos] = s[u];
+      dstl[pos] = (int32_t)(row0 + t);
+    }
+  }
+  sp_lds_barrier();
+  const int np = *cnt;
+  const int nj = (np + 15) >> 4;
+
+  const __amdgpu_buffer_rsrc_t s_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(a.S), (short)0, (int)(n * Cin * 2), kSpBufferWord3);
+  unsigned char* pj = reinterpret_cast<unsigned char*>(a.P) + (int64_t)(j - 1) * n * Cout * 4;
+  const __amdgpu_buffer_rsrc_t p_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(pj, (short)0, (int)(n * Cout * 4), kSpBufferWord3);
+
+  // job q: pairs 16 q .. 16 q + 15; lane (g, i) loads k-group g of pair i
+  auto load_a = [&](int q, i32x4 (&af)[KS]) {
+    const int p = q * 16 + l16;
+    const int32_t src = p < np ? srcl[p] : -1;
+    const uint32_t off = (uint32_t)src * (uint32_t)(Cin * 2) + (uint32_t)g * 16u;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      af[ks] = __builtin_bit_cast(
+          i32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     s_rsrc, src >= 0 ? off + (uint32_t)ks * 64u : kSpOutOfRange, 0, 0));
+  };
+  // jobs q and q + NW together: every weight fragment read from LDS feeds
+  // both (a job past the last has no pairs: zero rows, nothing stored)
+  auto jobs2 = [&](int q, const i32x4 (&fa)[KS], const i32x4 (&fb)[KS]) {
+    f32x4 acc[2][NCT];
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+      acc[0][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+      acc[1][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 sa = __builtin_bit_cast(bf16x8, fa[ks]);
+      const bf16x8 sb = __builtin_bit_cast(bf16x8, fb[ks]);
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+        const bf16x8 wf = SW::read(wbuf, ks, ct, g, l16);
+        acc[0][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, sa, acc[0][ct], 0, 0, 0);
+        acc[1][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, sb, acc[1][ct], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int p = (q + h * NW) * 16 + l16;
+      const int32_t dst = p < np ? dstl[p] : -1;
+      const uint32_t off = (uint32_t)dst * (uint32_t)(Cout * 4) + (uint32_t)g * 16u;
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct)
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(sp_v4u32, acc[h][ct]), p_rsrc,
+            dst >= 0 ? off + (uint32_t)ct * 64u : kSpOutOfRange, 0, 0);
+    }
+  };
+
+  // a wavefront takes jobs wave, wave + NW, ... two at a time; the next two
+  // jobs' rows are in flight while two compute
+  i32x4 a0[KS], a1[KS], b0[KS], b1[KS];
+  int q = wave;
+  if (q < nj) {
+    load_a(q, a0);
+    load_a(q + NW, a1);
+  }
+  for (; q < nj; q += 4 * NW) {
+    const bool more = q + 2 * NW < nj;
+    if (more) {
+      load_a(q + 2 * NW, b0);
+      load_a(q + 3 * NW, b1);
+    }
+    jobs2(q, a0, a1);
+    if (!more) break;
+    if (q + 4 * NW < nj) {
+      load_a(q + 4 * NW, a0);
+      load_a(q + 5 * NW, a1);
+    }
+    jobs2(q + 2 * NW, b0, b1);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// row launch: NW wavefronts per workgroup; a wavefront's task is BPW
+// consecutive 16-row blocks (every weight fragment read from LDS serves all
+// of them), tasks handed out grid-stride; JQ table entries per lane and
+// block (lane (g, i) reads slots g, g + 4, ... of row i)
+// ---------------------------------------------------------------------------
+template <int KS, int NCT, int NW, int BPW, int JQ, int MINW>
+__global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArgs a) {
+  constexpr int NT = 64 * NW;
+  using SW = SlotWeights<KS, NCT, NT>;
+  constexpr int Cin = SW::Cin;
+  constexpr int Cout = SW::Cout;
+
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  unsigned char* wbuf = smem;  // W[0]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int g = lane >> 4;
+  const int l16 = lane & 15;
+  const int64_t n = a.n_rows;
+  const int K = a.K;
+  const int64_t ntask = (n + 16 * BPW - 1) / (16 * BPW);
+  const int64_t stride = (int64_t)gridDim.x * NW;
+
+  const __amdgpu_buffer_rsrc_t s_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(a.S), (short)0, (int)(n * Cin * 2), kSpBufferWord3);
+  const __amdgpu_buffer_rsrc_t p_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      a.P, (short)0, (int)((int64_t)(K > 1 ? K - 1 : 1) * n * Cout * 4), kSpBufferWord3);
+  const __amdgpu_buffer_rsrc_t o_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      a.out, (short)0, (int)(n * Cout * 2), kSpBufferWord3);
+  auto load_s = [&](int64_t src, i32x4 (&af)[KS]) {
+    const uint32_t off = (uint32_t)src * (uint32_t)(Cin * 2) + (uint32_t)g * 16u;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      af[ks] = __builtin_bit_cast(
+          i32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     s_rsrc, src >= 0 ? off + (uint32_t)ks * 64u : kSpOutOfRange, 0, 0));
+  };
+  auto row_of = [&](int64_t task, int u) -> int64_t {
+    return task * (16 * BPW) + u * 16 + l16;
+  };
+  // A task's loads that need no table entry go out first: its table entries
+  // and each row's own input row, which is slot 0's neighbour row in a
+  // spiral or k-NN table (checked once the entries are in; any other slot-0
+  // entry is loaded again).
+  int32_t sv[BPW][JQ];
+  i32x4 af[BPW][KS];
+  auto issue = [&](int64_t task) {
+#pragma unroll
+    for (int u = 0; u < BPW; ++u) {
+      const int64_t row = row_of(task, u);
+      const bool valid = row < n;
+#pragma unroll
+      for (int q = 0; q < JQ; ++q) {
+        const int jq = g + 4 * q;
+        const int jc = jq < K ? jq : K - 1;
+        sv[u][q] = valid ? a.table[(int64_t)jc * n + row] : -1;
+      }
+      load_s(valid ? row : -1, af[u]);
+    }
+  };
+
+  int64_t task = (int64_t)blockIdx.x * NW + wave;
+  SW::load(a.W, 0, tid, wbuf);
+  if (task < ntask) issue(task);
+  __builtin_amdgcn_s_waitcnt(0);  // the direct weight loads (and the first task's) are in
+  sp_lds_barrier();
+
+  for (; task < ntask; task += stride) {
+    int64_t row[BPW];
+    bool valid[BPW];
+    uint32_t m[BPW];
+#pragma unroll
+    for (int u = 0; u < BPW; ++u) {
+      row[u] = row_of(task, u);
+      valid[u] = row[u] < n;
+      // present-slot mask and slot 0's row
+      m[u] = 0;
+      int32_t s0 = -1;
+#pragma unroll
+      for (int q = 0; q < JQ; ++q) {
+        const int jq = g + 4 * q;
+        const bool ok = jq < K && (uint32_t)sv[u][q] < (uint32_t)n;
+        m[u] |= (ok ? 1u : 0u) << jq;
+        if (q == 0) s0 = ok ? sv[u][0] : -1;
+      }
+      m[u] |= (uint32_t)__shfl_xor((int)m[u], 16);
+      m[u] |= (uint32_t)__shfl_xor((int)m[u], 32);
+      s0 = __shfl(s0, l16);  // from lane (0, i)
+      if (__ballot(valid[u] && s0 != row[u]) != 0) load_s(s0, af[u]);
+    }
+
+    // Accumulators: the first present slot j >= 1's partial row loaded into
+    // them (zeros when there is none), plus the bias, plus the second present
+    // slot's partial row (loaded beside the first); then any further present
+    // slots of the row in order, one whole partial row per round trip, for as
+    // many rounds as the wavefront's row with the most of them needs.  Adding
+    // an absent slot's zeros changes nothing.
+    auto p_off = [&](int j, int64_t r) -> uint32_t {
+      return ((uint32_t)(j - 1) * (uint32_t)n + (uint32_t)r) * (uint32_t)(Cout * 4) +
+             (uint32_t)g * 16u;
+    };
+    auto load_p = [&](int j, int64_t r, f32x4 (&c)[NCT]) {
+      const uint32_t off = j > 0 ? p_off(j, r) : 0u;
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct)
+        c[ct] = __builtin_bit_cast(
+            f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                       p_rsrc, j > 0 ? off + (uint32_t)ct * 64u : kSpOutOfRange, 0, 0));
+    };
+    f32x4 acc[BPW][NCT];
+    f32x4 c2[BPW][NCT];
+    uint32_t rest[BPW];
+#pragma unroll
+    for (int u = 0; u < BPW; ++u) {
+      const uint32_t sp = m[u] & ~1u;
+      const uint32_t sp2 = sp & (sp - 1u);
+      load_p(sp ? __builtin_ctz(sp) : 0, row[u], acc[u]);
+      load_p(sp2 ? __builtin_ctz(sp2) : 0, row[u], c2[u]);
+      rest[u] = sp2 & (sp2 - 1u);
+    }
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+      f32x4 b = {0.f, 0.f, 0.f, 0.f};
+      if (a.bias != nullptr)
+        b = f32x4{a.bias[ct * 16 + 4 * g], a.bias[ct * 16 + 4 * g + 1],
+                  a.bias[ct * 16 + 4 * g + 2], a.bias[ct * 16 + 4 * g + 3]};
+#pragma unroll
+      for (int u = 0; u < BPW; ++u) acc[u][ct] = (acc[u][ct] + b) + c2[u][ct];
+    }
+#pragma unroll
+    for (int u = 0; u < BPW; ++u) {
+      uint32_t v = rest[u];
+      while (__ballot(v != 0) != 0) {
+        f32x4 c[NCT];
+        load_p(v != 0 ? __builtin_ctz(v) : 0, row[u], c);
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) acc[u][ct] += c[ct];
+        v &= v - 1u;
+      }
+    }
+
+    // slot 0 on the matrix cores, each weight fragment serving every block
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+        const bf16x8 wf = SW::read(wbuf, ks, ct, g, l16);
+#pragma unroll
+        for (int u = 0; u < BPW; ++u)
+          acc[u][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              wf, __builtin_bit_cast(bf16x8, af[u][ks]), acc[u][ct], 0, 0, 0);
+      }
+    }
+
+    // the next task's loads go out before this one's stores
+    if (task + stride < ntask) issue(task + stride);
+
+    // activation, bf16 (round to nearest even), 8 bytes per lane and block
+    const bool relu = a.relu != 0;
+#pragma unroll
+    for (int u = 0; u < BPW; ++u) {
+      const uint32_t ooff = (uint32_t)row[u] * (uint32_t)(Cout * 2) + (uint32_t)g * 8u;
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float x = acc[u][ct][r];
+          v[r] = relu ? (x > 0.f ? x : 0.f) : x;
+        }
+        const sp_bf16x2 h0 = __builtin_convertvector(sp_f32x2{v[0], v[1]}, sp_bf16x2);
+        const sp_bf16x2 h1 = __builtin_convertvector(sp_f32x2{v[2], v[3]}, sp_bf16x2);
+        const sp_v2u32 w = {__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1)};
+        __builtin_amdgcn_raw_buffer_store_b64(
+            w, o_rsrc, valid[u] ? ooff + (uint32_t)ct * 32u : kSpOutOfRange, 0, 0);
+      }
+    }
+  }
+}
+
+template <typename Kern>
+hipError_t sp_allow_lds(Kern kern, std::once_flag& once, hipError_t& err) {
+  std::call_once(once, [&] {
+    err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kSpLdsLimit);
+  });
+  return err;
+}
+
+// Workgroups of either launch that one CU holds at once: one for "big"
+// shapes (a slot's weights at 64 KB or more, or 256 output columns, whose
+// row blocks take a SIMD's whole register file), else two.
+constexpr bool split_big(int wbytes, int nct) { return wbytes >= 64 * 1024 || nct >= 16; }
+int split_wgs_per_cu(bool big) { return big ? 1 : 2; }
+
+// Rows per pair workgroup: about split_wgs_per_cu workgroups per CU over the
+// K - 1 slots, a multiple of 64, within one pass of the table loads and the
+// LDS left beside the weights.
+int split_chunk_rows(int64_t n, int32_t K, int num_cus, int wbytes, bool big) {
+  const int64_t slots = K > 1 ? K - 1 : 1;
+  const int64_t wgs = (int64_t)num_cus * split_wgs_per_cu(big);
+  int64_t chunks = (wgs + slots - 1) / slots;
+  if (chunks < 1) chunks = 1;
+  int64_t rc = (n + chunks - 1) / chunks;
+  rc = (rc + 63) / 64 * 64;
+  const int64_t lds_rows = ((kSpLdsLimit - wbytes - 16) / 8) / 64 * 64;
+  if (rc > lds_rows) rc = lds_rows;
+  if (rc > kMaxChunkRows) rc = kMaxChunkRows;
+  if (rc < 64) rc = 64;
+  return (int)rc;
+}
+
+// For big shapes one workgroup of either launch fits a CU: the row
+// workgroups then have four wavefronts, one per SIMD with the SIMD's whole
+// register file.  Two 16-row blocks per wavefront while their accumulators,
+// first two partial rows, input rows and table entries fit the registers,
+// else one.
+template <int KS, int NCT>
+hipError_t launch_split_k(const SplitArgs& a0, int num_cus, hipStream_t stream) {
+  SplitArgs a = a0;
+  constexpr int wbytes = KS * 32 * NCT * 16 * 2;
+  constexpr bool big = split_big(wbytes, NCT);
+  constexpr int MINW = big ? 1 : 2;
+  if (a.K > 1) {
+    a.chunk_rows = split_chunk_rows(a.n_rows, a.K, num_cus, wbytes, big);
+    auto kp = conv_pairs_kernel<KS, NCT, MINW>;
+    static std::once_flag once;
+    static hipError_t err = hipSuccess;
+    if (sp_allow_lds(kp, once, err) != hipSuccess) return err;
+    const size_t lds = (size_t)wbytes + 2 * (size_t)a.chunk_rows * 4 + 16;
+    const unsigned chunks = (unsigned)((a.n_rows + a.chunk_rows - 1) / a.chunk_rows);
+    hipLaunchKernelGGL(kp, dim3(chunks, (unsigned)(a.K - 1)), dim3(kPairThreads), lds, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  constexpr int NW = big ? 4 : 8;
+  constexpr int B3 = KS * NCT >= 128 ? 1 : kRowsBlocks;  // K <= 12
+  constexpr int B8 = KS * NCT >= 32 ? 1 : kRowsBlocks;   // K > 12
+  const int BPW = a.K <= 12 ? B3 : B8;
+  const int64_t tasks = (a.n_rows + 16 * BPW - 1) / (16 * BPW);
+  int64_t grid = (tasks + NW - 1) / NW;
+  const int64_t cap = (int64_t)num_cus * split_wgs_per_cu(big);
+  if (grid > cap) grid = cap;
+  if (a.K <= 12) {
+    auto kr = conv_rows_kernel<KS, NCT, NW, B3, 3, MINW>;
+    static std::once_flag once;
+    static hipError_t err = hipSuccess;
+    if (sp_allow_lds(kr, once, err) != hipSuccess) return err;
+    hipLaunchKernelGGL(kr, dim3((unsigned)grid), dim3(64 * NW), (size_t)wbytes, stream, a);
+  } else {
+    auto kr = conv_rows_kernel<KS, NCT, NW, B8, 8, MINW>;
+    static std::once_flag once;
+    static hipError_t err = hipSuccess;
+    if (sp_allow_lds(kr, once, err) != hipSuccess) return err;
+    hipLaunchKernelGGL(kr, dim3((unsigned)grid), dim3(64 * NW), (size_t)wbytes, stream, a);
+  }
+  return hipGetLastError();
+}
+
+bool split_channels_ok(int32_t C) { return C == 64 || C == 128 || C == 256; }
+
+}  // namespace
+
+int64_t conv_split_workspace_bytes(int64_t n_rows, int32_t K, int32_t Cout) {
+  return (int64_t)(K > 1 ? K - 1 : 0) * n_rows * Cout * 4;
+}
+
+bool conv_split_supported(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout) {
+  if (K < 1 || K > 32) return false;
+  if (!split_channels_ok(Cin) || !split_channels_ok(Cout)) return false;
+  // 32-bit buffer offsets into S, out and the workspace
+  if (n_rows * Cin * 2 > 0x7FFF0000LL || n_rows * Cout * 2 > 0x7FFF0000LL) return false;
+  return (int64_t)(K > 1 ? K - 1 : 1) * n_rows * Cout * 4 <= 0x7FFF0000LL;
+}
+
+hipError_t launch_conv_split(const void* S, const int32_t* table, int64_t n_rows, int32_t K,
+                             const void* W, const float* bias, int32_t Cin, int32_t Cout,
+                             int32_t relu, void* out, float* workspace, int num_cus,
+                             hipStream_t stream) {
+  if (n_rows == 0) return hipSuccess;
+  SplitArgs a{};
+  a.S = S;
+  a.table = table;
+  a.W = W;
+  a.bias = bias;
+  a.out = out;
+  a.P = workspace;
+  a.n_rows = n_rows;
+  a.K = K;
+  a.relu = relu;
+#define SHC_SPLIT_CASE(CI, CO)                                                      \
+  if (Cin == CI && Cout == CO) return launch_split_k<CI / 32, CO / 16>(a, num_cus, stream);
+  SHC_SPLIT_CASE(64, 64) SHC_SPLIT_CASE(64, 128) SHC_SPLIT_CASE(64, 256)
+  SHC_SPLIT_CASE(128, 64) SHC_SPLIT_CASE(128, 128) SHC_SPLIT_CASE(128, 256)
+  SHC_SPLIT_CASE(256, 64) SHC_SPLIT_CASE(256, 128) SHC_SPLIT_CASE(256, 256)
+#undef SHC_SPLIT_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace shc

@@ -180,5 +180,15 @@ hipError_t launch_ws_gemm(const GemmArgs& a, bool conv, bool bf16, const WsPlan&
 // C_out in {64, 128}, K <= 32, no plan
 bool conv_sm_supported(const GemmArgs& a, bool bf16);
 hipError_t launch_conv_sm(const GemmArgs& a, int num_cus, hipStream_t stream);
+// conv from a neighbour-row table with slot 0 and the other slots apart
+// (conv_split.hip): bf16, C_in and C_out in {64, 128, 256}, K <= 32; the
+// other slots' partial rows go through an fp32 workspace of
+// conv_split_workspace_bytes bytes
+int64_t conv_split_workspace_bytes(int64_t n_rows, int32_t K, int32_t Cout);
+bool conv_split_supported(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout);
+hipError_t launch_conv_split(const void* S, const int32_t* table, int64_t n_rows, int32_t K,
+                             const void* W, const float* bias, int32_t Cin, int32_t Cout,
+                             int32_t relu, void* out, float* workspace, int num_cus,
+                             hipStream_t stream);
 
 }  // namespace shc

@@ -105,6 +105,8 @@ struct Stack {
     return plan_owner[l] >= 0 && n > 0 && n <= d.layers[l].plan_rows;
   }
 
+  bool split(int l, int64_t n) const { return n > 0 && n <= d.layers[l].split_rows; }
+
   int plans(int s, int64_t n, hipStream_t st) const {
     for (int l = 0; l < d.n_layers; ++l) {
       if (plan_owner[l] != l || !planned(l, n)) continue;
@@ -125,6 +127,10 @@ struct Stack {
     const shc_stack_layer& L = d.layers[l];
     const shc_stack_index_set& x = d.sets[s];
     if (L.kind == SHC_LAYER_CONV) {
+      if (split(l, n))
+        return shc_sparse_neighbor_conv_split(d.acts[l], x.table, n, d.K, L.W, L.bias, L.Cin,
+                                              L.Cout, d.dtype, L.act, dst, d.split_ws,
+                                              d.split_ws_bytes, st);
       if (planned(l, n))
         return shc_sparse_neighbor_conv_planned(d.acts[l], x.plan[l], x.plan_bytes[l], n, d.K,
                                                 L.W, L.bias, L.Cin, L.Cout, d.dtype, L.act, dst,
@@ -323,6 +329,7 @@ int check_desc(const shc_stack_desc& d, Stack* k) {
   STK_TRY(check_channels(d.C0, 0, "C0"));
   k->has_conv = false;
   int32_t c_prev = d.C0;
+  size_t split_need = 0;  // the largest split workspace of any layer
   for (int l = 0; l < d.n_layers; ++l) {
     const shc_stack_layer& L = d.layers[l];
     if (L.kind != SHC_LAYER_LINEAR && L.kind != SHC_LAYER_CONV)
@@ -340,6 +347,23 @@ int check_desc(const shc_stack_desc& d, Stack* k) {
     if (L.plan_rows < 0)
       return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: plan_rows = %lld is negative", l,
                             (long long)L.plan_rows);
+    if (L.split_rows < 0)
+      return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: split_rows = %lld is negative", l,
+                            (long long)L.split_rows);
+    if (L.split_rows > 0) {
+      if (L.kind != SHC_LAYER_CONV)
+        return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: a linear layer takes no split "
+                              "conv", l);
+      if (L.plan_rows > 0)
+        return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: plan_rows and split_rows both "
+                              "set", l);
+      const size_t need = shc_conv_split_workspace_bytes(L.split_rows, d.K, L.Cin, L.Cout,
+                                                         d.dtype);
+      if (need == 0)
+        return shc::set_error(SHC_ERR_UNSUPPORTED, "layer %d: no split conv for %lld rows of "
+                              "this shape", l, (long long)L.split_rows);
+      split_need = need > split_need ? need : split_need;
+    }
     if (L.kind == SHC_LAYER_CONV) {
       k->has_conv = true;
       if (L.plan_rows > 0) {
@@ -355,6 +379,14 @@ int check_desc(const shc_stack_desc& d, Stack* k) {
     STK_TRY(need_ptr(d.acts[l + 1], "acts", l + 1));
   }
   k->c_last = c_prev;
+  if (split_need > 0) {
+    STK_TRY(need_ptr(d.split_ws, "split_ws"));
+    if (d.split_ws_bytes < split_need)
+      return shc::set_error(SHC_ERR_CAPACITY, "split_ws_bytes = %zu is below the %zu bytes the "
+                            "split layers need", d.split_ws_bytes, split_need);
+  } else if (d.split_ws != nullptr) {
+    return shc::set_error(SHC_ERR_INVALID_ARG, "split_ws given but no layer has split_rows > 0");
+  }
   k->fused_gather = d.layers[0].kind == SHC_LAYER_LINEAR;
   if (!k->fused_gather) STK_TRY(need_ptr(d.acts[0], "acts", 0));
   if (k->has_conv) {

@@ -54,6 +54,13 @@ from .synth import Workload
 
 TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
 
+# Active fraction of the B*V rows up to which a 256-channel conv layer runs as
+# the split conv by default.  On the sequence workload's mesh (2048 x 655
+# vertices, K = 9, 256 -> 256) the split conv took 61 / 146 / 245 us against
+# 130 / 226 / 343 us for the table conv at 5 / 10 / 15% Bernoulli masks; its
+# workspace limit (2^31 bytes) ends it near 20% there.
+SPLIT_DENSITY = 0.2
+
 
 def to_device(a: np.ndarray, dtype: str, device) -> torch.Tensor:
     """Upload fp32 values that are exact in `dtype` as a tensor of that dtype."""
@@ -158,6 +165,10 @@ class _IndexSet:
         if spec.kind == "conv":
             table = shc.prepare_sparse_neighbor_conv_table(src, self.table, st.weights[l],
                                                            st.biases[l], dst, a)
+            if l in st.split_rows:
+                split = shc.prepare_sparse_neighbor_conv_split(src, self.table, st.weights[l],
+                                                               st.biases[l], dst, st.split_ws, a)
+                return _SplitConv(table, split, st.split_rows[l])
             plan = self.plans.get(tuple(st.weights[l].shape))
             if plan is None:
                 return table
@@ -187,6 +198,34 @@ class _IncrementalScatter:
         st.prev_n = n
 
 
+class _SplitConv:
+    """A conv layer that runs as the split conv when the batch's row count is
+    within its limit, else from the table."""
+
+    def __init__(self, table, split, n_lim: int):
+        self.table, self.split, self.n_lim = table, split, n_lim
+
+    def __call__(self, n: int):
+        return self.split(n) if 0 < n <= self.n_lim else self.table(n)
+
+
+def _split_rows_limit(want: int, K: int, Cin: int, Cout: int) -> int:
+    """The largest row count up to `want` whose split conv of this shape the
+    library takes (0: none)."""
+    if want <= 0 or shc.conv_split_workspace_bytes(1, K, Cin, Cout) == 0:
+        return 0
+    if shc.conv_split_workspace_bytes(want, K, Cin, Cout) > 0:
+        return want
+    lo, hi = 1, want  # split at lo, none at hi
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        if shc.conv_split_workspace_bytes(mid, K, Cin, Cout) > 0:
+            lo = mid
+        else:
+            hi = mid
+    return lo
+
+
 class _PlannedConv:
     """A conv layer that reads its set's plan when the batch's row count has
     one (the plan was built for it), else the table."""
@@ -201,7 +240,8 @@ class _PlannedConv:
 class SparseStack:
     def __init__(self, w: Workload, device: str = "cuda", act: int = shc.SHC_ACT_RELU,
                  side_stream: bool = False, conv_plans: Optional[bool] = None,
-                 incremental_scatter: bool = False, executor: str = "native"):
+                 incremental_scatter: bool = False, executor: str = "native",
+                 split_conv: Optional[bool] = None):
         if executor not in ("native", "python"):
             raise ValueError(f"executor = {executor!r}: 'native' or 'python'")
         self.w = w
@@ -261,7 +301,31 @@ class SparseStack:
         # 4.4 us saved per planned layer), so by default a shape takes one
         # only when two or more conv layers share it; conv_plans = True /
         # False forces plans on / off for every conv shape that can take one.
+        # Conv layers that run as shc_sparse_neighbor_conv_split (slot 0 apart
+        # from the other slots, through a workspace) for batches of at most
+        # split_rows[l] rows.  By default: layers with 256 input or output
+        # channels, up to SPLIT_DENSITY of the B*V rows (the table conv runs
+        # them on its tiled kernel, which re-reads the weights per row tile);
+        # split_conv = True / False forces it on every shape that takes it / off.
+        self.split_rows: Dict[int, int] = {}
+        if w.dtype == "bf16" and split_conv is not False:
+            for l, spec in enumerate(w.layers):
+                if spec.kind != "conv":
+                    continue
+                K_, Cin, Cout = self.weights[l].shape
+                if split_conv is None and max(Cin, Cout) < 256:
+                    continue
+                want = BV if split_conv else int(SPLIT_DENSITY * BV)
+                rows = _split_rows_limit(min(want, BV), K_, Cin, Cout)
+                if rows > 0:
+                    self.split_rows[l] = rows
+        self.split_ws = None
+        if self.split_rows:
+            need = max(shc.conv_split_workspace_bytes(r, *self.weights[l].shape)
+                       for l, r in self.split_rows.items())
+            self.split_ws = torch.empty(need, dtype=torch.uint8, device=dev)
         self.plan_shapes: Dict[Tuple[int, int, int], int] = {}
+        split_shapes = {tuple(self.weights[l].shape) for l in self.split_rows}
         if w.dtype == "bf16":
             shapes: Dict[Tuple[int, int, int], int] = {}
             for l, spec in enumerate(w.layers):
@@ -269,6 +333,8 @@ class SparseStack:
                     key = tuple(self.weights[l].shape)
                     shapes[key] = shapes.get(key, 0) + 1
             for key, count in shapes.items():
+                if key in split_shapes:
+                    continue  # a layer takes a plan or the split conv, not both
                 use = conv_plans if conv_plans is not None else count >= 2
                 n_lim = shc.conv_plan_max_rows(*key) if use else 0
                 if n_lim > 0:
@@ -306,6 +372,7 @@ class SparseStack:
             L.bias = self.biases[l].data_ptr() if self.biases[l] is not None else None
             n_lim = self.plan_shapes.get(tuple(W.shape), 0) if spec.kind == "conv" else 0
             L.plan_rows = min(BV, n_lim)
+            L.split_rows = self.split_rows.get(l, 0)
         for i, a in enumerate(self.acts):
             d.acts[i] = a.data_ptr()
         d.last_alt = self.last_alt.data_ptr() if self.last_alt is not None else None
@@ -331,6 +398,8 @@ class SparseStack:
                     S.plan[l], S.plan_bytes[l] = plan[0].data_ptr(), plan[0].numel()
         d.side = self.side.cuda_stream if self.side is not None else None
         d.tail = self.tail.cuda_stream if self.tail is not None else None
+        if self.split_ws is not None:
+            d.split_ws, d.split_ws_bytes = self.split_ws.data_ptr(), self.split_ws.numel()
         return shc.StackExecutor(d, keep)
 
     # -- the index set of the current mask -------------------------------------

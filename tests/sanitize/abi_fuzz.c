@@ -82,6 +82,7 @@ static void random_layer(shc_stack_layer* L) {
   L->W = P();
   L->bias = P();
   L->plan_rows = I64();
+  L->split_rows = I64();
 }
 
 static void random_set(shc_stack_index_set* x, int s) {
@@ -124,6 +125,8 @@ static void stack_desc(shc_stack_desc* d) {
     for (int s = 0; s < 3; ++s) random_set(&d->sets[s], s);
     d->side = (hipStream_t)P();
     d->tail = (hipStream_t)P();
+    d->split_ws = P();
+    d->split_ws_bytes = SZ();
     return;
   }
   /* coherent base; buffers at distinct aligned stand-in addresses */
@@ -171,11 +174,19 @@ static void stack_desc(shc_stack_desc* d) {
   }
   d->side = (hipStream_t)NEXT();
   d->tail = (hipStream_t)NEXT();
+  if (next_u64() & 1) {
+    /* layer 1 by the split conv instead of its plan, with a workspace */
+    d->layers[1].plan_rows = 0;
+    d->layers[1].split_rows = 1000;
+    for (int s = 0; s < 3; ++s) d->sets[s].plan[1] = NULL;
+    d->split_ws = NEXT();
+    d->split_ws_bytes = (size_t)1 << 30;
+  }
 #undef NEXT
   const int changes = 1 + (int)(next_u64() % 3);
   for (int c = 0; c < changes; ++c) {
     const int s = (int)(next_u64() % 3), l = (int)(next_u64() % 2);
-    switch (next_u64() % 16) {
+    switch (next_u64() % 17) {
       case 0: d->B = I32(); break;
       case 1: d->V = I32(); break;
       case 2: d->K = I32(); break;
@@ -191,6 +202,7 @@ static void stack_desc(shc_stack_desc* d) {
       case 12: d->side = (hipStream_t)P(); break;
       case 13: d->tail = d->side; break;
       case 14: d->table_in_compaction = CODE(); d->nbr = P(); break;
+      case 15: d->split_ws = P(); d->split_ws_bytes = SZ(); break;
       default: d->sets[s].coords = d->sets[(s + 1) % 3].coords; break;
     }
   }
@@ -215,6 +227,7 @@ int main(void) {
     (void)shc_sparse_neighbor_conv_backward_workspace(I64(), I32(), I32(), I32(), CODE());
     (void)shc_conv_plan_max_rows(I32(), I32(), I32(), CODE());
     (void)shc_conv_plan_bytes(I64(), I32(), I32(), I32(), CODE());
+    (void)shc_conv_split_workspace_bytes(I64(), I32(), I32(), I32(), CODE());
     host_count = (next_u64() & 1) ? -1 : 5;
     int64_t* hc = (next_u64() & 1) ? &host_count : NULL;
     check(shc_compact_mask(P(), I32(), I32(), P(), P(), P(), P(), hc, I64(), P(), SZ(), NULL),
@@ -253,6 +266,9 @@ int main(void) {
           "sparse_neighbor_conv_table");
     check(shc_build_conv_plan(P(), I64(), I32(), I32(), I32(), CODE(), P(), SZ(), NULL),
           "build_conv_plan");
+    check(shc_sparse_neighbor_conv_split(P(), P(), I64(), I32(), P(), P(), I32(), I32(), CODE(),
+                                         CODE(), P(), P(), SZ(), NULL),
+          "sparse_neighbor_conv_split");
     check(shc_sparse_neighbor_conv_planned(P(), P(), SZ(), I64(), I32(), P(), P(), I32(), I32(),
                                            CODE(), CODE(), P(), NULL),
           "sparse_neighbor_conv_planned");

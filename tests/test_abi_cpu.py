@@ -384,6 +384,48 @@ def test_neighbor_table_validation(lib):
     assert conv(n=0, S=None, table=None, out=None) == 0
 
 
+def test_conv_split_validation(lib):
+    """shc_conv_split_workspace_bytes's closed form and the split conv's
+    argument checks, without a device."""
+    Q = lib.shc_conv_split_workspace_bytes
+    bf = shc.SHC_BF16
+    assert Q(1000, 9, 128, 128, bf) == 8 * 1000 * 128 * 4
+    assert Q(1000, 9, 256, 64, bf) == 8 * 1000 * 64 * 4
+    assert Q(1000, 1, 64, 64, bf) == 16          # no pairs: the minimum
+    assert Q(0, 9, 128, 128, bf) == 16
+    assert Q(-1, 9, 128, 128, bf) == 0
+    assert Q(1000, 9, 128, 128, shc.SHC_F32) == 0
+    assert Q(1000, 9, 96, 128, bf) == 0          # channels outside {64, 128, 256}
+    assert Q(1000, 9, 128, 512, bf) == 0
+    assert Q(1000, 0, 128, 128, bf) == 0
+    assert Q(1000, 33, 128, 128, bf) == 0
+    n_max = (0x7FFF0000 // (8 * 256 * 4))         # the workspace stays below 2^31 bytes
+    assert Q(n_max, 9, 256, 256, bf) > 0 and Q(n_max + 1, 9, 256, 256, bf) == 0
+    C = lib.shc_sparse_neighbor_conv_split
+
+    def conv(**kw):
+        a = dict(S=A, table=A, n=10, K=9, W=A, bias=None, Cin=128, Cout=128, dt=bf, act=1,
+                 out=A, ws=A, nb=8 * 10 * 128 * 4)
+        a.update(kw)
+        return C(a["S"], a["table"], a["n"], a["K"], a["W"], a["bias"], a["Cin"], a["Cout"],
+                 a["dt"], a["act"], a["out"], a["ws"], a["nb"], None)
+
+    assert conv(table=None) == -1 and "table" in err(lib)
+    assert conv(S=MIS) == -3
+    assert conv(ws=None) == -1 and "workspace" in err(lib)
+    assert conv(ws=MIS) == -3
+    assert conv(nb=8 * 10 * 128 * 4 - 1) == -2 and "workspace_bytes" in err(lib)
+    assert conv(dt=shc.SHC_F32) == -4 and "bf16" in err(lib)
+    assert conv(Cin=96) == -4
+    assert conv(Cout=512) == -4
+    assert conv(K=0) == -1
+    assert conv(K=33) == -4
+    assert conv(act=3) == -4
+    assert conv(n=-1) == -1
+    assert conv(bias=MIS) == -3
+    assert conv(n=0, S=None, table=None, out=None, ws=None, nb=0) == 0   # N' = 0 is a no-op
+
+
 def test_conv_plan_validation(lib):
     Q = lib.shc_conv_plan_bytes
     bf = shc.SHC_BF16
@@ -594,6 +636,23 @@ def test_stack_validation(lib):
     assert create(d) == -1 and "linear" in err(lib)
     # prev_coords aliasing an index set's coords
     assert create(desc(prev_coords=A + 0x200000)) == -1
+    # the split conv: a row limit per conv layer, one shared workspace
+    need = lib.shc_conv_split_workspace_bytes(100, K, 64, 64, shc.SHC_BF16)
+    assert create(desc(layers0__split_rows=-1)) == -1 and "split_rows" in err(lib)
+    assert create(desc(layers0__split_rows=100)) == -1 and "split_ws" in err(lib)
+    assert create(desc(layers0__split_rows=100, split_ws=MIS, split_ws_bytes=need)) == -3
+    assert create(desc(layers0__split_rows=100, layers1__split_rows=100, split_ws=A + 0x9000,
+                       split_ws_bytes=need - 1)) == -2
+    assert create(desc(split_ws=A + 0x9000, split_ws_bytes=need)) == -1 and \
+        "no layer" in err(lib)
+    assert create(desc(layers0__split_rows=100, layers0__plan_rows=100, split_ws=A + 0x9000,
+                       split_ws_bytes=need)) == -1 and "both" in err(lib)
+    assert create(desc(layers0__split_rows=100, dtype=shc.SHC_F32, split_ws=A + 0x9000,
+                       split_ws_bytes=need)) == -4
+    d = desc(split_ws=A + 0x9000, split_ws_bytes=need)
+    d.layers[0].kind = shc.SHC_LAYER_LINEAR
+    d.layers[0].split_rows = 100
+    assert create(d) == -1 and "linear" in err(lib)
     assert lib.shc_stack_destroy(None) == 0
     cur, prev, n = ctypes.c_int32(0), ctypes.c_int64(0), ctypes.c_int64(0)
     assert lib.shc_stack_run(None, 1, None, ctypes.cast(None, shc.STACK_FEED_FN), None, 0, None,

@@ -3,7 +3,8 @@ consecutive batches issued from the library's native loop must leave exactly
 the outputs of the same calls issued one by one from Python (pipeline.py's
 own schedules), on every workload shape the stack takes: linear-first and
 conv-first stacks, fp32 and bf16, fused and separate neighbour tables, conv
-plans, zero-fill and incremental scatter, pool only, serial and pipelined.
+plans, the split conv (256-channel layers), zero-fill and incremental
+scatter, pool only, serial and pipelined.
 The per-call results themselves are checked against the oracle by the layer
 tests; the stack's against the oracle by test_stack_outputs_match_oracle.
 Every input is seeded and synthetic.
@@ -16,7 +17,7 @@ from oracle import shc_oracle as O
 from paper_2608_09388_amd import binding as shc
 from paper_2608_09388_amd import synth
 from paper_2608_09388_amd.pipeline import SparseStack
-from tests.gpu_util import require_gpu
+from tests.gpu_util import assert_scaled_close, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -146,6 +147,28 @@ def test_stack_outputs_match_oracle(dev):
     assert np.array_equal(dense, O.scatter(rows, inv, zero_fill=True))
     pooled = st.pooled.float().cpu().numpy().astype(np.float64)
     assert np.array_equal(pooled, O.segment_max(rows, row_ptr, 0.0))
+
+
+def test_split_conv_layers_in_stack_match_oracle(dev):
+    """The sequence workload's stack (256-channel convs, which take the split
+    conv by default at this density) on a small batch, pipelined: every
+    layer's rows against the oracle's conv of that layer's own input rows,
+    on sampled rows at the layer bound."""
+    w = synth.workload_c5(4, 8)
+    st = SparseStack(w, device=dev, side_stream=True)
+    assert sorted(st.split_rows) == [0, 1, 2]
+    n = st.run(2)
+    torch.cuda.synchronize()
+    assert 0 < n <= min(st.split_rows.values())
+    coords = st.coords[:n].cpu().numpy()
+    rows = np.random.default_rng(3).choice(n, size=min(n, 400), replace=False)
+    for l, spec in enumerate(w.layers):
+        S = st.acts[l][:n].float().cpu().numpy().astype(np.float64)
+        got = st.acts[l + 1][:n].float().cpu().numpy().astype(np.float64)
+        ref = O.conv_at(S, coords, w.B, w.V, w.nbr, spec.W, rows, spec.bias, act=spec.relu)
+        scale = O.conv_at(S, coords, w.B, w.V, w.nbr, spec.W, rows, spec.bias, scale=True)
+        assert_scaled_close(got[rows], ref, scale, "bf16", f"stack layer {l}",
+                            n_terms=w.K * spec.Cin)
 
 
 def test_native_time_events_and_feed_errors(dev):
