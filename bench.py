@@ -463,8 +463,10 @@ def conv_plan_measure(st, shc, torch, reps):
 def config_stacks_measure(torch, steps=500, warmup=30, reps=50):
     """The other configurations' whole stacks (the tiny fp32 layer, the
     4-layer encoder, the sequence workload), pipelined as the headline step:
-    ms per step, rows/s per sparse layer, and each layer's launch on its own
-    (back to back between HIP events)."""
+    ms per step, rows/s per sparse layer, each layer's launch on its own
+    (back to back between HIP events) and which conv kernel it ran; a layer
+    that runs as the split conv is also timed as the table conv."""
+    from paper_2608_09388_amd import binding as shc
     from paper_2608_09388_amd import synth
     from paper_2608_09388_amd.pipeline import SparseStack
     out = []
@@ -485,8 +487,29 @@ def config_stacks_measure(torch, steps=500, warmup=30, reps=50):
             st.build_table()
         layer_us = [round(_time_us(lambda l=l: st.layer(l), torch, reps), 2)
                     for l in range(len(w.layers))]
+        kinds = []
+        for l, spec in enumerate(w.layers):
+            if spec.kind != "conv":
+                kinds.append("linear")
+            elif 0 < n <= st.split_rows.get(l, 0):
+                kinds.append("split conv")
+            elif 0 < n <= st.plan_shapes.get(tuple(st.weights[l].shape), 0):
+                kinds.append("planned conv")
+            else:
+                kinds.append("table conv")
+        # the split layers' table conv on the same rows, for comparison
+        table_us = {}
+        for l, kind in enumerate(kinds):
+            if kind == "split conv":
+                tmp = torch.empty_like(st.acts[l + 1][:max(n, 1)])
+                call = shc.prepare_sparse_neighbor_conv_table(st.acts[l], st.table, st.weights[l],
+                                                              st.biases[l], tmp)
+                table_us[l] = round(_time_us(lambda c=call: c(n), torch, reps), 2)
+                del tmp
         out.append({"workload": w.name, "dtype": w.dtype, "B": w.B, "V": w.V, "n_active": n,
                     "layers": [f"{l.kind} {l.Cin}->{l.Cout}" for l in w.layers],
+                    "layer_kernels": kinds,
+                    "split_layers_table_conv_us": table_us,
                     "ends_in": ("scatter" if w.scatter else "") + (" pool" if w.pool else ""),
                     "ms_per_step": round(ms, 4),
                     "rows_per_s_per_layer": round(n * len(w.layers) / (ms / 1e3), 1),
