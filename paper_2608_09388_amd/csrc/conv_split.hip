@@ -48,8 +48,9 @@ constexpr int kSpLdsLimit = 160 * 1024;
 constexpr int kSpBufferWord3 = 0x00020000;  // raw buffer resource, 32-bit data
 constexpr uint32_t kSpOutOfRange = 0x80000000u;
 constexpr int kPairThreads = 256;
-constexpr int kPairLoads = 16;                               // table loads per thread
+constexpr int kPairLoads = 24;                               // table loads per thread
 constexpr int kMaxChunkRows = kPairLoads * kPairThreads;     // one pass over a chunk
+static_assert(kMaxChunkRows <= 65536, "chunk rows fit the 16-bit pair lists");
 constexpr int kRowsBlocks = 2;                               // 16-row blocks per wavefront
 #define SHC_SP_LDS __attribute__((address_space(3)))
 
@@ -130,7 +131,49 @@ struct SlotWeights {
         (SHC_SP_LDS sp_bf16x4*)(const_cast<unsigned char*>(p0 + 4 * WROW)));
     return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   }
+  // every column block of k-step ks
+  __device__ static void read_k(const unsigned char* wbuf, int ks, int g, int l16,
+                                bf16x8 (&out)[NCT]) {
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) out[ct] = read(wbuf, ks, ct, g, l16);
+  }
 };
+
+// The MFMAs of one k-sweep: acc[b][ct] += W^T-block (ks, ct) x B-operand b of
+// k-step ks, for NB B operands (bfrag(b, ks)).  With PREF the next k-step's
+// weight fragments are read from LDS while this one's MFMAs run (twice the
+// fragment registers; with one wavefront per SIMD nothing else hides the
+// LDS latency); else each fragment is read just before its MFMAs.
+template <int KS, int NCT, int NT, bool PREF, int NB, typename BFrag>
+__device__ __forceinline__ void sp_mfma_sweep(const unsigned char* wbuf, int g, int l16,
+                                              f32x4 (&acc)[NB][NCT], BFrag bfrag) {
+  using SW = SlotWeights<KS, NCT, NT>;
+  if constexpr (PREF) {
+    bf16x8 wf[2][NCT];
+    SW::read_k(wbuf, 0, g, l16, wf[0]);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) SW::read_k(wbuf, ks + 1, g, l16, wf[(ks + 1) & 1]);
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          acc[b][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[ks & 1][ct], bfrag(b, ks),
+                                                               acc[b][ct], 0, 0, 0);
+    }
+  } else {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+        const bf16x8 wf = SW::read(wbuf, ks, ct, g, l16);
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          acc[b][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, bfrag(b, ks), acc[b][ct],
+                                                               0, 0, 0);
+      }
+  }
+}
 
 __device__ __forceinline__ int sp_lanes_below(uint64_t bal) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
@@ -153,9 +196,11 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int rc = a.chunk_rows;
   unsigned char* wbuf = smem;                                        // W[j]
-  int32_t* srcl = reinterpret_cast<int32_t*>(smem + SW::bytes);     // [rc] neighbour rows
-  int32_t* dstl = srcl + rc;                                         // [rc] their rows
-  int32_t* cnt = dstl + rc;                                          // pairs listed
+  // pair lists: neighbour rows, then the rows themselves relative to the
+  // chunk (16 bits: rc <= kMaxChunkRows), then the count
+  int32_t* srcl = reinterpret_cast<int32_t*>(smem + SW::bytes);     // [rc]
+  uint16_t* dstl = reinterpret_cast<uint16_t*>(srcl + rc);           // [rc]
+  int32_t* cnt = reinterpret_cast<int32_t*>(dstl + ((rc + 1) & ~1)); // pairs listed
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -181,21 +226,26 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
   sp_lds_barrier();
 
   // the present pairs (list order is immaterial: every pair's partial row is
-  // computed on its own and stored by row)
+  // computed on its own and stored by row): one LDS atomic per wavefront
+  // reserves its pairs' places, the lanes' ballots place them
+  uint64_t bal[kPairLoads];
+  int total = 0;
 #pragma unroll
   for (int u = 0; u < kPairLoads; ++u) {
-    const int t = u * NT + tid;
-    const bool ok = (uint32_t)s[u] < (uint32_t)n;  // t >= nrows gives s = -1
-    const uint64_t bal = __ballot(ok);
-    if (bal == 0) continue;
-    int base = 0;
-    if (lane == 0) base = atomicAdd(cnt, (int)__popcll(bal));
-    base = __shfl(base, 0);
-    if (ok) {
-      const int pos = base + sp_lanes_below(bal);
+    bal[u] = __ballot((uint32_t)s[u] < (uint32_t)n);  // rows past the chunk read -1
+    total += (int)__popcll(bal[u]);
+  }
+  int base = 0;
+  if (lane == 0 && total > 0) base = atomicAdd(cnt, total);
+  base = __shfl(base, 0);
+#pragma unroll
+  for (int u = 0; u < kPairLoads; ++u) {
+    if ((bal[u] >> lane) & 1) {
+      const int pos = base + sp_lanes_below(bal[u]);
       srcl[pos] = s[u];
-      dstl[pos] = (int32_t)(row0 + t);
+      dstl[pos] = (uint16_t)(u * NT + tid);
     }
+    base += (int)__popcll(bal[u]);
   }
   sp_lds_barrier();
   const int np = *cnt;
@@ -227,21 +277,13 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
       acc[0][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
       acc[1][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 sa = __builtin_bit_cast(bf16x8, fa[ks]);
-      const bf16x8 sb = __builtin_bit_cast(bf16x8, fb[ks]);
-#pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
-        const bf16x8 wf = SW::read(wbuf, ks, ct, g, l16);
-        acc[0][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, sa, acc[0][ct], 0, 0, 0);
-        acc[1][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, sb, acc[1][ct], 0, 0, 0);
-      }
-    }
+    sp_mfma_sweep<KS, NCT, NT, MINW == 1, 2>(wbuf, g, l16, acc, [&](int b, int ks) {
+      return __builtin_bit_cast(bf16x8, b == 0 ? fa[ks] : fb[ks]);
+    });
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int p = (q + h * NW) * 16 + l16;
-      const int32_t dst = p < np ? dstl[p] : -1;
+      const int32_t dst = p < np ? (int32_t)(row0 + dstl[p]) : -1;
       const uint32_t off = (uint32_t)dst * (uint32_t)(Cout * 4) + (uint32_t)g * 16u;
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
@@ -420,17 +462,9 @@ __global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArg
     }
 
     // slot 0 on the matrix cores, each weight fragment serving every block
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
-        const bf16x8 wf = SW::read(wbuf, ks, ct, g, l16);
-#pragma unroll
-        for (int u = 0; u < BPW; ++u)
-          acc[u][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              wf, __builtin_bit_cast(bf16x8, af[u][ks]), acc[u][ct], 0, 0, 0);
-      }
-    }
+    sp_mfma_sweep<KS, NCT, NT, MINW == 1, BPW>(wbuf, g, l16, acc, [&](int u, int ks) {
+      return __builtin_bit_cast(bf16x8, af[u][ks]);
+    });
 
     // the next task's loads go out before this one's stores
     if (task + stride < ntask) issue(task + stride);
@@ -483,7 +517,7 @@ int split_chunk_rows(int64_t n, int32_t K, int num_cus, int wbytes, bool big) {
   if (chunks < 1) chunks = 1;
   int64_t rc = (n + chunks - 1) / chunks;
   rc = (rc + 63) / 64 * 64;
-  const int64_t lds_rows = ((kSpLdsLimit - wbytes - 16) / 8) / 64 * 64;
+  const int64_t lds_rows = ((kSpLdsLimit - wbytes - 16) / 6) / 64 * 64;
   if (rc > lds_rows) rc = lds_rows;
   if (rc > kMaxChunkRows) rc = kMaxChunkRows;
   if (rc < 64) rc = 64;
@@ -507,7 +541,7 @@ hipError_t launch_split_k(const SplitArgs& a0, int num_cus, hipStream_t stream) 
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     if (sp_allow_lds(kp, once, err) != hipSuccess) return err;
-    const size_t lds = (size_t)wbytes + 2 * (size_t)a.chunk_rows * 4 + 16;
+    const size_t lds = (size_t)wbytes + 6 * (size_t)a.chunk_rows + 16;
     const unsigned chunks = (unsigned)((a.n_rows + a.chunk_rows - 1) / a.chunk_rows);
     hipLaunchKernelGGL(kp, dim3(chunks, (unsigned)(a.K - 1)), dim3(kPairThreads), lds, stream, a);
     const hipError_t e = hipGetLastError();
