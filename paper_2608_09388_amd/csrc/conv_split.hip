@@ -366,7 +366,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArg
   // entry is loaded again).
   int32_t sv[BPW][JQ];
   i32x4 af[BPW][KS];
-  auto issue = [&](int64_t task) {
+  auto issue_into = [&](int64_t task, int32_t (&svx)[BPW][JQ], i32x4 (&afx)[BPW][KS]) {
 #pragma unroll
     for (int u = 0; u < BPW; ++u) {
       const int64_t row = row_of(task, u);
@@ -375,11 +375,17 @@ __global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArg
       for (int q = 0; q < JQ; ++q) {
         const int jq = g + 4 * q;
         const int jc = jq < K ? jq : K - 1;
-        sv[u][q] = valid ? a.table[(int64_t)jc * n + row] : -1;
+        svx[u][q] = valid ? a.table[(int64_t)jc * n + row] : -1;
       }
-      load_s(valid ? row : -1, af[u]);
+      load_s(valid ? row : -1, afx[u]);
     }
   };
+  auto issue = [&](int64_t task) { issue_into(task, sv, af); };
+  // With the SIMD's whole register file (MINW = 1) the next task's loads go
+  // out before this task waits for its partial rows, into a second set.
+  constexpr bool kEarly = MINW == 1;
+  int32_t svn[kEarly ? BPW : 1][JQ];
+  i32x4 afn[kEarly ? BPW : 1][KS];
 
   int64_t task = (int64_t)blockIdx.x * NW + wave;
   SW::load(a.W, 0, tid, wbuf);
@@ -421,6 +427,7 @@ __global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArg
       return ((uint32_t)(j - 1) * (uint32_t)n + (uint32_t)r) * (uint32_t)(Cout * 4) +
              (uint32_t)g * 16u;
     };
+    const bool more = task + stride < ntask;
     auto load_p = [&](int j, int64_t r, f32x4 (&c)[NCT]) {
       const uint32_t off = j > 0 ? p_off(j, r) : 0u;
 #pragma unroll
@@ -439,6 +446,9 @@ __global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArg
       load_p(sp ? __builtin_ctz(sp) : 0, row[u], acc[u]);
       load_p(sp2 ? __builtin_ctz(sp2) : 0, row[u], c2[u]);
       rest[u] = sp2 & (sp2 - 1u);
+    }
+    if constexpr (kEarly) {
+      if (more) issue_into(task + stride, svn, afn);
     }
 #pragma unroll
     for (int ct = 0; ct < NCT; ++ct) {
@@ -466,8 +476,21 @@ __global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArg
       return __builtin_bit_cast(bf16x8, af[u][ks]);
     });
 
-    // the next task's loads go out before this one's stores
-    if (task + stride < ntask) issue(task + stride);
+    // the next task's loads go out before this one's stores (or went out
+    // already, into the second set)
+    if constexpr (kEarly) {
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < BPW; ++u) {
+#pragma unroll
+          for (int q = 0; q < JQ; ++q) sv[u][q] = svn[u][q];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) af[u][ks] = afn[u][ks];
+        }
+      }
+    } else if (more) {
+      issue(task + stride);
+    }
 
     // activation, bf16 (round to nearest even), 8 bytes per lane and block
     const bool relu = a.relu != 0;
@@ -548,7 +571,7 @@ hipError_t launch_split_k(const SplitArgs& a0, int num_cus, hipStream_t stream) 
     if (e != hipSuccess) return e;
   }
   constexpr int NW = big ? 4 : 8;
-  constexpr int B3 = KS * NCT >= 128 ? 1 : kRowsBlocks;  // K <= 12
+  constexpr int B3 = (KS * NCT >= 128 || (NCT >= 16 && KS >= 4)) ? 1 : kRowsBlocks;  // K <= 12
   constexpr int B8 = KS * NCT >= 32 ? 1 : kRowsBlocks;   // K > 12
   const int BPW = a.K <= 12 ? B3 : B8;
   const int64_t tasks = (a.n_rows + 16 * BPW - 1) / (16 * BPW);
