@@ -181,8 +181,25 @@ __device__ __forceinline__ int sp_lanes_below(uint64_t bal) {
 }
 
 // ---------------------------------------------------------------------------
-// pair launch: grid (chunks, K - 1), workgroup (chunk c, slot j = 1 + y)
+// pair launch: grid (chunks, K - 1), workgroup (chunk c, slot j = 1 + y).
+// Wavefront w owns a quarter of the output columns: it reads its weight
+// fragments of W[j] from LDS once, into registers, and then takes every job
+// of the workgroup for those columns.  A job's 16 neighbour rows are staged
+// in LDS once for the four wavefronts, kPairBatch jobs at a time and double
+// buffered (the next batch's rows in flight in registers while one batch
+// computes); the weights' LDS region holds the staging buffers once the
+// fragments are in registers.
 // ---------------------------------------------------------------------------
+constexpr int kPairBatch = 4;  // jobs staged per barrier
+
+__host__ __device__ constexpr int sp_stage_row(int cin) { return cin * 2 + 16; }
+__host__ __device__ constexpr int sp_pair_region(int cin, int cout) {
+  // the slot's weights, or two staging buffers of kPairBatch jobs, the larger
+  return cin * cout * 2 > 2 * kPairBatch * 16 * sp_stage_row(cin)
+             ? cin * cout * 2
+             : 2 * kPairBatch * 16 * sp_stage_row(cin);
+}
+
 // (MINW: wavefronts per SIMD the registers must allow; one when a slot's
 // weights take most of the LDS, so that only one workgroup fits a CU anyway)
 template <int KS, int NCT, int MINW>
@@ -192,15 +209,22 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
   using SW = SlotWeights<KS, NCT, NT>;
   constexpr int Cin = SW::Cin;
   constexpr int Cout = SW::Cout;
+  constexpr int NCTW = NCT / NW;                 // column blocks per wavefront
+  static_assert(NCT % NW == 0, "whole column blocks per wavefront");
+  constexpr int SROW = sp_stage_row(Cin);        // staged row, padded by 16 bytes
+  constexpr int SBUF = kPairBatch * 16 * SROW;   // one staging buffer
+  constexpr int VPRow = Cin * 2 / 16;            // 16-byte vectors per row
+  constexpr int SV = kPairBatch * 16 * VPRow / NT;  // staged vectors per thread
+  static_assert((kPairBatch * 16 * VPRow) % NT == 0, "whole staged vectors per thread");
 
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int rc = a.chunk_rows;
-  unsigned char* wbuf = smem;                                        // W[j]
+  unsigned char* region = smem;  // W[j], then the staging buffers
   // pair lists: neighbour rows, then the rows themselves relative to the
   // chunk (16 bits: rc <= kMaxChunkRows), then the count
-  int32_t* srcl = reinterpret_cast<int32_t*>(smem + SW::bytes);     // [rc]
-  uint16_t* dstl = reinterpret_cast<uint16_t*>(srcl + rc);           // [rc]
-  int32_t* cnt = reinterpret_cast<int32_t*>(dstl + ((rc + 1) & ~1)); // pairs listed
+  int32_t* srcl = reinterpret_cast<int32_t*>(smem + sp_pair_region(Cin, Cout));  // [rc]
+  uint16_t* dstl = reinterpret_cast<uint16_t*>(srcl + rc);                        // [rc]
+  int32_t* cnt = reinterpret_cast<int32_t*>(dstl + ((rc + 1) & ~1));              // pairs
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -212,7 +236,7 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
   const int64_t row0 = (int64_t)blockIdx.x * rc;
   const int nrows = (int)min((int64_t)rc, n - row0);
 
-  SW::load(a.W, j, tid, wbuf);
+  SW::load(a.W, j, tid, region);
   if (tid == 0) *cnt = 0;
   // the chunk's slot-j entries, all in flight at once (rc <= kMaxChunkRows)
   const int32_t* tj = a.table + (int64_t)j * n + row0;
@@ -224,6 +248,13 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
   }
   __builtin_amdgcn_s_waitcnt(0);  // the direct weight loads and the entries are in
   sp_lds_barrier();
+
+  // this wavefront's weight fragments, for good
+  bf16x8 wreg[KS][NCTW];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int c = 0; c < NCTW; ++c) wreg[ks][c] = SW::read(region, ks, wave * NCTW + c, g, l16);
 
   // the present pairs (list order is immaterial: every pair's partial row is
   // computed on its own and stored by row): one LDS atomic per wavefront
@@ -247,9 +278,12 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
     }
     base += (int)__popcll(bal[u]);
   }
+  // the lists are complete and every wavefront's fragments are read: the
+  // weights' region becomes the staging buffers
+  __builtin_amdgcn_s_waitcnt(0);
   sp_lds_barrier();
   const int np = *cnt;
-  const int nj = (np + 15) >> 4;
+  const int nb = (np + kPairBatch * 16 - 1) / (kPairBatch * 16);  // batches of jobs
 
   const __amdgpu_buffer_rsrc_t s_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(a.S), (short)0, (int)(n * Cin * 2), kSpBufferWord3);
@@ -257,63 +291,72 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
   const __amdgpu_buffer_rsrc_t p_rsrc =
       __builtin_amdgcn_make_buffer_rsrc(pj, (short)0, (int)(n * Cout * 4), kSpBufferWord3);
 
-  // job q: pairs 16 q .. 16 q + 15; lane (g, i) loads k-group g of pair i
-  auto load_a = [&](int q, i32x4 (&af)[KS]) {
-    const int p = q * 16 + l16;
-    const int32_t src = p < np ? srcl[p] : -1;
-    const uint32_t off = (uint32_t)src * (uint32_t)(Cin * 2) + (uint32_t)g * 16u;
+  // batch b: pairs kPairBatch * 16 * b + r, r < kPairBatch * 16; staged
+  // vector v = u * NT + tid is row r = v / VPRow, 16 bytes c = v % VPRow
+  // (an absent pair's row reads zeros)
+  i32x4 sreg[SV];
+  auto load_batch = [&](int b) {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      af[ks] = __builtin_bit_cast(
+    for (int u = 0; u < SV; ++u) {
+      const int v = u * NT + tid;
+      const int r = v / VPRow, c = v - (v / VPRow) * VPRow;
+      const int p = b * kPairBatch * 16 + r;
+      const int32_t src = p < np ? srcl[p] : -1;
+      sreg[u] = __builtin_bit_cast(
           i32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                     s_rsrc, src >= 0 ? off + (uint32_t)ks * 64u : kSpOutOfRange, 0, 0));
-  };
-  // jobs q and q + NW together: every weight fragment read from LDS feeds
-  // both (a job past the last has no pairs: zero rows, nothing stored)
-  auto jobs2 = [&](int q, const i32x4 (&fa)[KS], const i32x4 (&fb)[KS]) {
-    f32x4 acc[2][NCT];
-#pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) {
-      acc[0][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-      acc[1][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
+                     s_rsrc,
+                     src >= 0 ? (uint32_t)src * (uint32_t)(Cin * 2) + (uint32_t)c * 16u
+                              : kSpOutOfRange,
+                     0, 0));
     }
-    sp_mfma_sweep<KS, NCT, NT, MINW == 1, 2>(wbuf, g, l16, acc, [&](int b, int ks) {
-      return __builtin_bit_cast(bf16x8, b == 0 ? fa[ks] : fb[ks]);
-    });
+  };
+  auto store_batch = [&](int buf) {
+    unsigned char* dst = region + buf * SBUF;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int p = (q + h * NW) * 16 + l16;
+    for (int u = 0; u < SV; ++u) {
+      const int v = u * NT + tid;
+      const int r = v / VPRow, c = v - (v / VPRow) * VPRow;
+      *reinterpret_cast<i32x4*>(dst + r * SROW + c * 16) = sreg[u];
+    }
+  };
+  auto compute_batch = [&](int b, int buf) {
+    const unsigned char* rows = region + buf * SBUF;
+#pragma unroll
+    for (int jj = 0; jj < kPairBatch; ++jj) {
+      // B operand of k-step ks: 16 bytes of staged row jj * 16 + i, k-group g
+      const unsigned char* rp = rows + (jj * 16 + l16) * SROW + g * 16;
+      f32x4 acc[NCTW];
+#pragma unroll
+      for (int c = 0; c < NCTW; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 sf = *reinterpret_cast<const bf16x8*>(rp + ks * 64);
+#pragma unroll
+        for (int c = 0; c < NCTW; ++c)
+          acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wreg[ks][c], sf, acc[c], 0, 0, 0);
+      }
+      const int p = (b * kPairBatch + jj) * 16 + l16;
       const int32_t dst = p < np ? (int32_t)(row0 + dstl[p]) : -1;
-      const uint32_t off = (uint32_t)dst * (uint32_t)(Cout * 4) + (uint32_t)g * 16u;
+      const uint32_t off = (uint32_t)dst * (uint32_t)(Cout * 4) +
+                           (uint32_t)(wave * NCTW) * 64u + (uint32_t)g * 16u;
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct)
+      for (int c = 0; c < NCTW; ++c)
         __builtin_amdgcn_raw_buffer_store_b128(
-            __builtin_bit_cast(sp_v4u32, acc[h][ct]), p_rsrc,
-            dst >= 0 ? off + (uint32_t)ct * 64u : kSpOutOfRange, 0, 0);
+            __builtin_bit_cast(sp_v4u32, acc[c]), p_rsrc,
+            dst >= 0 ? off + (uint32_t)c * 64u : kSpOutOfRange, 0, 0);
     }
   };
 
-  // a wavefront takes jobs wave, wave + NW, ... two at a time; the next two
-  // jobs' rows are in flight while two compute
-  i32x4 a0[KS], a1[KS], b0[KS], b1[KS];
-  int q = wave;
-  if (q < nj) {
-    load_a(q, a0);
-    load_a(q + NW, a1);
+  if (nb > 0) {
+    load_batch(0);
+    store_batch(0);
+    sp_lds_barrier();
   }
-  for (; q < nj; q += 4 * NW) {
-    const bool more = q + 2 * NW < nj;
-    if (more) {
-      load_a(q + 2 * NW, b0);
-      load_a(q + 3 * NW, b1);
-    }
-    jobs2(q, a0, a1);
-    if (!more) break;
-    if (q + 4 * NW < nj) {
-      load_a(q + 4 * NW, a0);
-      load_a(q + 5 * NW, a1);
-    }
-    jobs2(q + 2 * NW, b0, b1);
+  for (int b = 0; b < nb; ++b) {
+    if (b + 1 < nb) load_batch(b + 1);
+    compute_batch(b, b & 1);
+    if (b + 1 < nb) store_batch((b + 1) & 1);
+    sp_lds_barrier();
   }
 }
 
@@ -532,15 +575,15 @@ int split_wgs_per_cu(bool big) { return big ? 1 : 2; }
 
 // Rows per pair workgroup: about split_wgs_per_cu workgroups per CU over the
 // K - 1 slots, a multiple of 64, within one pass of the table loads and the
-// LDS left beside the weights.
-int split_chunk_rows(int64_t n, int32_t K, int num_cus, int wbytes, bool big) {
+// LDS left beside the weights / staging region (`region` bytes).
+int split_chunk_rows(int64_t n, int32_t K, int num_cus, int region, bool big) {
   const int64_t slots = K > 1 ? K - 1 : 1;
   const int64_t wgs = (int64_t)num_cus * split_wgs_per_cu(big);
   int64_t chunks = (wgs + slots - 1) / slots;
   if (chunks < 1) chunks = 1;
   int64_t rc = (n + chunks - 1) / chunks;
   rc = (rc + 63) / 64 * 64;
-  const int64_t lds_rows = ((kSpLdsLimit - wbytes - 16) / 6) / 64 * 64;
+  const int64_t lds_rows = ((kSpLdsLimit - region - 16) / 6) / 64 * 64;
   if (rc > lds_rows) rc = lds_rows;
   if (rc > kMaxChunkRows) rc = kMaxChunkRows;
   if (rc < 64) rc = 64;
@@ -559,12 +602,13 @@ hipError_t launch_split_k(const SplitArgs& a0, int num_cus, hipStream_t stream) 
   constexpr bool big = split_big(wbytes, NCT);
   constexpr int MINW = big ? 1 : 2;
   if (a.K > 1) {
-    a.chunk_rows = split_chunk_rows(a.n_rows, a.K, num_cus, wbytes, big);
+    a.chunk_rows = split_chunk_rows(a.n_rows, a.K, num_cus, sp_pair_region(KS * 32, NCT * 16),
+                                    big);
     auto kp = conv_pairs_kernel<KS, NCT, MINW>;
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     if (sp_allow_lds(kp, once, err) != hipSuccess) return err;
-    const size_t lds = (size_t)wbytes + 6 * (size_t)a.chunk_rows + 16;
+    const size_t lds = (size_t)sp_pair_region(KS * 32, NCT * 16) + 6 * (size_t)a.chunk_rows + 16;
     const unsigned chunks = (unsigned)((a.n_rows + a.chunk_rows - 1) / a.chunk_rows);
     hipLaunchKernelGGL(kp, dim3(chunks, (unsigned)(a.K - 1)), dim3(kPairThreads), lds, stream, a);
     const hipError_t e = hipGetLastError();
