@@ -51,7 +51,6 @@ constexpr int kPairThreads = 256;
 constexpr int kPairLoads = 24;                               // table loads per thread
 constexpr int kMaxChunkRows = kPairLoads * kPairThreads;     // one pass over a chunk
 static_assert(kMaxChunkRows <= 65536, "chunk rows fit the 16-bit pair lists");
-constexpr int kRowsBlocks = 2;                               // 16-row blocks per wavefront
 #define SHC_SP_LDS __attribute__((address_space(3)))
 
 typedef __bf16 sp_bf16x4 __attribute__((__vector_size__(4 * sizeof(__bf16))));
@@ -107,10 +106,12 @@ struct SlotWeights {
   // q's chunk swizzled to p's (the XOR is its own inverse).  A wavefront's
   // load writes 64 consecutive vectors; the caller waits for its own loads
   // (s_waitcnt) before the barrier that publishes them.
-  __device__ static void load(const void* W, int j, int tid, unsigned char* wbuf) {
-    const unsigned char* src = static_cast<const unsigned char*>(W) + (int64_t)j * bytes;
+  __device__ static void load(const void* W, int j, int tid, unsigned char* wbuf,
+                              int k0 = 0, int kr = Cin) {
+    const unsigned char* src =
+        static_cast<const unsigned char*>(W) + (int64_t)j * bytes + (int64_t)k0 * WROW;
     const int lane = tid & 63;
-    for (int c = tid >> 6; c < VECS / 64; c += NT / 64) {
+    for (int c = tid >> 6; c < kr * VPR / 64; c += NT / 64) {
       const int v = c * 64 + lane;
       const int k = v / VPR;
       const int p = v - k * VPR;
@@ -361,20 +362,44 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
 }
 
 // ---------------------------------------------------------------------------
-// row launch: NW wavefronts per workgroup; a wavefront's task is BPW
-// consecutive 16-row blocks (every weight fragment read from LDS serves all
-// of them), tasks handed out grid-stride; JQ table entries per lane and
-// block (lane (g, i) reads slots g, g + 4, ... of row i)
+// row launch: four wavefronts per workgroup, wavefront w owning a quarter of
+// the output columns with its weight fragments of W[0] in registers for the
+// whole launch.  Workgroups walk batches of kRowBatch 16-row blocks,
+// grid-stride; a batch's input rows are staged in LDS once for the four
+// wavefronts (the next batch's rows and table entries in flight while one
+// computes), each wavefront loads its own columns of the rows' partial rows.
+// JQ table entries per lane and block (lane (g, i) reads slots g, g + 4, ...
+// of row i).
 // ---------------------------------------------------------------------------
-template <int KS, int NCT, int NW, int BPW, int JQ, int MINW>
-__global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArgs a) {
-  constexpr int NT = 64 * NW;
+constexpr int kRowBatch = 4;  // 16-row blocks per batch (two for big shapes)
+
+__host__ __device__ constexpr int sp_row_region(int cin, int cout, int rb, int wp) {
+  // a slice of W[0], or two staging buffers of a batch's rows, the larger
+  return cin * cout * 2 / wp > 2 * rb * 16 * sp_stage_row(cin) ? cin * cout * 2 / wp
+                                                               : 2 * rb * 16 * sp_stage_row(cin);
+}
+
+// RB: 16-row blocks per batch; WP: parts W[0] is staged in (its rows in WP
+// slices of Cin / WP), so that the LDS a workgroup holds is the larger of a
+// slice and the two staging buffers.
+template <int KS, int NCT, int JQ, int MINW, int RB, int WP>
+__global__ __launch_bounds__(kPairThreads, MINW) void conv_rows_kernel(const SplitArgs a) {
+  constexpr int NT = kPairThreads;
+  constexpr int NW = NT / 64;
   using SW = SlotWeights<KS, NCT, NT>;
   constexpr int Cin = SW::Cin;
   constexpr int Cout = SW::Cout;
+  constexpr int NCTW = NCT / NW;
+  static_assert(NCT % NW == 0, "whole column blocks per wavefront");
+  static_assert(KS % WP == 0, "whole k-steps per slice of W[0]");
+  constexpr int SROW = sp_stage_row(Cin);
+  constexpr int SBUF = RB * 16 * SROW;
+  constexpr int VPRow = Cin * 2 / 16;
+  constexpr int SV = RB * 16 * VPRow / NT;  // staged vectors per thread
+  static_assert((RB * 16 * VPRow) % NT == 0, "whole staged vectors per thread");
 
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  unsigned char* wbuf = smem;  // W[0]
+  unsigned char* region = smem;  // W[0], then the staging buffers
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -383,8 +408,8 @@ __global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArg
   const int l16 = lane & 15;
   const int64_t n = a.n_rows;
   const int K = a.K;
-  const int64_t ntask = (n + 16 * BPW - 1) / (16 * BPW);
-  const int64_t stride = (int64_t)gridDim.x * NW;
+  const int64_t nbatch = (n + RB * 16 - 1) / (RB * 16);
+  const int64_t stride = gridDim.x;
 
   const __amdgpu_buffer_rsrc_t s_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<void*>(a.S), (short)0, (int)(n * Cin * 2), kSpBufferWord3);
@@ -392,169 +417,205 @@ __global__ __launch_bounds__(64 * NW, MINW) void conv_rows_kernel(const SplitArg
       a.P, (short)0, (int)((int64_t)(K > 1 ? K - 1 : 1) * n * Cout * 4), kSpBufferWord3);
   const __amdgpu_buffer_rsrc_t o_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       a.out, (short)0, (int)(n * Cout * 2), kSpBufferWord3);
-  auto load_s = [&](int64_t src, i32x4 (&af)[KS]) {
-    const uint32_t off = (uint32_t)src * (uint32_t)(Cin * 2) + (uint32_t)g * 16u;
+
+  // this wavefront's weight fragments of W[0], for good, a slice of W[0]'s
+  // rows at a time through LDS
+  bf16x8 wreg[KS][NCTW];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      af[ks] = __builtin_bit_cast(
-          i32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                     s_rsrc, src >= 0 ? off + (uint32_t)ks * 64u : kSpOutOfRange, 0, 0));
-  };
-  auto row_of = [&](int64_t task, int u) -> int64_t {
-    return task * (16 * BPW) + u * 16 + l16;
-  };
-  // A task's loads that need no table entry go out first: its table entries
-  // and each row's own input row, which is slot 0's neighbour row in a
-  // spiral or k-NN table (checked once the entries are in; any other slot-0
-  // entry is loaded again).
-  int32_t sv[BPW][JQ];
-  i32x4 af[BPW][KS];
-  auto issue_into = [&](int64_t task, int32_t (&svx)[BPW][JQ], i32x4 (&afx)[BPW][KS]) {
+  for (int wp = 0; wp < WP; ++wp) {
+    constexpr int KSP = KS / WP;  // k-steps per slice
+    SW::load(a.W, 0, tid, region, wp * KSP * 32, KSP * 32);
+    __builtin_amdgcn_s_waitcnt(0);
+    sp_lds_barrier();
 #pragma unroll
-    for (int u = 0; u < BPW; ++u) {
-      const int64_t row = row_of(task, u);
+    for (int ks = 0; ks < KSP; ++ks)
+#pragma unroll
+      for (int c = 0; c < NCTW; ++c)
+        wreg[wp * KSP + ks][c] = SW::read(region, ks, wave * NCTW + c, g, l16);
+    sp_lds_barrier();  // the slice's fragments are read: the region is free again
+  }
+
+  // A batch's table entries (this lane's row of each block) and input rows.
+  // The rows are staged as each row's own input row, which is slot 0's
+  // neighbour row in a spiral or k-NN table; a block whose table says
+  // otherwise reads its slot-0 rows from memory instead.
+  int32_t sv[RB][JQ];
+  i32x4 sreg[SV];
+  auto load_entries = [&](int64_t b) {
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+      const int64_t row = (b * RB + u) * 16 + l16;
       const bool valid = row < n;
 #pragma unroll
       for (int q = 0; q < JQ; ++q) {
         const int jq = g + 4 * q;
         const int jc = jq < K ? jq : K - 1;
-        svx[u][q] = valid ? a.table[(int64_t)jc * n + row] : -1;
+        sv[u][q] = valid ? a.table[(int64_t)jc * n + row] : -1;
       }
-      load_s(valid ? row : -1, afx[u]);
     }
   };
-  auto issue = [&](int64_t task) { issue_into(task, sv, af); };
-  // With the SIMD's whole register file (MINW = 1) the next task's loads go
-  // out before this task waits for its partial rows, into a second set.
-  constexpr bool kEarly = MINW == 1;
-  int32_t svn[kEarly ? BPW : 1][JQ];
-  i32x4 afn[kEarly ? BPW : 1][KS];
-
-  int64_t task = (int64_t)blockIdx.x * NW + wave;
-  SW::load(a.W, 0, tid, wbuf);
-  if (task < ntask) issue(task);
-  __builtin_amdgcn_s_waitcnt(0);  // the direct weight loads (and the first task's) are in
-  sp_lds_barrier();
-
-  for (; task < ntask; task += stride) {
-    int64_t row[BPW];
-    bool valid[BPW];
-    uint32_t m[BPW];
+  auto load_rows = [&](int64_t b) {
 #pragma unroll
-    for (int u = 0; u < BPW; ++u) {
-      row[u] = row_of(task, u);
-      valid[u] = row[u] < n;
-      // present-slot mask and slot 0's row
+    for (int u = 0; u < SV; ++u) {
+      const int v = u * NT + tid;
+      const int r = v / VPRow, c = v - (v / VPRow) * VPRow;
+      const int64_t row = b * RB * 16 + r;
+      sreg[u] = __builtin_bit_cast(
+          i32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     s_rsrc,
+                     row < n ? (uint32_t)row * (uint32_t)(Cin * 2) + (uint32_t)c * 16u
+                             : kSpOutOfRange,
+                     0, 0));
+    }
+  };
+  auto store_rows = [&](int buf) {
+    unsigned char* dst = region + buf * SBUF;
+#pragma unroll
+    for (int u = 0; u < SV; ++u) {
+      const int v = u * NT + tid;
+      const int r = v / VPRow, c = v - (v / VPRow) * VPRow;
+      *reinterpret_cast<i32x4*>(dst + r * SROW + c * 16) = sreg[u];
+    }
+  };
+  // this wavefront's columns of partial row P[j][r] (zeros for j = 0)
+  auto load_p = [&](int j, int64_t r, f32x4 (&c)[NCTW]) {
+    const uint32_t off = j > 0 ? ((uint32_t)(j - 1) * (uint32_t)n + (uint32_t)r) *
+                                         (uint32_t)(Cout * 4) +
+                                     (uint32_t)(wave * NCTW) * 64u + (uint32_t)g * 16u
+                               : 0u;
+#pragma unroll
+    for (int q = 0; q < NCTW; ++q)
+      c[q] = __builtin_bit_cast(
+          f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     p_rsrc, j > 0 ? off + (uint32_t)q * 64u : kSpOutOfRange, 0, 0));
+  };
+
+  int64_t b = blockIdx.x;
+  if (b < nbatch) {
+    load_entries(b);
+    load_rows(b);
+    store_rows(0);
+  }
+  sp_lds_barrier();
+  int buf = 0;
+  const bool relu = a.relu != 0;
+  for (; b < nbatch; b += stride) {
+    // present-slot masks and slot-0 rows of the batch's blocks
+    int64_t row[RB];
+    uint32_t m[RB];
+    int32_t s0[RB];
+    bool staged[RB];
+#pragma unroll
+    for (int u = 0; u < RB; ++u) {
+      row[u] = (b * RB + u) * 16 + l16;
       m[u] = 0;
-      int32_t s0 = -1;
+      s0[u] = -1;
 #pragma unroll
       for (int q = 0; q < JQ; ++q) {
         const int jq = g + 4 * q;
         const bool ok = jq < K && (uint32_t)sv[u][q] < (uint32_t)n;
         m[u] |= (ok ? 1u : 0u) << jq;
-        if (q == 0) s0 = ok ? sv[u][0] : -1;
+        if (q == 0) s0[u] = ok ? sv[u][0] : -1;
       }
       m[u] |= (uint32_t)__shfl_xor((int)m[u], 16);
       m[u] |= (uint32_t)__shfl_xor((int)m[u], 32);
-      s0 = __shfl(s0, l16);  // from lane (0, i)
-      if (__ballot(valid[u] && s0 != row[u]) != 0) load_s(s0, af[u]);
+      s0[u] = __shfl(s0[u], l16);  // from lane (0, i)
+      staged[u] = __ballot(row[u] < n && s0[u] != row[u]) == 0;
     }
-
-    // Accumulators: the first present slot j >= 1's partial row loaded into
-    // them (zeros when there is none), plus the bias, plus the second present
-    // slot's partial row (loaded beside the first); then any further present
-    // slots of the row in order, one whole partial row per round trip, for as
-    // many rounds as the wavefront's row with the most of them needs.  Adding
-    // an absent slot's zeros changes nothing.
-    auto p_off = [&](int j, int64_t r) -> uint32_t {
-      return ((uint32_t)(j - 1) * (uint32_t)n + (uint32_t)r) * (uint32_t)(Cout * 4) +
-             (uint32_t)g * 16u;
-    };
-    const bool more = task + stride < ntask;
-    auto load_p = [&](int j, int64_t r, f32x4 (&c)[NCT]) {
-      const uint32_t off = j > 0 ? p_off(j, r) : 0u;
+    // accumulators: first present slot j >= 1's partial row, plus the bias,
+    // plus the second one (loaded beside the first); then any further ones
+    f32x4 acc[RB][NCTW], c2[RB][NCTW];
+    uint32_t rest[RB];
 #pragma unroll
-      for (int ct = 0; ct < NCT; ++ct)
-        c[ct] = __builtin_bit_cast(
-            f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                       p_rsrc, j > 0 ? off + (uint32_t)ct * 64u : kSpOutOfRange, 0, 0));
-    };
-    f32x4 acc[BPW][NCT];
-    f32x4 c2[BPW][NCT];
-    uint32_t rest[BPW];
-#pragma unroll
-    for (int u = 0; u < BPW; ++u) {
+    for (int u = 0; u < RB; ++u) {
       const uint32_t sp = m[u] & ~1u;
       const uint32_t sp2 = sp & (sp - 1u);
       load_p(sp ? __builtin_ctz(sp) : 0, row[u], acc[u]);
       load_p(sp2 ? __builtin_ctz(sp2) : 0, row[u], c2[u]);
       rest[u] = sp2 & (sp2 - 1u);
     }
-    if constexpr (kEarly) {
-      if (more) issue_into(task + stride, svn, afn);
+    // the next batch's entries and rows go out now
+    const bool more = b + stride < nbatch;
+    if (more) {
+      load_entries(b + stride);
+      load_rows(b + stride);
     }
 #pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) {
-      f32x4 b = {0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < NCTW; ++q) {
+      const int col = (wave * NCTW + q) * 16 + 4 * g;
+      f32x4 bv = {0.f, 0.f, 0.f, 0.f};
       if (a.bias != nullptr)
-        b = f32x4{a.bias[ct * 16 + 4 * g], a.bias[ct * 16 + 4 * g + 1],
-                  a.bias[ct * 16 + 4 * g + 2], a.bias[ct * 16 + 4 * g + 3]};
+        bv = f32x4{a.bias[col], a.bias[col + 1], a.bias[col + 2], a.bias[col + 3]};
 #pragma unroll
-      for (int u = 0; u < BPW; ++u) acc[u][ct] = (acc[u][ct] + b) + c2[u][ct];
+      for (int u = 0; u < RB; ++u) acc[u][q] = (acc[u][q] + bv) + c2[u][q];
     }
+    // (all blocks' next further slots in one round trip per round)
+    uint32_t any = 0;
 #pragma unroll
-    for (int u = 0; u < BPW; ++u) {
-      uint32_t v = rest[u];
-      while (__ballot(v != 0) != 0) {
-        f32x4 c[NCT];
-        load_p(v != 0 ? __builtin_ctz(v) : 0, row[u], c);
+    for (int u = 0; u < RB; ++u) any |= rest[u];
+    while (__ballot(any != 0) != 0) {
+      f32x4 c[RB][NCTW];
 #pragma unroll
-        for (int ct = 0; ct < NCT; ++ct) acc[u][ct] += c[ct];
-        v &= v - 1u;
+      for (int u = 0; u < RB; ++u) load_p(rest[u] != 0 ? __builtin_ctz(rest[u]) : 0, row[u], c[u]);
+      any = 0;
+#pragma unroll
+      for (int u = 0; u < RB; ++u) {
+#pragma unroll
+        for (int q = 0; q < NCTW; ++q) acc[u][q] += c[u][q];
+        rest[u] &= rest[u] - 1u;
+        any |= rest[u];
       }
     }
 
-    // slot 0 on the matrix cores, each weight fragment serving every block
-    sp_mfma_sweep<KS, NCT, NT, MINW == 1, BPW>(wbuf, g, l16, acc, [&](int u, int ks) {
-      return __builtin_bit_cast(bf16x8, af[u][ks]);
-    });
-
-    // the next task's loads go out before this one's stores (or went out
-    // already, into the second set)
-    if constexpr (kEarly) {
-      if (more) {
+    // slot 0 on the matrix cores: B operands from the staged rows, or from
+    // memory for a block whose slot 0 is not the row itself
+    const unsigned char* rows = region + buf * SBUF;
 #pragma unroll
-        for (int u = 0; u < BPW; ++u) {
+    for (int u = 0; u < RB; ++u) {
+      if (staged[u]) {
+        const unsigned char* rp = rows + (u * 16 + l16) * SROW + g * 16;
 #pragma unroll
-          for (int q = 0; q < JQ; ++q) sv[u][q] = svn[u][q];
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 sf = *reinterpret_cast<const bf16x8*>(rp + ks * 64);
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks) af[u][ks] = afn[u][ks];
+          for (int q = 0; q < NCTW; ++q)
+            acc[u][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wreg[ks][q], sf, acc[u][q], 0, 0,
+                                                                0);
+        }
+      } else {
+        const uint32_t off = (uint32_t)s0[u] * (uint32_t)(Cin * 2) + (uint32_t)g * 16u;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 sf = __builtin_bit_cast(
+              bf16x8, __builtin_amdgcn_raw_buffer_load_b128(
+                          s_rsrc, s0[u] >= 0 ? off + (uint32_t)ks * 64u : kSpOutOfRange, 0, 0));
+#pragma unroll
+          for (int q = 0; q < NCTW; ++q)
+            acc[u][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wreg[ks][q], sf, acc[u][q], 0, 0,
+                                                                0);
         }
       }
-    } else if (more) {
-      issue(task + stride);
-    }
-
-    // activation, bf16 (round to nearest even), 8 bytes per lane and block
-    const bool relu = a.relu != 0;
+      // activation, bf16 (round to nearest even), 8 bytes per lane and block
+      const uint32_t ooff = (uint32_t)row[u] * (uint32_t)(Cout * 2) +
+                            (uint32_t)(wave * NCTW) * 32u + (uint32_t)g * 8u;
 #pragma unroll
-    for (int u = 0; u < BPW; ++u) {
-      const uint32_t ooff = (uint32_t)row[u] * (uint32_t)(Cout * 2) + (uint32_t)g * 8u;
-#pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
+      for (int q = 0; q < NCTW; ++q) {
         float v[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float x = acc[u][ct][r];
+          const float x = acc[u][q][r];
           v[r] = relu ? (x > 0.f ? x : 0.f) : x;
         }
         const sp_bf16x2 h0 = __builtin_convertvector(sp_f32x2{v[0], v[1]}, sp_bf16x2);
         const sp_bf16x2 h1 = __builtin_convertvector(sp_f32x2{v[2], v[3]}, sp_bf16x2);
         const sp_v2u32 w = {__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1)};
         __builtin_amdgcn_raw_buffer_store_b64(
-            w, o_rsrc, valid[u] ? ooff + (uint32_t)ct * 32u : kSpOutOfRange, 0, 0);
+            w, o_rsrc, row[u] < n ? ooff + (uint32_t)q * 32u : kSpOutOfRange, 0, 0);
       }
     }
+    if (more) store_rows(buf ^ 1);
+    sp_lds_barrier();
+    buf ^= 1;
   }
 }
 
@@ -590,50 +651,48 @@ int split_chunk_rows(int64_t n, int32_t K, int num_cus, int region, bool big) {
   return (int)rc;
 }
 
-// For big shapes one workgroup of either launch fits a CU: the row
-// workgroups then have four wavefronts, one per SIMD with the SIMD's whole
-// register file.  Two 16-row blocks per wavefront while their accumulators,
-// first two partial rows, input rows and table entries fit the registers,
-// else one.
+// For big shapes one workgroup of either launch fits a CU (the LDS of one
+// slot's weights, or the registers of a quarter of 256 columns' fragments).
 template <int KS, int NCT>
 hipError_t launch_split_k(const SplitArgs& a0, int num_cus, hipStream_t stream) {
   SplitArgs a = a0;
-  constexpr int wbytes = KS * 32 * NCT * 16 * 2;
+  constexpr int Cin = KS * 32, Cout = NCT * 16;
+  constexpr int wbytes = Cin * Cout * 2;
   constexpr bool big = split_big(wbytes, NCT);
   constexpr int MINW = big ? 1 : 2;
   if (a.K > 1) {
-    a.chunk_rows = split_chunk_rows(a.n_rows, a.K, num_cus, sp_pair_region(KS * 32, NCT * 16),
-                                    big);
+    a.chunk_rows = split_chunk_rows(a.n_rows, a.K, num_cus, sp_pair_region(Cin, Cout), big);
     auto kp = conv_pairs_kernel<KS, NCT, MINW>;
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     if (sp_allow_lds(kp, once, err) != hipSuccess) return err;
-    const size_t lds = (size_t)sp_pair_region(KS * 32, NCT * 16) + 6 * (size_t)a.chunk_rows + 16;
+    const size_t lds = (size_t)sp_pair_region(Cin, Cout) + 6 * (size_t)a.chunk_rows + 16;
     const unsigned chunks = (unsigned)((a.n_rows + a.chunk_rows - 1) / a.chunk_rows);
     hipLaunchKernelGGL(kp, dim3(chunks, (unsigned)(a.K - 1)), dim3(kPairThreads), lds, stream, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  constexpr int NW = big ? 4 : 8;
-  constexpr int B3 = (KS * NCT >= 128 || (NCT >= 16 && KS >= 4)) ? 1 : kRowsBlocks;  // K <= 12
-  constexpr int B8 = KS * NCT >= 32 ? 1 : kRowsBlocks;   // K > 12
-  const int BPW = a.K <= 12 ? B3 : B8;
-  const int64_t tasks = (a.n_rows + 16 * BPW - 1) / (16 * BPW);
-  int64_t grid = (tasks + NW - 1) / NW;
-  const int64_t cap = (int64_t)num_cus * split_wgs_per_cu(big);
+  // row workgroups: two per CU; for big shapes W[0] is staged in two slices
+  // and a batch has two blocks (one at 256 x 256: the fragments of a quarter
+  // of W[0] and a batch's accumulators then fill a wavefront's registers)
+  constexpr int RB = big ? (KS * NCT >= 128 ? 1 : 2) : kRowBatch, WP = big ? 2 : 1;
+  const int64_t batches = (a.n_rows + RB * 16 - 1) / (RB * 16);
+  int64_t grid = batches;
+  const int64_t cap = (int64_t)num_cus * 2;
   if (grid > cap) grid = cap;
+  const size_t lds = (size_t)sp_row_region(Cin, Cout, RB, WP);
   if (a.K <= 12) {
-    auto kr = conv_rows_kernel<KS, NCT, NW, B3, 3, MINW>;
+    auto kr = conv_rows_kernel<KS, NCT, 3, 2, RB, WP>;
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     if (sp_allow_lds(kr, once, err) != hipSuccess) return err;
-    hipLaunchKernelGGL(kr, dim3((unsigned)grid), dim3(64 * NW), (size_t)wbytes, stream, a);
+    hipLaunchKernelGGL(kr, dim3((unsigned)grid), dim3(kPairThreads), lds, stream, a);
   } else {
-    auto kr = conv_rows_kernel<KS, NCT, NW, B8, 8, MINW>;
+    auto kr = conv_rows_kernel<KS, NCT, 8, 2, RB, WP>;
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     if (sp_allow_lds(kr, once, err) != hipSuccess) return err;
-    hipLaunchKernelGGL(kr, dim3((unsigned)grid), dim3(64 * NW), (size_t)wbytes, stream, a);
+    hipLaunchKernelGGL(kr, dim3((unsigned)grid), dim3(kPairThreads), lds, stream, a);
   }
   return hipGetLastError();
 }
