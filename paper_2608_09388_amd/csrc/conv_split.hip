@@ -194,17 +194,18 @@ __device__ __forceinline__ int sp_lanes_below(uint64_t bal) {
 constexpr int kPairBatch = 4;  // jobs staged per barrier
 
 __host__ __device__ constexpr int sp_stage_row(int cin) { return cin * 2 + 16; }
-__host__ __device__ constexpr int sp_pair_region(int cin, int cout) {
-  // the slot's weights, or two staging buffers of kPairBatch jobs, the larger
-  return cin * cout * 2 > 2 * kPairBatch * 16 * sp_stage_row(cin)
-             ? cin * cout * 2
+__host__ __device__ constexpr int sp_pair_region(int cin, int cout, int wp) {
+  // a slice of the slot's weights, or two staging buffers of kPairBatch
+  // jobs, the larger
+  return cin * cout * 2 / wp > 2 * kPairBatch * 16 * sp_stage_row(cin)
+             ? cin * cout * 2 / wp
              : 2 * kPairBatch * 16 * sp_stage_row(cin);
 }
 
-// (MINW: wavefronts per SIMD the registers must allow; one when a slot's
-// weights take most of the LDS, so that only one workgroup fits a CU anyway)
-template <int KS, int NCT, int MINW>
-__global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const SplitArgs a) {
+// (WP: parts the slot's weights are staged in, a slice of Cin / WP rows at a
+// time, so that two workgroups fit a CU)
+template <int KS, int NCT, int WP>
+__global__ __launch_bounds__(kPairThreads, 2) void conv_pairs_kernel(const SplitArgs a) {
   constexpr int NT = kPairThreads;
   constexpr int NW = NT / 64;
   using SW = SlotWeights<KS, NCT, NT>;
@@ -223,7 +224,7 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
   unsigned char* region = smem;  // W[j], then the staging buffers
   // pair lists: neighbour rows, then the rows themselves relative to the
   // chunk (16 bits: rc <= kMaxChunkRows), then the count
-  int32_t* srcl = reinterpret_cast<int32_t*>(smem + sp_pair_region(Cin, Cout));  // [rc]
+  int32_t* srcl = reinterpret_cast<int32_t*>(smem + sp_pair_region(Cin, Cout, WP));  // [rc]
   uint16_t* dstl = reinterpret_cast<uint16_t*>(srcl + rc);                        // [rc]
   int32_t* cnt = reinterpret_cast<int32_t*>(dstl + ((rc + 1) & ~1));              // pairs
 
@@ -237,7 +238,9 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
   const int64_t row0 = (int64_t)blockIdx.x * rc;
   const int nrows = (int)min((int64_t)rc, n - row0);
 
-  SW::load(a.W, j, tid, region);
+  static_assert(KS % WP == 0, "whole k-steps per slice of the weights");
+  constexpr int KSP = KS / WP;  // k-steps per slice
+  SW::load(a.W, j, tid, region, 0, KSP * 32);
   if (tid == 0) *cnt = 0;
   // the chunk's slot-j entries, all in flight at once (rc <= kMaxChunkRows)
   const int32_t* tj = a.table + (int64_t)j * n + row0;
@@ -250,12 +253,22 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_pairs_kernel(const Sp
   __builtin_amdgcn_s_waitcnt(0);  // the direct weight loads and the entries are in
   sp_lds_barrier();
 
-  // this wavefront's weight fragments, for good
+  // this wavefront's weight fragments, for good, slice by slice
   bf16x8 wreg[KS][NCTW];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
+  for (int wp = 0; wp < WP; ++wp) {
+    if (wp > 0) {
+      sp_lds_barrier();  // the previous slice's fragments are read
+      SW::load(a.W, j, tid, region, wp * KSP * 32, KSP * 32);
+      __builtin_amdgcn_s_waitcnt(0);
+      sp_lds_barrier();
+    }
 #pragma unroll
-    for (int c = 0; c < NCTW; ++c) wreg[ks][c] = SW::read(region, ks, wave * NCTW + c, g, l16);
+    for (int ks = 0; ks < KSP; ++ks)
+#pragma unroll
+      for (int c = 0; c < NCTW; ++c)
+        wreg[wp * KSP + ks][c] = SW::read(region, ks, wave * NCTW + c, g, l16);
+  }
 
   // the present pairs (list order is immaterial: every pair's partial row is
   // computed on its own and stored by row): one LDS atomic per wavefront
@@ -628,18 +641,18 @@ hipError_t sp_allow_lds(Kern kern, std::once_flag& once, hipError_t& err) {
   return err;
 }
 
-// Workgroups of either launch that one CU holds at once: one for "big"
-// shapes (a slot's weights at 64 KB or more, or 256 output columns, whose
-// row blocks take a SIMD's whole register file), else two.
+// "Big" shapes (a slot's weights at 64 KB or more, or 256 output columns)
+// stage the weights in two slices; either launch then fits two workgroups
+// per CU.
 constexpr bool split_big(int wbytes, int nct) { return wbytes >= 64 * 1024 || nct >= 16; }
-int split_wgs_per_cu(bool big) { return big ? 1 : 2; }
+constexpr int kSplitWgsPerCu = 2;
 
-// Rows per pair workgroup: about split_wgs_per_cu workgroups per CU over the
+// Rows per pair workgroup: about kSplitWgsPerCu workgroups per CU over the
 // K - 1 slots, a multiple of 64, within one pass of the table loads and the
 // LDS left beside the weights / staging region (`region` bytes).
-int split_chunk_rows(int64_t n, int32_t K, int num_cus, int region, bool big) {
+int split_chunk_rows(int64_t n, int32_t K, int num_cus, int region) {
   const int64_t slots = K > 1 ? K - 1 : 1;
-  const int64_t wgs = (int64_t)num_cus * split_wgs_per_cu(big);
+  const int64_t wgs = (int64_t)num_cus * kSplitWgsPerCu;
   int64_t chunks = (wgs + slots - 1) / slots;
   if (chunks < 1) chunks = 1;
   int64_t rc = (n + chunks - 1) / chunks;
@@ -659,14 +672,14 @@ hipError_t launch_split_k(const SplitArgs& a0, int num_cus, hipStream_t stream) 
   constexpr int Cin = KS * 32, Cout = NCT * 16;
   constexpr int wbytes = Cin * Cout * 2;
   constexpr bool big = split_big(wbytes, NCT);
-  constexpr int MINW = big ? 1 : 2;
+  constexpr int WP = big ? 2 : 1;
   if (a.K > 1) {
-    a.chunk_rows = split_chunk_rows(a.n_rows, a.K, num_cus, sp_pair_region(Cin, Cout), big);
-    auto kp = conv_pairs_kernel<KS, NCT, MINW>;
+    a.chunk_rows = split_chunk_rows(a.n_rows, a.K, num_cus, sp_pair_region(Cin, Cout, WP));
+    auto kp = conv_pairs_kernel<KS, NCT, WP>;
     static std::once_flag once;
     static hipError_t err = hipSuccess;
     if (sp_allow_lds(kp, once, err) != hipSuccess) return err;
-    const size_t lds = (size_t)sp_pair_region(Cin, Cout) + 6 * (size_t)a.chunk_rows + 16;
+    const size_t lds = (size_t)sp_pair_region(Cin, Cout, WP) + 6 * (size_t)a.chunk_rows + 16;
     const unsigned chunks = (unsigned)((a.n_rows + a.chunk_rows - 1) / a.chunk_rows);
     hipLaunchKernelGGL(kp, dim3(chunks, (unsigned)(a.K - 1)), dim3(kPairThreads), lds, stream, a);
     const hipError_t e = hipGetLastError();
@@ -675,10 +688,10 @@ hipError_t launch_split_k(const SplitArgs& a0, int num_cus, hipStream_t stream) 
   // row workgroups: two per CU; for big shapes W[0] is staged in two slices
   // and a batch has two blocks (one at 256 x 256: the fragments of a quarter
   // of W[0] and a batch's accumulators then fill a wavefront's registers)
-  constexpr int RB = big ? (KS * NCT >= 128 ? 1 : 2) : kRowBatch, WP = big ? 2 : 1;
+  constexpr int RB = big ? (KS * NCT >= 128 ? 1 : 2) : kRowBatch;
   const int64_t batches = (a.n_rows + RB * 16 - 1) / (RB * 16);
   int64_t grid = batches;
-  const int64_t cap = (int64_t)num_cus * 2;
+  const int64_t cap = (int64_t)num_cus * kSplitWgsPerCu;
   if (grid > cap) grid = cap;
   const size_t lds = (size_t)sp_row_region(Cin, Cout, RB, WP);
   if (a.K <= 12) {
