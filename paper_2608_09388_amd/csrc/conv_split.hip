@@ -586,15 +586,17 @@ __global__ __launch_bounds__(kPairThreads, MINW) void conv_rows_kernel(const Spl
 #pragma unroll
     for (int u = 0; u < RB; ++u) {
       if (staged[u]) {
+        // every k-step's B operand read first: the reads' latency is paid once
         const unsigned char* rp = rows + (u * 16 + l16) * SROW + g * 16;
+        bf16x8 sf[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 sf = *reinterpret_cast<const bf16x8*>(rp + ks * 64);
+        for (int ks = 0; ks < KS; ++ks) sf[ks] = *reinterpret_cast<const bf16x8*>(rp + ks * 64);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
           for (int q = 0; q < NCTW; ++q)
-            acc[u][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wreg[ks][q], sf, acc[u][q], 0, 0,
-                                                                0);
-        }
+            acc[u][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wreg[ks][q], sf[ks], acc[u][q],
+                                                                0, 0, 0);
       } else {
         const uint32_t off = (uint32_t)s0[u] * (uint32_t)(Cin * 2) + (uint32_t)g * 16u;
 #pragma unroll
