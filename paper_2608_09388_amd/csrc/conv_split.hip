@@ -132,49 +132,7 @@ struct SlotWeights {
         (SHC_SP_LDS sp_bf16x4*)(const_cast<unsigned char*>(p0 + 4 * WROW)));
     return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   }
-  // every column block of k-step ks
-  __device__ static void read_k(const unsigned char* wbuf, int ks, int g, int l16,
-                                bf16x8 (&out)[NCT]) {
-#pragma unroll
-    for (int ct = 0; ct < NCT; ++ct) out[ct] = read(wbuf, ks, ct, g, l16);
-  }
 };
-
-// The MFMAs of one k-sweep: acc[b][ct] += W^T-block (ks, ct) x B-operand b of
-// k-step ks, for NB B operands (bfrag(b, ks)).  With PREF the next k-step's
-// weight fragments are read from LDS while this one's MFMAs run (twice the
-// fragment registers; with one wavefront per SIMD nothing else hides the
-// LDS latency); else each fragment is read just before its MFMAs.
-template <int KS, int NCT, int NT, bool PREF, int NB, typename BFrag>
-__device__ __forceinline__ void sp_mfma_sweep(const unsigned char* wbuf, int g, int l16,
-                                              f32x4 (&acc)[NB][NCT], BFrag bfrag) {
-  using SW = SlotWeights<KS, NCT, NT>;
-  if constexpr (PREF) {
-    bf16x8 wf[2][NCT];
-    SW::read_k(wbuf, 0, g, l16, wf[0]);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (ks + 1 < KS) SW::read_k(wbuf, ks + 1, g, l16, wf[(ks + 1) & 1]);
-#pragma unroll
-      for (int ct = 0; ct < NCT; ++ct)
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-          acc[b][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[ks & 1][ct], bfrag(b, ks),
-                                                               acc[b][ct], 0, 0, 0);
-    }
-  } else {
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int ct = 0; ct < NCT; ++ct) {
-        const bf16x8 wf = SW::read(wbuf, ks, ct, g, l16);
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-          acc[b][ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, bfrag(b, ks), acc[b][ct],
-                                                               0, 0, 0);
-      }
-  }
-}
 
 __device__ __forceinline__ int sp_lanes_below(uint64_t bal) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
