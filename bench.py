@@ -59,6 +59,9 @@ def parse():
     p.add_argument("--step-only", action="store_true",
                    help="the step, its per-kernel times and roofline only (one workload, "
                         "for kernel traces of the density-sweep batch alone)")
+    p.add_argument("--stacks-only", action="store_true",
+                   help="only the other configurations' stacks (config_stacks), with --steps, "
+                        "--warmup and --reps (for kernel traces of the split conv)")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--reps", type=int, default=50,
                    help="back-to-back launches per kernel for the per-kernel times")
@@ -259,6 +262,10 @@ def main():
     shc.load()
     if args.copy_calibration:
         copy_calibration(torch, args.copy_calibration)
+        return
+    if args.stacks_only:
+        print(json.dumps({"config_stacks": config_stacks_measure(
+            torch, steps=args.steps, warmup=args.warmup, reps=args.reps)}))
         return
     w = synth.workload_c4(args.density)
     # the next batch's compaction and neighbour table run on a second stream
