@@ -319,7 +319,11 @@ def main():
         roof = {"bound": "mfma", "achieved": round(ach, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(ach / BF16_MFMA_PEAK_TFLOPS, 4),
                 "traffic": traffic}
-    roof["kernel"] = ("shc_sparse_neighbor_conv_table (ws_kernel: weight slice resident in "
+    roof["kernel"] = ("shc_sparse_neighbor_conv_packed (conv_packed_kernel: every slot's "
+                      "weights in registers, one chunk of active rows per CU, rows grouped by "
+                      "their slots in LDS)"
+                      if max(1, st.packed_min_rows) <= n <= st.packed_rows.get(1, 0) else
+                      "shc_sparse_neighbor_conv_table (ws_kernel: weight slice resident in "
                       "LDS, index sets from the neighbour-row table)")
     roof["algorithmic_bytes"] = int(cbytes)
     roof["useful_flops"] = cflops
@@ -498,6 +502,8 @@ def config_stacks_measure(torch, steps=500, warmup=30, reps=50):
         for l, spec in enumerate(w.layers):
             if spec.kind != "conv":
                 kinds.append("linear")
+            elif max(1, st.packed_min_rows) <= n <= st.packed_rows.get(l, 0):
+                kinds.append("packed conv")
             elif 0 < n <= st.split_rows.get(l, 0):
                 kinds.append("split conv")
             elif 0 < n <= st.plan_shapes.get(tuple(st.weights[l].shape), 0):

@@ -393,6 +393,45 @@ int shc_sparse_neighbor_conv_split(const void* S, const int32_t* table, int64_t 
                                    int32_t Cout, int32_t dtype, int32_t act, void* out,
                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Sparse neighbourhood conv with pre-arranged weights (Eqs. 4-5, with the
+ * activation of Eq. 10), bf16: the same y_i as shc_sparse_neighbor_conv_table,
+ *
+ *   out[i] = act( bias + sum_{j < K, table[j][i] present} S[table[j][i]] W[j] ),
+ *
+ * summed in fp32 per row with slot 0 first and the other present slots
+ * ascending.  Every slot's weights stay in the matrix cores' operand
+ * registers for the whole launch, one workgroup per compute unit over a chunk
+ * of consecutive active rows: the chunk's input rows are read once into LDS,
+ * rows are grouped by the slots they have, and only neighbour rows outside
+ * the chunk are gathered again.  Shapes: bf16, Cin and Cout in {64, 128},
+ * 1 <= K <= 9.
+ *
+ * shc_conv_packed_weights_bytes: bytes of the packed weights of a shape,
+ *   K * Cin * Cout * 2; 0 when the shape has no packed conv.
+ * shc_pack_conv_weights: W [K][Cin][Cout] bf16 (device) -> Wp (device, at
+ *   least shc_conv_packed_weights_bytes bytes, 16-byte aligned, owned by the
+ *   caller).  For slot j, 16-column block ct and 32-channel step ks, Wp holds
+ *   the 64 lanes' 16-byte operand fragments of a 16x16x32 matrix-core step
+ *   contiguously: lane 16 g + i gets W[j][32 ks + 8 g + e][16 ct + i], e < 8.
+ *   Pack once per weight update; stream-ordered, no host wait.
+ * shc_sparse_neighbor_conv_packed: S, table, bias, out, act as for
+ *   shc_sparse_neighbor_conv_table; Wp from shc_pack_conv_weights of the same
+ *   K, Cin, Cout.  Table entries outside [0, n_rows) count as absent.
+ *   Stream-ordered, no host wait, allocates nothing.
+ *
+ * Errors: those of shc_sparse_neighbor_conv_table; SHC_ERR_UNSUPPORTED for a
+ * shape without a packed conv or a table of 2^31 bytes or more,
+ * SHC_ERR_CAPACITY when Wp_bytes is too small.
+ */
+size_t shc_conv_packed_weights_bytes(int32_t K, int32_t Cin, int32_t Cout, int32_t dtype);
+int shc_pack_conv_weights(const void* W, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype,
+                          void* Wp, size_t Wp_bytes, hipStream_t stream);
+int shc_sparse_neighbor_conv_packed(const void* S, const int32_t* table, int64_t n_rows,
+                                    int32_t K, const void* Wp, const float* bias, int32_t Cin,
+                                    int32_t Cout, int32_t dtype, int32_t act, void* out,
+                                    hipStream_t stream);
+
 int64_t shc_conv_plan_max_rows(int32_t K, int32_t Cin, int32_t Cout, int32_t dtype);
 size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype);
 int shc_build_conv_plan(const int32_t* table, int64_t n_rows, int32_t K, int32_t Cin,
@@ -718,6 +757,11 @@ typedef struct shc_stack_layer {
   int64_t split_rows; /* conv: shc_sparse_neighbor_conv_split, with the description's
                          split workspace, when 0 < N' <= split_rows; 0: never.  A layer
                          takes a plan or the split conv, not both. */
+  const void* Wp;     /* conv: W packed by shc_pack_conv_weights, or NULL */
+  int64_t packed_rows; /* conv: shc_sparse_neighbor_conv_packed with Wp when
+                          max(1, packed_min_rows) <= N' <= packed_rows; 0: never.
+                          Excludes a plan and the split conv. */
+  int64_t packed_min_rows;
 } shc_stack_layer;
 
 typedef struct shc_stack_index_set {

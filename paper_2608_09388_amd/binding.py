@@ -48,7 +48,8 @@ SHC_LAYER_LINEAR, SHC_LAYER_CONV = 0, 1
 
 class StackLayer(ctypes.Structure):
     _fields_ = [("kind", _c_i32), ("Cin", _c_i32), ("Cout", _c_i32), ("act", _c_i32),
-                ("W", _c_ptr), ("bias", _c_ptr), ("plan_rows", _c_i64), ("split_rows", _c_i64)]
+                ("W", _c_ptr), ("bias", _c_ptr), ("plan_rows", _c_i64), ("split_rows", _c_i64),
+                ("Wp", _c_ptr), ("packed_rows", _c_i64), ("packed_min_rows", _c_i64)]
 
 
 class StackIndexSet(ctypes.Structure):
@@ -115,6 +116,12 @@ _SIGS = {
     "shc_sparse_neighbor_conv_split": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_ptr,
                                                       _c_ptr, _c_i32, _c_i32, _c_i32, _c_i32,
                                                       _c_ptr, _c_ptr, _c_sz, _c_ptr]),
+    "shc_conv_packed_weights_bytes": (_c_sz, [_c_i32, _c_i32, _c_i32, _c_i32]),
+    "shc_pack_conv_weights": (ctypes.c_int, [_c_ptr, _c_i32, _c_i32, _c_i32, _c_i32, _c_ptr,
+                                             _c_sz, _c_ptr]),
+    "shc_sparse_neighbor_conv_packed": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_ptr,
+                                                       _c_ptr, _c_i32, _c_i32, _c_i32, _c_i32,
+                                                       _c_ptr, _c_ptr]),
     "shc_conv_plan_max_rows": (_c_i64, [_c_i32, _c_i32, _c_i32, _c_i32]),
     "shc_conv_plan_bytes": (_c_sz, [_c_i64, _c_i32, _c_i32, _c_i32, _c_i32]),
     "shc_build_conv_plan": (ctypes.c_int, [_c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
@@ -424,6 +431,33 @@ def sparse_neighbor_conv_split(S: torch.Tensor, table: torch.Tensor, n_rows: int
             _dev(out, "out", S.dtype, n_rows * Cout), _dev(workspace, "workspace"),
             workspace.numel() * workspace.element_size(), _stream(stream)]
     _check(load().shc_sparse_neighbor_conv_split(*args), "shc_sparse_neighbor_conv_split")
+
+
+def conv_packed_weights_bytes(K: int, Cin: int, Cout: int, dtype: int = SHC_BF16) -> int:
+    """shc_conv_packed_weights_bytes: bytes of the packed weights (0: the
+    shape has no packed conv)."""
+    return int(load().shc_conv_packed_weights_bytes(K, Cin, Cout, dtype))
+
+
+def pack_conv_weights(W: torch.Tensor, Wp: torch.Tensor, stream=None):
+    """shc_pack_conv_weights: W [K][Cin][Cout] bf16 into the device buffer Wp
+    (conv_packed_weights_bytes bytes)."""
+    K, Cin, Cout = W.shape
+    args = [_dev(W, "W", W.dtype, K * Cin * Cout), K, Cin, Cout, _dtype_code(W),
+            _dev(Wp, "Wp"), Wp.numel() * Wp.element_size(), _stream(stream)]
+    _check(load().shc_pack_conv_weights(*args), "shc_pack_conv_weights")
+
+
+def sparse_neighbor_conv_packed(S: torch.Tensor, table: torch.Tensor, n_rows: int,
+                                Wp: torch.Tensor, K: int, Cin: int, Cout: int,
+                                bias: Optional[torch.Tensor], out: torch.Tensor,
+                                act: int = SHC_ACT_RELU, stream=None):
+    """shc_sparse_neighbor_conv_packed: the conv of sparse_neighbor_conv_table
+    with weights from pack_conv_weights."""
+    args = [_dev(S, "S", S.dtype, n_rows * Cin), _dev(table, "table", torch.int32, K * n_rows),
+            n_rows, K, _dev(Wp, "Wp"), _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout,
+            _dtype_code(S), act, _dev(out, "out", S.dtype, n_rows * Cout), _stream(stream)]
+    _check(load().shc_sparse_neighbor_conv_packed(*args), "shc_sparse_neighbor_conv_packed")
 
 
 def conv_plan_max_rows(K: int, Cin: int, Cout: int, dtype: int = SHC_BF16) -> int:
@@ -995,6 +1029,17 @@ def prepare_sparse_neighbor_conv_split(S, table, W, bias, out, workspace, act=SH
             workspace.numel() * workspace.element_size(), _stream(stream)]
     return Prepared("shc_sparse_neighbor_conv_split", args, 2, n_max,
                     (S, table, W, bias, out, workspace))
+
+
+def prepare_sparse_neighbor_conv_packed(S, table, Wp, K, Cin, Cout, bias, out,
+                                        act=SHC_ACT_RELU, stream=None) -> Prepared:
+    """shc_sparse_neighbor_conv_packed with n_rows given per call."""
+    n_max = min(S.numel() // Cin, table.numel() // K, out.numel() // Cout)
+    args = [_dev(S, "S", S.dtype), _dev(table, "table", torch.int32), 0, K, _dev(Wp, "Wp"),
+            _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, _dtype_code(S), act,
+            _dev(out, "out", S.dtype), _stream(stream)]
+    return Prepared("shc_sparse_neighbor_conv_packed", args, 2, n_max,
+                    (S, table, Wp, bias, out))
 
 
 def prepare_build_conv_plan(table, K, Cin, Cout, plan, dtype=SHC_BF16, stream=None) -> Prepared:

@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libshc.so")
 SOURCES = ["compact.hip", "neighbors.hip", "rows.hip", "norm.hip", "scores.hip", "backward.hip",
-           "gemm.hip", "conv_ws.hip", "conv_sm.hip", "conv_split.hip", "abi.hip",
+           "gemm.hip", "conv_ws.hip", "conv_sm.hip", "conv_split.hip", "conv_packed.hip", "abi.hip",
            "stack.hip"]
 ARCH = os.environ.get("SHC_OFFLOAD_ARCH", "gfx950")
 

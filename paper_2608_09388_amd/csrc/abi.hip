@@ -668,6 +668,60 @@ int shc_sparse_neighbor_conv_split(const void* S, const int32_t* table, int64_t 
                     "sparse_neighbor_conv_split launch");
 }
 
+size_t shc_conv_packed_weights_bytes(int32_t K, int32_t Cin, int32_t Cout, int32_t dtype) {
+  if (dtype != SHC_BF16 || !shc::conv_packed_supported(1, K, Cin, Cout)) return 0;
+  return (size_t)shc::conv_packed_weights_bytes(K, Cin, Cout);
+}
+
+int shc_pack_conv_weights(const void* W, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype,
+                          void* Wp, size_t Wp_bytes, hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_conv_shape(1, K, Cin, Cout, dtype, SHC_ACT_NONE));
+  if (dtype != SHC_BF16 || !shc::conv_packed_supported(1, K, Cin, Cout))
+    return fail(SHC_ERR_UNSUPPORTED,
+                "no packed conv for dtype %d, K = %d, Cin = %d, Cout = %d (bf16, K <= 9, "
+                "channels in {64, 128})",
+                dtype, K, Cin, Cout);
+  SHC_PTR(W, "W");
+  SHC_PTR(Wp, "Wp");
+  const int64_t need = shc::conv_packed_weights_bytes(K, Cin, Cout);
+  if ((int64_t)Wp_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "Wp_bytes = %zu is below the %lld bytes of the packed weights",
+                Wp_bytes, (long long)need);
+  return hip_status(shc::launch_pack_conv_weights(W, K, Cin, Cout, Wp, stream),
+                    "pack_conv_weights launch");
+}
+
+int shc_sparse_neighbor_conv_packed(const void* S, const int32_t* table, int64_t n_rows,
+                                    int32_t K, const void* Wp, const float* bias, int32_t Cin,
+                                    int32_t Cout, int32_t dtype, int32_t act, void* out,
+                                    hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_conv_shape(n_rows, K, Cin, Cout, dtype, act));
+  if (dtype != SHC_BF16 || !shc::conv_packed_supported(n_rows, K, Cin, Cout))
+    return fail(SHC_ERR_UNSUPPORTED,
+                "no packed conv for dtype %d, K = %d, Cin = %d, Cout = %d (bf16, K <= 9, "
+                "channels in {64, 128})",
+                dtype, K, Cin, Cout);
+  // the table is read through a buffer resource of K * n_rows * 4 bytes
+  if ((int64_t)K * n_rows * 4 > 0x7FFFFFFFLL)
+    return fail(SHC_ERR_UNSUPPORTED, "K * n_rows * 4 = %lld bytes of table exceed 2^31 - 1",
+                (long long)((int64_t)K * n_rows * 4));
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(S, "S");
+  SHC_PTR(table, "table");
+  SHC_PTR(Wp, "Wp");
+  SHC_OPT_PTR(bias, "bias");
+  SHC_PTR(out, "out");
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_status(e, "sparse_neighbor_conv_packed device query");
+  return hip_status(shc::launch_conv_packed(S, table, n_rows, K, Wp, bias, Cin, Cout,
+                                            act == SHC_ACT_RELU, out, cus, stream),
+                    "sparse_neighbor_conv_packed launch");
+}
+
 size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype) {
   if (!plan_query_args_ok(n_rows, K, Cin, Cout, dtype)) return 0;
   shc::GemmArgs a{};

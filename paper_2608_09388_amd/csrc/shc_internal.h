@@ -191,4 +191,15 @@ hipError_t launch_conv_split(const void* S, const int32_t* table, int64_t n_rows
                              int32_t relu, void* out, float* workspace, int num_cus,
                              hipStream_t stream);
 
+// conv from a neighbour-row table with every slot's weights in registers
+// (conv_packed.hip): bf16, C_in and C_out in {64, 128}, K <= 9, weights
+// pre-arranged by launch_pack_conv_weights into conv_packed_weights_bytes
+bool conv_packed_supported(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout);
+int64_t conv_packed_weights_bytes(int32_t K, int32_t Cin, int32_t Cout);
+hipError_t launch_pack_conv_weights(const void* W, int32_t K, int32_t Cin, int32_t Cout,
+                                    void* Wp, hipStream_t stream);
+hipError_t launch_conv_packed(const void* S, const int32_t* table, int64_t n_rows, int32_t K,
+                              const void* Wp, const float* bias, int32_t Cin, int32_t Cout,
+                              int32_t relu, void* out, int num_cus, hipStream_t stream);
+
 }  // namespace shc

@@ -107,6 +107,10 @@ struct Stack {
 
   bool split(int l, int64_t n) const { return n > 0 && n <= d.layers[l].split_rows; }
 
+  bool packed(int l, int64_t n) const {
+    return n > 0 && n >= d.layers[l].packed_min_rows && n <= d.layers[l].packed_rows;
+  }
+
   int plans(int s, int64_t n, hipStream_t st) const {
     for (int l = 0; l < d.n_layers; ++l) {
       if (plan_owner[l] != l || !planned(l, n)) continue;
@@ -127,6 +131,9 @@ struct Stack {
     const shc_stack_layer& L = d.layers[l];
     const shc_stack_index_set& x = d.sets[s];
     if (L.kind == SHC_LAYER_CONV) {
+      if (packed(l, n))
+        return shc_sparse_neighbor_conv_packed(d.acts[l], x.table, n, d.K, L.Wp, L.bias, L.Cin,
+                                               L.Cout, d.dtype, L.act, dst, st);
       if (split(l, n))
         return shc_sparse_neighbor_conv_split(d.acts[l], x.table, n, d.K, L.W, L.bias, L.Cin,
                                               L.Cout, d.dtype, L.act, dst, d.split_ws,
@@ -350,6 +357,26 @@ int check_desc(const shc_stack_desc& d, Stack* k) {
     if (L.split_rows < 0)
       return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: split_rows = %lld is negative", l,
                             (long long)L.split_rows);
+    if (L.packed_min_rows < 0)
+      return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: packed_min_rows = %lld is negative",
+                            l, (long long)L.packed_min_rows);
+    if (L.packed_rows < 0)
+      return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: packed_rows = %lld is negative", l,
+                            (long long)L.packed_rows);
+    if (L.packed_rows > 0) {
+      if (L.kind != SHC_LAYER_CONV)
+        return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: a linear layer takes no packed "
+                              "conv", l);
+      if (L.plan_rows > 0 || L.split_rows > 0)
+        return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: packed_rows with plan_rows or "
+                              "split_rows", l);
+      if (shc_conv_packed_weights_bytes(d.K, L.Cin, L.Cout, d.dtype) == 0)
+        return shc::set_error(SHC_ERR_UNSUPPORTED, "layer %d: no packed conv for this shape", l);
+      if ((int64_t)d.K * L.packed_rows * 4 > 0x7FFFFFFFLL)
+        return shc::set_error(SHC_ERR_UNSUPPORTED, "layer %d: packed_rows = %lld too large", l,
+                              (long long)L.packed_rows);
+      STK_TRY(need_ptr(L.Wp, "layers.Wp", l));
+    }
     if (L.split_rows > 0) {
       if (L.kind != SHC_LAYER_CONV)
         return shc::set_error(SHC_ERR_INVALID_ARG, "layer %d: a linear layer takes no split "

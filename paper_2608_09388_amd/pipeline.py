@@ -61,6 +61,19 @@ TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
 # workspace limit (2^31 bytes) ends it near 20% there.
 SPLIT_DENSITY = 0.2
 
+# Active fraction of the B*V rows up to which a conv layer of a shape the
+# packed conv takes (bf16, 64 or 128 channels, K <= 9) runs as the packed conv
+# by default.  On the density-sweep batch (B = 128, V = 10475, K = 9,
+# 128 -> 128) it took 10.3 / 21.6 / 109.9 us against 12.6 / 25.9 / 114.9 us
+# for the table conv at 1 / 5 / 20% Bernoulli masks.  It runs one workgroup
+# of eight wavefronts per CU when C_out = 128 and four when C_out = 64; with
+# four (one per SIMD) and on small batches (under PACKED_MIN_ROWS_PER_CU rows
+# per CU the weights' load dominates) the other kernels were faster: the
+# full-mesh 64 -> 64 layer at its 5% cap took 66 us against 36 us, the
+# encoder's step 0.069 ms against 0.052 ms.
+PACKED_DENSITY = 0.25
+PACKED_MIN_ROWS_PER_CU = 32
+
 
 def to_device(a: np.ndarray, dtype: str, device) -> torch.Tensor:
     """Upload fp32 values that are exact in `dtype` as a tensor of that dtype."""
@@ -165,6 +178,12 @@ class _IndexSet:
         if spec.kind == "conv":
             table = shc.prepare_sparse_neighbor_conv_table(src, self.table, st.weights[l],
                                                            st.biases[l], dst, a)
+            if l in st.packed_rows:
+                K_, Cin, Cout = st.weights[l].shape
+                packed = shc.prepare_sparse_neighbor_conv_packed(src, self.table, st.packed_w[l],
+                                                                 K_, Cin, Cout, st.biases[l],
+                                                                 dst, a)
+                return _SplitConv(table, packed, st.packed_rows[l], st.packed_min_rows)
             if l in st.split_rows:
                 split = shc.prepare_sparse_neighbor_conv_split(src, self.table, st.weights[l],
                                                                st.biases[l], dst, st.split_ws, a)
@@ -199,14 +218,14 @@ class _IncrementalScatter:
 
 
 class _SplitConv:
-    """A conv layer that runs as the split conv when the batch's row count is
-    within its limit, else from the table."""
+    """A conv layer that runs as the split (or packed) conv when the batch's
+    row count is within its limit, else from the table."""
 
-    def __init__(self, table, split, n_lim: int):
-        self.table, self.split, self.n_lim = table, split, n_lim
+    def __init__(self, table, split, n_lim: int, n_min: int = 0):
+        self.table, self.split, self.n_lim, self.n_min = table, split, n_lim, max(n_min, 1)
 
     def __call__(self, n: int):
-        return self.split(n) if 0 < n <= self.n_lim else self.table(n)
+        return self.split(n) if self.n_min <= n <= self.n_lim else self.table(n)
 
 
 def _split_rows_limit(want: int, K: int, Cin: int, Cout: int) -> int:
@@ -241,7 +260,7 @@ class SparseStack:
     def __init__(self, w: Workload, device: str = "cuda", act: int = shc.SHC_ACT_RELU,
                  side_stream: bool = False, conv_plans: Optional[bool] = None,
                  incremental_scatter: bool = False, executor: str = "native",
-                 split_conv: Optional[bool] = None):
+                 split_conv: Optional[bool] = None, packed_conv: Optional[bool] = None):
         if executor not in ("native", "python"):
             raise ValueError(f"executor = {executor!r}: 'native' or 'python'")
         self.w = w
@@ -307,10 +326,33 @@ class SparseStack:
         # channels, up to SPLIT_DENSITY of the B*V rows (the table conv runs
         # them on its tiled kernel, which re-reads the weights per row tile);
         # split_conv = True / False forces it on every shape that takes it / off.
+        # Conv layers that run as shc_sparse_neighbor_conv_packed (every slot's
+        # weights in registers, packed once here) for batches of at most
+        # packed_rows[l] rows.  By default: every shape it takes, up to
+        # PACKED_DENSITY of the B*V rows; packed_conv = True / False forces it
+        # up to all rows / off.
+        self.packed_rows: Dict[int, int] = {}
+        self.packed_w: Dict[int, torch.Tensor] = {}
+        if w.dtype == "bf16" and packed_conv is not False:
+            for l, spec in enumerate(w.layers):
+                if spec.kind != "conv":
+                    continue
+                K_, Cin, Cout = self.weights[l].shape
+                nb = shc.conv_packed_weights_bytes(K_, Cin, Cout)
+                if nb == 0 or (packed_conv is None and Cout != 128):
+                    continue
+                rows = BV if packed_conv else int(PACKED_DENSITY * BV)
+                rows = min(rows, (2 ** 31 - 1) // (4 * K_))
+                if rows > 0:
+                    Wp = torch.empty(nb, dtype=torch.uint8, device=dev)
+                    shc.pack_conv_weights(self.weights[l], Wp)
+                    self.packed_w[l], self.packed_rows[l] = Wp, rows
+        cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        self.packed_min_rows = 0 if packed_conv else PACKED_MIN_ROWS_PER_CU * cus
         self.split_rows: Dict[int, int] = {}
         if w.dtype == "bf16" and split_conv is not False:
             for l, spec in enumerate(w.layers):
-                if spec.kind != "conv":
+                if spec.kind != "conv" or l in self.packed_rows:
                     continue
                 K_, Cin, Cout = self.weights[l].shape
                 if split_conv is None and max(Cin, Cout) < 256:
@@ -325,7 +367,8 @@ class SparseStack:
                        for l, r in self.split_rows.items())
             self.split_ws = torch.empty(need, dtype=torch.uint8, device=dev)
         self.plan_shapes: Dict[Tuple[int, int, int], int] = {}
-        split_shapes = {tuple(self.weights[l].shape) for l in self.split_rows}
+        split_shapes = {tuple(self.weights[l].shape)
+                        for l in list(self.split_rows) + list(self.packed_rows)}
         if w.dtype == "bf16":
             shapes: Dict[Tuple[int, int, int], int] = {}
             for l, spec in enumerate(w.layers):
@@ -334,7 +377,7 @@ class SparseStack:
                     shapes[key] = shapes.get(key, 0) + 1
             for key, count in shapes.items():
                 if key in split_shapes:
-                    continue  # a layer takes a plan or the split conv, not both
+                    continue  # a layer takes a plan, the split or the packed conv
                 use = conv_plans if conv_plans is not None else count >= 2
                 n_lim = shc.conv_plan_max_rows(*key) if use else 0
                 if n_lim > 0:
@@ -373,6 +416,9 @@ class SparseStack:
             n_lim = self.plan_shapes.get(tuple(W.shape), 0) if spec.kind == "conv" else 0
             L.plan_rows = min(BV, n_lim)
             L.split_rows = self.split_rows.get(l, 0)
+            L.Wp = self.packed_w[l].data_ptr() if l in self.packed_w else None
+            L.packed_rows = self.packed_rows.get(l, 0)
+            L.packed_min_rows = self.packed_min_rows if l in self.packed_rows else 0
         for i, a in enumerate(self.acts):
             d.acts[i] = a.data_ptr()
         d.last_alt = self.last_alt.data_ptr() if self.last_alt is not None else None

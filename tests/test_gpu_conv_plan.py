@@ -229,7 +229,7 @@ def test_stack_with_plans_matches_without(dev, side):
     w = synth.workload_c4(0.05, B=24)
     outs = {}
     for use in (False, True):
-        st = SparseStack(w, device=dev, side_stream=side, conv_plans=use)
+        st = SparseStack(w, device=dev, side_stream=side, conv_plans=use, packed_conv=False)
         assert bool(st.plan_shapes) == use
         masks = [np.random.default_rng(40 + k).random(w.B * w.V) < 0.03 + 0.02 * k
                  for k in range(3)]
@@ -255,7 +255,7 @@ def test_encoder_stack_mixed_plans(dev, side):
     w = synth.workload_c2()
     outs = {}
     for use in (False, True):
-        st = SparseStack(w, device=dev, side_stream=side, conv_plans=use)
+        st = SparseStack(w, device=dev, side_stream=side, conv_plans=use, packed_conv=False)
         if use:
             assert (9, 16, 64) not in st.plan_shapes
             assert {(9, 64, 64), (9, 64, 128), (9, 128, 128)} <= set(st.plan_shapes)

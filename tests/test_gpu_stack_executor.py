@@ -69,8 +69,10 @@ def masks_for(w, k0, n=4):
 
 
 def run_stack(w, dev, executor, side, inc, plans, masks, batched):
+    # plans are taken by shapes the packed conv does not run
     st = SparseStack(w, device=dev, side_stream=side, conv_plans=plans,
-                     incremental_scatter=inc, executor=executor)
+                     incremental_scatter=inc, executor=executor,
+                     packed_conv=False if plans else None)
     assert st.executor == executor
     md = [torch.from_numpy(m).to(dev) for m in masks]
     snaps = []
@@ -202,7 +204,7 @@ def test_create_refuses_plan_misuse(dev):
     """Plan buffers on the device: below a plan's size, shared by layers of
     different shapes, or shared differently in another index set."""
     w = synth.workload_c2()
-    st = SparseStack(w, device=dev, side_stream=True, conv_plans=True)
+    st = SparseStack(w, device=dev, side_stream=True, conv_plans=True, packed_conv=False)
     base = st._native._desc
     planned = [l for l in range(len(w.layers)) if base.sets[0].plan[l]]
     assert len(planned) >= 2
