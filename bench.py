@@ -39,7 +39,8 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_sparse_conv_c4_5pct.txt")
 # only used while they are unchanged
 EVENT_EVERY = 50  # steps between two sampled conv launches in the timed region
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_09388_amd", "csrc", f)
-                  for f in ("gemm.hip", "conv_ws.hip", "conv_sm.hip", "shc_internal.h")]
+                  for f in ("conv_packed.hip", "gemm.hip", "conv_ws.hip", "conv_sm.hip",
+                            "shc_internal.h")]
 
 
 def log(msg):
