@@ -432,6 +432,46 @@ int shc_sparse_neighbor_conv_packed(const void* S, const int32_t* table, int64_t
                                     int32_t Cout, int32_t dtype, int32_t act, void* out,
                                     hipStream_t stream);
 
+/*
+ * The packed conv's plan (Sec. 3.2: the index sets C'_k = C_k are the same
+ * for every layer, so the grouping of the active rows by their slots is a
+ * property of the active set, not of a layer): shc_build_conv_packed_plan
+ * does the packed conv's grouping of each chunk of rows (the rows' order,
+ * every (row, slot) entry as the LDS row to read, the neighbour rows to
+ * stage, the staging rounds) and writes it to `plan`;
+ * shc_sparse_neighbor_conv_packed_planned then computes the layer from it,
+ * without the table, with the same result as shc_sparse_neighbor_conv_packed
+ * on that table.  Build once per active set (after the table), on any
+ * stream ordered before the layers that read it.
+ *
+ * shc_conv_packed_plan_bytes: bytes of a plan buffer that holds the plan of
+ *   any row count up to n_rows on the current device (0: no packed conv for
+ *   the shape).
+ * shc_build_conv_packed_plan: table [K][n_rows] as for
+ *   shc_sparse_neighbor_conv_table; plan: device memory of at least the bytes
+ *   the call's n_rows needs (shc_conv_packed_plan_bytes(n_rows, ...) is
+ *   enough), 16-byte aligned, owned by the caller.  Stream-ordered.
+ * shc_sparse_neighbor_conv_packed_planned: S, bias, out, act as for
+ *   shc_sparse_neighbor_conv_packed; plan from shc_build_conv_packed_plan of
+ *   the same n_rows, K, Cin and Cout.  A chunk whose plan was built for
+ *   another row count is skipped (its rows are not written); a plan of another
+ *   table of the same row count gives wrong values but no access out of
+ *   range.  Stream-ordered, allocates nothing.
+ *
+ * Errors: those of shc_sparse_neighbor_conv_packed; SHC_ERR_CAPACITY when
+ * plan_bytes is below what the call's n_rows needs.
+ */
+size_t shc_conv_packed_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout,
+                                  int32_t dtype);
+int shc_build_conv_packed_plan(const int32_t* table, int64_t n_rows, int32_t K, int32_t Cin,
+                               int32_t Cout, int32_t dtype, void* plan, size_t plan_bytes,
+                               hipStream_t stream);
+int shc_sparse_neighbor_conv_packed_planned(const void* S, const void* plan, size_t plan_bytes,
+                                            int64_t n_rows, int32_t K, const void* Wp,
+                                            const float* bias, int32_t Cin, int32_t Cout,
+                                            int32_t dtype, int32_t act, void* out,
+                                            hipStream_t stream);
+
 int64_t shc_conv_plan_max_rows(int32_t K, int32_t Cin, int32_t Cout, int32_t dtype);
 size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype);
 int shc_build_conv_plan(const int32_t* table, int64_t n_rows, int32_t K, int32_t Cin,

@@ -122,6 +122,13 @@ _SIGS = {
     "shc_sparse_neighbor_conv_packed": (ctypes.c_int, [_c_ptr, _c_ptr, _c_i64, _c_i32, _c_ptr,
                                                        _c_ptr, _c_i32, _c_i32, _c_i32, _c_i32,
                                                        _c_ptr, _c_ptr]),
+    "shc_conv_packed_plan_bytes": (_c_sz, [_c_i64, _c_i32, _c_i32, _c_i32, _c_i32]),
+    "shc_build_conv_packed_plan": (ctypes.c_int, [_c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
+                                                  _c_ptr, _c_sz, _c_ptr]),
+    "shc_sparse_neighbor_conv_packed_planned": (ctypes.c_int, [_c_ptr, _c_ptr, _c_sz, _c_i64,
+                                                               _c_i32, _c_ptr, _c_ptr, _c_i32,
+                                                               _c_i32, _c_i32, _c_i32, _c_ptr,
+                                                               _c_ptr]),
     "shc_conv_plan_max_rows": (_c_i64, [_c_i32, _c_i32, _c_i32, _c_i32]),
     "shc_conv_plan_bytes": (_c_sz, [_c_i64, _c_i32, _c_i32, _c_i32, _c_i32]),
     "shc_build_conv_plan": (ctypes.c_int, [_c_ptr, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32,
@@ -1040,6 +1047,52 @@ def prepare_sparse_neighbor_conv_packed(S, table, Wp, K, Cin, Cout, bias, out,
             _dev(out, "out", S.dtype), _stream(stream)]
     return Prepared("shc_sparse_neighbor_conv_packed", args, 2, n_max,
                     (S, table, Wp, bias, out))
+
+
+def conv_packed_plan_bytes(n_rows: int, K: int, Cin: int, Cout: int,
+                           dtype: int = SHC_BF16) -> int:
+    """shc_conv_packed_plan_bytes: a packed-conv plan buffer for up to n_rows
+    rows (0: the shape has no packed conv)."""
+    return int(load().shc_conv_packed_plan_bytes(n_rows, K, Cin, Cout, dtype))
+
+
+def build_conv_packed_plan(table: torch.Tensor, n_rows: int, K: int, Cin: int, Cout: int,
+                           plan: torch.Tensor, stream=None):
+    """shc_build_conv_packed_plan (bf16 shapes)."""
+    args = [_dev(table, "table", torch.int32, K * n_rows), n_rows, K, Cin, Cout, SHC_BF16,
+            _dev(plan, "plan"), plan.numel() * plan.element_size(), _stream(stream)]
+    _check(load().shc_build_conv_packed_plan(*args), "shc_build_conv_packed_plan")
+
+
+def sparse_neighbor_conv_packed_planned(S: torch.Tensor, plan: torch.Tensor, n_rows: int,
+                                        Wp: torch.Tensor, K: int, Cin: int, Cout: int,
+                                        bias: Optional[torch.Tensor], out: torch.Tensor,
+                                        act: int = SHC_ACT_RELU, stream=None):
+    """shc_sparse_neighbor_conv_packed_planned."""
+    args = [_dev(S, "S", S.dtype, n_rows * Cin), _dev(plan, "plan"),
+            plan.numel() * plan.element_size(), n_rows, K, _dev(Wp, "Wp"),
+            _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout, _dtype_code(S), act,
+            _dev(out, "out", S.dtype, n_rows * Cout), _stream(stream)]
+    _check(load().shc_sparse_neighbor_conv_packed_planned(*args),
+           "shc_sparse_neighbor_conv_packed_planned")
+
+
+def prepare_build_conv_packed_plan(table, K, Cin, Cout, plan, stream=None) -> Prepared:
+    """shc_build_conv_packed_plan with n_rows given per call."""
+    args = [_dev(table, "table", torch.int32), 0, K, Cin, Cout, SHC_BF16, _dev(plan, "plan"),
+            plan.numel() * plan.element_size(), _stream(stream)]
+    return Prepared("shc_build_conv_packed_plan", args, 1, table.numel() // K, (table, plan))
+
+
+def prepare_sparse_neighbor_conv_packed_planned(S, plan, Wp, K, Cin, Cout, bias, out,
+                                                act=SHC_ACT_RELU, stream=None) -> Prepared:
+    """shc_sparse_neighbor_conv_packed_planned with n_rows given per call."""
+    n_max = min(S.numel() // Cin, out.numel() // Cout)
+    args = [_dev(S, "S", S.dtype), _dev(plan, "plan"), plan.numel() * plan.element_size(), 0, K,
+            _dev(Wp, "Wp"), _opt_dev(bias, "bias", torch.float32, Cout), Cin, Cout,
+            _dtype_code(S), act, _dev(out, "out", S.dtype), _stream(stream)]
+    return Prepared("shc_sparse_neighbor_conv_packed_planned", args, 3, n_max,
+                    (S, plan, Wp, bias, out))
 
 
 def prepare_build_conv_plan(table, K, Cin, Cout, plan, dtype=SHC_BF16, stream=None) -> Prepared:

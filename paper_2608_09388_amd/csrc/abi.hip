@@ -722,6 +722,82 @@ int shc_sparse_neighbor_conv_packed(const void* S, const int32_t* table, int64_t
                     "sparse_neighbor_conv_packed launch");
 }
 
+namespace {
+int device_cus(int* cus) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(cus, hipDeviceAttributeMultiprocessorCount, dev);
+  return e == hipSuccess ? SHC_OK : hip_status(e, "device query");
+}
+
+int check_packed_shape(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype,
+                       int32_t act) {
+  SHC_TRY(check_conv_shape(n_rows, K, Cin, Cout, dtype, act));
+  if (dtype != SHC_BF16 || !shc::conv_packed_supported(n_rows, K, Cin, Cout))
+    return fail(SHC_ERR_UNSUPPORTED,
+                "no packed conv for dtype %d, K = %d, Cin = %d, Cout = %d (bf16, K <= 9, "
+                "channels in {64, 128})",
+                dtype, K, Cin, Cout);
+  if ((int64_t)K * n_rows * 4 > 0x7FFFFFFFLL)
+    return fail(SHC_ERR_UNSUPPORTED, "K * n_rows * 4 = %lld bytes of table exceed 2^31 - 1",
+                (long long)((int64_t)K * n_rows * 4));
+  return SHC_OK;
+}
+}  // namespace
+
+size_t shc_conv_packed_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout,
+                                  int32_t dtype) {
+  if (n_rows < 0 || dtype != SHC_BF16 || !shc::conv_packed_supported(n_rows, K, Cin, Cout) ||
+      (int64_t)K * n_rows * 4 > 0x7FFFFFFFLL)
+    return 0;
+  int cus = 0;
+  if (device_cus(&cus) != SHC_OK) return 0;
+  const int64_t b = shc::conv_packed_plan_bytes_upto(n_rows, Cin, Cout, cus);
+  return (size_t)(b > 16 ? b : 16);
+}
+
+int shc_build_conv_packed_plan(const int32_t* table, int64_t n_rows, int32_t K, int32_t Cin,
+                               int32_t Cout, int32_t dtype, void* plan, size_t plan_bytes,
+                               hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_packed_shape(n_rows, K, Cin, Cout, dtype, SHC_ACT_NONE));
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(table, "table");
+  SHC_PTR(plan, "plan");
+  int cus = 0;
+  SHC_TRY(device_cus(&cus));
+  const int64_t need = shc::conv_packed_plan_bytes(n_rows, Cin, Cout, cus);
+  if ((int64_t)plan_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "plan_bytes = %zu is below the %lld bytes of this plan",
+                plan_bytes, (long long)need);
+  return hip_status(shc::launch_build_packed_plan(table, n_rows, K, Cin, Cout, plan, cus, stream),
+                    "build_conv_packed_plan launch");
+}
+
+int shc_sparse_neighbor_conv_packed_planned(const void* S, const void* plan, size_t plan_bytes,
+                                            int64_t n_rows, int32_t K, const void* Wp,
+                                            const float* bias, int32_t Cin, int32_t Cout,
+                                            int32_t dtype, int32_t act, void* out,
+                                            hipStream_t stream) {
+  g_last_error[0] = 0;
+  SHC_TRY(check_packed_shape(n_rows, K, Cin, Cout, dtype, act));
+  if (n_rows == 0) return SHC_OK;
+  SHC_PTR(S, "S");
+  SHC_PTR(plan, "plan");
+  SHC_PTR(Wp, "Wp");
+  SHC_OPT_PTR(bias, "bias");
+  SHC_PTR(out, "out");
+  int cus = 0;
+  SHC_TRY(device_cus(&cus));
+  const int64_t need = shc::conv_packed_plan_bytes(n_rows, Cin, Cout, cus);
+  if ((int64_t)plan_bytes < need)
+    return fail(SHC_ERR_CAPACITY, "plan_bytes = %zu is below the %lld bytes of a plan of "
+                "%lld rows", plan_bytes, (long long)need, (long long)n_rows);
+  return hip_status(shc::launch_conv_packed_planned(S, plan, n_rows, K, Wp, bias, Cin, Cout,
+                                                    act == SHC_ACT_RELU, out, cus, stream),
+                    "sparse_neighbor_conv_packed_planned launch");
+}
+
 size_t shc_conv_plan_bytes(int64_t n_rows, int32_t K, int32_t Cin, int32_t Cout, int32_t dtype) {
   if (!plan_query_args_ok(n_rows, K, Cin, Cout, dtype)) return 0;
   shc::GemmArgs a{};

@@ -65,7 +65,13 @@ struct PackedArgs {
   int32_t relu;
   int32_t chunk_rows;     // rows per chunk (<= RMAX)
   int32_t n_chunks;
+  void* plan;             // chunk images (plan launch: written; planned conv: read)
 };
+
+// The three launches of one kernel body: the conv grouping its rows itself,
+// the plan (the grouping alone, written out per chunk), and the conv reading
+// a plan.
+enum PkMode { kPkFull = 0, kPkPlan = 1, kPkPlanned = 2 };
 
 // Per shape: wavefronts (one 16-column block each), rows of the chunk held
 // in LDS, staged neighbour rows per round, and the LDS layout (bytes).
@@ -83,19 +89,27 @@ struct PkShape {
   static constexpr int SMAX = RMAX * kPkMaxK;       // staged pairs of a chunk, at most
   static constexpr int ZROW = RMAX + PCAP;                      // a row of zeros
   static constexpr int NBLK = RMAX / 16;                         // 16-row blocks of a chunk
+  // the chunk's plan: what the blocks read, in one contiguous image (the
+  // packed-plan launch writes it to global memory, the planned conv reads
+  // it back): positions' rows, slot entries, block slot sets, rounds, block
+  // boundaries in the staging list, header, staging sources
   static constexpr int off_prow = (ZROW + 1) * RB;               // uint16 [RMAX]
-  static constexpr int off_rowpos = off_prow + RMAX * 2;        // uint16 [RMAX]
-  static constexpr int off_obase = off_rowpos + RMAX * 2;       // int32 [NPOS + 1]
-  static constexpr int off_ltab = off_obase + (NPOS + 1) * 4 + 12;  // uint16 [RMAX][16]
-  static constexpr int off_ssrc = off_ltab + RMAX * 32;         // int32 [SMAX]
-  static constexpr int off_hist = off_ssrc + SMAX * 4;          // int32 [kPkKeys]
-  static constexpr int off_kbase = off_hist + kPkKeys * 4;      // int32 [kPkKeys + 1]
-  static constexpr int off_union = off_kbase + (kPkKeys + 1) * 4;  // uint32 [RMAX / 16]
-  static constexpr int off_wsum = off_union + RMAX / 16 * 4;    // int32 [NW]
-  static constexpr int off_bsb = off_wsum + NW * 4;             // int32 [NBLK]
-  static constexpr int off_rnd = off_bsb + NBLK * 4;            // int32 [NBLK + 2]
-  static constexpr int bytes = off_rnd + (NBLK + 2) * 4;
-  static_assert(off_ltab % 16 == 0, "aligned slot entries");
+  static constexpr int off_ltab = off_prow + RMAX * 2;           // uint16 [RMAX][16]
+  static constexpr int off_union = off_ltab + RMAX * 32;         // uint32 [NBLK]
+  static constexpr int off_rnd = off_union + NBLK * 4;           // int32 [NBLK + 2]
+  static constexpr int off_bnd = off_rnd + (NBLK + 2) * 4;       // int32 [NBLK + 1]
+  static constexpr int off_hdr = off_bnd + (NBLK + 1) * 4;       // int32 [4]
+  static constexpr int off_ssrc = (off_hdr + 16 + 15) / 16 * 16;  // int32 [SMAX]
+  static constexpr int IMG = (off_ssrc + SMAX * 4 + 15) / 16 * 16 - off_prow;
+  // working arrays of the grouping
+  static constexpr int off_rowpos = off_prow + IMG;              // uint16 [RMAX]
+  static constexpr int off_obase = off_rowpos + RMAX * 2;        // int32 [NPOS + 1]
+  static constexpr int off_hist = off_obase + (NPOS + 1) * 4;    // int32 [kPkKeys]
+  static constexpr int off_kbase = off_hist + kPkKeys * 4;       // int32 [kPkKeys + 1]
+  static constexpr int off_wsum = off_kbase + (kPkKeys + 1) * 4;  // int32 [NW]
+  static constexpr int off_bsb = off_wsum + NW * 4;              // int32 [NBLK]
+  static constexpr int bytes = off_bsb + NBLK * 4;
+  static_assert(off_ltab % 16 == 0 && off_prow % 16 == 0, "aligned slot entries");
   static_assert(bytes <= kPkLdsLimit, "one workgroup per CU");
   static_assert(RMAX % 16 == 0 && PCAP >= 16 * kPkMaxK, "chunk shape");
   static_assert(ZROW < 65536, "LDS rows fit 16 bits");
@@ -133,14 +147,16 @@ __device__ __forceinline__ int pk_chunk_at(int L, int c) {
   return L * RB + ((c ^ (L & (VPR - 1))) << 4);
 }
 
-template <int KS, int NCT>
+template <int KS, int NCT, int MODE>
 __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedArgs a) {
   using SH = PkShape<KS, NCT>;
   constexpr int NT = SH::NT, RPT = SH::RPT;
   constexpr int Cout = NCT * 16;
   constexpr int RB = SH::RB, VPR = SH::VPR, RMAX = SH::RMAX, PCAP = SH::PCAP;
 
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem_base[];
+  // the plan launch holds no rows: its LDS starts at the plan image
+  unsigned char* smem = MODE == kPkPlan ? smem_base - SH::off_prow : smem_base;
   unsigned char* rows = smem;  // [RMAX] chunk rows, then [PCAP] staged rows
   uint16_t* prow = reinterpret_cast<uint16_t*>(smem + SH::off_prow);      // position -> row
   uint16_t* rowpos = reinterpret_cast<uint16_t*>(smem + SH::off_rowpos);  // row -> position
@@ -153,7 +169,9 @@ __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedAr
   int32_t* wsum = reinterpret_cast<int32_t*>(smem + SH::off_wsum);
   int32_t* blk_sb = reinterpret_cast<int32_t*>(smem + SH::off_bsb);
   int32_t* rnd = reinterpret_cast<int32_t*>(smem + SH::off_rnd);
-  constexpr int ZROW = SH::ZROW, NBLK = SH::NBLK;
+  int32_t* bnd = reinterpret_cast<int32_t*>(smem + SH::off_bnd);
+  int32_t* hdr = reinterpret_cast<int32_t*>(smem + SH::off_hdr);
+  constexpr int ZROW = SH::ZROW, NBLK = SH::NBLK, IMG = SH::IMG;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -182,9 +200,12 @@ __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedAr
                                                             (j * NCT * KS + ks) * 1024, 0));
   };
   // slot 0's fragments now; the other slots' after the first chunk's table
-  // entries, so that the sort waits for slot 0's and the table only
-  load_w(0, 1);
-  bool w_rest = true;
+  // entries, so that the grouping waits for slot 0's and the table only (a
+  // planned conv loads them all beside its first chunk's plan; the plan
+  // launch needs none)
+  if (MODE == kPkFull) load_w(0, 1);
+  if (MODE == kPkPlanned) load_w(0, kPkMaxK);
+  bool w_rest = MODE == kPkFull;
   f32x4 bias4;
   {
     const int col = wave * 16 + 4 * g;
@@ -193,7 +214,8 @@ __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedAr
   }
   // the row of zeros that absent neighbours read (published by the chunk's
   // first barrier)
-  if (tid < VPR) *reinterpret_cast<pk_v4u32*>(rows + ZROW * RB + tid * 16) = pk_v4u32{0, 0, 0, 0};
+  if (MODE != kPkPlan && tid < VPR)
+    *reinterpret_cast<pk_v4u32*>(rows + ZROW * RB + tid * 16) = pk_v4u32{0, 0, 0, 0};
   // lane constant of the B-operand addresses: 16-byte chunk 4 ks + g of a row
   int gk[KS];
 #pragma unroll
@@ -206,7 +228,26 @@ __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedAr
     const int64_t row0 = chunk * a.chunk_rows;
     const int nrows = (int)min((int64_t)a.chunk_rows, n - row0);
     const int nblk = (nrows + 15) >> 4;
-
+    int nin;
+    if constexpr (MODE == kPkPlanned) {
+      // the chunk's plan image into LDS (direct loads), then its header: a
+      // plan of another row count or chunking is refused chunk by chunk
+      const unsigned char* img = static_cast<const unsigned char*>(a.plan) + chunk * (int64_t)IMG;
+      for (int v0 = wave * 64; v0 < IMG / 16; v0 += NT) {
+        const int v = v0 + lane;
+        if (v < IMG / 16)
+          __builtin_amdgcn_global_load_lds(img + v * 16,
+                                           (SHC_PK_LDS void*)(smem + SH::off_prow + v0 * 16), 16,
+                                           0, 0);
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+      pk_lds_barrier();
+      if (hdr[1] != nrows || hdr[2] != (int)(n & 0x7FFFFFFF) || hdr[3] != (int)chunk) {
+        pk_lds_barrier();
+        continue;
+      }
+      nin = hdr[0];
+    } else {
     // 1. the table entries of this thread's rows (branch-free: an entry past
     // the chunk or the slots reads the buffer out of range); the key counts
     // and block unions start at zero
@@ -274,7 +315,7 @@ __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedAr
         atomicOr(&bunion[pos[u] >> 4], m[u]);
       }
     }
-    const int nin = kbase[kPkMaxK];
+    nin = kbase[kPkMaxK];
     pk_lds_barrier();
     // 4. staged-pair numbers by position (exclusive prefix over positions)
     {
@@ -352,7 +393,25 @@ __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedAr
         for (int j = 0; j < kPkMaxK; ++j) ltab[q * 16 + j] = (uint16_t)ZROW;
       }
     }
+    // block boundaries in the staging list, and the header
+    if (tid <= nblk) bnd[tid] = obase[min(tid * 16, nrows)];
+    if (tid == 0) {
+      hdr[0] = nin;
+      hdr[1] = nrows;
+      hdr[2] = (int)(n & 0x7FFFFFFF);
+      hdr[3] = (int)chunk;
+    }
     pk_lds_barrier();
+    if constexpr (MODE == kPkPlan) {
+      // the chunk's image out, then the next chunk
+      unsigned char* img = static_cast<unsigned char*>(a.plan) + chunk * (int64_t)IMG;
+      for (int v = tid; v < IMG / 16; v += NT)
+        *reinterpret_cast<pk_v4u32*>(img + v * 16) =
+            *reinterpret_cast<const pk_v4u32*>(smem + SH::off_prow + v * 16);
+      pk_lds_barrier();
+      continue;
+    }
+    }  // steps 1-5
 
     // 6. blocks [b0, b1): every lane reads an operand for every slot present
     // in the block (a row without the slot reads the row of zeros)
@@ -388,7 +447,8 @@ __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedAr
           __builtin_amdgcn_sched_group_barrier(0x100, KS, 0);
           __builtin_amdgcn_sched_group_barrier(0x008, KS, 0);
         }
-        if (p < nrows) {
+        const int prw = p < nrows ? prow[p] : nrows;
+        if (prw < nrows) {
           float v[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -398,7 +458,7 @@ __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedAr
           const pk_bf16x2 h0 = __builtin_convertvector(pk_f32x2{v[0], v[1]}, pk_bf16x2);
           const pk_bf16x2 h1 = __builtin_convertvector(pk_f32x2{v[2], v[3]}, pk_bf16x2);
           unsigned char* orow = static_cast<unsigned char*>(a.out) +
-                                (row0 + prow[p]) * (int64_t)(Cout * 2) + wave * 32 + g * 8;
+                                (row0 + prw) * (int64_t)(Cout * 2) + wave * 32 + g * 8;
           *reinterpret_cast<pk_v2u32*>(orow) =
               pk_v2u32{__builtin_bit_cast(uint32_t, h0), __builtin_bit_cast(uint32_t, h1)};
         }
@@ -423,24 +483,28 @@ __global__ __launch_bounds__(64 * NCT, 1) void conv_packed_kernel(const PackedAr
         const int L = v / VPR;
         const int c = (v % VPR) ^ (L & (VPR - 1));
         const int r = v < nvec ? prow[L] : 0;
-        if (v < nvec)
+        if (v < nvec && r < nrows)
           __builtin_amdgcn_global_load_lds(src + r * RB + c * 16,
                                            (SHC_PK_LDS void*)(rows + v0 * 16), 16, 0, 0);
       }
     }
-    const int nr = rnd[NBLK + 1];
+    // (every index read from the plan is clamped to the chunk: a plan built
+    // for another table of the same row count gives wrong values, never an
+    // access out of range)
+    nin = min(max(nin, 0), nrows);
+    const int nr = min(max(rnd[NBLK + 1], 0), nblk);
     for (int r = 0; r == 0 || r < nr; ++r) {
-      const int bs = nr ? rnd[r] : nblk;
-      const int be = nr ? rnd[r + 1] : nblk;
-      const int sb = obase[min(bs * 16, nrows)];
-      const int nvec = (obase[min(be * 16, nrows)] - sb) * VPR;
+      const int bs = nr ? min(max(rnd[r], 0), nblk) : nblk;
+      const int be = nr ? min(max(rnd[r + 1], bs), nblk) : nblk;
+      const int sb = min(max(bnd[bs], 0), SH::SMAX);
+      const int nvec = min(max(bnd[be] - sb, 0), PCAP) * VPR;
       for (int v0 = wave * 64; v0 < nvec; v0 += NT) {
         const int v = v0 + lane;
         const int q = v / VPR;
         const int L = RMAX + q;
         const int c = (v % VPR) ^ (L & (VPR - 1));
-        const int64_t src = v < nvec ? ssrc[sb + q] : 0;
-        if (v < nvec)
+        const int64_t src = v < nvec ? ssrc[min(sb + q, SH::SMAX - 1)] : 0;
+        if (v < nvec && (uint64_t)src < (uint64_t)n)
           __builtin_amdgcn_global_load_lds(S + src * RB + c * 16,
                                            (SHC_PK_LDS void*)(rows + RMAX * RB + v0 * 16), 16, 0,
                                            0);
@@ -480,25 +544,35 @@ __global__ void pack_weights_kernel(const uint16_t* W, int32_t K, int32_t Cin, i
   for (int e = 0; e < 8; ++e) dst[e] = v[e];
 }
 
+// Rows per chunk: about one chunk per CU, at most RMAX.
 template <int KS, int NCT>
+void packed_chunks(int64_t n_rows, int num_cus, int32_t* rc_out, int32_t* chunks_out) {
+  using SH = PkShape<KS, NCT>;
+  int64_t rc = (n_rows + num_cus - 1) / num_cus;
+  if (rc > SH::RMAX) rc = SH::RMAX;
+  if (rc < 16) rc = 16;
+  *rc_out = (int32_t)rc;
+  *chunks_out = (int32_t)((n_rows + rc - 1) / rc);
+}
+
+template <int KS, int NCT, int MODE>
 hipError_t launch_packed_k(const PackedArgs& a0, int num_cus, hipStream_t stream) {
   using SH = PkShape<KS, NCT>;
   PackedArgs a = a0;
-  int64_t rc = (a.n_rows + num_cus - 1) / num_cus;
-  if (rc > SH::RMAX) rc = SH::RMAX;
-  if (rc < 16) rc = 16;
-  a.chunk_rows = (int)rc;
-  a.n_chunks = (int)((a.n_rows + rc - 1) / rc);
-  const int grid = a.n_chunks < num_cus ? a.n_chunks : num_cus;
-  auto kern = conv_packed_kernel<KS, NCT>;
+  packed_chunks<KS, NCT>(a.n_rows, num_cus, &a.chunk_rows, &a.n_chunks);
+  // the conv: one workgroup per CU; the plan launch (LDS for the plan image
+  // only) every chunk at once
+  const int grid = MODE == kPkPlan || a.n_chunks < num_cus ? a.n_chunks : num_cus;
+  const int lds = MODE == kPkPlan ? SH::bytes - SH::off_prow : SH::bytes;
+  auto kern = conv_packed_kernel<KS, NCT, MODE>;
   static std::once_flag once;
   static hipError_t err = hipSuccess;
   std::call_once(once, [&] {
     err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, SH::bytes);
+                              hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   });
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(SH::NT), (size_t)SH::bytes, stream, a);
+  hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(SH::NT), (size_t)lds, stream, a);
   return hipGetLastError();
 }
 
@@ -526,6 +600,8 @@ hipError_t launch_pack_conv_weights(const void* W, int32_t K, int32_t Cin, int32
   return hipGetLastError();
 }
 
+#define SHC_PACKED_SHAPES(X) X(64, 64) X(64, 128) X(128, 64) X(128, 128)
+
 hipError_t launch_conv_packed(const void* S, const int32_t* table, int64_t n_rows, int32_t K,
                               const void* Wp, const float* bias, int32_t Cin, int32_t Cout,
                               int32_t relu, void* out, int num_cus, hipStream_t stream) {
@@ -539,12 +615,77 @@ hipError_t launch_conv_packed(const void* S, const int32_t* table, int64_t n_row
   a.n_rows = n_rows;
   a.K = K;
   a.relu = relu;
-#define SHC_PACKED_CASE(CI, CO)                                                      \
-  if (Cin == CI && Cout == CO) return launch_packed_k<CI / 32, CO / 16>(a, num_cus, stream);
-  SHC_PACKED_CASE(64, 64) SHC_PACKED_CASE(64, 128) SHC_PACKED_CASE(128, 64)
-  SHC_PACKED_CASE(128, 128)
+#define SHC_PACKED_CASE(CI, CO)                                                              \
+  if (Cin == CI && Cout == CO) return launch_packed_k<CI / 32, CO / 16, kPkFull>(a, num_cus, stream);
+  SHC_PACKED_SHAPES(SHC_PACKED_CASE)
 #undef SHC_PACKED_CASE
   return hipErrorInvalidValue;
 }
+
+int64_t conv_packed_plan_bytes(int64_t n_rows, int32_t Cin, int32_t Cout, int num_cus) {
+  int32_t rc = 0, chunks = 0;
+#define SHC_PACKED_CASE(CI, CO)                                                   \
+  if (Cin == CI && Cout == CO) {                                                  \
+    packed_chunks<CI / 32, CO / 16>(n_rows, num_cus, &rc, &chunks);               \
+    return (int64_t)chunks * PkShape<CI / 32, CO / 16>::IMG;                      \
+  }
+  SHC_PACKED_SHAPES(SHC_PACKED_CASE)
+#undef SHC_PACKED_CASE
+  return 0;
+}
+
+int64_t conv_packed_plan_bytes_upto(int64_t n_rows, int32_t Cin, int32_t Cout, int num_cus) {
+  // chunks(n) is at most max(CUs, ceil(n / RMAX)) for every n <= n_rows
+  int64_t rmax = 0, img = 0;
+#define SHC_PACKED_CASE(CI, CO)                                                   \
+  if (Cin == CI && Cout == CO) {                                                  \
+    rmax = PkShape<CI / 32, CO / 16>::RMAX;                                       \
+    img = PkShape<CI / 32, CO / 16>::IMG;                                         \
+  }
+  SHC_PACKED_SHAPES(SHC_PACKED_CASE)
+#undef SHC_PACKED_CASE
+  if (img == 0) return 0;
+  int64_t chunks = (n_rows + rmax - 1) / rmax;
+  if (chunks < num_cus) chunks = num_cus;
+  return chunks * img;
+}
+
+hipError_t launch_build_packed_plan(const int32_t* table, int64_t n_rows, int32_t K, int32_t Cin,
+                                    int32_t Cout, void* plan, int num_cus, hipStream_t stream) {
+  if (n_rows == 0) return hipSuccess;
+  PackedArgs a{};
+  a.table = table;
+  a.n_rows = n_rows;
+  a.K = K;
+  a.plan = plan;
+#define SHC_PACKED_CASE(CI, CO)                                                              \
+  if (Cin == CI && Cout == CO) return launch_packed_k<CI / 32, CO / 16, kPkPlan>(a, num_cus, stream);
+  SHC_PACKED_SHAPES(SHC_PACKED_CASE)
+#undef SHC_PACKED_CASE
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_conv_packed_planned(const void* S, const void* plan, int64_t n_rows, int32_t K,
+                                      const void* Wp, const float* bias, int32_t Cin,
+                                      int32_t Cout, int32_t relu, void* out, int num_cus,
+                                      hipStream_t stream) {
+  if (n_rows == 0) return hipSuccess;
+  PackedArgs a{};
+  a.S = S;
+  a.Wp = Wp;
+  a.bias = bias;
+  a.out = out;
+  a.n_rows = n_rows;
+  a.K = K;
+  a.relu = relu;
+  a.plan = const_cast<void*>(plan);
+#define SHC_PACKED_CASE(CI, CO)                                                              \
+  if (Cin == CI && Cout == CO)                                                               \
+    return launch_packed_k<CI / 32, CO / 16, kPkPlanned>(a, num_cus, stream);
+  SHC_PACKED_SHAPES(SHC_PACKED_CASE)
+#undef SHC_PACKED_CASE
+  return hipErrorInvalidValue;
+}
+#undef SHC_PACKED_SHAPES
 
 }  // namespace shc

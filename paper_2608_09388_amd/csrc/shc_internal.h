@@ -201,5 +201,16 @@ hipError_t launch_pack_conv_weights(const void* W, int32_t K, int32_t Cin, int32
 hipError_t launch_conv_packed(const void* S, const int32_t* table, int64_t n_rows, int32_t K,
                               const void* Wp, const float* bias, int32_t Cin, int32_t Cout,
                               int32_t relu, void* out, int num_cus, hipStream_t stream);
+// its plan: the rows' grouping and slot entries of every chunk, built once per
+// active set (launch_build_packed_plan) and read by every packed layer of the
+// shape (launch_conv_packed_planned)
+int64_t conv_packed_plan_bytes(int64_t n_rows, int32_t Cin, int32_t Cout, int num_cus);
+int64_t conv_packed_plan_bytes_upto(int64_t n_rows, int32_t Cin, int32_t Cout, int num_cus);
+hipError_t launch_build_packed_plan(const int32_t* table, int64_t n_rows, int32_t K, int32_t Cin,
+                                    int32_t Cout, void* plan, int num_cus, hipStream_t stream);
+hipError_t launch_conv_packed_planned(const void* S, const void* plan, int64_t n_rows, int32_t K,
+                                      const void* Wp, const float* bias, int32_t Cin,
+                                      int32_t Cout, int32_t relu, void* out, int num_cus,
+                                      hipStream_t stream);
 
 }  // namespace shc

@@ -189,3 +189,78 @@ def test_packed_stack_against_oracle(dev, executor):
         scale = O.conv_at(S, coords, w.B, w.V, w.nbr, w.layers[1].W, rows, None, scale=True)
         assert_scaled_close(down(st.acts[2][:n])[rows], ref, scale, "bf16",
                             f"packed stack batch {k}", n_terms=9 * 128)
+
+
+@pytest.mark.parametrize("B,V,K,Cin,Cout,p,slot0", [
+    (64, 655, 9, 128, 128, 0.1, "self"),
+    (16, 655, 9, 64, 64, 0.1, "self"),
+    (16, 655, 9, 64, 128, 0.2, "self"),
+    (6, 700, 5, 128, 64, 0.4, "self"),
+    (1, 40, 9, 128, 128, 0.5, "self"),
+    (8, 655, 9, 128, 128, 0.9, "self"),      # several staging rounds
+    (24, 4000, 9, 128, 128, 1.0, "self"),    # several chunks per workgroup
+    (8, 655, 9, 128, 128, 0.3, "other"),
+    (8, 655, 9, 64, 64, 0.3, "absent"),
+])
+def test_packed_plan_matches_packed(dev, B, V, K, Cin, Cout, p, slot0):
+    """The planned packed conv (shc_build_conv_packed_plan, then
+    shc_sparse_neighbor_conv_packed_planned) writes exactly what the packed
+    conv writes from the table, with and without bias and ReLU; and it is
+    within the derived bound of the oracle on sampled rows."""
+    rng = np.random.default_rng(B * 13 + V + K + Cin + 7 * Cout)
+    nbr = rand_nbr(V, K, rng, slot0=slot0)
+    m = (rng.random((B, V)) < p).astype(np.uint8)
+    c = Compaction(m)
+    n = c.run()
+    table = torch.empty(K * n, dtype=torch.int32, device=dev)
+    shc.build_neighbor_table(c.coords, c.inv, n, B, V, up(nbr), table)
+    S = synth.as_dtype(rng.standard_normal((n, Cin)).astype(np.float32), "bf16")[1]
+    W = synth.as_dtype((rng.standard_normal((K, Cin, Cout)) / np.sqrt(K * Cin))
+                       .astype(np.float32), "bf16")[1]
+    bias = up(rng.standard_normal(Cout).astype(np.float32))
+    Wp, Sd = packed(W, dev), up(S, "bf16")
+    plan = torch.empty(shc.conv_packed_plan_bytes(B * V, K, Cin, Cout), dtype=torch.uint8,
+                       device=dev)
+    plan.fill_(0xA5)   # garbage before the build
+    shc.build_conv_packed_plan(table, n, K, Cin, Cout, plan)
+    for b, act in ((bias, shc.SHC_ACT_RELU), (None, shc.SHC_ACT_NONE)):
+        o1 = torch.full((n + 2, Cout), float("nan"), dtype=torch.bfloat16, device=dev)
+        o2 = o1.clone()
+        shc.sparse_neighbor_conv_packed(Sd, table, n, Wp, K, Cin, Cout, b, o1, act)
+        shc.sparse_neighbor_conv_packed_planned(Sd, plan, n, Wp, K, Cin, Cout, b, o2, act)
+        torch.cuda.synchronize()
+        assert torch.equal(o1[:n], o2[:n]), f"planned != packed K={K} {Cin}->{Cout} p={p}"
+        assert torch.isnan(o2[n:].float()).all()
+    coords = O.compact(m)[0]
+    rows = rng.choice(n, size=min(n, 200), replace=False)
+    ref = O.conv_at(S, coords, B, V, nbr, W, rows)
+    scale = O.conv_at(S, coords, B, V, nbr, W, rows, scale=True)
+    assert_scaled_close(down(o2)[rows], ref, scale, "bf16", "planned packed conv",
+                        n_terms=K * Cin)
+
+
+def test_packed_plan_other_row_count_and_errors(dev):
+    """A plan of another row count writes nothing (every chunk's header
+    disagrees); a plan buffer below the call's size is refused."""
+    rng = np.random.default_rng(21)
+    B, V, K, C = 8, 655, 9, 128
+    nbr = rand_nbr(V, K, rng)
+    m = (rng.random((B, V)) < 0.2).astype(np.uint8)
+    c = Compaction(m)
+    n = c.run()
+    table = torch.empty(K * n, dtype=torch.int32, device=dev)
+    shc.build_neighbor_table(c.coords, c.inv, n, B, V, up(nbr), table)
+    plan = torch.empty(shc.conv_packed_plan_bytes(B * V, K, C, C), dtype=torch.uint8, device=dev)
+    shc.build_conv_packed_plan(table, n, K, C, C, plan)
+    W = torch.zeros((K, C, C), dtype=torch.bfloat16, device=dev)
+    Wp = packed(W.cpu().float().numpy(), dev)
+    S = torch.zeros((n, C), dtype=torch.bfloat16, device=dev)
+    out = torch.full((n, C), 7.0, dtype=torch.bfloat16, device=dev)
+    shc.sparse_neighbor_conv_packed_planned(S, plan, n - 5, Wp, K, C, C, None, out)
+    torch.cuda.synchronize()
+    assert (out.float() == 7.0).all()
+    small = plan[:16]
+    with pytest.raises(shc.ShcError, match="CAPACITY"):
+        shc.build_conv_packed_plan(table, n, K, C, C, small)
+    with pytest.raises(shc.ShcError, match="CAPACITY"):
+        shc.sparse_neighbor_conv_packed_planned(S, small, n, Wp, K, C, C, None, out)
