@@ -10,24 +10,29 @@
 // wavefront loads its fragments with plain 16-byte loads, straight into
 // registers, with no LDS transpose.
 //
-// One workgroup of four wavefronts per CU; wavefront w owns a quarter of the
-// output columns and holds the fragments of every slot for them (for
-// 128 -> 128 and K = 9: 288 registers a lane).  A workgroup takes a chunk of
-// consecutive active rows (about N' / CUs, so one round of workgroups covers
-// the rows) and
-//   1. loads the chunk's table entries into registers and the chunk's input
-//      rows into LDS (direct global->LDS loads, 16-byte chunks swizzled by
-//      row), all in flight together;
-//   2. sorts the rows by two keys, stably, in LDS: whether any present
-//      neighbour lies outside the chunk, then the first present slot after
-//      slot 0, so that a 16-row block mostly shares its slots;
-//   3. numbers the present (row, slot) pairs by position: a pair whose
-//      neighbour row lies in the chunk reads it from the chunk's LDS copy,
-//      the others are staged in LDS by one direct load per 16 bytes;
-//   4. multiplies, block by block, every slot present in any of the block's
-//      rows (a row without the slot contributes a zero operand), slot 0
-//      first and the others ascending, into fp32 accumulators; blocks whose
-//      pairs all lie in the chunk run while the staged rows are in flight.
+// One workgroup per CU of one wavefront per 16 output columns (eight for
+// 128 columns: two per SIMD); a wavefront holds the fragments of every slot
+// for its columns (for 128 -> 128 and K = 9: 144 registers a lane).  A
+// workgroup takes a chunk of consecutive active rows (about N' / CUs, so one
+// round of workgroups covers the rows) and
+//   1. loads slot 0's fragments and the chunk's table entries into
+//      registers (the other slots' fragments follow while it groups);
+//   2. groups the rows in LDS by two keys, whether any present neighbour lies
+//      outside the chunk, then the first present slot after slot 0 (one LDS
+//      counter per key; the order within a key is immaterial), so that a
+//      16-row block mostly shares its slots;
+//   3. writes every (position, slot) entry as the LDS row its operand is
+//      read from: a neighbour in the chunk from the chunk's copy, the others
+//      from staging rows filled in rounds of at most PCAP rows, an absent
+//      one from a row of zeros;
+//   4. loads the chunk's rows into LDS in position order and the round's
+//      staged rows (direct global->LDS loads, 16-byte chunks swizzled by
+//      row), then multiplies, block by block, every slot present in any of
+//      the block's rows, slot 0 first and the others ascending, into one
+//      fp32 accumulator.
+// Steps 1-3 depend only on the table: the plan launch runs them alone and
+// writes each chunk's result out (an image of the LDS it filled), and the
+// planned conv reads that image back in their place.
 // Each row's sum runs in a fixed order (slots ascending, each MFMA's 32
 // products as the hardware sums them), so the result does not depend on the
 // grid or on where a row lands in the sort.  Then bias, activation and the
